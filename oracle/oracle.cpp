@@ -1,0 +1,433 @@
+// Oracle of the NoScope cascade filter: a plain, slow, single-threaded fp64
+// CPU implementation, written from the paper.
+//
+// TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the
+// benchmark's CPU-baseline leg may load or call this library; the product
+// path never does.  It shares no code, header or table with the HIP library.
+//
+// What it computes, step by step (paper section in brackets):
+//   1. area sums: frames are resized before the models [Sec. 7]; read as the
+//      exact area average of the piecewise-constant image, kept as integer
+//      sums S with a common integer denominator den (value = S / den);
+//   2. difference detector [Sec. 5]: MSE against the frame delta earlier or a
+//      fixed reference image, over the whole image or per grid block weighed
+//      by a logistic regression; it fires when the metric is higher than
+//      delta_diff [Sec. 6.2];
+//   3. the frames that fire, in ascending order [Sec. 7, batching];
+//   4. specialized CNN [Sec. 4]: pre-processing to [-1, 1] [Sec. 7], conv3x3
+//      + ReLU (+ 2x2 max-pool) layers, a ReLU dense layer and one output
+//      logit, confidence c = sigmoid(logit);
+//   5. decision [Sec. 3, Sec. 4]: c below c_low -> no object, above c_high
+//      -> object, otherwise defer to the reference network; a frame on which
+//      the earlier-frame detector does not fire reuses the compared frame's
+//      output [Sec. 5].
+// Readings where the paper is silent (rounding points of bf16 networks,
+// forced firing of the first delta frames, ties) are listed in the design
+// notes; each is marked "reading" below.
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <limits>
+#include <vector>
+
+namespace {
+
+int64_t gcd64(int64_t a, int64_t b) {
+  while (b) {
+    int64_t t = a % b;
+    a = b;
+    b = t;
+  }
+  return a;
+}
+
+// Overlap of output cell o = [o*p, (o+1)*p) with input pixel i = [i*q, (i+1)*q),
+// in units where one input pixel has length q = n_out/g and one output cell
+// length p = n_in/g.
+std::vector<int64_t> overlap_table(int n_in, int n_out) {
+  int64_t g = gcd64(n_in, n_out);
+  int64_t p = n_in / g, q = n_out / g;
+  std::vector<int64_t> w((size_t)n_in * n_out, 0);
+  for (int o = 0; o < n_out; ++o) {
+    int64_t a0 = (int64_t)o * p, a1 = a0 + p;
+    for (int i = 0; i < n_in; ++i) {
+      int64_t b0 = (int64_t)i * q, b1 = b0 + q;
+      int64_t lo = a0 > b0 ? a0 : b0;
+      int64_t hi = a1 < b1 ? a1 : b1;
+      w[(size_t)o * n_in + i] = hi > lo ? hi - lo : 0;
+    }
+  }
+  return w;
+}
+
+// Round to the nearest bfloat16 value (8 significant bits), ties to even,
+// from the definition: scale the significand to [128, 256) and round.
+double round_bf16(double v) {
+  if (v == 0.0 || !std::isfinite(v)) return v;
+  int e;
+  double m = std::frexp(v, &e);          // v = m * 2^e, 0.5 <= |m| < 1
+  double r = std::nearbyint(m * 256.0);  // default rounding mode: ties to even
+  return std::ldexp(r, e - 8);
+}
+
+struct Net {
+  int n_conv;
+  int cout[8];
+  int pool[8];
+  int dense;
+  int in_h, in_w;
+  bool bf16;
+  // weights (fp64 copies of the fp32 blob)
+  std::vector<std::vector<double>> cw, cb;
+  std::vector<double> w1, b1, w2;
+  double b2;
+  int flat;
+};
+
+}  // namespace
+
+extern "C" {
+
+// ---------------------------------------------------------------- area sums
+
+// Integer overlap weights w[o*n_in + i]; returns their per-row sum p.
+int64_t oracle_area_weights(int32_t n_in, int32_t n_out, int64_t* w_out) {
+  std::vector<int64_t> w = overlap_table(n_in, n_out);
+  std::memcpy(w_out, w.data(), w.size() * sizeof(int64_t));
+  int64_t s = 0;
+  for (int i = 0; i < n_in; ++i) s += w[i];
+  return s;
+}
+
+// Common denominator of the area sums: (row weight sum) * (column weight sum).
+int64_t oracle_area_den(int32_t H, int32_t W, int32_t Ho, int32_t Wo) {
+  std::vector<int64_t> wy = overlap_table(H, Ho), wx = overlap_table(W, Wo);
+  int64_t sy = 0, sx = 0;
+  for (int j = 0; j < H; ++j) sy += wy[j];
+  for (int i = 0; i < W; ++i) sx += wx[i];
+  return sy * sx;
+}
+
+// S[Y][X][c] = sum_j sum_i wy[Y][j] * wx[X][i] * F[j][i][c]   (frame: [H][W][3] uint8)
+// The sum runs over the support of each output cell (the input indices whose
+// overlap weight is non-zero), found by scanning the weight table.
+void oracle_area_sums(const uint8_t* frame, int32_t H, int32_t W, int32_t Ho, int32_t Wo,
+                      int64_t* S) {
+  std::vector<int64_t> wy = overlap_table(H, Ho), wx = overlap_table(W, Wo);
+  auto support = [](const std::vector<int64_t>& w, int n_in, int o, int* lo, int* hi) {
+    *lo = n_in;
+    *hi = 0;
+    for (int i = 0; i < n_in; ++i)
+      if (w[(size_t)o * n_in + i] != 0) {
+        if (i < *lo) *lo = i;
+        *hi = i + 1;
+      }
+  };
+  for (int Y = 0; Y < Ho; ++Y) {
+    int j0, j1;
+    support(wy, H, Y, &j0, &j1);
+    for (int X = 0; X < Wo; ++X) {
+      int i0, i1;
+      support(wx, W, X, &i0, &i1);
+      for (int c = 0; c < 3; ++c) {
+        int64_t s = 0;
+        for (int j = j0; j < j1; ++j) {
+          int64_t a = wy[(size_t)Y * H + j];
+          for (int i = i0; i < i1; ++i) {
+            int64_t b = wx[(size_t)X * W + i];
+            s += a * b * (int64_t)frame[((size_t)j * W + i) * 3 + c];
+          }
+        }
+        S[((size_t)Y * Wo + X) * 3 + c] = s;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------- difference detector
+
+// Global MSE between two area-sum images (Sec. 5): mean over Ho*Wo*3 values of
+// ((a - b) / den)^2 on the 0..255 scale.  E_out receives sum (a - b)^2 exactly.
+double oracle_global_mse(const int64_t* a, const int64_t* b, int32_t Ho, int32_t Wo, int64_t den,
+                         int64_t* E_out) {
+  int64_t N = (int64_t)Ho * Wo * 3;
+  int64_t E = 0;
+  for (int64_t k = 0; k < N; ++k) {
+    int64_t d = a[k] - b[k];
+    E += d * d;
+  }
+  if (E_out) *E_out = E;
+  return (double)E / ((double)den * (double)den * (double)N);
+}
+
+// Blocked detector (Sec. 5): MSE m_k per grid block k = by*Gw + bx (block rows
+// [floor(by*Ho/Gh), floor((by+1)*Ho/Gh)), columns likewise), weighed by a
+// logistic regression: score = bias + sum_k w_k m_k.
+double oracle_blocked_score(const int64_t* a, const int64_t* b, int32_t Ho, int32_t Wo,
+                            int64_t den, int32_t Gh, int32_t Gw, const float* w, double bias,
+                            double* m_out) {
+  double z = bias;
+  for (int by = 0; by < Gh; ++by) {
+    int y0 = (int)((int64_t)by * Ho / Gh), y1 = (int)((int64_t)(by + 1) * Ho / Gh);
+    for (int bx = 0; bx < Gw; ++bx) {
+      int x0 = (int)((int64_t)bx * Wo / Gw), x1 = (int)((int64_t)(bx + 1) * Wo / Gw);
+      int64_t E = 0;
+      for (int y = y0; y < y1; ++y)
+        for (int x = x0; x < x1; ++x)
+          for (int c = 0; c < 3; ++c) {
+            size_t k = ((size_t)y * Wo + x) * 3 + c;
+            int64_t d = a[k] - b[k];
+            E += d * d;
+          }
+      double cells = (double)(y1 - y0) * (double)(x1 - x0) * 3.0;
+      double m = (double)E / ((double)den * (double)den * cells);
+      if (m_out) m_out[by * Gw + bx] = m;
+      z += (double)w[by * Gw + bx] * m;
+    }
+  }
+  return z;
+}
+
+// ------------------------------------------------------------ specialized CNN
+
+struct oracle_cnn_desc {
+  int32_t n_conv;
+  int32_t conv_out[8];
+  int32_t pool_after[8];
+  int32_t dense;
+  int32_t in_h, in_w;
+  int32_t bf16;
+};
+
+double oracle_round_bf16(double v) { return round_bf16(v); }
+
+static bool load_net(const oracle_cnn_desc* d, const float* blob, Net* net) {
+  if (d->n_conv < 1 || d->n_conv > 8) return false;
+  net->n_conv = d->n_conv;
+  net->dense = d->dense;
+  net->in_h = d->in_h;
+  net->in_w = d->in_w;
+  net->bf16 = d->bf16 != 0;
+  const float* p = blob;
+  int cin = 3, h = d->in_h, w = d->in_w;
+  for (int l = 0; l < d->n_conv; ++l) {
+    net->cout[l] = d->conv_out[l];
+    net->pool[l] = d->pool_after[l];
+    size_t nw = (size_t)d->conv_out[l] * cin * 9;
+    net->cw.emplace_back(p, p + nw);
+    p += nw;
+    net->cb.emplace_back(p, p + d->conv_out[l]);
+    p += d->conv_out[l];
+    cin = d->conv_out[l];
+    if (d->pool_after[l]) {
+      h /= 2;
+      w /= 2;
+    }
+  }
+  net->flat = cin * h * w;
+  net->w1.assign(p, p + (size_t)d->dense * net->flat);
+  p += (size_t)d->dense * net->flat;
+  net->b1.assign(p, p + d->dense);
+  p += d->dense;
+  net->w2.assign(p, p + d->dense);
+  p += d->dense;
+  net->b2 = *p;
+  return true;
+}
+
+// Number of floats in the canonical weight blob of a network.
+int64_t oracle_cnn_blob_floats(const oracle_cnn_desc* d) {
+  int64_t n = 0;
+  int cin = 3, h = d->in_h, w = d->in_w;
+  for (int l = 0; l < d->n_conv; ++l) {
+    n += (int64_t)d->conv_out[l] * cin * 9 + d->conv_out[l];
+    cin = d->conv_out[l];
+    if (d->pool_after[l]) {
+      h /= 2;
+      w /= 2;
+    }
+  }
+  int64_t flat = (int64_t)cin * h * w;
+  return n + d->dense * flat + d->dense + d->dense + 1;
+}
+
+// Direct convolution, 3x3, stride 1, zero padding 1, input/output [C][H][W].
+void oracle_conv3x3(const double* in, int32_t cin, int32_t h, int32_t w, const double* wt,
+                    const double* bias, int32_t cout, double* out) {
+  for (int o = 0; o < cout; ++o)
+    for (int y = 0; y < h; ++y)
+      for (int x = 0; x < w; ++x) {
+        double s = bias[o];
+        for (int c = 0; c < cin; ++c)
+          for (int dy = 0; dy < 3; ++dy)
+            for (int dx = 0; dx < 3; ++dx) {
+              int yy = y + dy - 1, xx = x + dx - 1;
+              if (yy < 0 || yy >= h || xx < 0 || xx >= w) continue;
+              s += wt[(((size_t)o * cin + c) * 3 + dy) * 3 + dx] * in[((size_t)c * h + yy) * w + xx];
+            }
+        out[((size_t)o * h + y) * w + x] = s;
+      }
+}
+
+// Evaluates the network on one frame's area sums S [in_h][in_w][3] with
+// denominator den; returns the output logit.  For bf16 networks (reading of
+// "bf16 weights and activations"), values are rounded to bf16 at the network
+// input, after each conv layer's ReLU and after the dense layer's ReLU;
+// arithmetic in between is fp64.  features_out (nullable) receives the
+// flattened input of the dense layer in (c, y, x) order.
+double oracle_cnn_logit(const oracle_cnn_desc* d, const float* blob, const int64_t* S, int64_t den,
+                        double* features_out) {
+  Net net;
+  if (!load_net(d, blob, &net)) return std::numeric_limits<double>::quiet_NaN();
+  auto rnd = [&](double v) { return net.bf16 ? round_bf16(v) : v; };
+  int c = 3, h = net.in_h, w = net.in_w;
+  // pre-processing [Sec. 7]: area average in [0, 255] mapped to [-1, 1]
+  std::vector<double> act((size_t)c * h * w);
+  for (int ch = 0; ch < 3; ++ch)
+    for (int y = 0; y < h; ++y)
+      for (int x = 0; x < w; ++x) {
+        double v = (double)S[((size_t)y * w + x) * 3 + ch] / (double)den;
+        act[((size_t)ch * h + y) * w + x] = rnd(v / 127.5 - 1.0);
+      }
+  for (int l = 0; l < net.n_conv; ++l) {
+    int co = net.cout[l];
+    std::vector<double> out((size_t)co * h * w);
+    oracle_conv3x3(act.data(), c, h, w, net.cw[l].data(), net.cb[l].data(), co, out.data());
+    for (double& v : out) v = rnd(v > 0.0 ? v : 0.0);
+    if (net.pool[l]) {
+      int ph = h / 2, pw = w / 2;
+      std::vector<double> pooled((size_t)co * ph * pw);
+      for (int o = 0; o < co; ++o)
+        for (int y = 0; y < ph; ++y)
+          for (int x = 0; x < pw; ++x) {
+            double m = out[((size_t)o * h + 2 * y) * w + 2 * x];
+            for (int dy = 0; dy < 2; ++dy)
+              for (int dx = 0; dx < 2; ++dx) {
+                double v = out[((size_t)o * h + 2 * y + dy) * w + 2 * x + dx];
+                if (v > m) m = v;
+              }
+            pooled[((size_t)o * ph + y) * pw + x] = m;
+          }
+      out.swap(pooled);
+      h = ph;
+      w = pw;
+    }
+    act.swap(out);
+    c = co;
+  }
+  if (features_out) std::memcpy(features_out, act.data(), act.size() * sizeof(double));
+  double z = net.b2;
+  for (int j = 0; j < net.dense; ++j) {
+    double s = net.b1[j];
+    for (int k = 0; k < net.flat; ++k) s += net.w1[(size_t)j * net.flat + k] * act[k];
+    double hj = rnd(s > 0.0 ? s : 0.0);
+    z += net.w2[j] * hj;
+  }
+  return z;
+}
+
+double oracle_sigmoid(double z) { return 1.0 / (1.0 + std::exp(-z)); }
+
+// Decision on the specialized model's confidence p (Sec. 3, Sec. 4):
+// p < c_low -> label 0; p > c_high -> label 1; otherwise defer (label 0).
+// Returns label | (defer << 1).
+int32_t oracle_decide(double p, double c_low, double c_high) {
+  if (p < c_low) return 0;
+  if (p > c_high) return 1;
+  return 2;
+}
+
+// ---------------------------------------------------------------- cascade
+
+struct oracle_cfg {
+  int32_t H, W;           // raw frame size
+  int32_t Ho, Wo;         // difference-detector grid
+  int32_t Hc, Wc;         // CNN input grid
+  int32_t ref_mode;       // 0: frame t - delta; 1: fixed reference image
+  int32_t delta;
+  int32_t Gh, Gw;         // 1x1: global MSE; otherwise blocked
+  const float* lr_w;      // Gh*Gw logistic-regression weights (blocked)
+  double lr_b;
+  const int64_t* ref_sums;  // fixed reference image area sums, Ho*Wo*3 (mode 1)
+  double delta_diff;
+  double c_low, c_high;
+};
+
+// Runs the cascade on frames [t0, t0 + n) (frames: n x H x W x 3 uint8).
+// state_S / state_dec: area sums (Ho*Wo*3 each) and decisions of frames
+// t0 - delta .. t0 - 1 (needed when t0 > 0 in mode 0); the updated state of
+// frames t0 + n - delta .. t0 + n - 1 is written to state_S_out / state_dec_out
+// (nullable).  Outputs per frame: score (+inf for a forced frame), fire,
+// logit and prob (NaN where the CNN did not run), label, defer.
+// Reading: frames with absolute index t < delta have no frame t - delta and
+// always fire.  Returns the number of frames that fired, or -1 on bad input.
+int64_t oracle_cascade(const oracle_cfg* cfg, const oracle_cnn_desc* net, const float* blob,
+                       const uint8_t* frames, int64_t n, int64_t t0, const int64_t* state_S,
+                       const uint8_t* state_dec, double* score, uint8_t* fire, double* logit,
+                       double* prob, uint8_t* label, uint8_t* defer, int64_t* state_S_out,
+                       uint8_t* state_dec_out) {
+  if (!cfg || !net || n < 0 || t0 < 0) return -1;
+  const int64_t cells = (int64_t)cfg->Ho * cfg->Wo * 3;
+  const int64_t den = oracle_area_den(cfg->H, cfg->W, cfg->Ho, cfg->Wo);
+  const int64_t den_c = oracle_area_den(cfg->H, cfg->W, cfg->Hc, cfg->Wc);
+  const int64_t fb = (int64_t)cfg->H * cfg->W * 3;
+  const int D = cfg->ref_mode == 0 ? cfg->delta : 0;
+  if (cfg->ref_mode == 0 && D < 1) return -1;
+  if (cfg->ref_mode == 0 && t0 > 0 && (!state_S || !state_dec)) return -1;
+  // area sums of every frame of the window (history first)
+  std::vector<int64_t> S((size_t)(D + n) * cells);
+  for (int64_t k = 0; k < D; ++k) {
+    if (t0 > 0) std::memcpy(&S[(size_t)k * cells], state_S + k * cells, cells * sizeof(int64_t));
+  }
+  for (int64_t k = 0; k < n; ++k)
+    oracle_area_sums(frames + k * fb, cfg->H, cfg->W, cfg->Ho, cfg->Wo, &S[(size_t)(D + k) * cells]);
+  std::vector<uint8_t> dec((size_t)(D + n), 0);
+  for (int64_t k = 0; k < D; ++k) dec[k] = (t0 > 0) ? state_dec[k] : 0;
+  const bool blocked = cfg->Gh * cfg->Gw > 1;
+  std::vector<int64_t> Sc((size_t)cfg->Hc * cfg->Wc * 3);
+  int64_t fired = 0;
+  for (int64_t k = 0; k < n; ++k) {
+    const int64_t t = t0 + k;
+    const int64_t* cur = &S[(size_t)(D + k) * cells];
+    double sc;
+    const bool forced = cfg->ref_mode == 0 && t < cfg->delta;
+    if (forced) {
+      sc = std::numeric_limits<double>::infinity();
+    } else {
+      const int64_t* ref = cfg->ref_mode == 0 ? &S[(size_t)k * cells] : cfg->ref_sums;
+      sc = blocked ? oracle_blocked_score(cur, ref, cfg->Ho, cfg->Wo, den, cfg->Gh, cfg->Gw,
+                                          cfg->lr_w, cfg->lr_b, nullptr)
+                   : oracle_global_mse(cur, ref, cfg->Ho, cfg->Wo, den, nullptr);
+    }
+    const bool f = forced || sc > cfg->delta_diff;
+    if (score) score[k] = sc;
+    if (fire) fire[k] = f ? 1 : 0;
+    uint8_t d;
+    if (f) {
+      ++fired;
+      oracle_area_sums(frames + k * fb, cfg->H, cfg->W, cfg->Hc, cfg->Wc, Sc.data());
+      double z = oracle_cnn_logit(net, blob, Sc.data(), den_c, nullptr);
+      double p = oracle_sigmoid(z);
+      if (logit) logit[k] = z;
+      if (prob) prob[k] = p;
+      d = (uint8_t)oracle_decide(p, cfg->c_low, cfg->c_high);
+    } else {
+      if (logit) logit[k] = std::numeric_limits<double>::quiet_NaN();
+      if (prob) prob[k] = std::numeric_limits<double>::quiet_NaN();
+      d = cfg->ref_mode == 0 ? dec[(size_t)k] : 0;  // reuse the compared frame's output
+    }
+    dec[(size_t)(D + k)] = d;
+    if (label) label[k] = d & 1;
+    if (defer) defer[k] = (d >> 1) & 1;
+  }
+  if (cfg->ref_mode == 0) {
+    for (int64_t k = 0; k < D; ++k) {
+      if (state_S_out)
+        std::memcpy(state_S_out + k * cells, &S[(size_t)(n + k) * cells], cells * sizeof(int64_t));
+      if (state_dec_out) state_dec_out[k] = dec[(size_t)(n + k)];
+    }
+  }
+  return fired;
+}
+
+}  // extern "C"

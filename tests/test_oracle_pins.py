@@ -1,0 +1,412 @@
+"""Pins of the fp64 oracle against facts fixed outside it.
+
+Each test checks the oracle against something other than itself: a hand-worked
+fixture, a closed form, an invariant, brute force on tiny inputs, or an
+independent library routine (torch CPU, numpy) for a special case.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+rng = np.random.default_rng(1234)
+
+
+def _read_golden(name):
+    rows = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                rows.append(line.split())
+    return rows
+
+
+# ------------------------------------------------------------ area averaging
+
+def test_area_5to2_hand_computed():
+    rows = _read_golden("area_5to2.txt")
+    frame = np.zeros((5, 5, 3), np.uint8)
+    for j in range(5):
+        for i in range(5):
+            frame[j, i] = (10 * j + i, 1, 0)
+    w, p = oracle.area_weights(5, 2)
+    assert p == 5
+    den = oracle.area_den(5, 5, 2, 2)
+    S = oracle.area_sums(frame, 2, 2)
+    for r in rows:
+        if r[0] == "den":
+            assert den == int(r[1])
+        elif r[0] == "weights0":
+            assert list(w[0]) == [int(x) for x in r[1:]]
+        elif r[0] == "weights1":
+            assert list(w[1]) == [int(x) for x in r[1:]]
+        elif r[0] == "S":
+            Y, X = int(r[1]), int(r[2])
+            assert list(S[Y, X]) == [int(x) for x in r[3:]]
+
+
+@pytest.mark.parametrize("n_in,n_out", [(640, 50), (480, 50), (1280, 50), (720, 50), (1280, 100),
+                                        (720, 100), (1920, 100), (1080, 100), (100, 50), (7, 3),
+                                        (13, 13)])
+def test_area_weights_partition(n_in, n_out):
+    """Every output cell receives p input units and every input pixel gives q units."""
+    w, p = oracle.area_weights(n_in, n_out)
+    g = math.gcd(n_in, n_out)
+    assert p == n_in // g
+    assert (w.sum(axis=1) == n_in // g).all()
+    assert (w.sum(axis=0) == n_out // g).all()
+    assert (w >= 0).all()
+
+
+@pytest.mark.parametrize("H,W,Ho,Wo", [(12, 20, 3, 8), (15, 10, 6, 4), (9, 9, 9, 9), (16, 24, 5, 7)])
+def test_area_sums_equal_replicated_block_sums(H, W, Ho, Wo):
+    """Exact area averaging equals: replicate each pixel q_y x q_x times, then sum
+    p_y x p_x blocks (a textbook definition, computed here with numpy)."""
+    f = rng.integers(0, 256, size=(H, W, 3), dtype=np.uint8)
+    gy, gx = math.gcd(H, Ho), math.gcd(W, Wo)
+    py, qy, px, qx = H // gy, Ho // gy, W // gx, Wo // gx
+    up = np.repeat(np.repeat(f.astype(np.int64), qy, axis=0), qx, axis=1)
+    blocks = up.reshape(Ho, py, Wo, px, 3).sum(axis=(1, 3))
+    assert (oracle.area_sums(f, Ho, Wo) == blocks).all()
+    assert oracle.area_den(H, W, Ho, Wo) == py * px
+
+
+def test_area_integer_ratio_is_box_sum():
+    f = rng.integers(0, 256, size=(100, 100, 3), dtype=np.uint8)
+    box = f.astype(np.int64).reshape(50, 2, 50, 2, 3).sum(axis=(1, 3))
+    assert (oracle.area_sums(f, 50, 50) == box).all()
+    assert oracle.area_den(100, 100, 50, 50) == 4
+
+
+@pytest.mark.parametrize("H,W,Ho,Wo", [(480, 640, 50, 50), (720, 1280, 100, 100), (33, 17, 5, 4)])
+def test_constant_frame(H, W, Ho, Wo):
+    v = 173
+    f = np.full((H, W, 3), v, np.uint8)
+    den = oracle.area_den(H, W, Ho, Wo)
+    assert (oracle.area_sums(f, Ho, Wo) == den * v).all()
+
+
+def test_nesting_100_to_50():
+    """2x2 sums of the 100-grid give exactly the 50-grid area average."""
+    f = rng.integers(0, 256, size=(720, 1280, 3), dtype=np.uint8)
+    S100 = oracle.area_sums(f, 100, 100)
+    S50 = oracle.area_sums(f, 50, 50)
+    d100, d50 = oracle.area_den(720, 1280, 100, 100), oracle.area_den(720, 1280, 50, 50)
+    nest = S100.reshape(50, 2, 50, 2, 3).sum(axis=(1, 3))
+    # value equality as exact rationals: nest / (4 d100) == S50 / d50
+    assert (nest * d50 == S50 * 4 * d100).all()
+
+
+# ------------------------------------------------------- difference detector
+
+def test_mse_hand_computed_4x4():
+    rows = _read_golden("mse_4x4.txt")
+    a = np.full((4, 4, 3), 10, np.uint8)
+    b = a.copy()
+    b[0, 0] = (13, 14, 10)
+    b[3, 3] = (10, 10, 0)
+    for r in rows:
+        g = int(r[1])
+        den = oracle.area_den(4, 4, g, g)
+        m, E = oracle.global_mse(oracle.area_sums(a, g, g), oracle.area_sums(b, g, g), den)
+        assert E == int(r[4])
+        assert m == pytest.approx(float(r[6]), rel=1e-15)
+    assert float(rows[0][6]) == 125 / 48 and float(rows[1][6]) == 125 / 192
+
+
+def test_identical_frames_mse_zero():
+    f = rng.integers(0, 256, size=(480, 640, 3), dtype=np.uint8)
+    S = oracle.area_sums(f, 50, 50)
+    m, E = oracle.global_mse(S, S, oracle.area_den(480, 640, 50, 50))
+    assert m == 0.0 and E == 0
+
+
+@pytest.mark.parametrize("k", [1, 3, 17])
+def test_mse_of_constant_offset(k):
+    """MSE(F, F + k) = k^2 exactly when nothing clips."""
+    f = rng.integers(20, 200, size=(480, 640, 3), dtype=np.uint8)
+    den = oracle.area_den(480, 640, 50, 50)
+    m, _ = oracle.global_mse(oracle.area_sums(f, 50, 50), oracle.area_sums(f + k, 50, 50), den)
+    assert m == k * k
+
+
+def test_blocked_mean_equals_global_and_unit_grid():
+    f = rng.integers(0, 256, size=(100, 100, 3), dtype=np.uint8)
+    g = rng.integers(0, 256, size=(100, 100, 3), dtype=np.uint8)
+    den = oracle.area_den(100, 100, 100, 100)
+    a, b = oracle.area_sums(f, 100, 100), oracle.area_sums(g, 100, 100)
+    mse, _ = oracle.global_mse(a, b, den)
+    # equal-size 10x10 blocks: the mean of the block MSEs is the global MSE
+    z, m = oracle.blocked_score(a, b, den, (10, 10), np.zeros(100, np.float32), 0.0)
+    assert m.mean() == pytest.approx(mse, rel=1e-13)
+    assert z == 0.0
+    # 1x1 grid with w = 1, b = 0 is the global detector
+    z1, _ = oracle.blocked_score(a, b, den, (1, 1), np.ones(1, np.float32), 0.0)
+    assert z1 == pytest.approx(mse, rel=1e-15)
+    # bias and weights enter linearly
+    w = rng.standard_normal(100).astype(np.float32)
+    zb, mb = oracle.blocked_score(a, b, den, (10, 10), w, -2.0)
+    assert zb == pytest.approx(-2.0 + float(np.dot(w.astype(np.float64), mb)), rel=1e-12)
+
+
+def test_blocked_uneven_grid_bounds():
+    """Block k covers rows floor(by*Ho/Gh)..floor((by+1)*Ho/Gh): checked by brute force."""
+    a = rng.integers(0, 5000, size=(7, 11, 3)).astype(np.int64)
+    b = rng.integers(0, 5000, size=(7, 11, 3)).astype(np.int64)
+    den = 3
+    z, m = oracle.blocked_score(a, b, den, (3, 4), np.ones(12, np.float32), 0.0)
+    for by in range(3):
+        for bx in range(4):
+            ys = slice(by * 7 // 3, (by + 1) * 7 // 3)
+            xs = slice(bx * 11 // 4, (bx + 1) * 11 // 4)
+            d = (a[ys, xs] - b[ys, xs]).astype(np.float64) / den
+            assert m[by * 4 + bx] == pytest.approx((d ** 2).mean(), rel=1e-13)
+
+
+# --------------------------------------------------------------- CNN pieces
+
+def test_round_bf16_against_torch_and_ties():
+    import torch
+    x = (rng.standard_normal(20000) * 10.0 ** rng.integers(-6, 6, 20000)).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    got = np.array([oracle.round_bf16(float(v)) for v in x])
+    assert (got == ref).all()
+    # ties go to the even significand: 1 + 2^-8 lies halfway between 1 and 1 + 2^-7
+    assert oracle.round_bf16(1.0 + 2.0 ** -8) == 1.0
+    assert oracle.round_bf16(1.0 + 3 * 2.0 ** -8) == 1.0 + 2.0 ** -6
+    assert oracle.round_bf16(-(1.0 + 2.0 ** -8)) == -1.0
+    # monotone, so it commutes with ReLU and with max-pooling
+    s = np.sort(rng.standard_normal(5000))
+    r = np.array([oracle.round_bf16(v) for v in s])
+    assert (np.diff(r) >= 0).all()
+    assert oracle.round_bf16(0.0) == 0.0
+
+
+def test_conv3x3_against_torch():
+    import torch
+    import torch.nn.functional as F
+    for (C, O, H, Wd) in [(3, 4, 5, 5), (2, 3, 7, 4), (5, 2, 1, 1)]:
+        x = rng.standard_normal((C, H, Wd))
+        w = rng.standard_normal((O, C, 3, 3))
+        b = rng.standard_normal(O)
+        ref = F.conv2d(torch.from_numpy(x)[None], torch.from_numpy(w), torch.from_numpy(b),
+                       padding=1)[0].numpy()
+        np.testing.assert_allclose(oracle.conv3x3(x, w, b), ref, rtol=1e-12, atol=1e-12)
+
+
+def test_conv3x3_brute_force_tiny():
+    """Six nested loops written out here on a 5x5x3 -> 4 filter case."""
+    x = rng.standard_normal((3, 5, 5))
+    w = rng.standard_normal((4, 3, 3, 3))
+    b = rng.standard_normal(4)
+    ref = np.zeros((4, 5, 5))
+    for o in range(4):
+        for y in range(5):
+            for xx in range(5):
+                s = b[o]
+                for c in range(3):
+                    for dy in range(3):
+                        for dx in range(3):
+                            yy, x2 = y + dy - 1, xx + dx - 1
+                            if 0 <= yy < 5 and 0 <= x2 < 5:
+                                s += w[o, c, dy, dx] * x[c, yy, x2]
+                ref[o, y, xx] = s
+    np.testing.assert_allclose(oracle.conv3x3(x, w, b), ref, rtol=1e-13, atol=1e-13)
+
+
+def _torch_net_logit(spec, wts, S, den, bf16):
+    """The specialized CNN as a torch CPU fp64 network (independent library path)."""
+    import torch
+    import torch.nn.functional as F
+
+    def rnd(t):
+        return t.to(torch.float32).to(torch.bfloat16).to(torch.float64) if bf16 else t
+
+    x = torch.from_numpy(S.astype(np.float64) / den).permute(2, 0, 1)[None] / 127.5 - 1.0
+    x = rnd(x)
+    for w, b, p in zip(wts["conv_w"], wts["conv_b"], spec.pool):
+        x = F.conv2d(x, torch.from_numpy(w.astype(np.float64)), torch.from_numpy(b.astype(np.float64)),
+                     padding=1)
+        x = rnd(F.relu(x))
+        if p:
+            x = F.max_pool2d(x, 2)
+    f = x.flatten(1)
+    h = rnd(F.relu(f @ torch.from_numpy(wts["w1"].astype(np.float64)).T +
+                   torch.from_numpy(wts["b1"].astype(np.float64))))
+    z = h @ torch.from_numpy(wts["w2"].astype(np.float64)) + float(wts["b2"][0])
+    return float(z[0])
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+@pytest.mark.parametrize("conv,pool,dense", [((8, 8), (True, True), 16),
+                                             ((8, 8, 8), (False, True, True), 12)])
+def test_cnn_against_torch(bf16, conv, pool, dense):
+    spec = synth.CNNSpec(in_h=11, in_w=9, conv=conv, pool=pool, dense=dense, bf16=bf16)
+    wts = synth.cnn_weights(spec, 7)
+    blob = synth.weight_blob(spec, wts)
+    for trial in range(3):
+        den = 7
+        S = rng.integers(0, 255 * den + 1, size=(11, 9, 3)).astype(np.int64)
+        z = oracle.cnn_logit(spec, blob, S, den)
+        ref = _torch_net_logit(spec, wts, S, den, bf16)
+        assert z == pytest.approx(ref, rel=1e-9, abs=1e-12)
+
+
+def test_cnn_zero_weights_and_center_tap():
+    spec = synth.CNNSpec(in_h=4, in_w=4, conv=(2,), pool=(False,), dense=3, bf16=False)
+    wts = synth.cnn_weights(spec, 3)
+    zero = {k: ([np.zeros_like(a) for a in v] if isinstance(v, list) else np.zeros_like(v))
+            for k, v in wts.items()}
+    zero["b2"] = np.array([0.75], np.float32)
+    S = rng.integers(0, 256, size=(4, 4, 3)).astype(np.int64)
+    z = oracle.cnn_logit(spec, synth.weight_blob(spec, zero), S, 1)
+    assert z == 0.75
+    # b2 = 0 gives p = 0.5, which defers under (0.2, 0.8)
+    assert oracle.sigmoid(0.0) == 0.5 and oracle.decide(0.5, 0.2, 0.8) == 2
+    # centre-tap-only conv: channel o of the conv output is a per-pixel linear map
+    cw = np.zeros((2, 3, 3, 3), np.float32)
+    cw[0, 0, 1, 1], cw[1, 2, 1, 1] = 2.0, -1.0
+    t = dict(conv_w=[cw], conv_b=[np.array([0.5, 0.25], np.float32)],
+             w1=np.zeros((3, 32), np.float32), b1=np.zeros(3, np.float32),
+             w2=np.zeros(3, np.float32), b2=np.zeros(1, np.float32))
+    t["w1"][0, 5] = 1.0    # feature (c=0, y=1, x=1)
+    t["w1"][1, 16 + 6] = 1.0  # feature (c=1, y=1, x=2)
+    t["w2"][:] = (1.0, 1.0, 0.0)
+    _, feats = oracle.cnn_logit(spec, synth.weight_blob(spec, t), S, 1, want_features=True)
+    x = S / 127.5 - 1.0
+    assert feats[5] == pytest.approx(max(0.0, 2.0 * x[1, 1, 0] + 0.5), rel=1e-15)
+    assert feats[16 + 6] == pytest.approx(max(0.0, -x[1, 2, 2] + 0.25), rel=1e-15)
+    z = oracle.cnn_logit(spec, synth.weight_blob(spec, t), S, 1)
+    assert z == pytest.approx(feats[5] + feats[16 + 6], rel=1e-15)
+
+
+def test_decision_rule_ties_defer():
+    assert oracle.decide(0.1, 0.2, 0.8) == 0
+    assert oracle.decide(0.9, 0.2, 0.8) == 1
+    assert oracle.decide(0.2, 0.2, 0.8) == 2
+    assert oracle.decide(0.8, 0.2, 0.8) == 2
+    assert oracle.decide(0.5, 0.2, 0.8) == 2
+
+
+# ------------------------------------------------------------------ cascade
+
+def _small(wl, n):
+    v = synth.Video(wl.video)
+    wts = synth.cnn_weights(wl.cnn, wl.weight_seed)
+    return v, synth.weight_blob(wl.cnn, wts)
+
+
+def _tiny_fast(**kw):
+    """TINY with a smaller CNN so the cascade pins run in seconds."""
+    spec = synth.CNNSpec(in_h=50, in_w=50, conv=(4, 4), pool=(True, True), dense=8, bf16=False)
+    return W.TINY.replace(cnn=spec, **kw)
+
+
+def test_cascade_chain_rule_brute_force():
+    for delta in (1, 3, 7):
+        wl = _tiny_fast(delta=delta)
+        v, blob = _small(wl, 300)
+        frames = v.frames(150, 450)
+        cfg, keep = oracle.make_cfg(wl)
+        out, _ = oracle.cascade(cfg, wl.cnn, blob, frames, t0=0)
+        n = len(frames)
+        # recompute the outputs in plain Python from the oracle's scores and probs
+        lab = np.zeros(n, np.uint8)
+        dfr = np.zeros(n, np.uint8)
+        for t in range(n):
+            fires = t < delta or out["score"][t] > wl.delta_diff
+            assert bool(out["fire"][t]) == fires
+            if fires:
+                p = out["prob"][t]
+                assert p == pytest.approx(1 / (1 + math.exp(-out["logit"][t])), rel=1e-15)
+                lab[t], dfr[t] = (0, 0) if p < wl.c_low else ((1, 0) if p > wl.c_high else (0, 1))
+            else:
+                lab[t], dfr[t] = lab[t - delta], dfr[t - delta]
+        assert (lab == out["label"]).all() and (dfr == out["defer"]).all()
+
+
+def test_cascade_delta1_forward_fill():
+    wl = _tiny_fast(delta=1, c_low=0.45, c_high=0.55)
+    v, blob = _small(wl, 400)
+    frames = v.frames(100, 500)
+    cfg, keep = oracle.make_cfg(wl)
+    out, _ = oracle.cascade(cfg, wl.cnn, blob, frames)
+    last = None
+    for t in range(len(frames)):
+        if out["fire"][t]:
+            last = t
+        assert last is not None
+        assert out["label"][t] == out["label"][last] and out["defer"][t] == out["defer"][last]
+
+
+def test_survivors_monotone_in_threshold():
+    wl = _tiny_fast()
+    v, blob = _small(wl, 300)
+    frames = v.frames(200, 500)
+    prev = None
+    for dd in [-1.0, 0.0, 4.5, 10.0, 20.0, 60.0, 1e9]:
+        cfg, keep = oracle.make_cfg(wl.replace(delta_diff=dd))
+        out, _ = oracle.cascade(cfg, wl.cnn, blob, frames)
+        s = set(np.flatnonzero(out["fire"]))
+        if prev is not None:
+            assert s <= prev
+        prev = s
+    # delta_diff = +inf leaves only the forced frames t < delta
+    cfg, keep = oracle.make_cfg(wl.replace(delta_diff=math.inf))
+    out, _ = oracle.cascade(cfg, wl.cnn, blob, frames)
+    assert list(np.flatnonzero(out["fire"])) == list(range(wl.delta))
+    cfg, keep = oracle.make_cfg(wl.replace(delta_diff=-math.inf))
+    out, _ = oracle.cascade(cfg, wl.cnn, blob, frames)
+    assert out["fire"].all()
+
+
+def test_compaction_is_ascending_fired_list():
+    wl = _tiny_fast()
+    v, blob = _small(wl, 300)
+    cfg, keep = oracle.make_cfg(wl)
+    out, _ = oracle.cascade(cfg, wl.cnn, blob, v.frames(300, 600))
+    idx = np.flatnonzero(out["fire"])
+    assert out["fired"] == len(idx) == int(out["fire"].sum())
+    assert np.isnan(out["logit"][out["fire"] == 0]).all()
+    assert not np.isnan(out["logit"][idx]).any()
+
+
+def test_chunk_invariance_and_determinism():
+    for delta in (1, 4):
+        wl = _tiny_fast(delta=delta, c_low=0.45, c_high=0.55)
+        v, blob = _small(wl, 300)
+        frames = v.frames(180, 480)
+        cfg, keep = oracle.make_cfg(wl)
+        full, _ = oracle.cascade(cfg, wl.cnn, blob, frames)
+        again, _ = oracle.cascade(cfg, wl.cnn, blob, frames)
+        for k in ("score", "fire", "label", "defer"):
+            assert (full[k] == again[k]).all()
+        parts, state, t0 = [], None, 0
+        for size in (37, 3, 1, 100, 159):
+            o, state = oracle.cascade(cfg, wl.cnn, blob, frames[t0:t0 + size], t0=t0, state=state)
+            parts.append(o)
+            t0 += size
+        for k in ("fire", "label", "defer"):
+            assert (np.concatenate([p[k] for p in parts]) == full[k]).all()
+        np.testing.assert_array_equal(np.concatenate([p["score"] for p in parts]), full["score"])
+
+
+def test_fixed_reference_mode():
+    wl = _tiny_fast(ref_mode=W.FIXED)
+    v, blob = _small(wl, 200)
+    frames = v.frames(0, 60)
+    ref = oracle.area_sums(frames[10], wl.dd_h, wl.dd_w)
+    cfg, keep = oracle.make_cfg(wl, ref_sums=ref)
+    out, _ = oracle.cascade(cfg, wl.cnn, blob, frames)
+    assert out["score"][10] == 0.0 and out["fire"][10] == 0
+    # a non-firing frame is labelled "no object" without deferring
+    nf = out["fire"] == 0
+    assert (out["label"][nf] == 0).all() and (out["defer"][nf] == 0).all()
+    assert np.isfinite(out["score"]).all()
