@@ -1,0 +1,236 @@
+/*
+ * nsc.h -- C ABI of the NoScope cascade filter on MI355X (gfx950).
+ *
+ * The cascade answers a binary presence query over fixed-camera video (Sec. 3
+ * of Kang et al., "NoScope: Optimizing Neural Network Queries over Video at
+ * Scale", VLDB 2017): for every frame it outputs a label (object present or
+ * not) or defers the frame to the expensive reference network.  The target
+ * object is implicit in the specialized model's weights (Sec. 4).
+ *
+ * Per frame the hot path is:
+ *   1. downsample: exact area average onto a small grid (Sec. 7 resizes frames
+ *      before the models); kept as integer area sums S with one denominator;
+ *   2. difference detector (Sec. 5): MSE against the frame `delta` earlier or
+ *      against a fixed reference image, globally or per grid block weighed by
+ *      logistic regression; fires when the metric exceeds delta_diff;
+ *   3. compaction of the frames that fire (Sec. 7 batches frames for the GPU);
+ *   4. specialized CNN on the survivors (Sec. 4), pre-processed to [-1, 1]
+ *      (Sec. 7); confidence c = sigmoid(logit) against c_low / c_high;
+ *   5. decision: c < c_low -> label 0, c > c_high -> label 1, otherwise defer;
+ *      a frame on which the earlier-frame detector does not fire reuses the
+ *      output of the frame it was compared with (Sec. 5); with a fixed
+ *      reference image it is labelled "no object".
+ *
+ * Conventions for every entry point:
+ *  - Pointers marked (device) are caller-owned device memory, (host) are host
+ *    memory.  Frames are uint8 RGB, interleaved, row-major [H][W][3], one
+ *    frame every `frame_stride` bytes.
+ *  - All GPU work is enqueued on `stream` (a hipStream_t passed as void*;
+ *    NULL is the default stream) and the call returns after enqueueing.
+ *  - Arguments are validated on the host before any HIP call; the return
+ *    value is NSC_OK (0) or a negative nsc_status, and nsc_last_error()
+ *    returns a thread-local description.  Outputs are unspecified after an
+ *    error.  Faults of already-enqueued work surface on a later HIP call.
+ *  - The library owns only what its own *_create calls allocate (packed CNN
+ *    weights); it allocates nothing else.  Scratch space is the caller's
+ *    workspace, whose size the *_workspace_bytes calls report.
+ *  - Calls that share a workspace or state buffer must be ordered on one
+ *    stream by the caller.
+ */
+#ifndef NSC_H_
+#define NSC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum nsc_status {
+  NSC_OK = 0,
+  NSC_E_INVAL = -1,     /* null pointer, NaN or out-of-range scalar        */
+  NSC_E_SHAPE = -2,     /* shape outside the supported limits             */
+  NSC_E_DTYPE = -3,     /* unknown element type                           */
+  NSC_E_WORKSPACE = -4, /* workspace missing, too small or misaligned     */
+  NSC_E_HIP = -5,       /* a HIP runtime call or kernel launch failed      */
+  NSC_E_NOMEM = -6,     /* device allocation failed                       */
+  NSC_E_STATE = -7      /* state does not hold the frames before t0       */
+} nsc_status;
+
+enum { NSC_REF_PREV = 0, NSC_REF_FIXED = 1 };
+enum { NSC_F32 = 0, NSC_BF16 = 1 };
+enum { NSC_MAX_CONV = 8, NSC_MAX_DELTA = 256, NSC_MAX_BLOCKS = 1024 };
+
+/* Stage boundaries at which nsc_cascade_run records optional events:
+ * [0] start, [1] after the area sums, [2] after the detector, [3] after the
+ * compaction, [4] after the CNN, [5] after label resolution (the end). */
+enum { NSC_STAGE_EVENTS = 6 };
+
+/* Difference-detector and decision settings of one video stream (Sec. 5, 6). */
+typedef struct nsc_cascade_cfg {
+  int32_t in_h, in_w;        /* raw frame size                                   */
+  int64_t frame_stride;      /* bytes between frames, >= in_h*in_w*3             */
+  int32_t dd_h, dd_w;        /* detector grid, 1 <= dd <= in (downsampling only)  */
+  int32_t cnn_h, cnn_w;      /* CNN input grid; dd_h = fy*cnn_h, dd_w = fx*cnn_w  */
+  int32_t ref_mode;          /* NSC_REF_PREV (frame t-delta) or NSC_REF_FIXED     */
+  int32_t delta;             /* PREV: comparison offset, 1..NSC_MAX_DELTA frames  */
+  int32_t grid_h, grid_w;    /* 1x1: global MSE; otherwise blocked detector       */
+  const float* lr_w;         /* (device) grid_h*grid_w LR weights, row-major;
+                                blocked only                                     */
+  double lr_b;               /* LR bias; blocked only                            */
+  const int32_t* ref_sums;   /* (device) FIXED: reference image area sums on the
+                                detector grid, [dd_h][dd_w][3], as produced by
+                                nsc_downsample                                   */
+  double delta_diff;         /* fire iff metric > delta_diff                      */
+  double c_low, c_high;      /* 0 <= c_low <= c_high <= 1                         */
+} nsc_cascade_cfg;
+
+/* Shape of a specialized CNN (Sec. 4): n_conv x [conv3x3 'same' + bias + ReLU
+ * (+ 2x2/2 max-pool, floor)], flatten, dense `dense` + ReLU, dense 1 -> logit. */
+typedef struct nsc_cnn_desc {
+  int32_t n_conv;                 /* 1..NSC_MAX_CONV                          */
+  int32_t conv_out[NSC_MAX_CONV]; /* output channels per layer: multiples of 16;
+                                     inner layers' inputs multiples of 32 (bf16)
+                                     or 4 (f32)                               */
+  uint32_t pool_after_mask;       /* bit l: max-pool after conv layer l        */
+  int32_t dense;                  /* hidden units, multiple of 16             */
+  int32_t in_h, in_w;             /* input grid (equal to cfg cnn_h, cnn_w)    */
+  int32_t dtype;                  /* NSC_F32 or NSC_BF16 weights/activations   */
+} nsc_cnn_desc;
+
+typedef struct nsc_cnn nsc_cnn; /* opaque: packed device weights */
+
+/* Optional per-frame outputs of nsc_cascade_run (each pointer nullable, device). */
+typedef struct nsc_frame_outputs {
+  double* score;  /* [n] detector metric (+inf for a frame forced to fire)   */
+  uint8_t* fire;  /* [n] 1 if the detector fired                             */
+  float* logit;   /* [n] CNN logit of fired frames, NaN elsewhere            */
+} nsc_frame_outputs;
+
+/* Host-side summary of a run; filling it synchronises `stream`. */
+typedef struct nsc_run_stats {
+  int64_t frames;   /* n                                  */
+  int64_t fired;    /* frames the detector passed to the CNN */
+  int64_t positive; /* frames labelled 1 without deferral */
+  int64_t deferred; /* frames deferred to the reference network */
+} nsc_run_stats;
+
+/* ---------------------------------------------------------------- helpers */
+
+/* Status name, e.g. "NSC_E_SHAPE".  Never NULL. */
+const char* nsc_status_string(int status);
+/* Description of the last error on the calling thread ("" if none). */
+const char* nsc_last_error(void);
+
+/* Denominator of the area sums from in_h x in_w onto out_h x out_w: an output
+ * value is S / den.  den = (in_h/g_h) * (in_w/g_w) with g = gcd(in, out).
+ * Returns a negative nsc_status on invalid sizes. */
+int64_t nsc_area_den(int32_t in_h, int32_t in_w, int32_t out_h, int32_t out_w);
+
+/* Validates a configuration without touching the GPU. */
+int nsc_cfg_check(const nsc_cascade_cfg* cfg);
+/* Validates a CNN description against an input grid without touching the GPU. */
+int nsc_cnn_check(const nsc_cnn_desc* desc);
+
+/* -------------------------------------------------------------- CNN handle */
+
+/* Number of floats of the canonical weight blob of `desc`:
+ *   per conv layer: weights [Cout][Cin][3][3] then bias [Cout];
+ *   dense: weights [D][F] (F = C*h*w of the last pooled map, flattened in
+ *   (c, y, x) order) then bias [D]; output: weights [D] then bias [1].
+ * Returns a negative nsc_status on an invalid description. */
+int64_t nsc_cnn_blob_floats(const nsc_cnn_desc* desc);
+
+/* Packs a host fp32 weight blob (NSC_BF16 nets round each value to the
+ * nearest bf16) into device memory owned by the returned handle.  Synchronous;
+ * uses the current HIP device.  Errors: NSC_E_INVAL, NSC_E_SHAPE,
+ * NSC_E_DTYPE, NSC_E_NOMEM, NSC_E_HIP. */
+int nsc_cnn_create(const nsc_cnn_desc* desc, const float* host_weights, int64_t n_floats,
+                   nsc_cnn** out);
+/* Frees the handle's device memory (NULL is a no-op).  The caller must make
+ * sure no enqueued work still uses it. */
+int nsc_cnn_destroy(nsc_cnn* cnn);
+
+/* ----------------------------------------------------------- workspace sizes */
+
+/* Workspace of nsc_cascade_run for up to max_frames frames per call. */
+int nsc_cascade_workspace_bytes(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn,
+                                int64_t max_frames, size_t* bytes);
+/* State carried between consecutive nsc_cascade_run calls on one stream
+ * (PREV mode: area sums and decisions of the last `delta` frames). */
+int nsc_state_bytes(const nsc_cascade_cfg* cfg, size_t* bytes);
+/* Workspace of nsc_compact for n flags. */
+int nsc_compact_workspace_bytes(int64_t n, size_t* bytes);
+/* Workspace of nsc_specialized_cnn for up to max_count images. */
+int nsc_cnn_workspace_bytes(const nsc_cnn* cnn, int64_t max_count, size_t* bytes);
+
+/* --------------------------------------------------------- hot-path calls */
+
+/* Step 1 (Sec. 7, resize; exact area average).  For each of n frames:
+ *   sums_out[f][Y][X][c] = sum_j sum_i wy[Y][j] * wx[X][i] * frame_f[j][i][c]
+ * with integer overlap weights wy, wx (row sums in_h/g_h and in_w/g_w).
+ * frames (device, n frames, frame_stride apart), sums_out (device,
+ * n*out_h*out_w*3 int32).  Requires 1 <= out <= in, 255*den < 2^31.
+ * Errors: NSC_E_INVAL, NSC_E_SHAPE, NSC_E_HIP. */
+int nsc_downsample(const uint8_t* frames, int64_t n, int32_t in_h, int32_t in_w,
+                   int64_t frame_stride, int32_t out_h, int32_t out_w, int32_t* sums_out,
+                   void* stream);
+
+/* Steps 1-2 (Sec. 5).  Downsamples frames [t0, t0+n) into sums_out (device,
+ * n*dd_h*dd_w*3 int32) and scores each against its reference:
+ *   global:  score = sum (S_t - S_ref)^2 / (den^2 * dd_h*dd_w*3)   (the MSE)
+ *   blocked: score = lr_b + sum_k lr_w[k] * MSE over block k, blocks being
+ *            rows [floor(by*dd_h/grid_h), floor((by+1)*dd_h/grid_h)) x
+ *            columns likewise, k = by*grid_w + bx;
+ * S_ref is frame t-delta (PREV) or cfg->ref_sums (FIXED).  In PREV mode a
+ * frame with absolute index t < delta has no reference: score = +inf and it
+ * fires.  fire_out[i] = score > delta_diff (device, n bytes); score_out
+ * (device, n doubles) is nullable.  prev_sums (device) holds the sums of
+ * frames t0-delta .. t0-1 and is required iff PREV and t0 > 0.
+ * Errors: NSC_E_INVAL, NSC_E_SHAPE, NSC_E_HIP. */
+int nsc_diff_detect(const nsc_cascade_cfg* cfg, const uint8_t* frames, int64_t n, int64_t t0,
+                    const int32_t* prev_sums, int32_t* sums_out, double* score_out,
+                    uint8_t* fire_out, void* stream);
+
+/* Step 3 (Sec. 7, batching).  idx_out (device, n int32) receives the
+ * ascending indices i with fire[i] != 0 and count_out (device, one int32) their
+ * number.  ws: nsc_compact_workspace_bytes(n).  Errors: NSC_E_INVAL,
+ * NSC_E_WORKSPACE, NSC_E_HIP. */
+int nsc_compact(const uint8_t* fire, int64_t n, int32_t* idx_out, int32_t* count_out, void* ws,
+                size_t ws_bytes, void* stream);
+
+/* Step 4 (Sec. 4 model, Sec. 7 pre-processing).  For i < *count (device),
+ * evaluates the network on frame idx[i]'s area sums: sums (device,
+ * [*][sums_h][sums_w][3] int32 with denominator den) are summed over
+ * fy x fx cells when sums_h = fy*in_h, sums_w = fx*in_w; the input is
+ * x = (S/den')/127.5 - 1.  Writes logit_out[i] (device, float) and, if
+ * prob_out is not NULL, prob_out[i] = sigmoid(logit).  max_count bounds
+ * *count (entries beyond max_count are not evaluated).  ws:
+ * nsc_cnn_workspace_bytes(cnn, max_count).  Errors: NSC_E_INVAL,
+ * NSC_E_SHAPE, NSC_E_WORKSPACE, NSC_E_HIP. */
+int nsc_specialized_cnn(const nsc_cnn* cnn, const int32_t* sums, int32_t sums_h, int32_t sums_w,
+                        int64_t den, const int32_t* idx, const int32_t* count, int64_t max_count,
+                        float* logit_out, float* prob_out, void* ws, size_t ws_bytes,
+                        void* stream);
+
+/* Steps 1-5 on frames [t0, t0+n) of one stream.  Writes label_out and
+ * defer_out (device, n bytes each; a deferred frame has label 0).  state
+ * (device, nsc_state_bytes) carries the last delta frames between calls: with
+ * t0 = 0 its content is ignored; with t0 > 0 it must hold what the previous
+ * call (ending at frame t0) left.  ws: nsc_cascade_workspace_bytes(cfg, cnn,
+ * >= n).  outs (host struct of device pointers) and stats (host) are nullable;
+ * stats synchronises the stream.  stage_events (host array of
+ * NSC_STAGE_EVENTS hipEvent_t, nullable, entries nullable) are recorded on
+ * `stream` at the stage boundaries, for timing.  Errors: NSC_E_INVAL,
+ * NSC_E_SHAPE, NSC_E_WORKSPACE, NSC_E_STATE, NSC_E_HIP. */
+int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_t* frames,
+                    int64_t n, int64_t t0, void* state, void* ws, size_t ws_bytes,
+                    uint8_t* label_out, uint8_t* defer_out, const nsc_frame_outputs* outs,
+                    nsc_run_stats* stats, void* const* stage_events, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NSC_H_ */

@@ -23,7 +23,8 @@ def build(force: bool = True) -> str:
     """Compile the oracle with g++ (single-threaded, -O2, no fast-math)."""
     if force or not os.path.exists(SO):
         tmp = SO + ".tmp"
-        subprocess.check_call(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", SRC, "-o", tmp])
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-ffp-contract=off", "-fPIC", "-shared",
+                               SRC, "-o", tmp])
         os.replace(tmp, SO)
     return SO
 
@@ -65,14 +66,14 @@ def lib() -> ctypes.CDLL:
         L.oracle_conv3x3.restype = None
         L.oracle_conv3x3.argtypes = [_vp, _i32, _i32, _i32, _vp, _vp, _i32, _vp]
         L.oracle_cnn_logit.restype = _dbl
-        L.oracle_cnn_logit.argtypes = [_vp, _vp, _vp, _i64, _vp]
+        L.oracle_cnn_logit.argtypes = [_vp, _vp, _vp, _i64, _vp, _vp]
         L.oracle_sigmoid.restype = _dbl
         L.oracle_sigmoid.argtypes = [_dbl]
         L.oracle_decide.restype = _i32
         L.oracle_decide.argtypes = [_dbl, _dbl, _dbl]
         L.oracle_cascade.restype = _i64
         L.oracle_cascade.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _vp,
-                                     _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+                                     _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
         _LIB = L
     return _LIB
 
@@ -145,7 +146,10 @@ def conv3x3(x: np.ndarray, w: np.ndarray, b: np.ndarray) -> np.ndarray:
     return out
 
 
-def cnn_logit(spec, blob: np.ndarray, S: np.ndarray, den: int, want_features=False):
+def cnn_logit(spec, blob: np.ndarray, S: np.ndarray, den: int, want_features=False,
+              want_scale=False):
+    """Logit of one image; optionally also the dense input and the logit's scale
+    |b2| + sum_j |w2_j h_j|."""
     d = cnn_desc(spec)
     blob = _c(blob, np.float32)
     if blob.size != lib().oracle_cnn_blob_floats(ctypes.byref(d)):
@@ -153,8 +157,10 @@ def cnn_logit(spec, blob: np.ndarray, S: np.ndarray, den: int, want_features=Fal
     S = _c(S, np.int64)
     _, flat, _ = spec.shapes()
     feats = np.zeros(flat, np.float64) if want_features else None
-    z = lib().oracle_cnn_logit(ctypes.byref(d), _p(blob), _p(S), int(den), _p(feats))
-    return (z, feats) if want_features else z
+    scale = np.zeros(1)
+    z = lib().oracle_cnn_logit(ctypes.byref(d), _p(blob), _p(S), int(den), _p(feats), _p(scale))
+    out = (z,) + ((feats,) if want_features else ()) + ((float(scale[0]),) if want_scale else ())
+    return out if len(out) > 1 else z
 
 
 def sigmoid(z: float) -> float:
@@ -199,14 +205,15 @@ def cascade(cfg: Cfg, spec, blob, frames: np.ndarray, t0: int = 0, state=None):
     D = cfg.delta if cfg.ref_mode == 0 else 0
     cells = cfg.Ho * cfg.Wo * 3
     out = dict(score=np.zeros(n), fire=np.zeros(n, np.uint8), logit=np.zeros(n),
-               prob=np.zeros(n), label=np.zeros(n, np.uint8), defer=np.zeros(n, np.uint8))
+               prob=np.zeros(n), lscale=np.zeros(n), label=np.zeros(n, np.uint8),
+               defer=np.zeros(n, np.uint8))
     sS = np.zeros((max(D, 1), cells), np.int64)
     sD = np.zeros(max(D, 1), np.uint8)
     inS, inD = (None, None) if state is None else (_c(state[0], np.int64), _c(state[1], np.uint8))
     fired = lib().oracle_cascade(ctypes.byref(cfg), ctypes.byref(d), _p(blob), _p(frames), n, t0,
                                  _p(inS), _p(inD), _p(out["score"]), _p(out["fire"]),
-                                 _p(out["logit"]), _p(out["prob"]), _p(out["label"]),
-                                 _p(out["defer"]), _p(sS), _p(sD))
+                                 _p(out["logit"]), _p(out["prob"]), _p(out["lscale"]),
+                                 _p(out["label"]), _p(out["defer"]), _p(sS), _p(sD))
     if fired < 0:
         raise ValueError("oracle_cascade rejected its arguments")
     out["fired"] = int(fired)

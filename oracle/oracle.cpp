@@ -274,9 +274,13 @@ void oracle_conv3x3(const double* in, int32_t cin, int32_t h, int32_t w, const d
 // "bf16 weights and activations"), values are rounded to bf16 at the network
 // input, after each conv layer's ReLU and after the dense layer's ReLU;
 // arithmetic in between is fp64.  features_out (nullable) receives the
-// flattened input of the dense layer in (c, y, x) order.
+// flattened input of the dense layer in (c, y, x) order.  scale_out (nullable)
+// receives the logit's scale |b2| + sum_j |w2_j h_j|: the magnitude of the
+// terms the output layer adds up, against which the logit's error is measured
+// (a logit that is a small difference of large terms has no finer relative
+// precision).
 double oracle_cnn_logit(const oracle_cnn_desc* d, const float* blob, const int64_t* S, int64_t den,
-                        double* features_out) {
+                        double* features_out, double* scale_out) {
   Net net;
   if (!load_net(d, blob, &net)) return std::numeric_limits<double>::quiet_NaN();
   auto rnd = [&](double v) { return net.bf16 ? round_bf16(v) : v; };
@@ -317,12 +321,15 @@ double oracle_cnn_logit(const oracle_cnn_desc* d, const float* blob, const int64
   }
   if (features_out) std::memcpy(features_out, act.data(), act.size() * sizeof(double));
   double z = net.b2;
+  double scale = std::fabs(net.b2);
   for (int j = 0; j < net.dense; ++j) {
     double s = net.b1[j];
     for (int k = 0; k < net.flat; ++k) s += net.w1[(size_t)j * net.flat + k] * act[k];
     double hj = rnd(s > 0.0 ? s : 0.0);
     z += net.w2[j] * hj;
+    scale += std::fabs(net.w2[j] * hj);
   }
+  if (scale_out) *scale_out = scale;
   return z;
 }
 
@@ -358,14 +365,14 @@ struct oracle_cfg {
 // t0 - delta .. t0 - 1 (needed when t0 > 0 in mode 0); the updated state of
 // frames t0 + n - delta .. t0 + n - 1 is written to state_S_out / state_dec_out
 // (nullable).  Outputs per frame: score (+inf for a forced frame), fire,
-// logit and prob (NaN where the CNN did not run), label, defer.
+// logit, prob and the logit's scale (NaN where the CNN did not run), label, defer.
 // Reading: frames with absolute index t < delta have no frame t - delta and
 // always fire.  Returns the number of frames that fired, or -1 on bad input.
 int64_t oracle_cascade(const oracle_cfg* cfg, const oracle_cnn_desc* net, const float* blob,
                        const uint8_t* frames, int64_t n, int64_t t0, const int64_t* state_S,
                        const uint8_t* state_dec, double* score, uint8_t* fire, double* logit,
-                       double* prob, uint8_t* label, uint8_t* defer, int64_t* state_S_out,
-                       uint8_t* state_dec_out) {
+                       double* prob, double* lscale, uint8_t* label, uint8_t* defer,
+                       int64_t* state_S_out, uint8_t* state_dec_out) {
   if (!cfg || !net || n < 0 || t0 < 0) return -1;
   const int64_t cells = (int64_t)cfg->Ho * cfg->Wo * 3;
   const int64_t den = oracle_area_den(cfg->H, cfg->W, cfg->Ho, cfg->Wo);
@@ -406,14 +413,17 @@ int64_t oracle_cascade(const oracle_cfg* cfg, const oracle_cnn_desc* net, const 
     if (f) {
       ++fired;
       oracle_area_sums(frames + k * fb, cfg->H, cfg->W, cfg->Hc, cfg->Wc, Sc.data());
-      double z = oracle_cnn_logit(net, blob, Sc.data(), den_c, nullptr);
+      double sc_z = 0.0;
+      double z = oracle_cnn_logit(net, blob, Sc.data(), den_c, nullptr, &sc_z);
       double p = oracle_sigmoid(z);
       if (logit) logit[k] = z;
+      if (lscale) lscale[k] = sc_z;
       if (prob) prob[k] = p;
       d = (uint8_t)oracle_decide(p, cfg->c_low, cfg->c_high);
     } else {
       if (logit) logit[k] = std::numeric_limits<double>::quiet_NaN();
       if (prob) prob[k] = std::numeric_limits<double>::quiet_NaN();
+      if (lscale) lscale[k] = std::numeric_limits<double>::quiet_NaN();
       d = cfg->ref_mode == 0 ? dec[(size_t)k] : 0;  // reuse the compared frame's output
     }
     dec[(size_t)(D + k)] = d;

@@ -1,0 +1,605 @@
+// Entry points of libnsc (declared in include/nsc.h): argument validation on
+// the host, workspace layout, weight packing and the ordering of the kernels
+// of the cascade on one stream.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "nsc_internal.h"
+
+namespace nsc {
+
+static thread_local char g_err[512];
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+size_t conv_lds_bytes(const CnnLayer& L, bool bf16, int32_t* cin_lds, int32_t* w_lds,
+                      int32_t* band_w);
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr size_t kMaxLds = 160 * 1024;
+constexpr int64_t kMaxFrames = 0x7FFFFFFF;
+
+#define NSC_REQUIRE(cond, code, ...) \
+  do {                               \
+    if (!(cond)) return ::nsc::fail(code, __VA_ARGS__); \
+  } while (0)
+
+int check_area(int32_t in_h, int32_t in_w, int32_t out_h, int32_t out_w) {
+  NSC_REQUIRE(in_h >= 1 && in_w >= 1, NSC_E_SHAPE, "frame size %dx%d must be positive", in_h, in_w);
+  NSC_REQUIRE(out_h >= 1 && out_w >= 1 && out_h <= in_h && out_w <= in_w, NSC_E_SHAPE,
+              "grid %dx%d must satisfy 1 <= grid <= frame %dx%d", out_h, out_w, in_h, in_w);
+  const Axis ay = Axis::make(in_h, out_h), ax = Axis::make(in_w, out_w);
+  const int64_t den = (int64_t)ay.p * ax.p;
+  NSC_REQUIRE(255 * den < ((int64_t)1 << 31), NSC_E_SHAPE,
+              "area denominator %lld overflows 32-bit sums", (long long)den);
+  return NSC_OK;
+}
+
+int check_cfg(const nsc_cascade_cfg* c) {
+  NSC_REQUIRE(c != nullptr, NSC_E_INVAL, "cfg is NULL");
+  if (int rc = check_area(c->in_h, c->in_w, c->dd_h, c->dd_w)) return rc;
+  NSC_REQUIRE(c->frame_stride >= (int64_t)c->in_h * c->in_w * 3, NSC_E_INVAL,
+              "frame_stride %lld is below one frame (%lld bytes)", (long long)c->frame_stride,
+              (long long)c->in_h * c->in_w * 3);
+  NSC_REQUIRE(c->cnn_h >= 1 && c->cnn_w >= 1 && c->dd_h % c->cnn_h == 0 && c->dd_w % c->cnn_w == 0,
+              NSC_E_SHAPE, "CNN grid %dx%d must divide the detector grid %dx%d", c->cnn_h, c->cnn_w,
+              c->dd_h, c->dd_w);
+  const int64_t den = nsc_area_den(c->in_h, c->in_w, c->dd_h, c->dd_w);
+  const int64_t f = (int64_t)(c->dd_h / c->cnn_h) * (c->dd_w / c->cnn_w);
+  NSC_REQUIRE(255 * den * f < ((int64_t)1 << 31), NSC_E_SHAPE,
+              "CNN input sums overflow 32 bits (den %lld x %lld cells)", (long long)den, (long long)f);
+  NSC_REQUIRE(c->ref_mode == NSC_REF_PREV || c->ref_mode == NSC_REF_FIXED, NSC_E_INVAL,
+              "ref_mode %d is neither NSC_REF_PREV nor NSC_REF_FIXED", c->ref_mode);
+  if (c->ref_mode == NSC_REF_PREV)
+    NSC_REQUIRE(c->delta >= 1 && c->delta <= NSC_MAX_DELTA, NSC_E_INVAL,
+                "delta %d outside 1..%d", c->delta, NSC_MAX_DELTA);
+  else
+    NSC_REQUIRE(c->ref_sums != nullptr, NSC_E_INVAL, "fixed-reference mode needs ref_sums");
+  NSC_REQUIRE(c->grid_h >= 1 && c->grid_w >= 1 && c->grid_h <= c->dd_h && c->grid_w <= c->dd_w,
+              NSC_E_SHAPE, "block grid %dx%d must lie within the detector grid %dx%d", c->grid_h,
+              c->grid_w, c->dd_h, c->dd_w);
+  NSC_REQUIRE((int64_t)c->grid_h * c->grid_w <= NSC_MAX_BLOCKS, NSC_E_SHAPE,
+              "block grid of %d blocks exceeds %d", c->grid_h * c->grid_w, NSC_MAX_BLOCKS);
+  if (c->grid_h * c->grid_w > 1) {
+    NSC_REQUIRE(c->lr_w != nullptr, NSC_E_INVAL, "blocked detector needs lr_w");
+    NSC_REQUIRE(isfinite(c->lr_b), NSC_E_INVAL, "lr_b must be finite");
+  }
+  NSC_REQUIRE(!isnan(c->delta_diff), NSC_E_INVAL, "delta_diff is NaN");
+  NSC_REQUIRE(!isnan(c->c_low) && !isnan(c->c_high) && c->c_low >= 0.0 && c->c_high <= 1.0 &&
+                  c->c_low <= c->c_high,
+              NSC_E_INVAL, "need 0 <= c_low (%g) <= c_high (%g) <= 1", c->c_low, c->c_high);
+  // exact int64 squared-difference sums
+  const double emax = (255.0 * (double)den) * (255.0 * (double)den) * (double)c->dd_h * c->dd_w * 3;
+  NSC_REQUIRE(emax < 9.0e18, NSC_E_SHAPE, "squared-difference sums may overflow 64 bits");
+  return NSC_OK;
+}
+
+// Layer shapes of a CNN description; fills `cnn` (no device memory).
+int plan_cnn(const nsc_cnn_desc* d, Cnn* cnn) {
+  NSC_REQUIRE(d != nullptr, NSC_E_INVAL, "CNN description is NULL");
+  NSC_REQUIRE(d->dtype == NSC_F32 || d->dtype == NSC_BF16, NSC_E_DTYPE, "dtype %d is unknown",
+              d->dtype);
+  NSC_REQUIRE(d->n_conv >= 1 && d->n_conv <= NSC_MAX_CONV, NSC_E_SHAPE,
+              "n_conv %d outside 1..%d", d->n_conv, NSC_MAX_CONV);
+  NSC_REQUIRE(d->in_h >= 2 && d->in_w >= 2, NSC_E_SHAPE, "CNN input %dx%d too small", d->in_h,
+              d->in_w);
+  NSC_REQUIRE(d->dense >= 16 && d->dense <= 256 && d->dense % 16 == 0 && (d->dense / 16) != 3 &&
+                  ((d->dense / 16) & (d->dense / 16 - 1)) == 0,
+              NSC_E_SHAPE, "dense width %d must be 16, 32, 64, 128 or 256", d->dense);
+  const bool bf16 = d->dtype == NSC_BF16;
+  Cnn c{};
+  c.desc = *d;
+  c.bf16 = bf16;
+  c.n_layers = d->n_conv;
+  int cin = 3, h = d->in_h, w = d->in_w;
+  size_t woff = 0, boff = 0, act = 0;
+  for (int l = 0; l < d->n_conv; ++l) {
+    const int co = d->conv_out[l];
+    const int nt = co / 16;
+    NSC_REQUIRE(co >= 16 && co % 16 == 0 && (nt <= 4 || nt == 6 || nt == 8 || nt == 16),
+                NSC_E_SHAPE, "conv layer %d: %d output channels unsupported", l, co);
+    if (l > 0)
+      NSC_REQUIRE(cin % (bf16 ? 32 : 4) == 0, NSC_E_SHAPE,
+                  "conv layer %d: %d input channels must be a multiple of %d", l, cin,
+                  bf16 ? 32 : 4);
+    const bool pool = (d->pool_after_mask >> l) & 1u;
+    NSC_REQUIRE(!pool || (h >= 2 && w >= 2), NSC_E_SHAPE, "conv layer %d pools a %dx%d map", l, h,
+                w);
+    CnnLayer& L = c.layers[l];
+    L.cin = cin;
+    L.cout = co;
+    L.h = h;
+    L.w = w;
+    L.pool = pool;
+    L.kpad = l == 0 ? (bf16 ? 32 : 28) : 9 * cin;
+    L.w_off = woff;
+    L.b_off = boff;
+    woff += (size_t)co * L.kpad;
+    boff += co;
+    const size_t lds = conv_lds_bytes(L, bf16, nullptr, nullptr, nullptr);
+    NSC_REQUIRE(lds <= kMaxLds, NSC_E_SHAPE,
+                "conv layer %d needs %zu bytes of LDS (limit %zu)", l, lds, kMaxLds);
+    if (pool) {
+      h /= 2;
+      w /= 2;
+    }
+    act = act > (size_t)h * w * co ? act : (size_t)h * w * co;
+    cin = co;
+  }
+  c.feat_c = cin;
+  c.feat_h = h;
+  c.feat_w = w;
+  c.flat = cin * h * w;
+  c.dense = d->dense;
+  c.act_elems = act;
+  *cnn = c;
+  return NSC_OK;
+}
+
+uint16_t host_bf16(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  if ((u & 0x7F800000u) == 0x7F800000u) return (uint16_t)(u >> 16);  // inf / nan
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Workspace layout of nsc_cascade_run.
+struct RunLayout {
+  size_t sums, fire, dec, idx, count, tiles, tile_last, carry, logit, scratch, cnn, total;
+};
+
+RunLayout run_layout(const nsc_cascade_cfg* c, const Cnn& cnn, int64_t n) {
+  RunLayout L{};
+  const size_t cells = (size_t)c->dd_h * c->dd_w * 3;
+  const ResolvePlan rp = make_resolve_plan(n, 0, c->ref_mode == NSC_REF_PREV ? c->delta : 1);
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + bytes, kAlign);
+    return at;
+  };
+  L.sums = take(cells * 4 * (size_t)n);
+  L.fire = take((size_t)n);
+  L.dec = take((size_t)n);
+  L.idx = take((size_t)n * 4);
+  L.count = take(64);
+  L.tiles = take((size_t)compact_tiles(n) * 4 + 4);
+  L.tile_last = take((size_t)rp.tiles * rp.delta * 4);
+  L.carry = take((size_t)rp.tiles * rp.delta * 4);
+  L.logit = take((size_t)n * 4);
+  const size_t dmax = c->ref_mode == NSC_REF_PREV ? (size_t)c->delta : 1;
+  L.scratch = take(dmax * cells * 4 + dmax);
+  L.cnn = take(cnn_workspace_bytes(cnn, n));
+  L.total = o;
+  return L;
+}
+
+size_t state_layout_bytes(const nsc_cascade_cfg* c, size_t* sums_off, size_t* dec_off) {
+  const size_t cells = (size_t)c->dd_h * c->dd_w * 3;
+  const size_t d = c->ref_mode == NSC_REF_PREV ? (size_t)c->delta : 0;
+  if (sums_off) *sums_off = 0;
+  if (dec_off) *dec_off = align_up(d * cells * 4, kAlign);
+  return align_up(d * cells * 4, kAlign) + align_up(d > 0 ? d : 1, kAlign);
+}
+
+}  // namespace
+}  // namespace nsc
+
+using namespace nsc;
+
+struct nsc_cnn {
+  Cnn c;
+};
+
+extern "C" {
+
+const char* nsc_status_string(int s) {
+  switch (s) {
+    case NSC_OK: return "NSC_OK";
+    case NSC_E_INVAL: return "NSC_E_INVAL";
+    case NSC_E_SHAPE: return "NSC_E_SHAPE";
+    case NSC_E_DTYPE: return "NSC_E_DTYPE";
+    case NSC_E_WORKSPACE: return "NSC_E_WORKSPACE";
+    case NSC_E_HIP: return "NSC_E_HIP";
+    case NSC_E_NOMEM: return "NSC_E_NOMEM";
+    case NSC_E_STATE: return "NSC_E_STATE";
+    default: return "NSC_E_UNKNOWN";
+  }
+}
+
+const char* nsc_last_error(void) { return g_err; }
+
+int64_t nsc_area_den(int32_t in_h, int32_t in_w, int32_t out_h, int32_t out_w) {
+  if (int rc = check_area(in_h, in_w, out_h, out_w)) return rc;
+  return (int64_t)Axis::make(in_h, out_h).p * Axis::make(in_w, out_w).p;
+}
+
+int nsc_cfg_check(const nsc_cascade_cfg* cfg) {
+  g_err[0] = 0;
+  return check_cfg(cfg);
+}
+
+int nsc_cnn_check(const nsc_cnn_desc* desc) {
+  g_err[0] = 0;
+  Cnn c;
+  return plan_cnn(desc, &c);
+}
+
+int64_t nsc_cnn_blob_floats(const nsc_cnn_desc* desc) {
+  Cnn c;
+  if (int rc = plan_cnn(desc, &c)) return rc;
+  int64_t n = 0;
+  for (int l = 0; l < c.n_layers; ++l)
+    n += (int64_t)c.layers[l].cout * c.layers[l].cin * 9 + c.layers[l].cout;
+  return n + (int64_t)c.dense * c.flat + 2 * c.dense + 1;
+}
+
+int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, nsc_cnn** out) {
+  g_err[0] = 0;
+  NSC_REQUIRE(out != nullptr && hw != nullptr, NSC_E_INVAL, "weights or out pointer is NULL");
+  *out = nullptr;
+  Cnn c;
+  if (int rc = plan_cnn(desc, &c)) return rc;
+  const int64_t need = nsc_cnn_blob_floats(desc);
+  NSC_REQUIRE(n_floats == need, NSC_E_INVAL, "weight blob has %lld floats, the network needs %lld",
+              (long long)n_floats, (long long)need);
+  const size_t es = c.bf16 ? 2 : 4;
+  // host packing
+  size_t conv_elems = 0, bias_elems = 0;
+  for (int l = 0; l < c.n_layers; ++l) {
+    conv_elems += (size_t)c.layers[l].cout * c.layers[l].kpad;
+    bias_elems += c.layers[l].cout;
+  }
+  std::vector<float> convw(conv_elems, 0.0f), convb(bias_elems, 0.0f);
+  const float* p = hw;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const CnnLayer& L = c.layers[l];
+    for (int o = 0; o < L.cout; ++o)
+      for (int ci = 0; ci < L.cin; ++ci)
+        for (int t = 0; t < 9; ++t) {
+          const float v = p[((size_t)o * L.cin + ci) * 9 + t];
+          const size_t k = l == 0 ? (size_t)t * 3 + ci : (size_t)t * L.cin + ci;
+          convw[L.w_off + (size_t)o * L.kpad + k] = v;
+        }
+    p += (size_t)L.cout * L.cin * 9;
+    for (int o = 0; o < L.cout; ++o) convb[L.b_off + o] = p[o];
+    p += L.cout;
+  }
+  std::vector<float> w1((size_t)c.dense * c.flat);
+  for (int j = 0; j < c.dense; ++j)
+    for (int ch = 0; ch < c.feat_c; ++ch)
+      for (int y = 0; y < c.feat_h; ++y)
+        for (int x = 0; x < c.feat_w; ++x)
+          w1[(size_t)j * c.flat + ((size_t)y * c.feat_w + x) * c.feat_c + ch] =
+              p[(size_t)j * c.flat + ((size_t)ch * c.feat_h + y) * c.feat_w + x];
+  p += (size_t)c.dense * c.flat;
+  std::vector<float> b1(p, p + c.dense);
+  p += c.dense;
+  std::vector<float> w2(p, p + c.dense);
+  p += c.dense;
+  c.b2 = *p;
+  // device image: [conv_w][conv_b][w1][b1][w2]
+  const size_t o_cw = 0;
+  const size_t o_cb = align_up(o_cw + conv_elems * es, kAlign);
+  const size_t o_w1 = align_up(o_cb + bias_elems * 4, kAlign);
+  const size_t o_b1 = align_up(o_w1 + w1.size() * es, kAlign);
+  const size_t o_w2 = align_up(o_b1 + (size_t)c.dense * 4, kAlign);
+  const size_t total = align_up(o_w2 + (size_t)c.dense * 4, kAlign);
+  std::vector<unsigned char> img(total, 0);
+  auto put = [&](size_t off, const std::vector<float>& v, bool as_bf16) {
+    if (as_bf16) {
+      uint16_t* d = reinterpret_cast<uint16_t*>(img.data() + off);
+      for (size_t i = 0; i < v.size(); ++i) d[i] = host_bf16(v[i]);
+    } else {
+      memcpy(img.data() + off, v.data(), v.size() * 4);
+    }
+  };
+  put(o_cw, convw, c.bf16);
+  put(o_cb, convb, false);
+  put(o_w1, w1, c.bf16);
+  put(o_b1, b1, false);
+  put(o_w2, w2, false);
+  void* dev = nullptr;
+  if (hipMalloc(&dev, total) != hipSuccess)
+    return fail(NSC_E_NOMEM, "hipMalloc of %zu bytes for CNN weights failed", total);
+  if (hipMemcpy(dev, img.data(), total, hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipFree(dev);
+    return fail(NSC_E_HIP, "copying CNN weights to the device failed");
+  }
+  unsigned char* b = static_cast<unsigned char*>(dev);
+  c.dev = dev;
+  c.conv_w = b + o_cw;
+  c.conv_b = reinterpret_cast<float*>(b + o_cb);
+  c.w1 = b + o_w1;
+  c.b1 = reinterpret_cast<float*>(b + o_b1);
+  c.w2 = reinterpret_cast<float*>(b + o_w2);
+  nsc_cnn* h = new (std::nothrow) nsc_cnn;
+  if (!h) {
+    (void)hipFree(dev);
+    return fail(NSC_E_NOMEM, "out of host memory");
+  }
+  h->c = c;
+  *out = h;
+  return NSC_OK;
+}
+
+int nsc_cnn_destroy(nsc_cnn* cnn) {
+  if (!cnn) return NSC_OK;
+  hipError_t e = hipFree(cnn->c.dev);
+  delete cnn;
+  return e == hipSuccess ? NSC_OK : fail(NSC_E_HIP, "hipFree failed: %s", hipGetErrorString(e));
+}
+
+int nsc_cascade_workspace_bytes(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, int64_t max_frames,
+                                size_t* bytes) {
+  g_err[0] = 0;
+  if (int rc = check_cfg(cfg)) return rc;
+  NSC_REQUIRE(cnn != nullptr && bytes != nullptr, NSC_E_INVAL, "cnn or bytes is NULL");
+  NSC_REQUIRE(max_frames >= 0 && max_frames <= kMaxFrames, NSC_E_INVAL, "max_frames %lld out of range",
+              (long long)max_frames);
+  *bytes = run_layout(cfg, cnn->c, max_frames).total;
+  return NSC_OK;
+}
+
+int nsc_state_bytes(const nsc_cascade_cfg* cfg, size_t* bytes) {
+  g_err[0] = 0;
+  if (int rc = check_cfg(cfg)) return rc;
+  NSC_REQUIRE(bytes != nullptr, NSC_E_INVAL, "bytes is NULL");
+  *bytes = state_layout_bytes(cfg, nullptr, nullptr);
+  return NSC_OK;
+}
+
+int nsc_compact_workspace_bytes(int64_t n, size_t* bytes) {
+  g_err[0] = 0;
+  NSC_REQUIRE(bytes != nullptr && n >= 0 && n <= kMaxFrames, NSC_E_INVAL, "bad arguments");
+  *bytes = (size_t)compact_tiles(n) * 4 + 4;
+  return NSC_OK;
+}
+
+int nsc_cnn_workspace_bytes(const nsc_cnn* cnn, int64_t max_count, size_t* bytes) {
+  g_err[0] = 0;
+  NSC_REQUIRE(cnn != nullptr && bytes != nullptr && max_count >= 0 && max_count <= kMaxFrames,
+              NSC_E_INVAL, "bad arguments");
+  *bytes = cnn_workspace_bytes(cnn->c, max_count);
+  return NSC_OK;
+}
+
+int nsc_downsample(const uint8_t* frames, int64_t n, int32_t in_h, int32_t in_w,
+                   int64_t frame_stride, int32_t out_h, int32_t out_w, int32_t* sums_out,
+                   void* stream) {
+  g_err[0] = 0;
+  if (int rc = check_area(in_h, in_w, out_h, out_w)) return rc;
+  NSC_REQUIRE(n >= 0 && n <= kMaxFrames, NSC_E_INVAL, "n = %lld out of range", (long long)n);
+  NSC_REQUIRE(frame_stride >= (int64_t)in_h * in_w * 3, NSC_E_INVAL, "frame_stride too small");
+  if (n == 0) return NSC_OK;
+  NSC_REQUIRE(frames != nullptr && sums_out != nullptr, NSC_E_INVAL, "frames or sums_out is NULL");
+  AreaPlan p;
+  if (int rc = make_area_plan(in_h, in_w, frame_stride, frames, out_h, out_w, n, &p)) return rc;
+  return launch_area_sums(p, frames, frame_stride, n, sums_out, (hipStream_t)stream);
+}
+
+int nsc_diff_detect(const nsc_cascade_cfg* cfg, const uint8_t* frames, int64_t n, int64_t t0,
+                    const int32_t* prev_sums, int32_t* sums_out, double* score_out,
+                    uint8_t* fire_out, void* stream) {
+  g_err[0] = 0;
+  if (int rc = check_cfg(cfg)) return rc;
+  NSC_REQUIRE(n >= 0 && n <= kMaxFrames && t0 >= 0, NSC_E_INVAL, "n or t0 out of range");
+  if (n == 0) return NSC_OK;
+  NSC_REQUIRE(frames && sums_out && fire_out, NSC_E_INVAL, "frames, sums_out or fire_out is NULL");
+  NSC_REQUIRE(!(cfg->ref_mode == NSC_REF_PREV && t0 > 0 && prev_sums == nullptr), NSC_E_STATE,
+              "t0 > 0 in earlier-frame mode needs the sums of the previous delta frames");
+  const hipStream_t st = (hipStream_t)stream;
+  AreaPlan p;
+  if (int rc = make_area_plan(cfg->in_h, cfg->in_w, cfg->frame_stride, frames, cfg->dd_h, cfg->dd_w,
+                              n, &p))
+    return rc;
+  if (int rc = launch_area_sums(p, frames, cfg->frame_stride, n, sums_out, st)) return rc;
+  const double den = (double)nsc_area_den(cfg->in_h, cfg->in_w, cfg->dd_h, cfg->dd_w);
+  DiffArgs a{};
+  a.sums = sums_out;
+  a.prev_sums = prev_sums;
+  a.ref_sums = cfg->ref_sums;
+  a.lr_w = cfg->lr_w;
+  a.lr_b = cfg->lr_b;
+  a.delta_diff = cfg->delta_diff;
+  a.den2 = den * den;
+  a.n = n;
+  a.t0 = t0;
+  a.dd_h = cfg->dd_h;
+  a.dd_w = cfg->dd_w;
+  a.grid_h = cfg->grid_h;
+  a.grid_w = cfg->grid_w;
+  a.ref_mode = cfg->ref_mode;
+  a.delta = cfg->ref_mode == NSC_REF_PREV ? cfg->delta : 0;
+  a.score = score_out;
+  a.fire = fire_out;
+  return launch_diff(a, st);
+}
+
+int nsc_compact(const uint8_t* fire, int64_t n, int32_t* idx_out, int32_t* count_out, void* ws,
+                size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  NSC_REQUIRE(n >= 0 && n <= kMaxFrames, NSC_E_INVAL, "n = %lld out of range", (long long)n);
+  NSC_REQUIRE(count_out != nullptr, NSC_E_INVAL, "count_out is NULL");
+  if (n > 0) {
+    NSC_REQUIRE(fire && idx_out, NSC_E_INVAL, "fire or idx_out is NULL");
+    const size_t need = (size_t)compact_tiles(n) * 4 + 4;
+    NSC_REQUIRE(ws != nullptr && ws_bytes >= need && ((uintptr_t)ws & 3) == 0, NSC_E_WORKSPACE,
+                "compaction needs %zu bytes of 4-byte aligned workspace", need);
+  }
+  return launch_compact(fire, n, idx_out, count_out, static_cast<int32_t*>(ws), (hipStream_t)stream);
+}
+
+int nsc_specialized_cnn(const nsc_cnn* cnn, const int32_t* sums, int32_t sums_h, int32_t sums_w,
+                        int64_t den, const int32_t* idx, const int32_t* count, int64_t max_count,
+                        float* logit_out, float* prob_out, void* ws, size_t ws_bytes,
+                        void* stream) {
+  g_err[0] = 0;
+  NSC_REQUIRE(cnn != nullptr, NSC_E_INVAL, "cnn is NULL");
+  const Cnn& c = cnn->c;
+  NSC_REQUIRE(max_count >= 0 && max_count <= kMaxFrames, NSC_E_INVAL, "max_count out of range");
+  NSC_REQUIRE(sums_h >= c.desc.in_h && sums_w >= c.desc.in_w && sums_h % c.desc.in_h == 0 &&
+                  sums_w % c.desc.in_w == 0,
+              NSC_E_SHAPE, "sums grid %dx%d does not nest onto the CNN input %dx%d", sums_h, sums_w,
+              c.desc.in_h, c.desc.in_w);
+  NSC_REQUIRE(den >= 1, NSC_E_INVAL, "den must be positive");
+  if (max_count == 0) return NSC_OK;
+  NSC_REQUIRE(sums && idx && count && logit_out, NSC_E_INVAL, "a required pointer is NULL");
+  NSC_REQUIRE(ws != nullptr && ((uintptr_t)ws % kAlign) == 0, NSC_E_WORKSPACE,
+              "workspace must be 256-byte aligned");
+  CnnRunArgs r{};
+  r.sums = sums;
+  r.sums_h = sums_h;
+  r.sums_w = sums_w;
+  r.fy = sums_h / c.desc.in_h;
+  r.fx = sums_w / c.desc.in_w;
+  r.den_c = (double)den * r.fy * r.fx;
+  r.idx = idx;
+  r.count = count;
+  r.max_count = max_count;
+  r.logit = logit_out;
+  r.prob = prob_out;
+  return run_cnn(c, r, ws, ws_bytes, (hipStream_t)stream);
+}
+
+int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_t* frames,
+                    int64_t n, int64_t t0, void* state, void* ws, size_t ws_bytes,
+                    uint8_t* label_out, uint8_t* defer_out, const nsc_frame_outputs* outs,
+                    nsc_run_stats* stats, void* const* stage_events, void* stream) {
+  g_err[0] = 0;
+  if (int rc = check_cfg(cfg)) return rc;
+  NSC_REQUIRE(cnn != nullptr, NSC_E_INVAL, "cnn is NULL");
+  auto mark = [&](int k) -> int {
+    if (stage_events && stage_events[k])
+      NSC_TRY_HIP(hipEventRecord((hipEvent_t)stage_events[k], (hipStream_t)stream));
+    return NSC_OK;
+  };
+  const Cnn& c = cnn->c;
+  NSC_REQUIRE(c.desc.in_h == cfg->cnn_h && c.desc.in_w == cfg->cnn_w, NSC_E_SHAPE,
+              "CNN input %dx%d differs from the configured %dx%d", c.desc.in_h, c.desc.in_w,
+              cfg->cnn_h, cfg->cnn_w);
+  NSC_REQUIRE(n >= 0 && n <= kMaxFrames && t0 >= 0, NSC_E_INVAL, "n or t0 out of range");
+  const bool prev = cfg->ref_mode == NSC_REF_PREV;
+  if (n == 0) {
+    if (stats) *stats = nsc_run_stats{0, 0, 0, 0};
+    return NSC_OK;
+  }
+  NSC_REQUIRE(frames && label_out && defer_out, NSC_E_INVAL, "frames, label_out or defer_out is NULL");
+  NSC_REQUIRE(!(prev && state == nullptr), NSC_E_STATE, "earlier-frame mode needs a state buffer");
+  const RunLayout L = run_layout(cfg, c, n);
+  NSC_REQUIRE(ws != nullptr && ((uintptr_t)ws % kAlign) == 0 && ws_bytes >= L.total,
+              NSC_E_WORKSPACE, "workspace needs %zu bytes (256-byte aligned), got %zu", L.total,
+              ws_bytes);
+  const hipStream_t st = (hipStream_t)stream;
+  unsigned char* w = static_cast<unsigned char*>(ws);
+  int32_t* sums = reinterpret_cast<int32_t*>(w + L.sums);
+  uint8_t* fire = outs && outs->fire ? outs->fire : w + L.fire;
+  uint8_t* dec = w + L.dec;
+  int32_t* idx = reinterpret_cast<int32_t*>(w + L.idx);
+  int32_t* count = reinterpret_cast<int32_t*>(w + L.count);
+  const int64_t cells = (int64_t)cfg->dd_h * cfg->dd_w * 3;
+  size_t st_dec_off = 0;
+  state_layout_bytes(cfg, nullptr, &st_dec_off);
+  int32_t* st_sums = prev ? static_cast<int32_t*>(state) : nullptr;
+  uint8_t* st_dec = prev ? static_cast<uint8_t*>(state) + st_dec_off : nullptr;
+
+  // 1: area sums
+  if (int rc = mark(0)) return rc;
+  AreaPlan ap;
+  if (int rc = make_area_plan(cfg->in_h, cfg->in_w, cfg->frame_stride, frames, cfg->dd_h,
+                              cfg->dd_w, n, &ap))
+    return rc;
+  if (int rc = launch_area_sums(ap, frames, cfg->frame_stride, n, sums, st)) return rc;
+  if (int rc = mark(1)) return rc;
+  // 2: detector
+  {
+    const double den = (double)nsc_area_den(cfg->in_h, cfg->in_w, cfg->dd_h, cfg->dd_w);
+    DiffArgs a{};
+    a.sums = sums;
+    a.prev_sums = t0 > 0 ? st_sums : nullptr;
+    a.ref_sums = cfg->ref_sums;
+    a.lr_w = cfg->lr_w;
+    a.lr_b = cfg->lr_b;
+    a.delta_diff = cfg->delta_diff;
+    a.den2 = den * den;
+    a.n = n;
+    a.t0 = t0;
+    a.dd_h = cfg->dd_h;
+    a.dd_w = cfg->dd_w;
+    a.grid_h = cfg->grid_h;
+    a.grid_w = cfg->grid_w;
+    a.ref_mode = cfg->ref_mode;
+    a.delta = prev ? cfg->delta : 0;
+    a.score = outs ? outs->score : nullptr;
+    a.fire = fire;
+    if (int rc = launch_diff(a, st)) return rc;
+  }
+  if (int rc = mark(2)) return rc;
+  // 3: compaction
+  if (int rc = launch_compact(fire, n, idx, count, reinterpret_cast<int32_t*>(w + L.tiles), st))
+    return rc;
+  if (int rc = mark(3)) return rc;
+  // 4: CNN on survivors with decisions written at their frame positions
+  if (outs && outs->logit)
+    if (int rc = launch_fill_nan(outs->logit, n, st)) return rc;
+  CnnRunArgs r{};
+  r.sums = sums;
+  r.sums_h = cfg->dd_h;
+  r.sums_w = cfg->dd_w;
+  r.fy = cfg->dd_h / cfg->cnn_h;
+  r.fx = cfg->dd_w / cfg->cnn_w;
+  r.den_c = (double)nsc_area_den(cfg->in_h, cfg->in_w, cfg->dd_h, cfg->dd_w) * r.fy * r.fx;
+  r.idx = idx;
+  r.count = count;
+  r.max_count = n;
+  r.logit = reinterpret_cast<float*>(w + L.logit);
+  r.prob = nullptr;
+  r.dec = dec;
+  r.c_low = cfg->c_low;
+  r.c_high = cfg->c_high;
+  r.frame_logit = outs ? outs->logit : nullptr;
+  if (int rc = run_cnn(c, r, w + L.cnn, L.total - L.cnn, st)) return rc;
+  if (int rc = mark(4)) return rc;
+  // 5: decisions of frames that did not fire
+  const ResolvePlan rp = make_resolve_plan(n, t0, prev ? cfg->delta : 1);
+  if (int rc = launch_resolve(rp, cfg->ref_mode, fire, dec, st_dec,
+                              reinterpret_cast<int32_t*>(w + L.tile_last),
+                              reinterpret_cast<int32_t*>(w + L.carry), label_out, defer_out, st))
+    return rc;
+  if (prev)
+    if (int rc = launch_state_update(sums, label_out, defer_out, n, cfg->delta, cells, st_sums,
+                                     st_dec, w + L.scratch, st))
+      return rc;
+  if (int rc = mark(5)) return rc;
+  if (stats) {
+    std::vector<uint8_t> hl(n), hd(n);
+    int32_t hc = 0;
+    NSC_TRY_HIP(hipMemcpyAsync(hl.data(), label_out, n, hipMemcpyDeviceToHost, st));
+    NSC_TRY_HIP(hipMemcpyAsync(hd.data(), defer_out, n, hipMemcpyDeviceToHost, st));
+    NSC_TRY_HIP(hipMemcpyAsync(&hc, count, 4, hipMemcpyDeviceToHost, st));
+    NSC_TRY_HIP(hipStreamSynchronize(st));
+    nsc_run_stats s{n, hc, 0, 0};
+    for (int64_t i = 0; i < n; ++i) {
+      s.positive += hl[i] && !hd[i];
+      s.deferred += hd[i];
+    }
+    *stats = s;
+  }
+  return NSC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,482 @@
+// Specialized CNN on the survivors (Sec. 4 model, Sec. 7 pre-processing), gfx950.
+//
+// Conv layers run as implicit GEMM on 16x16 MFMA tiles: M = 16 output pixels
+// of a 4x4 tile, N = 16 output channels, K = 9 taps x input channels.  The
+// 16 pixels are ordered so that each lane's four accumulator rows form one
+// 2x2 pooling window, so bias + ReLU + 2x2 max-pool + rounding happen in
+// registers in the epilogue.  A workgroup stages the layer's packed weights in
+// LDS once and then loops over (image, tile-row) work items, staging the
+// input band (4 output rows + halo, zero padded) in LDS per item.  The first
+// layer's staging gathers the survivor's area sums, sums nested cells and
+// applies the [-1, 1] pre-processing.  bf16 layers use
+// v_mfma_f32_16x16x32_bf16, fp32 layers v_mfma_f32_16x16x4_f32; both
+// accumulate in fp32.
+//
+// The dense layer is a GEMM over 16-survivor tiles (M) x hidden units (N) x
+// features (K) on the same MFMA shapes; its epilogue adds the bias, applies
+// ReLU and rounding, folds the 1-unit output layer in with a 16-lane
+// shuffle reduction, and writes the logit, the sigmoid confidence and the
+// c_low / c_high decision of each frame.
+#include "nsc_internal.h"
+
+#include <math.h>
+
+namespace nsc {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- numerics
+
+// Round an fp32 value to bf16 (nearest, ties to even); finite inputs.
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
+  return __uint_as_float((uint32_t)b << 16);
+}
+// Round an fp64 value straight to bf16 (nearest, ties to even; finite, normal
+// range): keep 8 significant bits of the 53.
+__device__ __forceinline__ uint16_t f64_to_bf16_bits(double d) {
+  uint64_t u = (uint64_t)__double_as_longlong(d);
+  u += 0x0FFFFFFFFFFFull + ((u >> 45) & 1ull);
+  u &= ~0x1FFFFFFFFFFFull;
+  return (uint16_t)(__float_as_uint((float)__longlong_as_double((long long)u)) >> 16);
+}
+
+// Element-type traits: E = elements per lane per MFMA, KS = K per MFMA.
+template <typename T> struct Elt;
+template <> struct Elt<uint16_t> {  // bf16 stored as raw bits
+  static constexpr int E = 8, KS = 32;
+  typedef bf16x8 frag;
+  static __device__ __forceinline__ uint16_t from_f32(float v) { return f32_to_bf16_bits(v); }
+  static __device__ __forceinline__ uint16_t from_f64(double v) { return f64_to_bf16_bits(v); }
+  static __device__ __forceinline__ float to_f32(uint16_t v) { return bf16_bits_to_f32(v); }
+  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ frag load(const uint16_t* p) {  // 16-byte aligned
+    return *reinterpret_cast<const frag*>(p);
+  }
+  static __device__ __forceinline__ frag zero() {
+    frag z;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) z[e] = (__bf16)0.0f;
+    return z;
+  }
+  static __device__ __forceinline__ void set(frag& f, int e, uint16_t v) {
+    f[e] = __builtin_bit_cast(__bf16, v);
+  }
+};
+template <> struct Elt<float> {
+  static constexpr int E = 1, KS = 4;
+  typedef float frag;
+  static __device__ __forceinline__ float from_f32(float v) { return v; }
+  static __device__ __forceinline__ float from_f64(double v) { return (float)v; }
+  static __device__ __forceinline__ float to_f32(float v) { return v; }
+  static __device__ __forceinline__ f32x4 mma(float a, float b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ float load(const float* p) { return *p; }
+  static __device__ __forceinline__ float zero() { return 0.0f; }
+  static __device__ __forceinline__ void set(float& f, int, float v) { f = v; }
+};
+
+// ------------------------------------------------------------------- conv
+
+struct ConvArgs {
+  // input: first layer reads area sums of frame idx[s]; others read act_in[s]
+  const int32_t* sums;
+  const int32_t* idx;
+  int32_t sums_h, sums_w, fy, fx;
+  double den_c;
+  const void* act_in;
+  void* act_out;
+  const void* wts;          // packed [cout][kpad]
+  const float* bias;        // [cout]
+  const int32_t* count;
+  int64_t max_count;
+  int32_t cin, cout, h, w, kpad;
+  int32_t pool;
+  int32_t tiles_y, tiles_x;
+  int32_t cin_lds;          // channel stride of a staged pixel (elements)
+  int32_t w_lds;            // row stride of staged weights (elements)
+  int32_t band_w;           // staged columns: 4 * tiles_x + 2 (halo and tail zero-filled)
+};
+
+// Pixel (py, px) of M row m inside a 4x4 tile: m = 4 * window + j, the four
+// windows being the 2x2 pooling windows of the tile.
+__device__ __forceinline__ void tile_pixel(int m, int& py, int& px) {
+  const int wi = m >> 2, j = m & 3;
+  py = 2 * (wi >> 1) + (j >> 1);
+  px = 2 * (wi & 1) + (j & 1);
+}
+
+template <typename T, bool FIRST, int NT>
+__global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
+  using X = Elt<T>;
+  constexpr int E = X::E, KS = X::KS;
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  T* wl = reinterpret_cast<T*>(lds_raw);
+  T* in = wl + (size_t)a.cout * a.w_lds;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nwaves = blockDim.x >> 6;
+
+  // stage packed weights once per workgroup
+  {
+    const T* src = reinterpret_cast<const T*>(a.wts);
+    const int per_row = a.kpad;
+    for (int e = tid; e < a.cout * per_row; e += blockDim.x) {
+      const int o = e / per_row, k = e - o * per_row;
+      wl[o * a.w_lds + k] = src[e];
+    }
+  }
+  int64_t cnt = *a.count;
+  if (cnt > a.max_count) cnt = a.max_count;
+  const int64_t items = cnt * a.tiles_y;
+  const int band_w = a.band_w;
+  const int ho = a.pool ? a.h / 2 : a.h, wo = a.pool ? a.w / 2 : a.w;
+  const int m = lane & 15, g = lane >> 4;
+  int py, px;
+  tile_pixel(m, py, px);
+
+  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+    const int64_t s = item / a.tiles_y;
+    const int ty = (int)(item - s * a.tiles_y);
+    const int y_top = 4 * ty - 1;  // input row of band row 0
+    __syncthreads();  // previous item's readers are done with `in` (and weights staged)
+    if constexpr (FIRST) {
+      const int32_t* S = a.sums + (int64_t)a.idx[s] * a.sums_h * a.sums_w * 3;
+      for (int e = tid; e < 6 * band_w * 4; e += blockDim.x) {
+        const int c = e & 3, pix = e >> 2;
+        const int br = pix / band_w, bc = pix - br * band_w;
+        const int y = y_top + br, x = bc - 1;
+        T v = X::from_f32(0.0f);
+        if (c < 3 && y >= 0 && y < a.h && x >= 0 && x < a.w) {
+          int64_t acc = 0;
+          for (int dy = 0; dy < a.fy; ++dy)
+            for (int dx = 0; dx < a.fx; ++dx)
+              acc += S[((int64_t)(y * a.fy + dy) * a.sums_w + (x * a.fx + dx)) * 3 + c];
+          v = X::from_f64((double)acc / a.den_c / 127.5 - 1.0);
+        }
+        in[pix * a.cin_lds + c] = v;
+      }
+    } else {
+      const T* src = reinterpret_cast<const T*>(a.act_in) + s * (int64_t)a.h * a.w * a.cin;
+      constexpr int V = 16 / sizeof(T);  // elements per 16-byte vector
+      const int vec_per_pix = a.cin / V;
+      for (int e = tid; e < 6 * band_w * vec_per_pix; e += blockDim.x) {
+        const int pix = e / vec_per_pix, cv = e - pix * vec_per_pix;
+        const int br = pix / band_w, bc = pix - br * band_w;
+        const int y = y_top + br, x = bc - 1;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (y >= 0 && y < a.h && x >= 0 && x < a.w)
+          v = *reinterpret_cast<const uint4*>(src + ((int64_t)y * a.w + x) * a.cin + cv * V);
+        *reinterpret_cast<uint4*>(in + pix * a.cin_lds + cv * V) = v;
+      }
+    }
+    __syncthreads();
+
+    for (int tx = wave; tx < a.tiles_x; tx += nwaves) {
+      f32x4 acc[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int col0 = 4 * tx + px;  // band column of tap dx = 0
+      if constexpr (FIRST) {
+        // K = 27 (tap-major, channel-minor) padded to kpad with zeros
+        for (int k0 = 0; k0 < a.kpad; k0 += KS) {
+          typename X::frag av = X::zero();
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            const int k = k0 + g * E + e;
+            if (k < 27) {
+              const int tap = k / 3, c = k - 3 * tap;
+              const int dy = tap / 3, dx = tap - 3 * dy;
+              X::set(av, e, in[((py + dy) * band_w + col0 + dx) * a.cin_lds + c]);
+            }
+          }
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            const typename X::frag bv = X::load(wl + (nt * 16 + m) * a.w_lds + k0 + g * E);
+            acc[nt] = X::mma(av, bv, acc[nt]);
+          }
+        }
+      } else {
+        const int chunks = a.cin / KS;
+        for (int tap = 0; tap < 9; ++tap) {
+          const int dy = tap / 3, dx = tap - 3 * dy;
+          const T* arow = in + ((py + dy) * band_w + col0 + dx) * a.cin_lds + g * E;
+          const T* brow = wl + m * a.w_lds + tap * a.cin + g * E;
+          for (int ch = 0; ch < chunks; ++ch) {
+            const typename X::frag av = X::load(arow + ch * KS);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+              const typename X::frag bv = X::load(brow + nt * 16 * a.w_lds + ch * KS);
+              acc[nt] = X::mma(av, bv, acc[nt]);
+            }
+          }
+        }
+      }
+      // epilogue: lane holds rows 4g..4g+3 (one pooling window) of column m
+      T* out = reinterpret_cast<T*>(a.act_out) + s * (int64_t)ho * wo * a.cout;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int n = nt * 16 + m;
+        const float b = a.bias[n];
+        const int wy = g >> 1, wx = g & 1;
+        if (a.pool) {
+          float v = 0.0f;  // ReLU floor
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v = fmaxf(v, acc[nt][r] + b);
+          const int oy = 2 * ty + wy, ox = 2 * tx + wx;
+          if (oy < ho && ox < wo) out[((int64_t)oy * wo + ox) * a.cout + n] = X::from_f32(v);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int oy = 4 * ty + 2 * wy + (r >> 1), ox = 4 * tx + 2 * wx + (r & 1);
+            if (oy < ho && ox < wo)
+              out[((int64_t)oy * wo + ox) * a.cout + n] = X::from_f32(fmaxf(acc[nt][r] + b, 0.0f));
+          }
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ dense
+
+struct DenseArgs {
+  const void* feat;         // [slot][flat] in (y, x, c) order
+  const void* w1;           // [D][flat]
+  const float* b1;
+  const float* w2;
+  float b2;
+  int32_t flat;
+  const int32_t* count;
+  int64_t max_count;
+  const int32_t* idx;
+  float* logit;
+  float* prob;
+  uint8_t* dec;
+  float* frame_logit;
+  double c_low, c_high;
+};
+
+template <typename T, int NT>
+__global__ void __launch_bounds__(256) k_dense(DenseArgs a) {
+  using X = Elt<T>;
+  constexpr int E = X::E, KS = X::KS;
+  const int lane = threadIdx.x & 63;
+  const int m = lane & 15, g = lane >> 4;
+  int64_t cnt = *a.count;
+  if (cnt > a.max_count) cnt = a.max_count;
+  const int64_t groups = (cnt + 15) / 16;
+  const int64_t wave_id = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  const int64_t nwaves = (int64_t)gridDim.x * (blockDim.x >> 6);
+  const T* feat = reinterpret_cast<const T*>(a.feat);
+  const T* w1 = reinterpret_cast<const T*>(a.w1);
+  for (int64_t grp = wave_id; grp < groups; grp += nwaves) {
+    const int64_t s = grp * 16 + m;
+    const bool valid = s < cnt;
+    const T* arow = feat + (valid ? s : 0) * (int64_t)a.flat + g * E;
+    f32x4 acc[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < a.flat; k0 += KS) {
+      typename X::frag av = valid ? X::load(arow + k0) : X::zero();
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const typename X::frag bv = X::load(w1 + (int64_t)(nt * 16 + m) * a.flat + k0 + g * E);
+        acc[nt] = X::mma(av, bv, acc[nt]);
+      }
+    }
+    // hidden = round(ReLU(acc + b1)); z = b2 + sum_n w2[n] * hidden[n]
+    float part[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int n = nt * 16 + m;
+      const float b = a.b1[n], w = a.w2[n];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float hval = X::to_f32(X::from_f32(fmaxf(acc[nt][r] + b, 0.0f)));
+        part[r] += w * hval;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) part[r] += __shfl_xor(part[r], o, 64);
+    }
+    if (m == 0) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t slot = grp * 16 + 4 * g + r;
+        if (slot < cnt) {
+          const float z = part[r] + a.b2;
+          const double p = 1.0 / (1.0 + exp(-(double)z));
+          a.logit[slot] = z;
+          if (a.prob) a.prob[slot] = (float)p;
+          if (a.dec || a.frame_logit) {
+            const int32_t f = a.idx[slot];
+            if (a.dec) a.dec[f] = p < a.c_low ? 0 : (p > a.c_high ? 1 : 2);
+            if (a.frame_logit) a.frame_logit[f] = z;
+          }
+        }
+      }
+    }
+  }
+}
+
+template <typename T, bool FIRST>
+int launch_conv_nt(int nt, const ConvArgs& a, unsigned grid, size_t lds, hipStream_t st) {
+#define NSC_CONV_CASE(N)                                                                       \
+  case N:                                                                                      \
+    hipLaunchKernelGGL((k_conv<T, FIRST, N>), dim3(grid), dim3(256), lds, st, a);              \
+    break;
+  switch (nt) {
+    NSC_CONV_CASE(1)
+    NSC_CONV_CASE(2)
+    NSC_CONV_CASE(3)
+    NSC_CONV_CASE(4)
+    NSC_CONV_CASE(6)
+    NSC_CONV_CASE(8)
+    NSC_CONV_CASE(16)
+    default:
+      return fail(NSC_E_SHAPE, "conv with %d output channels is not supported", nt * 16);
+  }
+#undef NSC_CONV_CASE
+  NSC_CHECK_LAUNCH("k_conv");
+  return NSC_OK;
+}
+
+template <typename T>
+int launch_dense_nt(int nt, const DenseArgs& a, unsigned grid, hipStream_t st) {
+#define NSC_DENSE_CASE(N)                                                          \
+  case N:                                                                          \
+    hipLaunchKernelGGL((k_dense<T, N>), dim3(grid), dim3(256), 0, st, a);           \
+    break;
+  switch (nt) {
+    NSC_DENSE_CASE(1)
+    NSC_DENSE_CASE(2)
+    NSC_DENSE_CASE(4)
+    NSC_DENSE_CASE(8)
+    NSC_DENSE_CASE(16)
+    default:
+      return fail(NSC_E_SHAPE, "dense layer of %d units is not supported", nt * 16);
+  }
+#undef NSC_DENSE_CASE
+  NSC_CHECK_LAUNCH("k_dense");
+  return NSC_OK;
+}
+
+}  // namespace
+
+// LDS bytes of one conv layer's workgroup (weights + input band).
+// Output tiles of a layer: 4x4 pixels; a pooled layer only needs the pixels
+// of whole pooling windows.
+void conv_tiles(const CnnLayer& L, int32_t* tiles_y, int32_t* tiles_x) {
+  const int hn = L.pool ? (L.h / 2) * 2 : L.h, wn = L.pool ? (L.w / 2) * 2 : L.w;
+  *tiles_y = (hn + 3) / 4;
+  *tiles_x = (wn + 3) / 4;
+}
+
+size_t conv_lds_bytes(const CnnLayer& L, bool bf16, int32_t* cin_lds, int32_t* w_lds,
+                      int32_t* band_w) {
+  const size_t es = bf16 ? 2 : 4;
+  const int32_t vec = (int32_t)(16 / es);
+  const int32_t cl = L.cin == 3 ? 4 : L.cin + vec;          // pad pixels by 16 bytes
+  const int32_t wr = L.kpad + vec;                          // pad weight rows by 16 bytes
+  int32_t ty, tx;
+  conv_tiles(L, &ty, &tx);
+  const int32_t bw = 4 * tx + 2;
+  if (cin_lds) *cin_lds = cl;
+  if (w_lds) *w_lds = wr;
+  if (band_w) *band_w = bw;
+  return ((size_t)L.cout * wr + (size_t)6 * bw * cl) * es;
+}
+
+size_t cnn_workspace_bytes(const Cnn& cnn, int64_t max_count) {
+  const size_t es = cnn.bf16 ? 2 : 4;
+  const size_t per = align_up(cnn.act_elems * es, 256);
+  return 2 * per * (size_t)(max_count > 0 ? max_count : 0) + 256;
+}
+
+int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (r.max_count <= 0) return NSC_OK;
+  const size_t es = cnn.bf16 ? 2 : 4;
+  const size_t per = align_up(cnn.act_elems * es, 256);
+  if (ws_bytes < cnn_workspace_bytes(cnn, r.max_count))
+    return fail(NSC_E_WORKSPACE, "CNN workspace of %zu bytes is below the %zu required", ws_bytes,
+                cnn_workspace_bytes(cnn, r.max_count));
+  unsigned char* buf[2] = {static_cast<unsigned char*>(ws),
+                           static_cast<unsigned char*>(ws) + per * (size_t)r.max_count};
+  for (int l = 0; l < cnn.n_layers; ++l) {
+    const CnnLayer& L = cnn.layers[l];
+    ConvArgs a{};
+    a.sums = r.sums;
+    a.idx = r.idx;
+    a.sums_h = r.sums_h;
+    a.sums_w = r.sums_w;
+    a.fy = r.fy;
+    a.fx = r.fx;
+    a.den_c = r.den_c;
+    a.act_in = l > 0 ? buf[(l - 1) & 1] : nullptr;
+    a.act_out = buf[l & 1];
+    a.wts = static_cast<const unsigned char*>(cnn.conv_w) + L.w_off * es;
+    a.bias = cnn.conv_b + L.b_off;
+    a.count = r.count;
+    a.max_count = r.max_count;
+    a.cin = L.cin;
+    a.cout = L.cout;
+    a.h = L.h;
+    a.w = L.w;
+    a.kpad = L.kpad;
+    a.pool = L.pool ? 1 : 0;
+    conv_tiles(L, &a.tiles_y, &a.tiles_x);
+    const size_t lds = conv_lds_bytes(L, cnn.bf16, &a.cin_lds, &a.w_lds, &a.band_w);
+    int per_cu = (int)((160 * 1024) / (lds + 1024));
+    if (per_cu > 8) per_cu = 8;
+    if (per_cu < 1) per_cu = 1;
+    int64_t items = r.max_count * a.tiles_y;
+    int64_t grid = (int64_t)kNumCU * per_cu;
+    if (grid > items) grid = items;
+    if (grid < 1) grid = 1;
+    int rc;
+    const int nt = L.cout / 16;
+    if (cnn.bf16)
+      rc = l == 0 ? launch_conv_nt<uint16_t, true>(nt, a, (unsigned)grid, lds, stream)
+                  : launch_conv_nt<uint16_t, false>(nt, a, (unsigned)grid, lds, stream);
+    else
+      rc = l == 0 ? launch_conv_nt<float, true>(nt, a, (unsigned)grid, lds, stream)
+                  : launch_conv_nt<float, false>(nt, a, (unsigned)grid, lds, stream);
+    if (rc) return rc;
+  }
+  DenseArgs d{};
+  d.feat = buf[(cnn.n_layers - 1) & 1];
+  d.w1 = cnn.w1;
+  d.b1 = cnn.b1;
+  d.w2 = cnn.w2;
+  d.b2 = cnn.b2;
+  d.flat = cnn.flat;
+  d.count = r.count;
+  d.max_count = r.max_count;
+  d.idx = r.idx;
+  d.logit = r.logit;
+  d.prob = r.prob;
+  d.dec = r.dec;
+  d.frame_logit = r.frame_logit;
+  d.c_low = r.c_low;
+  d.c_high = r.c_high;
+  int64_t groups = (r.max_count + 15) / 16;
+  int64_t grid = (groups + 3) / 4;
+  if (grid > kNumCU * 8) grid = kNumCU * 8;
+  if (grid < 1) grid = 1;
+  const int nt = cnn.dense / 16;
+  return cnn.bf16 ? launch_dense_nt<uint16_t>(nt, d, (unsigned)grid, stream)
+                  : launch_dense_nt<float>(nt, d, (unsigned)grid, stream);
+}
+
+}  // namespace nsc

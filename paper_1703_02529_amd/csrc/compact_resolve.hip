@@ -1,0 +1,306 @@
+// Stream compaction of fired frames and label resolution (gfx950).
+//
+// Compaction (frames batched for the GPU model, Sec. 7): tiles of 4096 flags.
+// A first kernel counts each tile with wave ballots; a second one gives every
+// tile its offset (sum of the earlier tiles' counts), scans its four waves'
+// counts in LDS and writes the ascending indices with ballot + lane-mask
+// popcounts, so the output order is the frame order.
+//
+// Resolution (Sec. 5: a frame on which the earlier-frame detector does not
+// fire reuses the compared frame's output): frame u copies frame u - delta,
+// so the decision of u is that of the last fired frame of its residue chain
+// u, u - delta, u - 2 delta, ...; that is a running max of fired indices per
+// residue class.  Frames are viewed as rows of `delta` columns, cut into
+// tiles of rows: per-tile last fired index per column, an exclusive max-scan
+// across tiles per column, and a per-tile sequential walk down each column.
+#include "nsc_internal.h"
+
+namespace nsc {
+namespace {
+
+constexpr int kTile = 4096;   // flags per compaction tile
+constexpr int kTileThreads = 256;
+
+__device__ __forceinline__ uint64_t lanemask_lt(int lane) {
+  return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+}
+
+__global__ void __launch_bounds__(kTileThreads) k_tile_count(const uint8_t* __restrict__ fire,
+                                                             int64_t n,
+                                                             int32_t* __restrict__ tile_counts) {
+  __shared__ int32_t wsum[kTileThreads / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)wave * (kTile / 4);
+  int32_t c = 0;
+  for (int s = 0; s < kTile / 4 / 64; ++s) {
+    const int64_t u = base + s * 64 + lane;
+    const bool f = u < n && fire[u] != 0;
+    c += __popcll(__ballot(f));
+  }
+  if (lane == 0) wsum[wave] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t t = 0;
+    for (int w = 0; w < kTileThreads / 64; ++w) t += wsum[w];
+    tile_counts[blockIdx.x] = t;
+  }
+}
+
+__global__ void __launch_bounds__(kTileThreads) k_tile_scatter(const uint8_t* __restrict__ fire,
+                                                               int64_t n,
+                                                               const int32_t* __restrict__ tile_counts,
+                                                               int32_t* __restrict__ idx,
+                                                               int32_t* __restrict__ count) {
+  __shared__ int64_t red[kTileThreads];
+  __shared__ int32_t wcount[kTileThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // offset of this tile = sum of the counts of all earlier tiles
+  int64_t s = 0;
+  for (int b = tid; b < (int)blockIdx.x; b += kTileThreads) s += tile_counts[b];
+  red[tid] = s;
+  __syncthreads();
+  for (int o = kTileThreads / 2; o > 0; o >>= 1) {
+    if (tid < o) red[tid] += red[tid + o];
+    __syncthreads();
+  }
+  const int64_t tile_off = red[0];
+  const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)wave * (kTile / 4);
+  // pass 1: this wave's count
+  int32_t c = 0;
+  for (int st = 0; st < kTile / 4 / 64; ++st) {
+    const int64_t u = base + st * 64 + lane;
+    c += __popcll(__ballot(u < n && fire[u] != 0));
+  }
+  if (lane == 0) wcount[wave] = c;
+  __syncthreads();
+  int64_t off = tile_off;
+  for (int w = 0; w < wave; ++w) off += wcount[w];
+  // pass 2: write ascending indices
+  for (int st = 0; st < kTile / 4 / 64; ++st) {
+    const int64_t u = base + st * 64 + lane;
+    const bool f = u < n && fire[u] != 0;
+    const uint64_t m = __ballot(f);
+    if (f) idx[off + __popcll(m & lanemask_lt(lane))] = (int32_t)u;
+    off += __popcll(m);
+  }
+  if (blockIdx.x == gridDim.x - 1 && tid == 0) {
+    int64_t total = tile_off;
+    for (int w = 0; w < kTileThreads / 64; ++w) total += wcount[w];
+    *count = (int32_t)total;
+  }
+}
+
+__global__ void k_set_i32(int32_t* p, int32_t v) { *p = v; }
+
+// Per-tile last fired local index per residue column (or -1).
+__global__ void __launch_bounds__(256) k_resolve_tile_last(const uint8_t* __restrict__ fire,
+                                                           int64_t n, int32_t delta,
+                                                           int32_t rows_per_tile,
+                                                           int32_t* __restrict__ tile_last) {
+  __shared__ int32_t last[NSC_MAX_DELTA];
+  for (int r = threadIdx.x; r < delta; r += blockDim.x) last[r] = -1;
+  __syncthreads();
+  const int64_t u0 = (int64_t)blockIdx.x * rows_per_tile * delta;
+  const int64_t span = (int64_t)rows_per_tile * delta;
+  for (int64_t k = threadIdx.x; k < span; k += blockDim.x) {
+    const int64_t u = u0 + k;
+    if (u < n && fire[u]) atomicMax(&last[(int)(u % delta)], (int32_t)u);
+  }
+  __syncthreads();
+  for (int r = threadIdx.x; r < delta; r += blockDim.x)
+    tile_last[(int64_t)blockIdx.x * delta + r] = last[r];
+}
+
+// carry[b][r] = max over tiles b' < b of tile_last[b'][r]; one block per column.
+__global__ void __launch_bounds__(1024) k_resolve_carry(const int32_t* __restrict__ tile_last,
+                                                        int32_t tiles, int32_t delta,
+                                                        int32_t* __restrict__ carry) {
+  __shared__ int32_t v[1024];
+  const int r = blockIdx.x, b = threadIdx.x;
+  v[b] = b < tiles ? tile_last[(int64_t)b * delta + r] : -1;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {
+    const int32_t x = b >= o ? v[b - o] : -1;
+    __syncthreads();
+    if (x > v[b]) v[b] = x;
+    __syncthreads();
+  }
+  if (b < tiles) carry[(int64_t)b * delta + r] = b > 0 ? v[b - 1] : -1;
+}
+
+// Walks each residue column of a tile and writes label / defer.
+__global__ void __launch_bounds__(256) k_resolve_apply(const uint8_t* __restrict__ fire,
+                                                       const uint8_t* __restrict__ dec,
+                                                       const uint8_t* __restrict__ prev_dec,
+                                                       int64_t n, int32_t delta,
+                                                       int32_t rows_per_tile,
+                                                       const int32_t* __restrict__ carry,
+                                                       uint8_t* __restrict__ label,
+                                                       uint8_t* __restrict__ defer) {
+  for (int r = threadIdx.x; r < delta; r += blockDim.x) {
+    int32_t cur = carry[(int64_t)blockIdx.x * delta + r];
+    const int64_t row0 = (int64_t)blockIdx.x * rows_per_tile;
+    for (int q = 0; q < rows_per_tile; ++q) {
+      const int64_t u = (row0 + q) * delta + r;
+      if (u >= n) break;
+      if (fire[u]) cur = (int32_t)u;
+      // no fired frame of this chain in the call: continue the carried state
+      const uint8_t d = cur >= 0 ? dec[cur] : (prev_dec ? prev_dec[r] : (uint8_t)0);
+      label[u] = d & 1;
+      defer[u] = (d >> 1) & 1;
+    }
+  }
+}
+
+// Fixed reference image: a frame that does not fire is labelled "no object".
+__global__ void __launch_bounds__(256) k_resolve_fixed(const uint8_t* __restrict__ fire,
+                                                       const uint8_t* __restrict__ dec, int64_t n,
+                                                       uint8_t* __restrict__ label,
+                                                       uint8_t* __restrict__ defer) {
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < n;
+       u += (int64_t)gridDim.x * blockDim.x) {
+    const uint8_t d = fire[u] ? dec[u] : (uint8_t)0;
+    label[u] = d & 1;
+    defer[u] = (d >> 1) & 1;
+  }
+}
+
+// State of the last `delta` frames after a call of n frames.  When n < delta
+// the old state is read from `old_*` (a copy), otherwise only from this call.
+__global__ void __launch_bounds__(256) k_state_update(const int32_t* __restrict__ sums,
+                                                      const uint8_t* __restrict__ label,
+                                                      const uint8_t* __restrict__ defer, int64_t n,
+                                                      int32_t delta, int64_t cells,
+                                                      const int32_t* __restrict__ old_sums,
+                                                      const uint8_t* __restrict__ old_dec,
+                                                      int32_t* __restrict__ st_sums,
+                                                      uint8_t* __restrict__ st_dec) {
+  const int64_t total = (int64_t)delta * cells;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t k = e / cells, c = e - k * cells;
+    const int64_t src = n - delta + k;  // local index of the frame kept in slot k
+    st_sums[e] = src >= 0 ? sums[src * cells + c] : old_sums[(k + n) * cells + c];
+    if (c == 0)
+      st_dec[k] = src >= 0 ? (uint8_t)(label[src] | (defer[src] << 1)) : old_dec[k + n];
+  }
+}
+
+__global__ void __launch_bounds__(256) k_copy_u8(const uint8_t* __restrict__ s,
+                                                 uint8_t* __restrict__ d, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    d[i] = s[i];
+}
+
+__global__ void __launch_bounds__(256) k_fill_nan(float* __restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = __builtin_nanf("");
+}
+
+unsigned grid_for(int64_t n, int per_block) {
+  int64_t b = (n + per_block - 1) / per_block;
+  if (b < 1) b = 1;
+  if (b > kNumCU * 16) b = kNumCU * 16;
+  return (unsigned)b;
+}
+
+}  // namespace
+
+int64_t compact_tiles(int64_t n) { return (n + kTile - 1) / kTile; }
+
+int launch_compact(const uint8_t* fire, int64_t n, int32_t* idx, int32_t* count,
+                   int32_t* tile_counts, hipStream_t stream) {
+  if (n <= 0) {
+    hipLaunchKernelGGL(k_set_i32, dim3(1), dim3(1), 0, stream, count, 0);
+    NSC_CHECK_LAUNCH("k_set_i32");
+    return NSC_OK;
+  }
+  const int64_t tiles = compact_tiles(n);
+  hipLaunchKernelGGL(k_tile_count, dim3((unsigned)tiles), dim3(kTileThreads), 0, stream, fire, n,
+                     tile_counts);
+  NSC_CHECK_LAUNCH("k_tile_count");
+  hipLaunchKernelGGL(k_tile_scatter, dim3((unsigned)tiles), dim3(kTileThreads), 0, stream, fire, n,
+                     tile_counts, idx, count);
+  NSC_CHECK_LAUNCH("k_tile_scatter");
+  return NSC_OK;
+}
+
+ResolvePlan make_resolve_plan(int64_t n, int64_t t0, int32_t delta) {
+  ResolvePlan p{};
+  p.n = n;
+  p.t0 = t0;
+  p.delta = delta < 1 ? 1 : delta;
+  const int64_t rows = (n + p.delta - 1) / p.delta;
+  int64_t rpt = (rows + 1023) / 1024;
+  if (rpt < 1) rpt = 1;
+  p.rows_per_tile = (int32_t)rpt;
+  p.tiles = (int32_t)((rows + rpt - 1) / rpt);
+  if (p.tiles < 1) p.tiles = 1;
+  return p;
+}
+
+int launch_resolve(const ResolvePlan& p, int32_t ref_mode, const uint8_t* fire, const uint8_t* dec,
+                   const uint8_t* prev_dec, int32_t* tile_last, int32_t* carry, uint8_t* label,
+                   uint8_t* defer, hipStream_t stream) {
+  if (p.n <= 0) return NSC_OK;
+  if (ref_mode == NSC_REF_FIXED) {
+    hipLaunchKernelGGL(k_resolve_fixed, dim3(grid_for(p.n, 256)), dim3(256), 0, stream, fire, dec,
+                       p.n, label, defer);
+    NSC_CHECK_LAUNCH("k_resolve_fixed");
+    return NSC_OK;
+  }
+  hipLaunchKernelGGL(k_resolve_tile_last, dim3(p.tiles), dim3(256), 0, stream, fire, p.n, p.delta,
+                     p.rows_per_tile, tile_last);
+  NSC_CHECK_LAUNCH("k_resolve_tile_last");
+  hipLaunchKernelGGL(k_resolve_carry, dim3(p.delta), dim3(1024), 0, stream, tile_last, p.tiles,
+                     p.delta, carry);
+  NSC_CHECK_LAUNCH("k_resolve_carry");
+  hipLaunchKernelGGL(k_resolve_apply, dim3(p.tiles), dim3(256), 0, stream, fire, dec,
+                     p.t0 > 0 ? prev_dec : nullptr, p.n, p.delta, p.rows_per_tile, carry, label,
+                     defer);
+  NSC_CHECK_LAUNCH("k_resolve_apply");
+  return NSC_OK;
+}
+
+int launch_state_update(const int32_t* sums, const uint8_t* label, const uint8_t* defer, int64_t n,
+                        int32_t delta, int64_t cells, int32_t* state_sums, uint8_t* state_dec,
+                        void* scratch, hipStream_t stream) {
+  if (n <= 0) return NSC_OK;
+  const int32_t* old_sums = state_sums;
+  const uint8_t* old_dec = state_dec;
+  if (n < delta) {
+    // slots k < delta - n keep frames of the previous state: copy it first
+    uint8_t* s = static_cast<uint8_t*>(scratch);
+    const int64_t sb = (int64_t)delta * cells * 4;
+    hipLaunchKernelGGL(k_copy_u8, dim3(grid_for(sb, 256)), dim3(256), 0, stream,
+                       reinterpret_cast<const uint8_t*>(state_sums), s, sb);
+    NSC_CHECK_LAUNCH("k_copy_u8");
+    hipLaunchKernelGGL(k_copy_u8, dim3(1), dim3(256), 0, stream, state_dec, s + sb, (int64_t)delta);
+    NSC_CHECK_LAUNCH("k_copy_u8");
+    old_sums = reinterpret_cast<const int32_t*>(s);
+    old_dec = s + sb;
+  }
+  hipLaunchKernelGGL(k_state_update, dim3(grid_for((int64_t)delta * cells, 256)), dim3(256), 0,
+                     stream, sums, label, defer, n, delta, cells, old_sums, old_dec, state_sums,
+                     state_dec);
+  NSC_CHECK_LAUNCH("k_state_update");
+  return NSC_OK;
+}
+
+int launch_fill_nan(float* p, int64_t n, hipStream_t stream) {
+  if (n <= 0) return NSC_OK;
+  hipLaunchKernelGGL(k_fill_nan, dim3(grid_for(n, 256)), dim3(256), 0, stream, p, n);
+  NSC_CHECK_LAUNCH("k_fill_nan");
+  return NSC_OK;
+}
+
+int launch_copy_u8(const uint8_t* src, uint8_t* dst, int64_t n, hipStream_t stream) {
+  if (n <= 0) return NSC_OK;
+  hipLaunchKernelGGL(k_copy_u8, dim3(grid_for(n, 256)), dim3(256), 0, stream, src, dst, n);
+  NSC_CHECK_LAUNCH("k_copy_u8");
+  return NSC_OK;
+}
+
+}  // namespace nsc

@@ -1,0 +1,138 @@
+// Internal declarations shared by the translation units of libnsc.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "nsc.h"
+
+namespace nsc {
+
+// Records a formatted description for nsc_last_error() and returns `code`.
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+
+#define NSC_TRY_HIP(call)                                                          \
+  do {                                                                             \
+    hipError_t e_ = (call);                                                        \
+    if (e_ != hipSuccess)                                                          \
+      return ::nsc::fail(NSC_E_HIP, "%s failed: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+#define NSC_CHECK_LAUNCH(what)                                                       \
+  do {                                                                               \
+    hipError_t e_ = hipGetLastError();                                               \
+    if (e_ != hipSuccess)                                                            \
+      return ::nsc::fail(NSC_E_HIP, "launch of %s failed: %s", what, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int kNumCU = 256;  // MI355X compute units (8 XCDs x 32)
+
+inline int64_t gcd64(int64_t a, int64_t b) {
+  while (b) {
+    int64_t t = a % b;
+    a = b;
+    b = t;
+  }
+  return a;
+}
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Exact area resampling of one axis: output cell o covers [o*p, (o+1)*p) and
+// input pixel i covers [i*q, (i+1)*q), both in units of 1/q input pixel.
+struct Axis {
+  int32_t n_in, n_out, p, q;
+  static Axis make(int32_t n_in, int32_t n_out) {
+    int64_t g = gcd64(n_in, n_out);
+    return Axis{n_in, n_out, (int32_t)(n_in / g), (int32_t)(n_out / g)};
+  }
+};
+
+// Area-sum launch plan for one frame geometry.
+struct AreaPlan {
+  Axis ay, ax;
+  int32_t chunk_bytes;   // bytes of a row one lane reads per load: 16, 4 or 1
+  int32_t lanes;         // row chunks = in_w*3 / chunk_bytes
+  int32_t threads;       // lanes rounded up to a multiple of 64
+  int32_t bands;         // output-row bands per frame
+  bool packed;           // 16-bit packed vertical accumulators are exact
+};
+int make_area_plan(int32_t in_h, int32_t in_w, int64_t stride, const void* frames,
+                   int32_t out_h, int32_t out_w, int64_t n, AreaPlan* plan);
+int launch_area_sums(const AreaPlan& plan, const uint8_t* frames, int64_t stride, int64_t n,
+                     int32_t* sums, hipStream_t stream);
+
+// Detector scoring of frames [t0, t0+n) whose area sums are in `sums`.
+struct DiffArgs {
+  const int32_t* sums;       // [n][cells]
+  const int32_t* prev_sums;  // [delta][cells] frames t0-delta..t0-1 (PREV, t0 > 0)
+  const int32_t* ref_sums;   // [cells] (FIXED)
+  const float* lr_w;         // [grid_h*grid_w] (blocked)
+  double lr_b, delta_diff, den2;  // den2 = den*den as a double
+  int64_t n, t0;
+  int32_t dd_h, dd_w, grid_h, grid_w, ref_mode, delta;
+  double* score;             // nullable
+  uint8_t* fire;
+};
+int launch_diff(const DiffArgs& a, hipStream_t stream);
+
+// Compaction of fire flags into ascending indices.
+int64_t compact_tiles(int64_t n);
+int launch_compact(const uint8_t* fire, int64_t n, int32_t* idx, int32_t* count, int32_t* tile_counts,
+                   hipStream_t stream);
+
+// Label resolution (PREV: reuse the decision of frame t-delta; FIXED: 0).
+struct ResolvePlan {
+  int64_t n, t0;
+  int32_t delta, rows_per_tile, tiles;
+};
+ResolvePlan make_resolve_plan(int64_t n, int64_t t0, int32_t delta);
+int launch_resolve(const ResolvePlan& p, int32_t ref_mode, const uint8_t* fire, const uint8_t* dec,
+                   const uint8_t* prev_dec, int32_t* tile_last, int32_t* carry, uint8_t* label,
+                   uint8_t* defer, hipStream_t stream);
+int launch_state_update(const int32_t* sums, const uint8_t* label, const uint8_t* defer, int64_t n,
+                        int32_t delta, int64_t cells, int32_t* state_sums, uint8_t* state_dec,
+                        void* scratch, hipStream_t stream);
+int launch_fill_nan(float* p, int64_t n, hipStream_t stream);
+int launch_copy_u8(const uint8_t* src, uint8_t* dst, int64_t n, hipStream_t stream);
+
+// Specialized CNN.
+struct CnnLayer {
+  int32_t cin, cout, h, w;  // input channels, output channels, input grid
+  bool pool;
+  int32_t kpad;             // padded reduction length of the packed weights
+  size_t w_off, b_off;      // offsets (elements) into the packed weight/bias arrays
+};
+struct Cnn {
+  nsc_cnn_desc desc;
+  int32_t n_layers;
+  CnnLayer layers[NSC_MAX_CONV];
+  int32_t feat_c, feat_h, feat_w, flat, dense;
+  bool bf16;
+  void* dev;                // one allocation holding everything below
+  void* conv_w;             // packed conv weights, bf16 or fp32
+  float* conv_b;            // fp32 biases
+  void* w1;                 // dense weights [D][flat] in (y, x, c) order
+  float* b1;
+  float* w2;                // output layer weights [D] (fp32)
+  float b2;
+  size_t act_elems;         // largest per-image activation (elements)
+};
+struct CnnRunArgs {
+  const int32_t* sums;
+  int32_t sums_h, sums_w, fy, fx;
+  double den_c;             // denominator of the fy x fx cell sums
+  const int32_t* idx;
+  const int32_t* count;
+  int64_t max_count;
+  float* logit;             // per survivor slot
+  float* prob;              // nullable
+  // decisions: written when dec != nullptr, at dec[idx[i]]
+  uint8_t* dec;
+  double c_low, c_high;
+  float* frame_logit;       // nullable: logit scattered to frame position idx[i]
+};
+size_t cnn_workspace_bytes(const Cnn& cnn, int64_t max_count);
+int run_cnn(const Cnn& cnn, const CnnRunArgs& a, void* ws, size_t ws_bytes, hipStream_t stream);
+
+}  // namespace nsc

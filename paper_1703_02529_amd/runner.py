@@ -1,0 +1,62 @@
+"""Convenience owner of the device buffers one cascade stream needs.
+
+Allocates (through torch) the workspace, the carried state and the per-frame
+output buffers, creates the CNN handle, and calls nsc_cascade_run.  It reads a
+workload description by attribute (video.h, video.w, dd_h, dd_w, cnn, ref_mode,
+delta, grid, delta_diff, c_low, c_high, lr_bias) and imports nothing else.
+"""
+from __future__ import annotations
+
+from typing import Optional
+
+import torch
+
+from . import (NSC_REF_FIXED, NSC_REF_PREV, Cnn, make_cfg, make_desc,
+               nsc_cascade_run, nsc_cascade_workspace_bytes, nsc_state_bytes)
+
+
+class CascadeRunner:
+    def __init__(self, wl, blob, max_frames: int, lr_w: Optional[torch.Tensor] = None,
+                 ref_sums: Optional[torch.Tensor] = None, device="cuda", frame_stride=None):
+        self.wl = wl
+        self.device = torch.device(device)
+        self.lr_w = lr_w
+        self.ref_sums = ref_sums
+        self.cfg = make_cfg(in_h=wl.video.h, in_w=wl.video.w, dd_h=wl.dd_h, dd_w=wl.dd_w,
+                            cnn_h=wl.cnn.in_h, cnn_w=wl.cnn.in_w, ref_mode=wl.ref_mode,
+                            delta=wl.delta, grid=tuple(wl.grid), lr_w=lr_w, lr_b=wl.lr_bias,
+                            ref_sums=ref_sums, delta_diff=wl.delta_diff, c_low=wl.c_low,
+                            c_high=wl.c_high, frame_stride=frame_stride)
+        self.desc = make_desc(wl.cnn.conv, wl.cnn.pool, wl.cnn.dense, wl.cnn.in_h, wl.cnn.in_w,
+                              wl.cnn.bf16)
+        self.cnn = Cnn(self.desc, blob)
+        self.max_frames = max_frames
+        ws = nsc_cascade_workspace_bytes(self.cfg, self.cnn, max_frames)
+        self.ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=self.device)
+        self.state = torch.zeros(max(nsc_state_bytes(self.cfg), 256), dtype=torch.uint8,
+                                 device=self.device)
+        self.label = torch.empty(max_frames, dtype=torch.uint8, device=self.device)
+        self.defer = torch.empty(max_frames, dtype=torch.uint8, device=self.device)
+        self.score = torch.empty(max_frames, dtype=torch.float64, device=self.device)
+        self.fire = torch.empty(max_frames, dtype=torch.uint8, device=self.device)
+        self.logit = torch.empty(max_frames, dtype=torch.float32, device=self.device)
+        self.next_t = 0
+
+    def run(self, frames: torch.Tensor, n: int, t0: Optional[int] = None, taps: bool = True,
+            want_stats: bool = False, stage_events=None, stream=None):
+        """Runs frames [t0, t0+n) (default: continue where the last call ended)."""
+        if n > self.max_frames:
+            raise ValueError(f"{n} frames exceed the workspace's {self.max_frames}")
+        t0 = self.next_t if t0 is None else t0
+        kw = dict(score=self.score[:n], fire=self.fire[:n], logit=self.logit[:n]) if taps else {}
+        st = nsc_cascade_run(self.cfg, self.cnn, frames, n, t0, self.state, self.ws,
+                             self.label[:n], self.defer[:n], want_stats=want_stats,
+                             stage_events=stage_events, stream=stream, **kw)
+        self.next_t = t0 + n
+        return st
+
+    def close(self):
+        self.cnn.close()
+
+
+__all__ = ["CascadeRunner", "NSC_REF_PREV", "NSC_REF_FIXED"]

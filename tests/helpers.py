@@ -1,0 +1,76 @@
+"""Shared helpers of the GPU parity tests: inputs, oracle runs and comparisons."""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+import oracle
+import synth
+
+LOGIT_TOL = {True: 1e-3, False: 1e-5}   # bf16 / fp32 networks: max relative logit error
+
+
+def logit_rel_err(g: np.ndarray, o: np.ndarray, scale: np.ndarray) -> np.ndarray:
+    """|g - o| / scale, scale = |b2| + sum_j |w2_j h_j| from the oracle: the error
+    relative to the magnitude of the terms the output layer sums (equal to the
+    plain relative error when they do not cancel)."""
+    g = np.asarray(g, np.float64)
+    o = np.asarray(o, np.float64)
+    if o.size == 0:
+        return np.zeros(0)
+    return np.abs(g - o) / np.maximum(np.asarray(scale, np.float64), 1e-300)
+
+
+def decision_excluded(z_oracle: float, c_low: float, c_high: float, tol: float, scale: float) -> bool:
+    """A fired frame's decision is only pinned when its logit is farther from the
+    logit of a threshold than the logit tolerance allows the GPU value to move."""
+    band = 2.0 * tol * scale
+    for c in (c_low, c_high):
+        if 0.0 < c < 1.0 and abs(z_oracle - math.log(c / (1.0 - c))) <= band:
+            return True
+    return False
+
+
+def oracle_decision(z: float, c_low: float, c_high: float) -> int:
+    return oracle.decide(oracle.sigmoid(z), c_low, c_high)
+
+
+def lr_weights_for(wl):
+    return synth.lr_weights(wl.grid[0] * wl.grid[1], wl.weight_seed, wl.lr_bias)[0]
+
+
+def compare_cascade(wl, gpu: dict, ref: dict, t0: int = 0, state_excluded=None):
+    """Element-by-element comparison of a GPU cascade run with the oracle's.
+
+    gpu / ref: dicts of numpy arrays score, fire, logit, label, defer over the
+    same frames.  Returns (report dict).  Scores and fire flags must be
+    bit-identical; logits within the network's tolerance; labels and defer
+    flags identical outside the excluded frames (fired frames whose logit lies
+    within the tolerance band of a threshold, and frames inheriting from them)."""
+    n = len(ref["fire"])
+    assert np.array_equal(gpu["fire"], ref["fire"]), "fire flags differ"
+    assert np.array_equal(gpu["score"], ref["score"]), \
+        f"scores differ at {np.flatnonzero(gpu['score'] != ref['score'])[:10]}"
+    fired = np.flatnonzero(ref["fire"])
+    tol = LOGIT_TOL[wl.cnn.bf16]
+    rel = logit_rel_err(gpu["logit"][fired], ref["logit"][fired], ref["lscale"][fired])
+    assert np.isnan(gpu["logit"][ref["fire"] == 0]).all()
+    assert rel.size == 0 or rel.max() <= tol, f"max logit rel err {rel.max():.3g} > {tol}"
+    excluded = np.zeros(n, bool)
+    for u in range(n):
+        if ref["fire"][u]:
+            excluded[u] = decision_excluded(ref["logit"][u], wl.c_low, wl.c_high, tol,
+                                            ref["lscale"][u])
+        elif wl.ref_mode == 0:
+            if u >= wl.delta:
+                excluded[u] = excluded[u - wl.delta]
+            elif state_excluded is not None:
+                excluded[u] = state_excluded[u]
+    keep = ~excluded
+    bad = np.flatnonzero(keep & ((gpu["label"] != ref["label"]) | (gpu["defer"] != ref["defer"])))
+    assert bad.size == 0, f"labels differ at frames {bad[:10] + t0}"
+    return dict(frames=n, fired=int(fired.size), excluded=int(excluded.sum()),
+                max_logit_rel=float(rel.max()) if rel.size else 0.0,
+                near_delta=int(np.sum(np.abs(ref["score"] - wl.delta_diff) <=
+                                      1e-5 * max(abs(wl.delta_diff), 1.0))))

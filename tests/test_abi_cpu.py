@@ -1,0 +1,119 @@
+"""Host-side checks of libnsc: exports, validation paths, sizes (no GPU calls)."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_1703_02529_amd as nsc
+import synth
+from synth import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "nsc.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(nsc_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = _declared_functions()
+    assert len(names) >= 17
+    L = ctypes.CDLL(nsc.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def _cfg(**kw):
+    base = dict(in_h=480, in_w=640, dd_h=50, dd_w=50, cnn_h=50, cnn_w=50, ref_mode=0, delta=15,
+                grid=(1, 1), delta_diff=15.0, c_low=0.2, c_high=0.8)
+    base.update(kw)
+    return nsc.make_cfg(**base)
+
+
+def test_valid_configs_pass():
+    assert nsc.nsc_cfg_check(_cfg()) == 0
+    for wl in W.ALL:
+        c = nsc.make_cfg(in_h=wl.video.h, in_w=wl.video.w, dd_h=wl.dd_h, dd_w=wl.dd_w,
+                         cnn_h=wl.cnn.in_h, cnn_w=wl.cnn.in_w, ref_mode=wl.ref_mode,
+                         delta=wl.delta, grid=wl.grid, delta_diff=wl.delta_diff)
+        # pointers the check requires are given as dummy non-null values
+        c.lr_w = 16 if wl.grid != (1, 1) else None
+        c.ref_sums = 16 if wl.ref_mode == 1 else None
+        assert nsc.nsc_cfg_check(c) == 0, (wl.name, nsc.last_error())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dd_h=600), -2),                 # grid larger than the frame
+    (dict(dd_w=0), -2),
+    (dict(cnn_h=30), -2),                 # does not divide the detector grid
+    (dict(delta=0), -1),
+    (dict(delta=257), -1),
+    (dict(ref_mode=2), -1),
+    (dict(ref_mode=1), -1),               # fixed reference without ref_sums
+    (dict(grid=(10, 10)), -1),            # blocked without lr_w
+    (dict(grid=(51, 1)), -2),
+    (dict(delta_diff=math.nan), -1),
+    (dict(c_low=0.9, c_high=0.1), -1),
+    (dict(c_low=-0.1), -1),
+    (dict(c_high=1.5), -1),
+])
+def test_invalid_configs(kw, code):
+    assert nsc.nsc_cfg_check(_cfg(**kw)) == code
+    assert nsc.last_error() != ""
+
+
+def test_frame_stride_and_overflow_limits():
+    c = _cfg()
+    c.frame_stride = 480 * 640 * 3 - 1
+    assert nsc.nsc_cfg_check(c) == -1
+    # 255 * den must fit 32-bit sums: 20000x20000 onto 1x1 has den 4e8
+    assert nsc.lib().nsc_area_den(20000, 20000, 1, 1) == -2
+    assert nsc.nsc_area_den(480, 640, 50, 50) == 3072
+    with pytest.raises(nsc.NscError):
+        nsc.nsc_area_den(10, 10, 20, 20)
+
+
+@pytest.mark.parametrize("H,W,Ho,Wo", [(480, 640, 50, 50), (720, 1280, 100, 100), (100, 100, 50, 50),
+                                       (1080, 1920, 100, 100), (7, 9, 3, 4)])
+def test_area_den_formula(H, W, Ho, Wo):
+    assert nsc.nsc_area_den(H, W, Ho, Wo) == (H // math.gcd(H, Ho)) * (W // math.gcd(W, Wo))
+
+
+def test_cnn_desc_checks_and_blob_size():
+    for wl in W.ALL:
+        d = nsc.make_desc(wl.cnn.conv, wl.cnn.pool, wl.cnn.dense, wl.cnn.in_h, wl.cnn.in_w,
+                          wl.cnn.bf16)
+        assert nsc.nsc_cnn_check(d) == 0, nsc.last_error()
+        blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, 1))
+        assert nsc.nsc_cnn_blob_floats(d) == blob.size
+    bad = [
+        nsc.make_desc((24,), (True,), 32, 50, 50, True),            # 24 output channels
+        nsc.make_desc((32, 40), (True, True), 32, 50, 50, True),    # 40 output channels
+        nsc.make_desc((32,), (True,), 48, 50, 50, True),            # dense 48
+        nsc.make_desc((), (), 32, 50, 50, True),                    # no conv
+        nsc.make_desc((256, 256), (False, False), 32, 50, 50, True),  # LDS too large
+    ]
+    for d in bad:
+        assert nsc.nsc_cnn_check(d) == -2, nsc.last_error()
+    d = nsc.make_desc((32,), (True,), 32, 50, 50, True)
+    d.dtype = 7
+    assert nsc.nsc_cnn_check(d) == -3
+
+
+def test_status_strings():
+    assert nsc.status_string(0) == "NSC_OK"
+    assert nsc.status_string(-4) == "NSC_E_WORKSPACE"
+    assert nsc.status_string(-99) == "NSC_E_UNKNOWN"
+
+
+def test_compact_workspace_size():
+    assert nsc.nsc_compact_workspace_bytes(0) >= 4
+    assert nsc.nsc_compact_workspace_bytes(4097) >= 2 * 4
+    with pytest.raises(nsc.NscError):
+        nsc.nsc_compact_workspace_bytes(-1)

@@ -266,8 +266,8 @@ def test_cnn_zero_weights_and_center_tap():
             for k, v in wts.items()}
     zero["b2"] = np.array([0.75], np.float32)
     S = rng.integers(0, 256, size=(4, 4, 3)).astype(np.int64)
-    z = oracle.cnn_logit(spec, synth.weight_blob(spec, zero), S, 1)
-    assert z == 0.75
+    z, sc = oracle.cnn_logit(spec, synth.weight_blob(spec, zero), S, 1, want_scale=True)
+    assert z == 0.75 and sc == 0.75
     # b2 = 0 gives p = 0.5, which defers under (0.2, 0.8)
     assert oracle.sigmoid(0.0) == 0.5 and oracle.decide(0.5, 0.2, 0.8) == 2
     # centre-tap-only conv: channel o of the conv output is a per-pixel linear map
@@ -283,8 +283,10 @@ def test_cnn_zero_weights_and_center_tap():
     x = S / 127.5 - 1.0
     assert feats[5] == pytest.approx(max(0.0, 2.0 * x[1, 1, 0] + 0.5), rel=1e-15)
     assert feats[16 + 6] == pytest.approx(max(0.0, -x[1, 2, 2] + 0.25), rel=1e-15)
-    z = oracle.cnn_logit(spec, synth.weight_blob(spec, t), S, 1)
+    z, sc = oracle.cnn_logit(spec, synth.weight_blob(spec, t), S, 1, want_scale=True)
     assert z == pytest.approx(feats[5] + feats[16 + 6], rel=1e-15)
+    # scale = |b2| + sum_j |w2_j h_j| with hidden units h = features picked by w1 (b1 = 0)
+    assert sc == pytest.approx(abs(feats[5]) + abs(feats[16 + 6]), rel=1e-15)
 
 
 def test_decision_rule_ties_defer():
