@@ -16,135 +16,298 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 namespace nsc {
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// Vertical pass over the source rows of output row Y for one lane's chunk.
-// Returns the per-byte weighted column sums in out[CB].
-template <int CB, bool PACKED>
-__device__ __forceinline__ void vertical_sums(const uint8_t* __restrict__ col, int64_t row_bytes,
-                                              int64_t a0, int64_t a1, int32_t q, int j0, int j1,
-                                              int32_t out[CB]) {
-  if constexpr (CB == 1) {
-    int32_t acc = 0;
-    for (int j = j0; j < j1; ++j) {
-      int64_t r0 = (int64_t)j * q;
-      int32_t w = (int32_t)(min(a1, r0 + q) - max(a0, r0));
-      acc += w * (int32_t)col[(int64_t)j * row_bytes];
-    }
-    out[0] = acc;
+#ifndef NSC_ROWS_BATCH
+#define NSC_ROWS_BATCH 8
+#endif
+
+// One lane's 4 bytes split into two words of two 16-bit fields:
+// e0 = (b0, b2), e1 = (b1, b3).
+__device__ __forceinline__ uint32_t bytes02(uint32_t x) { return x & 0x00FF00FFu; }
+__device__ __forceinline__ uint32_t bytes13(uint32_t x) {
+  return __builtin_amdgcn_perm(0u, x, 0x0C030C01u);  // (x.b1, 0, x.b3, 0)
+}
+
+template <int CB>
+__device__ __forceinline__ void load_chunk(const uint8_t* p, uint32_t (&v)[CB >= 4 ? CB / 4 : 1]) {
+  if constexpr (CB == 16) {
+    const u32x4 x = *reinterpret_cast<const u32x4*>(p);
+    v[0] = x[0];
+    v[1] = x[1];
+    v[2] = x[2];
+    v[3] = x[3];
+  } else if constexpr (CB == 4) {
+    v[0] = *reinterpret_cast<const uint32_t*>(p);
   } else {
-    constexpr int ND = CB / 4;
-    uint32_t lo[ND], hi[ND];
-#pragma unroll
-    for (int d = 0; d < ND; ++d) lo[d] = hi[d] = 0;
-    for (int j = j0; j < j1; j += 4) {
-      uint32_t v[4][ND];
-      uint32_t w[4];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int jj = j + k;
-        w[k] = 0;
-#pragma unroll
-        for (int d = 0; d < ND; ++d) v[k][d] = 0;
-        if (jj < j1) {
-          const int64_t r0 = (int64_t)jj * q;
-          w[k] = (uint32_t)(min(a1, r0 + q) - max(a0, r0));
-          const uint8_t* p = col + (int64_t)jj * row_bytes;
-          if constexpr (CB == 16) {
-            const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-            v[k][0] = x[0];
-            v[k][1] = x[1];
-            v[k][2] = x[2];
-            v[k][3] = x[3];
-          } else {
-            v[k][0] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p));
-          }
-        }
-      }
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-#pragma unroll
-        for (int d = 0; d < ND; ++d) {
-          if constexpr (PACKED) {
-            lo[d] += w[k] * (v[k][d] & 0x00FF00FFu);
-            hi[d] += w[k] * ((v[k][d] >> 8) & 0x00FF00FFu);
-          } else {
-            // unpacked: lo/hi hold bytes 0,1 and bytes 2,3 would overflow; use 4 sums
-            // (stored in out directly below)
-            out[4 * d + 0] += (int32_t)(w[k] * (v[k][d] & 0xFFu));
-            out[4 * d + 1] += (int32_t)(w[k] * ((v[k][d] >> 8) & 0xFFu));
-            out[4 * d + 2] += (int32_t)(w[k] * ((v[k][d] >> 16) & 0xFFu));
-            out[4 * d + 3] += (int32_t)(w[k] * (v[k][d] >> 24));
-          }
-        }
-      }
-    }
-    if constexpr (PACKED) {
-#pragma unroll
-      for (int d = 0; d < ND; ++d) {
-        out[4 * d + 0] = (int32_t)(lo[d] & 0xFFFFu);
-        out[4 * d + 1] = (int32_t)(hi[d] & 0xFFFFu);
-        out[4 * d + 2] = (int32_t)(lo[d] >> 16);
-        out[4 * d + 3] = (int32_t)(hi[d] >> 16);
-      }
-    }
+    v[0] = *p;
   }
 }
 
+// Vertical pass of one output row for one lane's chunk of CB bytes: the
+// output row covers source rows j0..j1-1; the first and last may be partial
+// (weights wf, wl), every row in between has the full weight q.  Interior
+// rows are summed without multiplies and scaled by q once.  PACKED keeps two
+// 16-bit fields per 32-bit register (exact while 255 * p < 65536).  All
+// control flow is uniform across the wave.
+template <int CB, bool PACKED, int RB = NSC_ROWS_BATCH>
+__device__ __forceinline__ void vertical_sums(const uint8_t* __restrict__ col, int64_t row_bytes,
+                                              int a0, int a1, int q, int j0, int j1,
+                                              int32_t out[CB]) {
+  constexpr int ND = CB >= 4 ? CB / 4 : 1;
+  constexpr int NA = CB == 1 ? 1 : (PACKED ? 2 * ND : CB);
+  const uint32_t wf = (uint32_t)(min(a1, (j0 + 1) * q) - a0);
+  const uint32_t wl = (uint32_t)(a1 - max(a0, (j1 - 1) * q));
+  uint32_t S[NA], A[NA];  // interior sums, weighted end rows
+#pragma unroll
+  for (int k = 0; k < NA; ++k) S[k] = A[k] = 0;
+  auto add = [&](uint32_t (&acc)[NA], const uint32_t (&v)[ND], uint32_t w, bool weighted) {
+#pragma unroll
+    for (int d = 0; d < ND; ++d) {
+      if constexpr (CB == 1) {
+        acc[0] += weighted ? __umul24(w, v[0]) : v[0];
+      } else if constexpr (PACKED) {
+        const uint32_t e0 = bytes02(v[d]), e1 = bytes13(v[d]);
+        acc[d] += weighted ? __umul24(w, e0) : e0;
+        acc[ND + d] += weighted ? __umul24(w, e1) : e1;
+      } else {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const uint32_t e = __builtin_amdgcn_ubfe(v[d], 8 * b, 8);
+          acc[4 * d + b] += weighted ? __umul24(w, e) : e;
+        }
+      }
+    }
+  };
+  {
+    uint32_t v[ND];
+    load_chunk<CB>(col + (int64_t)j0 * row_bytes, v);
+    add(A, v, j1 - 1 > j0 ? wf : (uint32_t)(a1 - a0), true);
+  }
+  const uint8_t* p = col + (int64_t)(j0 + 1) * row_bytes;
+  int j = j0 + 1;
+  for (; j + RB <= j1 - 1; j += RB, p += RB * row_bytes) {  // full batches: RB loads in flight
+    uint32_t v[RB][ND];
+#pragma unroll
+    for (int k = 0; k < RB; ++k) load_chunk<CB>(p + k * row_bytes, v[k]);
+#pragma unroll
+    for (int k = 0; k < RB; ++k) add(S, v[k], 0u, false);
+  }
+  for (; j < j1 - 1; ++j, p += row_bytes) {
+    uint32_t v[ND];
+    load_chunk<CB>(p, v);
+    add(S, v, 0u, false);
+  }
+  if (j1 - 1 > j0) {
+    uint32_t v[ND];
+    load_chunk<CB>(col + (int64_t)(j1 - 1) * row_bytes, v);
+    add(A, v, wl, true);
+  }
+#pragma unroll
+  for (int k = 0; k < NA; ++k) A[k] += (uint32_t)q * S[k];  // full 32 bits: two packed fields
+  if constexpr (CB == 1) {
+    out[0] = (int32_t)A[0];
+  } else if constexpr (PACKED) {
+#pragma unroll
+    for (int d = 0; d < ND; ++d) {
+      out[4 * d + 0] = (int32_t)(A[d] & 0xFFFFu);
+      out[4 * d + 1] = (int32_t)(A[ND + d] & 0xFFFFu);
+      out[4 * d + 2] = (int32_t)(A[d] >> 16);
+      out[4 * d + 3] = (int32_t)(A[ND + d] >> 16);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < CB; ++k) out[k] = (int32_t)A[k];
+  }
+}
+
+// Per-output-row kernel (any chunk width): for each output row, the lanes
+// load its source rows in batches of four and accumulate vertically; the
+// column sums go to a double-buffered LDS row (16-bit when exact) and, after
+// one barrier, one thread per output cell applies the column weights.
 template <int CB, bool PACKED>
-__global__ void __launch_bounds__(1024) k_area_sums(const uint8_t* __restrict__ frames,
-                                                    int64_t stride, Axis ay, Axis ax,
-                                                    int32_t lanes, int32_t bands,
-                                                    int32_t* __restrict__ sums) {
-  extern __shared__ int32_t rowbuf[];  // 2 x (in_w * 3) int32, double buffered
+__global__ void __launch_bounds__(1024) k_area_sums_rows(const uint8_t* __restrict__ frames,
+                                                         int64_t stride, Axis ay, Axis ax,
+                                                         int32_t lanes, int32_t bands,
+                                                         int32_t* __restrict__ sums) {
+  using cell_t = typename std::conditional<PACKED, uint16_t, int32_t>::type;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int row_bytes = ax.n_in * 3;
+  cell_t* rowbuf = reinterpret_cast<cell_t*>(smem);  // 2 x row_bytes, double buffered
   const int64_t f = blockIdx.x / bands;
   const int band = blockIdx.x - (int)(f * bands);
   const int Ho = ay.n_out, Wo = ax.n_out;
   const int Y0 = (int)((int64_t)band * Ho / bands);
   const int Y1 = (int)((int64_t)(band + 1) * Ho / bands);
-  const int64_t row_bytes = (int64_t)ax.n_in * 3;
+  const int px = ax.p, qx = ax.q;
   const int tid = threadIdx.x;
-  const uint8_t* col = frames + f * stride + (int64_t)tid * CB;
+  const bool active = tid < lanes;
+  const uint8_t* col = frames + f * stride + (int64_t)(active ? tid : 0) * CB;
   int32_t* out = sums + f * (int64_t)Ho * Wo * 3;
+  // Output column X covers source pixels i0..il: interior pixels have weight
+  // qx, the end pixels the partial overlaps wf, wl.
+  size_t xoff = (2 * (size_t)row_bytes * sizeof(cell_t) + 15) / 16 * 16;
+  int4* xtab = reinterpret_cast<int4*>(smem + xoff);
+  for (int X = tid; X < Wo; X += blockDim.x) {
+    const int b0 = X * px, b1 = b0 + px;
+    const int i0 = b0 / qx, il = (b1 - 1) / qx;
+    xtab[X] = make_int4(i0, il - i0, il == i0 ? px : (i0 + 1) * qx - b0, b1 - il * qx);
+  }
   for (int Y = Y0; Y < Y1; ++Y) {
-    const int64_t a0 = (int64_t)Y * ay.p, a1 = a0 + ay.p;
-    const int j0 = (int)(a0 / ay.q), j1 = (int)((a1 + ay.q - 1) / ay.q);
-    int32_t* buf = rowbuf + (Y & 1) * row_bytes;
-    if (tid < lanes) {
-      int32_t v[CB];
+    // uniform row bounds (divisions run on the vector unit; move them to scalars)
+    const int a0 = Y * ay.p, a1 = a0 + ay.p;
+    const int j0 = __builtin_amdgcn_readfirstlane(a0 / ay.q);
+    const int j1 = __builtin_amdgcn_readfirstlane((a1 + ay.q - 1) / ay.q);
+    cell_t* buf = rowbuf + (Y & 1) * row_bytes;
+    int32_t v[CB];
+    vertical_sums<CB, PACKED>(col, row_bytes, a0, a1, ay.q, j0, j1, v);
+    if (active) {
 #pragma unroll
-      for (int b = 0; b < CB; ++b) v[b] = 0;
-      vertical_sums<CB, PACKED>(col, row_bytes, a0, a1, ay.q, j0, j1, v);
-      if constexpr (CB == 16) {
-        int4* dst = reinterpret_cast<int4*>(buf + tid * 16);
-        dst[0] = make_int4(v[0], v[1], v[2], v[3]);
-        dst[1] = make_int4(v[4], v[5], v[6], v[7]);
-        dst[2] = make_int4(v[8], v[9], v[10], v[11]);
-        dst[3] = make_int4(v[12], v[13], v[14], v[15]);
-      } else {
-#pragma unroll
-        for (int b = 0; b < CB; ++b) buf[tid * CB + b] = v[b];
-      }
+      for (int b = 0; b < CB; ++b) buf[tid * CB + b] = (cell_t)v[b];
     }
     __syncthreads();
-    // Horizontal pass: thread t owns output cell (X, c) = (t / 3, t % 3).
+    int32_t* orow = out + (int64_t)Y * Wo * 3;
     for (int t = tid; t < Wo * 3; t += blockDim.x) {
-      const int X = t / 3, c = t - 3 * (t / 3);
-      const int64_t b0 = (int64_t)X * ax.p, b1 = b0 + ax.p;
-      const int i0 = (int)(b0 / ax.q), i1 = (int)((b1 + ax.q - 1) / ax.q);
-      int32_t s = 0;
-      for (int i = i0; i < i1; ++i) {
-        const int64_t c0 = (int64_t)i * ax.q;
-        const int32_t w = (int32_t)(min(b1, c0 + ax.q) - max(b0, c0));
-        s += w * buf[3 * i + c];
+      const int X = t / 3, c = t - 3 * X;
+      const int4 e = xtab[X];  // i0, number of pixels after the first, wf, wl
+      const cell_t* bp = buf + 3 * e.x + c;
+      int32_t mid = 0;
+      int i = 1;
+      for (; i + 8 <= e.y; i += 8) {  // eight independent LDS reads per step
+        int32_t m8 = 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) m8 += (int32_t)bp[3 * (i + u)];
+        mid += m8;
       }
-      out[((int64_t)Y * Wo + X) * 3 + c] = s;
+      for (; i < e.y; ++i) mid += (int32_t)bp[3 * i];
+      int32_t s;
+      if constexpr (PACKED) {  // all factors below 2^24
+        s = (int32_t)(__umul24((uint32_t)e.z, bp[0]) + __umul24((uint32_t)qx, (uint32_t)mid));
+        if (e.y > 0) s += (int32_t)__umul24((uint32_t)e.w, bp[3 * e.y]);
+      } else {
+        s = e.z * (int32_t)bp[0] + qx * mid;
+        if (e.y > 0) s += e.w * (int32_t)bp[3 * e.y];
+      }
+      orow[t] = s;
     }
     // The next row writes the other buffer; its readers (row Y-1) all passed
     // this row's barrier, so no second barrier is needed.
+  }
+}
+
+// Wave-autonomous kernel: no workgroup barriers, and no global stores until
+// the end of a wave's work.  The horizontal resampling pattern repeats every
+// p_x source pixels (q_x output columns); a "group" is the smallest whole
+// number of periods whose bytes split into 16/4-byte lane chunks.  Each wave
+// owns a strip of whole groups of one band of output rows of one frame, so
+// the horizontal reduction stays inside the wave: lanes write their vertical
+// sums to a wave-private LDS strip, __syncwarp() orders the writes before the
+// reads, and the same lanes produce the strip's output cells into a
+// wave-private LDS block of the band's sums.  That block is written to HBM
+// once, after the last source row: on this architecture a store makes the
+// wave wait for it before it may consume later loads, so stores interleaved
+// with the row stream would stall it.
+template <int CB, bool PACKED, int RB = NSC_ROWS_BATCH>
+__global__ void __launch_bounds__(256) k_area_sums_wave(const uint8_t* __restrict__ frames,
+                                                        int64_t stride, Axis ay, Axis ax,
+                                                        WaveGeom g, int32_t bands, int64_t n,
+                                                        int32_t* __restrict__ sums) {
+  using cell_t = typename std::conditional<PACKED, uint16_t, int32_t>::type;
+  extern __shared__ __align__(16) unsigned char smem[];
+  // the wave index is uniform across the wave; say so, so that everything
+  // derived from it (frame, strip, rows) lives in scalar registers
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int Ho = ay.n_out, Wo = ax.n_out;
+  const int px = ax.p, qx = ax.q;
+  const int scols = g.groups_per_wave * g.group_cols;  // output columns of a full strip
+  // per-column table of a strip (identical for every strip): first pixel,
+  // pixels after the first, partial weights of the first and last pixel
+  int4* xtab = reinterpret_cast<int4*>(smem);
+  for (int x = threadIdx.x; x < scols; x += blockDim.x) {
+    const int b0 = x * px, b1 = b0 + px;
+    const int i0 = b0 / qx, il = (b1 - 1) / qx;
+    xtab[x] = make_int4(i0, il - i0, il == i0 ? px : (i0 + 1) * qx - b0, b1 - il * qx);
+  }
+  __syncthreads();  // the only workgroup barrier
+  const size_t per_wave = (size_t)64 * CB * sizeof(cell_t) + (size_t)g.band_rows * scols * 3 * 4;
+  unsigned char* wbase = smem + (size_t)scols * 16 + (size_t)wv * per_wave;
+  cell_t* buf = reinterpret_cast<cell_t*>(wbase);                              // column sums
+  int32_t* sbuf = reinterpret_cast<int32_t*>(wbase + (size_t)64 * CB * sizeof(cell_t));  // band sums
+
+  const int64_t unit = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
+  const int64_t per_frame = (int64_t)bands * g.waves_per_frame;
+  if (unit >= n * per_frame) return;
+  const int64_t f = unit / per_frame;
+  const int rem = (int)(unit - f * per_frame);
+  const int band = rem / g.waves_per_frame, strip = rem - band * g.waves_per_frame;
+  const int group0 = strip * g.groups_per_wave;
+  const int ngroups = min(g.groups_per_wave, g.groups_per_row - group0);
+  const bool active = lane < ngroups * g.group_lanes;
+  const int ncells = ngroups * g.group_cols * 3;
+  const int X0 = group0 * g.group_cols;
+  const int Y0 = (int)((int64_t)band * Ho / bands);
+  const int Y1 = (int)((int64_t)(band + 1) * Ho / bands);
+  const int64_t row_bytes = (int64_t)ax.n_in * 3;
+  const uint8_t* col =
+      frames + f * stride + ((int64_t)group0 * g.group_lanes + (active ? lane : 0)) * CB;
+  for (int Y = Y0; Y < Y1; ++Y) {
+    // uniform row bounds (divisions run on the vector unit; move them to scalars)
+    const int a0 = Y * ay.p, a1 = a0 + ay.p;
+    const int j0 = __builtin_amdgcn_readfirstlane(a0 / ay.q);
+    const int j1 = __builtin_amdgcn_readfirstlane((a1 + ay.q - 1) / ay.q);
+    int32_t v[CB];
+    vertical_sums<CB, PACKED, RB>(col, row_bytes, a0, a1, ay.q, j0, j1, v);
+    if (active) {
+      if constexpr (PACKED && CB == 16) {  // 32 bytes per lane as two 16-byte stores
+        uint4* d = reinterpret_cast<uint4*>(buf + lane * CB);
+        d[0] = make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16),
+                          v[6] | (v[7] << 16));
+        d[1] = make_uint4(v[8] | (v[9] << 16), v[10] | (v[11] << 16), v[12] | (v[13] << 16),
+                          v[14] | (v[15] << 16));
+      } else {
+#pragma unroll
+        for (int b = 0; b < CB; ++b) buf[lane * CB + b] = (cell_t)v[b];
+      }
+    }
+    __syncwarp();
+    int32_t* srow = sbuf + (Y - Y0) * ncells;
+    for (int t = lane; t < ncells; t += 64) {
+      const int x = t / 3, c = t - 3 * x;
+      const int4 e = xtab[x];
+      const cell_t* bp = buf + 3 * e.x + c;
+      int32_t mid = 0;
+      int i = 1;
+      for (; i + 8 <= e.y; i += 8) {
+        int32_t m8 = 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) m8 += (int32_t)bp[3 * (i + u)];
+        mid += m8;
+      }
+      for (; i < e.y; ++i) mid += (int32_t)bp[3 * i];
+      int32_t s;
+      if constexpr (PACKED) {  // all factors below 2^24
+        s = (int32_t)(__umul24((uint32_t)e.z, bp[0]) + __umul24((uint32_t)qx, (uint32_t)mid));
+        if (e.y > 0) s += (int32_t)__umul24((uint32_t)e.w, bp[3 * e.y]);
+      } else {
+        s = e.z * (int32_t)bp[0] + qx * mid;
+        if (e.y > 0) s += e.w * (int32_t)bp[3 * e.y];
+      }
+      srow[t] = s;
+    }
+    __syncwarp();  // reads of this row's strip precede the next row's writes
+  }
+  // the band's sums, one output row segment after another
+  int32_t* out = sums + (f * (int64_t)Ho * Wo + X0) * 3;
+  for (int Y = Y0; Y < Y1; ++Y) {
+    const int32_t* srow = sbuf + (Y - Y0) * ncells;
+    int32_t* orow = out + (int64_t)Y * Wo * 3;
+    for (int t = lane; t < ncells; t += 64) orow[t] = srow[t];
   }
 }
 
@@ -247,8 +410,36 @@ int make_area_plan(int32_t in_h, int32_t in_w, int64_t stride, const void* frame
                 (long long)row_bytes, p.lanes, p.chunk_bytes);
   p.threads = (p.lanes + 63) / 64 * 64;
   if (p.threads < 64) p.threads = 64;
+  // wave strips: whole periods of the horizontal pattern in 16/4-byte chunks
+  p.wave = false;
+  if (p.chunk_bytes != 1) {
+    int k = 1;
+    while ((3 * (int64_t)p.ax.p * k) % p.chunk_bytes != 0) k *= 2;
+    const int64_t glanes = 3 * (int64_t)p.ax.p * k / p.chunk_bytes;
+    const int64_t gpix = (int64_t)p.ax.p * k;
+    if (glanes <= 64 && in_w % gpix == 0) {
+      WaveGeom& g = p.wg;
+      g.group_lanes = (int32_t)glanes;
+      g.group_cols = p.ax.q * k;
+      g.groups_per_wave = (int32_t)(64 / glanes);
+      g.groups_per_row = (int32_t)(in_w / gpix);
+      g.waves_per_frame = (g.groups_per_row + g.groups_per_wave - 1) / g.groups_per_wave;
+      // bands of about 10 output rows; more when there are too few frames to fill the chip
+      int64_t wb = (out_h + 9) / 10;
+      const int64_t fill = (16384 + n * g.waves_per_frame - 1) / (n * g.waves_per_frame > 0 ? n * g.waves_per_frame : 1);
+      if (fill > wb) wb = fill;
+      if (wb > out_h) wb = out_h;
+      g.bands = (int32_t)wb;
+      g.band_rows = (int32_t)((out_h + wb - 1) / wb);
+      const int64_t scols = (int64_t)g.groups_per_wave * g.group_cols;
+      const int64_t cellb = p.packed ? 2 : 4;
+      g.lds_bytes = (size_t)(scols * 16 + 4 * (64 * p.chunk_bytes * cellb + (int64_t)g.band_rows * scols * 3 * 4));
+      p.wave = g.lds_bytes <= 64 * 1024;
+    }
+  }
   // vertical column sums reach 255 * p_y; 16-bit packing is exact below 65536
   p.packed = 255LL * p.ay.p < 65536;
+  // split frames into bands of output rows when there are too few frames to fill the chip
   int64_t bands = (4096 + n - 1) / (n > 0 ? n : 1);
   if (bands < 1) bands = 1;
   if (bands > out_h) bands = out_h;
@@ -262,19 +453,40 @@ int launch_area_sums(const AreaPlan& p, const uint8_t* frames, int64_t stride, i
   if (n <= 0) return NSC_OK;
   const int64_t blocks = n * p.bands;
   if (blocks > 0x7FFFFFFF) return fail(NSC_E_SHAPE, "too many frames in one call");
-  const size_t lds = 2 * (size_t)p.ax.n_in * 3 * sizeof(int32_t);
+  const size_t row_bytes = (size_t)p.ax.n_in * 3;
   dim3 grid((unsigned)blocks), block(p.threads);
-#define NSC_AREA_LAUNCH(CB, PK)                                                          \
-  hipLaunchKernelGGL((k_area_sums<CB, PK>), grid, block, lds, stream, frames, stride, p.ay, \
-                     p.ax, p.lanes, p.bands, sums)
-  if (p.chunk_bytes == 16) {
-    if (p.packed) NSC_AREA_LAUNCH(16, true); else NSC_AREA_LAUNCH(16, false);
-  } else if (p.chunk_bytes == 4) {
-    if (p.packed) NSC_AREA_LAUNCH(4, true); else NSC_AREA_LAUNCH(4, false);
-  } else {
-    NSC_AREA_LAUNCH(1, false);
+  if (p.wave) {
+    const WaveGeom& g = p.wg;
+    const int64_t units = n * g.bands * g.waves_per_frame;
+    const int64_t wblocks = (units + 3) / 4;
+    if (wblocks > 0x7FFFFFFF) return fail(NSC_E_SHAPE, "too many frames in one call");
+#define NSC_WAVE_LAUNCH(CB, PK)                                                          \
+  hipLaunchKernelGGL((k_area_sums_wave<CB, PK>), dim3((unsigned)wblocks), dim3(256),      \
+                     g.lds_bytes, stream, frames, stride, p.ay, p.ax, g, g.bands, n, sums)
+    if (p.chunk_bytes == 16) {
+      if (p.packed) NSC_WAVE_LAUNCH(16, true); else NSC_WAVE_LAUNCH(16, false);
+    } else {
+      if (p.packed) NSC_WAVE_LAUNCH(4, true); else NSC_WAVE_LAUNCH(4, false);
+    }
+#undef NSC_WAVE_LAUNCH
+    NSC_CHECK_LAUNCH("k_area_sums_wave");
+    return NSC_OK;
   }
-#undef NSC_AREA_LAUNCH
+  {
+    const size_t cell = p.packed ? 2 : 4;
+    const size_t lds = (2 * row_bytes * cell + 15) / 16 * 16 + (size_t)p.ax.n_out * 16;
+#define NSC_ROWS_LAUNCH(CB, PK)                                                              \
+  hipLaunchKernelGGL((k_area_sums_rows<CB, PK>), grid, block, lds, stream, frames, stride, p.ay, \
+                     p.ax, p.lanes, p.bands, sums)
+    if (p.chunk_bytes == 16) {
+      if (p.packed) NSC_ROWS_LAUNCH(16, true); else NSC_ROWS_LAUNCH(16, false);
+    } else if (p.chunk_bytes == 4) {
+      if (p.packed) NSC_ROWS_LAUNCH(4, true); else NSC_ROWS_LAUNCH(4, false);
+    } else {
+      if (p.packed) NSC_ROWS_LAUNCH(1, true); else NSC_ROWS_LAUNCH(1, false);
+    }
+#undef NSC_ROWS_LAUNCH
+  }
   NSC_CHECK_LAUNCH("k_area_sums");
   return NSC_OK;
 }

@@ -48,6 +48,18 @@ struct Axis {
   }
 };
 
+// Column strips of the wave-autonomous area kernel.
+struct WaveGeom {
+  int32_t group_lanes;      // lanes of one group (whole periods of the column pattern)
+  int32_t group_cols;       // output columns of one group
+  int32_t groups_per_wave;  // groups in one wave's strip
+  int32_t groups_per_row;   // groups across the frame
+  int32_t waves_per_frame;  // strips across the frame
+  int32_t bands;            // bands of output rows per frame (one wave each per strip)
+  int32_t band_rows;        // at most this many output rows per band
+  size_t lds_bytes;         // dynamic LDS of a 4-wave workgroup
+};
+
 // Area-sum launch plan for one frame geometry.
 struct AreaPlan {
   Axis ay, ax;
@@ -56,6 +68,8 @@ struct AreaPlan {
   int32_t threads;       // lanes rounded up to a multiple of 64
   int32_t bands;         // output-row bands per frame
   bool packed;           // 16-bit packed vertical accumulators are exact
+  bool wave;             // wave-autonomous strips apply (else the per-row kernel)
+  WaveGeom wg;
 };
 int make_area_plan(int32_t in_h, int32_t in_w, int64_t stride, const void* frames,
                    int32_t out_h, int32_t out_w, int64_t n, AreaPlan* plan);
