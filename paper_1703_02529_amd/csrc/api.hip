@@ -24,7 +24,7 @@ int fail(int code, const char* fmt, ...) {
 }
 
 size_t conv_lds_bytes(const CnnLayer& L, bool bf16, int32_t* cin_lds, int32_t* w_lds,
-                      int32_t* band_w);
+                      int32_t* band_w, int32_t* band_tiles);
 
 namespace {
 
@@ -124,12 +124,13 @@ int plan_cnn(const nsc_cnn_desc* d, Cnn* cnn) {
     L.h = h;
     L.w = w;
     L.pool = pool;
-    L.kpad = l == 0 ? (bf16 ? 32 : 28) : 9 * cin;
+    // layer 0: K = (dy, dx of 4, c of 4) = 48, padded with zero weights to whole MFMA steps
+    L.kpad = l == 0 ? (bf16 ? 64 : 48) : 9 * cin;
     L.w_off = woff;
     L.b_off = boff;
     woff += (size_t)co * L.kpad;
     boff += co;
-    const size_t lds = conv_lds_bytes(L, bf16, nullptr, nullptr, nullptr);
+    const size_t lds = conv_lds_bytes(L, bf16, nullptr, nullptr, nullptr, nullptr);
     NSC_REQUIRE(lds <= kMaxLds, NSC_E_SHAPE,
                 "conv layer %d needs %zu bytes of LDS (limit %zu)", l, lds, kMaxLds);
     if (pool) {
@@ -272,7 +273,7 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
       for (int ci = 0; ci < L.cin; ++ci)
         for (int t = 0; t < 9; ++t) {
           const float v = p[((size_t)o * L.cin + ci) * 9 + t];
-          const size_t k = l == 0 ? (size_t)t * 3 + ci : (size_t)t * L.cin + ci;
+          const size_t k = l == 0 ? (size_t)(t / 3) * 16 + (t % 3) * 4 + ci : (size_t)t * L.cin + ci;
           convw[L.w_off + (size_t)o * L.kpad + k] = v;
         }
     p += (size_t)L.cout * L.cin * 9;

@@ -61,6 +61,12 @@ template <> struct Elt<uint16_t> {  // bf16 stored as raw bits
   static __device__ __forceinline__ frag load(const uint16_t* p) {  // 16-byte aligned
     return *reinterpret_cast<const frag*>(p);
   }
+  static __device__ __forceinline__ frag load8(const uint16_t* p) {  // 8-byte aligned
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    const bf16x4 lo = *reinterpret_cast<const bf16x4*>(p);
+    const bf16x4 hi = *reinterpret_cast<const bf16x4*>(p + 4);
+    return frag{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  }
   static __device__ __forceinline__ frag zero() {
     frag z;
 #pragma unroll
@@ -81,6 +87,7 @@ template <> struct Elt<float> {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
   }
   static __device__ __forceinline__ float load(const float* p) { return *p; }
+  static __device__ __forceinline__ float load8(const float* p) { return *p; }
   static __device__ __forceinline__ float zero() { return 0.0f; }
   static __device__ __forceinline__ void set(float& f, int, float v) { f = v; }
 };
@@ -88,11 +95,11 @@ template <> struct Elt<float> {
 // ------------------------------------------------------------------- conv
 
 struct ConvArgs {
-  // input: first layer reads area sums of frame idx[s]; others read act_in[s]
+  // input: the first layer reads area sums of frame idx[s]; others read act_in[s]
   const int32_t* sums;
   const int32_t* idx;
   int32_t sums_h, sums_w, fy, fx;
-  double den_c;
+  int64_t den255;           // 255 * den_c: pre-processing x = (2 S - den255) / den255
   const void* act_in;
   void* act_out;
   const void* wts;          // packed [cout][kpad]
@@ -102,9 +109,10 @@ struct ConvArgs {
   int32_t cin, cout, h, w, kpad;
   int32_t pool;
   int32_t tiles_y, tiles_x;
+  int32_t band_tiles;       // tile rows per work item
   int32_t cin_lds;          // channel stride of a staged pixel (elements)
   int32_t w_lds;            // row stride of staged weights (elements)
-  int32_t band_w;           // staged columns: 4 * tiles_x + 2 (halo and tail zero-filled)
+  int32_t band_w;           // staged columns (halo and tail zero-filled)
 };
 
 // Pixel (py, px) of M row m inside a 4x4 tile: m = 4 * window + j, the four
@@ -115,28 +123,64 @@ __device__ __forceinline__ void tile_pixel(int m, int& py, int& px) {
   px = 2 * (wi & 1) + (j & 1);
 }
 
-template <typename T, bool FIRST, int NT>
-__global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
+template <typename T>
+__device__ __forceinline__ void stage_weights(const ConvArgs& a, T* wl) {
+  const T* src = reinterpret_cast<const T*>(a.wts);
+  for (int e = threadIdx.x; e < a.cout * a.kpad; e += blockDim.x) {
+    const int o = e / a.kpad, k = e - o * a.kpad;
+    wl[o * a.w_lds + k] = src[e];
+  }
+}
+
+// Bias, ReLU, optional 2x2 max-pool, rounding, NHWC store of one 4x4 tile.
+// Lane (m, g) holds rows 4g..4g+3 (one pooling window) of output channel m.
+template <typename T, int NT>
+__device__ __forceinline__ void conv_epilogue(const ConvArgs& a, const f32x4 (&acc)[NT], T* out,
+                                              int ty, int tx, int ho, int wo, int m, int g) {
+  using X = Elt<T>;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int n = nt * 16 + m;
+    const float b = a.bias[n];
+    const int wy = g >> 1, wx = g & 1;
+    if (a.pool) {
+      float v = 0.0f;  // ReLU floor
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v = fmaxf(v, acc[nt][r] + b);
+      const int oy = 2 * ty + wy, ox = 2 * tx + wx;
+      if (oy < ho && ox < wo) out[((int64_t)oy * wo + ox) * a.cout + n] = X::from_f32(v);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int oy = 4 * ty + 2 * wy + (r >> 1), ox = 4 * tx + 2 * wx + (r & 1);
+        if (oy < ho && ox < wo)
+          out[((int64_t)oy * wo + ox) * a.cout + n] = X::from_f32(fmaxf(acc[nt][r] + b, 0.0f));
+      }
+    }
+  }
+}
+
+// First layer (3 input channels).  The survivor's area sums are gathered
+// (fy x fx nested cells summed) and pre-processed into a zero-padded band in
+// LDS, 4 channels per pixel (the fourth is 0).  K is ordered (dy, dx, c) with
+// dx padded to 4 and c to 4 (zero weights), so the 8 K values of a lane group
+// are the 4 channels of two horizontally adjacent pixels: one 16-byte LDS read
+// per MFMA for bf16.  K = 48, run as 2 steps of 32 (bf16) or 12 of 4 (fp32).
+template <typename T, int NT>
+__global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
   using X = Elt<T>;
   constexpr int E = X::E, KS = X::KS;
   extern __shared__ __align__(16) unsigned char lds_raw[];
   T* wl = reinterpret_cast<T*>(lds_raw);
   T* in = wl + (size_t)a.cout * a.w_lds;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int nwaves = blockDim.x >> 6;
-
-  // stage packed weights once per workgroup
-  {
-    const T* src = reinterpret_cast<const T*>(a.wts);
-    const int per_row = a.kpad;
-    for (int e = tid; e < a.cout * per_row; e += blockDim.x) {
-      const int o = e / per_row, k = e - o * per_row;
-      wl[o * a.w_lds + k] = src[e];
-    }
-  }
+  stage_weights(a, wl);
   int64_t cnt = *a.count;
   if (cnt > a.max_count) cnt = a.max_count;
-  const int64_t items = cnt * a.tiles_y;
+  const int bands = (a.tiles_y + a.band_tiles - 1) / a.band_tiles;
+  const int64_t items = cnt * bands;
   const int band_w = a.band_w;
   const int ho = a.pool ? a.h / 2 : a.h, wo = a.pool ? a.w / 2 : a.w;
   const int m = lane & 15, g = lane >> 4;
@@ -144,13 +188,16 @@ __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
   tile_pixel(m, py, px);
 
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
-    const int64_t s = item / a.tiles_y;
-    const int ty = (int)(item - s * a.tiles_y);
-    const int y_top = 4 * ty - 1;  // input row of band row 0
+    const int64_t s = item / bands;
+    const int band = (int)(item - s * bands);
+    const int ty0 = band * a.band_tiles;
+    const int nty = min(a.band_tiles, a.tiles_y - ty0);
+    const int rows = 4 * nty + 2;
+    const int y_top = 4 * ty0 - 1;  // input row of band row 0
     __syncthreads();  // previous item's readers are done with `in` (and weights staged)
-    if constexpr (FIRST) {
+    {
       const int32_t* S = a.sums + (int64_t)a.idx[s] * a.sums_h * a.sums_w * 3;
-      for (int e = tid; e < 6 * band_w * 4; e += blockDim.x) {
+      for (int e = tid; e < rows * band_w * 4; e += blockDim.x) {
         const int c = e & 3, pix = e >> 2;
         const int br = pix / band_w, bc = pix - br * band_w;
         const int y = y_top + br, x = bc - 1;
@@ -160,15 +207,76 @@ __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
           for (int dy = 0; dy < a.fy; ++dy)
             for (int dx = 0; dx < a.fx; ++dx)
               acc += S[((int64_t)(y * a.fy + dy) * a.sums_w + (x * a.fx + dx)) * 3 + c];
-          v = X::from_f64((double)acc / a.den_c / 127.5 - 1.0);
+          // (S / den) / 127.5 - 1 as one correctly rounded division of integers:
+          // bf16 rounding of it matches the exact value's (exact ties included)
+          v = X::from_f64((double)(2 * acc - a.den255) / (double)a.den255);
         }
-        in[pix * a.cin_lds + c] = v;
+        in[pix * 4 + c] = v;
       }
-    } else {
+    }
+    __syncthreads();
+    T* out = reinterpret_cast<T*>(a.act_out) + s * (int64_t)ho * wo * a.cout;
+    for (int t = wave; t < nty * a.tiles_x; t += nwaves) {
+      const int tyl = t / a.tiles_x, tx = t - tyl * a.tiles_x;
+      f32x4 acc[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int row0 = 4 * tyl + py, col0 = 4 * tx + px;  // band coordinates of tap (0, 0)
+#pragma unroll
+      for (int k0 = 0; k0 < 48; k0 += KS) {
+        const int k = k0 + g * E;  // first K value of this lane group
+        typename X::frag av = X::zero();
+        if (k < 48) {
+          const int dy = k >> 4, dx = (k >> 2) & 3, c = k & 3;
+          av = X::load8(in + ((row0 + dy) * band_w + col0 + dx) * 4 + c);
+        }
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const typename X::frag bv = X::load(wl + (nt * 16 + m) * a.w_lds + k);
+          acc[nt] = X::mma(av, bv, acc[nt]);
+        }
+      }
+      conv_epilogue<T, NT>(a, acc, out, ty0 + tyl, tx, ho, wo, m, g);
+    }
+  }
+}
+
+// Inner layers (input channels a multiple of KS): K = 9 taps x cin, tap-major.
+template <typename T, int NT>
+__global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
+  using X = Elt<T>;
+  constexpr int E = X::E, KS = X::KS;
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  T* wl = reinterpret_cast<T*>(lds_raw);
+  T* in = wl + (size_t)a.cout * a.w_lds;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nwaves = blockDim.x >> 6;
+  stage_weights(a, wl);
+  int64_t cnt = *a.count;
+  if (cnt > a.max_count) cnt = a.max_count;
+  const int bands = (a.tiles_y + a.band_tiles - 1) / a.band_tiles;
+  const int64_t items = cnt * bands;
+  const int band_w = a.band_w;
+  const int ho = a.pool ? a.h / 2 : a.h, wo = a.pool ? a.w / 2 : a.w;
+  const int m = lane & 15, g = lane >> 4;
+  int py, px;
+  tile_pixel(m, py, px);
+  constexpr int V = 16 / sizeof(T);  // elements per 16-byte vector
+  const int vec_per_pix = a.cin / V;
+  const int chunks = a.cin / KS;
+
+  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+    const int64_t s = item / bands;
+    const int band = (int)(item - s * bands);
+    const int ty0 = band * a.band_tiles;
+    const int nty = min(a.band_tiles, a.tiles_y - ty0);
+    const int rows = 4 * nty + 2;
+    const int y_top = 4 * ty0 - 1;
+    __syncthreads();  // previous item's readers are done with `in` (and weights staged)
+    {
       const T* src = reinterpret_cast<const T*>(a.act_in) + s * (int64_t)a.h * a.w * a.cin;
-      constexpr int V = 16 / sizeof(T);  // elements per 16-byte vector
-      const int vec_per_pix = a.cin / V;
-      for (int e = tid; e < 6 * band_w * vec_per_pix; e += blockDim.x) {
+      for (int e = tid; e < rows * band_w * vec_per_pix; e += blockDim.x) {
         const int pix = e / vec_per_pix, cv = e - pix * vec_per_pix;
         const int br = pix / band_w, bc = pix - br * band_w;
         const int y = y_top + br, x = bc - 1;
@@ -179,69 +287,27 @@ __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
       }
     }
     __syncthreads();
-
-    for (int tx = wave; tx < a.tiles_x; tx += nwaves) {
+    T* out = reinterpret_cast<T*>(a.act_out) + s * (int64_t)ho * wo * a.cout;
+    for (int t = wave; t < nty * a.tiles_x; t += nwaves) {
+      const int tyl = t / a.tiles_x, tx = t - tyl * a.tiles_x;
       f32x4 acc[NT];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int col0 = 4 * tx + px;  // band column of tap dx = 0
-      if constexpr (FIRST) {
-        // K = 27 (tap-major, channel-minor) padded to kpad with zeros
-        for (int k0 = 0; k0 < a.kpad; k0 += KS) {
-          typename X::frag av = X::zero();
-#pragma unroll
-          for (int e = 0; e < E; ++e) {
-            const int k = k0 + g * E + e;
-            if (k < 27) {
-              const int tap = k / 3, c = k - 3 * tap;
-              const int dy = tap / 3, dx = tap - 3 * dy;
-              X::set(av, e, in[((py + dy) * band_w + col0 + dx) * a.cin_lds + c]);
-            }
-          }
+      const int row0 = 4 * tyl + py, col0 = 4 * tx + px;
+      for (int tap = 0; tap < 9; ++tap) {
+        const int dy = tap / 3, dx = tap - 3 * dy;
+        const T* arow = in + ((row0 + dy) * band_w + col0 + dx) * a.cin_lds + g * E;
+        const T* brow = wl + m * a.w_lds + tap * a.cin + g * E;
+        for (int ch = 0; ch < chunks; ++ch) {
+          const typename X::frag av = X::load(arow + ch * KS);
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) {
-            const typename X::frag bv = X::load(wl + (nt * 16 + m) * a.w_lds + k0 + g * E);
+            const typename X::frag bv = X::load(brow + nt * 16 * a.w_lds + ch * KS);
             acc[nt] = X::mma(av, bv, acc[nt]);
           }
         }
-      } else {
-        const int chunks = a.cin / KS;
-        for (int tap = 0; tap < 9; ++tap) {
-          const int dy = tap / 3, dx = tap - 3 * dy;
-          const T* arow = in + ((py + dy) * band_w + col0 + dx) * a.cin_lds + g * E;
-          const T* brow = wl + m * a.w_lds + tap * a.cin + g * E;
-          for (int ch = 0; ch < chunks; ++ch) {
-            const typename X::frag av = X::load(arow + ch * KS);
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-              const typename X::frag bv = X::load(brow + nt * 16 * a.w_lds + ch * KS);
-              acc[nt] = X::mma(av, bv, acc[nt]);
-            }
-          }
-        }
       }
-      // epilogue: lane holds rows 4g..4g+3 (one pooling window) of column m
-      T* out = reinterpret_cast<T*>(a.act_out) + s * (int64_t)ho * wo * a.cout;
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int n = nt * 16 + m;
-        const float b = a.bias[n];
-        const int wy = g >> 1, wx = g & 1;
-        if (a.pool) {
-          float v = 0.0f;  // ReLU floor
-#pragma unroll
-          for (int r = 0; r < 4; ++r) v = fmaxf(v, acc[nt][r] + b);
-          const int oy = 2 * ty + wy, ox = 2 * tx + wx;
-          if (oy < ho && ox < wo) out[((int64_t)oy * wo + ox) * a.cout + n] = X::from_f32(v);
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int oy = 4 * ty + 2 * wy + (r >> 1), ox = 4 * tx + 2 * wx + (r & 1);
-            if (oy < ho && ox < wo)
-              out[((int64_t)oy * wo + ox) * a.cout + n] = X::from_f32(fmaxf(acc[nt][r] + b, 0.0f));
-          }
-        }
-      }
+      conv_epilogue<T, NT>(a, acc, out, ty0 + tyl, tx, ho, wo, m, g);
     }
   }
 }
@@ -334,7 +400,10 @@ template <typename T, bool FIRST>
 int launch_conv_nt(int nt, const ConvArgs& a, unsigned grid, size_t lds, hipStream_t st) {
 #define NSC_CONV_CASE(N)                                                                       \
   case N:                                                                                      \
-    hipLaunchKernelGGL((k_conv<T, FIRST, N>), dim3(grid), dim3(256), lds, st, a);              \
+    if (FIRST)                                                                                 \
+      hipLaunchKernelGGL((k_conv_first<T, N>), dim3(grid), dim3(256), lds, st, a);             \
+    else                                                                                       \
+      hipLaunchKernelGGL((k_conv<T, N>), dim3(grid), dim3(256), lds, st, a);                   \
     break;
   switch (nt) {
     NSC_CONV_CASE(1)
@@ -383,19 +452,29 @@ void conv_tiles(const CnnLayer& L, int32_t* tiles_y, int32_t* tiles_x) {
   *tiles_x = (wn + 3) / 4;
 }
 
+// LDS of one conv layer's workgroup: staged weights plus an input band of
+// band_tiles tile rows (4 output rows each + 2 halo rows).  The band is as tall
+// as fits a budget of about 48 KB (the whole image when possible), at least
+// one tile row.
 size_t conv_lds_bytes(const CnnLayer& L, bool bf16, int32_t* cin_lds, int32_t* w_lds,
-                      int32_t* band_w) {
+                      int32_t* band_w, int32_t* band_tiles) {
   const size_t es = bf16 ? 2 : 4;
   const int32_t vec = (int32_t)(16 / es);
-  const int32_t cl = L.cin == 3 ? 4 : L.cin + vec;          // pad pixels by 16 bytes
-  const int32_t wr = L.kpad + vec;                          // pad weight rows by 16 bytes
+  const bool first = L.cin == 3;
+  const int32_t cl = first ? 4 : L.cin + vec;          // inner layers: pad pixels by 16 bytes
+  const int32_t wr = L.kpad + vec;                     // pad weight rows by 16 bytes
   int32_t ty, tx;
   conv_tiles(L, &ty, &tx);
-  const int32_t bw = 4 * tx + 2;
+  const int32_t bw = 4 * tx + (first ? 3 : 2);         // first layer reads tap dx = 3 (weight 0)
+  const size_t wbytes = (size_t)L.cout * wr * es;
+  const size_t row_bytes = (size_t)bw * cl * es;
+  int32_t bt = 1;
+  while (bt < ty && wbytes + (size_t)(4 * (bt + 1) + 2) * row_bytes <= 48 * 1024) ++bt;
   if (cin_lds) *cin_lds = cl;
   if (w_lds) *w_lds = wr;
   if (band_w) *band_w = bw;
-  return ((size_t)L.cout * wr + (size_t)6 * bw * cl) * es;
+  if (band_tiles) *band_tiles = bt;
+  return wbytes + (size_t)(4 * bt + 2) * row_bytes;
 }
 
 size_t cnn_workspace_bytes(const Cnn& cnn, int64_t max_count) {
@@ -422,7 +501,7 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
     a.sums_w = r.sums_w;
     a.fy = r.fy;
     a.fx = r.fx;
-    a.den_c = r.den_c;
+    a.den255 = (int64_t)(255.0 * r.den_c);
     a.act_in = l > 0 ? buf[(l - 1) & 1] : nullptr;
     a.act_out = buf[l & 1];
     a.wts = static_cast<const unsigned char*>(cnn.conv_w) + L.w_off * es;
@@ -436,11 +515,12 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
     a.kpad = L.kpad;
     a.pool = L.pool ? 1 : 0;
     conv_tiles(L, &a.tiles_y, &a.tiles_x);
-    const size_t lds = conv_lds_bytes(L, cnn.bf16, &a.cin_lds, &a.w_lds, &a.band_w);
+    const size_t lds =
+        conv_lds_bytes(L, cnn.bf16, &a.cin_lds, &a.w_lds, &a.band_w, &a.band_tiles);
     int per_cu = (int)((160 * 1024) / (lds + 1024));
     if (per_cu > 8) per_cu = 8;
     if (per_cu < 1) per_cu = 1;
-    int64_t items = r.max_count * a.tiles_y;
+    int64_t items = r.max_count * ((a.tiles_y + a.band_tiles - 1) / a.band_tiles);
     int64_t grid = (int64_t)kNumCU * per_cu;
     if (grid > items) grid = items;
     if (grid < 1) grid = 1;
