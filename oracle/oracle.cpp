@@ -270,20 +270,20 @@ void oracle_conv3x3(const double* in, int32_t cin, int32_t h, int32_t w, const d
 }
 
 // Evaluates the network on one frame's area sums S [in_h][in_w][3] with
-// denominator den; returns the output logit.  For bf16 networks (reading of
-// "bf16 weights and activations"), values are rounded to bf16 at the network
-// input, after each conv layer's ReLU and after the dense layer's ReLU;
-// arithmetic in between is fp64.  features_out (nullable) receives the
-// flattened input of the dense layer in (c, y, x) order.  scale_out (nullable)
-// receives the logit's scale |b2| + sum_j |w2_j h_j|: the magnitude of the
-// terms the output layer adds up, against which the logit's error is measured
-// (a logit that is a small difference of large terms has no finer relative
-// precision).
+// denominator den; returns the output logit.  For bf16 networks (reading: the
+// weights are bf16 values and the pre-processed input is rounded to bf16; the
+// activations of later layers are not rounded), everything after the input
+// rounding is fp64 arithmetic on those values.  features_out (nullable)
+// receives the flattened input of the dense layer in (c, y, x) order.
+// scale_out (nullable) receives the logit's scale |b2| + sum_j |w2_j h_j|: the
+// magnitude of the terms the output layer adds up, against which the logit's
+// error is measured (a logit that is a small difference of large terms has no
+// finer relative precision).
 double oracle_cnn_logit(const oracle_cnn_desc* d, const float* blob, const int64_t* S, int64_t den,
                         double* features_out, double* scale_out) {
   Net net;
   if (!load_net(d, blob, &net)) return std::numeric_limits<double>::quiet_NaN();
-  auto rnd = [&](double v) { return net.bf16 ? round_bf16(v) : v; };
+  auto rnd_input = [&](double v) { return net.bf16 ? round_bf16(v) : v; };
   int c = 3, h = net.in_h, w = net.in_w;
   // pre-processing [Sec. 7]: area average in [0, 255] mapped to [-1, 1]
   std::vector<double> act((size_t)c * h * w);
@@ -291,13 +291,13 @@ double oracle_cnn_logit(const oracle_cnn_desc* d, const float* blob, const int64
     for (int y = 0; y < h; ++y)
       for (int x = 0; x < w; ++x) {
         double v = (double)S[((size_t)y * w + x) * 3 + ch] / (double)den;
-        act[((size_t)ch * h + y) * w + x] = rnd(v / 127.5 - 1.0);
+        act[((size_t)ch * h + y) * w + x] = rnd_input(v / 127.5 - 1.0);
       }
   for (int l = 0; l < net.n_conv; ++l) {
     int co = net.cout[l];
     std::vector<double> out((size_t)co * h * w);
     oracle_conv3x3(act.data(), c, h, w, net.cw[l].data(), net.cb[l].data(), co, out.data());
-    for (double& v : out) v = rnd(v > 0.0 ? v : 0.0);
+    for (double& v : out) v = v > 0.0 ? v : 0.0;
     if (net.pool[l]) {
       int ph = h / 2, pw = w / 2;
       std::vector<double> pooled((size_t)co * ph * pw);
@@ -325,7 +325,7 @@ double oracle_cnn_logit(const oracle_cnn_desc* d, const float* blob, const int64
   for (int j = 0; j < net.dense; ++j) {
     double s = net.b1[j];
     for (int k = 0; k < net.flat; ++k) s += net.w1[(size_t)j * net.flat + k] * act[k];
-    double hj = rnd(s > 0.0 ? s : 0.0);
+    double hj = s > 0.0 ? s : 0.0;
     z += net.w2[j] * hj;
     scale += std::fabs(net.w2[j] * hj);
   }

@@ -230,16 +230,16 @@ def _torch_net_logit(spec, wts, S, den, bf16):
         return t.to(torch.float32).to(torch.bfloat16).to(torch.float64) if bf16 else t
 
     x = torch.from_numpy(S.astype(np.float64) / den).permute(2, 0, 1)[None] / 127.5 - 1.0
-    x = rnd(x)
+    x = rnd(x)  # a bf16 network rounds its input only
     for w, b, p in zip(wts["conv_w"], wts["conv_b"], spec.pool):
         x = F.conv2d(x, torch.from_numpy(w.astype(np.float64)), torch.from_numpy(b.astype(np.float64)),
                      padding=1)
-        x = rnd(F.relu(x))
+        x = F.relu(x)
         if p:
             x = F.max_pool2d(x, 2)
     f = x.flatten(1)
-    h = rnd(F.relu(f @ torch.from_numpy(wts["w1"].astype(np.float64)).T +
-                   torch.from_numpy(wts["b1"].astype(np.float64))))
+    h = F.relu(f @ torch.from_numpy(wts["w1"].astype(np.float64)).T +
+               torch.from_numpy(wts["b1"].astype(np.float64)))
     z = h @ torch.from_numpy(wts["w2"].astype(np.float64)) + float(wts["b2"][0])
     return float(z[0])
 
