@@ -24,7 +24,7 @@ int fail(int code, const char* fmt, ...) {
 }
 
 size_t conv_lds_bytes(const CnnLayer& L, bool bf16, int32_t* cin_lds, int32_t* w_lds,
-                      int32_t* band_w, int32_t* band_tiles);
+                      int32_t* band_w, int32_t* band_tiles, int32_t* seg_tiles);
 
 namespace {
 
@@ -130,7 +130,7 @@ int plan_cnn(const nsc_cnn_desc* d, Cnn* cnn) {
     L.b_off = boff;
     woff += (size_t)co * L.kpad;
     boff += co;
-    const size_t lds = conv_lds_bytes(L, bf16, nullptr, nullptr, nullptr, nullptr);
+    const size_t lds = conv_lds_bytes(L, bf16, nullptr, nullptr, nullptr, nullptr, nullptr);
     NSC_REQUIRE(lds <= kMaxLds, NSC_E_SHAPE,
                 "conv layer %d needs %zu bytes of LDS (limit %zu)", l, lds, kMaxLds);
     if (pool) {

@@ -3,8 +3,8 @@
 // Conv layers run as implicit GEMM on 16x16 MFMA tiles: M = 16 output pixels
 // of a 4x4 tile, N = 16 output channels, K = 9 taps x input channels.  The
 // 16 pixels are ordered so that each lane's four accumulator rows form one
-// 2x2 pooling window, so bias + ReLU + 2x2 max-pool + rounding happen in
-// registers in the epilogue.  A workgroup stages the layer's packed weights in
+// 2x2 pooling window, so bias + ReLU + 2x2 max-pool happen in registers in
+// the epilogue.  A workgroup stages the layer's packed weights in
 // LDS once and then loops over (image, tile-row) work items, staging the
 // input band (4 output rows + halo, zero padded) in LDS per item.  The first
 // layer's staging gathers the survivor's area sums, sums nested cells and
@@ -12,9 +12,17 @@
 // v_mfma_f32_16x16x32_bf16, fp32 layers v_mfma_f32_16x16x4_f32; both
 // accumulate in fp32.
 //
+// Activations between layers are fp32 in the workspace.  A bf16 network has
+// bf16 weights and a bf16-rounded input; each later activation a enters the
+// bf16 matrix cores as the pair hi = bf16(a), lo = bf16(a - hi) (the
+// difference is exact in fp32), multiplied by the same weights into a second
+// accumulator.  a is then carried to about 2^-17 of itself, so the result is a
+// continuous function of the fp32 accumulation error instead of flipping
+// bf16 roundings of intermediate values.
+//
 // The dense layer is a GEMM over 16-survivor tiles (M) x hidden units (N) x
 // features (K) on the same MFMA shapes; its epilogue adds the bias, applies
-// ReLU and rounding, folds the 1-unit output layer in with a 16-lane
+// ReLU, folds the 1-unit output layer in with a 16-lane
 // shuffle reduction, and writes the logit, the sigmoid confidence and the
 // c_low / c_high decision of each frame.
 #include "nsc_internal.h"
@@ -76,6 +84,35 @@ template <> struct Elt<uint16_t> {  // bf16 stored as raw bits
   static __device__ __forceinline__ void set(frag& f, int e, uint16_t v) {
     f[e] = __builtin_bit_cast(__bf16, v);
   }
+  // Activations enter as hi + lo pairs (see the top of this file).
+  static constexpr bool SPLIT = true;
+  static __device__ __forceinline__ void split1(float v, uint16_t& hi, uint16_t& lo) {
+    hi = f32_to_bf16_bits(v);
+    lo = f32_to_bf16_bits(v - bf16_bits_to_f32(hi));
+  }
+  // 4 fp32 values -> 4 hi and 4 lo bf16 values, packed pairwise in uint2
+  static __device__ __forceinline__ void split4(const float4& v, uint2& hi, uint2& lo) {
+    uint16_t h[4], l[4];
+    split1(v.x, h[0], l[0]);
+    split1(v.y, h[1], l[1]);
+    split1(v.z, h[2], l[2]);
+    split1(v.w, h[3], l[3]);
+    hi = make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+    lo = make_uint2((uint32_t)l[0] | ((uint32_t)l[1] << 16), (uint32_t)l[2] | ((uint32_t)l[3] << 16));
+  }
+  // A fragment pair from 8 consecutive fp32 values (16-byte aligned)
+  static __device__ __forceinline__ void split8(const float* p, frag& hi, frag& lo) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint16_t h, l;
+      split1(v[e], h, l);
+      set(hi, e, h);
+      set(lo, e, l);
+    }
+  }
 };
 template <> struct Elt<float> {
   static constexpr int E = 1, KS = 4;
@@ -90,6 +127,7 @@ template <> struct Elt<float> {
   static __device__ __forceinline__ float load8(const float* p) { return *p; }
   static __device__ __forceinline__ float zero() { return 0.0f; }
   static __device__ __forceinline__ void set(float& f, int, float v) { f = v; }
+  static constexpr bool SPLIT = false;
 };
 
 // ------------------------------------------------------------------- conv
@@ -100,8 +138,8 @@ struct ConvArgs {
   const int32_t* idx;
   int32_t sums_h, sums_w, fy, fx;
   int64_t den255;           // 255 * den_c: pre-processing x = (2 S - den255) / den255
-  const void* act_in;
-  void* act_out;
+  const float* act_in;      // [slot][h][w][cin] fp32
+  float* act_out;           // [slot][ho][wo][cout] fp32
   const void* wts;          // packed [cout][kpad]
   const float* bias;        // [cout]
   const int32_t* count;
@@ -110,9 +148,11 @@ struct ConvArgs {
   int32_t pool;
   int32_t tiles_y, tiles_x;
   int32_t band_tiles;       // tile rows per work item
+  int32_t seg_tiles;        // tile columns per work item
   int32_t cin_lds;          // channel stride of a staged pixel (elements)
   int32_t w_lds;            // row stride of staged weights (elements)
-  int32_t band_w;           // staged columns (halo and tail zero-filled)
+  int32_t band_w;           // staged columns of a segment (halo and tail zero-filled)
+  int32_t lo_plane;         // elements from a staged hi value to its lo value (split layers)
 };
 
 // Pixel (py, px) of M row m inside a 4x4 tile: m = 4 * window + j, the four
@@ -132,12 +172,11 @@ __device__ __forceinline__ void stage_weights(const ConvArgs& a, T* wl) {
   }
 }
 
-// Bias, ReLU, optional 2x2 max-pool, rounding, NHWC store of one 4x4 tile.
+// Bias, ReLU, optional 2x2 max-pool and fp32 NHWC store of one 4x4 tile.
 // Lane (m, g) holds rows 4g..4g+3 (one pooling window) of output channel m.
-template <typename T, int NT>
-__device__ __forceinline__ void conv_epilogue(const ConvArgs& a, const f32x4 (&acc)[NT], T* out,
+template <int NT>
+__device__ __forceinline__ void conv_epilogue(const ConvArgs& a, const f32x4 (&acc)[NT], float* out,
                                               int ty, int tx, int ho, int wo, int m, int g) {
-  using X = Elt<T>;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const int n = nt * 16 + m;
@@ -148,13 +187,13 @@ __device__ __forceinline__ void conv_epilogue(const ConvArgs& a, const f32x4 (&a
 #pragma unroll
       for (int r = 0; r < 4; ++r) v = fmaxf(v, acc[nt][r] + b);
       const int oy = 2 * ty + wy, ox = 2 * tx + wx;
-      if (oy < ho && ox < wo) out[((int64_t)oy * wo + ox) * a.cout + n] = X::from_f32(v);
+      if (oy < ho && ox < wo) out[((int64_t)oy * wo + ox) * a.cout + n] = v;
     } else {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int oy = 4 * ty + 2 * wy + (r >> 1), ox = 4 * tx + 2 * wx + (r & 1);
         if (oy < ho && ox < wo)
-          out[((int64_t)oy * wo + ox) * a.cout + n] = X::from_f32(fmaxf(acc[nt][r] + b, 0.0f));
+          out[((int64_t)oy * wo + ox) * a.cout + n] = fmaxf(acc[nt][r] + b, 0.0f);
       }
     }
   }
@@ -180,7 +219,8 @@ __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
   int64_t cnt = *a.count;
   if (cnt > a.max_count) cnt = a.max_count;
   const int bands = (a.tiles_y + a.band_tiles - 1) / a.band_tiles;
-  const int64_t items = cnt * bands;
+  const int segs = (a.tiles_x + a.seg_tiles - 1) / a.seg_tiles;
+  const int64_t items = cnt * bands * segs;
   const int band_w = a.band_w;
   const int ho = a.pool ? a.h / 2 : a.h, wo = a.pool ? a.w / 2 : a.w;
   const int m = lane & 15, g = lane >> 4;
@@ -188,10 +228,12 @@ __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
   tile_pixel(m, py, px);
 
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
-    const int64_t s = item / bands;
-    const int band = (int)(item - s * bands);
-    const int ty0 = band * a.band_tiles;
+    const int64_t s = item / (bands * segs);
+    const int bs = (int)(item - s * (bands * segs));
+    const int band = bs / segs, seg = bs - band * segs;
+    const int ty0 = band * a.band_tiles, tx0 = seg * a.seg_tiles;
     const int nty = min(a.band_tiles, a.tiles_y - ty0);
+    const int ntx = min(a.seg_tiles, a.tiles_x - tx0);
     const int rows = 4 * nty + 2;
     const int y_top = 4 * ty0 - 1;  // input row of band row 0
     __syncthreads();  // previous item's readers are done with `in` (and weights staged)
@@ -200,7 +242,7 @@ __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
       for (int e = tid; e < rows * band_w * 4; e += blockDim.x) {
         const int c = e & 3, pix = e >> 2;
         const int br = pix / band_w, bc = pix - br * band_w;
-        const int y = y_top + br, x = bc - 1;
+        const int y = y_top + br, x = 4 * tx0 + bc - 1;
         T v = X::from_f32(0.0f);
         if (c < 3 && y >= 0 && y < a.h && x >= 0 && x < a.w) {
           int64_t acc = 0;
@@ -215,13 +257,13 @@ __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
       }
     }
     __syncthreads();
-    T* out = reinterpret_cast<T*>(a.act_out) + s * (int64_t)ho * wo * a.cout;
-    for (int t = wave; t < nty * a.tiles_x; t += nwaves) {
-      const int tyl = t / a.tiles_x, tx = t - tyl * a.tiles_x;
+    float* out = a.act_out + s * (int64_t)ho * wo * a.cout;
+    for (int t = wave; t < nty * ntx; t += nwaves) {
+      const int tyl = t / ntx, txl = t - tyl * ntx;
       f32x4 acc[NT];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int row0 = 4 * tyl + py, col0 = 4 * tx + px;  // band coordinates of tap (0, 0)
+      const int row0 = 4 * tyl + py, col0 = 4 * txl + px;  // band coordinates of tap (0, 0)
 #pragma unroll
       for (int k0 = 0; k0 < 48; k0 += KS) {
         const int k = k0 + g * E;  // first K value of this lane group
@@ -236,16 +278,20 @@ __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
           acc[nt] = X::mma(av, bv, acc[nt]);
         }
       }
-      conv_epilogue<T, NT>(a, acc, out, ty0 + tyl, tx, ho, wo, m, g);
+      conv_epilogue<NT>(a, acc, out, ty0 + tyl, tx0 + txl, ho, wo, m, g);
     }
   }
 }
 
 // Inner layers (input channels a multiple of KS): K = 9 taps x cin, tap-major.
+// The fp32 input band is staged as fp32 (fp32 nets) or as hi and lo bf16
+// planes lo_plane elements apart (bf16 nets); the lo plane is multiplied by the
+// same weight fragments into a second set of accumulators.
 template <typename T, int NT>
 __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
   using X = Elt<T>;
   constexpr int E = X::E, KS = X::KS;
+  constexpr bool SPLIT = X::SPLIT;
   extern __shared__ __align__(16) unsigned char lds_raw[];
   T* wl = reinterpret_cast<T*>(lds_raw);
   T* in = wl + (size_t)a.cout * a.w_lds;
@@ -256,58 +302,78 @@ __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
   int64_t cnt = *a.count;
   if (cnt > a.max_count) cnt = a.max_count;
   const int bands = (a.tiles_y + a.band_tiles - 1) / a.band_tiles;
-  const int64_t items = cnt * bands;
+  const int segs = (a.tiles_x + a.seg_tiles - 1) / a.seg_tiles;
+  const int64_t items = cnt * bands * segs;
   const int band_w = a.band_w;
   const int ho = a.pool ? a.h / 2 : a.h, wo = a.pool ? a.w / 2 : a.w;
   const int m = lane & 15, g = lane >> 4;
   int py, px;
   tile_pixel(m, py, px);
-  constexpr int V = 16 / sizeof(T);  // elements per 16-byte vector
-  const int vec_per_pix = a.cin / V;
+  const int vec_per_pix = a.cin / 4;  // float4 vectors per input pixel
   const int chunks = a.cin / KS;
 
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
-    const int64_t s = item / bands;
-    const int band = (int)(item - s * bands);
-    const int ty0 = band * a.band_tiles;
+    const int64_t s = item / (bands * segs);
+    const int bs = (int)(item - s * (bands * segs));
+    const int band = bs / segs, seg = bs - band * segs;
+    const int ty0 = band * a.band_tiles, tx0 = seg * a.seg_tiles;
     const int nty = min(a.band_tiles, a.tiles_y - ty0);
+    const int ntx = min(a.seg_tiles, a.tiles_x - tx0);
     const int rows = 4 * nty + 2;
     const int y_top = 4 * ty0 - 1;
     __syncthreads();  // previous item's readers are done with `in` (and weights staged)
     {
-      const T* src = reinterpret_cast<const T*>(a.act_in) + s * (int64_t)a.h * a.w * a.cin;
+      const float* src = a.act_in + s * (int64_t)a.h * a.w * a.cin;
       for (int e = tid; e < rows * band_w * vec_per_pix; e += blockDim.x) {
         const int pix = e / vec_per_pix, cv = e - pix * vec_per_pix;
         const int br = pix / band_w, bc = pix - br * band_w;
-        const int y = y_top + br, x = bc - 1;
-        uint4 v = make_uint4(0, 0, 0, 0);
+        const int y = y_top + br, x = 4 * tx0 + bc - 1;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
         if (y >= 0 && y < a.h && x >= 0 && x < a.w)
-          v = *reinterpret_cast<const uint4*>(src + ((int64_t)y * a.w + x) * a.cin + cv * V);
-        *reinterpret_cast<uint4*>(in + pix * a.cin_lds + cv * V) = v;
+          v = *reinterpret_cast<const float4*>(src + ((int64_t)y * a.w + x) * a.cin + cv * 4);
+        T* dst = in + pix * a.cin_lds + cv * 4;
+        if constexpr (SPLIT) {
+          uint2 hi, lo;
+          X::split4(v, hi, lo);
+          *reinterpret_cast<uint2*>(dst) = hi;
+          *reinterpret_cast<uint2*>(dst + a.lo_plane) = lo;
+        } else {
+          *reinterpret_cast<float4*>(dst) = v;
+        }
       }
     }
     __syncthreads();
-    T* out = reinterpret_cast<T*>(a.act_out) + s * (int64_t)ho * wo * a.cout;
-    for (int t = wave; t < nty * a.tiles_x; t += nwaves) {
-      const int tyl = t / a.tiles_x, tx = t - tyl * a.tiles_x;
-      f32x4 acc[NT];
+    float* out = a.act_out + s * (int64_t)ho * wo * a.cout;
+    for (int t = wave; t < nty * ntx; t += nwaves) {
+      const int tyl = t / ntx, txl = t - tyl * ntx;
+      f32x4 acc[NT], acc_lo[NT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int row0 = 4 * tyl + py, col0 = 4 * tx + px;
+      for (int nt = 0; nt < NT; ++nt) {
+        acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        acc_lo[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+      const int row0 = 4 * tyl + py, col0 = 4 * txl + px;
       for (int tap = 0; tap < 9; ++tap) {
         const int dy = tap / 3, dx = tap - 3 * dy;
         const T* arow = in + ((row0 + dy) * band_w + col0 + dx) * a.cin_lds + g * E;
         const T* brow = wl + m * a.w_lds + tap * a.cin + g * E;
         for (int ch = 0; ch < chunks; ++ch) {
           const typename X::frag av = X::load(arow + ch * KS);
+          typename X::frag av_lo;
+          if constexpr (SPLIT) av_lo = X::load(arow + a.lo_plane + ch * KS);
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) {
             const typename X::frag bv = X::load(brow + nt * 16 * a.w_lds + ch * KS);
             acc[nt] = X::mma(av, bv, acc[nt]);
+            if constexpr (SPLIT) acc_lo[nt] = X::mma(av_lo, bv, acc_lo[nt]);
           }
         }
       }
-      conv_epilogue<T, NT>(a, acc, out, ty0 + tyl, tx, ho, wo, m, g);
+      if constexpr (SPLIT) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[nt] += acc_lo[nt];
+      }
+      conv_epilogue<NT>(a, acc, out, ty0 + tyl, tx0 + txl, ho, wo, m, g);
     }
   }
 }
@@ -315,7 +381,7 @@ __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
 // ------------------------------------------------------------------ dense
 
 struct DenseArgs {
-  const void* feat;         // [slot][flat] in (y, x, c) order
+  const float* feat;        // [slot][flat] fp32 in (y, x, c) order
   const void* w1;           // [D][flat]
   const float* b1;
   const float* w2;
@@ -335,6 +401,7 @@ template <typename T, int NT>
 __global__ void __launch_bounds__(256) k_dense(DenseArgs a) {
   using X = Elt<T>;
   constexpr int E = X::E, KS = X::KS;
+  constexpr bool SPLIT = X::SPLIT;
   const int lane = threadIdx.x & 63;
   const int m = lane & 15, g = lane >> 4;
   int64_t cnt = *a.count;
@@ -342,24 +409,36 @@ __global__ void __launch_bounds__(256) k_dense(DenseArgs a) {
   const int64_t groups = (cnt + 15) / 16;
   const int64_t wave_id = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
   const int64_t nwaves = (int64_t)gridDim.x * (blockDim.x >> 6);
-  const T* feat = reinterpret_cast<const T*>(a.feat);
   const T* w1 = reinterpret_cast<const T*>(a.w1);
   for (int64_t grp = wave_id; grp < groups; grp += nwaves) {
     const int64_t s = grp * 16 + m;
     const bool valid = s < cnt;
-    const T* arow = feat + (valid ? s : 0) * (int64_t)a.flat + g * E;
-    f32x4 acc[NT];
+    const float* arow = a.feat + (valid ? s : 0) * (int64_t)a.flat + g * E;
+    f32x4 acc[NT], acc_lo[NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nt = 0; nt < NT; ++nt) {
+      acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      acc_lo[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
     for (int k0 = 0; k0 < a.flat; k0 += KS) {
-      typename X::frag av = valid ? X::load(arow + k0) : X::zero();
+      typename X::frag av = X::zero(), av_lo = X::zero();
+      if constexpr (SPLIT) {
+        if (valid) X::split8(arow + k0, av, av_lo);
+      } else {
+        if (valid) av = arow[k0];
+      }
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         const typename X::frag bv = X::load(w1 + (int64_t)(nt * 16 + m) * a.flat + k0 + g * E);
         acc[nt] = X::mma(av, bv, acc[nt]);
+        if constexpr (SPLIT) acc_lo[nt] = X::mma(av_lo, bv, acc_lo[nt]);
       }
     }
-    // hidden = round(ReLU(acc + b1)); z = b2 + sum_n w2[n] * hidden[n]
+    if constexpr (SPLIT) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[nt] += acc_lo[nt];
+    }
+    // hidden = ReLU(acc + b1); z = b2 + sum_n w2[n] * hidden[n]
     float part[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -367,7 +446,7 @@ __global__ void __launch_bounds__(256) k_dense(DenseArgs a) {
       const float b = a.b1[n], w = a.w2[n];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float hval = X::to_f32(X::from_f32(fmaxf(acc[nt][r] + b, 0.0f)));
+        const float hval = fmaxf(acc[nt][r] + b, 0.0f);
         part[r] += w * hval;
       }
     }
@@ -453,11 +532,13 @@ void conv_tiles(const CnnLayer& L, int32_t* tiles_y, int32_t* tiles_x) {
 }
 
 // LDS of one conv layer's workgroup: staged weights plus an input band of
-// band_tiles tile rows (4 output rows each + 2 halo rows).  The band is as tall
-// as fits a budget of about 48 KB (the whole image when possible), at least
-// one tile row.
+// band_tiles tile rows (4 output rows each + 2 halo rows) by seg_tiles tile
+// columns (+ halo), in two planes (hi, lo) for the inner layers of a bf16
+// network.  A band spans the full width unless that does not fit 128 KB (then
+// the width is halved until it does); it is as tall as fits a budget of about
+// 48 KB (the whole image when possible), at least one tile row.
 size_t conv_lds_bytes(const CnnLayer& L, bool bf16, int32_t* cin_lds, int32_t* w_lds,
-                      int32_t* band_w, int32_t* band_tiles) {
+                      int32_t* band_w, int32_t* band_tiles, int32_t* seg_tiles) {
   const size_t es = bf16 ? 2 : 4;
   const int32_t vec = (int32_t)(16 / es);
   const bool first = L.cin == 3;
@@ -465,33 +546,39 @@ size_t conv_lds_bytes(const CnnLayer& L, bool bf16, int32_t* cin_lds, int32_t* w
   const int32_t wr = L.kpad + vec;                     // pad weight rows by 16 bytes
   int32_t ty, tx;
   conv_tiles(L, &ty, &tx);
-  const int32_t bw = 4 * tx + (first ? 3 : 2);         // first layer reads tap dx = 3 (weight 0)
+  const size_t planes = bf16 && !first ? 2 : 1;
   const size_t wbytes = (size_t)L.cout * wr * es;
-  const size_t row_bytes = (size_t)bw * cl * es;
+  // staged columns of st tile columns; the first layer also reads tap dx = 3 (weight 0)
+  auto cols = [&](int32_t st) { return 4 * st + (first ? 3 : 2); };
+  int32_t st = tx;
+  while (st > 1 && wbytes + (size_t)6 * cols(st) * cl * es * planes > 128 * 1024) st = (st + 1) / 2;
+  const int32_t bw = cols(st);
+  const size_t row_bytes = (size_t)bw * cl * es * planes;
   int32_t bt = 1;
   while (bt < ty && wbytes + (size_t)(4 * (bt + 1) + 2) * row_bytes <= 48 * 1024) ++bt;
   if (cin_lds) *cin_lds = cl;
   if (w_lds) *w_lds = wr;
   if (band_w) *band_w = bw;
   if (band_tiles) *band_tiles = bt;
+  if (seg_tiles) *seg_tiles = st;
   return wbytes + (size_t)(4 * bt + 2) * row_bytes;
 }
 
+// Two ping-pong buffers of fp32 activations per image.
 size_t cnn_workspace_bytes(const Cnn& cnn, int64_t max_count) {
-  const size_t es = cnn.bf16 ? 2 : 4;
-  const size_t per = align_up(cnn.act_elems * es, 256);
+  const size_t per = align_up(cnn.act_elems * sizeof(float), 256);
   return 2 * per * (size_t)(max_count > 0 ? max_count : 0) + 256;
 }
 
 int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (r.max_count <= 0) return NSC_OK;
-  const size_t es = cnn.bf16 ? 2 : 4;
-  const size_t per = align_up(cnn.act_elems * es, 256);
+  const size_t es = cnn.bf16 ? 2 : 4;  // weight element bytes
+  const size_t per = align_up(cnn.act_elems * sizeof(float), 256);
   if (ws_bytes < cnn_workspace_bytes(cnn, r.max_count))
     return fail(NSC_E_WORKSPACE, "CNN workspace of %zu bytes is below the %zu required", ws_bytes,
                 cnn_workspace_bytes(cnn, r.max_count));
-  unsigned char* buf[2] = {static_cast<unsigned char*>(ws),
-                           static_cast<unsigned char*>(ws) + per * (size_t)r.max_count};
+  float* buf[2] = {static_cast<float*>(ws),
+                   reinterpret_cast<float*>(static_cast<unsigned char*>(ws) + per * (size_t)r.max_count)};
   for (int l = 0; l < cnn.n_layers; ++l) {
     const CnnLayer& L = cnn.layers[l];
     ConvArgs a{};
@@ -516,11 +603,13 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
     a.pool = L.pool ? 1 : 0;
     conv_tiles(L, &a.tiles_y, &a.tiles_x);
     const size_t lds =
-        conv_lds_bytes(L, cnn.bf16, &a.cin_lds, &a.w_lds, &a.band_w, &a.band_tiles);
+        conv_lds_bytes(L, cnn.bf16, &a.cin_lds, &a.w_lds, &a.band_w, &a.band_tiles, &a.seg_tiles);
+    a.lo_plane = (4 * a.band_tiles + 2) * a.band_w * a.cin_lds;
     int per_cu = (int)((160 * 1024) / (lds + 1024));
     if (per_cu > 8) per_cu = 8;
     if (per_cu < 1) per_cu = 1;
-    int64_t items = r.max_count * ((a.tiles_y + a.band_tiles - 1) / a.band_tiles);
+    int64_t items = r.max_count * ((a.tiles_y + a.band_tiles - 1) / a.band_tiles) *
+                    ((a.tiles_x + a.seg_tiles - 1) / a.seg_tiles);
     int64_t grid = (int64_t)kNumCU * per_cu;
     if (grid > items) grid = items;
     if (grid < 1) grid = 1;

@@ -1,0 +1,192 @@
+"""Full-size runs of the workloads, checked on sampled frames against the oracle
+and on every frame against properties that hold at any size.
+
+The 100,000-frame 640x480 run uses the launch configuration bench.py times
+(one nsc_cascade_run over all frames resident in HBM).  Larger videos run in
+chunks through the carried state.  For sampled frames the oracle recomputes,
+from host-rendered frames t and t - delta, the detector score (bit-exact), the
+fire flag, and for fired frames the logit (relative to its scale) and the
+decision.  For every frame: frames t < delta fire; a frame that does not fire
+repeats the output of frame t - delta (or is "no object" with a fixed
+reference); logits exist exactly for fired frames; runs are deterministic.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from paper_1703_02529_amd.runner import CascadeRunner
+from synth import workloads as W
+
+from helpers import LOGIT_TOL, decision_excluded, logit_rel_err, lr_weights_for
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _oracle_frame(wl, v, blob, lr, ref_sums_o, t):
+    """Oracle score of frame t and, when it fires, its logit, scale and decision."""
+    den = oracle.area_den(wl.video.h, wl.video.w, wl.dd_h, wl.dd_w)
+    cur = oracle.area_sums(v.frame(t), wl.dd_h, wl.dd_w)
+    if wl.ref_mode == W.PREV:
+        if t < wl.delta:
+            score = math.inf
+        else:
+            ref = oracle.area_sums(v.frame(t - wl.delta), wl.dd_h, wl.dd_w)
+            score = (oracle.global_mse(cur, ref, den)[0] if wl.grid == (1, 1) else
+                     oracle.blocked_score(cur, ref, den, wl.grid, lr, wl.lr_bias)[0])
+    else:
+        score = (oracle.global_mse(cur, ref_sums_o, den)[0] if wl.grid == (1, 1) else
+                 oracle.blocked_score(cur, ref_sums_o, den, wl.grid, lr, wl.lr_bias)[0])
+    fires = score > wl.delta_diff or (wl.ref_mode == W.PREV and t < wl.delta)
+    out = dict(score=score, fire=fires)
+    if fires:
+        Sc = oracle.area_sums(v.frame(t), wl.cnn.in_h, wl.cnn.in_w)
+        den_c = oracle.area_den(wl.video.h, wl.video.w, wl.cnn.in_h, wl.cnn.in_w)
+        z, sc = oracle.cnn_logit(wl.cnn, blob, Sc, den_c, want_scale=True)
+        out.update(logit=z, scale=sc, dec=oracle.decide(oracle.sigmoid(z), wl.c_low, wl.c_high))
+    return out
+
+
+def _check_properties(wl, g, t0=0):
+    n = len(g["fire"])
+    t = np.arange(t0, t0 + n)
+    fire = g["fire"].astype(bool)
+    if wl.ref_mode == W.PREV:
+        assert fire[t < wl.delta].all()
+        assert np.isfinite(g["score"][t >= wl.delta]).all()
+        nf = np.flatnonzero(~fire)
+        nf = nf[nf >= wl.delta]
+        assert (g["label"][nf] == g["label"][nf - wl.delta]).all()
+        assert (g["defer"][nf] == g["defer"][nf - wl.delta]).all()
+    else:
+        assert ((g["label"][~fire] == 0) & (g["defer"][~fire] == 0)).all()
+    assert np.isnan(g["logit"][~fire]).all() and not np.isnan(g["logit"][fire]).any()
+    assert not (g["label"].astype(bool) & g["defer"].astype(bool)).any()
+
+
+def _check_samples(wl, v, blob, lr, ref_o, g, ts, t0=0):
+    tol = LOGIT_TOL[wl.cnn.bf16]
+    worst = 0.0
+    for t in ts:
+        o = _oracle_frame(wl, v, blob, lr, ref_o, int(t))
+        u = int(t) - t0
+        assert g["score"][u] == o["score"], (t, g["score"][u], o["score"])
+        assert bool(g["fire"][u]) == o["fire"], t
+        if o["fire"]:
+            err = float(logit_rel_err(np.array([g["logit"][u]]), np.array([o["logit"]]),
+                                      np.array([o["scale"]]))[0])
+            worst = max(worst, err)
+            assert err <= tol, (t, g["logit"][u], o["logit"], err)
+            if not decision_excluded(o["logit"], wl.c_low, wl.c_high, tol, o["scale"]):
+                dec = int(g["label"][u]) | (int(g["defer"][u]) << 1)
+                assert dec == o["dec"], (t, dec, o["dec"])
+    return worst
+
+
+def _thresholds_from_oracle(wl, v, blob, ts):
+    """c_low / c_high at the 30 % / 70 % quantiles of oracle confidences, so that
+    all three decisions occur."""
+    ps = []
+    den_c = oracle.area_den(wl.video.h, wl.video.w, wl.cnn.in_h, wl.cnn.in_w)
+    for t in ts:
+        Sc = oracle.area_sums(v.frame(int(t)), wl.cnn.in_h, wl.cnn.in_w)
+        ps.append(oracle.sigmoid(oracle.cnn_logit(wl.cnn, blob, Sc, den_c)))
+    lo, hi = np.quantile(ps, [0.3, 0.7])
+    return float(lo), float(hi)
+
+
+def _sample_times(v, t0, n, rng, k=12):
+    """Absolute frame indices in [t0, t0 + n): random ones, occupied ones, the ends."""
+    occ = np.flatnonzero(v.occupied[t0:t0 + n])
+    ts = set(rng.integers(0, n, k).tolist()) | {0, n - 1}
+    if occ.size:
+        ts |= set(rng.choice(occ, min(k, occ.size), replace=False).tolist())
+    return sorted(t0 + u for u in ts)
+
+
+def test_vga_100k_as_benchmarked():
+    wl = W.VGA
+    n, fb = wl.video.n, wl.video.frame_bytes
+    v = synth.Video(wl.video)
+    blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
+    rng = np.random.default_rng(7)
+    occ = np.flatnonzero(v.occupied)
+    lo, hi = _thresholds_from_oracle(wl, v, blob, rng.choice(occ, 24, replace=False))
+    frames = torch.empty(n * fb, dtype=torch.uint8, device=DEV)
+    v.render_device(frames, 0, n)
+    results = {}
+    for name, w in (("benchmark thresholds", wl), ("quantile thresholds", wl.replace(c_low=lo, c_high=hi))):
+        run = CascadeRunner(w, blob, max_frames=n)
+        outs = []
+        for rep in range(2):
+            st = run.run(frames, n, t0=0, want_stats=True)
+            outs.append({k: getattr(run, k)[:n].cpu().numpy().copy()
+                         for k in ("score", "fire", "logit", "label", "defer")})
+        run.close()
+        for k in outs[0]:
+            assert np.array_equal(np.nan_to_num(outs[0][k], nan=-7), np.nan_to_num(outs[1][k], nan=-7)), k
+        g = outs[0]
+        assert st["fired"] == int(g["fire"].sum())
+        _check_properties(w, g)
+        ts = _sample_times(v, 0, n, rng)
+        worst = _check_samples(w, v, blob, None, None, g, ts)
+        results[name] = dict(fired=int(g["fire"].sum()), positive=int(st["positive"]),
+                             deferred=int(st["deferred"]), samples=len(ts), worst_logit=worst)
+    print(results)
+    q = results["quantile thresholds"]
+    assert q["positive"] > 0 and q["deferred"] > 0 and q["positive"] + q["deferred"] < n
+    del frames
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("wl,chunk", [(W.HD_REF, 16384), (W.HD_BLOCKED, 16384)],
+                         ids=["hd-ref-100k", "hd-blocked-200k"])
+def test_hd_full_length_in_chunks(wl, chunk):
+    n, fb = wl.video.n, wl.video.frame_bytes
+    v = synth.Video(wl.video)
+    blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
+    lr = lr_weights_for(wl) if wl.grid != (1, 1) else None
+    ref_img = v.median_background() if wl.ref_mode == W.FIXED else None
+    ref_o = oracle.area_sums(ref_img, wl.dd_h, wl.dd_w) if ref_img is not None else None
+    ref_d = None
+    if ref_img is not None:
+        ref_d = torch.empty(wl.dd_h * wl.dd_w * 3, dtype=torch.int32, device=DEV)
+        import paper_1703_02529_amd as nsc
+        nsc.nsc_downsample(torch.from_numpy(ref_img.reshape(-1)).to(DEV), 1, wl.video.h,
+                           wl.video.w, wl.dd_h, wl.dd_w, ref_d)
+    run = CascadeRunner(wl, blob, max_frames=chunk,
+                        lr_w=torch.from_numpy(lr).to(DEV) if lr is not None else None,
+                        ref_sums=ref_d)
+    buf = torch.empty(chunk * fb, dtype=torch.uint8, device=DEV)
+    tables = v.device_tables(DEV)
+    rng = np.random.default_rng(11)
+    keys = ("score", "fire", "logit", "label", "defer")
+    prev_tail = None   # label/defer of the last delta frames of the previous chunk
+    worst, fired, checked = 0.0, 0, 0
+    for t0 in range(0, n, chunk):
+        m = min(chunk, n - t0)
+        v.render_device(buf, t0, m, tables)
+        run.run(buf, m, t0=t0)
+        g = {k: getattr(run, k)[:m].cpu().numpy().copy() for k in keys}
+        _check_properties(wl, g, t0)
+        if wl.ref_mode == W.PREV and prev_tail is not None:
+            # chains that cross the chunk boundary continue from the carried state
+            d = wl.delta
+            head = np.flatnonzero(g["fire"][:d] == 0)
+            assert (g["label"][head] == prev_tail[0][head]).all()
+            assert (g["defer"][head] == prev_tail[1][head]).all()
+        if wl.ref_mode == W.PREV:
+            prev_tail = (g["label"][-wl.delta:].copy(), g["defer"][-wl.delta:].copy())
+        fired += int(g["fire"].sum())
+        if t0 % (3 * chunk) == 0 or t0 + m == n:
+            ts = _sample_times(v, t0, m, rng, k=3)
+            worst = max(worst, _check_samples(wl, v, blob, lr, ref_o, g, ts, t0))
+            checked += len(ts)
+    run.close()
+    print(dict(frames=n, fired=fired, sampled=checked, worst_logit=worst))
+    del buf
+    torch.cuda.empty_cache()

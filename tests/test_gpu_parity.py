@@ -2,7 +2,7 @@
 
 Every input is seeded and synthetic; every expected value comes from the
 oracle on the host.  Integer and index outputs must match bit for bit; logits
-within the network's tolerance (1e-3 bf16, 1e-5 fp32, relative with a floor).
+within the network's tolerance (1e-3 bf16, 1e-5 fp32, relative to the logit's scale).
 """
 import math
 
@@ -207,6 +207,17 @@ def test_cnn_fp32_variants():
     _cnn_case(spec, n_frames=20, n_img=19)
     spec = synth.CNNSpec(in_h=9, in_w=21, conv=(32, 64), pool=(False, True), dense=64, bf16=True)
     _cnn_case(spec, n_frames=20, n_img=3)
+
+
+def test_cnn_column_segments():
+    # layers whose weights plus a full-width band exceed the LDS budget run in
+    # column segments (ragged last segment): bf16 64 -> 64 on a 120-wide map,
+    # and an fp32 64 -> 64 layer whose weights alone fill most of the LDS
+    spec = synth.CNNSpec(in_h=10, in_w=120, conv=(64, 64), pool=(False, True), dense=32, bf16=True)
+    _cnn_case(spec, n_frames=12, n_img=5)
+    spec = synth.CNNSpec(in_h=12, in_w=40, conv=(16, 64, 64), pool=(False, False, True), dense=16,
+                         bf16=False)
+    _cnn_case(spec, n_frames=12, n_img=5)
 
 
 def test_cnn_zero_count():
