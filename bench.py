@@ -23,6 +23,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+AREA_KERNEL = "k_area_sums_wave"
+AREA_SOURCES = ("paper_1703_02529_amd/csrc/area_diff.hip", "paper_1703_02529_amd/csrc/nsc_internal.h")
+COPY_BYTES = 1 << 31           # plain copy of known size for counter calibration
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 FP32_PEAK_TFLOPS = 157.3
 
@@ -62,6 +65,35 @@ class HipEvents:
     def destroy(self, evs):
         for e in evs:
             self.hip.hipEventDestroy(ctypes.c_void_p(e))
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the area kernel from the committed counter
+    summary, or None when there is none or the kernel's sources changed since."""
+    from paper_1703_02529_amd.profsum import sources_hash
+
+    path = os.path.join(ROOT, "profiles", f"traffic_{AREA_KERNEL}_{workload}.json")
+    if not os.path.exists(path):
+        return None, "no counter summary"
+    with open(path) as fh:
+        t = json.load(fh)
+    now = sources_hash([os.path.join(ROOT, p) for p in AREA_SOURCES])
+    if t.get("sources_sha256_16") != now:
+        return None, "kernel sources changed since the counters were taken"
+    return float(t["traffic_bytes"]), os.path.relpath(path, ROOT)
+
+
+def copy_calibration(torch, dev):
+    """A plain copy (negation) of COPY_BYTES bytes: the reference point that
+    scales the FETCH_SIZE / WRITE_SIZE counters of a profiled run."""
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
+    torch.cuda.empty_cache()
+    log(f"copy calibration: 2 x neg over {COPY_BYTES} bytes")
 
 
 def cnn_flops(spec) -> int:
@@ -108,6 +140,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="oracle time budget for the CPU baseline (0 disables it)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain copy of known size (for counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (the cascade's frames are independent across "
@@ -137,6 +171,9 @@ def main():
     del tables
     log("frames rendered on the device")
 
+    if args.calibrate_copy:
+        copy_calibration(torch, dev)
+
     blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
     run = CascadeRunner(wl, blob, max_frames=n, device=dev)
     stats = run.run(frames, n, t0=0, taps=False, want_stats=True)
@@ -162,6 +199,7 @@ def main():
     area_ms = float(stage[:, 0].mean())
     area_bytes = n * fb                       # algorithmic: every raw byte read once
     achieved = area_bytes / (area_ms * 1e-3) / 1e9
+    traffic, traffic_src = measured_traffic(wl.name)
     cnn_ms = float(stage[:, 3].mean())
     fired = int(stats["fired"])
     cnn_tflops = fired * cnn_flops(wl.cnn) / (cnn_ms * 1e-3) / 1e12 if cnn_ms > 0 else 0.0
@@ -194,12 +232,13 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_area_sums",
+            "kernel": AREA_KERNEL,
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": None,
+            "traffic": traffic,
+            "traffic_source": traffic_src,
             "bytes_per_launch": area_bytes,
             "avg_launch_ms": area_ms,
         },
