@@ -8,6 +8,14 @@ bf16) on the frames that fire; c_low = 0.2, c_high = 0.8.  One step is one
 nsc_cascade_run over all frames (downsample, detector, compaction, CNN,
 decisions and label resolution).
 
+With --workload fhd-stream it instead runs the 1,000,000-frame 1920x1080 video
+(detector 100x100, 10x10 blocked logistic score against frame t-30, 4-layer
+64-channel bf16 CNN) in chunks of 4096 through two frame buffers on two
+streams, the synthetic generator filling one buffer while the cascade reads the
+other.  Its `value` is the cascade-only rate (each chunk's cascade timed alone
+with HIP events, generator time excluded, as the paper excludes decoding); the
+overlapped wall-clock rate, bound by the generator, is reported beside it.
+
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
 from __future__ import annotations
@@ -133,21 +141,92 @@ def cpu_baseline(wl, budget_s: float) -> dict:
                       f"host has {os.cpu_count()} logical CPUs"}
 
 
+def bench_stream(args):
+    """The chunked 1080p million-frame run (see the module docstring)."""
+    import torch
+
+    import synth
+    from paper_1703_02529_amd.streaming import StreamingCascade
+    from synth import workloads as W
+
+    wl = W.FHD_STREAM
+    n, fb, chunk = wl.video.n, wl.video.frame_bytes, wl.chunk
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    v = synth.Video(wl.video)
+    tables = v.device_tables(dev)
+    blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
+    lr = synth.lr_weights(wl.grid[0] * wl.grid[1], wl.weight_seed, wl.lr_bias)[0]
+    sc = StreamingCascade(wl, blob, chunk, lr_w=torch.from_numpy(lr).to(dev), device=dev)
+    label = torch.empty(n, dtype=torch.uint8, device=dev)
+    defer = torch.empty(n, dtype=torch.uint8, device=dev)
+    fire = torch.empty(n, dtype=torch.uint8, device=dev)
+
+    def produce(buf, t0, m, stream):
+        v.render_device(buf, t0, m, tables, stream=stream)
+
+    log(f"workload {wl.name}: {n} frames x {fb} bytes in chunks of {chunk}")
+    for _ in range(args.warmup):
+        sc.run(2 * chunk, produce, label, defer, fire=fire)
+    torch.cuda.synchronize()
+    alone, over = [], []
+    for k in range(args.steps):
+        alone.append(sc.run(n, produce, label, defer, fire=fire, timing=True, overlap=False))
+        log(f"pass {k}: chunks run alone: {alone[-1]}")
+        over.append(sc.run(n, produce, label, defer, fire=fire, timing=True, overlap=True))
+        log(f"pass {k}: overlapped: {over[-1]}")
+    fired = int(fire.sum().item())
+    sc.close()
+    casc_ms = sum(a["cascade_ms"] for a in alone) / len(alone)
+    wall_ms = sum(o["wall_ms"] for o in over) / len(over)
+    result = {
+        "metric": "cascade frames/sec on 1 MI355X (chunked 1080p stream)",
+        "value": n / (casc_ms * 1e-3),
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": casc_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8 frames, i32/i64 detector, bf16 CNN (fp32 accumulate)",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "frames": n, "frame": f"{wl.video.w}x{wl.video.h} RGB u8",
+                   "chunk": chunk, "fired": fired},
+        "cascade_only_ms": casc_ms,
+        "overlapped_wall_ms": wall_ms,
+        "overlapped_wall_fps": n / (wall_ms * 1e-3),
+        "note": "value: each chunk's cascade timed alone with HIP events (generator excluded); "
+                "overlapped: generator filling the other buffer concurrently, wall clock",
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (20; fhd-stream: 1)")
+    ap.add_argument("--warmup", type=int, default=None, help="warm-up steps (3; fhd-stream: 1)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="oracle time budget for the CPU baseline (0 disables it)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain copy of known size (for counter calibration)")
+    ap.add_argument("--workload", choices=("vga", "fhd-stream"), default="vga")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (the cascade's frames are independent across "
               f"streams; see the design notes for how it would shard): got --gpus {args.gpus}",
               file=sys.stderr)
         sys.exit(2)
+    stream = args.workload == "fhd-stream"
+    if args.steps is None:
+        args.steps = 1 if stream else 20
+    if args.warmup is None:
+        args.warmup = 1 if stream else 3
+    if stream:
+        bench_stream(args)
+        return
 
     import numpy as np
     import torch

@@ -22,66 +22,103 @@ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
   return z ^ (z >> 31);
 }
 
-// One thread renders 16 consecutive bytes of the [n][H][W][3] chunk.
-__global__ void __launch_bounds__(256) render16(uint8_t* __restrict__ out, int64_t t0,
-                                                int64_t total_bytes, int32_t H, int32_t W,
-                                                uint64_t key, const uint8_t* __restrict__ bg,
-                                                const int16_t* __restrict__ noise,
-                                                const int8_t* __restrict__ drift,
-                                                const int32_t* __restrict__ rects, int32_t K) {
-  const int64_t frame_bytes = (int64_t)H * W * 3;
-  for (int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; chunk * 16 < total_bytes;
-       chunk += (int64_t)gridDim.x * blockDim.x) {
-    int64_t b = chunk * 16;
-    int64_t lt = b / frame_bytes;
-    int64_t rem = b - lt * frame_bytes;
-    int64_t pix_in_frame = rem / 3;
-    int c = (int)(rem - pix_in_frame * 3);
-    int y = (int)(pix_in_frame / W);
-    int x = (int)(pix_in_frame - (int64_t)y * W);
-    int64_t t = t0 + lt;
-    uint8_t vals[16];
-    uint64_t h = 0;
-    bool have_h = false;
-    for (int k = 0; k < 16; ++k) {
-      if (b + k >= total_bytes) {
-        vals[k] = 0;
-        continue;
+constexpr int kNoiseEntries = 65536;
+constexpr int kMaxRects = 32;
+
+// One workgroup per CU holds the 128 KB noise table in LDS (the per-byte
+// lookups are random, so from L2 they would bound the rate) and loops over work
+// items: a frame, or a segment of a frame's 16-byte chunks when there are few
+// frames.  One thread renders 16 consecutive bytes of one frame; the pixel's
+// hash, colour and rectangle cover are computed once per pixel (3 bytes).
+// Frame-uniform values (the rectangle table row, the drift) are read once per
+// item; the rectangle row goes to LDS, and each thread keeps a bit mask of the
+// rectangles that cover its row so that a pixel tests only those.
+__global__ void __launch_bounds__(1024) render_frames(uint8_t* __restrict__ out, int64_t t0,
+                                                      int64_t n, int32_t segs, int32_t H, int32_t W,
+                                                      uint64_t key, const uint8_t* __restrict__ bg,
+                                                      const int16_t* __restrict__ noise,
+                                                      const int8_t* __restrict__ drift,
+                                                      const int32_t* __restrict__ rects, int32_t K) {
+  extern __shared__ __align__(16) int16_t tab[];
+  __shared__ int32_t rt[kMaxRects * kRectFields];
+  for (int i = threadIdx.x; i < kNoiseEntries / 8; i += blockDim.x)
+    reinterpret_cast<uint4*>(tab)[i] = reinterpret_cast<const uint4*>(noise)[i];
+  __syncthreads();
+  const int32_t fb = H * W * 3;
+  const int32_t chunks = (fb + 15) / 16;
+  const int32_t per_seg = (chunks + segs - 1) / segs;
+  const bool aligned = (fb & 15) == 0;
+  for (int64_t item = blockIdx.x; item < n * segs; item += gridDim.x) {
+    const int64_t f = item / segs;
+    const int32_t seg = (int32_t)(item - f * segs);
+    const int64_t t = t0 + f;
+    const int32_t* R = rects + t * K * kRectFields;
+    __syncthreads();  // the previous item's readers of rt are done
+    for (int i = threadIdx.x; i < K * kRectFields; i += blockDim.x) rt[i] = R[i];
+    __syncthreads();
+    const int dr = drift[t];
+    auto row_mask = [&](int yy) {
+      uint32_t m = 0;
+      for (int j = 0; j < K; ++j) {
+        const int32_t* r = rt + j * kRectFields;
+        if (r[7] && yy >= r[1] && yy < r[3]) m |= 1u << j;
       }
-      if (!have_h) {
-        uint64_t pix = ((uint64_t)t * (uint64_t)H + (uint64_t)y) * (uint64_t)W + (uint64_t)x;
-        h = mix64(key + (pix + 1ull) * kGolden);
-        have_h = true;
-      }
-      int base = bg[((int64_t)y * W + x) * 3 + c];
-      const int32_t* r = rects + (t * K) * kRectFields;
-      for (int j = 0; j < K; ++j, r += kRectFields) {
-        if (r[7] && x >= r[0] && x < r[2] && y >= r[1] && y < r[3]) base = r[4 + c];
-      }
-      int v = base + (int)drift[t] + (int)noise[(h >> (16 * c)) & 0xFFFFull];
-      vals[k] = (uint8_t)(v < 0 ? 0 : (v > 255 ? 255 : v));
-      // advance to the next byte
-      if (++c == 3) {
-        c = 0;
-        have_h = false;
-        if (++x == W) {
-          x = 0;
-          if (++y == H) {
-            y = 0;
-            ++t;
+      return m;
+    };
+    uint8_t* fo = out + f * (int64_t)fb;
+    const int32_t c1 = min(chunks, (seg + 1) * per_seg);
+    for (int32_t ch = seg * per_seg + threadIdx.x; ch < c1; ch += blockDim.x) {
+      const int32_t b = ch * 16;
+      int32_t pix = b / 3;
+      int c = b - pix * 3;
+      int y = pix / W;
+      int x = pix - y * W;
+      uint8_t vals[16];
+      int base[3] = {0, 0, 0};
+      uint64_t h = 0;
+      uint32_t rows = row_mask(y);
+      for (int k = 0; k < 16; ++k) {
+        if (b + k >= fb) {
+          vals[k] = 0;
+          continue;
+        }
+        if (k == 0 || c == 0) {  // entering a pixel
+          const uint64_t gp = ((uint64_t)t * (uint64_t)H + (uint64_t)y) * (uint64_t)W + (uint64_t)x;
+          h = mix64(key + (gp + 1ull) * kGolden);
+          const uint8_t* bp = bg + ((int64_t)y * W + x) * 3;
+          base[0] = bp[0];
+          base[1] = bp[1];
+          base[2] = bp[2];
+          for (uint32_t mm = rows; mm; mm &= mm - 1) {  // ascending: the last cover wins
+            const int32_t* r = rt + (__builtin_ctz(mm)) * kRectFields;
+            if (x >= r[0] && x < r[2]) {
+              base[0] = r[4];
+              base[1] = r[5];
+              base[2] = r[6];
+            }
+          }
+        }
+        const int v = base[c] + dr + (int)tab[(h >> (16 * c)) & 0xFFFFull];
+        vals[k] = (uint8_t)(v < 0 ? 0 : (v > 255 ? 255 : v));
+        if (++c == 3) {
+          c = 0;
+          if (++x == W) {
+            x = 0;
+            ++y;
+            if (y < H) rows = row_mask(y);
           }
         }
       }
-    }
-    if (b + 16 <= total_bytes) {
-      uint4 v;
-      v.x = vals[0] | (vals[1] << 8) | (vals[2] << 16) | ((uint32_t)vals[3] << 24);
-      v.y = vals[4] | (vals[5] << 8) | (vals[6] << 16) | ((uint32_t)vals[7] << 24);
-      v.z = vals[8] | (vals[9] << 8) | (vals[10] << 16) | ((uint32_t)vals[11] << 24);
-      v.w = vals[12] | (vals[13] << 8) | (vals[14] << 16) | ((uint32_t)vals[15] << 24);
-      *reinterpret_cast<uint4*>(out + b) = v;
-    } else {
-      for (int k = 0; b + k < total_bytes; ++k) out[b + k] = vals[k];
+      if (aligned && b + 16 <= fb) {
+        uint4 v;
+        v.x = vals[0] | (vals[1] << 8) | (vals[2] << 16) | ((uint32_t)vals[3] << 24);
+        v.y = vals[4] | (vals[5] << 8) | (vals[6] << 16) | ((uint32_t)vals[7] << 24);
+        v.z = vals[8] | (vals[9] << 8) | (vals[10] << 16) | ((uint32_t)vals[11] << 24);
+        v.w = vals[12] | (vals[13] << 8) | (vals[14] << 16) | ((uint32_t)vals[15] << 24);
+        *reinterpret_cast<uint4*>(fo + b) = v;
+      } else {
+        for (int k = 0; k < 16 && b + k < fb; ++k) fo[b + k] = vals[k];
+      }
     }
   }
 }
@@ -89,20 +126,26 @@ __global__ void __launch_bounds__(256) render16(uint8_t* __restrict__ out, int64
 }  // namespace
 
 // Renders frames [t0, t0 + n) of the video into `out` (device, n*H*W*3 bytes,
-// 16-byte aligned).  Tables are device pointers: bg [H][W][3] uint8, noise
-// [65536] int16, drift [n_total] int8, rects [n_total][K][8] int32.
+// 16-byte aligned; frames of a size that is not a multiple of 16 bytes are
+// written byte by byte).  Tables are device pointers: bg [H][W][3] uint8, noise
+// [65536] int16, drift [n_total] int8, rects [n_total][K][8] int32 with K <= 32.
 // Returns 0 or the HIP error code of the launch.
 extern "C" int synth_render(void* out, int64_t t0, int64_t n, int32_t H, int32_t W, uint64_t key,
                             const void* bg, const void* noise, const void* drift,
                             const void* rects, int32_t K, void* stream) {
   if (n <= 0) return 0;
   if (((uintptr_t)out & 15) != 0) return (int)hipErrorInvalidValue;
-  int64_t total = n * (int64_t)H * W * 3;
-  int64_t chunks = (total + 15) / 16;
-  int64_t blocks = (chunks + 255) / 256;
-  if (blocks > 65536 * 8) blocks = 65536 * 8;
-  hipLaunchKernelGGL(render16, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
-                     (uint8_t*)out, t0, total, H, W, key, (const uint8_t*)bg,
-                     (const int16_t*)noise, (const int8_t*)drift, (const int32_t*)rects, K);
+  if ((int64_t)H * W * 3 > 0x7FFFFFF0 || K < 0 || K > kMaxRects) return (int)hipErrorInvalidValue;
+  const int64_t chunks = ((int64_t)H * W * 3 + 15) / 16;
+  // enough work items for 4 per workgroup, segments of at least 1024 chunks
+  constexpr int64_t kBlocks = 256;
+  int64_t segs = (4 * kBlocks + n - 1) / n;
+  const int64_t max_segs = (chunks + 1023) / 1024;
+  if (segs > max_segs) segs = max_segs;
+  if (segs < 1) segs = 1;
+  hipLaunchKernelGGL(render_frames, dim3((unsigned)kBlocks), dim3(1024),
+                     kNoiseEntries * sizeof(int16_t), (hipStream_t)stream, (uint8_t*)out, t0, n,
+                     (int32_t)segs, H, W, key, (const uint8_t*)bg, (const int16_t*)noise,
+                     (const int8_t*)drift, (const int32_t*)rects, K);
   return (int)hipGetLastError();
 }

@@ -7,6 +7,7 @@ import numpy as np
 
 import oracle
 import synth
+from synth import workloads as W
 
 LOGIT_TOL = {True: 1e-3, False: 1e-5}   # bf16 / fp32 networks: max relative logit error
 
@@ -74,3 +75,65 @@ def compare_cascade(wl, gpu: dict, ref: dict, t0: int = 0, state_excluded=None):
                 max_logit_rel=float(rel.max()) if rel.size else 0.0,
                 near_delta=int(np.sum(np.abs(ref["score"] - wl.delta_diff) <=
                                       1e-5 * max(abs(wl.delta_diff), 1.0))))
+
+
+# ------------------------------------------- sampled frames of long runs
+
+def oracle_frame(wl, v, blob, lr, ref_sums_o, t):
+    """Oracle score of frame t and, when it fires, its logit, scale and decision."""
+    den = oracle.area_den(wl.video.h, wl.video.w, wl.dd_h, wl.dd_w)
+    cur = oracle.area_sums(v.frame(t), wl.dd_h, wl.dd_w)
+    if wl.ref_mode == W.PREV:
+        if t < wl.delta:
+            score = math.inf
+        else:
+            ref = oracle.area_sums(v.frame(t - wl.delta), wl.dd_h, wl.dd_w)
+            score = (oracle.global_mse(cur, ref, den)[0] if wl.grid == (1, 1) else
+                     oracle.blocked_score(cur, ref, den, wl.grid, lr, wl.lr_bias)[0])
+    else:
+        score = (oracle.global_mse(cur, ref_sums_o, den)[0] if wl.grid == (1, 1) else
+                 oracle.blocked_score(cur, ref_sums_o, den, wl.grid, lr, wl.lr_bias)[0])
+    fires = score > wl.delta_diff or (wl.ref_mode == W.PREV and t < wl.delta)
+    out = dict(score=score, fire=fires)
+    if fires:
+        Sc = oracle.area_sums(v.frame(t), wl.cnn.in_h, wl.cnn.in_w)
+        den_c = oracle.area_den(wl.video.h, wl.video.w, wl.cnn.in_h, wl.cnn.in_w)
+        z, sc = oracle.cnn_logit(wl.cnn, blob, Sc, den_c, want_scale=True)
+        out.update(logit=z, scale=sc, dec=oracle.decide(oracle.sigmoid(z), wl.c_low, wl.c_high))
+    return out
+
+
+def check_properties(wl, g, t0=0):
+    n = len(g["fire"])
+    t = np.arange(t0, t0 + n)
+    fire = g["fire"].astype(bool)
+    if wl.ref_mode == W.PREV:
+        assert fire[t < wl.delta].all()
+        assert np.isfinite(g["score"][t >= wl.delta]).all()
+        nf = np.flatnonzero(~fire)
+        nf = nf[nf >= wl.delta]
+        assert (g["label"][nf] == g["label"][nf - wl.delta]).all()
+        assert (g["defer"][nf] == g["defer"][nf - wl.delta]).all()
+    else:
+        assert ((g["label"][~fire] == 0) & (g["defer"][~fire] == 0)).all()
+    assert np.isnan(g["logit"][~fire]).all() and not np.isnan(g["logit"][fire]).any()
+    assert not (g["label"].astype(bool) & g["defer"].astype(bool)).any()
+
+
+def check_samples(wl, v, blob, lr, ref_o, g, ts, t0=0):
+    tol = LOGIT_TOL[wl.cnn.bf16]
+    worst = 0.0
+    for t in ts:
+        o = oracle_frame(wl, v, blob, lr, ref_o, int(t))
+        u = int(t) - t0
+        assert g["score"][u] == o["score"], (t, g["score"][u], o["score"])
+        assert bool(g["fire"][u]) == o["fire"], t
+        if o["fire"]:
+            err = float(logit_rel_err(np.array([g["logit"][u]]), np.array([o["logit"]]),
+                                      np.array([o["scale"]]))[0])
+            worst = max(worst, err)
+            assert err <= tol, (t, g["logit"][u], o["logit"], err)
+            if not decision_excluded(o["logit"], wl.c_low, wl.c_high, tol, o["scale"]):
+                dec = int(g["label"][u]) | (int(g["defer"][u]) << 1)
+                assert dec == o["dec"], (t, dec, o["dec"])
+    return worst

@@ -10,8 +10,6 @@ decision.  For every frame: frames t < delta fire; a frame that does not fire
 repeats the output of frame t - delta (or is "no object" with a fixed
 reference); logits exist exactly for fired frames; runs are deterministic.
 """
-import math
-
 import numpy as np
 import pytest
 import torch
@@ -19,72 +17,13 @@ import torch
 import oracle
 import synth
 from paper_1703_02529_amd.runner import CascadeRunner
+from paper_1703_02529_amd.streaming import StreamingCascade
 from synth import workloads as W
 
-from helpers import LOGIT_TOL, decision_excluded, logit_rel_err, lr_weights_for
+from helpers import check_properties, check_samples, lr_weights_for
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
-
-
-def _oracle_frame(wl, v, blob, lr, ref_sums_o, t):
-    """Oracle score of frame t and, when it fires, its logit, scale and decision."""
-    den = oracle.area_den(wl.video.h, wl.video.w, wl.dd_h, wl.dd_w)
-    cur = oracle.area_sums(v.frame(t), wl.dd_h, wl.dd_w)
-    if wl.ref_mode == W.PREV:
-        if t < wl.delta:
-            score = math.inf
-        else:
-            ref = oracle.area_sums(v.frame(t - wl.delta), wl.dd_h, wl.dd_w)
-            score = (oracle.global_mse(cur, ref, den)[0] if wl.grid == (1, 1) else
-                     oracle.blocked_score(cur, ref, den, wl.grid, lr, wl.lr_bias)[0])
-    else:
-        score = (oracle.global_mse(cur, ref_sums_o, den)[0] if wl.grid == (1, 1) else
-                 oracle.blocked_score(cur, ref_sums_o, den, wl.grid, lr, wl.lr_bias)[0])
-    fires = score > wl.delta_diff or (wl.ref_mode == W.PREV and t < wl.delta)
-    out = dict(score=score, fire=fires)
-    if fires:
-        Sc = oracle.area_sums(v.frame(t), wl.cnn.in_h, wl.cnn.in_w)
-        den_c = oracle.area_den(wl.video.h, wl.video.w, wl.cnn.in_h, wl.cnn.in_w)
-        z, sc = oracle.cnn_logit(wl.cnn, blob, Sc, den_c, want_scale=True)
-        out.update(logit=z, scale=sc, dec=oracle.decide(oracle.sigmoid(z), wl.c_low, wl.c_high))
-    return out
-
-
-def _check_properties(wl, g, t0=0):
-    n = len(g["fire"])
-    t = np.arange(t0, t0 + n)
-    fire = g["fire"].astype(bool)
-    if wl.ref_mode == W.PREV:
-        assert fire[t < wl.delta].all()
-        assert np.isfinite(g["score"][t >= wl.delta]).all()
-        nf = np.flatnonzero(~fire)
-        nf = nf[nf >= wl.delta]
-        assert (g["label"][nf] == g["label"][nf - wl.delta]).all()
-        assert (g["defer"][nf] == g["defer"][nf - wl.delta]).all()
-    else:
-        assert ((g["label"][~fire] == 0) & (g["defer"][~fire] == 0)).all()
-    assert np.isnan(g["logit"][~fire]).all() and not np.isnan(g["logit"][fire]).any()
-    assert not (g["label"].astype(bool) & g["defer"].astype(bool)).any()
-
-
-def _check_samples(wl, v, blob, lr, ref_o, g, ts, t0=0):
-    tol = LOGIT_TOL[wl.cnn.bf16]
-    worst = 0.0
-    for t in ts:
-        o = _oracle_frame(wl, v, blob, lr, ref_o, int(t))
-        u = int(t) - t0
-        assert g["score"][u] == o["score"], (t, g["score"][u], o["score"])
-        assert bool(g["fire"][u]) == o["fire"], t
-        if o["fire"]:
-            err = float(logit_rel_err(np.array([g["logit"][u]]), np.array([o["logit"]]),
-                                      np.array([o["scale"]]))[0])
-            worst = max(worst, err)
-            assert err <= tol, (t, g["logit"][u], o["logit"], err)
-            if not decision_excluded(o["logit"], wl.c_low, wl.c_high, tol, o["scale"]):
-                dec = int(g["label"][u]) | (int(g["defer"][u]) << 1)
-                assert dec == o["dec"], (t, dec, o["dec"])
-    return worst
 
 
 def _thresholds_from_oracle(wl, v, blob, ts):
@@ -131,9 +70,9 @@ def test_vga_100k_as_benchmarked():
             assert np.array_equal(np.nan_to_num(outs[0][k], nan=-7), np.nan_to_num(outs[1][k], nan=-7)), k
         g = outs[0]
         assert st["fired"] == int(g["fire"].sum())
-        _check_properties(w, g)
+        check_properties(w, g)
         ts = _sample_times(v, 0, n, rng)
-        worst = _check_samples(w, v, blob, None, None, g, ts)
+        worst = check_samples(w, v, blob, None, None, g, ts)
         results[name] = dict(fired=int(g["fire"].sum()), positive=int(st["positive"]),
                              deferred=int(st["deferred"]), samples=len(ts), worst_logit=worst)
     print(results)
@@ -172,7 +111,7 @@ def test_hd_full_length_in_chunks(wl, chunk):
         v.render_device(buf, t0, m, tables)
         run.run(buf, m, t0=t0)
         g = {k: getattr(run, k)[:m].cpu().numpy().copy() for k in keys}
-        _check_properties(wl, g, t0)
+        check_properties(wl, g, t0)
         if wl.ref_mode == W.PREV and prev_tail is not None:
             # chains that cross the chunk boundary continue from the carried state
             d = wl.delta
@@ -184,9 +123,45 @@ def test_hd_full_length_in_chunks(wl, chunk):
         fired += int(g["fire"].sum())
         if t0 % (3 * chunk) == 0 or t0 + m == n:
             ts = _sample_times(v, t0, m, rng, k=3)
-            worst = max(worst, _check_samples(wl, v, blob, lr, ref_o, g, ts, t0))
+            worst = max(worst, check_samples(wl, v, blob, lr, ref_o, g, ts, t0))
             checked += len(ts)
     run.close()
     print(dict(frames=n, fired=fired, sampled=checked, worst_logit=worst))
     del buf
+    torch.cuda.empty_cache()
+
+
+def test_fhd_1m_streamed():
+    """The million-frame 1080p video in chunks of 4096 through two frame buffers
+    on two streams (the generator fills one while the cascade reads the other)."""
+    wl = W.FHD_STREAM
+    n = wl.video.n
+    v = synth.Video(wl.video)
+    blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
+    lr = lr_weights_for(wl)
+    tables = v.device_tables(DEV)
+    sc = StreamingCascade(wl, blob, wl.chunk, lr_w=torch.from_numpy(lr).to(DEV))
+    out = dict(label=torch.empty(n, dtype=torch.uint8, device=DEV),
+               defer=torch.empty(n, dtype=torch.uint8, device=DEV),
+               score=torch.empty(n, dtype=torch.float64, device=DEV),
+               fire=torch.empty(n, dtype=torch.uint8, device=DEV),
+               logit=torch.empty(n, dtype=torch.float32, device=DEV))
+
+    def produce(buf, t0, m, stream):
+        v.render_device(buf, t0, m, tables, stream=stream)
+
+    st = sc.run(n, produce, timing=True, **out)
+    sc.close()
+    g = {k: t.cpu().numpy() for k, t in out.items()}
+    check_properties(wl, g)
+    rng = np.random.default_rng(5)
+    # frames at chunk boundaries (their reference frame t - 30 lies in the previous chunk)
+    # and random / occupied ones
+    ts = sorted(set(_sample_times(v, 0, n, rng, k=5)) |
+                {wl.chunk, wl.chunk + wl.delta - 1, 100 * wl.chunk + 7, n - 1})
+    worst = check_samples(wl, v, blob, lr, None, g, ts)
+    print(dict(frames=n, chunks=st["chunks"], fired=int(g["fire"].sum()),
+               cascade_ms=round(st["cascade_ms"], 1), wall_ms=round(st["wall_ms"], 1),
+               sampled=len(ts), worst_logit=worst))
+    del out
     torch.cuda.empty_cache()

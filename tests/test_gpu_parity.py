@@ -14,9 +14,11 @@ import oracle
 import paper_1703_02529_amd as nsc
 import synth
 from paper_1703_02529_amd.runner import CascadeRunner
+from paper_1703_02529_amd.streaming import StreamingCascade
 from synth import workloads as W
 
-from helpers import LOGIT_TOL, compare_cascade, logit_rel_err, lr_weights_for
+from helpers import (LOGIT_TOL, check_properties, check_samples, compare_cascade,
+                     logit_rel_err, lr_weights_for)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -44,6 +46,15 @@ def test_device_renderer_matches_host(wl):
     t0 = min(t0, wl.video.n - 3)
     d = _render(v, t0, 3).cpu().numpy().reshape(3, wl.video.h, wl.video.w, 3)
     assert np.array_equal(d, v.frames(t0, t0 + 3))
+
+
+def test_device_renderer_odd_frame_size():
+    # 33 x 17 x 3 = 1683 bytes per frame: frames start off 16-byte boundaries
+    spec = synth.VideoSpec(n=600, h=33, w=17, seed=3, obj_min=4, obj_max=12, occupancy=0.6, vmax=3)
+    v = synth.Video(spec)
+    t0 = int(np.flatnonzero(v.occupied)[0])
+    d = _render(v, t0, 7).cpu().numpy().reshape(7, 33, 17, 3)
+    assert np.array_equal(d, v.frames(t0, t0 + 7))
 
 
 # ------------------------------------------------------------- downsample
@@ -399,3 +410,37 @@ def test_state_required_and_workspace_checks():
         nsc.nsc_cascade_run(run.cfg, run.cnn, d, 8, 0, None, run.ws, run.label, run.defer)
     assert e.value.status == -7
     run.close()
+
+
+# --------------------------------------------------------------- streaming
+
+def test_streamed_chunks_equal_one_shot():
+    """Two frame buffers on two streams, ragged last chunk, reference frame
+    t - 30 across chunk boundaries: every output equals a one-shot run."""
+    wl = W.FHD_STREAM.with_frames(3 * 512 + 77)
+    n, fb, chunk = wl.video.n, wl.video.frame_bytes, 512
+    v, blob, lr, _ = _prepare(wl, 0, n)
+    lr_d = _dev(lr)
+    tables = v.device_tables(DEV)
+    frames = torch.empty(n * fb, dtype=torch.uint8, device=DEV)
+    v.render_device(frames, 0, n, tables)
+    one = CascadeRunner(wl, blob, max_frames=n, lr_w=lr_d)
+    one.run(frames, n, t0=0)
+    keys = ("score", "fire", "logit", "label", "defer")
+    ref = {k: getattr(one, k)[:n].cpu().numpy().copy() for k in keys}
+    one.close()
+    del frames
+    out = {k: torch.full((n,), 77, dtype=getattr(one, k).dtype, device=DEV) for k in keys}
+    sc = StreamingCascade(wl, blob, chunk, lr_w=lr_d)
+    st = sc.run(n, lambda buf, t0, m, s: v.render_device(buf, t0, m, tables, stream=s),
+                timing=True, **out)
+    sc.close()
+    assert st["chunks"] == 4
+    g = {k: out[k].cpu().numpy() for k in keys}
+    for k in keys:
+        assert np.array_equal(np.nan_to_num(g[k], nan=-7), np.nan_to_num(ref[k], nan=-7)), k
+    check_properties(wl, g)
+    # oracle on frames around the chunk boundaries
+    ts = [0, 29, 30, 511, 512, 541, 1024 + 13, n - 1]
+    check_samples(wl, v, blob, lr, None, g, ts)
+    torch.cuda.empty_cache()
