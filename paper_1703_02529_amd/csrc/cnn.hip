@@ -33,6 +33,7 @@ namespace nsc {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------- numerics
@@ -53,6 +54,23 @@ __device__ __forceinline__ uint16_t f64_to_bf16_bits(double d) {
   u += 0x0FFFFFFFFFFFull + ((u >> 45) & 1ull);
   u &= ~0x1FFFFFFFFFFFull;
   return (uint16_t)(__float_as_uint((float)__longlong_as_double((long long)u)) >> 16);
+}
+
+// bf16 (nearest, ties to even) of the exact quotient N / D for 0 < D < 2^24,
+// |N| <= D.  Both are exact in fp32 and the fp32 division is correctly
+// rounded, so rounding its result to bf16 can only differ from rounding the
+// exact quotient when the fp32 result is itself a bf16 midpoint m; then the
+// side of m the quotient lies on (N - m D, exact in fp64 as m has 9
+// significant bits) decides, and an exact tie stays a tie.
+__device__ __forceinline__ uint16_t div_to_bf16_bits(int32_t N, int32_t D) {
+  const float r = (float)N / (float)D;
+  uint32_t u = __float_as_uint(r);
+  if ((u & 0xFFFFu) == 0x8000u) {  // r != 0: step one fp32 ulp toward the quotient
+    const double diff = (double)N - (double)r * (double)D;
+    const bool up_in_magnitude = r > 0.0f ? diff > 0.0 : diff < 0.0;
+    if (diff != 0.0) u = up_in_magnitude ? u + 1 : u - 1;
+  }
+  return f32_to_bf16_bits(__uint_as_float(u));
 }
 
 // Element-type traits: E = elements per lane per MFMA, KS = K per MFMA.
@@ -84,21 +102,24 @@ template <> struct Elt<uint16_t> {  // bf16 stored as raw bits
   static __device__ __forceinline__ void set(frag& f, int e, uint16_t v) {
     f[e] = __builtin_bit_cast(__bf16, v);
   }
-  // Activations enter as hi + lo pairs (see the top of this file).
+  // Activations enter as hi + lo pairs (see the top of this file); the
+  // conversions are the hardware's packed round-to-nearest-even.
   static constexpr bool SPLIT = true;
-  static __device__ __forceinline__ void split1(float v, uint16_t& hi, uint16_t& lo) {
-    hi = f32_to_bf16_bits(v);
-    lo = f32_to_bf16_bits(v - bf16_bits_to_f32(hi));
+  // two fp32 values -> (hi0, hi1) and (lo0, lo1), packed as bf16 pairs
+  static __device__ __forceinline__ void split2(float v0, float v1, bf16x2& hi, bf16x2& lo) {
+    hi = bf16x2{(__bf16)v0, (__bf16)v1};
+    lo = bf16x2{(__bf16)(v0 - (float)hi[0]), (__bf16)(v1 - (float)hi[1])};
+  }
+  static __device__ __forceinline__ void split2(float v0, float v1, uint32_t& hi, uint32_t& lo) {
+    bf16x2 h, l;
+    split2(v0, v1, h, l);
+    hi = __builtin_bit_cast(uint32_t, h);
+    lo = __builtin_bit_cast(uint32_t, l);
   }
   // 4 fp32 values -> 4 hi and 4 lo bf16 values, packed pairwise in uint2
   static __device__ __forceinline__ void split4(const float4& v, uint2& hi, uint2& lo) {
-    uint16_t h[4], l[4];
-    split1(v.x, h[0], l[0]);
-    split1(v.y, h[1], l[1]);
-    split1(v.z, h[2], l[2]);
-    split1(v.w, h[3], l[3]);
-    hi = make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
-    lo = make_uint2((uint32_t)l[0] | ((uint32_t)l[1] << 16), (uint32_t)l[2] | ((uint32_t)l[3] << 16));
+    split2(v.x, v.y, hi.x, lo.x);
+    split2(v.z, v.w, hi.y, lo.y);
   }
   // A fragment pair from 8 consecutive fp32 values (16-byte aligned)
   static __device__ __forceinline__ void split8(const float* p, frag& hi, frag& lo) {
@@ -106,11 +127,13 @@ template <> struct Elt<uint16_t> {  // bf16 stored as raw bits
     const float4 b = *reinterpret_cast<const float4*>(p + 4);
     const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      uint16_t h, l;
-      split1(v[e], h, l);
-      set(hi, e, h);
-      set(lo, e, l);
+    for (int e = 0; e < 8; e += 2) {
+      bf16x2 h, l;
+      split2(v[e], v[e + 1], h, l);
+      hi[e] = h[0];
+      hi[e + 1] = h[1];
+      lo[e] = l[0];
+      lo[e + 1] = l[1];
     }
   }
 };
@@ -172,15 +195,23 @@ __device__ __forceinline__ void stage_weights(const ConvArgs& a, T* wl) {
   }
 }
 
+// The lane's bias of output channel nt * 16 + m, for each nt.
+template <int NT>
+__device__ __forceinline__ void load_bias(const float* bias, int m, float (&b)[NT]) {
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) b[nt] = bias[nt * 16 + m];
+}
+
 // Bias, ReLU, optional 2x2 max-pool and fp32 NHWC store of one 4x4 tile.
 // Lane (m, g) holds rows 4g..4g+3 (one pooling window) of output channel m.
 template <int NT>
-__device__ __forceinline__ void conv_epilogue(const ConvArgs& a, const f32x4 (&acc)[NT], float* out,
-                                              int ty, int tx, int ho, int wo, int m, int g) {
+__device__ __forceinline__ void conv_epilogue(const ConvArgs& a, const f32x4 (&acc)[NT],
+                                              const float (&bias)[NT], float* out, int ty, int tx,
+                                              int ho, int wo, int m, int g) {
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const int n = nt * 16 + m;
-    const float b = a.bias[n];
+    const float b = bias[nt];
     const int wy = g >> 1, wx = g & 1;
     if (a.pool) {
       float v = 0.0f;  // ReLU floor
@@ -205,15 +236,108 @@ __device__ __forceinline__ void conv_epilogue(const ConvArgs& a, const f32x4 (&a
 // dx padded to 4 and c to 4 (zero weights), so the 8 K values of a lane group
 // are the 4 channels of two horizontally adjacent pixels: one 16-byte LDS read
 // per MFMA for bf16.  K = 48, run as 2 steps of 32 (bf16) or 12 of 4 (fp32).
+
+// Stages rows x band_w pixels starting at input (y_top, x_left) of frame
+// idx[s], one pixel (3 channels + a zero, one 8- or 16-byte LDS store) per
+// thread and step, by the nthreads threads from thread tid0 on.
+template <typename T>
+__device__ __forceinline__ void stage_first(const ConvArgs& a, T* in, int64_t s, int y_top,
+                                            int x_left, int rows, int band_w, int tid0,
+                                            int nthreads) {
+  using X = Elt<T>;
+  if ((int)threadIdx.x < tid0) return;
+  const int32_t* S = a.sums + (int64_t)a.idx[s] * a.sums_h * a.sums_w * 3;
+  const int npix = rows * band_w;
+  const bool f32div = a.den255 < (1 << 24);  // the fp32 quotient path is exact
+#pragma unroll 2
+  for (int p = threadIdx.x - tid0; p < npix; p += nthreads) {
+    const int br = p / band_w, bc = p - br * band_w;
+    const int y = y_top + br, x = x_left + bc;
+    T v[4] = {X::from_f32(0.0f), X::from_f32(0.0f), X::from_f32(0.0f), X::from_f32(0.0f)};
+    if (y >= 0 && y < a.h && x >= 0 && x < a.w) {
+      int64_t acc[3] = {0, 0, 0};
+      for (int dy = 0; dy < a.fy; ++dy)
+        for (int dx = 0; dx < a.fx; ++dx) {
+          const int32_t* q = S + ((int64_t)(y * a.fy + dy) * a.sums_w + (x * a.fx + dx)) * 3;
+          acc[0] += q[0];
+          acc[1] += q[1];
+          acc[2] += q[2];
+        }
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+        // (S / den) / 127.5 - 1 = (2 S - den255) / den255, rounded once (exact ties included)
+        const int64_t num = 2 * acc[c] - a.den255;
+        if constexpr (X::SPLIT) {
+          v[c] = f32div ? div_to_bf16_bits((int32_t)num, (int32_t)a.den255)
+                        : X::from_f64((double)num / (double)a.den255);
+        } else {
+          v[c] = X::from_f64((double)num / (double)a.den255);
+        }
+      }
+    }
+    if constexpr (sizeof(T) == 2) {
+      *reinterpret_cast<uint2*>(in + p * 4) =
+          make_uint2((uint32_t)v[0] | ((uint32_t)v[1] << 16), (uint32_t)v[2] | ((uint32_t)v[3] << 16));
+    } else {
+      *reinterpret_cast<float4*>(in + p * 4) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+  }
+}
+
+// MFMA accumulation of one first-layer 4x4 tile whose tap (0, 0) of the
+// lane's pixel is band pixel (row0, col0).
 template <typename T, int NT>
-__global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
+__device__ __forceinline__ void first_tile(const T* in, const T* wl, int w_lds, int band_w,
+                                           int row0, int col0, int m, int g, f32x4 (&acc)[NT]) {
   using X = Elt<T>;
   constexpr int E = X::E, KS = X::KS;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k0 = 0; k0 < 48; k0 += KS) {
+    const int k = k0 + g * E;  // first K value of this lane group
+    typename X::frag av = X::zero();
+    if (k < 48) {
+      const int dy = k >> 4, dx = (k >> 2) & 3, c = k & 3;
+      av = X::load8(in + ((row0 + dy) * band_w + col0 + dx) * 4 + c);
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const typename X::frag bv = X::load(wl + (nt * 16 + m) * w_lds + k);
+      acc[nt] = X::mma(av, bv, acc[nt]);
+    }
+  }
+}
+
+// The same with the weight fragments already in registers (bf16: K = 64 in two
+// steps of 32, fragment [step][nt]).
+template <int NT>
+__device__ __forceinline__ void first_tile_b(const uint16_t* in, const bf16x8 (&bw)[2][NT],
+                                             int band_w, int row0, int col0, int g,
+                                             f32x4 (&acc)[NT]) {
+  using X = Elt<uint16_t>;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    const int k = ks * 32 + g * 8;
+    bf16x8 av = X::zero();
+    if (k < 48) {
+      const int dy = k >> 4, dx = (k >> 2) & 3;
+      av = X::load8(in + ((row0 + dy) * band_w + col0 + dx) * 4);
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[nt] = X::mma(av, bw[ks][nt], acc[nt]);
+  }
+}
+
+template <typename T, int NT>
+__global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   T* wl = reinterpret_cast<T*>(lds_raw);
   T* in = wl + (size_t)a.cout * a.w_lds;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nwaves = blockDim.x >> 6;
   stage_weights(a, wl);
   int64_t cnt = *a.count;
@@ -221,11 +345,12 @@ __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
   const int bands = (a.tiles_y + a.band_tiles - 1) / a.band_tiles;
   const int segs = (a.tiles_x + a.seg_tiles - 1) / a.seg_tiles;
   const int64_t items = cnt * bands * segs;
-  const int band_w = a.band_w;
   const int ho = a.pool ? a.h / 2 : a.h, wo = a.pool ? a.w / 2 : a.w;
   const int m = lane & 15, g = lane >> 4;
   int py, px;
   tile_pixel(m, py, px);
+  float bias[NT];
+  load_bias(a.bias, m, bias);
 
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
     const int64_t s = item / (bands * segs);
@@ -234,51 +359,15 @@ __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
     const int ty0 = band * a.band_tiles, tx0 = seg * a.seg_tiles;
     const int nty = min(a.band_tiles, a.tiles_y - ty0);
     const int ntx = min(a.seg_tiles, a.tiles_x - tx0);
-    const int rows = 4 * nty + 2;
-    const int y_top = 4 * ty0 - 1;  // input row of band row 0
     __syncthreads();  // previous item's readers are done with `in` (and weights staged)
-    {
-      const int32_t* S = a.sums + (int64_t)a.idx[s] * a.sums_h * a.sums_w * 3;
-      for (int e = tid; e < rows * band_w * 4; e += blockDim.x) {
-        const int c = e & 3, pix = e >> 2;
-        const int br = pix / band_w, bc = pix - br * band_w;
-        const int y = y_top + br, x = 4 * tx0 + bc - 1;
-        T v = X::from_f32(0.0f);
-        if (c < 3 && y >= 0 && y < a.h && x >= 0 && x < a.w) {
-          int64_t acc = 0;
-          for (int dy = 0; dy < a.fy; ++dy)
-            for (int dx = 0; dx < a.fx; ++dx)
-              acc += S[((int64_t)(y * a.fy + dy) * a.sums_w + (x * a.fx + dx)) * 3 + c];
-          // (S / den) / 127.5 - 1 as one correctly rounded division of integers:
-          // bf16 rounding of it matches the exact value's (exact ties included)
-          v = X::from_f64((double)(2 * acc - a.den255) / (double)a.den255);
-        }
-        in[pix * 4 + c] = v;
-      }
-    }
+    stage_first(a, in, s, 4 * ty0 - 1, 4 * tx0 - 1, 4 * nty + 2, a.band_w, 0, (int)blockDim.x);
     __syncthreads();
     float* out = a.act_out + s * (int64_t)ho * wo * a.cout;
     for (int t = wave; t < nty * ntx; t += nwaves) {
       const int tyl = t / ntx, txl = t - tyl * ntx;
       f32x4 acc[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int row0 = 4 * tyl + py, col0 = 4 * txl + px;  // band coordinates of tap (0, 0)
-#pragma unroll
-      for (int k0 = 0; k0 < 48; k0 += KS) {
-        const int k = k0 + g * E;  // first K value of this lane group
-        typename X::frag av = X::zero();
-        if (k < 48) {
-          const int dy = k >> 4, dx = (k >> 2) & 3, c = k & 3;
-          av = X::load8(in + ((row0 + dy) * band_w + col0 + dx) * 4 + c);
-        }
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const typename X::frag bv = X::load(wl + (nt * 16 + m) * a.w_lds + k);
-          acc[nt] = X::mma(av, bv, acc[nt]);
-        }
-      }
-      conv_epilogue<NT>(a, acc, out, ty0 + tyl, tx0 + txl, ho, wo, m, g);
+      first_tile<T, NT>(in, wl, a.w_lds, a.band_w, 4 * tyl + py, 4 * txl + px, m, g, acc);
+      conv_epilogue<NT>(a, acc, bias, out, ty0 + tyl, tx0 + txl, ho, wo, m, g);
     }
   }
 }
@@ -287,16 +376,105 @@ __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
 // The fp32 input band is staged as fp32 (fp32 nets) or as hi and lo bf16
 // planes lo_plane elements apart (bf16 nets); the lo plane is multiplied by the
 // same weight fragments into a second set of accumulators.
+
+// Stages rows x band_w pixels starting at input (y_top, x_left) of image s's
+// fp32 activations; every thread of the workgroup takes part.
+template <typename T>
+__device__ __forceinline__ void stage_inner(const ConvArgs& a, T* in, int64_t s, int y_top,
+                                            int x_left, int rows, int band_w) {
+  using X = Elt<T>;
+  const float* src = a.act_in + s * (int64_t)a.h * a.w * a.cin;
+  const int vec_per_pix = a.cin / 4;  // float4 vectors per input pixel
+  const int total = rows * band_w * vec_per_pix;
+#pragma unroll 4
+  for (int e = threadIdx.x; e < total; e += blockDim.x) {
+    const int pix = e / vec_per_pix, cv = e - pix * vec_per_pix;
+    const int br = pix / band_w, bc = pix - br * band_w;
+    const int y = y_top + br, x = x_left + bc;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (y >= 0 && y < a.h && x >= 0 && x < a.w)
+      v = *reinterpret_cast<const float4*>(src + ((int64_t)y * a.w + x) * a.cin + cv * 4);
+    T* dst = in + pix * a.cin_lds + cv * 4;
+    if constexpr (X::SPLIT) {
+      uint2 hi, lo;
+      X::split4(v, hi, lo);
+      *reinterpret_cast<uint2*>(dst) = hi;
+      *reinterpret_cast<uint2*>(dst + a.lo_plane) = lo;
+    } else {
+      *reinterpret_cast<float4*>(dst) = v;
+    }
+  }
+}
+
+// MFMA accumulation of one inner-layer 4x4 tile from a band with pixel stride
+// cin_lds (and, for bf16, its lo plane lo_plane elements further).
 template <typename T, int NT>
-__global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
+__device__ __forceinline__ void inner_tile(const T* in, const T* wl, int w_lds, int cin,
+                                           int cin_lds, int lo_plane, int band_w, int row0,
+                                           int col0, int m, int g, f32x4 (&acc)[NT]) {
   using X = Elt<T>;
   constexpr int E = X::E, KS = X::KS;
   constexpr bool SPLIT = X::SPLIT;
+  f32x4 acc_lo[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    acc_lo[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const int chunks = cin / KS;
+  for (int tap = 0; tap < 9; ++tap) {
+    const int dy = tap / 3, dx = tap - 3 * dy;
+    const T* arow = in + ((row0 + dy) * band_w + col0 + dx) * cin_lds + g * E;
+    const T* brow = wl + m * w_lds + tap * cin + g * E;
+    for (int ch = 0; ch < chunks; ++ch) {
+      const typename X::frag av = X::load(arow + ch * KS);
+      typename X::frag av_lo;
+      if constexpr (SPLIT) av_lo = X::load(arow + lo_plane + ch * KS);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const typename X::frag bv = X::load(brow + nt * 16 * w_lds + ch * KS);
+        acc[nt] = X::mma(av, bv, acc[nt]);
+        if constexpr (SPLIT) acc_lo[nt] = X::mma(av_lo, bv, acc_lo[nt]);
+      }
+    }
+  }
+  if constexpr (SPLIT) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[nt] += acc_lo[nt];
+  }
+}
+
+// bf16 inner layer with 32 input channels (one K step per tap) and the weight
+// fragments of all 9 taps in registers ([tap][nt]); the hi and lo products go
+// into the same accumulators (registers are the limit here).
+template <int NT>
+__device__ __forceinline__ void inner_tile32_b(const uint16_t* in, const bf16x8 (&bw)[9][NT],
+                                               int cin_lds, int lo_plane, int band_w, int row0,
+                                               int col0, int g, f32x4 (&acc)[NT]) {
+  using X = Elt<uint16_t>;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int tap = 0; tap < 9; ++tap) {
+    const int dy = tap / 3, dx = tap - 3 * dy;
+    const uint16_t* arow = in + ((row0 + dy) * band_w + col0 + dx) * cin_lds + g * 8;
+    const bf16x8 av = X::load(arow);
+    const bf16x8 av_lo = X::load(arow + lo_plane);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      acc[nt] = X::mma(av, bw[tap][nt], acc[nt]);
+      acc[nt] = X::mma(av_lo, bw[tap][nt], acc[nt]);
+    }
+  }
+}
+
+template <typename T, int NT>
+__global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   T* wl = reinterpret_cast<T*>(lds_raw);
   T* in = wl + (size_t)a.cout * a.w_lds;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nwaves = blockDim.x >> 6;
   stage_weights(a, wl);
   int64_t cnt = *a.count;
@@ -304,13 +482,12 @@ __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
   const int bands = (a.tiles_y + a.band_tiles - 1) / a.band_tiles;
   const int segs = (a.tiles_x + a.seg_tiles - 1) / a.seg_tiles;
   const int64_t items = cnt * bands * segs;
-  const int band_w = a.band_w;
   const int ho = a.pool ? a.h / 2 : a.h, wo = a.pool ? a.w / 2 : a.w;
   const int m = lane & 15, g = lane >> 4;
   int py, px;
   tile_pixel(m, py, px);
-  const int vec_per_pix = a.cin / 4;  // float4 vectors per input pixel
-  const int chunks = a.cin / KS;
+  float bias[NT];
+  load_bias(a.bias, m, bias);
 
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
     const int64_t s = item / (bands * segs);
@@ -319,62 +496,141 @@ __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
     const int ty0 = band * a.band_tiles, tx0 = seg * a.seg_tiles;
     const int nty = min(a.band_tiles, a.tiles_y - ty0);
     const int ntx = min(a.seg_tiles, a.tiles_x - tx0);
-    const int rows = 4 * nty + 2;
-    const int y_top = 4 * ty0 - 1;
     __syncthreads();  // previous item's readers are done with `in` (and weights staged)
-    {
-      const float* src = a.act_in + s * (int64_t)a.h * a.w * a.cin;
-      for (int e = tid; e < rows * band_w * vec_per_pix; e += blockDim.x) {
-        const int pix = e / vec_per_pix, cv = e - pix * vec_per_pix;
-        const int br = pix / band_w, bc = pix - br * band_w;
-        const int y = y_top + br, x = 4 * tx0 + bc - 1;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (y >= 0 && y < a.h && x >= 0 && x < a.w)
-          v = *reinterpret_cast<const float4*>(src + ((int64_t)y * a.w + x) * a.cin + cv * 4);
-        T* dst = in + pix * a.cin_lds + cv * 4;
-        if constexpr (SPLIT) {
-          uint2 hi, lo;
-          X::split4(v, hi, lo);
-          *reinterpret_cast<uint2*>(dst) = hi;
-          *reinterpret_cast<uint2*>(dst + a.lo_plane) = lo;
-        } else {
-          *reinterpret_cast<float4*>(dst) = v;
-        }
-      }
-    }
+    stage_inner(a, in, s, 4 * ty0 - 1, 4 * tx0 - 1, 4 * nty + 2, a.band_w);
     __syncthreads();
     float* out = a.act_out + s * (int64_t)ho * wo * a.cout;
     for (int t = wave; t < nty * ntx; t += nwaves) {
       const int tyl = t / ntx, txl = t - tyl * ntx;
-      f32x4 acc[NT], acc_lo[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        acc_lo[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-      const int row0 = 4 * tyl + py, col0 = 4 * txl + px;
-      for (int tap = 0; tap < 9; ++tap) {
-        const int dy = tap / 3, dx = tap - 3 * dy;
-        const T* arow = in + ((row0 + dy) * band_w + col0 + dx) * a.cin_lds + g * E;
-        const T* brow = wl + m * a.w_lds + tap * a.cin + g * E;
-        for (int ch = 0; ch < chunks; ++ch) {
-          const typename X::frag av = X::load(arow + ch * KS);
-          typename X::frag av_lo;
-          if constexpr (SPLIT) av_lo = X::load(arow + a.lo_plane + ch * KS);
-#pragma unroll
-          for (int nt = 0; nt < NT; ++nt) {
-            const typename X::frag bv = X::load(brow + nt * 16 * a.w_lds + ch * KS);
-            acc[nt] = X::mma(av, bv, acc[nt]);
-            if constexpr (SPLIT) acc_lo[nt] = X::mma(av_lo, bv, acc_lo[nt]);
-          }
-        }
-      }
-      if constexpr (SPLIT) {
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) acc[nt] += acc_lo[nt];
-      }
-      conv_epilogue<NT>(a, acc, out, ty0 + tyl, tx0 + txl, ho, wo, m, g);
+      f32x4 acc[NT];
+      inner_tile<T, NT>(in, wl, a.w_lds, a.cin, a.cin_lds, a.lo_plane, a.band_w, 4 * tyl + py,
+                        4 * txl + px, m, g, acc);
+      conv_epilogue<NT>(a, acc, bias, out, ty0 + tyl, tx0 + txl, ho, wo, m, g);
     }
+  }
+}
+
+// The first two layers of a bf16 network fused per image, when the pooled
+// output of the first fits in LDS beside both layers' weights: a workgroup
+// (one per CU, 16 waves) stages the first layer's whole input, runs it into
+// the second layer's hi / lo input band in LDS (halo and tail kept zero), and
+// runs the second layer from there into the fp32 workspace.  The first
+// layer's input of the next image is staged while the second layer runs.
+struct PairArgs {
+  int32_t off_w1, off_in0, off_in1;  // LDS offsets (bf16 elements) of w1, in0, in1
+};
+
+// Bias, ReLU and 2x2 max-pool of one first-layer tile, stored as hi / lo bf16
+// at (oy + 1, ox + 1) of the second layer's band (row / column 0 are halo).
+template <int NT>
+__device__ __forceinline__ void pair_epilogue(const ConvArgs& a1, const f32x4 (&acc)[NT],
+                                              const float (&bias)[NT], uint16_t* in1, int ty,
+                                              int tx, int ho, int wo, int m, int g) {
+  const int oy = 2 * ty + (g >> 1), ox = 2 * tx + (g & 1);
+  const bool store = oy < ho && ox < wo && (m & 1) == 0;
+  uint16_t* p = in1 + ((oy + 1) * a1.band_w + ox + 1) * a1.cin_lds;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int n = nt * 16 + m;
+    float v = 0.0f;  // ReLU floor
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v = fmaxf(v, acc[nt][r] + bias[nt]);
+    // even lanes store channels n, n + 1 (the odd neighbour's value) as dwords
+    const float v1 = __shfl_down(v, 1, 16);
+    uint32_t hi, lo;
+    Elt<uint16_t>::split2(v, v1, hi, lo);
+    if (store) {
+      *reinterpret_cast<uint32_t*>(p + n) = hi;
+      *reinterpret_cast<uint32_t*>(p + n + a1.lo_plane) = lo;
+    }
+  }
+}
+
+template <int NT0, int NT1, bool B1REG>
+__global__ void __launch_bounds__(1024) k_conv_pair(ConvArgs a0, ConvArgs a1, PairArgs pa) {
+  using T = uint16_t;
+  using X = Elt<T>;
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  T* lds = reinterpret_cast<T*>(lds_raw);
+  T* w0 = lds;
+  T* w1 = lds + pa.off_w1;
+  T* in0 = lds + pa.off_in0;
+  T* in1 = lds + pa.off_in1;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nwaves = blockDim.x >> 6;
+  stage_weights(a0, w0);
+  stage_weights(a1, w1);
+  for (int i = threadIdx.x; i < 2 * a1.lo_plane; i += blockDim.x) in1[i] = 0;
+  int64_t cnt = *a0.count;
+  if (cnt > a0.max_count) cnt = a0.max_count;
+  const int ho0 = a0.h / 2, wo0 = a0.w / 2;  // the first layer pools
+  const int ho1 = a1.pool ? a1.h / 2 : a1.h, wo1 = a1.pool ? a1.w / 2 : a1.w;
+  const int rows0 = 4 * a0.tiles_y + 2;
+  const int m = lane & 15, g = lane >> 4;
+  int py, px;
+  tile_pixel(m, py, px);
+  float bias0[NT0], bias1[NT1];
+  load_bias(a0.bias, m, bias0);
+  load_bias(a1.bias, m, bias1);
+  // the next image is staged by the waves that run one second-layer tile fewer
+  const int tiles1 = a1.tiles_y * a1.tiles_x;
+  const int extra = tiles1 % nwaves;
+  const int stage_tid0 = extra ? extra * 64 : 0;
+  int64_t s = blockIdx.x;
+  if (s < cnt) stage_first(a0, in0, s, -1, -1, rows0, a0.band_w, 0, (int)blockDim.x);
+  for (; s < cnt; s += gridDim.x) {
+    __syncthreads();  // in0 staged; the previous image's second layer is done with in1
+    if constexpr (NT0 <= 2) {
+      // each wave keeps the first layer's weight fragments in registers
+      bf16x8 bw0[2][NT0];
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int nt = 0; nt < NT0; ++nt)
+          bw0[ks][nt] = X::load(w0 + (nt * 16 + m) * a0.w_lds + ks * 32 + g * 8);
+      for (int t = wave; t < a0.tiles_y * a0.tiles_x; t += nwaves) {
+        const int ty = t / a0.tiles_x, tx = t - ty * a0.tiles_x;
+        f32x4 acc[NT0];
+        first_tile_b<NT0>(in0, bw0, a0.band_w, 4 * ty + py, 4 * tx + px, g, acc);
+        pair_epilogue<NT0>(a1, acc, bias0, in1, ty, tx, ho0, wo0, m, g);
+      }
+    } else {
+      for (int t = wave; t < a0.tiles_y * a0.tiles_x; t += nwaves) {
+        const int ty = t / a0.tiles_x, tx = t - ty * a0.tiles_x;
+        f32x4 acc[NT0];
+        first_tile<T, NT0>(in0, w0, a0.w_lds, a0.band_w, 4 * ty + py, 4 * tx + px, m, g, acc);
+        pair_epilogue<NT0>(a1, acc, bias0, in1, ty, tx, ho0, wo0, m, g);
+      }
+    }
+    __syncthreads();  // in1 complete; in0 free
+    float* out = a1.act_out + s * (int64_t)ho1 * wo1 * a1.cout;
+    if constexpr (B1REG) {  // 32 input channels: all 9 taps' fragments in registers
+      bf16x8 bw1[9][NT1];
+#pragma unroll
+      for (int tap = 0; tap < 9; ++tap)
+#pragma unroll
+        for (int nt = 0; nt < NT1; ++nt)
+          bw1[tap][nt] = X::load(w1 + (nt * 16 + m) * a1.w_lds + tap * 32 + g * 8);
+      for (int t = wave; t < a1.tiles_y * a1.tiles_x; t += nwaves) {
+        const int ty = t / a1.tiles_x, tx = t - ty * a1.tiles_x;
+        f32x4 acc[NT1];
+        inner_tile32_b<NT1>(in1, bw1, a1.cin_lds, a1.lo_plane, a1.band_w, 4 * ty + py,
+                            4 * tx + px, g, acc);
+        conv_epilogue<NT1>(a1, acc, bias1, out, ty, tx, ho1, wo1, m, g);
+      }
+    } else {
+      for (int t = wave; t < a1.tiles_y * a1.tiles_x; t += nwaves) {
+        const int ty = t / a1.tiles_x, tx = t - ty * a1.tiles_x;
+        f32x4 acc[NT1];
+        inner_tile<T, NT1>(in1, w1, a1.w_lds, a1.cin, a1.cin_lds, a1.lo_plane, a1.band_w,
+                           4 * ty + py, 4 * tx + px, m, g, acc);
+        conv_epilogue<NT1>(a1, acc, bias1, out, ty, tx, ho1, wo1, m, g);
+      }
+    }
+    if (s + gridDim.x < cnt)
+      stage_first(a0, in0, s + gridDim.x, -1, -1, rows0, a0.band_w, stage_tid0,
+                  (int)blockDim.x - stage_tid0);
   }
 }
 
@@ -420,16 +676,20 @@ __global__ void __launch_bounds__(256) k_dense(DenseArgs a) {
       acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
       acc_lo[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
+    // flat is a multiple of 16 (and of E): a lane group's E values of the last,
+    // partial K step are either all inside or all past the end (zero)
     for (int k0 = 0; k0 < a.flat; k0 += KS) {
+      const bool kin = k0 + g * E < a.flat;
       typename X::frag av = X::zero(), av_lo = X::zero();
       if constexpr (SPLIT) {
-        if (valid) X::split8(arow + k0, av, av_lo);
+        if (valid && kin) X::split8(arow + k0, av, av_lo);
       } else {
-        if (valid) av = arow[k0];
+        if (valid && kin) av = arow[k0];
       }
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        const typename X::frag bv = X::load(w1 + (int64_t)(nt * 16 + m) * a.flat + k0 + g * E);
+        typename X::frag bv = X::zero();
+        if (kin) bv = X::load(w1 + (int64_t)(nt * 16 + m) * a.flat + k0 + g * E);
         acc[nt] = X::mma(av, bv, acc[nt]);
         if constexpr (SPLIT) acc_lo[nt] = X::mma(av_lo, bv, acc_lo[nt]);
       }
@@ -531,6 +791,12 @@ void conv_tiles(const CnnLayer& L, int32_t* tiles_y, int32_t* tiles_x) {
   *tiles_x = (wn + 3) / 4;
 }
 
+// Smallest n' >= n with n' = 12 (mod 16).
+int32_t pad_row_pixels(int32_t n) {
+  int32_t p = (n + 3) / 16 * 16 + 12;
+  return p - 16 >= n ? p - 16 : p;
+}
+
 // LDS of one conv layer's workgroup: staged weights plus an input band of
 // band_tiles tile rows (4 output rows each + 2 halo rows) by seg_tiles tile
 // columns (+ halo), in two planes (hi, lo) for the inner layers of a bf16
@@ -548,14 +814,26 @@ size_t conv_lds_bytes(const CnnLayer& L, bool bf16, int32_t* cin_lds, int32_t* w
   conv_tiles(L, &ty, &tx);
   const size_t planes = bf16 && !first ? 2 : 1;
   const size_t wbytes = (size_t)L.cout * wr * es;
-  // staged columns of st tile columns; the first layer also reads tap dx = 3 (weight 0)
-  auto cols = [&](int32_t st) { return 4 * st + (first ? 3 : 2); };
-  int32_t st = tx;
-  while (st > 1 && wbytes + (size_t)6 * cols(st) * cl * es * planes > 128 * 1024) st = (st + 1) / 2;
-  const int32_t bw = cols(st);
-  const size_t row_bytes = (size_t)bw * cl * es * planes;
-  int32_t bt = 1;
-  while (bt < ty && wbytes + (size_t)(4 * (bt + 1) + 2) * row_bytes <= 48 * 1024) ++bt;
+  // staged columns of st tile columns (the first layer also reads tap dx = 3,
+  // weight 0), padded to 12 (mod 16) pixels: the 16 pixels of a 4x4 tile then
+  // fall on distinct LDS banks (pixel strides of 8 bytes, or an odd number of
+  // 16 bytes).  Without the padding when only that fits the LDS.
+  int32_t st = tx, bw = 0, bt = 1;
+  size_t row_bytes = 0;
+  for (int pad = 1; pad >= 0; --pad) {
+    auto cols = [&](int32_t n) {
+      const int32_t c = 4 * n + (first ? 3 : 2);
+      return pad ? pad_row_pixels(c) : c;
+    };
+    st = tx;
+    while (st > 1 && wbytes + (size_t)6 * cols(st) * cl * es * planes > 128 * 1024)
+      st = (st + 1) / 2;
+    bw = cols(st);
+    row_bytes = (size_t)bw * cl * es * planes;
+    bt = 1;
+    while (bt < ty && wbytes + (size_t)(4 * (bt + 1) + 2) * row_bytes <= 48 * 1024) ++bt;
+    if (wbytes + (size_t)(4 * bt + 2) * row_bytes <= 160 * 1024) break;
+  }
   if (cin_lds) *cin_lds = cl;
   if (w_lds) *w_lds = wr;
   if (band_w) *band_w = bw;
@@ -563,6 +841,75 @@ size_t conv_lds_bytes(const CnnLayer& L, bool bf16, int32_t* cin_lds, int32_t* w
   if (seg_tiles) *seg_tiles = st;
   return wbytes + (size_t)(4 * bt + 2) * row_bytes;
 }
+
+// Whether the first two layers run fused (k_conv_pair): a bf16 network whose
+// first layer pools, with output channel counts the kernel is built for, and
+// whose weights, first-layer input and second-layer hi / lo band fit the LDS
+// of one CU.  Fills the whole-image geometry of both layers and the LDS
+// offsets.
+bool pair_plan(const Cnn& cnn, ConvArgs* a0, ConvArgs* a1, PairArgs* pa, size_t* lds_bytes) {
+  const CnnLayer& L0 = cnn.layers[0];
+  const CnnLayer& L1 = cnn.layers[1];
+  auto nt_ok = [](int c) { return c == 16 || c == 32 || c == 64; };
+  if (!cnn.bf16 || !L0.pool || !nt_ok(L0.cout) || !nt_ok(L1.cout)) return false;
+  if (L0.cout == 64 && L1.cout == 64) return false;  // register pressure: run layered
+  auto al8 = [](int64_t e) { return (e + 7) / 8 * 8; };  // 16-byte alignment of bf16 arrays
+  a0->cin_lds = 4;
+  a0->w_lds = L0.kpad + 8;
+  a0->band_tiles = a0->tiles_y;
+  a0->seg_tiles = a0->tiles_x;
+  a0->band_w = 4 * a0->tiles_x + 3;
+  a0->lo_plane = 0;
+  a1->cin_lds = L1.cin + 8;
+  a1->w_lds = L1.kpad + 8;
+  a1->band_tiles = a1->tiles_y;
+  a1->seg_tiles = a1->tiles_x;
+  // row stride of the band padded to 12 (mod 16) pixels: with the 80-byte
+  // pixel stride (odd in 16-byte units) the 16 pixels of a 4x4 tile then fall
+  // on distinct 16-byte bank groups
+  a1->band_w = pad_row_pixels(4 * a1->tiles_x + 2);
+  const int64_t plane = al8((int64_t)(4 * a1->tiles_y + 2) * a1->band_w * a1->cin_lds);
+  a1->lo_plane = (int32_t)plane;
+  const int64_t w0 = al8((int64_t)L0.cout * a0->w_lds);
+  const int64_t w1 = al8((int64_t)L1.cout * a1->w_lds);
+  const int64_t in0 = al8((int64_t)(4 * a0->tiles_y + 2) * a0->band_w * 4);
+  const int64_t total = w0 + w1 + in0 + 2 * plane;
+  if (total * 2 > 160 * 1024) return false;
+  pa->off_w1 = (int32_t)w0;
+  pa->off_in0 = (int32_t)(w0 + w1);
+  pa->off_in1 = (int32_t)(w0 + w1 + in0);
+  *lds_bytes = (size_t)total * 2;
+  return true;
+}
+
+namespace {
+int launch_pair(int nt0, int nt1, const ConvArgs& a0, const ConvArgs& a1, const PairArgs& pa,
+                unsigned grid, size_t lds, hipStream_t st) {
+  // second-layer weights in registers when they are 9 taps x 32 channels x <= 32 outputs
+  const bool breg = a1.cin == 32 && nt1 <= 2;
+#define NSC_PAIR_CASE(A, B)                                                                  \
+  if (nt0 == A && nt1 == B) {                                                                \
+    if (breg && A <= 2 && B <= 2)                                                            \
+      hipLaunchKernelGGL((k_conv_pair<A, B, (A <= 2 && B <= 2)>), dim3(grid), dim3(1024), lds,\
+                         st, a0, a1, pa);                                                    \
+    else                                                                                     \
+      hipLaunchKernelGGL((k_conv_pair<A, B, false>), dim3(grid), dim3(1024), lds, st, a0, a1, \
+                         pa);                                                                \
+    NSC_CHECK_LAUNCH("k_conv_pair");                                                         \
+    return NSC_OK;                                                                           \
+  }
+  NSC_PAIR_CASE(1, 1)
+  NSC_PAIR_CASE(1, 2)
+  NSC_PAIR_CASE(1, 4)
+  NSC_PAIR_CASE(2, 1)
+  NSC_PAIR_CASE(2, 2)
+  NSC_PAIR_CASE(2, 4)
+  NSC_PAIR_CASE(4, 1)
+  NSC_PAIR_CASE(4, 2)
+#undef NSC_PAIR_CASE
+  return fail(NSC_E_SHAPE, "fused conv pair with %d and %d output channels", nt0 * 16, nt1 * 16);
+}
+}  // namespace
 
 // Two ping-pong buffers of fp32 activations per image.
 size_t cnn_workspace_bytes(const Cnn& cnn, int64_t max_count) {
@@ -579,7 +926,7 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
                 cnn_workspace_bytes(cnn, r.max_count));
   float* buf[2] = {static_cast<float*>(ws),
                    reinterpret_cast<float*>(static_cast<unsigned char*>(ws) + per * (size_t)r.max_count)};
-  for (int l = 0; l < cnn.n_layers; ++l) {
+  auto layer_args = [&](int l) {
     const CnnLayer& L = cnn.layers[l];
     ConvArgs a{};
     a.sums = r.sums;
@@ -602,6 +949,26 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
     a.kpad = L.kpad;
     a.pool = L.pool ? 1 : 0;
     conv_tiles(L, &a.tiles_y, &a.tiles_x);
+    return a;
+  };
+  int first_layered = 0;
+  {
+    ConvArgs a0 = layer_args(0);
+    ConvArgs a1{};
+    PairArgs pa{};
+    size_t lds = 0;
+    if (cnn.n_layers >= 2) a1 = layer_args(1);
+    if (cnn.n_layers >= 2 && pair_plan(cnn, &a0, &a1, &pa, &lds)) {
+      int64_t grid = r.max_count < kNumCU ? r.max_count : kNumCU;
+      const int rc = launch_pair(cnn.layers[0].cout / 16, cnn.layers[1].cout / 16, a0, a1, pa,
+                                 (unsigned)grid, lds, stream);
+      if (rc) return rc;
+      first_layered = 2;
+    }
+  }
+  for (int l = first_layered; l < cnn.n_layers; ++l) {
+    const CnnLayer& L = cnn.layers[l];
+    ConvArgs a = layer_args(l);
     const size_t lds =
         conv_lds_bytes(L, cnn.bf16, &a.cin_lds, &a.w_lds, &a.band_w, &a.band_tiles, &a.seg_tiles);
     a.lo_plane = (4 * a.band_tiles + 2) * a.band_w * a.cin_lds;

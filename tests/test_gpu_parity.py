@@ -231,6 +231,18 @@ def test_cnn_column_segments():
     _cnn_case(spec, n_frames=12, n_img=5)
 
 
+@pytest.mark.parametrize("conv,pool,hw,fy", [
+    ((32, 64, 32), (True, False, True), (23, 31), 1),   # fused pair + a layered third layer
+    ((64, 16), (True, True), (20, 20), 1),              # 64 then 16 channels
+    ((32, 32), (True, True), (50, 50), 2),              # nested 2x2 cells into the first layer
+    ((32, 32), (True, False), (13, 9), 1),              # unpooled second layer, tiny odd map
+])
+def test_cnn_fused_pair_shapes(conv, pool, hw, fy):
+    # bf16 nets whose pooled first layer fits in LDS run their first two layers fused
+    spec = synth.CNNSpec(in_h=hw[0], in_w=hw[1], conv=conv, pool=pool, dense=32, bf16=True)
+    _cnn_case(spec, n_frames=24, n_img=11, fy=fy)
+
+
 def test_cnn_zero_count():
     spec = W.VGA.cnn
     desc = nsc.make_desc(spec.conv, spec.pool, spec.dense, 50, 50, True)
