@@ -7,8 +7,8 @@ cascade on a buffer waits for that buffer's fill, and the next fill of a buffer
 waits for the cascade that read it.  Between chunks the carried state (area
 sums and decisions of the last delta frames) continues the reuse of frame
 t - delta across the boundary (Sec. 5), so the chunked result equals a one-shot
-run of the whole video.  Batching frames into large chunks trades latency for
-throughput (Sec. 7, batching).
+run of the whole video.  Frames are batched for the GPU (Sec. 7); larger
+chunks raise throughput and add latency on live video (Sec. 8).
 
 Streams are created at the default priority.  Nothing here computes: filling
 is the caller's `produce` callback, and every cascade step runs in libnsc.
