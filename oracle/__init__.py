@@ -38,7 +38,7 @@ class Cfg(ctypes.Structure):
     _fields_ = [("H", _i32), ("W", _i32), ("Ho", _i32), ("Wo", _i32), ("Hc", _i32), ("Wc", _i32),
                 ("ref_mode", _i32), ("delta", _i32), ("Gh", _i32), ("Gw", _i32),
                 ("lr_w", _vp), ("lr_b", _dbl), ("ref_sums", _vp), ("delta_diff", _dbl),
-                ("c_low", _dbl), ("c_high", _dbl)]
+                ("c_low", _dbl), ("c_high", _dbl), ("check_stride", _i32)]
 
 
 _LIB = None
@@ -51,6 +51,8 @@ def lib() -> ctypes.CDLL:
         L = ctypes.CDLL(SO)
         L.oracle_area_weights.restype = _i64
         L.oracle_area_weights.argtypes = [_i32, _i32, _vp]
+        L.oracle_history.restype = _i64
+        L.oracle_history.argtypes = [_vp]
         L.oracle_area_den.restype = _i64
         L.oracle_area_den.argtypes = [_i32] * 4
         L.oracle_area_sums.restype = None
@@ -190,19 +192,26 @@ def make_cfg(wl, lr_w=None, ref_sums=None, **over) -> tuple:
         keep.append(rs)
         c.ref_sums = rs.ctypes.data
     c.delta_diff, c.c_low, c.c_high = wl.delta_diff, wl.c_low, wl.c_high
+    c.check_stride = getattr(wl, "check_stride", 1)
     for k, v in over.items():
         setattr(c, k, v)
     return c, keep
 
 
+def history(cfg: Cfg) -> int:
+    """Frames before t0 whose sums and decisions a chunked run needs."""
+    return int(lib().oracle_history(ctypes.byref(cfg)))
+
+
 def cascade(cfg: Cfg, spec, blob, frames: np.ndarray, t0: int = 0, state=None):
     """Run the oracle cascade on frames [t0, t0+n); returns a dict of outputs
-    and the new state (area sums and decisions of the last delta frames)."""
+    and the new state (area sums and decisions of the last history(cfg)
+    frames: delta for the earlier-frame detector, s - 1 for frame skipping)."""
     frames = _c(frames, np.uint8)
     n = frames.shape[0]
     d = cnn_desc(spec)
     blob = _c(blob, np.float32)
-    D = cfg.delta if cfg.ref_mode == 0 else 0
+    D = history(cfg)
     cells = cfg.Ho * cfg.Wo * 3
     out = dict(score=np.zeros(n), fire=np.zeros(n, np.uint8), logit=np.zeros(n),
                prob=np.zeros(n), lscale=np.zeros(n), label=np.zeros(n, np.uint8),

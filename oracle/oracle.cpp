@@ -358,16 +358,32 @@ struct oracle_cfg {
   const int64_t* ref_sums;  // fixed reference image area sums, Ho*Wo*3 (mode 1)
   double delta_diff;
   double c_low, c_high;
+  int32_t check_stride;   // frame skipping: check frames t with t mod s = 0 (0 or 1: all)
 };
 
+// Number of earlier frames whose sums and decisions a chunked run carries:
+// delta (mode 0) for the compared frame, s - 1 for the last checked frame.
+int64_t oracle_history(const oracle_cfg* cfg) {
+  const int64_t s = cfg->check_stride > 1 ? cfg->check_stride : 1;
+  const int64_t d = cfg->ref_mode == 0 ? cfg->delta : 0;
+  return d > s - 1 ? d : s - 1;
+}
+
 // Runs the cascade on frames [t0, t0 + n) (frames: n x H x W x 3 uint8).
-// state_S / state_dec: area sums (Ho*Wo*3 each) and decisions of frames
-// t0 - delta .. t0 - 1 (needed when t0 > 0 in mode 0); the updated state of
-// frames t0 + n - delta .. t0 + n - 1 is written to state_S_out / state_dec_out
-// (nullable).  Outputs per frame: score (+inf for a forced frame), fire,
-// logit, prob and the logit's scale (NaN where the CNN did not run), label, defer.
-// Reading: frames with absolute index t < delta have no frame t - delta and
-// always fire.  Returns the number of frames that fired, or -1 on bad input.
+// state_S / state_dec: area sums (Ho*Wo*3 each) and decisions of the
+// oracle_history() frames before t0 (needed when t0 > 0 and the history is
+// not empty); the same of the frames before t0 + n is written to state_S_out /
+// state_dec_out (nullable).  Outputs per frame: score (+inf for a forced
+// frame, NaN for a frame that is not checked), fire, logit, prob and the
+// logit's scale (NaN where the CNN did not run), label, defer.
+// Frame skipping (Sec. 5, the check interval t_skip, here s frames): only
+// frames with t mod s = 0 run the difference detector (and, if it fires, the
+// CNN).  Readings: a frame that is not checked keeps the output of the last
+// checked frame, floor(t / s) * s; with the earlier-frame detector delta is a
+// multiple of s, so the compared frame t - delta is a checked one.
+// Reading: checked frames with absolute index t < delta have no frame
+// t - delta and always fire.  Returns the number of frames that fired, or -1
+// on bad input.
 int64_t oracle_cascade(const oracle_cfg* cfg, const oracle_cnn_desc* net, const float* blob,
                        const uint8_t* frames, int64_t n, int64_t t0, const int64_t* state_S,
                        const uint8_t* state_dec, double* score, uint8_t* fire, double* logit,
@@ -378,9 +394,12 @@ int64_t oracle_cascade(const oracle_cfg* cfg, const oracle_cnn_desc* net, const 
   const int64_t den = oracle_area_den(cfg->H, cfg->W, cfg->Ho, cfg->Wo);
   const int64_t den_c = oracle_area_den(cfg->H, cfg->W, cfg->Hc, cfg->Wc);
   const int64_t fb = (int64_t)cfg->H * cfg->W * 3;
-  const int D = cfg->ref_mode == 0 ? cfg->delta : 0;
-  if (cfg->ref_mode == 0 && D < 1) return -1;
-  if (cfg->ref_mode == 0 && t0 > 0 && (!state_S || !state_dec)) return -1;
+  const int64_t s = cfg->check_stride > 1 ? cfg->check_stride : 1;
+  if (cfg->check_stride < 0) return -1;
+  if (cfg->ref_mode == 0 && cfg->delta < 1) return -1;
+  if (cfg->ref_mode == 0 && cfg->delta % s != 0) return -1;
+  const int64_t D = oracle_history(cfg);  // history frames before t0
+  if (D > 0 && t0 > 0 && (!state_S || !state_dec)) return -1;
   // area sums of every frame of the window (history first)
   std::vector<int64_t> S((size_t)(D + n) * cells);
   for (int64_t k = 0; k < D; ++k) {
@@ -393,15 +412,29 @@ int64_t oracle_cascade(const oracle_cfg* cfg, const oracle_cnn_desc* net, const 
   const bool blocked = cfg->Gh * cfg->Gw > 1;
   std::vector<int64_t> Sc((size_t)cfg->Hc * cfg->Wc * 3);
   int64_t fired = 0;
+  const double nan = std::numeric_limits<double>::quiet_NaN();
   for (int64_t k = 0; k < n; ++k) {
     const int64_t t = t0 + k;
+    if (t % s != 0) {  // not checked: the output of the last checked frame
+      const uint8_t d = dec[(size_t)(D + k - t % s)];
+      dec[(size_t)(D + k)] = d;
+      if (score) score[k] = nan;
+      if (fire) fire[k] = 0;
+      if (logit) logit[k] = nan;
+      if (prob) prob[k] = nan;
+      if (lscale) lscale[k] = nan;
+      if (label) label[k] = d & 1;
+      if (defer) defer[k] = (d >> 1) & 1;
+      continue;
+    }
     const int64_t* cur = &S[(size_t)(D + k) * cells];
     double sc;
     const bool forced = cfg->ref_mode == 0 && t < cfg->delta;
     if (forced) {
       sc = std::numeric_limits<double>::infinity();
     } else {
-      const int64_t* ref = cfg->ref_mode == 0 ? &S[(size_t)k * cells] : cfg->ref_sums;
+      const int64_t* ref =
+          cfg->ref_mode == 0 ? &S[(size_t)(D + k - cfg->delta) * cells] : cfg->ref_sums;
       sc = blocked ? oracle_blocked_score(cur, ref, cfg->Ho, cfg->Wo, den, cfg->Gh, cfg->Gw,
                                           cfg->lr_w, cfg->lr_b, nullptr)
                    : oracle_global_mse(cur, ref, cfg->Ho, cfg->Wo, den, nullptr);
@@ -424,18 +457,16 @@ int64_t oracle_cascade(const oracle_cfg* cfg, const oracle_cnn_desc* net, const 
       if (logit) logit[k] = std::numeric_limits<double>::quiet_NaN();
       if (prob) prob[k] = std::numeric_limits<double>::quiet_NaN();
       if (lscale) lscale[k] = std::numeric_limits<double>::quiet_NaN();
-      d = cfg->ref_mode == 0 ? dec[(size_t)k] : 0;  // reuse the compared frame's output
+      d = cfg->ref_mode == 0 ? dec[(size_t)(D + k - cfg->delta)] : 0;  // the compared frame's output
     }
     dec[(size_t)(D + k)] = d;
     if (label) label[k] = d & 1;
     if (defer) defer[k] = (d >> 1) & 1;
   }
-  if (cfg->ref_mode == 0) {
-    for (int64_t k = 0; k < D; ++k) {
-      if (state_S_out)
-        std::memcpy(state_S_out + k * cells, &S[(size_t)(n + k) * cells], cells * sizeof(int64_t));
-      if (state_dec_out) state_dec_out[k] = dec[(size_t)(n + k)];
-    }
+  for (int64_t k = 0; k < D; ++k) {
+    if (state_S_out)
+      std::memcpy(state_S_out + k * cells, &S[(size_t)(n + k) * cells], cells * sizeof(int64_t));
+    if (state_dec_out) state_dec_out[k] = dec[(size_t)(n + k)];
   }
   return fired;
 }

@@ -32,6 +32,7 @@ class Workload:
     weight_seed: int = 1000
     lr_bias: float = -2.0
     chunk: Optional[int] = None
+    check_stride: int = 1          # frame skipping: check frames t with t mod s = 0
 
     def with_frames(self, n: int) -> "Workload":
         return dataclasses.replace(self, video=dataclasses.replace(self.video, n=n))

@@ -412,3 +412,101 @@ def test_fixed_reference_mode():
     nf = out["fire"] == 0
     assert (out["label"][nf] == 0).all() and (out["defer"][nf] == 0).all()
     assert np.isfinite(out["score"]).all()
+
+
+# ------------------------------------------------------------- frame skipping
+
+def _brute_skip(wl, blob, frames, s, ref=None):
+    """The cascade with check stride s in plain Python loops over the oracle's
+    per-frame primitives (area sums, MSE, CNN logit, decision rule)."""
+    n = len(frames)
+    den = oracle.area_den(wl.video.h, wl.video.w, wl.dd_h, wl.dd_w)
+    den_c = oracle.area_den(wl.video.h, wl.video.w, wl.cnn.in_h, wl.cnn.in_w)
+    S = [oracle.area_sums(f, wl.dd_h, wl.dd_w) for f in frames]
+    lab = np.zeros(n, np.uint8)
+    dfr = np.zeros(n, np.uint8)
+    fire = np.zeros(n, np.uint8)
+    for t in range(n):
+        if t % s:
+            lab[t], dfr[t] = lab[t - t % s], dfr[t - t % s]
+            continue
+        if wl.ref_mode == W.PREV:
+            score = math.inf if t < wl.delta else oracle.global_mse(S[t], S[t - wl.delta], den)[0]
+        else:
+            score = oracle.global_mse(S[t], ref, den)[0]
+        fire[t] = score > wl.delta_diff or (wl.ref_mode == W.PREV and t < wl.delta)
+        if fire[t]:
+            z = oracle.cnn_logit(wl.cnn, blob, oracle.area_sums(frames[t], wl.cnn.in_h, wl.cnn.in_w),
+                                 den_c)
+            d = oracle.decide(oracle.sigmoid(z), wl.c_low, wl.c_high)
+            lab[t], dfr[t] = d & 1, (d >> 1) & 1
+        elif wl.ref_mode == W.PREV:
+            lab[t], dfr[t] = lab[t - wl.delta], dfr[t - wl.delta]
+    return lab, dfr, fire
+
+
+@pytest.mark.parametrize("s,delta,ref_mode", [(3, 3, W.PREV), (4, 8, W.PREV), (5, 5, W.PREV),
+                                              (4, 1, W.FIXED)])
+def test_skipping_brute_force(s, delta, ref_mode):
+    wl = _tiny_fast(delta=delta, ref_mode=ref_mode, c_low=0.45, c_high=0.55, check_stride=s)
+    if ref_mode == W.FIXED:  # the reference is a noisy frame: a threshold at the noise level
+        wl = wl.replace(delta_diff=4.4)
+    v, blob = _small(wl, 200)
+    frames = v.frames(150, 350)
+    ref = oracle.area_sums(frames[7], wl.dd_h, wl.dd_w) if ref_mode == W.FIXED else None
+    cfg, keep = oracle.make_cfg(wl, ref_sums=ref)
+    out, _ = oracle.cascade(cfg, wl.cnn, blob, frames)
+    lab, dfr, fire = _brute_skip(wl, blob, frames, s, ref)
+    assert (out["fire"] == fire).all() and (out["label"] == lab).all() and (out["defer"] == dfr).all()
+    unchecked = np.arange(len(frames)) % s != 0
+    assert np.isnan(out["score"][unchecked]).all() and np.isnan(out["logit"][unchecked]).all()
+    assert np.isfinite(out["score"][~unchecked][delta if ref_mode == W.PREV else 0:]).all()
+    assert fire.sum() > 0 and (fire[~unchecked] == 0).sum() > 0  # both branches exercised
+
+
+@pytest.mark.parametrize("s,delta", [(3, 6), (2, 2)])
+def test_skipping_equals_subsampled_video(s, delta):
+    # checking every s-th frame is the cascade on the subsampled video (delta / s
+    # checked frames back) with each skip block taking its checked frame's output
+    wl = _tiny_fast(delta=delta, c_low=0.45, c_high=0.55, check_stride=s)
+    v, blob = _small(wl, 200)
+    frames = v.frames(120, 360)
+    cfg, keep = oracle.make_cfg(wl)
+    out, _ = oracle.cascade(cfg, wl.cnn, blob, frames)
+    sub_wl = wl.replace(delta=delta // s, check_stride=1)
+    cfg2, keep2 = oracle.make_cfg(sub_wl)
+    sub, _ = oracle.cascade(cfg2, wl.cnn, blob, frames[::s])
+    blk = np.arange(len(frames)) // s
+    for k in ("label", "defer"):
+        assert (out[k] == sub[k][blk]).all()
+    for k in ("fire", "score", "logit"):
+        np.testing.assert_array_equal(out[k][::s], sub[k])
+
+
+def test_skipping_chunk_invariance():
+    wl = _tiny_fast(delta=6, c_low=0.45, c_high=0.55, check_stride=3)
+    v, blob = _small(wl, 200)
+    frames = v.frames(150, 400)
+    cfg, keep = oracle.make_cfg(wl)
+    full, _ = oracle.cascade(cfg, wl.cnn, blob, frames)
+    parts, state, t0 = [], None, 0
+    for size in (37, 3, 1, 2, 100, 107):   # boundaries inside skip blocks
+        o, state = oracle.cascade(cfg, wl.cnn, blob, frames[t0:t0 + size], t0=t0, state=state)
+        parts.append(o)
+        t0 += size
+    for k in ("fire", "label", "defer"):
+        assert (np.concatenate([p[k] for p in parts]) == full[k]).all()
+    np.testing.assert_array_equal(np.concatenate([p["score"] for p in parts]), full["score"])
+
+
+def test_skipping_stride_one_and_bad_delta():
+    wl = _tiny_fast(delta=2, c_low=0.45, c_high=0.55)
+    v, blob = _small(wl, 200)
+    frames = v.frames(150, 230)
+    a, _ = oracle.cascade(oracle.make_cfg(wl)[0], wl.cnn, blob, frames)
+    for s in (0, 1):
+        b, _ = oracle.cascade(oracle.make_cfg(wl.replace(check_stride=s))[0], wl.cnn, blob, frames)
+        for k in ("fire", "label", "defer", "score"):
+            np.testing.assert_array_equal(a[k], b[k])
+    with pytest.raises(ValueError):   # reading: delta must be a multiple of the stride
+        oracle.cascade(oracle.make_cfg(wl.replace(check_stride=3))[0], wl.cnn, blob, frames)
