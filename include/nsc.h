@@ -60,7 +60,7 @@ typedef enum nsc_status {
 
 enum { NSC_REF_PREV = 0, NSC_REF_FIXED = 1 };
 enum { NSC_F32 = 0, NSC_BF16 = 1 };
-enum { NSC_MAX_CONV = 8, NSC_MAX_DELTA = 256, NSC_MAX_BLOCKS = 1024 };
+enum { NSC_MAX_CONV = 8, NSC_MAX_DELTA = 256, NSC_MAX_BLOCKS = 1024, NSC_MAX_STRIDE = 4096 };
 
 /* Stage boundaries at which nsc_cascade_run records optional events:
  * [0] start, [1] after the area sums, [2] after the detector, [3] after the
@@ -84,6 +84,13 @@ typedef struct nsc_cascade_cfg {
                                 nsc_downsample                                   */
   double delta_diff;         /* fire iff metric > delta_diff                      */
   double c_low, c_high;      /* 0 <= c_low <= c_high <= 1                         */
+  int32_t check_stride;      /* frame skipping (Sec. 5, t_skip in frames): only
+                                frames with absolute index t mod s = 0 are
+                                checked; a frame in between keeps the output
+                                of the last checked frame.  0 or 1: every frame;
+                                at most NSC_MAX_STRIDE; PREV needs delta to be
+                                a multiple of s (the compared frame is then a
+                                checked one)                                   */
 } nsc_cascade_cfg;
 
 /* Shape of a specialized CNN (Sec. 4): n_conv x [conv3x3 'same' + bias + ReLU
@@ -158,7 +165,8 @@ int nsc_cnn_destroy(nsc_cnn* cnn);
 int nsc_cascade_workspace_bytes(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn,
                                 int64_t max_frames, size_t* bytes);
 /* State carried between consecutive nsc_cascade_run calls on one stream
- * (PREV mode: area sums and decisions of the last `delta` frames). */
+ * (PREV mode: area sums and decisions of the last `delta` frames, counted in
+ * checked frames; with frame skipping also the last checked frame's output). */
 int nsc_state_bytes(const nsc_cascade_cfg* cfg, size_t* bytes);
 /* Workspace of nsc_compact for n flags. */
 int nsc_compact_workspace_bytes(int64_t n, size_t* bytes);
@@ -218,7 +226,11 @@ int nsc_specialized_cnn(const nsc_cnn* cnn, const int32_t* sums, int32_t sums_h,
  * defer_out (device, n bytes each; a deferred frame has label 0).  state
  * (device, nsc_state_bytes) carries the last delta frames between calls: with
  * t0 = 0 its content is ignored; with t0 > 0 it must hold what the previous
- * call (ending at frame t0) left.  ws: nsc_cascade_workspace_bytes(cfg, cnn,
+ * call (ending at frame t0) left.  With check_stride s > 1 only the checked
+ * frames (t mod s = 0) are read and run through steps 1-4 (the cascade on the
+ * subsampled video, delta / s checked frames back), and every frame then takes
+ * its checked frame's output: frames between checks get score NaN, fire 0 and
+ * logit NaN in `outs`; state is required (it holds the last checked output).  ws: nsc_cascade_workspace_bytes(cfg, cnn,
  * >= n).  outs (host struct of device pointers) and stats (host) are nullable;
  * stats synchronises the stream.  stage_events (host array of
  * NSC_STAGE_EVENTS hipEvent_t, nullable, entries nullable) are recorded on

@@ -81,6 +81,14 @@ int check_cfg(const nsc_cascade_cfg* c) {
   NSC_REQUIRE(!isnan(c->c_low) && !isnan(c->c_high) && c->c_low >= 0.0 && c->c_high <= 1.0 &&
                   c->c_low <= c->c_high,
               NSC_E_INVAL, "need 0 <= c_low (%g) <= c_high (%g) <= 1", c->c_low, c->c_high);
+  NSC_REQUIRE(c->check_stride >= 0 && c->check_stride <= NSC_MAX_STRIDE, NSC_E_INVAL,
+              "check_stride %d outside 0..%d", c->check_stride, NSC_MAX_STRIDE);
+  if (c->ref_mode == NSC_REF_PREV && c->check_stride > 1)
+    NSC_REQUIRE(c->delta % c->check_stride == 0, NSC_E_INVAL,
+                "delta %d must be a multiple of check_stride %d (the compared frame is a checked "
+                "one)", c->delta, c->check_stride);
+  NSC_REQUIRE(c->frame_stride <= ((int64_t)1 << 62) / (c->check_stride > 1 ? c->check_stride : 1),
+              NSC_E_INVAL, "frame_stride x check_stride overflows");
   // exact int64 squared-difference sums
   const double emax = (255.0 * (double)den) * (255.0 * (double)den) * (double)c->dd_h * c->dd_w * 3;
   NSC_REQUIRE(emax < 9.0e18, NSC_E_SHAPE, "squared-difference sums may overflow 64 bits");
@@ -158,13 +166,40 @@ uint16_t host_bf16(float f) {
   return (uint16_t)(u >> 16);
 }
 
-// Workspace layout of nsc_cascade_run.
+// Frame skipping: the checked frames of a stream form a video of their own
+// (every s-th frame, frames s * frame_stride bytes apart, delta / s checked
+// frames back); the cascade runs on it unchanged.
+int32_t stride_of(const nsc_cascade_cfg* c) { return c->check_stride > 1 ? c->check_stride : 1; }
+
+nsc_cascade_cfg checked_cfg(const nsc_cascade_cfg* c) {
+  nsc_cascade_cfg k = *c;
+  const int32_t s = stride_of(c);
+  k.frame_stride = c->frame_stride * s;
+  if (c->ref_mode == NSC_REF_PREV) k.delta = c->delta / s;
+  k.check_stride = 1;
+  return k;
+}
+
+// Checked frames among [t0, t0 + n): absolute checked indices [k0, k0 + nc).
+void checked_range(int64_t t0, int64_t n, int32_t s, int64_t* k0, int64_t* nc) {
+  *k0 = (t0 + s - 1) / s;
+  *nc = (t0 + n + s - 1) / s - *k0;
+}
+
+// Workspace layout of nsc_cascade_run (of the checked-frame cascade, plus the
+// checked frames' outputs before they are spread over their skip blocks).
 struct RunLayout {
-  size_t sums, fire, dec, idx, count, tiles, tile_last, carry, logit, scratch, cnn, total;
+  size_t sums, fire, dec, idx, count, tiles, tile_last, carry, logit, scratch, cnn;
+  size_t sk_label, sk_defer, sk_fire, sk_score, sk_logit;
+  size_t total;
 };
 
-RunLayout run_layout(const nsc_cascade_cfg* c, const Cnn& cnn, int64_t n) {
+RunLayout run_layout(const nsc_cascade_cfg* c0, const Cnn& cnn, int64_t n_frames) {
   RunLayout L{};
+  const nsc_cascade_cfg kc = checked_cfg(c0);
+  const nsc_cascade_cfg* c = &kc;
+  const int32_t s = stride_of(c0);
+  const int64_t n = s > 1 ? n_frames / s + 1 : n_frames;  // checked frames of any window
   const size_t cells = (size_t)c->dd_h * c->dd_w * 3;
   const ResolvePlan rp = make_resolve_plan(n, 0, c->ref_mode == NSC_REF_PREV ? c->delta : 1);
   size_t o = 0;
@@ -184,17 +219,31 @@ RunLayout run_layout(const nsc_cascade_cfg* c, const Cnn& cnn, int64_t n) {
   L.logit = take((size_t)n * 4);
   const size_t dmax = c->ref_mode == NSC_REF_PREV ? (size_t)c->delta : 1;
   L.scratch = take(dmax * cells * 4 + dmax);
+  if (s > 1) {
+    L.sk_label = take((size_t)n);
+    L.sk_defer = take((size_t)n);
+    L.sk_fire = take((size_t)n);
+    L.sk_score = take((size_t)n * 8);
+    L.sk_logit = take((size_t)n * 4);
+  }
   L.cnn = take(cnn_workspace_bytes(cnn, n));
   L.total = o;
   return L;
 }
 
-size_t state_layout_bytes(const nsc_cascade_cfg* c, size_t* sums_off, size_t* dec_off) {
+// State: sums and decisions of the last delta checked frames (PREV), then,
+// with frame skipping, one byte with the last checked frame's decision.
+size_t state_layout_bytes(const nsc_cascade_cfg* c0, size_t* sums_off, size_t* dec_off,
+                          size_t* last_off = nullptr) {
+  const nsc_cascade_cfg kc = checked_cfg(c0);
+  const nsc_cascade_cfg* c = &kc;
   const size_t cells = (size_t)c->dd_h * c->dd_w * 3;
   const size_t d = c->ref_mode == NSC_REF_PREV ? (size_t)c->delta : 0;
   if (sums_off) *sums_off = 0;
   if (dec_off) *dec_off = align_up(d * cells * 4, kAlign);
-  return align_up(d * cells * 4, kAlign) + align_up(d > 0 ? d : 1, kAlign);
+  const size_t core = align_up(d * cells * 4, kAlign) + align_up(d > 0 ? d : 1, kAlign);
+  if (last_off) *last_off = core;
+  return core + (stride_of(c0) > 1 ? kAlign : 0);
 }
 
 }  // namespace
@@ -477,38 +526,21 @@ int nsc_specialized_cnn(const nsc_cnn* cnn, const int32_t* sums, int32_t sums_h,
   return run_cnn(c, r, ws, ws_bytes, (hipStream_t)stream);
 }
 
-int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_t* frames,
-                    int64_t n, int64_t t0, void* state, void* ws, size_t ws_bytes,
-                    uint8_t* label_out, uint8_t* defer_out, const nsc_frame_outputs* outs,
-                    nsc_run_stats* stats, void* const* stage_events, void* stream) {
-  g_err[0] = 0;
-  if (int rc = check_cfg(cfg)) return rc;
-  NSC_REQUIRE(cnn != nullptr, NSC_E_INVAL, "cnn is NULL");
-  auto mark = [&](int k) -> int {
-    if (stage_events && stage_events[k])
-      NSC_TRY_HIP(hipEventRecord((hipEvent_t)stage_events[k], (hipStream_t)stream));
-    return NSC_OK;
-  };
-  const Cnn& c = cnn->c;
-  NSC_REQUIRE(c.desc.in_h == cfg->cnn_h && c.desc.in_w == cfg->cnn_w, NSC_E_SHAPE,
-              "CNN input %dx%d differs from the configured %dx%d", c.desc.in_h, c.desc.in_w,
-              cfg->cnn_h, cfg->cnn_w);
-  NSC_REQUIRE(n >= 0 && n <= kMaxFrames && t0 >= 0, NSC_E_INVAL, "n or t0 out of range");
+}  // extern "C"
+
+namespace nsc {
+namespace {
+
+// Steps 1-5 on frames [t0, t0 + n) of a configuration without frame skipping
+// (the checked frames); records stage events 0..4 through `mark`.
+template <class Mark>
+int run_checked(const nsc_cascade_cfg* cfg, const Cnn& c, const uint8_t* frames, int64_t n,
+                int64_t t0, void* state, unsigned char* w, const RunLayout& L, uint8_t* label_out,
+                uint8_t* defer_out, double* score_out, uint8_t* fire_out, float* logit_out,
+                hipStream_t st, Mark&& mark) {
   const bool prev = cfg->ref_mode == NSC_REF_PREV;
-  if (n == 0) {
-    if (stats) *stats = nsc_run_stats{0, 0, 0, 0};
-    return NSC_OK;
-  }
-  NSC_REQUIRE(frames && label_out && defer_out, NSC_E_INVAL, "frames, label_out or defer_out is NULL");
-  NSC_REQUIRE(!(prev && state == nullptr), NSC_E_STATE, "earlier-frame mode needs a state buffer");
-  const RunLayout L = run_layout(cfg, c, n);
-  NSC_REQUIRE(ws != nullptr && ((uintptr_t)ws % kAlign) == 0 && ws_bytes >= L.total,
-              NSC_E_WORKSPACE, "workspace needs %zu bytes (256-byte aligned), got %zu", L.total,
-              ws_bytes);
-  const hipStream_t st = (hipStream_t)stream;
-  unsigned char* w = static_cast<unsigned char*>(ws);
   int32_t* sums = reinterpret_cast<int32_t*>(w + L.sums);
-  uint8_t* fire = outs && outs->fire ? outs->fire : w + L.fire;
+  uint8_t* fire = fire_out ? fire_out : w + L.fire;
   uint8_t* dec = w + L.dec;
   int32_t* idx = reinterpret_cast<int32_t*>(w + L.idx);
   int32_t* count = reinterpret_cast<int32_t*>(w + L.count);
@@ -545,7 +577,7 @@ int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_
     a.grid_w = cfg->grid_w;
     a.ref_mode = cfg->ref_mode;
     a.delta = prev ? cfg->delta : 0;
-    a.score = outs ? outs->score : nullptr;
+    a.score = score_out;
     a.fire = fire;
     if (int rc = launch_diff(a, st)) return rc;
   }
@@ -555,8 +587,8 @@ int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_
     return rc;
   if (int rc = mark(3)) return rc;
   // 4: CNN on survivors with decisions written at their frame positions
-  if (outs && outs->logit)
-    if (int rc = launch_fill_nan(outs->logit, n, st)) return rc;
+  if (logit_out)
+    if (int rc = launch_fill_nan(logit_out, n, st)) return rc;
   CnnRunArgs r{};
   r.sums = sums;
   r.sums_h = cfg->dd_h;
@@ -572,7 +604,7 @@ int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_
   r.dec = dec;
   r.c_low = cfg->c_low;
   r.c_high = cfg->c_high;
-  r.frame_logit = outs ? outs->logit : nullptr;
+  r.frame_logit = logit_out;
   if (int rc = run_cnn(c, r, w + L.cnn, L.total - L.cnn, st)) return rc;
   if (int rc = mark(4)) return rc;
   // 5: decisions of frames that did not fire
@@ -585,6 +617,96 @@ int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_
     if (int rc = launch_state_update(sums, label_out, defer_out, n, cfg->delta, cells, st_sums,
                                      st_dec, w + L.scratch, st))
       return rc;
+  return NSC_OK;
+}
+
+}  // namespace
+}  // namespace nsc
+
+extern "C" {
+
+int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_t* frames,
+                    int64_t n, int64_t t0, void* state, void* ws, size_t ws_bytes,
+                    uint8_t* label_out, uint8_t* defer_out, const nsc_frame_outputs* outs,
+                    nsc_run_stats* stats, void* const* stage_events, void* stream) {
+  g_err[0] = 0;
+  if (int rc = check_cfg(cfg)) return rc;
+  NSC_REQUIRE(cnn != nullptr, NSC_E_INVAL, "cnn is NULL");
+  auto mark = [&](int k) -> int {
+    if (stage_events && stage_events[k])
+      NSC_TRY_HIP(hipEventRecord((hipEvent_t)stage_events[k], (hipStream_t)stream));
+    return NSC_OK;
+  };
+  const Cnn& c = cnn->c;
+  NSC_REQUIRE(c.desc.in_h == cfg->cnn_h && c.desc.in_w == cfg->cnn_w, NSC_E_SHAPE,
+              "CNN input %dx%d differs from the configured %dx%d", c.desc.in_h, c.desc.in_w,
+              cfg->cnn_h, cfg->cnn_w);
+  NSC_REQUIRE(n >= 0 && n <= kMaxFrames && t0 >= 0, NSC_E_INVAL, "n or t0 out of range");
+  const bool prev = cfg->ref_mode == NSC_REF_PREV;
+  const int32_t s = stride_of(cfg);
+  if (n == 0) {
+    if (stats) *stats = nsc_run_stats{0, 0, 0, 0};
+    return NSC_OK;
+  }
+  NSC_REQUIRE(frames && label_out && defer_out, NSC_E_INVAL, "frames, label_out or defer_out is NULL");
+  NSC_REQUIRE(!(prev && state == nullptr), NSC_E_STATE, "earlier-frame mode needs a state buffer");
+  NSC_REQUIRE(!(s > 1 && state == nullptr), NSC_E_STATE, "frame skipping needs a state buffer");
+  const RunLayout L = run_layout(cfg, c, n);
+  NSC_REQUIRE(ws != nullptr && ((uintptr_t)ws % kAlign) == 0 && ws_bytes >= L.total,
+              NSC_E_WORKSPACE, "workspace needs %zu bytes (256-byte aligned), got %zu", L.total,
+              ws_bytes);
+  const hipStream_t st = (hipStream_t)stream;
+  unsigned char* w = static_cast<unsigned char*>(ws);
+  int32_t* count = reinterpret_cast<int32_t*>(w + L.count);
+  size_t last_off = 0;
+  state_layout_bytes(cfg, nullptr, nullptr, &last_off);
+
+  if (s == 1) {
+    if (int rc = run_checked(cfg, c, frames, n, t0, state, w, L, label_out, defer_out,
+                             outs ? outs->score : nullptr, outs ? outs->fire : nullptr,
+                             outs ? outs->logit : nullptr, st, mark))
+      return rc;
+  } else {
+    // the checked frames [k0, k0 + nc) as a video of their own, then every frame
+    // takes the output of its checked frame
+    const nsc_cascade_cfg kc = checked_cfg(cfg);
+    int64_t k0, nc;
+    checked_range(t0, n, s, &k0, &nc);
+    uint8_t* k_label = w + L.sk_label;
+    uint8_t* k_defer = w + L.sk_defer;
+    uint8_t* k_fire = w + L.sk_fire;
+    double* k_score = reinterpret_cast<double*>(w + L.sk_score);
+    float* k_logit = reinterpret_cast<float*>(w + L.sk_logit);
+    if (nc > 0) {
+      const uint8_t* kf = frames + (k0 * s - t0) * cfg->frame_stride;
+      if (int rc = run_checked(&kc, c, kf, nc, k0, state, w, L, k_label, k_defer, k_score, k_fire,
+                               k_logit, st, mark))
+        return rc;
+    } else {
+      for (int k = 0; k < 5; ++k)
+        if (int rc = mark(k)) return rc;
+      if (int rc = launch_set_i32(count, 0, st)) return rc;
+    }
+    uint8_t* last = static_cast<uint8_t*>(state) + last_off;
+    SkipExpand e{};
+    e.n = n;
+    e.t0 = t0;
+    e.s = s;
+    e.k0 = k0;
+    e.nc = nc;
+    e.k_label = k_label;
+    e.k_defer = k_defer;
+    e.k_score = k_score;
+    e.k_fire = k_fire;
+    e.k_logit = k_logit;
+    e.last = last;
+    e.label = label_out;
+    e.defer = defer_out;
+    e.score = outs ? outs->score : nullptr;
+    e.fire = outs ? outs->fire : nullptr;
+    e.logit = outs ? outs->logit : nullptr;
+    if (int rc = launch_skip_expand(e, st)) return rc;
+  }
   if (int rc = mark(5)) return rc;
   if (stats) {
     std::vector<uint8_t> hl(n), hd(n);
@@ -593,12 +715,12 @@ int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_
     NSC_TRY_HIP(hipMemcpyAsync(hd.data(), defer_out, n, hipMemcpyDeviceToHost, st));
     NSC_TRY_HIP(hipMemcpyAsync(&hc, count, 4, hipMemcpyDeviceToHost, st));
     NSC_TRY_HIP(hipStreamSynchronize(st));
-    nsc_run_stats s{n, hc, 0, 0};
+    nsc_run_stats r{n, hc, 0, 0};
     for (int64_t i = 0; i < n; ++i) {
-      s.positive += hl[i] && !hd[i];
-      s.deferred += hd[i];
+      r.positive += hl[i] && !hd[i];
+      r.deferred += hd[i];
     }
-    *stats = s;
+    *stats = r;
   }
   return NSC_OK;
 }

@@ -186,6 +186,35 @@ __global__ void __launch_bounds__(256) k_state_update(const int32_t* __restrict_
   }
 }
 
+// Frame skipping (Sec. 5): each frame takes its checked frame's output.
+__global__ void __launch_bounds__(256) k_skip_expand(SkipExpand e) {
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < e.n;
+       u += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t t = e.t0 + u;
+    const int64_t k = t / e.s;
+    const bool checked = k * e.s == t;  // then k >= k0
+    uint8_t l, d;
+    if (k >= e.k0) {
+      l = e.k_label[k - e.k0];
+      d = e.k_defer[k - e.k0];
+    } else {
+      const uint8_t v = *e.last;
+      l = v & 1;
+      d = (v >> 1) & 1;
+    }
+    e.label[u] = l;
+    e.defer[u] = d;
+    if (e.score) e.score[u] = checked ? e.k_score[k - e.k0] : __builtin_nan("");
+    if (e.fire) e.fire[u] = checked ? e.k_fire[k - e.k0] : 0;
+    if (e.logit) e.logit[u] = checked ? e.k_logit[k - e.k0] : __builtin_nanf("");
+  }
+}
+
+__global__ void k_skip_last(const uint8_t* __restrict__ label, const uint8_t* __restrict__ defer,
+                            int64_t nc, uint8_t* __restrict__ last) {
+  if (threadIdx.x == 0) *last = (uint8_t)(label[nc - 1] | (defer[nc - 1] << 1));
+}
+
 __global__ void __launch_bounds__(256) k_copy_u8(const uint8_t* __restrict__ s,
                                                  uint8_t* __restrict__ d, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
@@ -286,6 +315,24 @@ int launch_state_update(const int32_t* sums, const uint8_t* label, const uint8_t
                      stream, sums, label, defer, n, delta, cells, old_sums, old_dec, state_sums,
                      state_dec);
   NSC_CHECK_LAUNCH("k_state_update");
+  return NSC_OK;
+}
+
+int launch_set_i32(int32_t* p, int32_t v, hipStream_t stream) {
+  hipLaunchKernelGGL(k_set_i32, dim3(1), dim3(1), 0, stream, p, v);
+  NSC_CHECK_LAUNCH("k_set_i32");
+  return NSC_OK;
+}
+
+int launch_skip_expand(const SkipExpand& e, hipStream_t stream) {
+  if (e.n <= 0) return NSC_OK;
+  hipLaunchKernelGGL(k_skip_expand, dim3(grid_for(e.n, 256)), dim3(256), 0, stream, e);
+  NSC_CHECK_LAUNCH("k_skip_expand");
+  if (e.nc > 0) {  // after every reader of the previous value
+    hipLaunchKernelGGL(k_skip_last, dim3(1), dim3(64), 0, stream, e.k_label, e.k_defer, e.nc,
+                       e.last);
+    NSC_CHECK_LAUNCH("k_skip_last");
+  }
   return NSC_OK;
 }
 

@@ -108,6 +108,30 @@ int launch_state_update(const int32_t* sums, const uint8_t* label, const uint8_t
                         int32_t delta, int64_t cells, int32_t* state_sums, uint8_t* state_dec,
                         void* scratch, hipStream_t stream);
 int launch_fill_nan(float* p, int64_t n, hipStream_t stream);
+int launch_set_i32(int32_t* p, int32_t v, hipStream_t stream);
+
+// Frame skipping: frames [t0, t0+n) take the outputs of their checked frame
+// floor(t / s) * s.  Checked frames [k0, k0+nc) (absolute checked indices)
+// have their outputs in k_*; frames before the first of them take `last`
+// (label | defer << 1 of the previous call's last checked frame), which is
+// then replaced by this call's last checked decision.  Per-frame outputs
+// (nullable) of frames between checks: score NaN, fire 0, logit NaN.
+struct SkipExpand {
+  int64_t n, t0, k0, nc;
+  int32_t s;
+  const uint8_t* k_label;
+  const uint8_t* k_defer;
+  const double* k_score;
+  const uint8_t* k_fire;
+  const float* k_logit;
+  uint8_t* last;
+  uint8_t* label;
+  uint8_t* defer;
+  double* score;
+  uint8_t* fire;
+  float* logit;
+};
+int launch_skip_expand(const SkipExpand& e, hipStream_t stream);
 int launch_copy_u8(const uint8_t* src, uint8_t* dst, int64_t n, hipStream_t stream);
 
 // Specialized CNN.

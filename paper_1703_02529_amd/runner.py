@@ -3,7 +3,8 @@
 Allocates (through torch) the workspace, the carried state and the per-frame
 output buffers, creates the CNN handle, and calls nsc_cascade_run.  It reads a
 workload description by attribute (video.h, video.w, dd_h, dd_w, cnn, ref_mode,
-delta, grid, delta_diff, c_low, c_high, lr_bias) and imports nothing else.
+delta, grid, delta_diff, c_low, c_high, lr_bias, check_stride if present) and
+imports nothing else.
 """
 from __future__ import annotations
 
@@ -26,7 +27,8 @@ class CascadeRunner:
                             cnn_h=wl.cnn.in_h, cnn_w=wl.cnn.in_w, ref_mode=wl.ref_mode,
                             delta=wl.delta, grid=tuple(wl.grid), lr_w=lr_w, lr_b=wl.lr_bias,
                             ref_sums=ref_sums, delta_diff=wl.delta_diff, c_low=wl.c_low,
-                            c_high=wl.c_high, frame_stride=frame_stride)
+                            c_high=wl.c_high, frame_stride=frame_stride,
+                            check_stride=getattr(wl, "check_stride", 1))
         self.desc = make_desc(wl.cnn.conv, wl.cnn.pool, wl.cnn.dense, wl.cnn.in_h, wl.cnn.in_w,
                               wl.cnn.bf16)
         self.cnn = Cnn(self.desc, blob)

@@ -62,10 +62,25 @@ def test_valid_configs_pass():
     (dict(c_low=0.9, c_high=0.1), -1),
     (dict(c_low=-0.1), -1),
     (dict(c_high=1.5), -1),
+    (dict(check_stride=-1), -1),
+    (dict(check_stride=4097), -1),
+    (dict(check_stride=4), -1),           # delta 15 is not a multiple of the stride
 ])
 def test_invalid_configs(kw, code):
     assert nsc.nsc_cfg_check(_cfg(**kw)) == code
     assert nsc.last_error() != ""
+
+
+def test_frame_skipping_sizes():
+    # stride 0 and 1 mean every frame; a stride that divides delta is valid
+    assert nsc.nsc_cfg_check(_cfg(check_stride=0)) == 0
+    assert nsc.nsc_cfg_check(_cfg(check_stride=5)) == 0
+    assert nsc.nsc_cfg_check(_cfg(ref_mode=1, check_stride=7, delta=1)) == -1  # no ref_sums
+    base = nsc.nsc_state_bytes(_cfg())
+    # delta / s = 3 checked frames of sums instead of 15, plus one decision byte
+    skip = nsc.nsc_state_bytes(_cfg(check_stride=5))
+    assert skip < base
+    assert skip == nsc.nsc_state_bytes(_cfg(delta=3)) + 256
 
 
 def test_frame_stride_and_overflow_limits():

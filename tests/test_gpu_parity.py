@@ -456,3 +456,49 @@ def test_streamed_chunks_equal_one_shot():
     ts = [0, 29, 30, 511, 512, 541, 1024 + 13, n - 1]
     check_samples(wl, v, blob, lr, None, g, ts)
     torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------- frame skipping
+
+@pytest.mark.parametrize("s,delta,ref_mode", [(3, 3, W.PREV), (4, 8, W.PREV), (5, 1, W.FIXED)])
+def test_skipping_tiny_full_video(s, delta, ref_mode):
+    wl = W.TINY.replace(check_stride=s, delta=delta, ref_mode=ref_mode)
+    rep = _run_and_compare(wl, wl.video.n)
+    assert rep["fired"] > 10
+    print(rep)
+    # chunk boundaries inside skip blocks, a chunk with no checked frame
+    rep = _run_and_compare(wl, 400, chunks=[101, 2, 1, 97, 199])
+    print(rep)
+
+
+def test_skipping_vga_window():
+    # the benchmark configuration checking every 5th frame (delta 15 = 3 checks back)
+    wl = W.VGA.replace(check_stride=5)
+    t0 = _first_occupied(wl, 40)
+    rep = _run_and_compare_from_zero_window(wl, t0, 160)
+    assert rep["fired"] > 0
+    print(rep)
+
+
+def test_skipping_streamed_equals_one_shot():
+    wl = W.HD_BLOCKED.with_frames(1300).replace(delta=2, check_stride=2)
+    n, fb = wl.video.n, wl.video.frame_bytes
+    v, blob, lr, _ = _prepare(wl, 0, n)
+    lr_d = _dev(lr)
+    tables = v.device_tables(DEV)
+    frames = torch.empty(n * fb, dtype=torch.uint8, device=DEV)
+    v.render_device(frames, 0, n, tables)
+    one = CascadeRunner(wl, blob, max_frames=n, lr_w=lr_d)
+    one.run(frames, n, t0=0)
+    keys = ("score", "fire", "logit", "label", "defer")
+    ref = {k: getattr(one, k)[:n].cpu().numpy().copy() for k in keys}
+    one.close()
+    del frames
+    out = {k: torch.full((n,), 77, dtype=getattr(one, k).dtype, device=DEV) for k in keys}
+    sc = StreamingCascade(wl, blob, 301, lr_w=lr_d)   # odd chunks: boundaries inside skip blocks
+    sc.run(n, lambda buf, t0, m, st: v.render_device(buf, t0, m, tables, stream=st), **out)
+    sc.close()
+    g = {k: out[k].cpu().numpy() for k in keys}
+    for k in keys:
+        assert np.array_equal(np.nan_to_num(g[k], nan=-7), np.nan_to_num(ref[k], nan=-7)), k
+    check_samples(wl, v, blob, lr, None, g, [0, 1, 2, 301, 302, 603, 1299])
