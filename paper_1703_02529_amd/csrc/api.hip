@@ -342,9 +342,26 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
   std::vector<float> w2(p, p + c.dense);
   p += c.dense;
   c.b2 = *p;
-  // device image: [conv_w][conv_b][w1][b1][w2]
+  // bf16: the conv weights again in MFMA fragment order (see CnnLayer)
+  std::vector<float> convwf(c.bf16 ? conv_elems : 0, 0.0f);
+  if (c.bf16) {
+    for (int l = 0; l < c.n_layers; ++l) {
+      const CnnLayer& L = c.layers[l];
+      const int nts = L.cout / 16, kst = L.kpad / 32;
+      for (int ks = 0; ks < kst; ++ks)
+        for (int nt = 0; nt < nts; ++nt)
+          for (int lane = 0; lane < 64; ++lane)
+            for (int e = 0; e < 8; ++e) {
+              const int o = nt * 16 + (lane & 15), k = ks * 32 + (lane >> 4) * 8 + e;
+              convwf[L.w_off + (((size_t)ks * nts + nt) * 64 + lane) * 8 + e] =
+                  convw[L.w_off + (size_t)o * L.kpad + k];
+            }
+    }
+  }
+  // device image: [conv_w][conv_wf][conv_b][w1][b1][w2]
   const size_t o_cw = 0;
-  const size_t o_cb = align_up(o_cw + conv_elems * es, kAlign);
+  const size_t o_cwf = align_up(o_cw + conv_elems * es, kAlign);
+  const size_t o_cb = align_up(o_cwf + convwf.size() * es, kAlign);
   const size_t o_w1 = align_up(o_cb + bias_elems * 4, kAlign);
   const size_t o_b1 = align_up(o_w1 + w1.size() * es, kAlign);
   const size_t o_w2 = align_up(o_b1 + (size_t)c.dense * 4, kAlign);
@@ -359,6 +376,7 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
     }
   };
   put(o_cw, convw, c.bf16);
+  if (c.bf16) put(o_cwf, convwf, true);
   put(o_cb, convb, false);
   put(o_w1, w1, c.bf16);
   put(o_b1, b1, false);
@@ -373,6 +391,7 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
   unsigned char* b = static_cast<unsigned char*>(dev);
   c.dev = dev;
   c.conv_w = b + o_cw;
+  c.conv_wf = c.bf16 ? b + o_cwf : nullptr;
   c.conv_b = reinterpret_cast<float*>(b + o_cb);
   c.w1 = b + o_w1;
   c.b1 = reinterpret_cast<float*>(b + o_b1);

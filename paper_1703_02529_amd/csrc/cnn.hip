@@ -634,6 +634,389 @@ __global__ void __launch_bounds__(1024) k_conv_pair(ConvArgs a0, ConvArgs a1, Pa
   }
 }
 
+// ------------------------------------------- 64-input-channel bf16 layers
+//
+// A layer with 64 input channels (bf16 network) keeps its weights in global
+// memory in fragment order (L2-resident, shared by every CU) and loads them
+// straight into registers, one K step ahead of their use; the LDS holds only
+// a band of the layer's input: the rows of band_tiles tile rows (4 output
+// rows each) plus one halo row above and below, every column of the image,
+// as bf16 hi and lo planes.  Each pixel's 64 channels are 8 chunks of 16
+// bytes, chunk c stored at position c ^ ((x + 4 r) & 7) for band row r and
+// column x: the 8 pixels (two rows by four columns of a 4x4 tile) that 8
+// lanes of one fragment read then fall on 8 distinct 16-byte bank groups.
+// Pixels outside the image read a zero pixel at the end of each plane, so no
+// halo is stored.  Without weights in LDS two workgroups fit on a CU, and one
+// stages while the other computes.
+//
+// The MFMA runs transposed: A = 16 output channels x 32 K of the weights,
+// B = 32 K x the 16 pixels of a 4x4 tile.  Lane (m, g) then holds channels
+// 16 nt + 4 g .. 16 nt + 4 g + 3 of pixel m, so a pooled output is a max over
+// the four lanes of one pooling window and every store is 16 bytes.
+
+constexpr int kBandWaves = 4;  // waves per workgroup of the banded kernels
+
+struct Band64 {
+  int32_t w, h;      // layer input grid
+  int32_t rows;      // staged rows of a band: 4 * band_tiles + 2
+  int32_t zp;        // pixel index of the zero pixel: rows * w
+  int32_t lo_plane;  // elements from the hi plane to the lo plane: (zp + 1) * 64
+};
+
+__device__ __forceinline__ int band_swz(int r, int x) { return (x + 4 * r) & 7; }
+
+// Work item -> (image, band).  Workgroup b of a grid that is a multiple of 8
+// runs on XCD b mod 8 and takes items b, b + grid, ...; all bands of one
+// image get the same residue mod 8, so their shared halo rows stay in one
+// XCD's L2.  Images past cnt (padding to a multiple of 8) are skipped.
+__device__ __forceinline__ void band_item(int64_t item, int bands, int64_t* s, int* band) {
+  const int64_t q = item >> 3;
+  const int64_t blk = q / bands;
+  *band = (int)(q - blk * bands);
+  *s = blk * 8 + (item & 7);
+}
+
+__device__ __forceinline__ void zero_pixel64(uint16_t* band, const Band64& b) {
+  for (int i = threadIdx.x; i < 64; i += blockDim.x) {
+    band[b.zp * 64 + i] = 0;
+    band[b.lo_plane + b.zp * 64 + i] = 0;
+  }
+}
+
+// Stages rows r in [0, rows_used) of a band (image rows y0 + r inside the
+// image) from one image's fp32 NHWC 64-channel activations, split into hi /
+// lo bf16 planes.  Eight consecutive threads read one pixel's 256 bytes.
+__device__ __forceinline__ void stage_band64(const float* __restrict__ src, const Band64& b,
+                                             uint16_t* band, int y0, int rows_used) {
+  const int r_lo = max(0, -y0), r_hi = min(rows_used, b.h - y0);
+  const int units = (r_hi - r_lo) * b.w * 8;
+  const float* base = src + (int64_t)(y0 + r_lo) * b.w * 64;
+  for (int u = threadIdx.x; u < units; u += blockDim.x) {
+    const int pix = u >> 3, c = u & 7;
+    const int rr = pix / b.w, x = pix - rr * b.w;
+    const int r = r_lo + rr;
+    const float* p = base + (int64_t)pix * 64 + c * 8;
+    const float4 v0 = *reinterpret_cast<const float4*>(p);
+    const float4 v1 = *reinterpret_cast<const float4*>(p + 4);
+    uint2 h0, l0, h1, l1;
+    Elt<uint16_t>::split4(v0, h0, l0);
+    Elt<uint16_t>::split4(v1, h1, l1);
+    const int e = (r * b.w + x) * 64 + ((c ^ band_swz(r, x)) << 3);
+    *reinterpret_cast<uint4*>(band + e) = make_uint4(h0.x, h0.y, h1.x, h1.y);
+    *reinterpret_cast<uint4*>(band + b.lo_plane + e) = make_uint4(l0.x, l0.y, l1.x, l1.y);
+  }
+}
+
+// MFMA accumulation of MT 4x4 output tiles from a staged band (band row 0 is
+// image row y0); tile i sits at band tile row tr[i], tile column tc[i].  K is
+// tap-major: 9 taps x 2 steps of 32 channels.  The hi products of all tiles
+// are issued before the lo products, so no MFMA waits on the one before.
+template <int MT, int NT>
+__device__ __forceinline__ void band64_tiles(const uint16_t* band, const Band64& b, int y0,
+                                             const bf16x8* __restrict__ wf, const int (&tr)[MT],
+                                             const int (&tc)[MT], int py, int px, int g, int lane,
+                                             f32x4 (&acc)[MT][NT]) {
+  using X = Elt<uint16_t>;
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 wa[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) wa[nt] = wf[nt * 64 + lane];
+#pragma unroll 1
+  for (int tap = 0; tap < 9; ++tap) {
+    const int dy = tap / 3, dx = tap - 3 * dy;
+    int pe[MT], key[MT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const int r = 4 * tr[i] + py + dy;
+      const int x = 4 * tc[i] + px + dx - 1;
+      const bool in = (unsigned)(y0 + r) < (unsigned)b.h && (unsigned)x < (unsigned)b.w;
+      pe[i] = (in ? r * b.w + x : b.zp) * 64;
+      key[i] = in ? band_swz(r, x) : 0;
+    }
+#pragma unroll
+    for (int ch = 0; ch < 2; ++ch) {
+      const int ks = tap * 2 + ch;
+      bf16x8 xh[MT], xl[MT];
+#pragma unroll
+      for (int i = 0; i < MT; ++i) {
+        const int e = pe[i] + (((ch * 4 + g) ^ key[i]) << 3);
+        xh[i] = X::load(band + e);
+        xl[i] = X::load(band + b.lo_plane + e);
+      }
+      bf16x8 wn[NT];
+      if (ks + 1 < 18) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) wn[nt] = wf[((ks + 1) * NT + nt) * 64 + lane];
+      }
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(wa[nt], xh[i], acc[i][nt]);
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(wa[nt], xl[i], acc[i][nt]);
+      if (ks + 1 < 18) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) wa[nt] = wn[nt];
+      }
+    }
+  }
+}
+
+// Bias, ReLU, optional 2x2 max-pool and 16-byte fp32 NHWC stores of one
+// transposed tile; (oy, ox) is this lane's pixel in the layer's input grid.
+template <int NT>
+__device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const float4 (&bias)[NT],
+                                                float* out, int cout, int oy, int ox, int h, int w,
+                                                int pool, int m, int g) {
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    float4 v = make_float4(fmaxf(acc[nt][0] + bias[nt].x, 0.f), fmaxf(acc[nt][1] + bias[nt].y, 0.f),
+                           fmaxf(acc[nt][2] + bias[nt].z, 0.f), fmaxf(acc[nt][3] + bias[nt].w, 0.f));
+    if (pool) {
+      // the pooling window's four pixels are lanes m ^ 1, m ^ 2 of this group
+#pragma unroll
+      for (int o = 1; o <= 2; o <<= 1) {
+        v.x = fmaxf(v.x, __shfl_xor(v.x, o));
+        v.y = fmaxf(v.y, __shfl_xor(v.y, o));
+        v.z = fmaxf(v.z, __shfl_xor(v.z, o));
+        v.w = fmaxf(v.w, __shfl_xor(v.w, o));
+      }
+      const int qy = oy >> 1, qx = ox >> 1;
+      if ((m & 3) == 0 && qy < h / 2 && qx < w / 2)
+        *reinterpret_cast<float4*>(out + ((int64_t)qy * (w / 2) + qx) * cout + nt * 16 + 4 * g) = v;
+    } else if (oy < h && ox < w) {
+      *reinterpret_cast<float4*>(out + ((int64_t)oy * w + ox) * cout + nt * 16 + 4 * g) = v;
+    }
+  }
+}
+
+// MT tiles of a band: tiles first, first + 4, ... (band-local tile index,
+// tiles_x per tile row), through the epilogue.
+template <int MT, int NT>
+__device__ __forceinline__ void band64_run(const uint16_t* band, const Band64& b, int y0, int ty0,
+                                           const bf16x8* __restrict__ wf, const float4 (&bias)[NT],
+                                           float* out, int cout, int pool, int tiles_x, int first,
+                                           int py, int px, int m, int g, int lane) {
+  int tr[MT], tc[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    const int t = first + kBandWaves * i;
+    tr[i] = t / tiles_x;
+    tc[i] = t - tr[i] * tiles_x;
+  }
+  f32x4 acc[MT][NT];
+  band64_tiles<MT, NT>(band, b, y0, wf, tr, tc, py, px, g, lane, acc);
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+    band64_epilogue<NT>(acc[i], bias, out, cout, 4 * (ty0 + tr[i]) + py, 4 * tc[i] + px, b.h, b.w,
+                        pool, m, g);
+}
+
+// The second-layer work of one band: ntile tiles over the 4 waves, at most 4
+// per wave per round.
+template <int NT>
+__device__ __forceinline__ void band64_layer(const uint16_t* band, const Band64& b, int y0, int ty0,
+                                             int ntile, const bf16x8* __restrict__ wf,
+                                             const float4 (&bias)[NT], float* out, int cout,
+                                             int pool, int tiles_x, int wave, int py, int px, int m,
+                                             int g, int lane) {
+  for (int base = 0; base < ntile; base += 4 * kBandWaves) {
+    const int first = base + wave;
+    const int mt = first >= ntile ? 0 : min(4, (ntile - first + kBandWaves - 1) / kBandWaves);
+    switch (mt) {
+      case 4:
+        band64_run<4, NT>(band, b, y0, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
+                          lane);
+        break;
+      case 3:
+        band64_run<3, NT>(band, b, y0, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
+                          lane);
+        break;
+      case 2:
+        band64_run<2, NT>(band, b, y0, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
+                          lane);
+        break;
+      case 1:
+        band64_run<1, NT>(band, b, y0, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
+                          lane);
+        break;
+      default:
+        break;
+    }
+  }
+}
+
+template <int NT>
+__device__ __forceinline__ void load_bias4(const float* bias, int g, float4 (&b)[NT]) {
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) b[nt] = *reinterpret_cast<const float4*>(bias + nt * 16 + 4 * g);
+}
+
+// One 64-input-channel layer over bands of fp32 activations.
+template <int NT>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+k_band64(ConvArgs a, Band64 b) {
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  uint16_t* band = reinterpret_cast<uint16_t*>(lds_raw);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int m = lane & 15, g = lane >> 4;
+  int py, px;
+  tile_pixel(m, py, px);
+  const bf16x8* wf = reinterpret_cast<const bf16x8*>(a.wts);
+  float4 bias[NT];
+  load_bias4<NT>(a.bias, g, bias);
+  zero_pixel64(band, b);
+  int64_t cnt = *a.count;
+  if (cnt > a.max_count) cnt = a.max_count;
+  const int bands = (a.tiles_y + a.band_tiles - 1) / a.band_tiles;
+  const int64_t items = (cnt + 7) / 8 * 8 * bands;
+  const int ho = a.pool ? a.h / 2 : a.h, wo = a.pool ? a.w / 2 : a.w;
+  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+    int64_t s;
+    int bi;
+    band_item(item, bands, &s, &bi);
+    if (s >= cnt) continue;  // workgroup-uniform
+    const int ty0 = bi * a.band_tiles;
+    const int nty = min(a.band_tiles, a.tiles_y - ty0);
+    const int y0 = 4 * ty0 - 1;
+    __syncthreads();  // the previous band's readers are done
+    stage_band64(a.act_in + s * (int64_t)a.h * a.w * 64, b, band, y0, 4 * nty + 2);
+    __syncthreads();
+    band64_layer<NT>(band, b, y0, ty0, nty * a.tiles_x, wf, bias,
+                     a.act_out + s * (int64_t)ho * wo * a.cout, a.cout, a.pool, a.tiles_x, wave,
+                     py, px, m, g, lane);
+  }
+}
+
+// The first two layers of a bf16 network fused per band, when the first
+// (3 -> 64 channels) does not pool: the first layer computes the band's rows
+// (with the halo rows) from the pre-processed input straight into the hi /
+// lo planes, then the second layer runs from them.  First-layer tiles are 2
+// rows x 8 columns; its K is (dy, dx of 4, c of 4) = 48 of 64, its weight
+// fragments stay in registers.  LDS: the two planes, then the first layer's
+// input band (rows + 2 rows, in0_w pixels of 4 bf16).
+template <int NT>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, int32_t in0_w) {
+  using X = Elt<uint16_t>;
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  uint16_t* band = reinterpret_cast<uint16_t*>(lds_raw);
+  uint16_t* in0 = band + 2 * b.lo_plane;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int m = lane & 15, g = lane >> 4;
+  int py, px;
+  tile_pixel(m, py, px);
+  const bf16x8* wf0 = reinterpret_cast<const bf16x8*>(a0.wts);
+  const bf16x8* wf1 = reinterpret_cast<const bf16x8*>(a1.wts);
+  float4 bias0[4], bias1[NT];
+  load_bias4<4>(a0.bias, g, bias0);
+  load_bias4<NT>(a1.bias, g, bias1);
+  zero_pixel64(band, b);
+  int64_t cnt = *a0.count;
+  if (cnt > a0.max_count) cnt = a0.max_count;
+  const int bands = (a1.tiles_y + a1.band_tiles - 1) / a1.band_tiles;
+  const int64_t items = (cnt + 7) / 8 * 8 * bands;
+  const int ho = a1.pool ? a1.h / 2 : a1.h, wo = a1.pool ? a1.w / 2 : a1.w;
+  const int tx0 = (b.w + 7) / 8;  // first-layer tile columns
+  // first-layer lane pixel: row qy, column qx of a 2 x 8 tile
+  const int qy = m >> 3, qx = m & 7;
+
+  auto geometry = [&](int64_t item, int64_t* s, int* ty0, int* nty) {
+    int bi;
+    band_item(item, bands, s, &bi);
+    *ty0 = bi * a1.band_tiles;
+    *nty = min(a1.band_tiles, a1.tiles_y - *ty0);
+  };
+  // this workgroup's items from `it` on, skipping padding images (uniform)
+  auto next_item = [&](int64_t it) {
+    for (; it < items; it += gridDim.x) {
+      int64_t s;
+      int ty0, nty;
+      geometry(it, &s, &ty0, &nty);
+      if (s < cnt) break;
+    }
+    return it;
+  };
+  auto stage = [&](int64_t it, int tid0) {
+    int64_t s;
+    int ty0, nty;
+    geometry(it, &s, &ty0, &nty);
+    stage_first(a0, in0, s, 4 * ty0 - 2, -1, 4 * nty + 4, in0_w, tid0, 256 - tid0);
+  };
+
+  int64_t item = next_item(blockIdx.x);
+  if (item < items) stage(item, 0);
+  while (item < items) {
+    int64_t s;
+    int ty0, nty;
+    geometry(item, &s, &ty0, &nty);
+    const int y0 = 4 * ty0 - 1;
+    const int rows = 4 * nty + 2;
+    __syncthreads();  // in0 staged; the previous band's second layer is done with the planes
+    // first layer: rows 0 .. rows - 1 of the band, 2 x 8 tiles; its weight
+    // fragments (8 KB, L2-resident) are held in registers for the phase
+    bf16x8 w0[2][4];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) w0[ks][nt] = wf0[(ks * 4 + nt) * 64 + lane];
+    const int t0n = (rows / 2) * tx0;
+    for (int t = wave; t < t0n; t += kBandWaves) {
+      const int ti = t / tx0, tj = t - ti * tx0;
+      const int r = 2 * ti + qy, x = 8 * tj + qx;
+      f32x4 acc[4];
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int k = ks * 32 + g * 8;
+        bf16x8 xin = X::zero();
+        if (k < 48) {
+          const int dy = k >> 4, dx = (k >> 2) & 3;
+          xin = X::load8(in0 + ((r + dy) * in0_w + x + dx) * 4);
+        }
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) acc[nt] = X::mma(w0[ks][nt], xin, acc[nt]);
+      }
+      const bool store = (unsigned)(y0 + r) < (unsigned)b.h && x < b.w;
+      const int e = (r * b.w + x) * 64 + (g & 1) * 4;
+      const int key = band_swz(r, x);
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        uint32_t h01, l01, h23, l23;
+        X::split2(fmaxf(acc[nt][0] + bias0[nt].x, 0.f), fmaxf(acc[nt][1] + bias0[nt].y, 0.f), h01,
+                  l01);
+        X::split2(fmaxf(acc[nt][2] + bias0[nt].z, 0.f), fmaxf(acc[nt][3] + bias0[nt].w, 0.f), h23,
+                  l23);
+        if (store) {
+          const int ee = e + (((2 * nt + (g >> 1)) ^ key) << 3);
+          *reinterpret_cast<uint2*>(band + ee) = make_uint2(h01, h23);
+          *reinterpret_cast<uint2*>(band + b.lo_plane + ee) = make_uint2(l01, l23);
+        }
+      }
+    }
+    __syncthreads();  // planes complete; in0 free
+    const int ntile = nty * a1.tiles_x;
+    band64_layer<NT>(band, b, y0, ty0, ntile, wf1, bias1,
+                     a1.act_out + s * (int64_t)ho * wo * a1.cout, a1.cout, a1.pool, a1.tiles_x, wave,
+                     py, px, m, g, lane);
+    // the waves with one tile fewer stage the next band's input
+    const int64_t nxt = next_item(item + gridDim.x);
+    if (nxt < items) {
+      const int extra = ntile % kBandWaves;
+      stage(nxt, extra ? extra * 64 : 0);
+    }
+    item = nxt;
+  }
+}
+
 // ------------------------------------------------------------------ dense
 
 struct DenseArgs {
@@ -911,6 +1294,67 @@ int launch_pair(int nt0, int nt1, const ConvArgs& a0, const ConvArgs& a1, const 
 }
 }  // namespace
 
+// Band plan of a 64-input-channel bf16 layer (k_band64, or with `pair` the
+// fused k_pair64 whose first layer's input band also sits in LDS): the
+// tallest band of at most 16 tiles (4 per wave) whose LDS fits 80 KB, so
+// that two workgroups share a CU, else one band row in up to 160 KB.  False
+// when the layer does not qualify or no band fits.
+int32_t pair64_in0_w(int32_t w) { return pad_row_pixels(8 * ((w + 7) / 8) + 3); }
+
+bool band64_plan(const CnnLayer& L, bool pair, Band64* b, int32_t* band_tiles, size_t* lds) {
+  if (L.cin != 64 || (L.cout != 64 && L.cout != 32)) return false;
+  int32_t ty, tx;
+  conv_tiles(L, &ty, &tx);
+  const int32_t in0_w = pair64_in0_w(L.w);
+  auto bytes = [&](int32_t bt) {
+    const size_t plane = ((size_t)(4 * bt + 2) * L.w + 1) * 64 * 2;
+    return 2 * plane + (pair ? (size_t)(4 * bt + 4) * in0_w * 8 : 0);
+  };
+  int32_t bt = 16 / tx;
+  if (bt > ty) bt = ty;
+  if (bt < 1) bt = 1;
+  while (bt > 1 && bytes(bt) > 80 * 1024) --bt;
+  if (bytes(bt) > 160 * 1024) return false;
+  b->w = L.w;
+  b->h = L.h;
+  b->rows = 4 * bt + 2;
+  b->zp = b->rows * L.w;
+  b->lo_plane = (b->zp + 1) * 64;
+  *band_tiles = bt;
+  *lds = bytes(bt);
+  return true;
+}
+
+namespace {
+int launch_band64(bool pair, int nt, const ConvArgs& a0, const ConvArgs& a1, const Band64& b,
+                  int32_t in0_w, size_t lds, int64_t max_count, hipStream_t st) {
+  const int64_t bands = (a1.tiles_y + a1.band_tiles - 1) / a1.band_tiles;
+  const int64_t items = (max_count + 7) / 8 * 8 * bands;
+  const int64_t per_cu = lds <= 80 * 1024 ? 2 : 1;
+  int64_t grid = kNumCU * per_cu;  // a multiple of 8 (see band_item)
+  if (grid > items) grid = items;
+  if (grid < 1) grid = 1;
+#define NSC_BAND_CASE(N)                                                                        \
+  case N:                                                                                       \
+    if (pair)                                                                                   \
+      hipLaunchKernelGGL((k_pair64<N>), dim3((unsigned)grid), dim3(64 * kBandWaves), lds, st, a0, \
+                         a1, b, in0_w);                                                         \
+    else                                                                                        \
+      hipLaunchKernelGGL((k_band64<N>), dim3((unsigned)grid), dim3(64 * kBandWaves), lds, st, a1, \
+                         b);                                                                    \
+    break;
+  switch (nt) {
+    NSC_BAND_CASE(2)
+    NSC_BAND_CASE(4)
+    default:
+      return fail(NSC_E_SHAPE, "banded layer with %d output channels", nt * 16);
+  }
+#undef NSC_BAND_CASE
+  NSC_CHECK_LAUNCH(pair ? "k_pair64" : "k_band64");
+  return NSC_OK;
+}
+}  // namespace
+
 // Two ping-pong buffers of fp32 activations per image.
 size_t cnn_workspace_bytes(const Cnn& cnn, int64_t max_count) {
   const size_t per = align_up(cnn.act_elems * sizeof(float), 256);
@@ -951,8 +1395,28 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
     conv_tiles(L, &a.tiles_y, &a.tiles_x);
     return a;
   };
+  // weights in fragment order for the banded kernels
+  auto frag_weights = [&](int l) {
+    return static_cast<const void*>(static_cast<const unsigned char*>(cnn.conv_wf) +
+                                    cnn.layers[l].w_off * 2);
+  };
   int first_layered = 0;
-  {
+  if (cnn.bf16 && cnn.n_layers >= 2 && cnn.layers[0].cout == 64 && !cnn.layers[0].pool) {
+    Band64 b{};
+    int32_t bt = 0;
+    size_t lds = 0;
+    if (band64_plan(cnn.layers[1], true, &b, &bt, &lds)) {
+      ConvArgs a0 = layer_args(0), a1 = layer_args(1);
+      a0.wts = frag_weights(0);
+      a1.wts = frag_weights(1);
+      a1.band_tiles = bt;
+      const int rc = launch_band64(true, cnn.layers[1].cout / 16, a0, a1, b,
+                                   pair64_in0_w(cnn.layers[1].w), lds, r.max_count, stream);
+      if (rc) return rc;
+      first_layered = 2;
+    }
+  }
+  if (first_layered == 0) {
     ConvArgs a0 = layer_args(0);
     ConvArgs a1{};
     PairArgs pa{};
@@ -969,6 +1433,18 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
   for (int l = first_layered; l < cnn.n_layers; ++l) {
     const CnnLayer& L = cnn.layers[l];
     ConvArgs a = layer_args(l);
+    if (cnn.bf16 && l > 0) {
+      Band64 b{};
+      int32_t bt = 0;
+      size_t lds = 0;
+      if (band64_plan(L, false, &b, &bt, &lds)) {
+        a.wts = frag_weights(l);
+        a.band_tiles = bt;
+        const int rc = launch_band64(false, L.cout / 16, a, a, b, 0, lds, r.max_count, stream);
+        if (rc) return rc;
+        continue;
+      }
+    }
     const size_t lds =
         conv_lds_bytes(L, cnn.bf16, &a.cin_lds, &a.w_lds, &a.band_w, &a.band_tiles, &a.seg_tiles);
     a.lo_plane = (4 * a.band_tiles + 2) * a.band_w * a.cin_lds;

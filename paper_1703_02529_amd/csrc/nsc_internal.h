@@ -141,6 +141,12 @@ struct CnnLayer {
   int32_t kpad;             // padded reduction length of the packed weights
   size_t w_off, b_off;      // offsets (elements) into the packed weight/bias arrays
 };
+// bf16 networks also hold every layer's weights in MFMA fragment order
+// (conv_wf, same offsets w_off): for K step ks (32 values of the layer's K
+// order) and output-channel block nt, lane l = 16 g + m holds the 8 values
+// W[16 nt + m][32 ks + 8 g .. 32 ks + 8 g + 7], 16 bytes at element
+// ((ks * (cout / 16) + nt) * 64 + l) * 8, so one wave's fragment is 1 KB of
+// consecutive memory.
 struct Cnn {
   nsc_cnn_desc desc;
   int32_t n_layers;
@@ -149,6 +155,7 @@ struct Cnn {
   bool bf16;
   void* dev;                // one allocation holding everything below
   void* conv_w;             // packed conv weights, bf16 or fp32
+  void* conv_wf;            // bf16 networks: the same in fragment order (else null)
   float* conv_b;            // fp32 biases
   void* w1;                 // dense weights [D][flat] in (y, x, c) order
   float* b1;

@@ -243,6 +243,21 @@ def test_cnn_fused_pair_shapes(conv, pool, hw, fy):
     _cnn_case(spec, n_frames=24, n_img=11, fy=fy)
 
 
+@pytest.mark.parametrize("conv,pool,hw,fy", [
+    ((64, 64), (False, True), (13, 9), 1),                 # fused 64-channel pair, ragged tiles
+    ((64, 32, 64), (False, False, True), (23, 31), 1),     # fused pair into 32 channels
+    ((64, 64, 64), (False, False, False), (7, 5), 1),      # map smaller than a band
+    ((64, 64, 64, 64), (False, True, False, True), (50, 50), 2),  # the 4-layer net, nested cells
+    ((32, 64, 64), (True, False, True), (30, 61), 1),      # banded layer after a layered one
+    ((64, 64), (False, False), (6, 80), 1),                # pair band over 80 KB: 1 group per CU
+    ((32, 64, 64), (True, False, False), (11, 200), 1),    # banded layer 100 wide (160 KB plan)
+])
+def test_cnn_banded_shapes(conv, pool, hw, fy):
+    # bf16 layers with 64 input channels run banded, weights streamed in fragment order
+    spec = synth.CNNSpec(in_h=hw[0], in_w=hw[1], conv=conv, pool=pool, dense=32, bf16=True)
+    _cnn_case(spec, n_frames=16, n_img=9, fy=fy)
+
+
 def test_cnn_zero_count():
     spec = W.VGA.cnn
     desc = nsc.make_desc(spec.conv, spec.pool, spec.dense, 50, 50, True)
