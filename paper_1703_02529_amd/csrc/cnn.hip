@@ -639,34 +639,45 @@ __global__ void __launch_bounds__(1024) k_conv_pair(ConvArgs a0, ConvArgs a1, Pa
 // A layer with 64 input channels (bf16 network) keeps its weights in global
 // memory in fragment order (L2-resident, shared by every CU) and loads them
 // straight into registers, one K step ahead of their use; the LDS holds only
-// a band of the layer's input: the rows of band_tiles tile rows (4 output
-// rows each) plus one halo row above and below, every column of the image,
-// as bf16 hi and lo planes.  Each pixel's 64 channels are 8 chunks of 16
-// bytes, chunk c stored at position c ^ ((x + 4 r) & 7) for band row r and
-// column x: the 8 pixels (two rows by four columns of a 4x4 tile) that 8
-// lanes of one fragment read then fall on 8 distinct 16-byte bank groups.
-// Pixels outside the image read a zero pixel at the end of each plane, so no
-// halo is stored.  Without weights in LDS two workgroups fit on a CU, and one
-// stages while the other computes.
+// a band of the layer's input: band_tiles tile rows (4 output rows each) plus
+// a halo row above and below, as bf16 hi and lo planes.  Without weights in
+// LDS two workgroups fit on a CU, and one stages while the other computes.
+//
+// Band layout: band row r is image row y0 + r, band column cb is image column
+// cb - 1; row stride wb >= w + 2 with wb = 4 (mod 8).  Each pixel's 64
+// channels are 8 chunks of 8 bf16, stored chunk-major: chunk c of band pixel
+// p = r * wb + cb is the 16 bytes at (c * cp + p) * 16 of the hi plane (and
+// lo_bytes further in the lo plane), with cp = rows * wb + 1 = 1 (mod 8).
+// The 16-byte index c * cp + p is then (c + p) mod 8 on the 8 LDS bank
+// groups, so the 8 pixels of two rows by four columns that a lane group
+// reads, and the 8 chunks of one pixel that staging writes, all fall on
+// distinct bank groups.  Image column -1, columns >= w and rows outside the
+// image hold zeros, so a tap needs no bounds test: its address is the tile's
+// address plus (dy * wb + dx) * 16.  A tile that overhangs column w reads up
+// to two pixels into the next row for outputs that are never stored.
 //
 // The MFMA runs transposed: A = 16 output channels x 32 K of the weights,
 // B = 32 K x the 16 pixels of a 4x4 tile.  Lane (m, g) then holds channels
 // 16 nt + 4 g .. 16 nt + 4 g + 3 of pixel m, so a pooled output is a max over
-// the four lanes of one pooling window and every store is 16 bytes.
+// the four lanes of one quad (DPP) and every store is 16 bytes.
 
 constexpr int kBandWaves = 4;  // waves per workgroup of the banded kernels
 
 struct Band64 {
   int32_t w, h;      // layer input grid
   int32_t rows;      // staged rows of a band: 4 * band_tiles + 2
-  int32_t zp;        // pixel index of the zero pixel: rows * w
-  int32_t lo_plane;  // elements from the hi plane to the lo plane: (zp + 1) * 64
+  int32_t wb;        // pixels per band row
+  int32_t cp;        // pixels per chunk plane: rows * wb + 1
+  int32_t lo_bytes;  // bytes from the hi plane to the lo plane: 8 * cp * 16
 };
 
-__device__ __forceinline__ int band_swz(int r, int x) { return (x + 4 * r) & 7; }
+// Bytes of the two planes plus 32 bytes for the overhanging reads.
+__host__ __device__ inline size_t band64_bytes(const Band64& b) {
+  return (size_t)2 * b.lo_bytes + 32;
+}
 
-// Work item -> (image, band).  Workgroup b of a grid that is a multiple of 8
-// runs on XCD b mod 8 and takes items b, b + grid, ...; all bands of one
+// Work item -> (image, band).  Workgroup i of a grid that is a multiple of 8
+// runs on XCD i mod 8 and takes items i, i + grid, ...; all bands of one
 // image get the same residue mod 8, so their shared halo rows stay in one
 // XCD's L2.  Images past cnt (padding to a multiple of 8) are skipped.
 __device__ __forceinline__ void band_item(int64_t item, int bands, int64_t* s, int* band) {
@@ -676,43 +687,47 @@ __device__ __forceinline__ void band_item(int64_t item, int bands, int64_t* s, i
   *s = blk * 8 + (item & 7);
 }
 
-__device__ __forceinline__ void zero_pixel64(uint16_t* band, const Band64& b) {
-  for (int i = threadIdx.x; i < 64; i += blockDim.x) {
-    band[b.zp * 64 + i] = 0;
-    band[b.lo_plane + b.zp * 64 + i] = 0;
-  }
+__device__ __forceinline__ void band64_clear(unsigned char* lds, const Band64& b) {
+  const int n = (int)(band64_bytes(b) / 16);
+  for (int i = threadIdx.x; i < n; i += blockDim.x)
+    *reinterpret_cast<uint4*>(lds + (size_t)i * 16) = make_uint4(0u, 0u, 0u, 0u);
 }
 
-// Stages rows r in [0, rows_used) of a band (image rows y0 + r inside the
-// image) from one image's fp32 NHWC 64-channel activations, split into hi /
-// lo bf16 planes.  Eight consecutive threads read one pixel's 256 bytes.
+// Stages band rows [0, rows_used), columns 1..w: image rows y0 + r inside the
+// image from one image's fp32 NHWC 64-channel activations split into hi / lo
+// bf16, zeros for rows outside.  Eight consecutive threads read one pixel's
+// 256 bytes.
 __device__ __forceinline__ void stage_band64(const float* __restrict__ src, const Band64& b,
-                                             uint16_t* band, int y0, int rows_used) {
-  const int r_lo = max(0, -y0), r_hi = min(rows_used, b.h - y0);
-  const int units = (r_hi - r_lo) * b.w * 8;
-  const float* base = src + (int64_t)(y0 + r_lo) * b.w * 64;
+                                             unsigned char* lds, int y0, int rows_used) {
+  const int units = rows_used * b.w * 8;
   for (int u = threadIdx.x; u < units; u += blockDim.x) {
     const int pix = u >> 3, c = u & 7;
-    const int rr = pix / b.w, x = pix - rr * b.w;
-    const int r = r_lo + rr;
-    const float* p = base + (int64_t)pix * 64 + c * 8;
-    const float4 v0 = *reinterpret_cast<const float4*>(p);
-    const float4 v1 = *reinterpret_cast<const float4*>(p + 4);
-    uint2 h0, l0, h1, l1;
-    Elt<uint16_t>::split4(v0, h0, l0);
-    Elt<uint16_t>::split4(v1, h1, l1);
-    const int e = (r * b.w + x) * 64 + ((c ^ band_swz(r, x)) << 3);
-    *reinterpret_cast<uint4*>(band + e) = make_uint4(h0.x, h0.y, h1.x, h1.y);
-    *reinterpret_cast<uint4*>(band + b.lo_plane + e) = make_uint4(l0.x, l0.y, l1.x, l1.y);
+    const int r = pix / b.w, x = pix - r * b.w;
+    const int y = y0 + r;
+    uint4 hi = make_uint4(0u, 0u, 0u, 0u), lo = hi;
+    if ((unsigned)y < (unsigned)b.h) {
+      const float* p = src + ((int64_t)y * b.w + x) * 64 + c * 8;
+      const float4 v0 = *reinterpret_cast<const float4*>(p);
+      const float4 v1 = *reinterpret_cast<const float4*>(p + 4);
+      uint2 h0, l0, h1, l1;
+      Elt<uint16_t>::split4(v0, h0, l0);
+      Elt<uint16_t>::split4(v1, h1, l1);
+      hi = make_uint4(h0.x, h0.y, h1.x, h1.y);
+      lo = make_uint4(l0.x, l0.y, l1.x, l1.y);
+    }
+    const int addr = (c * b.cp + r * b.wb + x + 1) * 16;
+    *reinterpret_cast<uint4*>(lds + addr) = hi;
+    *reinterpret_cast<uint4*>(lds + b.lo_bytes + addr) = lo;
   }
 }
 
-// MFMA accumulation of MT 4x4 output tiles from a staged band (band row 0 is
-// image row y0); tile i sits at band tile row tr[i], tile column tc[i].  K is
-// tap-major: 9 taps x 2 steps of 32 channels.  The hi products of all tiles
-// are issued before the lo products, so no MFMA waits on the one before.
+// MFMA accumulation of MT 4x4 output tiles from a staged band; tile i sits at
+// band tile row tr[i], tile column tc[i].  K is tap-major: 9 taps x 2 steps
+// of 32 channels (chunks 0-3, then 4-7).  The weight fragments of the two
+// steps of a tap alternate between two register sets, each loaded one step
+// ahead; the hi products of all tiles are issued before the lo products.
 template <int MT, int NT>
-__device__ __forceinline__ void band64_tiles(const uint16_t* band, const Band64& b, int y0,
+__device__ __forceinline__ void band64_tiles(const unsigned char* lds, const Band64& b,
                                              const bf16x8* __restrict__ wf, const int (&tr)[MT],
                                              const int (&tc)[MT], int py, int px, int g, int lane,
                                              f32x4 (&acc)[MT][NT]) {
@@ -721,76 +736,90 @@ __device__ __forceinline__ void band64_tiles(const uint16_t* band, const Band64&
   for (int i = 0; i < MT; ++i)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  bf16x8 wa[NT];
+  uint32_t base[MT], base_lo[MT];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) wa[nt] = wf[nt * 64 + lane];
+  for (int i = 0; i < MT; ++i) {
+    base[i] = (uint32_t)(g * b.cp + (4 * tr[i] + py) * b.wb + 4 * tc[i] + px) * 16u;
+    base_lo[i] = base[i] + (uint32_t)b.lo_bytes;
+  }
+  const uint32_t step2 = (uint32_t)b.cp * 64u;  // chunks 4..7: 4 chunk planes on
+  const bf16x8* wp = wf + lane;
+  bf16x8 wa[NT], wb[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) wa[nt] = wp[nt * 64];
 #pragma unroll 1
   for (int tap = 0; tap < 9; ++tap) {
     const int dy = tap / 3, dx = tap - 3 * dy;
-    int pe[MT], key[MT];
+    const uint32_t toff = (uint32_t)(dy * b.wb + dx) * 16u;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) wb[nt] = wp[((2 * tap + 1) * NT + nt) * 64];
+    bf16x8 xh[MT], xl[MT];
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      const int r = 4 * tr[i] + py + dy;
-      const int x = 4 * tc[i] + px + dx - 1;
-      const bool in = (unsigned)(y0 + r) < (unsigned)b.h && (unsigned)x < (unsigned)b.w;
-      pe[i] = (in ? r * b.w + x : b.zp) * 64;
-      key[i] = in ? band_swz(r, x) : 0;
+      xh[i] = X::load(reinterpret_cast<const uint16_t*>(lds + base[i] + toff));
+      xl[i] = X::load(reinterpret_cast<const uint16_t*>(lds + base_lo[i] + toff));
     }
 #pragma unroll
-    for (int ch = 0; ch < 2; ++ch) {
-      const int ks = tap * 2 + ch;
-      bf16x8 xh[MT], xl[MT];
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int i = 0; i < MT; ++i) {
-        const int e = pe[i] + (((ch * 4 + g) ^ key[i]) << 3);
-        xh[i] = X::load(band + e);
-        xl[i] = X::load(band + b.lo_plane + e);
-      }
-      bf16x8 wn[NT];
-      if (ks + 1 < 18) {
+      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(wa[nt], xh[i], acc[i][nt]);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) wn[nt] = wf[((ks + 1) * NT + nt) * 64 + lane];
-      }
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
+      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(wa[nt], xl[i], acc[i][nt]);
+    // the next tap's first step (the last tap reloads a valid fragment, unused)
+    const int kn = tap < 8 ? 2 * tap + 2 : 2 * tap;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(wa[nt], xh[i], acc[i][nt]);
+    for (int nt = 0; nt < NT; ++nt) wa[nt] = wp[(kn * NT + nt) * 64];
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(wa[nt], xl[i], acc[i][nt]);
-      if (ks + 1 < 18) {
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) wa[nt] = wn[nt];
-      }
+    for (int i = 0; i < MT; ++i) {
+      xh[i] = X::load(reinterpret_cast<const uint16_t*>(lds + base[i] + toff + step2));
+      xl[i] = X::load(reinterpret_cast<const uint16_t*>(lds + base_lo[i] + toff + step2));
     }
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(wb[nt], xh[i], acc[i][nt]);
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(wb[nt], xl[i], acc[i][nt]);
   }
 }
+
+// Lane permutation within quads of lanes (DPP quad_perm).
+template <int CTRL>
+__device__ __forceinline__ float quad_perm(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kQuadXor1 = 0xB1;  // [1, 0, 3, 2]
+constexpr int kQuadXor2 = 0x4E;  // [2, 3, 0, 1]
 
 // Bias, ReLU, optional 2x2 max-pool and 16-byte fp32 NHWC stores of one
 // transposed tile; (oy, ox) is this lane's pixel in the layer's input grid.
 template <int NT>
-__device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const float4 (&bias)[NT],
+__device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const float* __restrict__ bp,
                                                 float* out, int cout, int oy, int ox, int h, int w,
                                                 int pool, int m, int g) {
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    float4 v = make_float4(fmaxf(acc[nt][0] + bias[nt].x, 0.f), fmaxf(acc[nt][1] + bias[nt].y, 0.f),
-                           fmaxf(acc[nt][2] + bias[nt].z, 0.f), fmaxf(acc[nt][3] + bias[nt].w, 0.f));
+    const float4 bb = *reinterpret_cast<const float4*>(bp + nt * 16 + 4 * g);
+    float v[4] = {fmaxf(acc[nt][0] + bb.x, 0.f), fmaxf(acc[nt][1] + bb.y, 0.f),
+                  fmaxf(acc[nt][2] + bb.z, 0.f), fmaxf(acc[nt][3] + bb.w, 0.f)};
     if (pool) {
-      // the pooling window's four pixels are lanes m ^ 1, m ^ 2 of this group
+      // the four pixels of a pooling window are the four lanes of a quad
 #pragma unroll
-      for (int o = 1; o <= 2; o <<= 1) {
-        v.x = fmaxf(v.x, __shfl_xor(v.x, o));
-        v.y = fmaxf(v.y, __shfl_xor(v.y, o));
-        v.z = fmaxf(v.z, __shfl_xor(v.z, o));
-        v.w = fmaxf(v.w, __shfl_xor(v.w, o));
+      for (int r = 0; r < 4; ++r) {
+        v[r] = fmaxf(v[r], quad_perm<kQuadXor1>(v[r]));
+        v[r] = fmaxf(v[r], quad_perm<kQuadXor2>(v[r]));
       }
       const int qy = oy >> 1, qx = ox >> 1;
       if ((m & 3) == 0 && qy < h / 2 && qx < w / 2)
-        *reinterpret_cast<float4*>(out + ((int64_t)qy * (w / 2) + qx) * cout + nt * 16 + 4 * g) = v;
+        *reinterpret_cast<float4*>(out + ((int64_t)qy * (w / 2) + qx) * cout + nt * 16 + 4 * g) =
+            make_float4(v[0], v[1], v[2], v[3]);
     } else if (oy < h && ox < w) {
-      *reinterpret_cast<float4*>(out + ((int64_t)oy * w + ox) * cout + nt * 16 + 4 * g) = v;
+      *reinterpret_cast<float4*>(out + ((int64_t)oy * w + ox) * cout + nt * 16 + 4 * g) =
+          make_float4(v[0], v[1], v[2], v[3]);
     }
   }
 }
@@ -798,8 +827,8 @@ __device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const fl
 // MT tiles of a band: tiles first, first + 4, ... (band-local tile index,
 // tiles_x per tile row), through the epilogue.
 template <int MT, int NT>
-__device__ __forceinline__ void band64_run(const uint16_t* band, const Band64& b, int y0, int ty0,
-                                           const bf16x8* __restrict__ wf, const float4 (&bias)[NT],
+__device__ __forceinline__ void band64_run(const unsigned char* lds, const Band64& b, int ty0,
+                                           const bf16x8* __restrict__ wf, const float* __restrict__ bias,
                                            float* out, int cout, int pool, int tiles_x, int first,
                                            int py, int px, int m, int g, int lane) {
   int tr[MT], tc[MT];
@@ -810,19 +839,19 @@ __device__ __forceinline__ void band64_run(const uint16_t* band, const Band64& b
     tc[i] = t - tr[i] * tiles_x;
   }
   f32x4 acc[MT][NT];
-  band64_tiles<MT, NT>(band, b, y0, wf, tr, tc, py, px, g, lane, acc);
+  band64_tiles<MT, NT>(lds, b, wf, tr, tc, py, px, g, lane, acc);
 #pragma unroll
   for (int i = 0; i < MT; ++i)
     band64_epilogue<NT>(acc[i], bias, out, cout, 4 * (ty0 + tr[i]) + py, 4 * tc[i] + px, b.h, b.w,
                         pool, m, g);
 }
 
-// The second-layer work of one band: ntile tiles over the 4 waves, at most 4
-// per wave per round.
+// One band's work of a 64-input-channel layer: ntile tiles over the 4 waves,
+// at most 4 per wave per round.
 template <int NT>
-__device__ __forceinline__ void band64_layer(const uint16_t* band, const Band64& b, int y0, int ty0,
+__device__ __forceinline__ void band64_layer(const unsigned char* lds, const Band64& b, int ty0,
                                              int ntile, const bf16x8* __restrict__ wf,
-                                             const float4 (&bias)[NT], float* out, int cout,
+                                             const float* __restrict__ bias, float* out, int cout,
                                              int pool, int tiles_x, int wave, int py, int px, int m,
                                              int g, int lane) {
   for (int base = 0; base < ntile; base += 4 * kBandWaves) {
@@ -830,19 +859,19 @@ __device__ __forceinline__ void band64_layer(const uint16_t* band, const Band64&
     const int mt = first >= ntile ? 0 : min(4, (ntile - first + kBandWaves - 1) / kBandWaves);
     switch (mt) {
       case 4:
-        band64_run<4, NT>(band, b, y0, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
+        band64_run<4, NT>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
                           lane);
         break;
       case 3:
-        band64_run<3, NT>(band, b, y0, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
+        band64_run<3, NT>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
                           lane);
         break;
       case 2:
-        band64_run<2, NT>(band, b, y0, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
+        band64_run<2, NT>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
                           lane);
         break;
       case 1:
-        band64_run<1, NT>(band, b, y0, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
+        band64_run<1, NT>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
                           lane);
         break;
       default:
@@ -851,27 +880,18 @@ __device__ __forceinline__ void band64_layer(const uint16_t* band, const Band64&
   }
 }
 
-template <int NT>
-__device__ __forceinline__ void load_bias4(const float* bias, int g, float4 (&b)[NT]) {
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) b[nt] = *reinterpret_cast<const float4*>(bias + nt * 16 + 4 * g);
-}
-
 // One 64-input-channel layer over bands of fp32 activations.
 template <int NT>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 k_band64(ConvArgs a, Band64 b) {
-  extern __shared__ __align__(16) unsigned char lds_raw[];
-  uint16_t* band = reinterpret_cast<uint16_t*>(lds_raw);
+  extern __shared__ __align__(16) unsigned char lds[];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int m = lane & 15, g = lane >> 4;
   int py, px;
   tile_pixel(m, py, px);
   const bf16x8* wf = reinterpret_cast<const bf16x8*>(a.wts);
-  float4 bias[NT];
-  load_bias4<NT>(a.bias, g, bias);
-  zero_pixel64(band, b);
+  band64_clear(lds, b);
   int64_t cnt = *a.count;
   if (cnt > a.max_count) cnt = a.max_count;
   const int bands = (a.tiles_y + a.band_tiles - 1) / a.band_tiles;
@@ -884,30 +904,78 @@ k_band64(ConvArgs a, Band64 b) {
     if (s >= cnt) continue;  // workgroup-uniform
     const int ty0 = bi * a.band_tiles;
     const int nty = min(a.band_tiles, a.tiles_y - ty0);
-    const int y0 = 4 * ty0 - 1;
-    __syncthreads();  // the previous band's readers are done
-    stage_band64(a.act_in + s * (int64_t)a.h * a.w * 64, b, band, y0, 4 * nty + 2);
+    __syncthreads();  // the previous band's readers are done (and the clear)
+    stage_band64(a.act_in + s * (int64_t)a.h * a.w * 64, b, lds, 4 * ty0 - 1, 4 * nty + 2);
     __syncthreads();
-    band64_layer<NT>(band, b, y0, ty0, nty * a.tiles_x, wf, bias,
+    band64_layer<NT>(lds, b, ty0, nty * a.tiles_x, wf, a.bias,
                      a.act_out + s * (int64_t)ho * wo * a.cout, a.cout, a.pool, a.tiles_x, wave,
                      py, px, m, g, lane);
   }
 }
 
+// The pre-processed bf16 input of one first-layer pixel: channels 0-2 of
+// (S / den) / 127.5 - 1 from the fy x fx cell sums of image pixel (y, x) of
+// frame idx[s], correctly rounded, and a zero channel 3.
+__device__ __forceinline__ uint2 first_input_bf16(const ConvArgs& a, int64_t s, int y, int x) {
+  const int32_t* S = a.sums + (int64_t)a.idx[s] * a.sums_h * a.sums_w * 3;
+  int64_t acc[3] = {0, 0, 0};
+  for (int dy = 0; dy < a.fy; ++dy)
+    for (int dx = 0; dx < a.fx; ++dx) {
+      const int32_t* q = S + ((int64_t)(y * a.fy + dy) * a.sums_w + (x * a.fx + dx)) * 3;
+      acc[0] += q[0];
+      acc[1] += q[1];
+      acc[2] += q[2];
+    }
+  uint16_t v[3];
+  const bool f32div = a.den255 < (1 << 24);
+#pragma unroll
+  for (int c = 0; c < 3; ++c) {
+    const int64_t num = 2 * acc[c] - a.den255;
+    v[c] = f32div ? div_to_bf16_bits((int32_t)num, (int32_t)a.den255)
+                  : f64_to_bf16_bits((double)num / (double)a.den255);
+  }
+  return make_uint2((uint32_t)v[0] | ((uint32_t)v[1] << 16), (uint32_t)v[2]);
+}
+
+// Pre-processed bf16 input of every survivor for k_pair64, zero-bordered:
+// xin[slot][xr][xw] pixels of 4 bf16, image pixel (y, x) at (y + 2, x + 1).
+__global__ void __launch_bounds__(256) k_prep_input(ConvArgs a, uint2* xin, int32_t xr, int32_t xw) {
+  int64_t cnt = *a.count;
+  if (cnt > a.max_count) cnt = a.max_count;
+  const int64_t per = (int64_t)xr * xw;
+  const int64_t total = cnt * per;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t s = i / per;
+    const int q = (int)(i - s * per);
+    const int row = q / xw, col = q - row * xw;
+    const int y = row - 2, x = col - 1;
+    uint2 v = make_uint2(0u, 0u);
+    if ((unsigned)y < (unsigned)a.h && (unsigned)x < (unsigned)a.w) v = first_input_bf16(a, s, y, x);
+    xin[i] = v;
+  }
+}
+
 // The first two layers of a bf16 network fused per band, when the first
 // (3 -> 64 channels) does not pool: the first layer computes the band's rows
-// (with the halo rows) from the pre-processed input straight into the hi /
-// lo planes, then the second layer runs from them.  First-layer tiles are 2
-// rows x 8 columns; its K is (dy, dx of 4, c of 4) = 48 of 64, its weight
-// fragments stay in registers.  LDS: the two planes, then the first layer's
-// input band (rows + 2 rows, in0_w pixels of 4 bf16).
+// (with the halo rows) from the pre-processed input (k_prep_input) straight
+// into the hi / lo planes, then the second layer runs from them.  First-layer
+// tiles are 2 rows x 8 columns; its K is (dy, dx of 4, c of 4) = 48 of 64.
+// Each wave loads its first-layer inputs of the next band (up to kL1Pre tiles)
+// into registers before running the second layer of the current one, so
+// that their HBM latency passes under the second layer's MFMA work.
+constexpr int kL1Pre = 6;
+
+struct L1Frags {
+  uint4 x[kL1Pre][2];  // per tile: the K chunks of steps 0 and 1
+};
+
 template <int NT>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
-k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, int32_t in0_w) {
+k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int32_t xr,
+         int32_t xw) {
   using X = Elt<uint16_t>;
-  extern __shared__ __align__(16) unsigned char lds_raw[];
-  uint16_t* band = reinterpret_cast<uint16_t*>(lds_raw);
-  uint16_t* in0 = band + 2 * b.lo_plane;
+  extern __shared__ __align__(16) unsigned char lds[];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int m = lane & 15, g = lane >> 4;
@@ -915,105 +983,128 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, int32_t in0_w) {
   tile_pixel(m, py, px);
   const bf16x8* wf0 = reinterpret_cast<const bf16x8*>(a0.wts);
   const bf16x8* wf1 = reinterpret_cast<const bf16x8*>(a1.wts);
-  float4 bias0[4], bias1[NT];
-  load_bias4<4>(a0.bias, g, bias0);
-  load_bias4<NT>(a1.bias, g, bias1);
-  zero_pixel64(band, b);
+  band64_clear(lds, b);
   int64_t cnt = *a0.count;
   if (cnt > a0.max_count) cnt = a0.max_count;
   const int bands = (a1.tiles_y + a1.band_tiles - 1) / a1.band_tiles;
   const int64_t items = (cnt + 7) / 8 * 8 * bands;
   const int ho = a1.pool ? a1.h / 2 : a1.h, wo = a1.pool ? a1.w / 2 : a1.w;
-  const int tx0 = (b.w + 7) / 8;  // first-layer tile columns
-  // first-layer lane pixel: row qy, column qx of a 2 x 8 tile
-  const int qy = m >> 3, qx = m & 7;
+  const int tx0 = (b.w + 7) / 8;      // first-layer tile columns
+  const int qy = m >> 3, qx = m & 7;  // first-layer lane pixel in a 2 x 8 tile
+  // this lane's K chunks of the first layer: pixels (dy, dx) and (dy, dx + 1)
+  // of steps 0 and 1 (step 1 only for lane groups 0 and 1: K = 48)
+  const int k0 = g * 8, k1 = 32 + g * 8;
+  const int off0 = (k0 >> 4) * xw + ((k0 >> 2) & 3);
+  const int off1 = (k1 >> 4) * xw + ((k1 >> 2) & 3);
+  const bool use1 = k1 < 48;
 
-  auto geometry = [&](int64_t item, int64_t* s, int* ty0, int* nty) {
-    int bi;
-    band_item(item, bands, s, &bi);
-    *ty0 = bi * a1.band_tiles;
-    *nty = min(a1.band_tiles, a1.tiles_y - *ty0);
-  };
   // this workgroup's items from `it` on, skipping padding images (uniform)
-  auto next_item = [&](int64_t it) {
+  auto next_item = [&](int64_t it, int64_t* s, int* ty0, int* nty) {
     for (; it < items; it += gridDim.x) {
-      int64_t s;
-      int ty0, nty;
-      geometry(it, &s, &ty0, &nty);
-      if (s < cnt) break;
+      int bi;
+      band_item(it, bands, s, &bi);
+      if (*s < cnt) {
+        *ty0 = bi * a1.band_tiles;
+        *nty = min(a1.band_tiles, a1.tiles_y - *ty0);
+        break;
+      }
     }
     return it;
   };
-  auto stage = [&](int64_t it, int tid0) {
-    int64_t s;
-    int ty0, nty;
-    geometry(it, &s, &ty0, &nty);
-    stage_first(a0, in0, s, 4 * ty0 - 2, -1, 4 * nty + 4, in0_w, tid0, 256 - tid0);
+  // the two K chunks of first-layer tile t of a band (band row 0 = image row y0)
+  auto l1_load = [&](const uint2* xs, int y0, int t, uint4 (&x)[2]) {
+    const int ti = t / tx0, tj = t - ti * tx0;
+    const int y = y0 + 2 * ti + qy, col = 8 * tj + qx;
+    // input pixel (y + dy - 1, col + dx - 1) is xin (y + dy + 1, col + dx)
+    const uint2* p = xs + (int64_t)(y + 1) * xw + col;
+    const uint2 p00 = p[off0], p01 = p[off0 + 1];
+    uint2 p10 = make_uint2(0u, 0u), p11 = p10;
+    if (use1) {
+      p10 = p[off1];
+      p11 = p[off1 + 1];
+    }
+    x[0] = make_uint4(p00.x, p00.y, p01.x, p01.y);
+    x[1] = make_uint4(p10.x, p10.y, p11.x, p11.y);
+  };
+  auto l1_prefetch = [&](int64_t s, int ty0, int nty, L1Frags& f) {
+    const uint2* xs = xin + s * (int64_t)xr * xw;
+    const int t0n = (2 * nty + 1) * tx0;
+#pragma unroll
+    for (int j = 0; j < kL1Pre; ++j) {
+      const int t = wave + kBandWaves * j;
+      if (t < t0n) l1_load(xs, 4 * ty0 - 1, t, f.x[j]);
+    }
+  };
+  // first-layer tile t: 8 MFMAs, bias, ReLU, hi / lo split into the planes
+  auto l1_tile = [&](const bf16x8 (&w0)[2][4], int y0, int t, const uint4 (&x)[2]) {
+    const int ti = t / tx0, tj = t - ti * tx0;
+    const int r = 2 * ti + qy, col = 8 * tj + qx;
+    const int y = y0 + r;
+    const bf16x8 x0 = __builtin_bit_cast(bf16x8, x[0]);
+    const bf16x8 x1 = __builtin_bit_cast(bf16x8, x[1]);
+    f32x4 acc[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+      acc[nt] = X::mma(w0[0][nt], x0, f32x4{0.f, 0.f, 0.f, 0.f});
+      acc[nt] = X::mma(w0[1][nt], x1, acc[nt]);
+    }
+    if (col < b.w) {
+      const bool inside = (unsigned)y < (unsigned)b.h;  // rows outside are zero
+      const int addr = ((g >> 1) * b.cp + r * b.wb + col + 1) * 16 + (g & 1) * 8;
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        const float4 bb = *reinterpret_cast<const float4*>(a0.bias + nt * 16 + 4 * g);
+        const float v0 = inside ? fmaxf(acc[nt][0] + bb.x, 0.f) : 0.f;
+        const float v1 = inside ? fmaxf(acc[nt][1] + bb.y, 0.f) : 0.f;
+        const float v2 = inside ? fmaxf(acc[nt][2] + bb.z, 0.f) : 0.f;
+        const float v3 = inside ? fmaxf(acc[nt][3] + bb.w, 0.f) : 0.f;
+        uint32_t h01, l01, h23, l23;
+        X::split2(v0, v1, h01, l01);
+        X::split2(v2, v3, h23, l23);
+        const int ad = addr + 2 * nt * b.cp * 16;  // chunk 2 nt + g / 2
+        *reinterpret_cast<uint2*>(lds + ad) = make_uint2(h01, h23);
+        *reinterpret_cast<uint2*>(lds + b.lo_bytes + ad) = make_uint2(l01, l23);
+      }
+    }
   };
 
-  int64_t item = next_item(blockIdx.x);
-  if (item < items) stage(item, 0);
+  int64_t s = 0;
+  int ty0 = 0, nty = 0;
+  int64_t item = next_item(blockIdx.x, &s, &ty0, &nty);
+  L1Frags pre;
+  if (item < items) l1_prefetch(s, ty0, nty, pre);
   while (item < items) {
-    int64_t s;
-    int ty0, nty;
-    geometry(item, &s, &ty0, &nty);
     const int y0 = 4 * ty0 - 1;
-    const int rows = 4 * nty + 2;
-    __syncthreads();  // in0 staged; the previous band's second layer is done with the planes
-    // first layer: rows 0 .. rows - 1 of the band, 2 x 8 tiles; its weight
-    // fragments (8 KB, L2-resident) are held in registers for the phase
+    const int t0n = (2 * nty + 1) * tx0;  // first-layer tiles: rows 4 nty + 2
     bf16x8 w0[2][4];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) w0[ks][nt] = wf0[(ks * 4 + nt) * 64 + lane];
-    const int t0n = (rows / 2) * tx0;
-    for (int t = wave; t < t0n; t += kBandWaves) {
-      const int ti = t / tx0, tj = t - ti * tx0;
-      const int r = 2 * ti + qy, x = 8 * tj + qx;
-      f32x4 acc[4];
+    __syncthreads();  // the previous band's second layer is done with the planes
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const int k = ks * 32 + g * 8;
-        bf16x8 xin = X::zero();
-        if (k < 48) {
-          const int dy = k >> 4, dx = (k >> 2) & 3;
-          xin = X::load8(in0 + ((r + dy) * in0_w + x + dx) * 4);
-        }
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) acc[nt] = X::mma(w0[ks][nt], xin, acc[nt]);
-      }
-      const bool store = (unsigned)(y0 + r) < (unsigned)b.h && x < b.w;
-      const int e = (r * b.w + x) * 64 + (g & 1) * 4;
-      const int key = band_swz(r, x);
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        uint32_t h01, l01, h23, l23;
-        X::split2(fmaxf(acc[nt][0] + bias0[nt].x, 0.f), fmaxf(acc[nt][1] + bias0[nt].y, 0.f), h01,
-                  l01);
-        X::split2(fmaxf(acc[nt][2] + bias0[nt].z, 0.f), fmaxf(acc[nt][3] + bias0[nt].w, 0.f), h23,
-                  l23);
-        if (store) {
-          const int ee = e + (((2 * nt + (g >> 1)) ^ key) << 3);
-          *reinterpret_cast<uint2*>(band + ee) = make_uint2(h01, h23);
-          *reinterpret_cast<uint2*>(band + b.lo_plane + ee) = make_uint2(l01, l23);
-        }
-      }
+    for (int j = 0; j < kL1Pre; ++j) {
+      const int t = wave + kBandWaves * j;
+      if (t < t0n) l1_tile(w0, y0, t, pre.x[j]);
     }
-    __syncthreads();  // planes complete; in0 free
-    const int ntile = nty * a1.tiles_x;
-    band64_layer<NT>(band, b, y0, ty0, ntile, wf1, bias1,
-                     a1.act_out + s * (int64_t)ho * wo * a1.cout, a1.cout, a1.pool, a1.tiles_x, wave,
-                     py, px, m, g, lane);
-    // the waves with one tile fewer stage the next band's input
-    const int64_t nxt = next_item(item + gridDim.x);
-    if (nxt < items) {
-      const int extra = ntile % kBandWaves;
-      stage(nxt, extra ? extra * 64 : 0);
+    for (int t = wave + kBandWaves * kL1Pre; t < t0n; t += kBandWaves) {  // wide images
+      uint4 x[2];
+      l1_load(xin + s * (int64_t)xr * xw, y0, t, x);
+      l1_tile(w0, y0, t, x);
     }
+    __syncthreads();  // planes complete
+    // the next band's first-layer inputs travel while the second layer runs
+    int64_t s2 = 0;
+    int ty2 = 0, nty2 = 0;
+    const int64_t nxt = next_item(item + gridDim.x, &s2, &ty2, &nty2);
+    if (nxt < items) l1_prefetch(s2, ty2, nty2, pre);
+    band64_layer<NT>(lds, b, ty0, nty * a1.tiles_x, wf1, a1.bias,
+                     a1.act_out + s * (int64_t)ho * wo * a1.cout, a1.cout, a1.pool, a1.tiles_x,
+                     wave, py, px, m, g, lane);
     item = nxt;
+    s = s2;
+    ty0 = ty2;
+    nty = nty2;
   }
 }
 
@@ -1294,40 +1385,55 @@ int launch_pair(int nt0, int nt1, const ConvArgs& a0, const ConvArgs& a1, const 
 }
 }  // namespace
 
-// Band plan of a 64-input-channel bf16 layer (k_band64, or with `pair` the
-// fused k_pair64 whose first layer's input band also sits in LDS): the
-// tallest band of at most 16 tiles (4 per wave) whose LDS fits 80 KB, so
+// Band plan of a 64-input-channel bf16 layer (k_band64 / k_pair64): the
+// tallest band of at most 16 tiles (4 per wave) whose planes fit 80 KB, so
 // that two workgroups share a CU, else one band row in up to 160 KB.  False
 // when the layer does not qualify or no band fits.
-int32_t pair64_in0_w(int32_t w) { return pad_row_pixels(8 * ((w + 7) / 8) + 3); }
-
-bool band64_plan(const CnnLayer& L, bool pair, Band64* b, int32_t* band_tiles, size_t* lds) {
+bool band64_plan(const CnnLayer& L, Band64* b, int32_t* band_tiles, size_t* lds) {
   if (L.cin != 64 || (L.cout != 64 && L.cout != 32)) return false;
   int32_t ty, tx;
   conv_tiles(L, &ty, &tx);
-  const int32_t in0_w = pair64_in0_w(L.w);
-  auto bytes = [&](int32_t bt) {
-    const size_t plane = ((size_t)(4 * bt + 2) * L.w + 1) * 64 * 2;
-    return 2 * plane + (pair ? (size_t)(4 * bt + 4) * in0_w * 8 : 0);
+  int32_t wb = L.w + 2;
+  wb += ((4 - wb) % 8 + 8) % 8;  // = 4 (mod 8)
+  auto plan = [&](int32_t bt) {
+    Band64 p{};
+    p.w = L.w;
+    p.h = L.h;
+    p.rows = 4 * bt + 2;
+    p.wb = wb;
+    p.cp = p.rows * wb + 1;
+    p.lo_bytes = 8 * p.cp * 16;
+    return p;
   };
   int32_t bt = 16 / tx;
   if (bt > ty) bt = ty;
   if (bt < 1) bt = 1;
-  while (bt > 1 && bytes(bt) > 80 * 1024) --bt;
-  if (bytes(bt) > 160 * 1024) return false;
-  b->w = L.w;
-  b->h = L.h;
-  b->rows = 4 * bt + 2;
-  b->zp = b->rows * L.w;
-  b->lo_plane = (b->zp + 1) * 64;
+  while (bt > 1 && band64_bytes(plan(bt)) > 80 * 1024) --bt;
+  if (band64_bytes(plan(bt)) > 160 * 1024) return false;
+  *b = plan(bt);
   *band_tiles = bt;
-  *lds = bytes(bt);
+  *lds = band64_bytes(*b);
+  return true;
+}
+
+// The fused k_pair64 plan of a network (first layer 3 -> 64 without pooling,
+// second with 64 input channels), with the size of the pre-processed input
+// per image (xr rows x xw pixels of 8 bytes).
+bool pair64_plan(const Cnn& cnn, Band64* b, int32_t* band_tiles, size_t* lds, int32_t* xr,
+                 int32_t* xw) {
+  if (!cnn.bf16 || cnn.n_layers < 2 || cnn.layers[0].cout != 64 || cnn.layers[0].pool) return false;
+  if (!band64_plan(cnn.layers[1], b, band_tiles, lds)) return false;
+  int32_t ty, tx;
+  conv_tiles(cnn.layers[1], &ty, &tx);
+  *xr = 4 * ty + 4;
+  *xw = 8 * ((cnn.layers[1].w + 7) / 8) + 3;
   return true;
 }
 
 namespace {
 int launch_band64(bool pair, int nt, const ConvArgs& a0, const ConvArgs& a1, const Band64& b,
-                  int32_t in0_w, size_t lds, int64_t max_count, hipStream_t st) {
+                  const uint2* xin, int32_t xr, int32_t xw, size_t lds, int64_t max_count,
+                  hipStream_t st) {
   const int64_t bands = (a1.tiles_y + a1.band_tiles - 1) / a1.band_tiles;
   const int64_t items = (max_count + 7) / 8 * 8 * bands;
   const int64_t per_cu = lds <= 80 * 1024 ? 2 : 1;
@@ -1338,7 +1444,7 @@ int launch_band64(bool pair, int nt, const ConvArgs& a0, const ConvArgs& a1, con
   case N:                                                                                       \
     if (pair)                                                                                   \
       hipLaunchKernelGGL((k_pair64<N>), dim3((unsigned)grid), dim3(64 * kBandWaves), lds, st, a0, \
-                         a1, b, in0_w);                                                         \
+                         a1, b, xin, xr, xw);                                                   \
     else                                                                                        \
       hipLaunchKernelGGL((k_band64<N>), dim3((unsigned)grid), dim3(64 * kBandWaves), lds, st, a1, \
                          b);                                                                    \
@@ -1355,10 +1461,19 @@ int launch_band64(bool pair, int nt, const ConvArgs& a0, const ConvArgs& a1, con
 }
 }  // namespace
 
-// Two ping-pong buffers of fp32 activations per image.
+// Two ping-pong buffers of fp32 activations per image, then (fused 64-channel
+// first pair) the pre-processed bf16 input of every image.
+size_t cnn_xin_bytes(const Cnn& cnn, int64_t max_count) {
+  Band64 b{};
+  int32_t bt = 0, xr = 0, xw = 0;
+  size_t lds = 0;
+  if (!pair64_plan(cnn, &b, &bt, &lds, &xr, &xw)) return 0;
+  return align_up((size_t)xr * xw * 8 * (size_t)(max_count > 0 ? max_count : 0), 256);
+}
+
 size_t cnn_workspace_bytes(const Cnn& cnn, int64_t max_count) {
   const size_t per = align_up(cnn.act_elems * sizeof(float), 256);
-  return 2 * per * (size_t)(max_count > 0 ? max_count : 0) + 256;
+  return 2 * per * (size_t)(max_count > 0 ? max_count : 0) + 256 + cnn_xin_bytes(cnn, max_count);
 }
 
 int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipStream_t stream) {
@@ -1401,17 +1516,25 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
                                     cnn.layers[l].w_off * 2);
   };
   int first_layered = 0;
-  if (cnn.bf16 && cnn.n_layers >= 2 && cnn.layers[0].cout == 64 && !cnn.layers[0].pool) {
+  {
     Band64 b{};
-    int32_t bt = 0;
+    int32_t bt = 0, xr = 0, xw = 0;
     size_t lds = 0;
-    if (band64_plan(cnn.layers[1], true, &b, &bt, &lds)) {
+    if (pair64_plan(cnn, &b, &bt, &lds, &xr, &xw)) {
       ConvArgs a0 = layer_args(0), a1 = layer_args(1);
       a0.wts = frag_weights(0);
       a1.wts = frag_weights(1);
       a1.band_tiles = bt;
-      const int rc = launch_band64(true, cnn.layers[1].cout / 16, a0, a1, b,
-                                   pair64_in0_w(cnn.layers[1].w), lds, r.max_count, stream);
+      uint2* xin = reinterpret_cast<uint2*>(static_cast<unsigned char*>(ws) +
+                                            2 * per * (size_t)r.max_count + 256);
+      int64_t pgrid = (r.max_count * xr * xw + 255) / 256;
+      if (pgrid > kNumCU * 8) pgrid = kNumCU * 8;
+      if (pgrid < 1) pgrid = 1;
+      hipLaunchKernelGGL(k_prep_input, dim3((unsigned)pgrid), dim3(256), 0, stream, a0, xin, xr,
+                         xw);
+      NSC_CHECK_LAUNCH("k_prep_input");
+      const int rc = launch_band64(true, cnn.layers[1].cout / 16, a0, a1, b, xin, xr, xw, lds,
+                                   r.max_count, stream);
       if (rc) return rc;
       first_layered = 2;
     }
@@ -1437,10 +1560,11 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
       Band64 b{};
       int32_t bt = 0;
       size_t lds = 0;
-      if (band64_plan(L, false, &b, &bt, &lds)) {
+      if (band64_plan(L, &b, &bt, &lds)) {
         a.wts = frag_weights(l);
         a.band_tiles = bt;
-        const int rc = launch_band64(false, L.cout / 16, a, a, b, 0, lds, r.max_count, stream);
+        const int rc =
+            launch_band64(false, L.cout / 16, a, a, b, nullptr, 0, 0, lds, r.max_count, stream);
         if (rc) return rc;
         continue;
       }
