@@ -447,6 +447,8 @@ __device__ __forceinline__ void inner_tile(const T* in, const T* wl, int w_lds, 
 // bf16 inner layer with 32 input channels (one K step per tap) and the weight
 // fragments of all 9 taps in registers ([tap][nt]); the hi and lo products go
 // into the same accumulators (registers are the limit here).
+// The LDS reads of tap t + 1 are issued before the MFMAs of tap t (two
+// register pairs; scheduling fences keep them there).
 template <int NT>
 __device__ __forceinline__ void inner_tile32_b(const uint16_t* in, const bf16x8 (&bw)[9][NT],
                                                int cin_lds, int lo_plane, int band_w, int row0,
@@ -454,17 +456,25 @@ __device__ __forceinline__ void inner_tile32_b(const uint16_t* in, const bf16x8 
   using X = Elt<uint16_t>;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const uint16_t* base = in + (row0 * band_w + col0) * cin_lds + g * 8;
+  bf16x8 av[2], av_lo[2];
+  av[0] = X::load(base);
+  av_lo[0] = X::load(base + lo_plane);
 #pragma unroll
   for (int tap = 0; tap < 9; ++tap) {
-    const int dy = tap / 3, dx = tap - 3 * dy;
-    const uint16_t* arow = in + ((row0 + dy) * band_w + col0 + dx) * cin_lds + g * 8;
-    const bf16x8 av = X::load(arow);
-    const bf16x8 av_lo = X::load(arow + lo_plane);
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      acc[nt] = X::mma(av, bw[tap][nt], acc[nt]);
-      acc[nt] = X::mma(av_lo, bw[tap][nt], acc[nt]);
+    const int cur = tap & 1, nxt = cur ^ 1;
+    if (tap + 1 < 9) {
+      const int dy = (tap + 1) / 3, dx = (tap + 1) - 3 * dy;
+      const uint16_t* arow = base + (dy * band_w + dx) * cin_lds;
+      av[nxt] = X::load(arow);
+      av_lo[nxt] = X::load(arow + lo_plane);
     }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[nt] = X::mma(av[cur], bw[tap][nt], acc[nt]);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[nt] = X::mma(av_lo[cur], bw[tap][nt], acc[nt]);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -723,15 +733,50 @@ __device__ __forceinline__ void stage_band64(const float* __restrict__ src, cons
 
 // MFMA accumulation of MT 4x4 output tiles from a staged band; tile i sits at
 // band tile row tr[i], tile column tc[i].  K is tap-major: 9 taps x 2 steps
-// of 32 channels (chunks 0-3, then 4-7).  The weight fragments of the two
-// steps of a tap alternate between two register sets, each loaded one step
-// ahead; the hi products of all tiles are issued before the lo products.
+// of 32 channels (chunks 0-3, then 4-7).  Software pipeline: the weight and
+// activation fragments of the next step are issued before the MFMAs of the
+// current one, in two register sets (steps A and B of a tap), and scheduling
+// fences keep the compiler from sinking those loads to their first use.  The
+// hi products of all tiles are issued before the lo products.
+template <int MT, int NT>
+struct Band64Step {
+  bf16x8 w[NT];
+  bf16x8 xh[MT], xl[MT];
+};
+
+template <int MT, int NT>
+__device__ __forceinline__ void band64_load(const unsigned char* lds, const bf16x8* __restrict__ wp,
+                                            int ks, const uint32_t (&base)[MT],
+                                            const uint32_t (&base_lo)[MT], uint32_t off,
+                                            Band64Step<MT, NT>& st) {
+  using X = Elt<uint16_t>;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) st.w[nt] = wp[(ks * NT + nt) * 64];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    st.xh[i] = X::load(reinterpret_cast<const uint16_t*>(lds + base[i] + off));
+    st.xl[i] = X::load(reinterpret_cast<const uint16_t*>(lds + base_lo[i] + off));
+  }
+}
+
+template <int MT, int NT>
+__device__ __forceinline__ void band64_mma(const Band64Step<MT, NT>& st, f32x4 (&acc)[MT][NT]) {
+  using X = Elt<uint16_t>;
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(st.w[nt], st.xh[i], acc[i][nt]);
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(st.w[nt], st.xl[i], acc[i][nt]);
+}
+
 template <int MT, int NT>
 __device__ __forceinline__ void band64_tiles(const unsigned char* lds, const Band64& b,
                                              const bf16x8* __restrict__ wf, const int (&tr)[MT],
                                              const int (&tc)[MT], int py, int px, int g, int lane,
                                              f32x4 (&acc)[MT][NT]) {
-  using X = Elt<uint16_t>;
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -744,46 +789,24 @@ __device__ __forceinline__ void band64_tiles(const unsigned char* lds, const Ban
   }
   const uint32_t step2 = (uint32_t)b.cp * 64u;  // chunks 4..7: 4 chunk planes on
   const bf16x8* wp = wf + lane;
-  bf16x8 wa[NT], wb[NT];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) wa[nt] = wp[nt * 64];
+  Band64Step<MT, NT> sa, sb;
+  band64_load<MT, NT>(lds, wp, 0, base, base_lo, 0u, sa);
 #pragma unroll 1
   for (int tap = 0; tap < 9; ++tap) {
     const int dy = tap / 3, dx = tap - 3 * dy;
     const uint32_t toff = (uint32_t)(dy * b.wb + dx) * 16u;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) wb[nt] = wp[((2 * tap + 1) * NT + nt) * 64];
-    bf16x8 xh[MT], xl[MT];
-#pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      xh[i] = X::load(reinterpret_cast<const uint16_t*>(lds + base[i] + toff));
-      xl[i] = X::load(reinterpret_cast<const uint16_t*>(lds + base_lo[i] + toff));
-    }
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(wa[nt], xh[i], acc[i][nt]);
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(wa[nt], xl[i], acc[i][nt]);
-    // the next tap's first step (the last tap reloads a valid fragment, unused)
-    const int kn = tap < 8 ? 2 * tap + 2 : 2 * tap;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) wa[nt] = wp[(kn * NT + nt) * 64];
-#pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      xh[i] = X::load(reinterpret_cast<const uint16_t*>(lds + base[i] + toff + step2));
-      xl[i] = X::load(reinterpret_cast<const uint16_t*>(lds + base_lo[i] + toff + step2));
-    }
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(wb[nt], xh[i], acc[i][nt]);
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(wb[nt], xl[i], acc[i][nt]);
+    // step B of this tap in flight while step A computes
+    band64_load<MT, NT>(lds, wp, 2 * tap + 1, base, base_lo, toff + step2, sb);
+    __builtin_amdgcn_sched_barrier(0);
+    band64_mma<MT, NT>(sa, acc);
+    __builtin_amdgcn_sched_barrier(0);
+    // step A of the next tap (the last tap reloads its own, unused)
+    const int tn = tap < 8 ? tap + 1 : tap;
+    const int dyn = tn / 3, dxn = tn - 3 * dyn;
+    band64_load<MT, NT>(lds, wp, 2 * tn, base, base_lo, (uint32_t)(dyn * b.wb + dxn) * 16u, sa);
+    __builtin_amdgcn_sched_barrier(0);
+    band64_mma<MT, NT>(sb, acc);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -882,7 +905,7 @@ __device__ __forceinline__ void band64_layer(const unsigned char* lds, const Ban
 
 // One 64-input-channel layer over bands of fp32 activations.
 template <int NT>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_band64(ConvArgs a, Band64 b) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int lane = threadIdx.x & 63;
@@ -961,17 +984,11 @@ __global__ void __launch_bounds__(256) k_prep_input(ConvArgs a, uint2* xin, int3
 // (with the halo rows) from the pre-processed input (k_prep_input) straight
 // into the hi / lo planes, then the second layer runs from them.  First-layer
 // tiles are 2 rows x 8 columns; its K is (dy, dx of 4, c of 4) = 48 of 64.
-// Each wave loads its first-layer inputs of the next band (up to kL1Pre tiles)
-// into registers before running the second layer of the current one, so
-// that their HBM latency passes under the second layer's MFMA work.
-constexpr int kL1Pre = 6;
-
-struct L1Frags {
-  uint4 x[kL1Pre][2];  // per tile: the K chunks of steps 0 and 1
-};
+// A wave loads the input of its next first-layer tile while computing the
+// current one.
 
 template <int NT>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int32_t xr,
          int32_t xw) {
   using X = Elt<uint16_t>;
@@ -1026,15 +1043,6 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     x[0] = make_uint4(p00.x, p00.y, p01.x, p01.y);
     x[1] = make_uint4(p10.x, p10.y, p11.x, p11.y);
   };
-  auto l1_prefetch = [&](int64_t s, int ty0, int nty, L1Frags& f) {
-    const uint2* xs = xin + s * (int64_t)xr * xw;
-    const int t0n = (2 * nty + 1) * tx0;
-#pragma unroll
-    for (int j = 0; j < kL1Pre; ++j) {
-      const int t = wave + kBandWaves * j;
-      if (t < t0n) l1_load(xs, 4 * ty0 - 1, t, f.x[j]);
-    }
-  };
   // first-layer tile t: 8 MFMAs, bias, ReLU, hi / lo split into the planes
   auto l1_tile = [&](const bf16x8 (&w0)[2][4], int y0, int t, const uint4 (&x)[2]) {
     const int ti = t / tx0, tj = t - ti * tx0;
@@ -1071,40 +1079,35 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
   int64_t s = 0;
   int ty0 = 0, nty = 0;
   int64_t item = next_item(blockIdx.x, &s, &ty0, &nty);
-  L1Frags pre;
-  if (item < items) l1_prefetch(s, ty0, nty, pre);
   while (item < items) {
     const int y0 = 4 * ty0 - 1;
     const int t0n = (2 * nty + 1) * tx0;  // first-layer tiles: rows 4 nty + 2
+    const uint2* xs = xin + s * (int64_t)xr * xw;
+    uint4 xc[2], xn[2];
+    if (wave < t0n) l1_load(xs, y0, wave, xc);
+    // first-layer weights for this band's first-layer phase only: an opaque
+    // zero keeps the compiler from hoisting them out of the band loop (which
+    // would hold 32 registers through the second layer)
+    int opaque = 0;
+    asm volatile("" : "+s"(opaque));
+    const bf16x8* w0p = wf0 + opaque + lane;
     bf16x8 w0[2][4];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) w0[ks][nt] = wf0[(ks * 4 + nt) * 64 + lane];
+      for (int nt = 0; nt < 4; ++nt) w0[ks][nt] = w0p[(ks * 4 + nt) * 64];
     __syncthreads();  // the previous band's second layer is done with the planes
-#pragma unroll
-    for (int j = 0; j < kL1Pre; ++j) {
-      const int t = wave + kBandWaves * j;
-      if (t < t0n) l1_tile(w0, y0, t, pre.x[j]);
-    }
-    for (int t = wave + kBandWaves * kL1Pre; t < t0n; t += kBandWaves) {  // wide images
-      uint4 x[2];
-      l1_load(xin + s * (int64_t)xr * xw, y0, t, x);
-      l1_tile(w0, y0, t, x);
+    for (int t = wave; t < t0n; t += kBandWaves) {
+      if (t + kBandWaves < t0n) l1_load(xs, y0, t + kBandWaves, xn);
+      l1_tile(w0, y0, t, xc);
+      xc[0] = xn[0];
+      xc[1] = xn[1];
     }
     __syncthreads();  // planes complete
-    // the next band's first-layer inputs travel while the second layer runs
-    int64_t s2 = 0;
-    int ty2 = 0, nty2 = 0;
-    const int64_t nxt = next_item(item + gridDim.x, &s2, &ty2, &nty2);
-    if (nxt < items) l1_prefetch(s2, ty2, nty2, pre);
     band64_layer<NT>(lds, b, ty0, nty * a1.tiles_x, wf1, a1.bias,
                      a1.act_out + s * (int64_t)ho * wo * a1.cout, a1.cout, a1.pool, a1.tiles_x,
                      wave, py, px, m, g, lane);
-    item = nxt;
-    s = s2;
-    ty0 = ty2;
-    nty = nty2;
+    item = next_item(item + gridDim.x, &s, &ty0, &nty);
   }
 }
 
