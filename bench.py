@@ -1,20 +1,30 @@
 #!/usr/bin/env python3
 """Cascade frames/s on one MI355X, with roofline fractions and the oracle's CPU rate.
 
-Workload: 100,000 synthetic fixed-camera frames of 640x480 RGB uint8, already
-resident in HBM; area downsample to 50x50, global MSE against frame t-15,
-delta_diff = 15; specialized CNN (2 x conv3x3 32 + ReLU + max-pool, dense 128,
-bf16) on the frames that fire; c_low = 0.2, c_high = 0.8.  One step is one
-nsc_cascade_run over all frames (downsample, detector, compaction, CNN,
-decisions and label resolution).
+Workload (default): 100,000 synthetic fixed-camera frames of 640x480 RGB
+uint8, already resident in HBM; area downsample to 50x50, global MSE against
+frame t-15, delta_diff = 15; specialized CNN (2 x conv3x3 32 + ReLU +
+max-pool, dense 128, bf16) on the frames that fire; c_low = 0.2, c_high =
+0.8.  One step is one nsc_cascade_run over all frames (downsample, detector,
+compaction, CNN, decisions and label resolution).
 
-With --workload fhd-stream it instead runs the 1,000,000-frame 1920x1080 video
-(detector 100x100, 10x10 blocked logistic score against frame t-30, 4-layer
-64-channel bf16 CNN) in chunks of 4096 through two frame buffers on two
-streams, the synthetic generator filling one buffer while the cascade reads the
-other.  Its `value` is the cascade-only rate (each chunk's cascade timed alone
-with HIP events, generator time excluded, as the paper excludes decoding); the
-overlapped wall-clock rate, bound by the generator, is reported beside it.
+--workload hd-ref / hd-blocked / fhd-stream run the larger videos in chunks
+through two frame buffers on two streams, the synthetic generator filling one
+buffer while the cascade reads the other:
+  hd-ref      100,000 frames of 1280x720, MSE against a fixed median-background
+              image, 4-layer 64-channel CNN (the CNN-heavy regime), chunks of 16,384;
+  hd-blocked  200,000 frames of 1280x720, 10x10 blocked logistic score against
+              frame t-1, 3-layer 64-channel CNN, chunks of 16,384;
+  fhd-stream  1,000,000 frames of 1920x1080, blocked score against frame t-30,
+              4-layer 64-channel CNN, chunks of 4,096.
+Their `value` is the cascade-only rate (each chunk's cascade timed alone with
+HIP events, generator time excluded, as the paper excludes decoding); the
+overlapped wall-clock rate, bound by the generator, is reported beside it, and
+the stage split comes from events at the stage boundaries of every chunk.
+
+Every run also measures the peaks the roofline fractions are quoted against:
+a streaming read of the resident frame buffer (HBM) and a loop of independent
+bf16 MFMAs, next to the published 8 TB/s and 2.5 PFLOP/s.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -110,7 +120,50 @@ def cnn_flops(spec) -> int:
     return f + 2 * flat * spec.dense + 2 * spec.dense
 
 
-def cpu_baseline(wl, budget_s: float) -> dict:
+def measured_peaks(torch, buf, nbytes: int) -> dict:
+    """Streaming read of `nbytes` of the device buffer `buf` (HBM) and a loop of
+    independent bf16 MFMAs, timed with events on torch's current stream (the
+    probes are launched there): the best of three runs each."""
+    import synth
+
+    lib = ctypes.CDLL(synth.SYNTH_SO)
+    lib.probe_read_launch.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                      ctypes.c_int32, ctypes.c_void_p]
+    lib.probe_mfma_launch.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                      ctypes.c_void_p]
+    dev = buf.device
+    out = torch.zeros(4, dtype=torch.int32, device=dev)
+    st = torch.cuda.current_stream(dev)
+    nbytes = nbytes // 16 * 16
+
+    def timed(launch):
+        best = None
+        for rep in range(4):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            if launch() != 0:
+                raise RuntimeError("probe launch failed")
+            e1.record(st)
+            e1.synchronize()
+            if rep:
+                ms = e0.elapsed_time(e1)
+                best = ms if best is None else min(best, ms)
+        return best
+
+    read_ms = timed(lambda: lib.probe_read_launch(ctypes.c_void_p(buf.data_ptr()), nbytes,
+                                                  ctypes.c_void_p(out.data_ptr()), 8192,
+                                                  ctypes.c_void_p(st.cuda_stream)))
+    iters, grid = 20000, 2048
+    mfma_ms = timed(lambda: lib.probe_mfma_launch(iters, grid, ctypes.c_void_p(out.data_ptr()),
+                                                  ctypes.c_void_p(st.cuda_stream)))
+    flop = grid * 4 * iters * 8 * 16 * 16 * 32 * 2
+    res = {"hbm_read_gbs": nbytes / (read_ms * 1e-3) / 1e9, "hbm_read_bytes": nbytes,
+           "mfma_bf16_tflops": flop / (mfma_ms * 1e-3) / 1e12}
+    log(f"measured peaks: {res}")
+    return res
+
+
+def cpu_baseline(wl, budget_s: float, lr_w=None, ref_img=None) -> dict:
     """The oracle, single-threaded, on a contiguous window of the same video."""
     import numpy as np
 
@@ -119,45 +172,69 @@ def cpu_baseline(wl, budget_s: float) -> dict:
 
     v = synth.Video(wl.video)
     blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
-    cfg, keep = oracle.make_cfg(wl)
+    ref_sums = oracle.area_sums(ref_img, wl.dd_h, wl.dd_w) if ref_img is not None else None
+    cfg, keep = oracle.make_cfg(wl, lr_w=lr_w, ref_sums=ref_sums)
     occ = v.occupied
     start = int(np.flatnonzero(occ)[0]) if occ.any() else 0
     start = max(0, start - 200)
-    # probe 40 frames to size the sample to the budget
-    probe = v.frames(start, start + 40)
+    # probe a few frames to size the sample to the budget
+    n_probe = 40 if wl.video.w <= 640 else 8
+    probe = v.frames(start, start + n_probe)
     t = time.perf_counter()
     oracle.cascade(cfg, wl.cnn, blob, probe, t0=0)
-    per = (time.perf_counter() - t) / 40
-    n = int(max(100, min(4000, budget_s / max(per, 1e-6))))
+    per = (time.perf_counter() - t) / n_probe
+    n = int(max(16, min(4000, budget_s / max(per, 1e-6))))
     log(f"cpu baseline: oracle ~{per * 1e3:.1f} ms/frame, sampling {n} frames from {start}")
     frames = v.frames(start, start + n)
     t = time.perf_counter()
     out, _ = oracle.cascade(cfg, wl.cnn, blob, frames, t0=0)
     dt = time.perf_counter() - t
+    forced = f"first {wl.delta} forced to fire; " if wl.ref_mode == 0 else ""
     return {"value": n / dt, "unit": "frames/s", "cores": 1, "kind": "oracle",
             "sample": f"frames [{start}, {start + n}) of the same video run as their own video "
-                      f"(first {wl.delta} forced to fire); {out['fired']} fired "
-                      f"({out['fired'] / n:.1%}); {dt:.1f} s single-threaded fp64; "
-                      f"host has {os.cpu_count()} logical CPUs"}
+                      f"({forced}{out['fired']} fired, {out['fired'] / n:.1%}); {dt:.1f} s "
+                      f"single-threaded fp64; host has {os.cpu_count()} logical CPUs"}
 
 
-def bench_stream(args):
-    """The chunked 1080p million-frame run (see the module docstring)."""
+CHUNKED = ("hd-ref", "hd-blocked", "fhd-stream")
+
+
+def bench_chunked(args):
+    """A larger video in chunks through two frame buffers (see the module docstring)."""
+    import numpy as np
     import torch
 
+    import paper_1703_02529_amd as nsc
     import synth
     from paper_1703_02529_amd.streaming import StreamingCascade
     from synth import workloads as W
 
-    wl = W.FHD_STREAM
-    n, fb, chunk = wl.video.n, wl.video.frame_bytes, wl.chunk
+    wl = {"hd-ref": W.HD_REF, "hd-blocked": W.HD_BLOCKED, "fhd-stream": W.FHD_STREAM}[args.workload]
+    chunk = wl.chunk or 16384
+    n, fb = wl.video.n, wl.video.frame_bytes
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     v = synth.Video(wl.video)
     tables = v.device_tables(dev)
     blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
-    lr = synth.lr_weights(wl.grid[0] * wl.grid[1], wl.weight_seed, wl.lr_bias)[0]
-    sc = StreamingCascade(wl, blob, chunk, lr_w=torch.from_numpy(lr).to(dev), device=dev)
+    lr = lr_d = None
+    if wl.grid != (1, 1):
+        lr = synth.lr_weights(wl.grid[0] * wl.grid[1], wl.weight_seed, wl.lr_bias)[0]
+        lr_d = torch.from_numpy(lr).to(dev)
+    ref_img = ref_d = None
+    if wl.ref_mode == W.FIXED:
+        # the median-background reference image (untimed setup): frames 0, 10, ..., 1000
+        # rendered on the device, per-pixel median (odd count: the middle value)
+        ts = list(range(0, 1001, 10))
+        stack = torch.empty(len(ts), fb, dtype=torch.uint8, device=dev)
+        for i, t in enumerate(ts):
+            v.render_device(stack[i], t, 1, tables)
+        med = stack.view(len(ts), -1).to(torch.int16).median(dim=0).values.to(torch.uint8)
+        del stack
+        ref_img = med.cpu().numpy().reshape(wl.video.h, wl.video.w, 3)
+        ref_d = torch.empty(wl.dd_h * wl.dd_w * 3, dtype=torch.int32, device=dev)
+        nsc.nsc_downsample(med, 1, wl.video.h, wl.video.w, wl.dd_h, wl.dd_w, ref_d)
+    sc = StreamingCascade(wl, blob, chunk, lr_w=lr_d, ref_sums=ref_d, device=dev)
     label = torch.empty(n, dtype=torch.uint8, device=dev)
     defer = torch.empty(n, dtype=torch.uint8, device=dev)
     fire = torch.empty(n, dtype=torch.uint8, device=dev)
@@ -166,21 +243,34 @@ def bench_stream(args):
         v.render_device(buf, t0, m, tables, stream=stream)
 
     log(f"workload {wl.name}: {n} frames x {fb} bytes in chunks of {chunk}")
+    peaks = measured_peaks(torch, sc.bufs[0], chunk * fb)
     for _ in range(args.warmup):
-        sc.run(2 * chunk, produce, label, defer, fire=fire)
+        sc.run(min(n, 2 * chunk), produce, label, defer, fire=fire)
     torch.cuda.synchronize()
-    alone, over = [], []
+    hip = HipEvents()
+    n_chunks = -(-n // chunk)
+    evs = [hip.create(6) for _ in range(n_chunks)]
+    alone, over, stage_tot = [], [], np.zeros(5)
     for k in range(args.steps):
-        alone.append(sc.run(n, produce, label, defer, fire=fire, timing=True, overlap=False))
+        alone.append(sc.run(n, produce, label, defer, fire=fire, timing=True, overlap=False,
+                            stage_events=lambda j: evs[j]))
+        stage_tot += np.array([[hip.ms(e[i], e[i + 1]) for i in range(5)] for e in evs]).sum(0)
         log(f"pass {k}: chunks run alone: {alone[-1]}")
         over.append(sc.run(n, produce, label, defer, fire=fire, timing=True, overlap=True))
         log(f"pass {k}: overlapped: {over[-1]}")
+    for e in evs:
+        hip.destroy(e)
     fired = int(fire.sum().item())
     sc.close()
+    stage = stage_tot / args.steps
     casc_ms = sum(a["cascade_ms"] for a in alone) / len(alone)
     wall_ms = sum(o["wall_ms"] for o in over) / len(over)
+    area_ms, cnn_ms = float(stage[0]), float(stage[3])
+    achieved = n * fb / (area_ms * 1e-3) / 1e9
+    cnn_tflops = fired * cnn_flops(wl.cnn) / (cnn_ms * 1e-3) / 1e12 if cnn_ms > 0 else 0.0
+    layers = ", ".join(f"{c}{'+pool' if p else ''}" for c, p in zip(wl.cnn.conv, wl.cnn.pool))
     result = {
-        "metric": "cascade frames/sec on 1 MI355X (chunked 1080p stream)",
+        "metric": "cascade frames/sec on 1 MI355X + % HBM roofline (diff) / % MFMA peak (CNN)",
         "value": n / (casc_ms * 1e-3),
         "unit": "frames/s",
         "n_gpus": 1,
@@ -193,26 +283,57 @@ def bench_stream(args):
         "dtype": "u8 frames, i32/i64 detector, bf16 CNN (fp32 accumulate)",
         "data": "synthetic",
         "config": {"workload": wl.name, "frames": n, "frame": f"{wl.video.w}x{wl.video.h} RGB u8",
-                   "chunk": chunk, "fired": fired},
+                   "chunk": chunk,
+                   "detector": f"{wl.dd_w}x{wl.dd_h}, " + (
+                       "fixed median-background reference" if wl.ref_mode == W.FIXED else
+                       f"frame t-{wl.delta}") + (
+                       f", {wl.grid[0]}x{wl.grid[1]} blocked logistic score" if wl.grid != (1, 1)
+                       else ", global MSE") + f", delta_diff {wl.delta_diff}",
+                   "cnn": f"conv3x3 [{layers}], dense {wl.cnn.dense}, sigmoid; bf16",
+                   "c_low": wl.c_low, "c_high": wl.c_high, "fired": fired},
+        "roofline": {
+            "bound": "hbm",
+            "kernel": AREA_KERNEL,
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": None,
+            "traffic_source": "counters were taken on the 640x480 workload only",
+            "bytes_per_launch": chunk * fb,
+            "avg_launch_ms": area_ms / n_chunks,
+            "measured_peak": peaks["hbm_read_gbs"],
+            "frac_of_measured": achieved / peaks["hbm_read_gbs"],
+        },
+        "stages_ms": {"area_sums": area_ms, "detector": float(stage[1]),
+                      "compaction": float(stage[2]), "cnn": cnn_ms, "resolve": float(stage[4])},
+        "cnn_mfma": {"achieved_tflops": cnn_tflops, "peak_tflops": BF16_PEAK_TFLOPS,
+                     "frac": cnn_tflops / BF16_PEAK_TFLOPS,
+                     "measured_peak_tflops": peaks["mfma_bf16_tflops"],
+                     "frac_of_measured": cnn_tflops / peaks["mfma_bf16_tflops"],
+                     "flop_per_survivor": cnn_flops(wl.cnn), "survivors": fired},
         "cascade_only_ms": casc_ms,
         "overlapped_wall_ms": wall_ms,
         "overlapped_wall_fps": n / (wall_ms * 1e-3),
         "note": "value: each chunk's cascade timed alone with HIP events (generator excluded); "
                 "overlapped: generator filling the other buffer concurrently, wall clock",
     }
+    torch.cuda.empty_cache()
+    result["cpu_baseline"] = (cpu_baseline(wl, args.cpu_seconds, lr_w=lr, ref_img=ref_img)
+                              if args.cpu_seconds > 0 else None)
     print(json.dumps(result), flush=True)
 
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=None, help="timed steps (20; fhd-stream: 1)")
-    ap.add_argument("--warmup", type=int, default=None, help="warm-up steps (3; fhd-stream: 1)")
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (20; chunked: 1)")
+    ap.add_argument("--warmup", type=int, default=None, help="warm-up steps (3; chunked: 1)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="oracle time budget for the CPU baseline (0 disables it)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain copy of known size (for counter calibration)")
-    ap.add_argument("--workload", choices=("vga", "fhd-stream"), default="vga")
+    ap.add_argument("--workload", choices=("vga",) + CHUNKED, default="vga")
     ap.add_argument("--check-stride", type=int, default=1,
                     help="frame skipping on the 640x480 workload: check every s-th frame "
                          "(s must divide 15); 1 is the headline configuration")
@@ -222,13 +343,13 @@ def main():
               f"streams; see the design notes for how it would shard): got --gpus {args.gpus}",
               file=sys.stderr)
         sys.exit(2)
-    stream = args.workload == "fhd-stream"
+    chunked = args.workload in CHUNKED
     if args.steps is None:
-        args.steps = 1 if stream else 20
+        args.steps = 1 if chunked else 20
     if args.warmup is None:
-        args.warmup = 1 if stream else 3
-    if stream:
-        bench_stream(args)
+        args.warmup = 1 if chunked else 3
+    if chunked:
+        bench_chunked(args)
         return
 
     import numpy as np
@@ -255,6 +376,7 @@ def main():
 
     if args.calibrate_copy:
         copy_calibration(torch, dev)
+    peaks = measured_peaks(torch, frames, n * fb)
 
     blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
     run = CascadeRunner(wl, blob, max_frames=n, device=dev)
@@ -327,6 +449,8 @@ def main():
             "traffic_source": traffic_src,
             "bytes_per_launch": area_bytes,
             "avg_launch_ms": area_ms,
+            "measured_peak": peaks["hbm_read_gbs"],
+            "frac_of_measured": achieved / peaks["hbm_read_gbs"],
         },
         "stages_ms": {
             "area_sums": area_ms,
@@ -340,6 +464,8 @@ def main():
             "achieved_tflops": cnn_tflops,
             "peak_tflops": BF16_PEAK_TFLOPS,
             "frac": cnn_tflops / BF16_PEAK_TFLOPS,
+            "measured_peak_tflops": peaks["mfma_bf16_tflops"],
+            "frac_of_measured": cnn_tflops / peaks["mfma_bf16_tflops"],
             "flop_per_survivor": cnn_flops(wl.cnn),
             "survivors": fired,
         },

@@ -3,7 +3,8 @@
     python -m paper_1703_02529_amd.build
 
 produces paper_1703_02529_amd/libnsc.so (the cascade) and synth/libsynth.so
-(the synthetic-video renderer used by tests and the benchmark).
+(the synthetic-video renderer used by tests and the benchmark, and the
+benchmark's peak probes).
 """
 from __future__ import annotations
 
@@ -59,7 +60,8 @@ def build_nsc() -> str:
 
 def build_synth() -> str:
     tmp = LIBSYNTH + ".tmp"
-    _run([HIPCC, *HIP_FLAGS, "-shared", os.path.join(SYNTH_DIR, "synth_kernel.hip"), "-o", tmp])
+    _run([HIPCC, *HIP_FLAGS, "-shared", os.path.join(SYNTH_DIR, "synth_kernel.hip"),
+          os.path.join(SYNTH_DIR, "probe_kernel.hip"), "-o", tmp])
     os.replace(tmp, LIBSYNTH)
     return LIBSYNTH
 

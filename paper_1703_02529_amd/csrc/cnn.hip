@@ -21,10 +21,11 @@
 // bf16 roundings of intermediate values.
 //
 // The dense layer is a GEMM over 16-survivor tiles (M) x hidden units (N) x
-// features (K) on the same MFMA shapes; its epilogue adds the bias, applies
-// ReLU, folds the 1-unit output layer in with a 16-lane
-// shuffle reduction, and writes the logit, the sigmoid confidence and the
-// c_low / c_high decision of each frame.
+// features (K) on the same MFMA shapes, one workgroup per tile whose waves
+// split K and add their partial sums through LDS; its epilogue adds the bias,
+// applies ReLU, folds the 1-unit output layer in with a 16-lane shuffle
+// reduction, and writes the logit, the sigmoid confidence and the c_low /
+// c_high decision of each frame.
 #include "nsc_internal.h"
 
 #include <math.h>
@@ -1130,20 +1131,31 @@ struct DenseArgs {
   double c_low, c_high;
 };
 
+// Waves of a dense workgroup: they split K, so that a group of 16 survivors
+// is a short dependence chain per wave even when there are few groups.
+template <int NT>
+constexpr int dense_waves() {
+  return NT >= 16 ? 4 : 8;
+}
+
 template <typename T, int NT>
-__global__ void __launch_bounds__(256) k_dense(DenseArgs a) {
+__global__ void __launch_bounds__(512) k_dense(DenseArgs a) {
   using X = Elt<T>;
   constexpr int E = X::E, KS = X::KS;
   constexpr bool SPLIT = X::SPLIT;
+  constexpr int NW = dense_waves<NT>();
+  // per wave and output tile, each lane's 4 partial sums
+  __shared__ f32x4 part[NW][NT][64];
   const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int m = lane & 15, g = lane >> 4;
   int64_t cnt = *a.count;
   if (cnt > a.max_count) cnt = a.max_count;
   const int64_t groups = (cnt + 15) / 16;
-  const int64_t wave_id = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  const int64_t nwaves = (int64_t)gridDim.x * (blockDim.x >> 6);
+  const int nks = (a.flat + KS - 1) / KS;  // K steps
+  const int ks0 = wave * nks / NW, ks1 = (wave + 1) * nks / NW;
   const T* w1 = reinterpret_cast<const T*>(a.w1);
-  for (int64_t grp = wave_id; grp < groups; grp += nwaves) {
+  for (int64_t grp = blockIdx.x; grp < groups; grp += gridDim.x) {
     const int64_t s = grp * 16 + m;
     const bool valid = s < cnt;
     const float* arow = a.feat + (valid ? s : 0) * (int64_t)a.flat + g * E;
@@ -1155,7 +1167,8 @@ __global__ void __launch_bounds__(256) k_dense(DenseArgs a) {
     }
     // flat is a multiple of 16 (and of E): a lane group's E values of the last,
     // partial K step are either all inside or all past the end (zero)
-    for (int k0 = 0; k0 < a.flat; k0 += KS) {
+    for (int ks = ks0; ks < ks1; ++ks) {
+      const int k0 = ks * KS;
       const bool kin = k0 + g * E < a.flat;
       typename X::frag av = X::zero(), av_lo = X::zero();
       if constexpr (SPLIT) {
@@ -1171,44 +1184,53 @@ __global__ void __launch_bounds__(256) k_dense(DenseArgs a) {
         if constexpr (SPLIT) acc_lo[nt] = X::mma(av_lo, bv, acc_lo[nt]);
       }
     }
-    if constexpr (SPLIT) {
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[nt] += acc_lo[nt];
-    }
-    // hidden = ReLU(acc + b1); z = b2 + sum_n w2[n] * hidden[n]
-    float part[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const int n = nt * 16 + m;
-      const float b = a.b1[n], w = a.w2[n];
+      if constexpr (SPLIT) acc[nt] += acc_lo[nt];
+      part[wave][nt][lane] = acc[nt];
+    }
+    __syncthreads();
+    if (wave == 0) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float hval = fmaxf(acc[nt][r] + b, 0.0f);
-        part[r] += w * hval;
+      for (int nt = 0; nt < NT; ++nt) {
+        f32x4 t = part[0][nt][lane];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) t += part[w][nt][lane];
+        acc[nt] = t;
       }
-    }
+      // hidden = ReLU(acc + b1); z = b2 + sum_n w2[n] * hidden[n]
+      float sum[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+      for (int nt = 0; nt < NT; ++nt) {
+        const int n = nt * 16 + m;
+        const float b = a.b1[n], w = a.w2[n];
 #pragma unroll
-      for (int o = 1; o < 16; o <<= 1) part[r] += __shfl_xor(part[r], o, 64);
-    }
-    if (m == 0) {
+        for (int r = 0; r < 4; ++r) sum[r] += w * fmaxf(acc[nt][r] + b, 0.0f);
+      }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t slot = grp * 16 + 4 * g + r;
-        if (slot < cnt) {
-          const float z = part[r] + a.b2;
-          const double p = 1.0 / (1.0 + exp(-(double)z));
-          a.logit[slot] = z;
-          if (a.prob) a.prob[slot] = (float)p;
-          if (a.dec || a.frame_logit) {
-            const int32_t f = a.idx[slot];
-            if (a.dec) a.dec[f] = p < a.c_low ? 0 : (p > a.c_high ? 1 : 2);
-            if (a.frame_logit) a.frame_logit[f] = z;
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) sum[r] += __shfl_xor(sum[r], o, 64);
+      }
+      if (m == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t slot = grp * 16 + 4 * g + r;
+          if (slot < cnt) {
+            const float z = sum[r] + a.b2;
+            const double p = 1.0 / (1.0 + exp(-(double)z));
+            a.logit[slot] = z;
+            if (a.prob) a.prob[slot] = (float)p;
+            if (a.dec || a.frame_logit) {
+              const int32_t f = a.idx[slot];
+              if (a.dec) a.dec[f] = p < a.c_low ? 0 : (p > a.c_high ? 1 : 2);
+              if (a.frame_logit) a.frame_logit[f] = z;
+            }
           }
         }
       }
     }
+    __syncthreads();  // the partial sums are read before the next group writes them
   }
 }
 
@@ -1239,9 +1261,9 @@ int launch_conv_nt(int nt, const ConvArgs& a, unsigned grid, size_t lds, hipStre
 
 template <typename T>
 int launch_dense_nt(int nt, const DenseArgs& a, unsigned grid, hipStream_t st) {
-#define NSC_DENSE_CASE(N)                                                          \
-  case N:                                                                          \
-    hipLaunchKernelGGL((k_dense<T, N>), dim3(grid), dim3(256), 0, st, a);           \
+#define NSC_DENSE_CASE(N)                                                                  \
+  case N:                                                                                  \
+    hipLaunchKernelGGL((k_dense<T, N>), dim3(grid), dim3(64 * dense_waves<N>()), 0, st, a); \
     break;
   switch (nt) {
     NSC_DENSE_CASE(1)
@@ -1609,9 +1631,9 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
   d.frame_logit = r.frame_logit;
   d.c_low = r.c_low;
   d.c_high = r.c_high;
-  int64_t groups = (r.max_count + 15) / 16;
-  int64_t grid = (groups + 3) / 4;
-  if (grid > kNumCU * 8) grid = kNumCU * 8;
+  int64_t groups = (r.max_count + 15) / 16;  // one workgroup per 16-survivor group
+  int64_t grid = groups;
+  if (grid > kNumCU * 2) grid = kNumCU * 2;
   if (grid < 1) grid = 1;
   const int nt = cnn.dense / 16;
   return cnn.bf16 ? launch_dense_nt<uint16_t>(nt, d, (unsigned)grid, stream)

@@ -46,7 +46,7 @@ class StreamingCascade:
     def run(self, n_total: int, produce: Producer, label: torch.Tensor, defer: torch.Tensor,
             score: Optional[torch.Tensor] = None, fire: Optional[torch.Tensor] = None,
             logit: Optional[torch.Tensor] = None, timing: bool = False, t_start: int = 0,
-            overlap: bool = True):
+            overlap: bool = True, stage_events: Optional[Callable[[int], list]] = None):
         """Runs frames [t_start, t_start + n_total) in chunks; per-frame outputs
         (device tensors of at least n_total entries, indexed from t_start) are
         written in place.  t_start is 0 or the frame where the previous run
@@ -57,7 +57,9 @@ class StreamingCascade:
         when `timing` is set, cascade_ms (sum over chunks of the cascade
         stream's time per chunk, the waits for fills excluded; with overlap it
         includes slowdown from sharing the GPU with the fills) and wall_ms
-        (first fill to last result)."""
+        (first fill to last result).  stage_events(k), when given, returns the
+        NSC_STAGE_EVENTS raw event handles that chunk k's cascade records at
+        its stage boundaries."""
         for name, t in (("label", label), ("defer", defer), ("score", score), ("fire", fire),
                         ("logit", logit)):
             if t is not None and t.numel() < n_total:
@@ -95,7 +97,9 @@ class StreamingCascade:
             nsc_cascade_run(r.cfg, r.cnn, self.bufs[b], m, t0, r.state, r.ws, label[sl], defer[sl],
                             score=score[sl] if score is not None else None,
                             fire=fire[sl] if fire is not None else None,
-                            logit=logit[sl] if logit is not None else None, stream=self.s_run)
+                            logit=logit[sl] if logit is not None else None,
+                            stage_events=stage_events(k) if stage_events is not None else None,
+                            stream=self.s_run)
             if timing:
                 ends[-1].record(self.s_run)
             consumed[b].record(self.s_run)

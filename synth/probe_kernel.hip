@@ -1,0 +1,71 @@
+// Measured peaks for the benchmark's roofline figures (measurement
+// infrastructure, not part of the cascade): a streaming read of a device
+// buffer, and a loop of independent bf16 MFMAs.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace {
+
+// Every thread reads 16-byte vectors a grid stride apart, four in flight; the
+// folded value is stored only under a condition that the data never meets, so
+// the loads stay live without any writes.
+__global__ void __launch_bounds__(256) probe_read(const uint4* __restrict__ p, int64_t n16,
+                                                  uint32_t* out) {
+  uint32_t acc = 0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (; i + 3 * stride < n16; i += 4 * stride) {
+    const uint4 a = p[i], b = p[i + stride], c = p[i + 2 * stride], d = p[i + 3 * stride];
+    acc ^= a.x ^ b.y ^ c.z ^ d.w ^ a.w ^ b.x ^ c.y ^ d.z;
+  }
+  for (; i < n16; i += stride) {
+    const uint4 v = p[i];
+    acc ^= v.x ^ v.w;
+  }
+  if (acc == 0x9E3779B9u) out[0] = acc;
+}
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Each wave runs `iters` rounds of 8 independent v_mfma_f32_16x16x32_bf16
+// (16 x 16 x 32 x 2 = 16,384 FLOP each) on register operands.
+__global__ void __launch_bounds__(256) probe_mfma(int32_t iters, float* out) {
+  const int lane = threadIdx.x & 63;
+  bf16x8 a, b;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    a[e] = (__bf16)(0.001f * (float)(lane + e));
+    b[e] = (__bf16)(0.002f * (float)(lane - e));
+  }
+  f32x4 acc[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[k], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) s += acc[k][0] + acc[k][1] + acc[k][2] + acc[k][3];
+  if (s == 1234.5f) out[0] = s;
+}
+
+}  // namespace
+
+// Streaming read of `bytes` (a multiple of 16) at device address p; out is a
+// device word that is not written in practice.  Enqueued on `stream`.
+extern "C" int probe_read_launch(const void* p, int64_t bytes, uint32_t* out, int32_t grid,
+                                 void* stream) {
+  if (!p || bytes <= 0 || (bytes & 15) || grid <= 0) return -1;
+  hipLaunchKernelGGL(probe_read, dim3((unsigned)grid), dim3(256), 0, (hipStream_t)stream,
+                     static_cast<const uint4*>(p), bytes / 16, out);
+  return hipGetLastError() == hipSuccess ? 0 : -2;
+}
+
+// grid workgroups of 4 waves, each wave iters x 8 MFMAs of 16,384 FLOP.
+extern "C" int probe_mfma_launch(int32_t iters, int32_t grid, float* out, void* stream) {
+  if (iters <= 0 || grid <= 0) return -1;
+  hipLaunchKernelGGL(probe_mfma, dim3((unsigned)grid), dim3(256), 0, (hipStream_t)stream, iters, out);
+  return hipGetLastError() == hipSuccess ? 0 : -2;
+}
