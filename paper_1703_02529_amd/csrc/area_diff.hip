@@ -53,15 +53,19 @@ __device__ __forceinline__ void load_chunk(const uint8_t* p, uint32_t (&v)[CB >=
 // output row covers source rows j0..j1-1; the first and last may be partial
 // (weights wf, wl), every row in between has the full weight q.  Interior
 // rows are summed without multiplies and scaled by q once.  PACKED keeps two
-// 16-bit fields per 32-bit register (exact while 255 * p < 65536).  All
-// control flow is uniform across the wave.
+// 16-bit fields per 32-bit register (exact while 255 * p < 65536).  The rows
+// are loaded in batches of up to RB, all loads of a batch issued before any
+// add, so that an output row's loads are in flight together (an output row
+// spans 7 to 16 source rows at the frame sizes here).  All control flow is
+// uniform across the wave.
 template <int CB, bool PACKED, int RB = NSC_ROWS_BATCH>
 __device__ __forceinline__ void vertical_sums(const uint8_t* __restrict__ col, int64_t row_bytes,
                                               int a0, int a1, int q, int j0, int j1,
                                               int32_t out[CB]) {
   constexpr int ND = CB >= 4 ? CB / 4 : 1;
   constexpr int NA = CB == 1 ? 1 : (PACKED ? 2 * ND : CB);
-  const uint32_t wf = (uint32_t)(min(a1, (j0 + 1) * q) - a0);
+  const int nrows = j1 - j0;
+  const uint32_t wf = nrows > 1 ? (uint32_t)(min(a1, (j0 + 1) * q) - a0) : (uint32_t)(a1 - a0);
   const uint32_t wl = (uint32_t)(a1 - max(a0, (j1 - 1) * q));
   uint32_t S[NA], A[NA];  // interior sums, weighted end rows
 #pragma unroll
@@ -84,29 +88,25 @@ __device__ __forceinline__ void vertical_sums(const uint8_t* __restrict__ col, i
       }
     }
   };
-  {
-    uint32_t v[ND];
-    load_chunk<CB>(col + (int64_t)j0 * row_bytes, v);
-    add(A, v, j1 - 1 > j0 ? wf : (uint32_t)(a1 - a0), true);
-  }
-  const uint8_t* p = col + (int64_t)(j0 + 1) * row_bytes;
-  int j = j0 + 1;
-  for (; j + RB <= j1 - 1; j += RB, p += RB * row_bytes) {  // full batches: RB loads in flight
+  const uint8_t* p = col + (int64_t)j0 * row_bytes;
+  for (int jb = 0; jb < nrows; jb += RB, p += RB * row_bytes) {
+    const int cnt = min(RB, nrows - jb);
     uint32_t v[RB][ND];
 #pragma unroll
-    for (int k = 0; k < RB; ++k) load_chunk<CB>(p + k * row_bytes, v[k]);
+    for (int k = 0; k < RB; ++k)
+      if (k < cnt) load_chunk<CB>(p + k * row_bytes, v[k]);
 #pragma unroll
-    for (int k = 0; k < RB; ++k) add(S, v[k], 0u, false);
-  }
-  for (; j < j1 - 1; ++j, p += row_bytes) {
-    uint32_t v[ND];
-    load_chunk<CB>(p, v);
-    add(S, v, 0u, false);
-  }
-  if (j1 - 1 > j0) {
-    uint32_t v[ND];
-    load_chunk<CB>(col + (int64_t)(j1 - 1) * row_bytes, v);
-    add(A, v, wl, true);
+    for (int k = 0; k < RB; ++k) {
+      if (k < cnt) {
+        const int r = jb + k;  // row j0 + r
+        if (r == 0)
+          add(A, v[k], wf, true);
+        else if (r == nrows - 1)
+          add(A, v[k], wl, true);
+        else
+          add(S, v[k], 0u, false);
+      }
+    }
   }
 #pragma unroll
   for (int k = 0; k < NA; ++k) A[k] += (uint32_t)q * S[k];  // full 32 bits: two packed fields
@@ -410,6 +410,8 @@ int make_area_plan(int32_t in_h, int32_t in_w, int64_t stride, const void* frame
                 (long long)row_bytes, p.lanes, p.chunk_bytes);
   p.threads = (p.lanes + 63) / 64 * 64;
   if (p.threads < 64) p.threads = 64;
+  // vertical column sums reach 255 * p_y; 16-bit packing is exact below 65536
+  p.packed = 255LL * p.ay.p < 65536;
   // wave strips: whole periods of the horizontal pattern in 16/4-byte chunks
   p.wave = false;
   if (p.chunk_bytes != 1) {
@@ -437,8 +439,6 @@ int make_area_plan(int32_t in_h, int32_t in_w, int64_t stride, const void* frame
       p.wave = g.lds_bytes <= 64 * 1024;
     }
   }
-  // vertical column sums reach 255 * p_y; 16-bit packing is exact below 65536
-  p.packed = 255LL * p.ay.p < 65536;
   // split frames into bands of output rows when there are too few frames to fill the chip
   int64_t bands = (4096 + n - 1) / (n > 0 ? n : 1);
   if (bands < 1) bands = 1;
