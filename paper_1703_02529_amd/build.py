@@ -26,6 +26,9 @@ HIP_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     # no packed-FP32 instructions in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in ordinary VGPRs: with accumulation registers the
+    # compiler shuffles loop-carried accumulators between register files
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall", "-Wno-unused-function",
 ]
 SOURCES = ["api.hip", "area_diff.hip", "compact_resolve.hip", "cnn.hip"]

@@ -29,7 +29,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // Each wave runs `iters` rounds of 8 independent v_mfma_f32_16x16x32_bf16
-// (16 x 16 x 32 x 2 = 16,384 FLOP each) on register operands.
+// (16 x 16 x 32 x 2 = 16,384 FLOP each) on register operands; the eight
+// accumulators are separate variables so that they keep fixed registers.
 __global__ void __launch_bounds__(256) probe_mfma(int32_t iters, float* out) {
   const int lane = threadIdx.x & 63;
   bf16x8 a, b;
@@ -38,17 +39,23 @@ __global__ void __launch_bounds__(256) probe_mfma(int32_t iters, float* out) {
     a[e] = (__bf16)(0.001f * (float)(lane + e));
     b[e] = (__bf16)(0.002f * (float)(lane - e));
   }
-  f32x4 acc[8];
-#pragma unroll
-  for (int k = 0; k < 8; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0, c3 = c0, c4 = c0, c5 = c0, c6 = c0, c7 = c0;
+#pragma unroll 1
   for (int it = 0; it < iters; ++it) {
-#pragma unroll
-    for (int k = 0; k < 8; ++k) acc[k] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[k], 0, 0, 0);
+    c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c0, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c1, 0, 0, 0);
+    c2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c2, 0, 0, 0);
+    c3 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c3, 0, 0, 0);
+    c4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c4, 0, 0, 0);
+    c5 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c5, 0, 0, 0);
+    c6 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c6, 0, 0, 0);
+    c7 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c7, 0, 0, 0);
   }
-  float s = 0.f;
-#pragma unroll
-  for (int k = 0; k < 8; ++k) s += acc[k][0] + acc[k][1] + acc[k][2] + acc[k][3];
-  if (s == 1234.5f) out[0] = s;
+  // stored only for a negative `iters`, which the host never passes
+  if (iters < 0) {
+    f32x4* o = reinterpret_cast<f32x4*>(out) + 8 * lane;
+    o[0] = c0; o[1] = c1; o[2] = c2; o[3] = c3; o[4] = c4; o[5] = c5; o[6] = c6; o[7] = c7;
+  }
 }
 
 }  // namespace
