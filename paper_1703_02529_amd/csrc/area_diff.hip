@@ -24,7 +24,7 @@ namespace {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 #ifndef NSC_ROWS_BATCH
-#define NSC_ROWS_BATCH 8
+#define NSC_ROWS_BATCH 12
 #endif
 
 // One lane's 4 bytes split into two words of two 16-bit fields:
@@ -51,13 +51,13 @@ __device__ __forceinline__ void load_chunk(const uint8_t* p, uint32_t (&v)[CB >=
 
 // Vertical pass of one output row for one lane's chunk of CB bytes: the
 // output row covers source rows j0..j1-1; the first and last may be partial
-// (weights wf, wl), every row in between has the full weight q.  Interior
-// rows are summed without multiplies and scaled by q once.  PACKED keeps two
-// 16-bit fields per 32-bit register (exact while 255 * p < 65536).  The rows
-// are loaded in batches of up to RB, all loads of a batch issued before any
-// add, so that an output row's loads are in flight together (an output row
-// spans 7 to 16 source rows at the frame sizes here).  All control flow is
-// uniform across the wave.
+// (weights wf, wl), every row in between has the full weight q.  Each row is
+// added with its weight by a 24-bit multiply-add; PACKED keeps two 16-bit
+// fields per 32-bit register (exact while 255 * p < 65536: the weights of an
+// output row add up to p).  The rows are loaded in batches of up to RB, all
+// loads of a batch issued before any add, so that an output row's loads are
+// in flight together (an output row spans 7 to 16 source rows at the frame
+// sizes here).  All control flow is uniform across the wave.
 template <int CB, bool PACKED, int RB = NSC_ROWS_BATCH>
 __device__ __forceinline__ void vertical_sums(const uint8_t* __restrict__ col, int64_t row_bytes,
                                               int a0, int a1, int q, int j0, int j1,
@@ -67,27 +67,9 @@ __device__ __forceinline__ void vertical_sums(const uint8_t* __restrict__ col, i
   const int nrows = j1 - j0;
   const uint32_t wf = nrows > 1 ? (uint32_t)(min(a1, (j0 + 1) * q) - a0) : (uint32_t)(a1 - a0);
   const uint32_t wl = (uint32_t)(a1 - max(a0, (j1 - 1) * q));
-  uint32_t S[NA], A[NA];  // interior sums, weighted end rows
+  uint32_t A[NA];
 #pragma unroll
-  for (int k = 0; k < NA; ++k) S[k] = A[k] = 0;
-  auto add = [&](uint32_t (&acc)[NA], const uint32_t (&v)[ND], uint32_t w, bool weighted) {
-#pragma unroll
-    for (int d = 0; d < ND; ++d) {
-      if constexpr (CB == 1) {
-        acc[0] += weighted ? __umul24(w, v[0]) : v[0];
-      } else if constexpr (PACKED) {
-        const uint32_t e0 = bytes02(v[d]), e1 = bytes13(v[d]);
-        acc[d] += weighted ? __umul24(w, e0) : e0;
-        acc[ND + d] += weighted ? __umul24(w, e1) : e1;
-      } else {
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const uint32_t e = __builtin_amdgcn_ubfe(v[d], 8 * b, 8);
-          acc[4 * d + b] += weighted ? __umul24(w, e) : e;
-        }
-      }
-    }
-  };
+  for (int k = 0; k < NA; ++k) A[k] = 0;
   const uint8_t* p = col + (int64_t)j0 * row_bytes;
   for (int jb = 0; jb < nrows; jb += RB, p += RB * row_bytes) {
     const int cnt = min(RB, nrows - jb);
@@ -99,17 +81,22 @@ __device__ __forceinline__ void vertical_sums(const uint8_t* __restrict__ col, i
     for (int k = 0; k < RB; ++k) {
       if (k < cnt) {
         const int r = jb + k;  // row j0 + r
-        if (r == 0)
-          add(A, v[k], wf, true);
-        else if (r == nrows - 1)
-          add(A, v[k], wl, true);
-        else
-          add(S, v[k], 0u, false);
+        const uint32_t w = r == 0 ? wf : (r == nrows - 1 ? wl : (uint32_t)q);
+#pragma unroll
+        for (int d = 0; d < ND; ++d) {
+          if constexpr (CB == 1) {
+            A[0] += __umul24(w, v[k][0]);
+          } else if constexpr (PACKED) {
+            A[d] += __umul24(w, bytes02(v[k][d]));
+            A[ND + d] += __umul24(w, bytes13(v[k][d]));
+          } else {
+#pragma unroll
+            for (int bb = 0; bb < 4; ++bb) A[4 * d + bb] += __umul24(w, __builtin_amdgcn_ubfe(v[k][d], 8 * bb, 8));
+          }
+        }
       }
     }
   }
-#pragma unroll
-  for (int k = 0; k < NA; ++k) A[k] += (uint32_t)q * S[k];  // full 32 bits: two packed fields
   if constexpr (CB == 1) {
     out[0] = (int32_t)A[0];
   } else if constexpr (PACKED) {
