@@ -41,6 +41,18 @@ class Cfg(ctypes.Structure):
                 ("c_low", _dbl), ("c_high", _dbl), ("check_stride", _i32)]
 
 
+class SweepCfg(ctypes.Structure):
+    _fields_ = [("ref_mode", _i32), ("delta", _i32), ("fp_target", _dbl), ("fn_target", _dbl),
+                ("t_mse", _dbl), ("t_snn", _dbl), ("t_full", _dbl)]
+
+
+SWEEP_ROW = np.dtype([("delta", "<f8"), ("c_low", "<f8"), ("c_high", "<f8"), ("f_m", "<f8"),
+                      ("f_c", "<f8"), ("cost", "<f8"), ("fired", "<i8"), ("deferred", "<i8"),
+                      ("fn_dd", "<i8"), ("fp_dd", "<i8"), ("fn_cnn", "<i8"), ("fp_cnn", "<i8"),
+                      ("positives", "<i8"), ("negatives", "<i8"), ("feasible", "<i4"),
+                      ("pad", "<i4")])
+
+
 _LIB = None
 
 
@@ -73,6 +85,8 @@ def lib() -> ctypes.CDLL:
         L.oracle_sigmoid.argtypes = [_dbl]
         L.oracle_decide.restype = _i32
         L.oracle_decide.argtypes = [_dbl, _dbl, _dbl]
+        L.oracle_threshold_sweep.restype = _i32
+        L.oracle_threshold_sweep.argtypes = [_vp, _vp, _vp, _vp, _i64, _vp, _i32, _vp]
         L.oracle_cascade.restype = _i64
         L.oracle_cascade.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _vp,
                                      _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
@@ -227,3 +241,25 @@ def cascade(cfg: Cfg, spec, blob, frames: np.ndarray, t0: int = 0, state=None):
         raise ValueError("oracle_cascade rejected its arguments")
     out["fired"] = int(fired)
     return out, (sS[:D].copy(), sD[:D].copy())
+
+
+def threshold_sweep(score, conf, truth, deltas, *, ref_mode: int, delta: int, fp_target: float,
+                    fn_target: float, t_mse: float, t_snn: float, t_full: float):
+    """Threshold search of the cost-based optimizer on logged per-frame scores
+    (oracle.cpp, oracle_threshold_sweep): one row per candidate delta_diff
+    (structured array of SWEEP_ROW) and the index of the cheapest feasible
+    one (-1 if none)."""
+    score = _c(score, np.float64)
+    conf = _c(conf, np.float32)
+    truth = _c(truth, np.uint8)
+    deltas = _c(deltas, np.float64)
+    n, n_t = score.size, deltas.size
+    if conf.size != n or truth.size != n:
+        raise ValueError("score, conf and truth need one entry per frame")
+    cfg = SweepCfg(ref_mode, delta, fp_target, fn_target, t_mse, t_snn, t_full)
+    rows = np.zeros(n_t, SWEEP_ROW)
+    best = lib().oracle_threshold_sweep(ctypes.byref(cfg), _p(score), _p(conf), _p(truth), n,
+                                        _p(deltas), n_t, rows.ctypes.data)
+    if best < -1:
+        raise ValueError("oracle_threshold_sweep rejected its arguments")
+    return rows, int(best)

@@ -21,9 +21,14 @@
 //      -> object, otherwise defer to the reference network; a frame on which
 //      the earlier-frame detector does not fire reuses the compared frame's
 //      output [Sec. 5].
+//   6. threshold search of the cost-based optimizer [Sec. 6.2 cost model,
+//      Sec. 6.3 step 3]: on logged per-frame detector scores, specialized-
+//      CNN confidences and reference labels, the cheapest delta_diff /
+//      c_low / c_high within false positive and false negative targets.
 // Readings where the paper is silent (rounding points of bf16 networks,
 // forced firing of the first delta frames, ties) are listed in the design
 // notes; each is marked "reading" below.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -469,6 +474,146 @@ int64_t oracle_cascade(const oracle_cfg* cfg, const oracle_cnn_desc* net, const 
     if (state_dec_out) state_dec_out[k] = dec[(size_t)(n + k)];
   }
   return fired;
+}
+
+
+// Threshold search of the cost-based optimizer [Sec. 6.3, step 3] with its
+// cost model [Sec. 6.2], on logged scores of every frame of an evaluation
+// video: the detector score s[t] (+inf for a frame that always fires), the
+// specialized CNN's confidence c[t], and the reference label y[t] (1 = the
+// object is present).  For each candidate threshold delta[k]:
+//   - the frames that fire are a prefix of the frames sorted by decreasing
+//     score; a frame that does not fire takes the label of the frame it is
+//     compared with (reading: its reference label, frame t - delta for the
+//     earlier-frame detector, "no object" for a fixed reference image), so
+//     the detector's false negatives / positives are the non-firing frames
+//     whose own label is 1 / 0 and the copied label 0 / 1;
+//   - on the fired frames sorted by confidence, c_low moves up until the
+//     combined false negative rate would reach FN*, and c_high down until
+//     the combined false positive rate would reach FP* (reading: rates are
+//     counts over the frames with / without the object, and must stay
+//     strictly below the targets; a frame at c_low or c_high is deferred,
+//     and a deferred frame gets the reference label; c_high >= c_low);
+//   - cost per frame = f_s T_MSE + f_s f_m T_SNN + f_s f_m f_c T_Full with
+//     f_s = 1 (every frame checked), f_m = fired / n, f_c = deferred / fired.
+// The candidate is feasible when the detector's errors alone stay below the
+// targets.  Returns the index of the cheapest feasible candidate (the first
+// on ties), or -1 when none is feasible or the input is invalid.
+struct oracle_sweep_cfg {
+  int32_t ref_mode;  // 0: earlier frame, 1: fixed reference image
+  int32_t delta;     // frames back (earlier-frame detector)
+  double fp_target, fn_target;
+  double t_mse, t_snn, t_full;  // per-frame costs
+};
+
+struct oracle_sweep_row {
+  double delta, c_low, c_high, f_m, f_c, cost;
+  int64_t fired, deferred, fn_dd, fp_dd, fn_cnn, fp_cnn, positives, negatives;
+  int32_t feasible, pad;
+};
+
+int32_t oracle_threshold_sweep(const oracle_sweep_cfg* cfg, const double* score, const float* conf,
+                               const uint8_t* truth, int64_t n, const double* deltas, int32_t n_t,
+                               oracle_sweep_row* rows) {
+  if (!cfg || n < 1 || n_t < 1 || (cfg->ref_mode == 0 && cfg->delta < 1)) return -1;
+  const double inf = std::numeric_limits<double>::infinity();
+  int64_t positives = 0;
+  for (int64_t t = 0; t < n; ++t) positives += truth[t] ? 1 : 0;
+  const int64_t negatives = n - positives;
+  // error budgets: count < target x (frames with / without the object); an
+  // empty class leaves nothing to get wrong
+  const double fn_budget = positives ? cfg->fn_target * (double)positives : inf;
+  const double fp_budget = negatives ? cfg->fp_target * (double)negatives : inf;
+  // L_D: frames in decreasing order of score (+inf first), and the detector
+  // errors of each frame if it does not fire
+  std::vector<int64_t> order((size_t)n);
+  for (int64_t t = 0; t < n; ++t) order[(size_t)t] = t;
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int64_t a, int64_t b) { return score[a] > score[b]; });
+  std::vector<int64_t> fn_suffix((size_t)n + 1, 0), fp_suffix((size_t)n + 1, 0);
+  for (int64_t i = n - 1; i >= 0; --i) {
+    const int64_t t = order[(size_t)i];
+    const int ref = cfg->ref_mode == 0 ? (t >= cfg->delta ? truth[t - cfg->delta] : 0) : 0;
+    fn_suffix[(size_t)i] = fn_suffix[(size_t)i + 1] + (truth[t] && !ref ? 1 : 0);
+    fp_suffix[(size_t)i] = fp_suffix[(size_t)i + 1] + (!truth[t] && ref ? 1 : 0);
+  }
+  int32_t best = -1;
+  for (int32_t k = 0; k < n_t; ++k) {
+    const double d = deltas[k];
+    // prefix of L_D that fires: score above the threshold, or +inf (forced)
+    int64_t fired = 0;
+    while (fired < n && (score[order[(size_t)fired]] == inf || score[order[(size_t)fired]] > d))
+      ++fired;
+    oracle_sweep_row r{};
+    r.delta = d;
+    r.fired = fired;
+    r.fn_dd = fn_suffix[(size_t)fired];
+    r.fp_dd = fp_suffix[(size_t)fired];
+    r.positives = positives;
+    r.negatives = negatives;
+    r.feasible = (double)r.fn_dd < fn_budget && (double)r.fp_dd < fp_budget ? 1 : 0;
+    // the fired frames by confidence
+    std::vector<int64_t> f(order.begin(), order.begin() + fired);
+    std::stable_sort(f.begin(), f.end(), [&](int64_t a, int64_t b) { return conf[a] < conf[b]; });
+    // c_low: up the list; the frames below c_low are labelled 0, and each with
+    // the object is a false negative.  c_low stops at the first confidence
+    // whose frames would bring the false negatives to the budget.
+    double c_low = 1.0;
+    {
+      int64_t fn = r.fn_dd;
+      for (size_t i = 0; i < f.size();) {
+        size_t j = i;
+        int64_t add = 0;
+        while (j < f.size() && conf[f[j]] == conf[f[i]]) add += truth[f[j++]] ? 1 : 0;
+        if ((double)(fn + add) >= fn_budget) {
+          c_low = (double)conf[f[i]];
+          break;
+        }
+        fn += add;
+        i = j;
+      }
+      if (c_low > 1.0) c_low = 1.0;
+    }
+    // c_high: down the list; the frames above c_high are labelled 1
+    double c_high = 0.0;
+    {
+      int64_t fp = r.fp_dd;
+      for (size_t i = f.size(); i > 0;) {
+        size_t j = i;
+        int64_t add = 0;
+        while (j > 0 && conf[f[j - 1]] == conf[f[i - 1]]) add += truth[f[--j]] ? 0 : 1;
+        if ((double)(fp + add) >= fp_budget) {
+          c_high = (double)conf[f[i - 1]];
+          break;
+        }
+        fp += add;
+        i = j;
+      }
+      if (c_high < c_low) c_high = c_low;
+    }
+    if (!r.feasible) {  // no thresholds meet the targets: report the extremes
+      c_low = 0.0;
+      c_high = 1.0;
+    }
+    r.c_low = c_low;
+    r.c_high = c_high;
+    for (int64_t t : f) {
+      const double c = (double)conf[t];
+      if (c < c_low) {
+        r.fn_cnn += truth[t] ? 1 : 0;
+      } else if (c > c_high) {
+        r.fp_cnn += truth[t] ? 0 : 1;
+      } else {
+        ++r.deferred;
+      }
+    }
+    r.f_m = (double)fired / (double)n;
+    r.f_c = fired ? (double)r.deferred / (double)fired : 0.0;
+    r.cost = cfg->t_mse + r.f_m * cfg->t_snn + (r.f_m * r.f_c) * cfg->t_full;
+    rows[k] = r;
+    if (r.feasible && (best < 0 || r.cost < rows[best].cost)) best = k;
+  }
+  return best;
 }
 
 }  // extern "C"

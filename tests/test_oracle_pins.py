@@ -510,3 +510,151 @@ def test_skipping_stride_one_and_bad_delta():
             np.testing.assert_array_equal(a[k], b[k])
     with pytest.raises(ValueError):   # reading: delta must be a multiple of the stride
         oracle.cascade(oracle.make_cfg(wl.replace(check_stride=3))[0], wl.cnn, blob, frames)
+
+
+# ------------------------------------------------- threshold search (Sec. 6.3)
+
+SWEEP_COSTS = dict(t_mse=1e-6, t_snn=1e-4, t_full=1e-2)
+
+
+def test_sweep_hand_worked():
+    rows = _read_golden("sweep_6.txt")
+    score = np.array([np.inf, 5, 1, 3, 0.5, 2])
+    conf = np.array([0.9, 0.1, 0.5, 0.7, 0.2, 0.95], np.float32)
+    truth = np.array([1, 0, 0, 1, 0, 1], np.uint8)
+    cands = [float(r[0]) for r in rows if r[0] != "best"]
+    got, best = oracle.threshold_sweep(score, conf, truth, cands, ref_mode=W.PREV, delta=1,
+                                       fp_target=0.5, fn_target=0.5, **SWEEP_COSTS)
+    for g, r in zip(got, [r for r in rows if r[0] != "best"]):
+        d, fired, fn_dd, fp_dd, cl, ch, deferred, fn_c, fp_c, feas, cost = r
+        assert (g["fired"], g["fn_dd"], g["fp_dd"]) == (int(fired), int(fn_dd), int(fp_dd))
+        assert g["c_low"] == float(np.float32(cl)) and g["c_high"] == float(np.float32(ch))
+        assert (g["deferred"], g["fn_cnn"], g["fp_cnn"], g["feasible"]) == (
+            int(deferred), int(fn_c), int(fp_c), int(feas))
+        assert g["cost"] == pytest.approx(float(cost), rel=1e-12)
+    assert best == int(rows[-1][1])
+
+
+def _sweep_brute(score, conf, truth, cands, ref_mode, delta, fp_t, fn_t, costs):
+    """Per-frame simulation of every threshold pair: the labels a cascade with
+    thresholds (delta_diff, c_low, c_high) gives, counted against the reference
+    labels; c_low is the largest candidate value meeting the false negative
+    target, c_high the smallest (not below c_low) meeting the false positive
+    target."""
+    n = len(score)
+    pos = int(truth.sum())
+    neg = n - pos
+    fn_b = fn_t * pos if pos else math.inf
+    fp_b = fp_t * neg if neg else math.inf
+    out = []
+    for d in cands:
+        fired = [t for t in range(n) if score[t] == math.inf or score[t] > d]
+        fs = set(fired)
+        fn_dd = fp_dd = 0
+        for t in range(n):
+            if t in fs:
+                continue
+            ref = truth[t - delta] if (ref_mode == W.PREV and t >= delta) else 0
+            fn_dd += int(truth[t] == 1 and ref == 0)
+            fp_dd += int(truth[t] == 0 and ref == 1)
+        values = sorted({0.0, 1.0} | {float(conf[t]) for t in fired})
+
+        def count(cl, ch):
+            fn = fp = dfr = 0
+            for t in fired:
+                c = float(conf[t])
+                if c < cl:
+                    fn += int(truth[t] == 1)
+                elif c > ch:
+                    fp += int(truth[t] == 0)
+                else:
+                    dfr += 1
+            return fn, fp, dfr
+
+        feasible = fn_dd < fn_b and fp_dd < fp_b
+        if feasible:
+            cl = max(v for v in values if fn_dd + count(v, 2.0)[0] < fn_b)
+            ch = min(v for v in values if v >= cl and fp_dd + count(cl, v)[1] < fp_b)
+        else:
+            cl, ch = 0.0, 1.0
+        fn, fp, dfr = count(cl, ch)
+        f_m = len(fired) / n
+        f_c = dfr / len(fired) if fired else 0.0
+        cost = costs["t_mse"] + f_m * costs["t_snn"] + (f_m * f_c) * costs["t_full"]
+        out.append(dict(fired=len(fired), fn_dd=fn_dd, fp_dd=fp_dd, c_low=cl, c_high=ch,
+                        deferred=dfr, fn_cnn=fn, fp_cnn=fp, feasible=int(feasible), cost=cost))
+    feas = [k for k, o in enumerate(out) if o["feasible"]]
+    best = min(feas, key=lambda k: (out[k]["cost"], k)) if feas else -1
+    return out, best
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_sweep_against_brute_force(seed):
+    r = np.random.default_rng([seed, 77])
+    n = int(r.integers(1, 15))
+    delta = int(r.integers(1, 4))
+    ref_mode = W.PREV if seed % 3 else W.FIXED
+    score = np.round(r.uniform(0, 10, n), 1)
+    if ref_mode == W.PREV:
+        score[:delta] = np.inf
+    # few distinct confidences, so that ties occur; 0 and 1 included
+    conf = r.choice(np.array([0.0, 0.125, 0.25, 0.5, 0.75, 1.0], np.float32), n)
+    truth = (r.random(n) < r.uniform(0.1, 0.9)).astype(np.uint8)
+    cands = np.concatenate([[-np.inf, np.inf], np.round(r.uniform(-1, 11, 6), 1), score[:3]])
+    fp_t, fn_t = float(r.choice([0.05, 0.2, 0.34, 0.5, 1.0])), float(r.choice([0.05, 0.2, 0.5, 1.0]))
+    got, best = oracle.threshold_sweep(score, conf, truth, cands, ref_mode=ref_mode, delta=delta,
+                                       fp_target=fp_t, fn_target=fn_t, **SWEEP_COSTS)
+    want, wbest = _sweep_brute(score, conf, truth, cands, ref_mode, delta, fp_t, fn_t,
+                               SWEEP_COSTS)
+    for g, w in zip(got, want):
+        for k in ("fired", "fn_dd", "fp_dd", "deferred", "fn_cnn", "fp_cnn", "feasible"):
+            assert int(g[k]) == w[k], (k, g, w)
+        assert g["c_low"] == w["c_low"] and g["c_high"] == w["c_high"], (g, w)
+        assert g["cost"] == w["cost"]
+        if w["feasible"]:  # the chosen thresholds meet the targets
+            pos, neg = int(truth.sum()), n - int(truth.sum())
+            assert not pos or g["fn_dd"] + g["fn_cnn"] < fn_t * pos
+            assert not neg or g["fp_dd"] + g["fp_cnn"] < fp_t * neg
+    assert best == wbest
+
+
+def test_sweep_monotone_in_delta():
+    # raising delta_diff never adds fired frames and never removes detector errors
+    r = np.random.default_rng(5)
+    n = 400
+    score = r.exponential(5, n)
+    score[:3] = np.inf
+    conf = r.random(n).astype(np.float32)
+    truth = (r.random(n) < 0.3).astype(np.uint8)
+    cands = np.sort(r.uniform(0, 20, 40))
+    got, _ = oracle.threshold_sweep(score, conf, truth, cands, ref_mode=W.PREV, delta=3,
+                                    fp_target=0.1, fn_target=0.1, **SWEEP_COSTS)
+    assert (np.diff(got["fired"]) <= 0).all()
+    assert (np.diff(got["fn_dd"]) >= 0).all() and (np.diff(got["fp_dd"]) >= 0).all()
+    assert got["fired"][0] == int((score > cands[0]).sum())
+
+
+def test_sweep_special_cases():
+    n = 50
+    r = np.random.default_rng(9)
+    conf = r.random(n).astype(np.float32)
+    truth = (r.random(n) < 0.4).astype(np.uint8)
+    score = r.uniform(0, 1, n)
+    # delta_diff = -inf: every frame fires, the detector makes no error; with
+    # targets of 100 % every frame can be labelled, so only frames at exactly
+    # c_low = c_high are deferred
+    got, best = oracle.threshold_sweep(score, conf, truth, [-np.inf], ref_mode=W.FIXED, delta=1,
+                                       fp_target=1.0, fn_target=1.0, **SWEEP_COSTS)
+    g = got[0]
+    assert g["fired"] == n and g["fn_dd"] == 0 and g["fp_dd"] == 0 and best == 0
+    assert g["deferred"] == int((conf.astype(np.float64) == g["c_low"]).sum())
+    # targets of 0: nothing may be labelled by the CNN, everything fired defers
+    got, best = oracle.threshold_sweep(score, conf, truth, [-np.inf], ref_mode=W.FIXED, delta=1,
+                                       fp_target=0.0, fn_target=0.0, **SWEEP_COSTS)
+    assert got[0]["feasible"] == 0 and best == -1
+    # fixed reference, delta_diff = +inf: nothing fires, every frame with the
+    # object is a false negative of the detector
+    got, _ = oracle.threshold_sweep(score, conf, truth, [np.inf], ref_mode=W.FIXED, delta=1,
+                                    fp_target=1.0, fn_target=1.0, **SWEEP_COSTS)
+    assert got[0]["fired"] == 0 and got[0]["fn_dd"] == int(truth.sum()) and got[0]["fp_dd"] == 0
+    assert got[0]["cost"] == SWEEP_COSTS["t_mse"]
