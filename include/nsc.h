@@ -60,7 +60,8 @@ typedef enum nsc_status {
 
 enum { NSC_REF_PREV = 0, NSC_REF_FIXED = 1 };
 enum { NSC_F32 = 0, NSC_BF16 = 1 };
-enum { NSC_MAX_CONV = 8, NSC_MAX_DELTA = 256, NSC_MAX_BLOCKS = 1024, NSC_MAX_STRIDE = 4096 };
+enum { NSC_MAX_CONV = 8, NSC_MAX_DELTA = 256, NSC_MAX_BLOCKS = 1024, NSC_MAX_STRIDE = 4096,
+       NSC_MAX_SWEEP = 65535 };
 
 /* Stage boundaries at which nsc_cascade_run records optional events:
  * [0] start, [1] after the area sums, [2] after the detector, [3] after the
@@ -240,6 +241,54 @@ int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_
                     int64_t n, int64_t t0, void* state, void* ws, size_t ws_bytes,
                     uint8_t* label_out, uint8_t* defer_out, const nsc_frame_outputs* outs,
                     nsc_run_stats* stats, void* const* stage_events, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Threshold search of the cost-based optimizer (Sec. 6.3, step 3) with its
+ * cost model (Sec. 6.2), on logged scores of every frame of an evaluation
+ * video.  For each candidate delta_diff[k]:
+ *   - a frame fires when its detector score is +inf (no compared frame) or
+ *     above delta_diff; a frame that does not fire takes the reference label
+ *     of the frame it is compared with (frame t - delta, or "no object" with
+ *     a fixed reference image): fn_dd / fp_dd count those with label 1 / 0
+ *     whose copied label is 0 / 1;
+ *   - c_low is the smallest confidence v of a fired frame with
+ *     fn_dd + #{fired, label 1, conf <= v} >= fn_target x positives (1 if
+ *     none), c_high the largest v with fp_dd + #{fired, label 0, conf >= v}
+ *     >= fp_target x negatives (0 if none), raised to c_low: the loosest
+ *     thresholds whose false negative / positive rates stay strictly below
+ *     the targets, frames below c_low labelled 0, above c_high 1, the others
+ *     deferred to the reference network (counted as right);
+ *   - cost = t_mse + f_m t_snn + f_m f_c t_full per frame, with f_m = fired
+ *     / n, f_c = deferred / fired (every frame checked: f_s = 1).
+ * A candidate is feasible when fn_dd and fp_dd alone stay below the
+ * targets; an infeasible one reports c_low = 0, c_high = 1. */
+typedef struct nsc_sweep_cfg {
+  int32_t ref_mode;          /* NSC_REF_PREV or NSC_REF_FIXED                    */
+  int32_t delta;             /* PREV: frames back, 1..NSC_MAX_DELTA              */
+  double fp_target, fn_target; /* FP*, FN*: rates in [0, 1] (FP / frames without
+                                the object, FN / frames with it)                 */
+  double t_mse, t_snn, t_full; /* per-frame costs of the detector, the specialized
+                                CNN and the reference network (finite, >= 0)     */
+} nsc_sweep_cfg;
+
+typedef struct nsc_sweep_row {  /* one per candidate, 120 bytes                  */
+  double delta, c_low, c_high, f_m, f_c, cost;
+  int64_t fired, deferred, fn_dd, fp_dd, fn_cnn, fp_cnn, positives, negatives;
+  int32_t feasible, pad;
+} nsc_sweep_row;
+
+/* score: device, n doubles (the detector score of every frame, +inf for a
+ * frame without a compared frame, as nsc_diff_detect writes them; no NaN);
+ * conf: device, n floats in [0, 1] (the specialized CNN's confidence of every
+ * frame); truth: device, n bytes (nonzero: the reference label says the
+ * object is present); deltas: device, n_t candidate thresholds (1 ..
+ * NSC_MAX_SWEEP); rows: device, n_t rows (written); best: device int32, the
+ * index of the cheapest feasible candidate (the first on ties) or -1.  All
+ * buffers are the caller's.  Enqueued on `stream`; the arguments are checked
+ * on the host (NSC_E_INVAL), launch failures give NSC_E_HIP. */
+int nsc_threshold_sweep(const nsc_sweep_cfg* cfg, const double* score, const float* conf,
+                        const uint8_t* truth, int64_t n, const double* deltas, int32_t n_t,
+                        nsc_sweep_row* rows, int32_t* best, void* stream);
 
 #ifdef __cplusplus
 }

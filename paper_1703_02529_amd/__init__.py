@@ -46,6 +46,15 @@ class FrameOutputs(ctypes.Structure):
     _fields_ = [("score", _vp), ("fire", _vp), ("logit", _vp)]
 
 
+class SweepCfg(ctypes.Structure):
+    _fields_ = [("ref_mode", _i32), ("delta", _i32), ("fp_target", _dbl), ("fn_target", _dbl),
+                ("t_mse", _dbl), ("t_snn", _dbl), ("t_full", _dbl)]
+
+
+# nsc_sweep_row, as numpy reads it from the bytes of the rows buffer
+SWEEP_ROW_BYTES = 120
+
+
 class RunStats(ctypes.Structure):
     _fields_ = [("frames", _i64), ("fired", _i64), ("positive", _i64), ("deferred", _i64)]
 
@@ -77,6 +86,8 @@ def lib() -> ctypes.CDLL:
             "nsc_downsample": (ctypes.c_int, [_vp, _i64, _i32, _i32, _i64, _i32, _i32, _vp, _vp]),
             "nsc_diff_detect": (ctypes.c_int, [_vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp]),
             "nsc_compact": (ctypes.c_int, [_vp, _i64, _vp, _vp, _vp, _sz, _vp]),
+            "nsc_threshold_sweep": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _i32, _vp, _vp,
+                                                   _vp]),
             "nsc_specialized_cnn": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i64, _vp, _vp, _i64,
                                                    _vp, _vp, _vp, _sz, _vp]),
             "nsc_cascade_run": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i64, _vp, _vp, _sz, _vp, _vp,
@@ -273,3 +284,14 @@ def nsc_cascade_run(cfg, cnn: Cnn, frames, n, t0, state, ws, label_out, defer_ou
         return dict(frames=st.frames, fired=st.fired, positive=st.positive, deferred=st.deferred)
     return None
 
+
+
+def nsc_threshold_sweep(cfg: SweepCfg, score, conf, truth, deltas, rows, best, stream=None):
+    """rows: device uint8 tensor of len(deltas) * SWEEP_ROW_BYTES bytes; best:
+    device int32 tensor of one element."""
+    n, n_t = score.numel(), deltas.numel()
+    if rows.numel() * rows.element_size() < n_t * SWEEP_ROW_BYTES:
+        raise ValueError("rows holds fewer than one nsc_sweep_row per candidate")
+    _check(lib().nsc_threshold_sweep(ctypes.byref(cfg), _ptr(score), _ptr(conf), _ptr(truth), n,
+                                     _ptr(deltas), n_t, _ptr(rows), _ptr(best), _stream(stream)),
+           "nsc_threshold_sweep")

@@ -31,7 +31,7 @@ HIP_FLAGS = [
     "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall", "-Wno-unused-function",
 ]
-SOURCES = ["api.hip", "area_diff.hip", "compact_resolve.hip", "cnn.hip"]
+SOURCES = ["api.hip", "area_diff.hip", "compact_resolve.hip", "cnn.hip", "sweep.hip"]
 
 
 def _run(cmd):

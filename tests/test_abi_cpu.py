@@ -132,3 +132,23 @@ def test_compact_workspace_size():
     assert nsc.nsc_compact_workspace_bytes(4097) >= 2 * 4
     with pytest.raises(nsc.NscError):
         nsc.nsc_compact_workspace_bytes(-1)
+
+
+def test_threshold_sweep_rejects_bad_arguments_on_the_host():
+    # every check runs before any HIP call; the dummy addresses are never read
+    L = nsc.lib()
+    good = nsc.SweepCfg(0, 1, 0.01, 0.01, 1e-6, 1e-4, 1e-2)
+    p = ctypes.c_void_p(16)
+    args = lambda cfg, n=10, n_t=4, ptr=p: (ctypes.byref(cfg), ptr, ptr, ptr, n, ptr, n_t, ptr, ptr,
+                                             None)
+    E_INVAL = -1
+    assert L.nsc_threshold_sweep(*args(good, ptr=None)) == E_INVAL
+    assert L.nsc_threshold_sweep(*args(good, n=0)) == E_INVAL
+    assert L.nsc_threshold_sweep(*args(good, n_t=0)) == E_INVAL
+    assert L.nsc_threshold_sweep(*args(good, n_t=70000)) == E_INVAL
+    for bad in (nsc.SweepCfg(2, 1, 0.01, 0.01, 0, 0, 0), nsc.SweepCfg(0, 0, 0.01, 0.01, 0, 0, 0),
+                nsc.SweepCfg(0, 1, 1.5, 0.01, 0, 0, 0), nsc.SweepCfg(0, 1, 0.01, -0.1, 0, 0, 0),
+                nsc.SweepCfg(0, 1, 0.01, 0.01, -1, 0, 0),
+                nsc.SweepCfg(0, 1, 0.01, 0.01, 0, math.inf, 0)):
+        assert L.nsc_threshold_sweep(*args(bad)) == E_INVAL
+        assert nsc.last_error()
