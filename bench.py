@@ -22,6 +22,15 @@ HIP events, generator time excluded, as the paper excludes decoding); the
 overlapped wall-clock rate, bound by the generator, is reported beside it, and
 the stage split comes from events at the stage boundaries of every chunk.
 
+--workload vga-sweep measures the threshold search of the cost-based optimizer
+(Sec. 6.3) on the 640x480 video: one cascade run with delta_diff = -inf logs
+every frame's detector score and CNN confidence (and, from its stage events,
+the per-frame costs T_MSE and T_SNN), the generator's object labels stand for
+the reference network's, and nsc_threshold_sweep costs 64 candidate
+thresholds at 1 % FP / FN targets; `value` is frames x candidates per second.
+The cascade is then run with the chosen thresholds, and its measured time per
+frame is reported beside the cost model's prediction.
+
 Every run also measures the peaks the roofline fractions are quoted against:
 a streaming read of the resident frame buffer (HBM) and a loop of independent
 bf16 MFMAs, next to the published 8 TB/s and 2.5 PFLOP/s.
@@ -197,6 +206,135 @@ def cpu_baseline(wl, budget_s: float, lr_w=None, ref_img=None) -> dict:
 
 
 CHUNKED = ("hd-ref", "hd-blocked", "fhd-stream")
+T_FULL_NN = 1.0 / 80.0  # reference network per frame: YOLOv2 at 80 frames/s (Sec. 2)
+
+
+def bench_sweep(args):
+    """Threshold search on the 640x480 video (see the module docstring)."""
+    import math
+
+    import numpy as np
+    import torch
+
+    import paper_1703_02529_amd as nsc
+    import synth
+    from paper_1703_02529_amd.runner import CascadeRunner
+    from synth import workloads as W
+
+    wl = W.VGA
+    n, fb = wl.video.n, wl.video.frame_bytes
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    v = synth.Video(wl.video)
+    frames = torch.empty(n * fb, dtype=torch.uint8, device=dev)
+    v.render_device(frames, 0, n, v.device_tables(dev))
+    blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
+    hip = HipEvents()
+    # 1. every frame through the detector and the CNN: the logged scores
+    run = CascadeRunner(wl.replace(delta_diff=-math.inf), blob, max_frames=n, device=dev)
+    run.run(frames, n, t0=0)
+    evs = hip.create(6)
+    run.run(frames, n, t0=0, stage_events=evs)
+    torch.cuda.synchronize()
+    st = [hip.ms(evs[i], evs[i + 1]) for i in range(5)]
+    hip.destroy(evs)
+    t_mse = (st[0] + st[1] + st[2]) * 1e-3 / n
+    t_snn = st[3] * 1e-3 / n
+    score = run.score[:n].clone()
+    conf = torch.sigmoid(run.logit[:n].double()).float()
+    run.close()
+    truth = torch.from_numpy(v.occupied.astype(np.uint8)).to(dev)
+    finite = score[torch.isfinite(score)]
+    n_t = 64
+    deltas = torch.quantile(finite[:: max(1, finite.numel() // 16384)].double(),
+                            torch.linspace(0, 1, n_t - 1, dtype=torch.float64, device=dev))
+    deltas = torch.cat([torch.tensor([-math.inf], dtype=torch.float64, device=dev), deltas])
+    cfg = nsc.SweepCfg(wl.ref_mode, wl.delta, 0.01, 0.01, t_mse, t_snn, T_FULL_NN)
+    rows = torch.zeros(n_t * nsc.SWEEP_ROW_BYTES, dtype=torch.uint8, device=dev)
+    best = torch.zeros(1, dtype=torch.int32, device=dev)
+    log(f"sweep: {n} frames x {n_t} candidates; T_MSE {t_mse * 1e9:.1f} ns, "
+        f"T_SNN {t_snn * 1e9:.1f} ns per frame")
+    # 2. timed searches
+    for _ in range(args.warmup):
+        nsc.nsc_threshold_sweep(cfg, score, conf, truth, deltas, rows, best)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        nsc.nsc_threshold_sweep(cfg, score, conf, truth, deltas, rows, best)
+    e1.record()
+    torch.cuda.synchronize()
+    sweep_ms = e0.elapsed_time(e1) / args.steps
+    bi = int(best.item())
+    row_bytes = rows.cpu().numpy()
+    fields = ("delta", "c_low", "c_high", "f_m", "f_c", "cost")
+    r = {}
+    if bi >= 0:
+        rec = row_bytes[bi * nsc.SWEEP_ROW_BYTES:(bi + 1) * nsc.SWEEP_ROW_BYTES]
+        r = dict(zip(fields, np.frombuffer(rec[:48].tobytes(), np.float64).tolist()))
+        ints = np.frombuffer(rec[48:112].tobytes(), np.int64).tolist()
+        r.update(zip(("fired", "deferred", "fn_dd", "fp_dd", "fn_cnn", "fp_cnn", "positives",
+                      "negatives"), ints))
+    # 3. the chosen cascade, measured against the cost model
+    check = None
+    if bi >= 0:
+        chosen = wl.replace(delta_diff=r["delta"], c_low=r["c_low"], c_high=r["c_high"])
+        run = CascadeRunner(chosen, blob, max_frames=n, device=dev)
+        run.run(frames, n, t0=0, taps=False)
+        torch.cuda.synchronize()
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record()
+        for _ in range(5):
+            run.run(frames, n, t0=0, taps=False)
+        c1.record()
+        torch.cuda.synchronize()
+        st2 = run.run(frames, n, t0=0, taps=False, want_stats=True)
+        run.close()
+        measured = c0.elapsed_time(c1) * 1e-3 / 5 / n
+        predicted = t_mse + r["f_m"] * t_snn
+        check = {"predicted_s_per_frame": predicted, "measured_s_per_frame": measured,
+                 "ratio": measured / predicted, "fired_measured": int(st2["fired"]),
+                 "fired_predicted": int(r["fired"]),
+                 "note": "cost model without the reference network term (it is not run)"}
+    del frames
+    torch.cuda.empty_cache()
+    result = {
+        "metric": "threshold search: frames x candidate thresholds per second on 1 MI355X",
+        "value": n * n_t / (sweep_ms * 1e-3),
+        "unit": "frame-candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": sweep_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64 scores and costs, f32 confidences, integer counts",
+        "data": "synthetic",
+        "config": {"workload": "vga-100k-640x480-prev15-bf16 threshold search", "frames": n,
+                   "candidates": n_t, "fp_target": 0.01, "fn_target": 0.01,
+                   "t_mse_s": t_mse, "t_snn_s": t_snn, "t_full_s": T_FULL_NN},
+        "best": r,
+        "cost_model_check": check,
+    }
+    if args.cpu_seconds > 0:
+        import oracle
+
+        sc, cf, tr = score.cpu().numpy(), conf.cpu().numpy(), truth.cpu().numpy()
+        dl = deltas.cpu().numpy()
+        t = time.perf_counter()
+        oracle.threshold_sweep(sc, cf, tr, dl, ref_mode=wl.ref_mode, delta=wl.delta,
+                               fp_target=0.01, fn_target=0.01, t_mse=t_mse, t_snn=t_snn,
+                               t_full=T_FULL_NN)
+        dt = time.perf_counter() - t
+        result["cpu_baseline"] = {"value": n * n_t / dt, "unit": "frame-candidates/s",
+                                  "cores": 1, "kind": "oracle",
+                                  "sample": f"the same {n} frames x {n_t} candidates, "
+                                            f"{dt:.2f} s single-threaded"}
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
 
 
 def bench_chunked(args):
@@ -333,7 +471,7 @@ def main():
                     help="oracle time budget for the CPU baseline (0 disables it)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain copy of known size (for counter calibration)")
-    ap.add_argument("--workload", choices=("vga",) + CHUNKED, default="vga")
+    ap.add_argument("--workload", choices=("vga", "vga-sweep") + CHUNKED, default="vga")
     ap.add_argument("--check-stride", type=int, default=1,
                     help="frame skipping on the 640x480 workload: check every s-th frame "
                          "(s must divide 15); 1 is the headline configuration")
@@ -343,6 +481,13 @@ def main():
               f"streams; see the design notes for how it would shard): got --gpus {args.gpus}",
               file=sys.stderr)
         sys.exit(2)
+    if args.workload == "vga-sweep":
+        if args.steps is None:
+            args.steps = 20
+        if args.warmup is None:
+            args.warmup = 2
+        bench_sweep(args)
+        return
     chunked = args.workload in CHUNKED
     if args.steps is None:
         args.steps = 1 if chunked else 20
