@@ -38,7 +38,11 @@ class Cfg(ctypes.Structure):
     _fields_ = [("H", _i32), ("W", _i32), ("Ho", _i32), ("Wo", _i32), ("Hc", _i32), ("Wc", _i32),
                 ("ref_mode", _i32), ("delta", _i32), ("Gh", _i32), ("Gw", _i32),
                 ("lr_w", _vp), ("lr_b", _dbl), ("ref_sums", _vp), ("delta_diff", _dbl),
-                ("c_low", _dbl), ("c_high", _dbl), ("check_stride", _i32)]
+                ("c_low", _dbl), ("c_high", _dbl), ("check_stride", _i32), ("metric", _i32)]
+
+
+# detector metrics (oracle.cpp, metric_of)
+MSE, SAD, NRMSE, PSNR = 0, 1, 2, 3
 
 
 class SweepCfg(ctypes.Structure):
@@ -71,6 +75,11 @@ def lib() -> ctypes.CDLL:
         L.oracle_area_sums.argtypes = [_vp, _i32, _i32, _i32, _i32, _vp]
         L.oracle_global_mse.restype = _dbl
         L.oracle_global_mse.argtypes = [_vp, _vp, _i32, _i32, _i64, _vp]
+        L.oracle_global_metric.restype = _dbl
+        L.oracle_global_metric.argtypes = [_i32, _vp, _vp, _i32, _i32, _i64, _vp]
+        L.oracle_blocked_metric.restype = _dbl
+        L.oracle_blocked_metric.argtypes = [_i32, _vp, _vp, _i32, _i32, _i64, _i32, _i32, _vp,
+                                            _dbl, _vp]
         L.oracle_blocked_score.restype = _dbl
         L.oracle_blocked_score.argtypes = [_vp, _vp, _i32, _i32, _i64, _i32, _i32, _vp, _dbl, _vp]
         L.oracle_round_bf16.restype = _dbl
@@ -127,6 +136,26 @@ def global_mse(a: np.ndarray, b: np.ndarray, den: int):
     E = np.zeros(1, np.int64)
     m = lib().oracle_global_mse(_p(a), _p(b), a.shape[0], a.shape[1], den, _p(E))
     return m, int(E[0])
+
+
+def global_metric(a: np.ndarray, b: np.ndarray, den: int, metric: int):
+    """Whole-image metric of frame sums a against compared sums b: MSE, SAD,
+    NRMSE or -PSNR (metric 0..3); returns (value, sum of squared differences)."""
+    a, b = _c(a, np.int64), _c(b, np.int64)
+    E = np.zeros(1, np.int64)
+    m = lib().oracle_global_metric(int(metric), _p(a), _p(b), a.shape[0], a.shape[1], den, _p(E))
+    return m, int(E[0])
+
+
+def blocked_metric(a, b, den, grid, w, bias, metric: int):
+    """Blocked detector score bias + sum_k w_k m_k with the per-block metric m_k
+    (MSE, SAD or NRMSE; NaN for PSNR); returns (score, m)."""
+    a, b = _c(a, np.int64), _c(b, np.int64)
+    w = _c(w, np.float32)
+    m = np.zeros(grid[0] * grid[1], np.float64)
+    z = lib().oracle_blocked_metric(int(metric), _p(a), _p(b), a.shape[0], a.shape[1], den,
+                                    grid[0], grid[1], _p(w), float(bias), _p(m))
+    return z, m
 
 
 def blocked_score(a, b, den, grid, w, bias):
@@ -207,6 +236,7 @@ def make_cfg(wl, lr_w=None, ref_sums=None, **over) -> tuple:
         c.ref_sums = rs.ctypes.data
     c.delta_diff, c.c_low, c.c_high = wl.delta_diff, wl.c_low, wl.c_high
     c.check_stride = getattr(wl, "check_stride", 1)
+    c.metric = getattr(wl, "metric", MSE)
     for k, v in over.items():
         setattr(c, k, v)
     return c, keep

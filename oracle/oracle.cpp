@@ -9,7 +9,8 @@
 //   1. area sums: frames are resized before the models [Sec. 7]; read as the
 //      exact area average of the piecewise-constant image, kept as integer
 //      sums S with a common integer denominator den (value = S / den);
-//   2. difference detector [Sec. 5]: MSE against the frame delta earlier or a
+//   2. difference detector [Sec. 5]: MSE (or one of the alternatives the
+//      paper names: SAD, NRMSE, PSNR) against the frame delta earlier or a
 //      fixed reference image, over the whole image or per grid block weighed
 //      by a logistic regression; it fires when the metric is higher than
 //      delta_diff [Sec. 6.2];
@@ -151,46 +152,111 @@ void oracle_area_sums(const uint8_t* frame, int32_t H, int32_t W, int32_t Ho, in
 
 // ------------------------------------------------------- difference detector
 
-// Global MSE between two area-sum images (Sec. 5): mean over Ho*Wo*3 values of
-// ((a - b) / den)^2 on the 0..255 scale.  E_out receives sum (a - b)^2 exactly.
-double oracle_global_mse(const int64_t* a, const int64_t* b, int32_t Ho, int32_t Wo, int64_t den,
-                         int64_t* E_out) {
-  int64_t N = (int64_t)Ho * Wo * 3;
-  int64_t E = 0;
+}  // extern "C"
+
+namespace {
+
+// Distance between two area-sum images a (the frame) and b (the frame it is
+// compared with), both holding N values with denominator den, i.e. a / den and
+// b / den on the 0..255 scale.  Sec. 5 uses the MSE and names three
+// alternatives that were tried: normalized root mean square error, peak
+// signal-to-noise ratio and the sum of absolute differences.  Readings:
+//   MSE   = sum ((a - b) / den)^2 / N;
+//   SAD   = sum |a - b| / den, the sum over all N values;
+//   NRMSE = sqrt(sum (a - b)^2 / sum b^2), the error's Euclidean norm relative
+//           to the compared image's (den cancels): 0 when both sums are 0,
+//           +inf when only the compared image is all zero;
+//   PSNR  = 10 log10(255^2 / MSE), a similarity; the metric reported is its
+//           negation, so that for every metric a larger value means "more
+//           different" and the detector fires above delta_diff (with PSNR:
+//           iff PSNR < -delta_diff); identical images give -inf.
+// The integer sums are exact; each metric is one fp64 expression of them.
+enum { METRIC_MSE = 0, METRIC_SAD = 1, METRIC_NRMSE = 2, METRIC_PSNR = 3 };
+
+double metric_of(int32_t metric, const std::vector<int64_t>& a, const std::vector<int64_t>& b,
+                 int64_t den, int64_t* E_out) {
+  const int64_t N = (int64_t)a.size();
+  int64_t E = 0, A = 0, R = 0;  // sum (a-b)^2, sum |a-b|, sum b^2
   for (int64_t k = 0; k < N; ++k) {
-    int64_t d = a[k] - b[k];
+    const int64_t d = a[k] - b[k];
     E += d * d;
+    A += d < 0 ? -d : d;
+    R += b[k] * b[k];
   }
   if (E_out) *E_out = E;
-  return (double)E / ((double)den * (double)den * (double)N);
+  const double mse = (double)E / ((double)den * (double)den * (double)N);
+  switch (metric) {
+    case METRIC_MSE:
+      return mse;
+    case METRIC_SAD:
+      return (double)A / (double)den;
+    case METRIC_NRMSE:
+      if (R == 0) return E == 0 ? 0.0 : std::numeric_limits<double>::infinity();
+      return std::sqrt((double)E / (double)R);
+    case METRIC_PSNR:
+      return -(10.0 * std::log10(65025.0 / mse));
+  }
+  return std::numeric_limits<double>::quiet_NaN();
 }
 
-// Blocked detector (Sec. 5): MSE m_k per grid block k = by*Gw + bx (block rows
-// [floor(by*Ho/Gh), floor((by+1)*Ho/Gh)), columns likewise), weighed by a
-// logistic regression: score = bias + sum_k w_k m_k.
-double oracle_blocked_score(const int64_t* a, const int64_t* b, int32_t Ho, int32_t Wo,
-                            int64_t den, int32_t Gh, int32_t Gw, const float* w, double bias,
-                            double* m_out) {
+// The values of block k = by*Gw + bx of an [Ho][Wo][3] image: rows
+// [floor(by*Ho/Gh), floor((by+1)*Ho/Gh)), columns likewise.
+std::vector<int64_t> block_values(const int64_t* a, int32_t Ho, int32_t Wo, int32_t Gh, int32_t Gw,
+                                  int by, int bx) {
+  (void)Ho;
+  const int y0 = (int)((int64_t)by * Ho / Gh), y1 = (int)((int64_t)(by + 1) * Ho / Gh);
+  const int x0 = (int)((int64_t)bx * Wo / Gw), x1 = (int)((int64_t)(bx + 1) * Wo / Gw);
+  std::vector<int64_t> v;
+  for (int y = y0; y < y1; ++y)
+    for (int x = x0; x < x1; ++x)
+      for (int c = 0; c < 3; ++c) v.push_back(a[((size_t)y * Wo + x) * 3 + c]);
+  return v;
+}
+
+}  // namespace
+
+extern "C" {
+
+// Whole-image metric (global detector, Sec. 5).  E_out (nullable) receives
+// sum (a - b)^2 exactly.
+double oracle_global_metric(int32_t metric, const int64_t* a, const int64_t* b, int32_t Ho,
+                            int32_t Wo, int64_t den, int64_t* E_out) {
+  const size_t N = (size_t)Ho * Wo * 3;
+  return metric_of(metric, std::vector<int64_t>(a, a + N), std::vector<int64_t>(b, b + N), den,
+                   E_out);
+}
+
+// Global MSE: mean over Ho*Wo*3 values of ((a - b) / den)^2 on the 0..255
+// scale.  E_out receives sum (a - b)^2 exactly.
+double oracle_global_mse(const int64_t* a, const int64_t* b, int32_t Ho, int32_t Wo, int64_t den,
+                         int64_t* E_out) {
+  return oracle_global_metric(METRIC_MSE, a, b, Ho, Wo, den, E_out);
+}
+
+// Blocked detector (Sec. 5): the metric m_k of every grid block k, weighed by
+// a logistic regression: score = bias + sum_k w_k m_k, added in block order.
+// Reading: with the PSNR metric an unchanged block has m_k = -inf and the sum
+// is undefined, so the blocked detector takes MSE, SAD and NRMSE only (NaN
+// returned for PSNR).
+double oracle_blocked_metric(int32_t metric, const int64_t* a, const int64_t* b, int32_t Ho,
+                             int32_t Wo, int64_t den, int32_t Gh, int32_t Gw, const float* w,
+                             double bias, double* m_out) {
+  if (metric == METRIC_PSNR) return std::numeric_limits<double>::quiet_NaN();
   double z = bias;
-  for (int by = 0; by < Gh; ++by) {
-    int y0 = (int)((int64_t)by * Ho / Gh), y1 = (int)((int64_t)(by + 1) * Ho / Gh);
+  for (int by = 0; by < Gh; ++by)
     for (int bx = 0; bx < Gw; ++bx) {
-      int x0 = (int)((int64_t)bx * Wo / Gw), x1 = (int)((int64_t)(bx + 1) * Wo / Gw);
-      int64_t E = 0;
-      for (int y = y0; y < y1; ++y)
-        for (int x = x0; x < x1; ++x)
-          for (int c = 0; c < 3; ++c) {
-            size_t k = ((size_t)y * Wo + x) * 3 + c;
-            int64_t d = a[k] - b[k];
-            E += d * d;
-          }
-      double cells = (double)(y1 - y0) * (double)(x1 - x0) * 3.0;
-      double m = (double)E / ((double)den * (double)den * cells);
+      const double m = metric_of(metric, block_values(a, Ho, Wo, Gh, Gw, by, bx),
+                                 block_values(b, Ho, Wo, Gh, Gw, by, bx), den, nullptr);
       if (m_out) m_out[by * Gw + bx] = m;
       z += (double)w[by * Gw + bx] * m;
     }
-  }
   return z;
+}
+
+double oracle_blocked_score(const int64_t* a, const int64_t* b, int32_t Ho, int32_t Wo,
+                            int64_t den, int32_t Gh, int32_t Gw, const float* w, double bias,
+                            double* m_out) {
+  return oracle_blocked_metric(METRIC_MSE, a, b, Ho, Wo, den, Gh, Gw, w, bias, m_out);
 }
 
 // ------------------------------------------------------------ specialized CNN
@@ -364,6 +430,7 @@ struct oracle_cfg {
   double delta_diff;
   double c_low, c_high;
   int32_t check_stride;   // frame skipping: check frames t with t mod s = 0 (0 or 1: all)
+  int32_t metric;         // 0 MSE, 1 SAD, 2 NRMSE, 3 -PSNR (see metric_of)
 };
 
 // Number of earlier frames whose sums and decisions a chunked run carries:
@@ -403,6 +470,8 @@ int64_t oracle_cascade(const oracle_cfg* cfg, const oracle_cnn_desc* net, const 
   if (cfg->check_stride < 0) return -1;
   if (cfg->ref_mode == 0 && cfg->delta < 1) return -1;
   if (cfg->ref_mode == 0 && cfg->delta % s != 0) return -1;
+  if (cfg->metric < METRIC_MSE || cfg->metric > METRIC_PSNR) return -1;
+  if (cfg->metric == METRIC_PSNR && cfg->Gh * cfg->Gw > 1) return -1;
   const int64_t D = oracle_history(cfg);  // history frames before t0
   if (D > 0 && t0 > 0 && (!state_S || !state_dec)) return -1;
   // area sums of every frame of the window (history first)
@@ -440,9 +509,9 @@ int64_t oracle_cascade(const oracle_cfg* cfg, const oracle_cnn_desc* net, const 
     } else {
       const int64_t* ref =
           cfg->ref_mode == 0 ? &S[(size_t)(D + k - cfg->delta) * cells] : cfg->ref_sums;
-      sc = blocked ? oracle_blocked_score(cur, ref, cfg->Ho, cfg->Wo, den, cfg->Gh, cfg->Gw,
-                                          cfg->lr_w, cfg->lr_b, nullptr)
-                   : oracle_global_mse(cur, ref, cfg->Ho, cfg->Wo, den, nullptr);
+      sc = blocked ? oracle_blocked_metric(cfg->metric, cur, ref, cfg->Ho, cfg->Wo, den, cfg->Gh,
+                                           cfg->Gw, cfg->lr_w, cfg->lr_b, nullptr)
+                   : oracle_global_metric(cfg->metric, cur, ref, cfg->Ho, cfg->Wo, den, nullptr);
     }
     const bool f = forced || sc > cfg->delta_diff;
     if (score) score[k] = sc;

@@ -14,6 +14,7 @@ from typing import Optional, Tuple
 from . import CNNSpec, VideoSpec
 
 PREV, FIXED = 0, 1
+MSE, SAD, NRMSE, PSNR = 0, 1, 2, 3      # difference metric (Sec. 5 and its alternatives)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -33,6 +34,7 @@ class Workload:
     lr_bias: float = -2.0
     chunk: Optional[int] = None
     check_stride: int = 1          # frame skipping: check frames t with t mod s = 0
+    metric: int = MSE              # detector metric; PSNR reports -PSNR (larger = more different)
 
     def with_frames(self, n: int) -> "Workload":
         return dataclasses.replace(self, video=dataclasses.replace(self.video, n=n))

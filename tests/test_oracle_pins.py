@@ -170,6 +170,156 @@ def test_blocked_uneven_grid_bounds():
             assert m[by * 4 + bx] == pytest.approx((d ** 2).mean(), rel=1e-13)
 
 
+# --------------------------------------------- alternative detector metrics
+
+def test_metrics_hand_computed_4x4():
+    """SAD, NRMSE and PSNR of the worked 4x4 example, at both grids."""
+    rows = _read_golden("metrics_4x4.txt")
+    r = np.full((4, 4, 3), 10, np.uint8)
+    f = r.copy()
+    f[0, 0] = (13, 14, 10)
+    f[3, 3] = (10, 10, 0)
+    for row in rows:
+        g = int(row[1])
+        den = oracle.area_den(4, 4, g, g)
+        a, b = oracle.area_sums(f, g, g), oracle.area_sums(r, g, g)
+        assert oracle.global_metric(a, b, den, oracle.SAD)[0] == float(row[3])
+        assert oracle.global_metric(a, b, den, oracle.NRMSE)[0] == pytest.approx(float(row[5]),
+                                                                                 rel=1e-15)
+        assert oracle.global_metric(a, b, den, oracle.PSNR)[0] == pytest.approx(-float(row[7]),
+                                                                                rel=1e-15)
+        # the MSE through the same entry point is the MSE
+        assert oracle.global_metric(a, b, den, oracle.MSE)[0] == oracle.global_mse(a, b, den)[0]
+    # NRMSE is relative to the compared frame: swapping the frames changes it
+    # (sum of F's squares is 45*100 + 13^2 + 14^2 + 0 = 4865)
+    a, b = oracle.area_sums(f, 4, 4), oracle.area_sums(r, 4, 4)
+    assert oracle.global_metric(b, a, 1, oracle.NRMSE)[0] == pytest.approx(math.sqrt(125 / 4865),
+                                                                           rel=1e-15)
+    assert oracle.global_metric(b, a, 1, oracle.SAD)[0] == 17.0
+
+
+@pytest.mark.parametrize("k", [1, 3, 51])
+def test_metrics_of_constant_offset(k):
+    """A uniform brightness change of k levels (no clipping): SAD = N k,
+    PSNR = 20 log10(255 / k), and NRMSE = k / v over a uniform image of v."""
+    den = oracle.area_den(480, 640, 50, 50)
+    N = 50 * 50 * 3
+    f = rng.integers(20, 200, size=(480, 640, 3), dtype=np.uint8)
+    a, b = oracle.area_sums(f + k, 50, 50), oracle.area_sums(f, 50, 50)
+    assert oracle.global_metric(a, b, den, oracle.SAD)[0] == N * k
+    assert -oracle.global_metric(a, b, den, oracle.PSNR)[0] == pytest.approx(
+        20 * math.log10(255 / k), rel=1e-14)
+    u = np.full((480, 640, 3), 120, np.uint8)
+    nr = oracle.global_metric(oracle.area_sums(u + k, 50, 50), oracle.area_sums(u, 50, 50), den,
+                              oracle.NRMSE)[0]
+    assert nr == pytest.approx(k / 120, rel=1e-15)
+    if k == 51:  # a fifth of the range: 20 log10(5)
+        assert -oracle.global_metric(a, b, den, oracle.PSNR)[0] == pytest.approx(
+            13.979400086720377, rel=1e-15)
+
+
+def test_metrics_special_cases():
+    """Identical images, an all-zero compared image, and the PSNR of MSE = 1."""
+    den = oracle.area_den(480, 640, 50, 50)
+    f = rng.integers(0, 256, size=(480, 640, 3), dtype=np.uint8)
+    S = oracle.area_sums(f, 50, 50)
+    assert oracle.global_metric(S, S, den, oracle.SAD)[0] == 0.0
+    assert oracle.global_metric(S, S, den, oracle.NRMSE)[0] == 0.0
+    assert oracle.global_metric(S, S, den, oracle.PSNR)[0] == -math.inf
+    Z = np.zeros_like(S)
+    assert oracle.global_metric(S, Z, den, oracle.NRMSE)[0] == math.inf
+    assert oracle.global_metric(Z, Z, den, oracle.NRMSE)[0] == 0.0
+    # a black frame compared with a non-black one is off by all of it
+    assert oracle.global_metric(Z, S, den, oracle.NRMSE)[0] == 1.0
+    # MSE = 1 (every value one level off): PSNR = 20 log10(255) = 48.1308... dB
+    one = np.ones((2, 2, 3), np.int64)
+    assert -oracle.global_metric(one, 0 * one, 1, oracle.PSNR)[0] == pytest.approx(
+        48.130803608679102, rel=1e-15)
+
+
+def test_metrics_bounds_and_equality_cases():
+    """(SAD / N)^2 <= MSE (Cauchy-Schwarz), with equality iff every |d| is equal;
+    the reverse triangle inequality bounds NRMSE below; -PSNR rises with MSE."""
+    N = 30 * 40 * 3
+    for seed in range(20):
+        r = np.random.default_rng(seed)
+        den = int(r.integers(1, 50))
+        b = r.integers(0, 255 * den + 1, size=(30, 40, 3)).astype(np.int64)
+        a = r.integers(0, 255 * den + 1, size=(30, 40, 3)).astype(np.int64)
+        mse = oracle.global_metric(a, b, den, oracle.MSE)[0]
+        sad = oracle.global_metric(a, b, den, oracle.SAD)[0]
+        nr = oracle.global_metric(a, b, den, oracle.NRMSE)[0]
+        assert (sad / N) ** 2 <= mse * (1 + 1e-12)
+        na, nb = np.linalg.norm(a.astype(np.float64)), np.linalg.norm(b.astype(np.float64))
+        assert abs(na / nb - 1) <= nr * (1 + 1e-12)
+        # equal magnitudes, mixed signs
+        k = int(r.integers(1, 9)) * den
+        sign = np.where(r.random((30, 40, 3)) < 0.5, -1, 1)
+        c = b + k * sign
+        assert oracle.global_metric(c, b, den, oracle.SAD)[0] == N * (k // den)
+        assert oracle.global_metric(c, b, den, oracle.MSE)[0] == (k // den) ** 2
+        # -PSNR is increasing in the MSE
+        m2 = oracle.global_metric(2 * a - b, b, den, oracle.MSE)[0]  # differences doubled
+        p1 = oracle.global_metric(a, b, den, oracle.PSNR)[0]
+        p2 = oracle.global_metric(2 * a - b, b, den, oracle.PSNR)[0]
+        assert m2 == pytest.approx(4 * mse, rel=1e-14)
+        assert p2 == pytest.approx(p1 + 20 * math.log10(2), rel=1e-13)
+
+
+def test_blocked_metrics_brute_force():
+    """Per-block SAD and NRMSE on an uneven 3x4 grid, block by block; a 1x1 grid
+    with weight 1 and bias 0 is the global metric; PSNR is not blocked."""
+    a = rng.integers(0, 5000, size=(7, 11, 3)).astype(np.int64)
+    b = rng.integers(1, 5000, size=(7, 11, 3)).astype(np.int64)
+    den = 3
+    w = rng.standard_normal(12).astype(np.float32)
+    for metric in (oracle.SAD, oracle.NRMSE):
+        z, m = oracle.blocked_metric(a, b, den, (3, 4), w, 0.25, metric)
+        zz = 0.25
+        for by in range(3):
+            for bx in range(4):
+                ys = slice(by * 7 // 3, (by + 1) * 7 // 3)
+                xs = slice(bx * 11 // 4, (bx + 1) * 11 // 4)
+                d = (a[ys, xs] - b[ys, xs]).astype(np.float64)
+                exp = (np.abs(d).sum() / den if metric == oracle.SAD else
+                       math.sqrt((d ** 2).sum() / (b[ys, xs].astype(np.float64) ** 2).sum()))
+                assert m[by * 4 + bx] == pytest.approx(exp, rel=1e-13)
+                zz += float(w[by * 4 + bx]) * m[by * 4 + bx]
+        assert z == pytest.approx(zz, rel=1e-12, abs=1e-9)
+        z1, _ = oracle.blocked_metric(a, b, den, (1, 1), np.ones(1, np.float32), 0.0, metric)
+        assert z1 == oracle.global_metric(a, b, den, metric)[0]
+    assert math.isnan(oracle.blocked_metric(a, b, den, (3, 4), w, 0.0, oracle.PSNR)[0])
+
+
+def test_cascade_psnr_fires_like_mse_at_the_matching_threshold():
+    """-PSNR > d  <=>  MSE > 255^2 10^(d/10): the PSNR detector fires on the same
+    frames as the MSE detector at the matching threshold (frames within rounding
+    of it aside); with every metric an unchanged frame never fires."""
+    wl = _tiny_fast()
+    v, blob = _small(wl, 300)
+    frames = v.frames(200, 500)
+    for d in (-35.0, -30.0, -25.0):
+        cfg_p, _ = oracle.make_cfg(wl.replace(delta_diff=d), metric=oracle.PSNR)
+        out_p, _ = oracle.cascade(cfg_p, wl.cnn, blob, frames)
+        m_thr = 65025.0 * 10 ** (d / 10)
+        cfg_m, _ = oracle.make_cfg(wl.replace(delta_diff=m_thr))
+        out_m, _ = oracle.cascade(cfg_m, wl.cnn, blob, frames)
+        near = np.abs(out_m["score"] - m_thr) <= 1e-9 * m_thr
+        assert not near.any()
+        assert 0 < out_p["fire"].sum() < len(frames)
+        for k in ("fire", "label", "defer"):
+            assert (out_p[k] == out_m[k]).all()
+    still = np.repeat(frames[:1], 6, axis=0)
+    for metric in (oracle.SAD, oracle.NRMSE, oracle.PSNR):
+        cfg, _ = oracle.make_cfg(wl.replace(delta_diff=0.0), metric=metric)
+        out, _ = oracle.cascade(cfg, wl.cnn, blob, still)
+        assert list(np.flatnonzero(out["fire"])) == [0]   # only the forced first frame
+    cfg, _ = oracle.make_cfg(wl.replace(grid=(2, 2)), lr_w=np.ones(4, np.float32),
+                             metric=oracle.PSNR)
+    with pytest.raises(ValueError):
+        oracle.cascade(cfg, wl.cnn, blob, frames[:5])
+
+
 # --------------------------------------------------------------- CNN pieces
 
 def test_round_bf16_against_torch_and_ties():
