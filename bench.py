@@ -31,6 +31,9 @@ thresholds at 1 % FP / FN targets; `value` is frames x candidates per second.
 The cascade is then run with the chosen thresholds, and its measured time per
 frame is reported beside the cost model's prediction.
 
+--metric sad / nrmse / psnr runs the 640x480 workload with one of the
+alternative detector metrics (Sec. 5), at a threshold matching MSE 15.
+
 Every run also measures the peaks the roofline fractions are quoted against:
 a streaming read of the resident frame buffer (HBM) and a loop of independent
 bf16 MFMAs, next to the published 8 TB/s and 2.5 PFLOP/s.
@@ -42,6 +45,7 @@ from __future__ import annotations
 import argparse
 import ctypes
 import json
+import math
 import os
 import sys
 import time
@@ -207,6 +211,17 @@ def cpu_baseline(wl, budget_s: float, lr_w=None, ref_img=None) -> dict:
 
 CHUNKED = ("hd-ref", "hd-blocked", "fhd-stream")
 T_FULL_NN = 1.0 / 80.0  # reference network per frame: YOLOv2 at 80 frames/s (Sec. 2)
+# Detector metric -> (code, delta_diff) on the 640x480 workload: thresholds that
+# match MSE 15 on the 50x50x3 = 7,500 values: -PSNR fires on the same frames
+# (10 log10(15 / 255^2)); SAD on a uniform error of sqrt(15) levels (N sqrt(15),
+# a subset of MSE's frames, since SAD <= N sqrt(MSE)); NRMSE on that error over
+# a mid-grey compared image (sqrt(15) / 128).
+METRIC_DD = {
+    "mse": (0, 15.0),
+    "sad": (1, 7500 * 15 ** 0.5),
+    "nrmse": (2, 15 ** 0.5 / 128.0),
+    "psnr": (3, 10.0 * math.log10(15.0 / 65025.0)),
+}
 
 
 def bench_sweep(args):
@@ -472,6 +487,9 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain copy of known size (for counter calibration)")
     ap.add_argument("--workload", choices=("vga", "vga-sweep") + CHUNKED, default="vga")
+    ap.add_argument("--metric", choices=tuple(METRIC_DD), default="mse",
+                    help="detector metric on the 640x480 workload (Sec. 5 and the alternatives "
+                         "it names), at the threshold matching MSE 15 (see METRIC_DD)")
     ap.add_argument("--check-stride", type=int, default=1,
                     help="frame skipping on the 640x480 workload: check every s-th frame "
                          "(s must divide 15); 1 is the headline configuration")
@@ -505,6 +523,9 @@ def main():
     from synth import workloads as W
 
     wl = W.VGA.replace(check_stride=args.check_stride)
+    if args.metric != "mse":
+        code, dd = METRIC_DD[args.metric]
+        wl = wl.replace(metric=code, delta_diff=dd, name=f"{wl.name}-{args.metric}")
     n = wl.video.n
     fb = wl.video.frame_bytes
     dev = torch.device("cuda:0")
@@ -549,7 +570,7 @@ def main():
     checked = -(-n // wl.check_stride)        # frames the detector reads
     area_bytes = checked * fb                 # algorithmic: every checked frame's bytes once
     achieved = area_bytes / (area_ms * 1e-3) / 1e9
-    traffic, traffic_src = measured_traffic(wl.name)
+    traffic, traffic_src = measured_traffic(W.VGA.name)  # the area kernel ignores the metric
     if wl.check_stride != 1:
         traffic, traffic_src = None, "counters were taken without frame skipping"
     cnn_ms = float(stage[:, 3].mean())
@@ -573,8 +594,9 @@ def main():
             "workload": wl.name,
             "frames": n,
             "frame": f"{wl.video.w}x{wl.video.h} RGB u8",
-            "detector": f"{wl.dd_w}x{wl.dd_h} area average, global MSE vs frame t-{wl.delta}, "
-                        f"delta_diff {wl.delta_diff}",
+            "detector": f"{wl.dd_w}x{wl.dd_h} area average, global "
+                        f"{'-PSNR' if args.metric == 'psnr' else args.metric.upper()} vs frame "
+                        f"t-{wl.delta}, delta_diff {wl.delta_diff:.6g}",
             "check_stride": wl.check_stride,
             "cnn": "2 x (conv3x3 32 + ReLU + maxpool2), dense 128, sigmoid; bf16",
             "c_low": wl.c_low,

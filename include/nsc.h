@@ -10,7 +10,8 @@
  * Per frame the hot path is:
  *   1. downsample: exact area average onto a small grid (Sec. 7 resizes frames
  *      before the models); kept as integer area sums S with one denominator;
- *   2. difference detector (Sec. 5): MSE against the frame `delta` earlier or
+ *   2. difference detector (Sec. 5): MSE (or SAD, NRMSE, PSNR, the
+ *      alternatives the paper names) against the frame `delta` earlier or
  *      against a fixed reference image, globally or per grid block weighed by
  *      logistic regression; fires when the metric exceeds delta_diff;
  *   3. compaction of the frames that fire (Sec. 7 batches frames for the GPU);
@@ -59,6 +60,19 @@ typedef enum nsc_status {
 } nsc_status;
 
 enum { NSC_REF_PREV = 0, NSC_REF_FIXED = 1 };
+/* Difference metric of the detector (Sec. 5 uses the MSE and names NRMSE,
+ * PSNR and SAD as alternatives it tried).  On the area-average values a
+ * (frame) and b (compared frame), N values on the 0..255 scale:
+ *   MSE   sum (a-b)^2 / N
+ *   SAD   sum |a-b|
+ *   NRMSE sqrt(sum (a-b)^2 / sum b^2)  (0 if both sums are 0, +inf if only
+ *         sum b^2 is 0)
+ *   PSNR  -10 log10(255^2 / MSE): the negated PSNR, so that for every metric
+ *         the detector fires when the value exceeds delta_diff (PSNR below
+ *         -delta_diff); identical images give -inf.
+ * MSE, SAD and NRMSE are correctly rounded fp64 functions of exact integer
+ * sums; PSNR goes through the device log10 (within a few ulp). */
+enum { NSC_METRIC_MSE = 0, NSC_METRIC_SAD = 1, NSC_METRIC_NRMSE = 2, NSC_METRIC_PSNR = 3 };
 enum { NSC_F32 = 0, NSC_BF16 = 1 };
 enum { NSC_MAX_CONV = 8, NSC_MAX_DELTA = 256, NSC_MAX_BLOCKS = 1024, NSC_MAX_STRIDE = 4096,
        NSC_MAX_SWEEP = 65535 };
@@ -76,7 +90,7 @@ typedef struct nsc_cascade_cfg {
   int32_t cnn_h, cnn_w;      /* CNN input grid; dd_h = fy*cnn_h, dd_w = fx*cnn_w  */
   int32_t ref_mode;          /* NSC_REF_PREV (frame t-delta) or NSC_REF_FIXED     */
   int32_t delta;             /* PREV: comparison offset, 1..NSC_MAX_DELTA frames  */
-  int32_t grid_h, grid_w;    /* 1x1: global MSE; otherwise blocked detector       */
+  int32_t grid_h, grid_w;    /* 1x1: global metric; otherwise blocked detector    */
   const float* lr_w;         /* (device) grid_h*grid_w LR weights, row-major;
                                 blocked only                                     */
   double lr_b;               /* LR bias; blocked only                            */
@@ -92,6 +106,8 @@ typedef struct nsc_cascade_cfg {
                                 at most NSC_MAX_STRIDE; PREV needs delta to be
                                 a multiple of s (the compared frame is then a
                                 checked one)                                   */
+  int32_t metric;            /* NSC_METRIC_* (0 = MSE); the blocked detector
+                                takes MSE, SAD or NRMSE per block              */
 } nsc_cascade_cfg;
 
 /* Shape of a specialized CNN (Sec. 4): n_conv x [conv3x3 'same' + bias + ReLU
@@ -188,8 +204,9 @@ int nsc_downsample(const uint8_t* frames, int64_t n, int32_t in_h, int32_t in_w,
 
 /* Steps 1-2 (Sec. 5).  Downsamples frames [t0, t0+n) into sums_out (device,
  * n*dd_h*dd_w*3 int32) and scores each against its reference:
- *   global:  score = sum (S_t - S_ref)^2 / (den^2 * dd_h*dd_w*3)   (the MSE)
- *   blocked: score = lr_b + sum_k lr_w[k] * MSE over block k, blocks being
+ *   global:  score = the metric of S_t / den against S_ref / den; with MSE
+ *            sum (S_t - S_ref)^2 / (den^2 * dd_h*dd_w*3)
+ *   blocked: score = lr_b + sum_k lr_w[k] * metric over block k, blocks being
  *            rows [floor(by*dd_h/grid_h), floor((by+1)*dd_h/grid_h)) x
  *            columns likewise, k = by*grid_w + bx;
  * S_ref is frame t-delta (PREV) or cfg->ref_sums (FIXED).  In PREV mode a

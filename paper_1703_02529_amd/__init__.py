@@ -16,6 +16,7 @@ from typing import Optional
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libnsc.so")
 
 NSC_REF_PREV, NSC_REF_FIXED = 0, 1
+NSC_METRIC_MSE, NSC_METRIC_SAD, NSC_METRIC_NRMSE, NSC_METRIC_PSNR = 0, 1, 2, 3
 NSC_F32, NSC_BF16 = 0, 1
 NSC_MAX_CONV = 8
 
@@ -34,7 +35,7 @@ class CascadeCfg(ctypes.Structure):
                 ("dd_w", _i32), ("cnn_h", _i32), ("cnn_w", _i32), ("ref_mode", _i32),
                 ("delta", _i32), ("grid_h", _i32), ("grid_w", _i32), ("lr_w", _vp),
                 ("lr_b", _dbl), ("ref_sums", _vp), ("delta_diff", _dbl), ("c_low", _dbl),
-                ("c_high", _dbl), ("check_stride", _i32)]
+                ("c_high", _dbl), ("check_stride", _i32), ("metric", _i32)]
 
 
 class CnnDesc(ctypes.Structure):
@@ -134,7 +135,7 @@ def _stream(stream) -> Optional[int]:
 
 def make_cfg(*, in_h, in_w, dd_h, dd_w, cnn_h, cnn_w, ref_mode=NSC_REF_PREV, delta=1,
              grid=(1, 1), lr_w=None, lr_b=0.0, ref_sums=None, delta_diff=0.0, c_low=0.2,
-             c_high=0.8, frame_stride=None, check_stride=1) -> CascadeCfg:
+             c_high=0.8, frame_stride=None, check_stride=1, metric=0) -> CascadeCfg:
     """Builds a CascadeCfg; lr_w and ref_sums are device tensors (kept alive by the caller)."""
     c = CascadeCfg()
     c.in_h, c.in_w = in_h, in_w
@@ -147,6 +148,7 @@ def make_cfg(*, in_h, in_w, dd_h, dd_w, cnn_h, cnn_w, ref_mode=NSC_REF_PREV, del
     c.ref_sums = _ptr(ref_sums)
     c.delta_diff, c.c_low, c.c_high = delta_diff, c_low, c_high
     c.check_stride = check_stride
+    c.metric = metric
     return c
 
 

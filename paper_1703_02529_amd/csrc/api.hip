@@ -89,7 +89,12 @@ int check_cfg(const nsc_cascade_cfg* c) {
                 "one)", c->delta, c->check_stride);
   NSC_REQUIRE(c->frame_stride <= ((int64_t)1 << 62) / (c->check_stride > 1 ? c->check_stride : 1),
               NSC_E_INVAL, "frame_stride x check_stride overflows");
-  // exact int64 squared-difference sums
+  NSC_REQUIRE(c->metric >= NSC_METRIC_MSE && c->metric <= NSC_METRIC_PSNR, NSC_E_INVAL,
+              "metric %d is not one of NSC_METRIC_MSE / SAD / NRMSE / PSNR", c->metric);
+  NSC_REQUIRE(!(c->metric == NSC_METRIC_PSNR && c->grid_h * c->grid_w > 1), NSC_E_INVAL,
+              "the blocked detector takes MSE, SAD or NRMSE (an unchanged block's -PSNR is "
+              "-inf)");
+  // exact int64 squared-difference sums (and sums of squared reference values)
   const double emax = (255.0 * (double)den) * (255.0 * (double)den) * (double)c->dd_h * c->dd_w * 3;
   NSC_REQUIRE(emax < 9.0e18, NSC_E_SHAPE, "squared-difference sums may overflow 64 bits");
   return NSC_OK;
@@ -486,6 +491,8 @@ int nsc_diff_detect(const nsc_cascade_cfg* cfg, const uint8_t* frames, int64_t n
   a.lr_b = cfg->lr_b;
   a.delta_diff = cfg->delta_diff;
   a.den2 = den * den;
+  a.den = den;
+  a.metric = cfg->metric;
   a.n = n;
   a.t0 = t0;
   a.dd_h = cfg->dd_h;
@@ -588,6 +595,8 @@ int run_checked(const nsc_cascade_cfg* cfg, const Cnn& c, const uint8_t* frames,
     a.lr_b = cfg->lr_b;
     a.delta_diff = cfg->delta_diff;
     a.den2 = den * den;
+    a.den = den;
+    a.metric = cfg->metric;
     a.n = n;
     a.t0 = t0;
     a.dd_h = cfg->dd_h;

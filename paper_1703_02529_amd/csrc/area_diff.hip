@@ -8,10 +8,11 @@
 // the sums fit in 16 bits, then the workgroup reduces horizontally through a
 // double-buffered LDS row, one output cell per thread.
 //
-// Detector (Sec. 5): one wavefront per frame reduces the squared differences
-// of its area sums against the reference with 64-bit shuffle reductions; the
-// blocked variant reduces per grid block and applies the logistic-regression
-// weights in fp64 in block order.
+// Detector (Sec. 5): one wavefront per frame reduces the squared (or
+// absolute) differences of its area sums against the reference with 64-bit
+// shuffle reductions and turns them into the metric (MSE, or SAD, NRMSE,
+// -PSNR); the blocked variant reduces per grid block and applies the
+// logistic-regression weights in fp64 in block order.
 #include "nsc_internal.h"
 
 #include <math.h>
@@ -306,6 +307,40 @@ __device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
   return v;
 }
 
+// The sums one metric needs over a set of values: squared differences e,
+// absolute differences s, squared reference values r.  All exact in int64.
+template <int M>
+struct DiffSums {
+  int64_t e = 0, s = 0, r = 0;
+  __device__ __forceinline__ void add(int32_t x, int32_t y) {
+    const int64_t d = (int64_t)x - y;
+    if constexpr (M != NSC_METRIC_SAD) e += d * d;
+    if constexpr (M == NSC_METRIC_SAD) s += d < 0 ? -d : d;
+    if constexpr (M == NSC_METRIC_NRMSE) r += (int64_t)y * y;
+  }
+  __device__ __forceinline__ void reduce() {
+    if constexpr (M != NSC_METRIC_SAD) e = wave_sum_i64(e);
+    if constexpr (M == NSC_METRIC_SAD) s = wave_sum_i64(s);
+    if constexpr (M == NSC_METRIC_NRMSE) r = wave_sum_i64(r);
+  }
+  // The metric over `count` values (Sec. 5 and the alternatives it names):
+  // each is one fp64 expression of the exact sums, in a fixed operation order.
+  __device__ __forceinline__ double value(const DiffArgs& a, double count) const {
+    if constexpr (M == NSC_METRIC_MSE) {
+      return (double)e / (a.den2 * count);
+    } else if constexpr (M == NSC_METRIC_SAD) {
+      return (double)s / a.den;
+    } else if constexpr (M == NSC_METRIC_NRMSE) {
+      if (r == 0) return e == 0 ? 0.0 : INFINITY;
+      return sqrt((double)e / (double)r);
+    } else {  // the negated PSNR, -10 log10(255^2 / MSE); -inf for identical images
+      const double mse = (double)e / (a.den2 * count);
+      return -(10.0 * log10(65025.0 / mse));
+    }
+  }
+};
+
+template <int M>
 __global__ void __launch_bounds__(256) k_diff(DiffArgs a) {
   // the blocked score is summed with separate multiplies and adds, in block
   // order, so it is reproducible bit for bit
@@ -327,23 +362,22 @@ __global__ void __launch_bounds__(256) k_diff(DiffArgs a) {
     else
       ref = a.prev_sums + i * cells;  // frame t - delta = t0 - delta + i
     if (a.grid_h * a.grid_w == 1) {
-      int64_t e = 0;
+      DiffSums<M> acc;
       if ((cells & 3) == 0 && (((uintptr_t)cur | (uintptr_t)ref) & 15) == 0) {
         const int4* c4 = reinterpret_cast<const int4*>(cur);
         const int4* r4 = reinterpret_cast<const int4*>(ref);
         for (int64_t k = lane; k < cells / 4; k += 64) {
           const int4 x = c4[k], y = r4[k];
-          const int64_t d0 = x.x - y.x, d1 = x.y - y.y, d2 = x.z - y.z, d3 = x.w - y.w;
-          e += d0 * d0 + d1 * d1 + d2 * d2 + d3 * d3;
+          acc.add(x.x, y.x);
+          acc.add(x.y, y.y);
+          acc.add(x.z, y.z);
+          acc.add(x.w, y.w);
         }
       } else {
-        for (int64_t k = lane; k < cells; k += 64) {
-          const int64_t d = cur[k] - ref[k];
-          e += d * d;
-        }
+        for (int64_t k = lane; k < cells; k += 64) acc.add(cur[k], ref[k]);
       }
-      e = wave_sum_i64(e);
-      score = (double)e / (a.den2 * (double)cells);
+      acc.reduce();
+      score = acc.value(a, (double)cells);
     } else {
       double z = a.lr_b;
       for (int by = 0; by < a.grid_h; ++by) {
@@ -354,16 +388,15 @@ __global__ void __launch_bounds__(256) k_diff(DiffArgs a) {
           const int x1 = (int)((int64_t)(bx + 1) * a.dd_w / a.grid_w);
           const int rl = (x1 - x0) * 3;
           const int total = (y1 - y0) * rl;
-          int64_t e = 0;
+          DiffSums<M> acc;
           for (int k = lane; k < total; k += 64) {
             const int r = k / rl, cc = k - r * rl;
             const int64_t off = ((int64_t)(y0 + r) * a.dd_w + x0) * 3 + cc;
-            const int64_t d = cur[off] - ref[off];
-            e += d * d;
+            acc.add(cur[off], ref[off]);
           }
-          e = wave_sum_i64(e);
+          acc.reduce();
           const double ncell = ((double)(y1 - y0) * (double)(x1 - x0)) * 3.0;
-          const double m = (double)e / (a.den2 * ncell);
+          const double m = acc.value(a, ncell);
           z = z + (double)a.lr_w[by * a.grid_w + bx] * m;
         }
       }
@@ -481,7 +514,24 @@ int launch_area_sums(const AreaPlan& p, const uint8_t* frames, int64_t stride, i
 int launch_diff(const DiffArgs& a, hipStream_t stream) {
   if (a.n <= 0) return NSC_OK;
   const int64_t blocks = (a.n + 3) / 4;
-  hipLaunchKernelGGL(k_diff, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+  switch (a.metric) {
+    case NSC_METRIC_MSE:
+      hipLaunchKernelGGL(k_diff<NSC_METRIC_MSE>, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+      break;
+    case NSC_METRIC_SAD:
+      hipLaunchKernelGGL(k_diff<NSC_METRIC_SAD>, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+      break;
+    case NSC_METRIC_NRMSE:
+      hipLaunchKernelGGL(k_diff<NSC_METRIC_NRMSE>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                         a);
+      break;
+    case NSC_METRIC_PSNR:
+      hipLaunchKernelGGL(k_diff<NSC_METRIC_PSNR>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                         a);
+      break;
+    default:
+      return fail(NSC_E_INVAL, "metric %d is unknown", a.metric);
+  }
   NSC_CHECK_LAUNCH("k_diff");
   return NSC_OK;
 }

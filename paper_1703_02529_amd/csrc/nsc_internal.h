@@ -82,9 +82,10 @@ struct DiffArgs {
   const int32_t* prev_sums;  // [delta][cells] frames t0-delta..t0-1 (PREV, t0 > 0)
   const int32_t* ref_sums;   // [cells] (FIXED)
   const float* lr_w;         // [grid_h*grid_w] (blocked)
-  double lr_b, delta_diff, den2;  // den2 = den*den as a double
+  double lr_b, delta_diff, den, den2;  // den2 = den*den as a double
   int64_t n, t0;
   int32_t dd_h, dd_w, grid_h, grid_w, ref_mode, delta;
+  int32_t metric;            // NSC_METRIC_*
   double* score;             // nullable
   uint8_t* fire;
 };

@@ -3,8 +3,8 @@
 Allocates (through torch) the workspace, the carried state and the per-frame
 output buffers, creates the CNN handle, and calls nsc_cascade_run.  It reads a
 workload description by attribute (video.h, video.w, dd_h, dd_w, cnn, ref_mode,
-delta, grid, delta_diff, c_low, c_high, lr_bias, check_stride if present) and
-imports nothing else.
+delta, grid, delta_diff, c_low, c_high, lr_bias; check_stride and metric if
+present) and imports nothing else.
 """
 from __future__ import annotations
 
@@ -12,7 +12,7 @@ from typing import Optional
 
 import torch
 
-from . import (NSC_REF_FIXED, NSC_REF_PREV, Cnn, make_cfg, make_desc,
+from . import (NSC_METRIC_MSE, NSC_REF_FIXED, NSC_REF_PREV, Cnn, make_cfg, make_desc,
                nsc_cascade_run, nsc_cascade_workspace_bytes, nsc_state_bytes)
 
 
@@ -28,7 +28,8 @@ class CascadeRunner:
                             delta=wl.delta, grid=tuple(wl.grid), lr_w=lr_w, lr_b=wl.lr_bias,
                             ref_sums=ref_sums, delta_diff=wl.delta_diff, c_low=wl.c_low,
                             c_high=wl.c_high, frame_stride=frame_stride,
-                            check_stride=getattr(wl, "check_stride", 1))
+                            check_stride=getattr(wl, "check_stride", 1),
+                            metric=getattr(wl, "metric", NSC_METRIC_MSE))
         self.desc = make_desc(wl.cnn.conv, wl.cnn.pool, wl.cnn.dense, wl.cnn.in_h, wl.cnn.in_w,
                               wl.cnn.bf16)
         self.cnn = Cnn(self.desc, blob)

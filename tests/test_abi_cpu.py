@@ -65,10 +65,25 @@ def test_valid_configs_pass():
     (dict(check_stride=-1), -1),
     (dict(check_stride=4097), -1),
     (dict(check_stride=4), -1),           # delta 15 is not a multiple of the stride
+    (dict(metric=-1), -1),
+    (dict(metric=4), -1),
 ])
 def test_invalid_configs(kw, code):
     assert nsc.nsc_cfg_check(_cfg(**kw)) == code
     assert nsc.last_error() != ""
+
+
+def test_detector_metrics():
+    for m in (nsc.NSC_METRIC_MSE, nsc.NSC_METRIC_SAD, nsc.NSC_METRIC_NRMSE, nsc.NSC_METRIC_PSNR):
+        assert nsc.nsc_cfg_check(_cfg(metric=m)) == 0
+    for m in (nsc.NSC_METRIC_MSE, nsc.NSC_METRIC_SAD, nsc.NSC_METRIC_NRMSE):
+        c = _cfg(metric=m, grid=(10, 10))
+        c.lr_w = 16
+        assert nsc.nsc_cfg_check(c) == 0
+    # the blocked detector does not take PSNR (an unchanged block is -inf)
+    c = _cfg(metric=nsc.NSC_METRIC_PSNR, grid=(10, 10))
+    c.lr_w = 16
+    assert nsc.nsc_cfg_check(c) == -1 and "PSNR" in nsc.last_error()
 
 
 def test_frame_skipping_sizes():

@@ -1,0 +1,195 @@
+"""GPU parity of the alternative detector metrics (SAD, NRMSE, -PSNR; Sec. 5
+names them as the alternatives to MSE it tried) against the fp64 oracle.
+
+Scores are bit-identical except -PSNR, whose log10 the host and the device
+round differently (within PSNR_SCORE_TOL); thresholds are placed half-way
+between two oracle scores, so that every fire flag is pinned exactly.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1703_02529_amd as nsc
+import synth
+from paper_1703_02529_amd.runner import CascadeRunner
+from synth import workloads as W
+
+from helpers import compare_scores, lr_weights_for
+from test_gpu_parity import (_dev, _first_occupied, _run_and_compare,
+                             _run_and_compare_from_zero_window)
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+METRICS = [W.MSE, W.SAD, W.NRMSE, W.PSNR]
+NAMES = {W.MSE: "mse", W.SAD: "sad", W.NRMSE: "nrmse", W.PSNR: "psnr"}
+
+
+def _threshold_between(scores, q):
+    """Half-way between the two distinct finite scores around quantile q (one
+    above the only finite score when there is just one)."""
+    s = np.unique(scores[np.isfinite(scores)])
+    if s.size < 2:
+        return float(s[0]) + 1.0 if s.size else 0.0
+    k = min(int(q * (s.size - 1)), s.size - 2)
+    return 0.5 * (s[k] + s[k + 1])
+
+
+def _oracle_score(metric, cur, ref, den, grid, lr_w, lr_b):
+    if grid == (1, 1):
+        return oracle.global_metric(cur, ref, den, metric)[0]
+    return oracle.blocked_metric(cur, ref, den, grid, lr_w, lr_b, metric)[0]
+
+
+# --------------------------------------------------------------- detector
+
+def _diff_metric_case(metric, H, W_, Ho, Wo, ref_mode, delta, grid, n, t0, black_ref=False,
+                      seed=0):
+    r = np.random.default_rng(seed)
+    frames = r.integers(0, 256, size=(n + delta, H, W_, 3), dtype=np.uint8)
+    for k in range(1, n + delta):
+        keep = r.random((H, W_, 1)) < 0.9
+        frames[k] = np.where(keep, frames[k - 1], frames[k])
+    # frames equal to the frame they are compared with, and an all-black frame
+    if ref_mode == 0:
+        for k in (delta + 2, delta + 5):
+            frames[k] = frames[k - delta]
+    frames[delta + 3] = 0
+    if black_ref:
+        frames[0] = 0
+    den = oracle.area_den(H, W_, Ho, Wo)
+    S = np.stack([oracle.area_sums(f, Ho, Wo) for f in frames])
+    lr_w = r.standard_normal(grid[0] * grid[1]).astype(np.float32)
+    lr_b = -0.5
+    exp = np.empty(n)
+    for i in range(n):
+        t = t0 + i
+        if ref_mode == 0 and t < delta:
+            exp[i] = math.inf
+        else:
+            ref = S[0] if ref_mode == 1 else S[i]
+            exp[i] = _oracle_score(metric, S[delta + i], ref, den, grid, lr_w, lr_b)
+    dd = _threshold_between(exp, 0.5)
+    lr_dev = _dev(lr_w)                      # the cfg holds raw pointers: keep these alive
+    ref_dev = _dev(S[0].astype(np.int32).reshape(-1))
+    cfg = nsc.make_cfg(in_h=H, in_w=W_, dd_h=Ho, dd_w=Wo, cnn_h=Ho, cnn_w=Wo, ref_mode=ref_mode,
+                       delta=delta, grid=grid, delta_diff=dd, lr_b=lr_b, metric=metric,
+                       lr_w=lr_dev if grid != (1, 1) else None,
+                       ref_sums=ref_dev if ref_mode == 1 else None)
+    dframes = _dev(frames[delta:].reshape(-1))
+    prev = _dev(S[:delta].astype(np.int32).reshape(-1)) if (ref_mode == 0 and t0 > 0) else None
+    sums = torch.empty(n * Ho * Wo * 3, dtype=torch.int32, device=DEV)
+    score = torch.empty(n, dtype=torch.float64, device=DEV)
+    fire = torch.empty(n, dtype=torch.uint8, device=DEV)
+    nsc.nsc_diff_detect(cfg, dframes, n, t0, sums, fire, score_out=score, prev_sums=prev)
+    g_s, g_f = score.cpu().numpy(), fire.cpu().numpy()
+    assert np.array_equal(sums.cpu().numpy().reshape(n, Ho, Wo, 3), S[delta:])
+    wl = W.TINY.replace(metric=metric, delta_diff=dd)
+    compare_scores(wl, g_s, exp)
+    forced = np.array([ref_mode == 0 and t0 + i < delta for i in range(n)])
+    assert np.array_equal(g_f, ((exp > dd) | forced).astype(np.uint8))
+    return exp
+
+
+CASES = {
+    "vga-prev3": dict(H=480, W_=640, Ho=50, Wo=50, ref_mode=0, delta=3, grid=(1, 1), n=24, t0=5),
+    "vga-prev3-t0": dict(H=480, W_=640, Ho=50, Wo=50, ref_mode=0, delta=3, grid=(1, 1), n=20,
+                         t0=0),
+    "fixed-black-ref": dict(H=100, W_=100, Ho=50, Wo=50, ref_mode=1, delta=1, grid=(1, 1), n=16,
+                            t0=5, black_ref=True),
+    "fixed-odd": dict(H=150, W_=150, Ho=75, Wo=75, ref_mode=1, delta=1, grid=(1, 1), n=9, t0=0),
+    "blocked-10x10": dict(H=200, W_=200, Ho=100, Wo=100, ref_mode=0, delta=1, grid=(10, 10),
+                          n=12, t0=9),
+    "blocked-uneven": dict(H=90, W_=120, Ho=50, Wo=50, ref_mode=0, delta=2, grid=(3, 4), n=12,
+                           t0=0),
+}
+
+
+@pytest.mark.parametrize("metric", METRICS, ids=lambda m: NAMES[m])
+@pytest.mark.parametrize("case", list(CASES), ids=list(CASES))
+def test_diff_detect_metric_parity(metric, case):
+    c = CASES[case]
+    if metric == W.PSNR and c["grid"] != (1, 1):
+        pytest.skip("the blocked detector does not take PSNR (checked on the host)")
+    exp = _diff_metric_case(metric, **c)
+    if metric == W.PSNR and c["ref_mode"] == 0:
+        assert (exp == -math.inf).any()       # the unchanged frames
+    if metric == W.NRMSE and c.get("black_ref"):
+        assert (exp == math.inf).sum() >= c["n"] - 1 and (exp == 0.0).any()
+
+
+def test_blocked_psnr_is_rejected():
+    lr = torch.zeros(100, device=DEV)
+    cfg = nsc.make_cfg(in_h=200, in_w=200, dd_h=100, dd_w=100, cnn_h=100, cnn_w=100, grid=(10, 10),
+                       lr_w=lr, metric=W.PSNR)
+    with pytest.raises(nsc.NscError, match="PSNR"):
+        nsc.nsc_diff_detect(cfg, torch.zeros(200 * 200 * 3, dtype=torch.uint8, device=DEV), 1, 0,
+                            torch.empty(100 * 100 * 3, dtype=torch.int32, device=DEV),
+                            torch.empty(1, dtype=torch.uint8, device=DEV))
+
+
+# ---------------------------------------------------------------- cascade
+
+def _with_threshold(wl, n, q, frames=None):
+    """wl with delta_diff half-way between two of the oracle's scores of the
+    first n frames (from a run whose detector never fires on its own)."""
+    v = synth.Video(wl.video)
+    frames = v.frames(0, n) if frames is None else frames
+    blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
+    lr = lr_weights_for(wl) if wl.grid != (1, 1) else None
+    ref_o = oracle.area_sums(v.median_background(), wl.dd_h, wl.dd_w) if wl.ref_mode == 1 else None
+    cfg, keep = oracle.make_cfg(wl.replace(delta_diff=math.inf), lr_w=lr, ref_sums=ref_o)
+    out, _ = oracle.cascade(cfg, wl.cnn, blob, frames)
+    return wl.replace(delta_diff=float(_threshold_between(out["score"], q)))
+
+
+@pytest.mark.parametrize("metric", METRICS, ids=lambda m: NAMES[m])
+def test_cascade_tiny_full_video_metrics(metric):
+    wl = _with_threshold(W.TINY.replace(metric=metric), W.TINY.video.n, 0.7)
+    rep = _run_and_compare(wl, wl.video.n)
+    assert 0.2 * wl.video.n < rep["fired"] < 0.5 * wl.video.n
+    print(NAMES[metric], wl.delta_diff, rep)
+    rep = _run_and_compare(wl, 400, chunks=[100, 1, 99, 200])
+    print(rep)
+
+
+@pytest.mark.parametrize("metric", [W.SAD, W.PSNR], ids=["sad", "psnr"])
+def test_cascade_vga_window_metrics(metric):
+    wl = W.VGA.replace(metric=metric)
+    t0 = _first_occupied(wl, 20)
+    frames = synth.Video(wl.video).frames(t0, t0 + 120)
+    wl = _with_threshold(wl, 120, 0.6, frames=frames)
+    rep = _run_and_compare_from_zero_window(wl, t0, 120)
+    assert rep["fired"] > 20
+    print(NAMES[metric], wl.delta_diff, rep)
+
+
+@pytest.mark.parametrize("metric", [W.SAD, W.NRMSE], ids=["sad", "nrmse"])
+def test_cascade_blocked_window_metrics(metric):
+    """The 720p blocked detector with per-block SAD / NRMSE under the LR weights
+    (delta_diff 0: the sign of the LR logit)."""
+    wl = W.HD_BLOCKED.replace(metric=metric)
+    t0 = _first_occupied(wl, 4)
+    rep = _run_and_compare_from_zero_window(wl, t0, 16)
+    print(NAMES[metric], rep)
+
+
+def test_psnr_fires_like_mse_at_the_matching_threshold():
+    """On the GPU too: -PSNR > d exactly where MSE > 255^2 10^(d/10)."""
+    wl = W.TINY
+    v = synth.Video(wl.video)
+    frames = v.frames(0, 600)
+    blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
+    d = -31.0
+    fires = []
+    for metric, dd in ((W.PSNR, d), (W.MSE, 65025.0 * 10 ** (d / 10))):
+        run = CascadeRunner(wl.replace(metric=metric, delta_diff=dd), blob, max_frames=600)
+        run.run(_dev(frames.reshape(-1)), 600, t0=0)
+        fires.append(run.fire[:600].cpu().numpy().copy())
+        mse_scores = run.score[:600].cpu().numpy().copy()
+        run.close()
+    near = np.abs(mse_scores - 65025.0 * 10 ** (d / 10)) <= 1e-9 * 65025.0 * 10 ** (d / 10)
+    assert not near.any() and 0 < fires[0].sum() < 600
+    assert np.array_equal(fires[0], fires[1])
