@@ -260,6 +260,54 @@ int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_
                     nsc_run_stats* stats, void* const* stage_events, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Camera groups (Sec. 8: a system that watches many streams can batch frames
+ * of different streams together, each stream with its own model).  A group of
+ * n_cams fixed cameras shares the frame geometry (in_h, in_w, frame_stride,
+ * dd_h, dd_w, cnn_h, cnn_w) and the detector metric; every camera keeps its
+ * own reference (ref_mode, delta, ref_sums), block grid and LR weights,
+ * thresholds (delta_diff, c_low, c_high) and specialized CNN (one network
+ * description for the whole group, each camera with its own weights).  One
+ * nsc_group_run call processes n frames of every camera, each stage as one
+ * launch over all cameras' frames: the CNN runs every survivor with its
+ * camera's weights (grouped GEMM).  Each camera's outputs are exactly those of
+ * nsc_cascade_run on its own frames with its own cfg and network.  Frame
+ * skipping is not available in a group (check_stride 0 or 1). */
+enum { NSC_MAX_CAMERAS = 65535 };
+
+typedef struct nsc_group nsc_group; /* opaque: per-camera device tables */
+
+/* cfgs: host array of n_cams configurations (1 .. NSC_MAX_CAMERAS); cnns:
+ * host array of n_cams network handles.  The device buffers the cfgs point to
+ * (lr_w, ref_sums) and the networks must outlive the group.  Allocates the
+ * group's device tables (synchronous, current device).  Errors: NSC_E_INVAL
+ * (a bad cfg, geometry or metric differing from camera 0's, frame skipping,
+ * a NULL handle), NSC_E_SHAPE (a network description differing from camera
+ * 0's, or not matching the CNN grid), NSC_E_NOMEM, NSC_E_HIP. */
+int nsc_group_create(const nsc_cascade_cfg* cfgs, const nsc_cnn* const* cnns, int32_t n_cams,
+                     nsc_group** out);
+/* Frees the group's tables (NULL is a no-op); no enqueued work may use it. */
+int nsc_group_destroy(nsc_group* group);
+/* State carried between consecutive nsc_group_run calls: camera c's slot
+ * (laid out as nsc_cascade_run's state of its cfg) at c * slot_bytes;
+ * bytes = n_cams * slot_bytes.  slot_bytes is nullable. */
+int nsc_group_state_bytes(const nsc_group* group, size_t* bytes, size_t* slot_bytes);
+/* Workspace of nsc_group_run for up to frames_per_cam frames per camera. */
+int nsc_group_workspace_bytes(const nsc_group* group, int64_t frames_per_cam, size_t* bytes);
+/* Steps 1-5 on frames [t0, t0+n) of every camera.  frames (device): camera
+ * c's frame t0 + j at frames + (c * n + j) * frame_stride.  label_out,
+ * defer_out (device, n_cams * n bytes) and the per-frame outputs of `outs`
+ * use the same order (camera-major).  state (device, nsc_group_state_bytes)
+ * is required when a camera compares with earlier frames; with t0 = 0 its
+ * content is ignored.  ws: nsc_group_workspace_bytes(group, >= n).  stats
+ * (host, nullable) sums over all cameras and synchronises the stream;
+ * stage_events as for nsc_cascade_run.  Errors: NSC_E_INVAL, NSC_E_SHAPE,
+ * NSC_E_WORKSPACE, NSC_E_STATE, NSC_E_HIP. */
+int nsc_group_run(const nsc_group* group, const uint8_t* frames, int64_t n, int64_t t0,
+                  void* state, void* ws, size_t ws_bytes, uint8_t* label_out, uint8_t* defer_out,
+                  const nsc_frame_outputs* outs, nsc_run_stats* stats,
+                  void* const* stage_events, void* stream);
+
+/* ------------------------------------------------------------------------
  * Threshold search of the cost-based optimizer (Sec. 6.3, step 3) with its
  * cost model (Sec. 6.2), on logged scores of every frame of an evaluation
  * video.  For each candidate delta_diff[k]:

@@ -93,6 +93,12 @@ def lib() -> ctypes.CDLL:
                                                    _vp, _vp, _vp, _sz, _vp]),
             "nsc_cascade_run": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i64, _vp, _vp, _sz, _vp, _vp,
                                                _vp, _vp, _vp, _vp]),
+            "nsc_group_create": (ctypes.c_int, [_vp, _vp, _i32, _vp]),
+            "nsc_group_destroy": (ctypes.c_int, [_vp]),
+            "nsc_group_state_bytes": (ctypes.c_int, [_vp, _vp, _vp]),
+            "nsc_group_workspace_bytes": (ctypes.c_int, [_vp, _i64, _vp]),
+            "nsc_group_run": (ctypes.c_int, [_vp, _vp, _i64, _i64, _vp, _vp, _sz, _vp, _vp, _vp,
+                                             _vp, _vp, _vp]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -286,6 +292,83 @@ def nsc_cascade_run(cfg, cnn: Cnn, frames, n, t0, state, ws, label_out, defer_ou
         return dict(frames=st.frames, fired=st.fired, positive=st.positive, deferred=st.deferred)
     return None
 
+
+class Group:
+    """Owns an nsc_group handle: cameras sharing a frame geometry, each with its
+    own cfg (CascadeCfg) and network (Cnn).  The cfgs' device buffers and the
+    networks must outlive the group."""
+
+    def __init__(self, cfgs, cnns):
+        if len(cfgs) != len(cnns) or not cfgs:
+            raise ValueError("one cfg and one network per camera")
+        self.n_cams = len(cfgs)
+        self._cfgs = (CascadeCfg * self.n_cams)(*cfgs)
+        self._cnns = (_vp * self.n_cams)(*[c.handle for c in cnns])
+        self.cnns = list(cnns)
+        h = _vp()
+        _check(lib().nsc_group_create(self._cfgs, self._cnns, self.n_cams, ctypes.byref(h)),
+               "nsc_group_create")
+        self.handle = h
+
+    def close(self):
+        if self.handle:
+            _check(lib().nsc_group_destroy(self.handle), "nsc_group_destroy")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def nsc_group_create_status(cfgs, cnn_handles) -> int:
+    """Raw status of nsc_group_create (host-side validation tests); destroys
+    the group when it was created."""
+    n = len(cfgs)
+    arr = (CascadeCfg * n)(*cfgs)
+    hs = (_vp * n)(*cnn_handles)
+    h = _vp()
+    rc = lib().nsc_group_create(arr, hs, n, ctypes.byref(h))
+    if rc == 0:
+        lib().nsc_group_destroy(h)
+    return rc
+
+
+def nsc_group_state_bytes(group: Group) -> tuple:
+    b, s = _sz(), _sz()
+    _check(lib().nsc_group_state_bytes(group.handle, ctypes.byref(b), ctypes.byref(s)),
+           "nsc_group_state_bytes")
+    return b.value, s.value
+
+
+def nsc_group_workspace_bytes(group: Group, frames_per_cam: int) -> int:
+    b = _sz()
+    _check(lib().nsc_group_workspace_bytes(group.handle, frames_per_cam, ctypes.byref(b)),
+           "nsc_group_workspace_bytes")
+    return b.value
+
+
+def nsc_group_run(group: Group, frames, n, t0, state, ws, label_out, defer_out, score=None,
+                  fire=None, logit=None, want_stats=False, stage_events=None, stream=None):
+    """n frames of every camera (camera-major in frames and in every output)."""
+    outs = None
+    if score is not None or fire is not None or logit is not None:
+        outs = FrameOutputs(_ptr(score), _ptr(fire), _ptr(logit))
+    st = RunStats() if want_stats else None
+    ev = None
+    if stage_events is not None:
+        if len(stage_events) != NSC_STAGE_EVENTS:
+            raise ValueError(f"stage_events needs {NSC_STAGE_EVENTS} entries")
+        ev = (_vp * NSC_STAGE_EVENTS)(*[e if e else None for e in stage_events])
+    _check(lib().nsc_group_run(group.handle, _ptr(frames), n, t0, _ptr(state), _ptr(ws),
+                               ws.numel() * ws.element_size(), _ptr(label_out), _ptr(defer_out),
+                               ctypes.byref(outs) if outs else None,
+                               ctypes.byref(st) if st else None, ev, _stream(stream)),
+           "nsc_group_run")
+    if st is not None:
+        return dict(frames=st.frames, fired=st.fired, positive=st.positive, deferred=st.deferred)
+    return None
 
 
 def nsc_threshold_sweep(cfg: SweepCfg, score, conf, truth, deltas, rows, best, stream=None):

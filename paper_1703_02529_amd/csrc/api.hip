@@ -754,3 +754,303 @@ int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------------ camera groups
+
+struct nsc_group {
+  int32_t n_cams;
+  nsc_cascade_cfg geo;   // camera 0's cfg: the shared geometry and metric
+  const nsc_cnn* base;   // camera 0's network: kernel plans and base weights
+  int32_t max_delta;     // largest delta of an earlier-frame camera (0: none)
+  int64_t slot;          // state bytes per camera
+  void* dev;             // CamDiff[n_cams], then CamNet[n_cams]
+  CamDiff* cams;
+  CamNet* nets;
+};
+
+namespace nsc {
+namespace {
+
+// Workspace of a group run of n frames per camera.
+struct GroupLayout {
+  size_t sums, fire, dec, idx, count, tiles, logit, scratch, cnn, total;
+};
+
+GroupLayout group_layout(const nsc_group* g, int64_t n) {
+  GroupLayout L{};
+  const int64_t N = (int64_t)g->n_cams * n;
+  const size_t cells = (size_t)g->geo.dd_h * g->geo.dd_w * 3;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + bytes, kAlign);
+    return at;
+  };
+  L.sums = take(cells * 4 * (size_t)N);
+  L.fire = take((size_t)N);
+  L.dec = take((size_t)N);
+  L.idx = take((size_t)N * 4);
+  L.count = take(64);
+  L.tiles = take((size_t)compact_tiles(N) * 4 + 4);
+  L.logit = take((size_t)N * 4);
+  L.scratch = take(g->max_delta > 0 ? (size_t)g->n_cams * (size_t)g->slot : 0);
+  L.cnn = take(cnn_workspace_bytes(g->base->c, N));
+  L.total = o;
+  return L;
+}
+
+bool same_desc(const nsc_cnn_desc& a, const nsc_cnn_desc& b) {
+  if (a.n_conv != b.n_conv || a.pool_after_mask != b.pool_after_mask || a.dense != b.dense ||
+      a.in_h != b.in_h || a.in_w != b.in_w || a.dtype != b.dtype)
+    return false;
+  for (int l = 0; l < a.n_conv; ++l)
+    if (a.conv_out[l] != b.conv_out[l]) return false;
+  return true;
+}
+
+}  // namespace
+}  // namespace nsc
+
+extern "C" {
+
+int nsc_group_create(const nsc_cascade_cfg* cfgs, const nsc_cnn* const* cnns, int32_t n_cams,
+                     nsc_group** out) {
+  g_err[0] = 0;
+  NSC_REQUIRE(out != nullptr && cfgs != nullptr && cnns != nullptr, NSC_E_INVAL,
+              "cfgs, cnns or out is NULL");
+  *out = nullptr;
+  NSC_REQUIRE(n_cams >= 1 && n_cams <= NSC_MAX_CAMERAS, NSC_E_INVAL, "n_cams %d outside 1..%d",
+              n_cams, NSC_MAX_CAMERAS);
+  const nsc_cascade_cfg& g0 = cfgs[0];
+  int32_t max_delta = 0;
+  size_t slot = kAlign;
+  for (int32_t c = 0; c < n_cams; ++c) {
+    const nsc_cascade_cfg& k = cfgs[c];
+    if (int rc = check_cfg(&k)) {
+      char msg[512];
+      snprintf(msg, sizeof msg, "%s", g_err);
+      return fail(rc, "camera %d: %s", c, msg);
+    }
+    NSC_REQUIRE(k.in_h == g0.in_h && k.in_w == g0.in_w && k.frame_stride == g0.frame_stride &&
+                    k.dd_h == g0.dd_h && k.dd_w == g0.dd_w && k.cnn_h == g0.cnn_h &&
+                    k.cnn_w == g0.cnn_w,
+                NSC_E_INVAL, "camera %d: frame, detector or CNN grid differs from camera 0's", c);
+    NSC_REQUIRE(k.metric == g0.metric, NSC_E_INVAL,
+                "camera %d: metric %d differs from camera 0's %d", c, k.metric, g0.metric);
+    NSC_REQUIRE(k.check_stride <= 1, NSC_E_INVAL,
+                "camera %d: frame skipping (check_stride %d) is not available in a group", c,
+                k.check_stride);
+    if (k.ref_mode == NSC_REF_PREV && k.delta > max_delta) max_delta = k.delta;
+    const size_t sb = state_layout_bytes(&k, nullptr, nullptr);
+    if (sb > slot) slot = sb;
+  }
+  slot = align_up(slot, kAlign);
+  for (int32_t c = 0; c < n_cams; ++c) {
+    NSC_REQUIRE(cnns[c] != nullptr, NSC_E_INVAL, "camera %d: network handle is NULL", c);
+    NSC_REQUIRE(same_desc(cnns[c]->c.desc, cnns[0]->c.desc), NSC_E_SHAPE,
+                "camera %d: network description differs from camera 0's", c);
+  }
+  NSC_REQUIRE(cnns[0]->c.desc.in_h == g0.cnn_h && cnns[0]->c.desc.in_w == g0.cnn_w, NSC_E_SHAPE,
+              "CNN input %dx%d differs from the configured %dx%d", cnns[0]->c.desc.in_h,
+              cnns[0]->c.desc.in_w, g0.cnn_h, g0.cnn_w);
+  std::vector<CamDiff> hd((size_t)n_cams);
+  std::vector<CamNet> hn((size_t)n_cams);
+  for (int32_t c = 0; c < n_cams; ++c) {
+    const nsc_cascade_cfg& k = cfgs[c];
+    CamDiff d{};
+    d.ref_sums = k.ref_sums;
+    d.lr_w = k.lr_w;
+    d.lr_b = k.lr_b;
+    d.delta_diff = k.delta_diff;
+    d.ref_mode = k.ref_mode;
+    d.delta = k.ref_mode == NSC_REF_PREV ? k.delta : 0;
+    d.grid_h = k.grid_h;
+    d.grid_w = k.grid_w;
+    size_t dec_off = 0;
+    state_layout_bytes(&k, nullptr, &dec_off);
+    d.dec_off = (int64_t)dec_off;
+    hd[c] = d;
+    CamNet t{};
+    t.woff = static_cast<const unsigned char*>(cnns[c]->c.dev) -
+             static_cast<const unsigned char*>(cnns[0]->c.dev);
+    t.c_low = k.c_low;
+    t.c_high = k.c_high;
+    t.b2 = cnns[c]->c.b2;
+    hn[c] = t;
+  }
+  const size_t diff_bytes = align_up(sizeof(CamDiff) * (size_t)n_cams, kAlign);
+  const size_t total = diff_bytes + sizeof(CamNet) * (size_t)n_cams;
+  void* dev = nullptr;
+  if (hipMalloc(&dev, total) != hipSuccess)
+    return fail(NSC_E_NOMEM, "hipMalloc of %zu bytes for the group tables failed", total);
+  unsigned char* b = static_cast<unsigned char*>(dev);
+  if (hipMemcpy(b, hd.data(), sizeof(CamDiff) * (size_t)n_cams, hipMemcpyHostToDevice) !=
+          hipSuccess ||
+      hipMemcpy(b + diff_bytes, hn.data(), sizeof(CamNet) * (size_t)n_cams,
+                hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipFree(dev);
+    return fail(NSC_E_HIP, "copying the group tables to the device failed");
+  }
+  nsc_group* g = new (std::nothrow) nsc_group{};
+  if (!g) {
+    (void)hipFree(dev);
+    return fail(NSC_E_NOMEM, "host allocation of the group failed");
+  }
+  g->n_cams = n_cams;
+  g->geo = g0;
+  g->base = cnns[0];
+  g->max_delta = max_delta;
+  g->slot = (int64_t)slot;
+  g->dev = dev;
+  g->cams = reinterpret_cast<CamDiff*>(b);
+  g->nets = reinterpret_cast<CamNet*>(b + diff_bytes);
+  *out = g;
+  return NSC_OK;
+}
+
+int nsc_group_destroy(nsc_group* g) {
+  g_err[0] = 0;
+  if (!g) return NSC_OK;
+  const hipError_t e = hipFree(g->dev);
+  delete g;
+  if (e != hipSuccess) return fail(NSC_E_HIP, "hipFree failed: %s", hipGetErrorString(e));
+  return NSC_OK;
+}
+
+int nsc_group_state_bytes(const nsc_group* g, size_t* bytes, size_t* slot_bytes) {
+  g_err[0] = 0;
+  NSC_REQUIRE(g != nullptr && bytes != nullptr, NSC_E_INVAL, "group or bytes is NULL");
+  *bytes = (size_t)g->n_cams * (size_t)g->slot;
+  if (slot_bytes) *slot_bytes = (size_t)g->slot;
+  return NSC_OK;
+}
+
+int nsc_group_workspace_bytes(const nsc_group* g, int64_t frames_per_cam, size_t* bytes) {
+  g_err[0] = 0;
+  NSC_REQUIRE(g != nullptr && bytes != nullptr, NSC_E_INVAL, "group or bytes is NULL");
+  NSC_REQUIRE(frames_per_cam >= 0 && frames_per_cam <= kMaxFrames / g->n_cams, NSC_E_INVAL,
+              "frames_per_cam %lld out of range for %d cameras", (long long)frames_per_cam,
+              g->n_cams);
+  *bytes = group_layout(g, frames_per_cam).total;
+  return NSC_OK;
+}
+
+int nsc_group_run(const nsc_group* g, const uint8_t* frames, int64_t n, int64_t t0, void* state,
+                  void* ws, size_t ws_bytes, uint8_t* label_out, uint8_t* defer_out,
+                  const nsc_frame_outputs* outs, nsc_run_stats* stats, void* const* stage_events,
+                  void* stream) {
+  g_err[0] = 0;
+  NSC_REQUIRE(g != nullptr, NSC_E_INVAL, "group is NULL");
+  NSC_REQUIRE(n >= 0 && n <= kMaxFrames / g->n_cams && t0 >= 0, NSC_E_INVAL,
+              "n or t0 out of range");
+  auto mark = [&](int k) -> int {
+    if (stage_events && stage_events[k])
+      NSC_TRY_HIP(hipEventRecord((hipEvent_t)stage_events[k], (hipStream_t)stream));
+    return NSC_OK;
+  };
+  const int64_t N = (int64_t)g->n_cams * n;
+  if (n == 0) {
+    if (stats) *stats = nsc_run_stats{0, 0, 0, 0};
+    return NSC_OK;
+  }
+  NSC_REQUIRE(frames && label_out && defer_out, NSC_E_INVAL,
+              "frames, label_out or defer_out is NULL");
+  NSC_REQUIRE(!(g->max_delta > 0 && state == nullptr), NSC_E_STATE,
+              "a camera compares with earlier frames: the group needs a state buffer");
+  const GroupLayout L = group_layout(g, n);
+  NSC_REQUIRE(ws != nullptr && ((uintptr_t)ws % kAlign) == 0 && ws_bytes >= L.total,
+              NSC_E_WORKSPACE, "workspace needs %zu bytes (256-byte aligned), got %zu", L.total,
+              ws_bytes);
+  const nsc_cascade_cfg* cfg = &g->geo;
+  const Cnn& c = g->base->c;
+  const hipStream_t st = (hipStream_t)stream;
+  unsigned char* w = static_cast<unsigned char*>(ws);
+  int32_t* sums = reinterpret_cast<int32_t*>(w + L.sums);
+  uint8_t* fire = outs && outs->fire ? outs->fire : w + L.fire;
+  uint8_t* dec = w + L.dec;
+  int32_t* idx = reinterpret_cast<int32_t*>(w + L.idx);
+  int32_t* count = reinterpret_cast<int32_t*>(w + L.count);
+  unsigned char* st_bytes = static_cast<unsigned char*>(state);
+  const int64_t cells = (int64_t)cfg->dd_h * cfg->dd_w * 3;
+  const double den = (double)nsc_area_den(cfg->in_h, cfg->in_w, cfg->dd_h, cfg->dd_w);
+
+  // 1: area sums of every camera's frames (one video of n_cams * n frames)
+  if (int rc = mark(0)) return rc;
+  AreaPlan ap;
+  if (int rc = make_area_plan(cfg->in_h, cfg->in_w, cfg->frame_stride, frames, cfg->dd_h,
+                              cfg->dd_w, N, &ap))
+    return rc;
+  if (int rc = launch_area_sums(ap, frames, cfg->frame_stride, N, sums, st)) return rc;
+  if (int rc = mark(1)) return rc;
+  // 2: detector, each frame with its camera's settings
+  {
+    DiffArgs a{};
+    a.sums = sums;
+    a.den = den;
+    a.den2 = den * den;
+    a.metric = cfg->metric;
+    a.n = N;
+    a.t0 = t0;
+    a.dd_h = cfg->dd_h;
+    a.dd_w = cfg->dd_w;
+    a.score = outs ? outs->score : nullptr;
+    a.fire = fire;
+    a.cams = g->cams;
+    a.per_cam = n;
+    a.state = st_bytes;
+    a.state_stride = g->slot;
+    if (int rc = launch_diff(a, st)) return rc;
+  }
+  if (int rc = mark(2)) return rc;
+  // 3: compaction over all cameras (survivors in camera-major frame order)
+  if (int rc = launch_compact(fire, N, idx, count, reinterpret_cast<int32_t*>(w + L.tiles), st))
+    return rc;
+  if (int rc = mark(3)) return rc;
+  // 4: CNN, every survivor with its camera's network and thresholds
+  if (outs && outs->logit)
+    if (int rc = launch_fill_nan(outs->logit, N, st)) return rc;
+  CnnRunArgs r{};
+  r.sums = sums;
+  r.sums_h = cfg->dd_h;
+  r.sums_w = cfg->dd_w;
+  r.fy = cfg->dd_h / cfg->cnn_h;
+  r.fx = cfg->dd_w / cfg->cnn_w;
+  r.den_c = den * r.fy * r.fx;
+  r.idx = idx;
+  r.count = count;
+  r.max_count = N;
+  r.logit = reinterpret_cast<float*>(w + L.logit);
+  r.prob = nullptr;
+  r.dec = dec;
+  r.frame_logit = outs ? outs->logit : nullptr;
+  r.nets = g->nets;
+  r.per_cam = n;
+  if (int rc = run_cnn(c, r, w + L.cnn, L.total - L.cnn, st)) return rc;
+  if (int rc = mark(4)) return rc;
+  // 5: decisions of the frames that did not fire, then the cameras' state
+  if (int rc = launch_group_resolve(g->cams, g->n_cams, fire, dec, n, t0, st_bytes, g->slot,
+                                    label_out, defer_out, st))
+    return rc;
+  if (g->max_delta > 0)
+    if (int rc = launch_group_state(g->cams, g->n_cams, g->max_delta, sums, label_out, defer_out,
+                                    n, cells, st_bytes, g->slot, w + L.scratch, st))
+      return rc;
+  if (int rc = mark(5)) return rc;
+  if (stats) {
+    std::vector<uint8_t> hl(N), hdf(N);
+    int32_t hc = 0;
+    NSC_TRY_HIP(hipMemcpyAsync(hl.data(), label_out, N, hipMemcpyDeviceToHost, st));
+    NSC_TRY_HIP(hipMemcpyAsync(hdf.data(), defer_out, N, hipMemcpyDeviceToHost, st));
+    NSC_TRY_HIP(hipMemcpyAsync(&hc, count, 4, hipMemcpyDeviceToHost, st));
+    NSC_TRY_HIP(hipStreamSynchronize(st));
+    nsc_run_stats rs{N, hc, 0, 0};
+    for (int64_t i = 0; i < N; ++i) {
+      rs.positive += hl[i] && !hdf[i];
+      rs.deferred += hdf[i];
+    }
+    *stats = rs;
+  }
+  return NSC_OK;
+}
+
+}  // extern "C"

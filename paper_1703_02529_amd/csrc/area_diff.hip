@@ -340,11 +340,61 @@ struct DiffSums {
   }
 };
 
+// The detector score of one frame (area sums `cur`) against its reference
+// `ref`, by one wave: the metric over the whole grid, or the logistic score of
+// the per-block metrics (blocks in row-major order, weights lr_w).
 template <int M>
-__global__ void __launch_bounds__(256) k_diff(DiffArgs a) {
+__device__ __forceinline__ double frame_score(const int32_t* cur, const int32_t* ref,
+                                              const DiffArgs& a, int32_t grid_h, int32_t grid_w,
+                                              const float* lr_w, double lr_b, int lane) {
   // the blocked score is summed with separate multiplies and adds, in block
   // order, so it is reproducible bit for bit
 #pragma clang fp contract(off)
+  const int64_t cells = (int64_t)a.dd_h * a.dd_w * 3;
+  if (grid_h * grid_w == 1) {
+    DiffSums<M> acc;
+    if ((cells & 3) == 0 && (((uintptr_t)cur | (uintptr_t)ref) & 15) == 0) {
+      const int4* c4 = reinterpret_cast<const int4*>(cur);
+      const int4* r4 = reinterpret_cast<const int4*>(ref);
+      for (int64_t k = lane; k < cells / 4; k += 64) {
+        const int4 x = c4[k], y = r4[k];
+        acc.add(x.x, y.x);
+        acc.add(x.y, y.y);
+        acc.add(x.z, y.z);
+        acc.add(x.w, y.w);
+      }
+    } else {
+      for (int64_t k = lane; k < cells; k += 64) acc.add(cur[k], ref[k]);
+    }
+    acc.reduce();
+    return acc.value(a, (double)cells);
+  }
+  double z = lr_b;
+  for (int by = 0; by < grid_h; ++by) {
+    const int y0 = (int)((int64_t)by * a.dd_h / grid_h);
+    const int y1 = (int)((int64_t)(by + 1) * a.dd_h / grid_h);
+    for (int bx = 0; bx < grid_w; ++bx) {
+      const int x0 = (int)((int64_t)bx * a.dd_w / grid_w);
+      const int x1 = (int)((int64_t)(bx + 1) * a.dd_w / grid_w);
+      const int rl = (x1 - x0) * 3;
+      const int total = (y1 - y0) * rl;
+      DiffSums<M> acc;
+      for (int k = lane; k < total; k += 64) {
+        const int r = k / rl, cc = k - r * rl;
+        const int64_t off = ((int64_t)(y0 + r) * a.dd_w + x0) * 3 + cc;
+        acc.add(cur[off], ref[off]);
+      }
+      acc.reduce();
+      const double ncell = ((double)(y1 - y0) * (double)(x1 - x0)) * 3.0;
+      const double m = acc.value(a, ncell);
+      z = z + (double)lr_w[by * grid_w + bx] * m;
+    }
+  }
+  return z;
+}
+
+template <int M>
+__global__ void __launch_bounds__(256) k_diff(DiffArgs a) {
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (i >= a.n) return;
@@ -361,50 +411,43 @@ __global__ void __launch_bounds__(256) k_diff(DiffArgs a) {
       ref = a.sums + (i - a.delta) * cells;
     else
       ref = a.prev_sums + i * cells;  // frame t - delta = t0 - delta + i
-    if (a.grid_h * a.grid_w == 1) {
-      DiffSums<M> acc;
-      if ((cells & 3) == 0 && (((uintptr_t)cur | (uintptr_t)ref) & 15) == 0) {
-        const int4* c4 = reinterpret_cast<const int4*>(cur);
-        const int4* r4 = reinterpret_cast<const int4*>(ref);
-        for (int64_t k = lane; k < cells / 4; k += 64) {
-          const int4 x = c4[k], y = r4[k];
-          acc.add(x.x, y.x);
-          acc.add(x.y, y.y);
-          acc.add(x.z, y.z);
-          acc.add(x.w, y.w);
-        }
-      } else {
-        for (int64_t k = lane; k < cells; k += 64) acc.add(cur[k], ref[k]);
-      }
-      acc.reduce();
-      score = acc.value(a, (double)cells);
-    } else {
-      double z = a.lr_b;
-      for (int by = 0; by < a.grid_h; ++by) {
-        const int y0 = (int)((int64_t)by * a.dd_h / a.grid_h);
-        const int y1 = (int)((int64_t)(by + 1) * a.dd_h / a.grid_h);
-        for (int bx = 0; bx < a.grid_w; ++bx) {
-          const int x0 = (int)((int64_t)bx * a.dd_w / a.grid_w);
-          const int x1 = (int)((int64_t)(bx + 1) * a.dd_w / a.grid_w);
-          const int rl = (x1 - x0) * 3;
-          const int total = (y1 - y0) * rl;
-          DiffSums<M> acc;
-          for (int k = lane; k < total; k += 64) {
-            const int r = k / rl, cc = k - r * rl;
-            const int64_t off = ((int64_t)(y0 + r) * a.dd_w + x0) * 3 + cc;
-            acc.add(cur[off], ref[off]);
-          }
-          acc.reduce();
-          const double ncell = ((double)(y1 - y0) * (double)(x1 - x0)) * 3.0;
-          const double m = acc.value(a, ncell);
-          z = z + (double)a.lr_w[by * a.grid_w + bx] * m;
-        }
-      }
-      score = z;
-    }
+    score = frame_score<M>(cur, ref, a, a.grid_h, a.grid_w, a.lr_w, a.lr_b, lane);
   }
   if (lane == 0) {
     a.fire[i] = (forced || score > a.delta_diff) ? 1 : 0;
+    if (a.score) a.score[i] = score;
+  }
+}
+
+// A camera group's frames: camera c's n = per_cam frames [t0, t0 + n) are
+// frames c * n .. c * n + n - 1 of the batch, each scored with its camera's
+// reference, blocks, weights and threshold; the frames before t0 come from
+// the camera's state slot.
+template <int M>
+__global__ void __launch_bounds__(256) k_diff_group(DiffArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= a.n) return;
+  const int64_t cam = i / a.per_cam;
+  const int64_t j = i - cam * a.per_cam;
+  const CamDiff cd = a.cams[cam];
+  const int64_t t = a.t0 + j;
+  const int64_t cells = (int64_t)a.dd_h * a.dd_w * 3;
+  const bool forced = cd.ref_mode == NSC_REF_PREV && t < cd.delta;
+  double score = INFINITY;
+  if (!forced) {
+    const int32_t* cur = a.sums + i * cells;
+    const int32_t* ref;
+    if (cd.ref_mode == NSC_REF_FIXED)
+      ref = cd.ref_sums;
+    else if (j >= cd.delta)
+      ref = a.sums + (i - cd.delta) * cells;
+    else  // frame t0 - delta + j, kept in the camera's state
+      ref = reinterpret_cast<const int32_t*>(a.state + cam * a.state_stride) + j * cells;
+    score = frame_score<M>(cur, ref, a, cd.grid_h, cd.grid_w, cd.lr_w, cd.lr_b, lane);
+  }
+  if (lane == 0) {
+    a.fire[i] = (forced || score > cd.delta_diff) ? 1 : 0;
     if (a.score) a.score[i] = score;
   }
 }
@@ -514,24 +557,29 @@ int launch_area_sums(const AreaPlan& p, const uint8_t* frames, int64_t stride, i
 int launch_diff(const DiffArgs& a, hipStream_t stream) {
   if (a.n <= 0) return NSC_OK;
   const int64_t blocks = (a.n + 3) / 4;
+  if (blocks > 0x7FFFFFFF) return fail(NSC_E_SHAPE, "too many frames in one call");
+#define NSC_DIFF_LAUNCH(M)                                                                    \
+  if (a.cams)                                                                                 \
+    hipLaunchKernelGGL(k_diff_group<M>, dim3((unsigned)blocks), dim3(256), 0, stream, a);     \
+  else                                                                                        \
+    hipLaunchKernelGGL(k_diff<M>, dim3((unsigned)blocks), dim3(256), 0, stream, a)
   switch (a.metric) {
     case NSC_METRIC_MSE:
-      hipLaunchKernelGGL(k_diff<NSC_METRIC_MSE>, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+      NSC_DIFF_LAUNCH(NSC_METRIC_MSE);
       break;
     case NSC_METRIC_SAD:
-      hipLaunchKernelGGL(k_diff<NSC_METRIC_SAD>, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+      NSC_DIFF_LAUNCH(NSC_METRIC_SAD);
       break;
     case NSC_METRIC_NRMSE:
-      hipLaunchKernelGGL(k_diff<NSC_METRIC_NRMSE>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                         a);
+      NSC_DIFF_LAUNCH(NSC_METRIC_NRMSE);
       break;
     case NSC_METRIC_PSNR:
-      hipLaunchKernelGGL(k_diff<NSC_METRIC_PSNR>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                         a);
+      NSC_DIFF_LAUNCH(NSC_METRIC_PSNR);
       break;
     default:
       return fail(NSC_E_INVAL, "metric %d is unknown", a.metric);
   }
+#undef NSC_DIFF_LAUNCH
   NSC_CHECK_LAUNCH("k_diff");
   return NSC_OK;
 }

@@ -177,7 +177,24 @@ struct ConvArgs {
   int32_t w_lds;            // row stride of staged weights (elements)
   int32_t band_w;           // staged columns of a segment (halo and tail zero-filled)
   int32_t lo_plane;         // elements from a staged hi value to its lo value (split layers)
+  const CamNet* nets;       // camera group: per-camera weight offsets (else null)
+  int64_t per_cam;          // frames per camera of a group
 };
+
+// Byte offset of survivor slot s's network from the base network's weights
+// in a camera group; s is uniform across the wave, and so is the result
+// (moved to scalar registers).
+__device__ __forceinline__ int64_t slot_woff(const CamNet* nets, int64_t per_cam,
+                                             const int32_t* idx, int64_t s) {
+  const uint64_t off = (uint64_t)nets[idx[s] / per_cam].woff;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)off);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(off >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+template <typename P>
+__device__ __forceinline__ const P* at_off(const P* p, int64_t off) {
+  return reinterpret_cast<const P*>(reinterpret_cast<const unsigned char*>(p) + off);
+}
 
 // Pixel (py, px) of M row m inside a 4x4 tile: m = 4 * window + j, the four
 // windows being the 2x2 pooling windows of the tile.
@@ -188,8 +205,8 @@ __device__ __forceinline__ void tile_pixel(int m, int& py, int& px) {
 }
 
 template <typename T>
-__device__ __forceinline__ void stage_weights(const ConvArgs& a, T* wl) {
-  const T* src = reinterpret_cast<const T*>(a.wts);
+__device__ __forceinline__ void stage_weights(const ConvArgs& a, T* wl, int64_t off = 0) {
+  const T* src = at_off(reinterpret_cast<const T*>(a.wts), off);
   for (int e = threadIdx.x; e < a.cout * a.kpad; e += blockDim.x) {
     const int o = e / a.kpad, k = e - o * a.kpad;
     wl[o * a.w_lds + k] = src[e];
@@ -332,7 +349,7 @@ __device__ __forceinline__ void first_tile_b(const uint16_t* in, const bf16x8 (&
   }
 }
 
-template <typename T, int NT>
+template <typename T, int NT, bool G>
 __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   T* wl = reinterpret_cast<T*>(lds_raw);
@@ -340,7 +357,10 @@ __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nwaves = blockDim.x >> 6;
-  stage_weights(a, wl);
+  // a camera group stages each item's network (when it changes) in the loop
+  if constexpr (!G) stage_weights(a, wl);
+  int64_t staged = 0;
+  bool have = !G;
   int64_t cnt = *a.count;
   if (cnt > a.max_count) cnt = a.max_count;
   const int bands = (a.tiles_y + a.band_tiles - 1) / a.band_tiles;
@@ -351,7 +371,7 @@ __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
   int py, px;
   tile_pixel(m, py, px);
   float bias[NT];
-  load_bias(a.bias, m, bias);
+  if constexpr (!G) load_bias(a.bias, m, bias);
 
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
     const int64_t s = item / (bands * segs);
@@ -361,6 +381,15 @@ __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
     const int nty = min(a.band_tiles, a.tiles_y - ty0);
     const int ntx = min(a.seg_tiles, a.tiles_x - tx0);
     __syncthreads();  // previous item's readers are done with `in` (and weights staged)
+    if constexpr (G) {
+      const int64_t off = slot_woff(a.nets, a.per_cam, a.idx, s);
+      if (!have || off != staged) {  // uniform: the item's camera
+        stage_weights(a, wl, off);
+        load_bias(at_off(a.bias, off), m, bias);
+        staged = off;
+        have = true;
+      }
+    }
     stage_first(a, in, s, 4 * ty0 - 1, 4 * tx0 - 1, 4 * nty + 2, a.band_w, 0, (int)blockDim.x);
     __syncthreads();
     float* out = a.act_out + s * (int64_t)ho * wo * a.cout;
@@ -479,7 +508,7 @@ __device__ __forceinline__ void inner_tile32_b(const uint16_t* in, const bf16x8 
   }
 }
 
-template <typename T, int NT>
+template <typename T, int NT, bool G>
 __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   T* wl = reinterpret_cast<T*>(lds_raw);
@@ -487,7 +516,10 @@ __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nwaves = blockDim.x >> 6;
-  stage_weights(a, wl);
+  // a camera group stages each item's network (when it changes) in the loop
+  if constexpr (!G) stage_weights(a, wl);
+  int64_t staged = 0;
+  bool have = !G;
   int64_t cnt = *a.count;
   if (cnt > a.max_count) cnt = a.max_count;
   const int bands = (a.tiles_y + a.band_tiles - 1) / a.band_tiles;
@@ -498,7 +530,7 @@ __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
   int py, px;
   tile_pixel(m, py, px);
   float bias[NT];
-  load_bias(a.bias, m, bias);
+  if constexpr (!G) load_bias(a.bias, m, bias);
 
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
     const int64_t s = item / (bands * segs);
@@ -508,6 +540,15 @@ __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
     const int nty = min(a.band_tiles, a.tiles_y - ty0);
     const int ntx = min(a.seg_tiles, a.tiles_x - tx0);
     __syncthreads();  // previous item's readers are done with `in` (and weights staged)
+    if constexpr (G) {
+      const int64_t off = slot_woff(a.nets, a.per_cam, a.idx, s);
+      if (!have || off != staged) {  // uniform: the item's camera
+        stage_weights(a, wl, off);
+        load_bias(at_off(a.bias, off), m, bias);
+        staged = off;
+        have = true;
+      }
+    }
     stage_inner(a, in, s, 4 * ty0 - 1, 4 * tx0 - 1, 4 * nty + 2, a.band_w);
     __syncthreads();
     float* out = a.act_out + s * (int64_t)ho * wo * a.cout;
@@ -557,7 +598,7 @@ __device__ __forceinline__ void pair_epilogue(const ConvArgs& a1, const f32x4 (&
   }
 }
 
-template <int NT0, int NT1, bool B1REG>
+template <int NT0, int NT1, bool B1REG, bool G>
 __global__ void __launch_bounds__(1024) k_conv_pair(ConvArgs a0, ConvArgs a1, PairArgs pa) {
   using T = uint16_t;
   using X = Elt<T>;
@@ -570,8 +611,13 @@ __global__ void __launch_bounds__(1024) k_conv_pair(ConvArgs a0, ConvArgs a1, Pa
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nwaves = blockDim.x >> 6;
-  stage_weights(a0, w0);
-  stage_weights(a1, w1);
+  // a camera group stages each image's networks (when they change) in the loop
+  if constexpr (!G) {
+    stage_weights(a0, w0);
+    stage_weights(a1, w1);
+  }
+  int64_t staged = 0;
+  bool have = !G;
   for (int i = threadIdx.x; i < 2 * a1.lo_plane; i += blockDim.x) in1[i] = 0;
   int64_t cnt = *a0.count;
   if (cnt > a0.max_count) cnt = a0.max_count;
@@ -582,8 +628,10 @@ __global__ void __launch_bounds__(1024) k_conv_pair(ConvArgs a0, ConvArgs a1, Pa
   int py, px;
   tile_pixel(m, py, px);
   float bias0[NT0], bias1[NT1];
-  load_bias(a0.bias, m, bias0);
-  load_bias(a1.bias, m, bias1);
+  if constexpr (!G) {
+    load_bias(a0.bias, m, bias0);
+    load_bias(a1.bias, m, bias1);
+  }
   // the next image is staged by the waves that run one second-layer tile fewer
   const int tiles1 = a1.tiles_y * a1.tiles_x;
   const int extra = tiles1 % nwaves;
@@ -592,6 +640,18 @@ __global__ void __launch_bounds__(1024) k_conv_pair(ConvArgs a0, ConvArgs a1, Pa
   if (s < cnt) stage_first(a0, in0, s, -1, -1, rows0, a0.band_w, 0, (int)blockDim.x);
   for (; s < cnt; s += gridDim.x) {
     __syncthreads();  // in0 staged; the previous image's second layer is done with in1
+    if constexpr (G) {
+      const int64_t off = slot_woff(a0.nets, a0.per_cam, a0.idx, s);
+      if (!have || off != staged) {  // uniform: the image's camera
+        stage_weights(a0, w0, off);
+        stage_weights(a1, w1, off);
+        load_bias(at_off(a0.bias, off), m, bias0);
+        load_bias(at_off(a1.bias, off), m, bias1);
+        staged = off;
+        have = true;
+        __syncthreads();  // weights staged before the first layer reads them
+      }
+    }
     if constexpr (NT0 <= 2) {
       // each wave keeps the first layer's weight fragments in registers
       bf16x8 bw0[2][NT0];
@@ -905,7 +965,7 @@ __device__ __forceinline__ void band64_layer(const unsigned char* lds, const Ban
 }
 
 // One 64-input-channel layer over bands of fp32 activations.
-template <int NT>
+template <int NT, bool G>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_band64(ConvArgs a, Band64 b) {
   extern __shared__ __align__(16) unsigned char lds[];
@@ -928,10 +988,11 @@ k_band64(ConvArgs a, Band64 b) {
     if (s >= cnt) continue;  // workgroup-uniform
     const int ty0 = bi * a.band_tiles;
     const int nty = min(a.band_tiles, a.tiles_y - ty0);
+    const int64_t off = G ? slot_woff(a.nets, a.per_cam, a.idx, s) : 0;  // camera group
     __syncthreads();  // the previous band's readers are done (and the clear)
     stage_band64(a.act_in + s * (int64_t)a.h * a.w * 64, b, lds, 4 * ty0 - 1, 4 * nty + 2);
     __syncthreads();
-    band64_layer<NT>(lds, b, ty0, nty * a.tiles_x, wf, a.bias,
+    band64_layer<NT>(lds, b, ty0, nty * a.tiles_x, at_off(wf, off), at_off(a.bias, off),
                      a.act_out + s * (int64_t)ho * wo * a.cout, a.cout, a.pool, a.tiles_x, wave,
                      py, px, m, g, lane);
   }
@@ -988,7 +1049,7 @@ __global__ void __launch_bounds__(256) k_prep_input(ConvArgs a, uint2* xin, int3
 // A wave loads the input of its next first-layer tile while computing the
 // current one.
 
-template <int NT>
+template <int NT, bool G>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int32_t xr,
          int32_t xw) {
@@ -1045,6 +1106,7 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     x[1] = make_uint4(p10.x, p10.y, p11.x, p11.y);
   };
   // first-layer tile t: 8 MFMAs, bias, ReLU, hi / lo split into the planes
+  const float* bias0 = a0.bias;  // the item's network (camera group)
   auto l1_tile = [&](const bf16x8 (&w0)[2][4], int y0, int t, const uint4 (&x)[2]) {
     const int ti = t / tx0, tj = t - ti * tx0;
     const int r = 2 * ti + qy, col = 8 * tj + qx;
@@ -1062,7 +1124,7 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
       const int addr = ((g >> 1) * b.cp + r * b.wb + col + 1) * 16 + (g & 1) * 8;
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) {
-        const float4 bb = *reinterpret_cast<const float4*>(a0.bias + nt * 16 + 4 * g);
+        const float4 bb = *reinterpret_cast<const float4*>(bias0 + nt * 16 + 4 * g);
         const float v0 = inside ? fmaxf(acc[nt][0] + bb.x, 0.f) : 0.f;
         const float v1 = inside ? fmaxf(acc[nt][1] + bb.y, 0.f) : 0.f;
         const float v2 = inside ? fmaxf(acc[nt][2] + bb.z, 0.f) : 0.f;
@@ -1084,6 +1146,8 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     const int y0 = 4 * ty0 - 1;
     const int t0n = (2 * nty + 1) * tx0;  // first-layer tiles: rows 4 nty + 2
     const uint2* xs = xin + s * (int64_t)xr * xw;
+    const int64_t off = G ? slot_woff(a0.nets, a0.per_cam, a0.idx, s) : 0;  // camera group
+    bias0 = at_off(a0.bias, off);
     uint4 xc[2], xn[2];
     if (wave < t0n) l1_load(xs, y0, wave, xc);
     // first-layer weights for this band's first-layer phase only: an opaque
@@ -1091,7 +1155,7 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     // would hold 32 registers through the second layer)
     int opaque = 0;
     asm volatile("" : "+s"(opaque));
-    const bf16x8* w0p = wf0 + opaque + lane;
+    const bf16x8* w0p = at_off(wf0, off) + opaque + lane;
     bf16x8 w0[2][4];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
@@ -1105,7 +1169,7 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
       xc[1] = xn[1];
     }
     __syncthreads();  // planes complete
-    band64_layer<NT>(lds, b, ty0, nty * a1.tiles_x, wf1, a1.bias,
+    band64_layer<NT>(lds, b, ty0, nty * a1.tiles_x, at_off(wf1, off), at_off(a1.bias, off),
                      a1.act_out + s * (int64_t)ho * wo * a1.cout, a1.cout, a1.pool, a1.tiles_x,
                      wave, py, px, m, g, lane);
     item = next_item(item + gridDim.x, &s, &ty0, &nty);
@@ -1129,6 +1193,8 @@ struct DenseArgs {
   uint8_t* dec;
   float* frame_logit;
   double c_low, c_high;
+  const CamNet* nets;       // camera group (else null)
+  int64_t per_cam;
 };
 
 // Waves of a dense workgroup: they split K, so that a group of 16 survivors
@@ -1138,7 +1204,7 @@ constexpr int dense_waves() {
   return NT >= 16 ? 4 : 8;
 }
 
-template <typename T, int NT>
+template <typename T, int NT, bool G>
 __global__ void __launch_bounds__(512) k_dense(DenseArgs a) {
   using X = Elt<T>;
   constexpr int E = X::E, KS = X::KS;
@@ -1154,83 +1220,112 @@ __global__ void __launch_bounds__(512) k_dense(DenseArgs a) {
   const int64_t groups = (cnt + 15) / 16;
   const int nks = (a.flat + KS - 1) / KS;  // K steps
   const int ks0 = wave * nks / NW, ks1 = (wave + 1) * nks / NW;
-  const T* w1 = reinterpret_cast<const T*>(a.w1);
+  // camera of survivor slot u of a camera group (slots are in frame order, so
+  // a group's cameras are non-decreasing)
+  auto cam_of = [&](int64_t u) -> int64_t { return a.idx[u] / a.per_cam; };
   for (int64_t grp = blockIdx.x; grp < groups; grp += gridDim.x) {
-    const int64_t s = grp * 16 + m;
-    const bool valid = s < cnt;
-    const float* arow = a.feat + (valid ? s : 0) * (int64_t)a.flat + g * E;
-    f32x4 acc[NT], acc_lo[NT];
+    // A group of 16 slots runs once per camera among its rows (once without a
+    // camera group), each pass with that camera's weights over its own rows.
+    int64_t cam = G ? cam_of(grp * 16) : 0;
+    for (;;) {
+      int64_t off = 0;
+      float b2 = a.b2;
+      double c_low = a.c_low, c_high = a.c_high;
+      if constexpr (G) {
+        const CamNet& cn = a.nets[cam];
+        off = cn.woff;
+        b2 = cn.b2;
+        c_low = cn.c_low;
+        c_high = cn.c_high;
+      }
+      const T* w1 = at_off(reinterpret_cast<const T*>(a.w1), off);
+      const float* b1 = at_off(a.b1, off);
+      const float* w2 = at_off(a.w2, off);
+      const int64_t s = grp * 16 + m;
+      const bool valid = s < cnt && (!G || cam_of(s) == cam);
+      const float* arow = a.feat + (valid ? s : 0) * (int64_t)a.flat + g * E;
+      f32x4 acc[NT], acc_lo[NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      acc_lo[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-    // flat is a multiple of 16 (and of E): a lane group's E values of the last,
-    // partial K step are either all inside or all past the end (zero)
-    for (int ks = ks0; ks < ks1; ++ks) {
-      const int k0 = ks * KS;
-      const bool kin = k0 + g * E < a.flat;
-      typename X::frag av = X::zero(), av_lo = X::zero();
-      if constexpr (SPLIT) {
-        if (valid && kin) X::split8(arow + k0, av, av_lo);
-      } else {
-        if (valid && kin) av = arow[k0];
+      for (int nt = 0; nt < NT; ++nt) {
+        acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        acc_lo[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+      // flat is a multiple of 16 (and of E): a lane group's E values of the last,
+      // partial K step are either all inside or all past the end (zero)
+      for (int ks = ks0; ks < ks1; ++ks) {
+        const int k0 = ks * KS;
+        const bool kin = k0 + g * E < a.flat;
+        typename X::frag av = X::zero(), av_lo = X::zero();
+        if constexpr (SPLIT) {
+          if (valid && kin) X::split8(arow + k0, av, av_lo);
+        } else {
+          if (valid && kin) av = arow[k0];
+        }
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          typename X::frag bv = X::zero();
+          if (kin) bv = X::load(w1 + (int64_t)(nt * 16 + m) * a.flat + k0 + g * E);
+          acc[nt] = X::mma(av, bv, acc[nt]);
+          if constexpr (SPLIT) acc_lo[nt] = X::mma(av_lo, bv, acc_lo[nt]);
+        }
       }
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        typename X::frag bv = X::zero();
-        if (kin) bv = X::load(w1 + (int64_t)(nt * 16 + m) * a.flat + k0 + g * E);
-        acc[nt] = X::mma(av, bv, acc[nt]);
-        if constexpr (SPLIT) acc_lo[nt] = X::mma(av_lo, bv, acc_lo[nt]);
+        if constexpr (SPLIT) acc[nt] += acc_lo[nt];
+        part[wave][nt][lane] = acc[nt];
       }
-    }
+      __syncthreads();
+      if (wave == 0) {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      if constexpr (SPLIT) acc[nt] += acc_lo[nt];
-      part[wave][nt][lane] = acc[nt];
-    }
-    __syncthreads();
-    if (wave == 0) {
+        for (int nt = 0; nt < NT; ++nt) {
+          f32x4 t = part[0][nt][lane];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        f32x4 t = part[0][nt][lane];
+          for (int w = 1; w < NW; ++w) t += part[w][nt][lane];
+          acc[nt] = t;
+        }
+        // hidden = ReLU(acc + b1); z = b2 + sum_n w2[n] * hidden[n]
+        float sum[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int w = 1; w < NW; ++w) t += part[w][nt][lane];
-        acc[nt] = t;
-      }
-      // hidden = ReLU(acc + b1); z = b2 + sum_n w2[n] * hidden[n]
-      float sum[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int nt = 0; nt < NT; ++nt) {
+          const int n = nt * 16 + m;
+          const float b = b1[n], w = w2[n];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int n = nt * 16 + m;
-        const float b = a.b1[n], w = a.w2[n];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sum[r] += w * fmaxf(acc[nt][r] + b, 0.0f);
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) sum[r] += __shfl_xor(sum[r], o, 64);
-      }
-      if (m == 0) {
+          for (int r = 0; r < 4; ++r) sum[r] += w * fmaxf(acc[nt][r] + b, 0.0f);
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int64_t slot = grp * 16 + 4 * g + r;
-          if (slot < cnt) {
-            const float z = sum[r] + a.b2;
-            const double p = 1.0 / (1.0 + exp(-(double)z));
-            a.logit[slot] = z;
-            if (a.prob) a.prob[slot] = (float)p;
-            if (a.dec || a.frame_logit) {
-              const int32_t f = a.idx[slot];
-              if (a.dec) a.dec[f] = p < a.c_low ? 0 : (p > a.c_high ? 1 : 2);
-              if (a.frame_logit) a.frame_logit[f] = z;
+#pragma unroll
+          for (int o = 1; o < 16; o <<= 1) sum[r] += __shfl_xor(sum[r], o, 64);
+        }
+        if (m == 0) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int64_t slot = grp * 16 + 4 * g + r;
+            if (slot < cnt && (!G || cam_of(slot) == cam)) {
+              const float z = sum[r] + b2;
+              const double p = 1.0 / (1.0 + exp(-(double)z));
+              a.logit[slot] = z;
+              if (a.prob) a.prob[slot] = (float)p;
+              if (a.dec || a.frame_logit) {
+                const int32_t f = a.idx[slot];
+                if (a.dec) a.dec[f] = p < c_low ? 0 : (p > c_high ? 1 : 2);
+                if (a.frame_logit) a.frame_logit[f] = z;
+              }
             }
           }
         }
       }
+      __syncthreads();  // the partial sums are read before the next pass writes them
+      if constexpr (!G) break;
+      // the next camera among the group's rows (uniform)
+      int64_t next = -1;
+      for (int r = 0; r < 16 && next < 0; ++r) {
+        const int64_t u = grp * 16 + r;
+        if (u < cnt && cam_of(u) > cam) next = cam_of(u);
+      }
+      if (next < 0) break;
+      cam = next;
     }
-    __syncthreads();  // the partial sums are read before the next group writes them
   }
 }
 
@@ -1238,10 +1333,14 @@ template <typename T, bool FIRST>
 int launch_conv_nt(int nt, const ConvArgs& a, unsigned grid, size_t lds, hipStream_t st) {
 #define NSC_CONV_CASE(N)                                                                       \
   case N:                                                                                      \
-    if (FIRST)                                                                                 \
-      hipLaunchKernelGGL((k_conv_first<T, N>), dim3(grid), dim3(256), lds, st, a);             \
+    if (FIRST && a.nets)                                                                       \
+      hipLaunchKernelGGL((k_conv_first<T, N, true>), dim3(grid), dim3(256), lds, st, a);       \
+    else if (FIRST)                                                                            \
+      hipLaunchKernelGGL((k_conv_first<T, N, false>), dim3(grid), dim3(256), lds, st, a);      \
+    else if (a.nets)                                                                           \
+      hipLaunchKernelGGL((k_conv<T, N, true>), dim3(grid), dim3(256), lds, st, a);             \
     else                                                                                       \
-      hipLaunchKernelGGL((k_conv<T, N>), dim3(grid), dim3(256), lds, st, a);                   \
+      hipLaunchKernelGGL((k_conv<T, N, false>), dim3(grid), dim3(256), lds, st, a);            \
     break;
   switch (nt) {
     NSC_CONV_CASE(1)
@@ -1261,9 +1360,14 @@ int launch_conv_nt(int nt, const ConvArgs& a, unsigned grid, size_t lds, hipStre
 
 template <typename T>
 int launch_dense_nt(int nt, const DenseArgs& a, unsigned grid, hipStream_t st) {
-#define NSC_DENSE_CASE(N)                                                                  \
-  case N:                                                                                  \
-    hipLaunchKernelGGL((k_dense<T, N>), dim3(grid), dim3(64 * dense_waves<N>()), 0, st, a); \
+#define NSC_DENSE_CASE(N)                                                                      \
+  case N:                                                                                      \
+    if (a.nets)                                                                                \
+      hipLaunchKernelGGL((k_dense<T, N, true>), dim3(grid), dim3(64 * dense_waves<N>()), 0, st, \
+                         a);                                                                   \
+    else                                                                                       \
+      hipLaunchKernelGGL((k_dense<T, N, false>), dim3(grid), dim3(64 * dense_waves<N>()), 0,   \
+                         st, a);                                                               \
     break;
   switch (nt) {
     NSC_DENSE_CASE(1)
@@ -1386,16 +1490,18 @@ int launch_pair(int nt0, int nt1, const ConvArgs& a0, const ConvArgs& a1, const 
                 unsigned grid, size_t lds, hipStream_t st) {
   // second-layer weights in registers when they are 9 taps x 32 channels x <= 32 outputs
   const bool breg = a1.cin == 32 && nt1 <= 2;
-#define NSC_PAIR_CASE(A, B)                                                                  \
-  if (nt0 == A && nt1 == B) {                                                                \
-    if (breg && A <= 2 && B <= 2)                                                            \
-      hipLaunchKernelGGL((k_conv_pair<A, B, (A <= 2 && B <= 2)>), dim3(grid), dim3(1024), lds,\
-                         st, a0, a1, pa);                                                    \
-    else                                                                                     \
-      hipLaunchKernelGGL((k_conv_pair<A, B, false>), dim3(grid), dim3(1024), lds, st, a0, a1, \
-                         pa);                                                                \
-    NSC_CHECK_LAUNCH("k_conv_pair");                                                         \
-    return NSC_OK;                                                                           \
+#define NSC_PAIR_LAUNCH(A, B, R, G)                                                            \
+  hipLaunchKernelGGL((k_conv_pair<A, B, R, G>), dim3(grid), dim3(1024), lds, st, a0, a1, pa)
+#define NSC_PAIR_CASE(A, B)                                                                    \
+  if (nt0 == A && nt1 == B) {                                                                  \
+    constexpr bool R = A <= 2 && B <= 2;                                                       \
+    if (breg && R) {                                                                           \
+      if (a0.nets) NSC_PAIR_LAUNCH(A, B, R, true); else NSC_PAIR_LAUNCH(A, B, R, false);       \
+    } else {                                                                                   \
+      if (a0.nets) NSC_PAIR_LAUNCH(A, B, false, true); else NSC_PAIR_LAUNCH(A, B, false, false); \
+    }                                                                                          \
+    NSC_CHECK_LAUNCH("k_conv_pair");                                                           \
+    return NSC_OK;                                                                             \
   }
   NSC_PAIR_CASE(1, 1)
   NSC_PAIR_CASE(1, 2)
@@ -1406,6 +1512,7 @@ int launch_pair(int nt0, int nt1, const ConvArgs& a0, const ConvArgs& a1, const 
   NSC_PAIR_CASE(4, 1)
   NSC_PAIR_CASE(4, 2)
 #undef NSC_PAIR_CASE
+#undef NSC_PAIR_LAUNCH
   return fail(NSC_E_SHAPE, "fused conv pair with %d and %d output channels", nt0 * 16, nt1 * 16);
 }
 }  // namespace
@@ -1465,14 +1572,20 @@ int launch_band64(bool pair, int nt, const ConvArgs& a0, const ConvArgs& a1, con
   int64_t grid = kNumCU * per_cu;  // a multiple of 8 (see band_item)
   if (grid > items) grid = items;
   if (grid < 1) grid = 1;
+#define NSC_BAND_LAUNCH(N, G)                                                                   \
+  if (pair)                                                                                     \
+    hipLaunchKernelGGL((k_pair64<N, G>), dim3((unsigned)grid), dim3(64 * kBandWaves), lds, st,  \
+                       a0, a1, b, xin, xr, xw);                                                 \
+  else                                                                                          \
+    hipLaunchKernelGGL((k_band64<N, G>), dim3((unsigned)grid), dim3(64 * kBandWaves), lds, st,  \
+                       a1, b)
 #define NSC_BAND_CASE(N)                                                                        \
   case N:                                                                                       \
-    if (pair)                                                                                   \
-      hipLaunchKernelGGL((k_pair64<N>), dim3((unsigned)grid), dim3(64 * kBandWaves), lds, st, a0, \
-                         a1, b, xin, xr, xw);                                                   \
-    else                                                                                        \
-      hipLaunchKernelGGL((k_band64<N>), dim3((unsigned)grid), dim3(64 * kBandWaves), lds, st, a1, \
-                         b);                                                                    \
+    if (a1.nets) {                                                                              \
+      NSC_BAND_LAUNCH(N, true);                                                                 \
+    } else {                                                                                    \
+      NSC_BAND_LAUNCH(N, false);                                                                \
+    }                                                                                           \
     break;
   switch (nt) {
     NSC_BAND_CASE(2)
@@ -1481,6 +1594,7 @@ int launch_band64(bool pair, int nt, const ConvArgs& a0, const ConvArgs& a1, con
       return fail(NSC_E_SHAPE, "banded layer with %d output channels", nt * 16);
   }
 #undef NSC_BAND_CASE
+#undef NSC_BAND_LAUNCH
   NSC_CHECK_LAUNCH(pair ? "k_pair64" : "k_band64");
   return NSC_OK;
 }
@@ -1533,6 +1647,8 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
     a.kpad = L.kpad;
     a.pool = L.pool ? 1 : 0;
     conv_tiles(L, &a.tiles_y, &a.tiles_x);
+    a.nets = r.nets;
+    a.per_cam = r.per_cam;
     return a;
   };
   // weights in fragment order for the banded kernels
@@ -1631,6 +1747,8 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
   d.frame_logit = r.frame_logit;
   d.c_low = r.c_low;
   d.c_high = r.c_high;
+  d.nets = r.nets;
+  d.per_cam = r.per_cam;
   int64_t groups = (r.max_count + 15) / 16;  // one workgroup per 16-survivor group
   int64_t grid = groups;
   if (grid > kNumCU * 2) grid = kNumCU * 2;

@@ -186,6 +186,73 @@ __global__ void __launch_bounds__(256) k_state_update(const int32_t* __restrict_
   }
 }
 
+// Camera group: one workgroup per camera resolves its n frames (frames
+// cam * n .. cam * n + n - 1 of the batch).  Earlier-frame cameras walk each
+// residue column down its chain (the decision of the last fired frame, else
+// the state slot's); fixed-reference cameras label non-firing frames 0.
+__global__ void __launch_bounds__(256) k_group_resolve(const CamDiff* __restrict__ cams,
+                                                       const uint8_t* __restrict__ fire,
+                                                       const uint8_t* __restrict__ dec, int64_t n,
+                                                       int64_t t0,
+                                                       const unsigned char* __restrict__ state,
+                                                       int64_t state_stride,
+                                                       uint8_t* __restrict__ label,
+                                                       uint8_t* __restrict__ defer) {
+  const int64_t cam = blockIdx.x;
+  const CamDiff cd = cams[cam];
+  const int64_t base = cam * n;
+  if (cd.ref_mode == NSC_REF_FIXED) {
+    for (int64_t u = threadIdx.x; u < n; u += blockDim.x) {
+      const uint8_t d = fire[base + u] ? dec[base + u] : (uint8_t)0;
+      label[base + u] = d & 1;
+      defer[base + u] = (d >> 1) & 1;
+    }
+    return;
+  }
+  const uint8_t* st_dec = state + cam * state_stride + cd.dec_off;
+  for (int r = threadIdx.x; r < cd.delta; r += blockDim.x) {
+    // frames of the chain before the call: slot r holds frame t0 - delta + r
+    // (frames t < delta always fire, so t0 = 0 never reads it)
+    uint8_t d = t0 > 0 ? st_dec[r] : (uint8_t)0;
+    for (int64_t u = r; u < n; u += cd.delta) {
+      if (fire[base + u]) d = dec[base + u];
+      label[base + u] = d & 1;
+      defer[base + u] = (d >> 1) & 1;
+    }
+  }
+}
+
+// Camera group state after a call of n frames per camera: every earlier-frame
+// camera keeps the sums and decisions of its last delta frames in its slot.
+// `old` is a copy of the state before the call, read where n < delta.
+__global__ void __launch_bounds__(256) k_group_state(const CamDiff* __restrict__ cams,
+                                                     const int32_t* __restrict__ sums,
+                                                     const uint8_t* __restrict__ label,
+                                                     const uint8_t* __restrict__ defer, int64_t n,
+                                                     int64_t cells,
+                                                     const unsigned char* __restrict__ old,
+                                                     unsigned char* __restrict__ state,
+                                                     int64_t state_stride) {
+  const int64_t cam = blockIdx.y;
+  const CamDiff cd = cams[cam];
+  if (cd.ref_mode != NSC_REF_PREV) return;
+  const int64_t total = (int64_t)cd.delta * cells;
+  int32_t* st_sums = reinterpret_cast<int32_t*>(state + cam * state_stride);
+  uint8_t* st_dec = state + cam * state_stride + cd.dec_off;
+  const int32_t* o_sums = reinterpret_cast<const int32_t*>(old + cam * state_stride);
+  const uint8_t* o_dec = old + cam * state_stride + cd.dec_off;
+  const int64_t base = cam * n;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t k = e / cells, c = e - k * cells;
+    const int64_t src = n - cd.delta + k;  // local index of the frame kept in slot k
+    st_sums[e] = src >= 0 ? sums[(base + src) * cells + c] : o_sums[(k + n) * cells + c];
+    if (c == 0)
+      st_dec[k] = src >= 0 ? (uint8_t)(label[base + src] | (defer[base + src] << 1))
+                           : o_dec[k + n];
+  }
+}
+
 // Frame skipping (Sec. 5): each frame takes its checked frame's output.
 __global__ void __launch_bounds__(256) k_skip_expand(SkipExpand e) {
   for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < e.n;
@@ -315,6 +382,39 @@ int launch_state_update(const int32_t* sums, const uint8_t* label, const uint8_t
                      stream, sums, label, defer, n, delta, cells, old_sums, old_dec, state_sums,
                      state_dec);
   NSC_CHECK_LAUNCH("k_state_update");
+  return NSC_OK;
+}
+
+int launch_group_resolve(const CamDiff* cams, int32_t n_cams, const uint8_t* fire,
+                         const uint8_t* dec, int64_t n, int64_t t0, const unsigned char* state,
+                         int64_t state_stride, uint8_t* label, uint8_t* defer,
+                         hipStream_t stream) {
+  if (n <= 0 || n_cams <= 0) return NSC_OK;
+  hipLaunchKernelGGL(k_group_resolve, dim3((unsigned)n_cams), dim3(256), 0, stream, cams, fire,
+                     dec, n, t0, state, state_stride, label, defer);
+  NSC_CHECK_LAUNCH("k_group_resolve");
+  return NSC_OK;
+}
+
+int launch_group_state(const CamDiff* cams, int32_t n_cams, int32_t max_delta,
+                       const int32_t* sums, const uint8_t* label, const uint8_t* defer, int64_t n,
+                       int64_t cells, unsigned char* state, int64_t state_stride, void* scratch,
+                       hipStream_t stream) {
+  if (n <= 0 || n_cams <= 0 || max_delta <= 0) return NSC_OK;
+  const unsigned char* old = state;
+  if (n < max_delta) {
+    // slots k < delta - n keep frames of the previous state: copy it first
+    unsigned char* cp = static_cast<unsigned char*>(scratch);
+    const int64_t bytes = (int64_t)n_cams * state_stride;
+    hipLaunchKernelGGL(k_copy_u8, dim3(grid_for(bytes, 256)), dim3(256), 0, stream, state, cp,
+                       bytes);
+    NSC_CHECK_LAUNCH("k_copy_u8");
+    old = cp;
+  }
+  const unsigned gx = grid_for((int64_t)max_delta * cells, 256);
+  hipLaunchKernelGGL(k_group_state, dim3(gx, (unsigned)n_cams), dim3(256), 0, stream, cams, sums,
+                     label, defer, n, cells, old, state, state_stride);
+  NSC_CHECK_LAUNCH("k_group_state");
   return NSC_OK;
 }
 

@@ -76,7 +76,20 @@ int make_area_plan(int32_t in_h, int32_t in_w, int64_t stride, const void* frame
 int launch_area_sums(const AreaPlan& plan, const uint8_t* frames, int64_t stride, int64_t n,
                      int32_t* sums, hipStream_t stream);
 
-// Detector scoring of frames [t0, t0+n) whose area sums are in `sums`.
+// One camera's detector settings in a camera group (device table).
+struct CamDiff {
+  const int32_t* ref_sums;  // FIXED: reference area sums
+  const float* lr_w;        // blocked: LR weights
+  double lr_b, delta_diff;
+  int32_t ref_mode, delta, grid_h, grid_w;
+  int64_t dec_off;          // PREV: offset of the decisions in the camera's state slot
+};
+
+// Detector scoring of frames [t0, t0+n) whose area sums are in `sums`.  With
+// a camera group (cams != null) the n frames are per_cam frames of each
+// camera in turn, every camera with its own settings from cams[] and its
+// earlier frames in its state slot (state + camera * state_stride); the
+// per-stream fields below are then unused.
 struct DiffArgs {
   const int32_t* sums;       // [n][cells]
   const int32_t* prev_sums;  // [delta][cells] frames t0-delta..t0-1 (PREV, t0 > 0)
@@ -88,6 +101,10 @@ struct DiffArgs {
   int32_t metric;            // NSC_METRIC_*
   double* score;             // nullable
   uint8_t* fire;
+  const CamDiff* cams;       // camera group (else null)
+  int64_t per_cam;
+  const unsigned char* state;
+  int64_t state_stride;
 };
 int launch_diff(const DiffArgs& a, hipStream_t stream);
 
@@ -109,6 +126,17 @@ int launch_state_update(const int32_t* sums, const uint8_t* label, const uint8_t
                         int32_t delta, int64_t cells, int32_t* state_sums, uint8_t* state_dec,
                         void* scratch, hipStream_t stream);
 int launch_fill_nan(float* p, int64_t n, hipStream_t stream);
+// Camera groups: label resolution of n frames per camera, and the state slots
+// (the last delta frames of every earlier-frame camera; scratch holds a copy
+// of n_cams * state_stride bytes when n < max_delta).
+int launch_group_resolve(const CamDiff* cams, int32_t n_cams, const uint8_t* fire,
+                         const uint8_t* dec, int64_t n, int64_t t0, const unsigned char* state,
+                         int64_t state_stride, uint8_t* label, uint8_t* defer,
+                         hipStream_t stream);
+int launch_group_state(const CamDiff* cams, int32_t n_cams, int32_t max_delta,
+                       const int32_t* sums, const uint8_t* label, const uint8_t* defer, int64_t n,
+                       int64_t cells, unsigned char* state, int64_t state_stride, void* scratch,
+                       hipStream_t stream);
 int launch_set_i32(int32_t* p, int32_t v, hipStream_t stream);
 
 // Frame skipping: frames [t0, t0+n) take the outputs of their checked frame
@@ -164,6 +192,17 @@ struct Cnn {
   float b2;
   size_t act_elems;         // largest per-image activation (elements)
 };
+// One camera's network in a camera group: the group's networks share one
+// description, so each camera's weights sit at the same offsets of its own
+// allocation, `woff` bytes from the base network's; its output bias and
+// decision thresholds.
+struct CamNet {
+  int64_t woff;
+  double c_low, c_high;
+  float b2;
+  int32_t pad;
+};
+
 struct CnnRunArgs {
   const int32_t* sums;
   int32_t sums_h, sums_w, fy, fx;
@@ -177,6 +216,10 @@ struct CnnRunArgs {
   uint8_t* dec;
   double c_low, c_high;
   float* frame_logit;       // nullable: logit scattered to frame position idx[i]
+  // camera group (nullable): survivor slot s is camera idx[s] / per_cam and
+  // runs that camera's network, bias b2 and thresholds from nets[]
+  const CamNet* nets;
+  int64_t per_cam;
 };
 size_t cnn_workspace_bytes(const Cnn& cnn, int64_t max_count);
 int run_cnn(const Cnn& cnn, const CnnRunArgs& a, void* ws, size_t ws_bytes, hipStream_t stream);

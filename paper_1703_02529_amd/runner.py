@@ -12,8 +12,18 @@ from typing import Optional
 
 import torch
 
-from . import (NSC_METRIC_MSE, NSC_REF_FIXED, NSC_REF_PREV, Cnn, make_cfg, make_desc,
-               nsc_cascade_run, nsc_cascade_workspace_bytes, nsc_state_bytes)
+from . import (NSC_METRIC_MSE, NSC_REF_FIXED, NSC_REF_PREV, Cnn, Group, make_cfg, make_desc,
+               nsc_cascade_run, nsc_cascade_workspace_bytes, nsc_group_run,
+               nsc_group_state_bytes, nsc_group_workspace_bytes, nsc_state_bytes)
+
+
+def _cfg_of(wl, lr_w=None, ref_sums=None, frame_stride=None):
+    return make_cfg(in_h=wl.video.h, in_w=wl.video.w, dd_h=wl.dd_h, dd_w=wl.dd_w,
+                    cnn_h=wl.cnn.in_h, cnn_w=wl.cnn.in_w, ref_mode=wl.ref_mode, delta=wl.delta,
+                    grid=tuple(wl.grid), lr_w=lr_w, lr_b=wl.lr_bias, ref_sums=ref_sums,
+                    delta_diff=wl.delta_diff, c_low=wl.c_low, c_high=wl.c_high,
+                    frame_stride=frame_stride, check_stride=getattr(wl, "check_stride", 1),
+                    metric=getattr(wl, "metric", NSC_METRIC_MSE))
 
 
 class CascadeRunner:
@@ -23,13 +33,7 @@ class CascadeRunner:
         self.device = torch.device(device)
         self.lr_w = lr_w
         self.ref_sums = ref_sums
-        self.cfg = make_cfg(in_h=wl.video.h, in_w=wl.video.w, dd_h=wl.dd_h, dd_w=wl.dd_w,
-                            cnn_h=wl.cnn.in_h, cnn_w=wl.cnn.in_w, ref_mode=wl.ref_mode,
-                            delta=wl.delta, grid=tuple(wl.grid), lr_w=lr_w, lr_b=wl.lr_bias,
-                            ref_sums=ref_sums, delta_diff=wl.delta_diff, c_low=wl.c_low,
-                            c_high=wl.c_high, frame_stride=frame_stride,
-                            check_stride=getattr(wl, "check_stride", 1),
-                            metric=getattr(wl, "metric", NSC_METRIC_MSE))
+        self.cfg = _cfg_of(wl, lr_w, ref_sums, frame_stride)
         self.desc = make_desc(wl.cnn.conv, wl.cnn.pool, wl.cnn.dense, wl.cnn.in_h, wl.cnn.in_w,
                               wl.cnn.bf16)
         self.cnn = Cnn(self.desc, blob)
@@ -62,4 +66,56 @@ class CascadeRunner:
         self.cnn.close()
 
 
-__all__ = ["CascadeRunner", "NSC_REF_PREV", "NSC_REF_FIXED"]
+class GroupRunner:
+    """Buffers of a camera group: one workload description per camera (same
+    frame geometry and metric), each with its weight blob and its device LR
+    weights / reference sums (None where unused).  Runs n frames of every
+    camera per call, camera-major."""
+
+    def __init__(self, wls, blobs, frames_per_cam: int, lr_ws=None, ref_sums=None,
+                 device="cuda"):
+        self.wls = list(wls)
+        k = len(self.wls)
+        self.device = torch.device(device)
+        self.lr_ws = list(lr_ws) if lr_ws is not None else [None] * k
+        self.ref_sums = list(ref_sums) if ref_sums is not None else [None] * k
+        self.cfgs = [_cfg_of(w, l, r) for w, l, r in zip(self.wls, self.lr_ws, self.ref_sums)]
+        self.cnns = [Cnn(make_desc(w.cnn.conv, w.cnn.pool, w.cnn.dense, w.cnn.in_h, w.cnn.in_w,
+                                   w.cnn.bf16), b) for w, b in zip(self.wls, blobs)]
+        self.group = Group(self.cfgs, self.cnns)
+        self.frames_per_cam = frames_per_cam
+        total = k * frames_per_cam
+        ws = nsc_group_workspace_bytes(self.group, frames_per_cam)
+        self.ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=self.device)
+        sb, self.slot_bytes = nsc_group_state_bytes(self.group)
+        self.state = torch.zeros(max(sb, 256), dtype=torch.uint8, device=self.device)
+        self.label = torch.empty(total, dtype=torch.uint8, device=self.device)
+        self.defer = torch.empty(total, dtype=torch.uint8, device=self.device)
+        self.score = torch.empty(total, dtype=torch.float64, device=self.device)
+        self.fire = torch.empty(total, dtype=torch.uint8, device=self.device)
+        self.logit = torch.empty(total, dtype=torch.float32, device=self.device)
+        self.next_t = 0
+
+    def run(self, frames: torch.Tensor, n: int, t0: Optional[int] = None, taps: bool = True,
+            want_stats: bool = False, stage_events=None, stream=None):
+        """Frames [t0, t0+n) of every camera: frames holds camera c's frame
+        t0 + j at index c * n + j; outputs are [camera][n] in the first
+        len(wls) * n entries of label / defer / score / fire / logit."""
+        if n > self.frames_per_cam:
+            raise ValueError(f"{n} frames per camera exceed the workspace's {self.frames_per_cam}")
+        t0 = self.next_t if t0 is None else t0
+        m = len(self.wls) * n
+        kw = dict(score=self.score[:m], fire=self.fire[:m], logit=self.logit[:m]) if taps else {}
+        st = nsc_group_run(self.group, frames, n, t0, self.state, self.ws, self.label[:m],
+                           self.defer[:m], want_stats=want_stats, stage_events=stage_events,
+                           stream=stream, **kw)
+        self.next_t = t0 + n
+        return st
+
+    def close(self):
+        self.group.close()
+        for c in self.cnns:
+            c.close()
+
+
+__all__ = ["CascadeRunner", "GroupRunner", "NSC_REF_PREV", "NSC_REF_FIXED"]

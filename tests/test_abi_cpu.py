@@ -86,6 +86,20 @@ def test_detector_metrics():
     assert nsc.nsc_cfg_check(c) == -1 and "PSNR" in nsc.last_error()
 
 
+def test_group_arguments_are_checked_on_the_host():
+    """nsc_group_create rejects bad camera sets before any device call (NULL
+    network handles are only looked at once every cfg has passed)."""
+    good = _cfg()
+    assert nsc.nsc_group_create_status([good, good], [None, None]) == -1   # NULL handles
+    assert "handle" in nsc.last_error()
+    for kw in (dict(in_h=240, in_w=320), dict(dd_h=25, dd_w=25, cnn_h=25, cnn_w=25),
+               dict(metric=nsc.NSC_METRIC_SAD), dict(check_stride=5)):
+        assert nsc.nsc_group_create_status([good, _cfg(**kw)], [None, None]) == -1, kw
+        assert "camera 1" in nsc.last_error()
+    assert nsc.nsc_group_create_status([good, _cfg(delta=0)], [None, None]) == -1
+    assert nsc.nsc_group_create_status([], []) == -1
+
+
 def test_frame_skipping_sizes():
     # stride 0 and 1 mean every frame; a stride that divides delta is valid
     assert nsc.nsc_cfg_check(_cfg(check_stride=0)) == 0

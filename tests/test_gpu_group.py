@@ -1,0 +1,193 @@
+"""GPU parity of camera groups (Sec. 8: frames of many streams batched, each
+stream with its own model) against the fp64 oracle.
+
+A group run must give every camera exactly the outputs of its own cascade:
+the oracle runs each camera's frames with that camera's cfg and network, and
+the group's outputs for that camera are compared element by element (scores
+and fire flags bit-exact, logits within the network's tolerance, labels and
+defer flags exact outside the threshold band).
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1703_02529_amd as nsc
+import synth
+from paper_1703_02529_amd.runner import CascadeRunner, GroupRunner
+from synth import workloads as W
+
+from helpers import compare_cascade, lr_weights_for
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _camera(base, seed, **kw):
+    """base with its own video (seed) and the given per-camera settings."""
+    return base.replace(video=dataclasses.replace(base.video, seed=seed), **kw)
+
+
+def _blob(wl):
+    return synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
+
+
+def _ref_image(wl):
+    return synth.Video(wl.video).median_background() if wl.ref_mode == W.FIXED else None
+
+
+def _run_group(cams, t_first, sizes):
+    """Runs the group over frames [t_first, t_first + sum(sizes)) of every
+    camera in calls of the given sizes; returns per-camera output dicts."""
+    videos = [synth.Video(w.video) for w in cams]
+    refs = [_ref_image(w) for w in cams]
+    ref_dev = []
+    for w, r in zip(cams, refs):
+        if r is None:
+            ref_dev.append(None)
+            continue
+        out = torch.empty(w.dd_h * w.dd_w * 3, dtype=torch.int32, device=DEV)
+        nsc.nsc_downsample(torch.from_numpy(r.reshape(-1)).to(DEV), 1, w.video.h, w.video.w,
+                           w.dd_h, w.dd_w, out)
+        ref_dev.append(out)
+    lr_dev = [torch.from_numpy(lr_weights_for(w)).to(DEV) if w.grid != (1, 1) else None
+              for w in cams]
+    run = GroupRunner(cams, [_blob(w) for w in cams], frames_per_cam=max(sizes), lr_ws=lr_dev,
+                      ref_sums=ref_dev)
+    keys = ("score", "fire", "logit", "label", "defer")
+    outs = [{k: [] for k in keys} for _ in cams]
+    t = 0
+    for n in sizes:
+        batch = np.concatenate([v.frames(t_first + t, t_first + t + n) for v in videos])
+        run.run(torch.from_numpy(batch.reshape(-1)).to(DEV), n, t0=t)
+        for k in keys:
+            a = getattr(run, k)[:len(cams) * n].cpu().numpy().reshape(len(cams), n)
+            for c in range(len(cams)):
+                outs[c][k].append(a[c].copy())
+        t += n
+    run.close()
+    return [{k: np.concatenate(o[k]) for k in keys} for o in outs], videos, refs
+
+
+def _oracle_camera(wl, video, ref_img, t_first, n):
+    lr = lr_weights_for(wl) if wl.grid != (1, 1) else None
+    ref_o = oracle.area_sums(ref_img, wl.dd_h, wl.dd_w) if ref_img is not None else None
+    cfg, keep = oracle.make_cfg(wl, lr_w=lr, ref_sums=ref_o)
+    out, _ = oracle.cascade(cfg, wl.cnn, _blob(wl), video.frames(t_first, t_first + n), t0=0)
+    return out
+
+
+def _check_group(cams, t_first, sizes):
+    gpu, videos, refs = _run_group(cams, t_first, sizes)
+    n = sum(sizes)
+    reps = []
+    for c, w in enumerate(cams):
+        ref = _oracle_camera(w, videos[c], refs[c], t_first, n)
+        reps.append(compare_cascade(w, gpu[c], ref, t0=0))
+    return reps
+
+
+def test_group_tiny_mixed_cameras():
+    """Six 100x100 cameras: earlier-frame detectors with delta 1, 3, 7 and 2,
+    two fixed-reference cameras, each with its own video, threshold, c_low /
+    c_high and fp32 network; calls of 40, 1, 59 and 100 frames per camera."""
+    b = W.TINY
+    cams = [
+        _camera(b, 11, delta=1, delta_diff=20.0, weight_seed=2001),
+        _camera(b, 12, delta=3, delta_diff=12.0, weight_seed=2002, c_low=0.4, c_high=0.6),
+        _camera(b, 13, delta=7, delta_diff=30.0, weight_seed=2003),
+        _camera(b, 14, ref_mode=W.FIXED, delta_diff=25.0, weight_seed=2004, c_low=0.1),
+        _camera(b, 15, delta=2, delta_diff=5.0, weight_seed=2005, c_high=0.95),
+        _camera(b, 16, ref_mode=W.FIXED, delta_diff=60.0, weight_seed=2006),
+    ]
+    reps = _check_group(cams, 0, [40, 1, 59, 100])
+    print(reps)
+    assert sum(r["fired"] for r in reps) > 100
+
+
+def test_group_single_camera_equals_cascade_run():
+    """A group of one camera gives nsc_cascade_run's outputs bit for bit (the
+    640x480 bf16 network: the fused first pair and the dense kernel)."""
+    wl = W.VGA
+    v = synth.Video(wl.video)
+    occ = np.flatnonzero(v.occupied)
+    t_first = max(0, int(occ[0]) - 20)
+    sizes = [30, 7, 43]
+    n = sum(sizes)
+    frames = v.frames(t_first, t_first + n)
+    blob = _blob(wl)
+    one = CascadeRunner(wl, blob, max_frames=max(sizes))
+    grp = GroupRunner([wl], [blob], frames_per_cam=max(sizes))
+    keys = ("score", "fire", "logit", "label", "defer")
+    t = 0
+    for m in sizes:
+        d = torch.from_numpy(frames[t:t + m].reshape(-1)).to(DEV)
+        one.run(d, m, t0=t)
+        grp.run(d, m, t0=t)
+        for k in keys:
+            a, g = getattr(one, k)[:m].cpu().numpy(), getattr(grp, k)[:m].cpu().numpy()
+            assert np.array_equal(a, g, equal_nan=True), (k, t)
+        t += m
+    one.close()
+    grp.close()
+
+
+def test_group_vga_cameras():
+    """Five 640x480 cameras with the bf16 network (each its own weights,
+    threshold, c_low / c_high and delta), two calls of 30 frames."""
+    b = W.VGA
+    cams = [
+        _camera(b, 21, weight_seed=3001),
+        _camera(b, 22, weight_seed=3002, delta=5, delta_diff=8.0, c_low=0.45, c_high=0.55),
+        _camera(b, 23, weight_seed=3003, delta=15, delta_diff=25.0),
+        _camera(b, 24, weight_seed=3004, delta=1, delta_diff=3.0, c_low=0.3, c_high=0.7),
+        _camera(b, 25, weight_seed=3005, delta=10, delta_diff=15.0),
+    ]
+    reps = _check_group(cams, 0, [30, 30])
+    print(reps)
+    assert sum(r["fired"] for r in reps) > 40
+
+
+def test_group_hd_fixed_reference_cameras():
+    """Two 1280x720 fixed-reference cameras with the 4-layer 64-channel bf16
+    network (fused first pair and banded layers with per-camera weights)."""
+    b = W.HD_REF
+    cams = [_camera(b, 31, weight_seed=4001, delta_diff=10.0),
+            _camera(b, 32, weight_seed=4002, delta_diff=0.3, c_low=0.4, c_high=0.6)]
+    occ = np.flatnonzero(synth.Video(cams[0].video).occupied)
+    reps = _check_group(cams, max(0, int(occ[0]) - 2), [3, 4])
+    print(reps)
+    assert sum(r["fired"] for r in reps) > 0
+
+
+def test_group_hd_blocked_cameras():
+    """Three 1280x720 blocked-detector cameras (own LR weights through their
+    weight seed), the 3-layer 64-channel network."""
+    b = W.HD_BLOCKED
+    cams = [_camera(b, 41, weight_seed=5001, delta=1),
+            _camera(b, 42, weight_seed=5002, delta=2, lr_bias=-1.0),
+            _camera(b, 43, weight_seed=5003, delta=1, c_low=0.45, c_high=0.55)]
+    occ = np.flatnonzero(synth.Video(cams[0].video).occupied)
+    reps = _check_group(cams, max(0, int(occ[0]) - 2), [4, 2])
+    print(reps)
+    assert sum(r["fired"] for r in reps) > 0
+
+
+def test_group_rejects_mixed_geometry_and_skipping():
+    a = W.TINY
+    blob = _blob(a)
+    cnn = nsc.Cnn(nsc.make_desc(a.cnn.conv, a.cnn.pool, a.cnn.dense, 50, 50, False), blob)
+    from paper_1703_02529_amd.runner import _cfg_of
+    good = _cfg_of(a)
+    skip = _cfg_of(a.replace(check_stride=2, delta=2))
+    assert nsc.nsc_group_create_status([good, good], [cnn.handle, cnn.handle]) == 0
+    assert nsc.nsc_group_create_status([good, skip], [cnn.handle, cnn.handle]) == -1
+    other = nsc.Cnn(nsc.make_desc((32, 16), (True, True), 32, 50, 50, False),
+                    synth.weight_blob(dataclasses.replace(a.cnn, conv=(32, 16)),
+                                      synth.cnn_weights(dataclasses.replace(a.cnn, conv=(32, 16)),
+                                                        1)))
+    assert nsc.nsc_group_create_status([good, good], [cnn.handle, other.handle]) == -2
+    cnn.close()
+    other.close()
