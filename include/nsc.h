@@ -230,7 +230,8 @@ int nsc_compact(const uint8_t* fire, int64_t n, int32_t* idx_out, int32_t* count
  * evaluates the network on frame idx[i]'s area sums: sums (device,
  * [*][sums_h][sums_w][3] int32 with denominator den) are summed over
  * fy x fx cells when sums_h = fy*in_h, sums_w = fx*in_w; the input is
- * x = (S/den')/127.5 - 1.  Writes logit_out[i] (device, float) and, if
+ * x = (S/den')/127.5 - 1 (den' = den * fy * fx, with 255 den' < 2^31, the
+ * sums being values of 0..255 times den).  Writes logit_out[i] (device, float) and, if
  * prob_out is not NULL, prob_out[i] = sigmoid(logit).  max_count bounds
  * *count (entries beyond max_count are not evaluated).  ws:
  * nsc_cnn_workspace_bytes(cnn, max_count).  Errors: NSC_E_INVAL,

@@ -533,6 +533,8 @@ int nsc_specialized_cnn(const nsc_cnn* cnn, const int32_t* sums, int32_t sums_h,
               NSC_E_SHAPE, "sums grid %dx%d does not nest onto the CNN input %dx%d", sums_h, sums_w,
               c.desc.in_h, c.desc.in_w);
   NSC_REQUIRE(den >= 1, NSC_E_INVAL, "den must be positive");
+  NSC_REQUIRE(255 * (double)den * (sums_h / c.desc.in_h) * (sums_w / c.desc.in_w) < 2147483648.0,
+              NSC_E_SHAPE, "den %lld: the CNN input sums overflow 32 bits", (long long)den);
   if (max_count == 0) return NSC_OK;
   NSC_REQUIRE(sums && idx && count && logit_out, NSC_E_INVAL, "a required pointer is NULL");
   NSC_REQUIRE(ws != nullptr && ((uintptr_t)ws % kAlign) == 0, NSC_E_WORKSPACE,

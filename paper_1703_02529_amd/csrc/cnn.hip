@@ -74,6 +74,17 @@ __device__ __forceinline__ uint16_t div_to_bf16_bits(int32_t N, int32_t D) {
   return f32_to_bf16_bits(__uint_as_float(u));
 }
 
+// The same from the product with inv = fp32(1 / D): N * inv is within 2 fp32
+// ulps of N / D (two roundings of 2^-24 each), so unless it lies within 2
+// ulps of a bf16 midpoint (low 16 bits 0x7FFE .. 0x8002) it rounds to bf16
+// like the exact quotient; those rare values take the division above.
+__device__ __forceinline__ uint16_t div_to_bf16_bits_fast(int32_t N, int32_t D, float inv) {
+  const float r = (float)N * inv;
+  const uint32_t low = __float_as_uint(r) & 0xFFFFu;
+  if (low - 0x7FFEu <= 4u) return div_to_bf16_bits(N, D);
+  return f32_to_bf16_bits(r);
+}
+
 // Element-type traits: E = elements per lane per MFMA, KS = K per MFMA.
 template <typename T> struct Elt;
 template <> struct Elt<uint16_t> {  // bf16 stored as raw bits
@@ -248,6 +259,20 @@ __device__ __forceinline__ void conv_epilogue(const ConvArgs& a, const f32x4 (&a
   }
 }
 
+// The pooled epilogue with the lane's output address precomputed: o is the
+// lane's channel m of its pooled pixel, inside when that pixel is stored.
+template <int NT>
+__device__ __forceinline__ void pool_epilogue_at(const f32x4 (&acc)[NT], const float (&bias)[NT],
+                                                 float* o, bool inside) {
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    float v = 0.0f;  // ReLU floor
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v = fmaxf(v, acc[nt][r] + bias[nt]);
+    if (inside) o[nt * 16] = v;
+  }
+}
+
 // First layer (3 input channels).  The survivor's area sums are gathered
 // (fy x fx nested cells summed) and pre-processed into a zero-padded band in
 // LDS, 4 channels per pixel (the fourth is 0).  K is ordered (dy, dx, c) with
@@ -267,13 +292,14 @@ __device__ __forceinline__ void stage_first(const ConvArgs& a, T* in, int64_t s,
   const int32_t* S = a.sums + (int64_t)a.idx[s] * a.sums_h * a.sums_w * 3;
   const int npix = rows * band_w;
   const bool f32div = a.den255 < (1 << 24);  // the fp32 quotient path is exact
+  const float inv = 1.0f / (float)a.den255;
 #pragma unroll 2
   for (int p = threadIdx.x - tid0; p < npix; p += nthreads) {
     const int br = p / band_w, bc = p - br * band_w;
     const int y = y_top + br, x = x_left + bc;
     T v[4] = {X::from_f32(0.0f), X::from_f32(0.0f), X::from_f32(0.0f), X::from_f32(0.0f)};
     if (y >= 0 && y < a.h && x >= 0 && x < a.w) {
-      int64_t acc[3] = {0, 0, 0};
+      int32_t acc[3] = {0, 0, 0};  // below 255 * den_c < 2^31 (checked on the host)
       for (int dy = 0; dy < a.fy; ++dy)
         for (int dx = 0; dx < a.fx; ++dx) {
           const int32_t* q = S + ((int64_t)(y * a.fy + dy) * a.sums_w + (x * a.fx + dx)) * 3;
@@ -284,9 +310,9 @@ __device__ __forceinline__ void stage_first(const ConvArgs& a, T* in, int64_t s,
 #pragma unroll
       for (int c = 0; c < 3; ++c) {
         // (S / den) / 127.5 - 1 = (2 S - den255) / den255, rounded once (exact ties included)
-        const int64_t num = 2 * acc[c] - a.den255;
+        const int64_t num = 2 * (int64_t)acc[c] - a.den255;
         if constexpr (X::SPLIT) {
-          v[c] = f32div ? div_to_bf16_bits((int32_t)num, (int32_t)a.den255)
+          v[c] = f32div ? div_to_bf16_bits_fast((int32_t)num, (int32_t)a.den255, inv)
                         : X::from_f64((double)num / (double)a.den255);
         } else {
           v[c] = X::from_f64((double)num / (double)a.den255);
@@ -482,11 +508,16 @@ __device__ __forceinline__ void inner_tile(const T* in, const T* wl, int w_lds, 
 template <int NT>
 __device__ __forceinline__ void inner_tile32_b(const uint16_t* in, const bf16x8 (&bw)[9][NT],
                                                int cin_lds, int lo_plane, int band_w, int row0,
-                                               int col0, int g, f32x4 (&acc)[NT]) {
+                                               int col0, int g, f32x4 (&acc)[NT]);
+
+// The same from the lane's address of tap (0, 0) (hi plane, its K chunk).
+template <int NT>
+__device__ __forceinline__ void inner_tile32_b_at(const uint16_t* base, const bf16x8 (&bw)[9][NT],
+                                                  int cin_lds, int lo_plane, int band_w,
+                                                  f32x4 (&acc)[NT]) {
   using X = Elt<uint16_t>;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const uint16_t* base = in + (row0 * band_w + col0) * cin_lds + g * 8;
   bf16x8 av[2], av_lo[2];
   av[0] = X::load(base);
   av_lo[0] = X::load(base + lo_plane);
@@ -506,6 +537,14 @@ __device__ __forceinline__ void inner_tile32_b(const uint16_t* in, const bf16x8 
     for (int nt = 0; nt < NT; ++nt) acc[nt] = X::mma(av_lo[cur], bw[tap][nt], acc[nt]);
     __builtin_amdgcn_sched_barrier(0);
   }
+}
+
+template <int NT>
+__device__ __forceinline__ void inner_tile32_b(const uint16_t* in, const bf16x8 (&bw)[9][NT],
+                                               int cin_lds, int lo_plane, int band_w, int row0,
+                                               int col0, int g, f32x4 (&acc)[NT]) {
+  inner_tile32_b_at<NT>(in + (row0 * band_w + col0) * cin_lds + g * 8, bw, cin_lds, lo_plane,
+                        band_w, acc);
 }
 
 template <typename T, int NT, bool G>
@@ -571,6 +610,33 @@ __global__ void __launch_bounds__(256) k_conv(ConvArgs a) {
 struct PairArgs {
   int32_t off_w1, off_in0, off_in1;  // LDS offsets (bf16 elements) of w1, in0, in1
 };
+
+// The value of lane l + 1 of each 16-lane row (DPP row shift; the last lane
+// of a row gets 0).
+__device__ __forceinline__ float row_next(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x101, 0xF, 0xF, false));
+}
+
+// The same epilogue with the lane's store address precomputed: p is the lane's
+// channel m at the tile's pooled pixel in the hi plane.
+template <int NT>
+__device__ __forceinline__ void pair_epilogue_at(const f32x4 (&acc)[NT], const float (&bias)[NT],
+                                                 uint16_t* p, bool store, int lo_plane) {
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    float v = 0.0f;  // ReLU floor
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v = fmaxf(v, acc[nt][r] + bias[nt]);
+    // even lanes store channels n, n + 1 (the odd neighbour's value) as dwords
+    const float v1 = row_next(v);
+    uint32_t hi, lo;
+    Elt<uint16_t>::split2(v, v1, hi, lo);
+    if (store) {
+      *reinterpret_cast<uint32_t*>(p + nt * 16) = hi;
+      *reinterpret_cast<uint32_t*>(p + nt * 16 + lo_plane) = lo;
+    }
+  }
+}
 
 // Bias, ReLU and 2x2 max-pool of one first-layer tile, stored as hi / lo bf16
 // at (oy + 1, ox + 1) of the second layer's band (row / column 0 are halo).
@@ -660,11 +726,30 @@ __global__ void __launch_bounds__(1024) k_conv_pair(ConvArgs a0, ConvArgs a1, Pa
 #pragma unroll
         for (int nt = 0; nt < NT0; ++nt)
           bw0[ks][nt] = X::load(w0 + (nt * 16 + m) * a0.w_lds + ks * 32 + g * 8);
+      // per-lane parts of the addresses; a tile adds wave-uniform offsets.
+      // K steps 0 and 1 of lane group g start at K = 8 g and 32 + 8 g, i.e.
+      // at tap (dy, dx) = (k / 16, k / 4 mod 4) of the lane's pixel (py, px);
+      // step 1 is past K = 48 (zero weights) for lane groups 2 and 3.
+      const int k1 = 32 + g * 8;
+      const int in_l0 = ((py + (g >> 1)) * a0.band_w + px + 2 * (g & 1)) * 4;
+      const int in_l1 = ((py + (k1 >> 4)) * a0.band_w + px + ((k1 >> 2) & 3)) * 4;
+      const bool use1 = k1 < 48;
+      const int out_l = (((g >> 1) + 1) * a1.band_w + (g & 1) + 1) * a1.cin_lds + m;
       for (int t = wave; t < a0.tiles_y * a0.tiles_x; t += nwaves) {
         const int ty = t / a0.tiles_x, tx = t - ty * a0.tiles_x;
+        const uint16_t* tin = in0 + (4 * ty * a0.band_w + 4 * tx) * 4;
+        const bf16x8 x0 = X::load8(tin + in_l0);
+        const bf16x8 x1 = use1 ? X::load8(tin + in_l1) : X::zero();
         f32x4 acc[NT0];
-        first_tile_b<NT0>(in0, bw0, a0.band_w, 4 * ty + py, 4 * tx + px, g, acc);
-        pair_epilogue<NT0>(a1, acc, bias0, in1, ty, tx, ho0, wo0, m, g);
+#pragma unroll
+        for (int nt = 0; nt < NT0; ++nt) {
+          acc[nt] = X::mma(x0, bw0[0][nt], f32x4{0.f, 0.f, 0.f, 0.f});
+          acc[nt] = X::mma(x1, bw0[1][nt], acc[nt]);
+        }
+        const int oy = 2 * ty + (g >> 1), ox = 2 * tx + (g & 1);
+        const bool store = oy < ho0 && ox < wo0 && (m & 1) == 0;
+        pair_epilogue_at<NT0>(acc, bias0, in1 + (2 * ty * a1.band_w + 2 * tx) * a1.cin_lds + out_l,
+                              store, a1.lo_plane);
       }
     } else {
       for (int t = wave; t < a0.tiles_y * a0.tiles_x; t += nwaves) {
@@ -683,12 +768,20 @@ __global__ void __launch_bounds__(1024) k_conv_pair(ConvArgs a0, ConvArgs a1, Pa
 #pragma unroll
         for (int nt = 0; nt < NT1; ++nt)
           bw1[tap][nt] = X::load(w1 + (nt * 16 + m) * a1.w_lds + tap * 32 + g * 8);
+      const int in_l = (py * a1.band_w + px) * a1.cin_lds + g * 8;  // per-lane address parts
+      const int out_l = ((g >> 1) * wo1 + (g & 1)) * a1.cout + m;
       for (int t = wave; t < a1.tiles_y * a1.tiles_x; t += nwaves) {
         const int ty = t / a1.tiles_x, tx = t - ty * a1.tiles_x;
         f32x4 acc[NT1];
-        inner_tile32_b<NT1>(in1, bw1, a1.cin_lds, a1.lo_plane, a1.band_w, 4 * ty + py,
-                            4 * tx + px, g, acc);
-        conv_epilogue<NT1>(a1, acc, bias1, out, ty, tx, ho1, wo1, m, g);
+        inner_tile32_b_at<NT1>(in1 + (4 * ty * a1.band_w + 4 * tx) * a1.cin_lds + in_l, bw1,
+                               a1.cin_lds, a1.lo_plane, a1.band_w, acc);
+        if (a1.pool) {
+          const bool inside = 2 * ty + (g >> 1) < ho1 && 2 * tx + (g & 1) < wo1;
+          pool_epilogue_at<NT1>(acc, bias1, out + (2 * ty * wo1 + 2 * tx) * a1.cout + out_l,
+                                inside);
+        } else {
+          conv_epilogue<NT1>(a1, acc, bias1, out, ty, tx, ho1, wo1, m, g);
+        }
       }
     } else {
       for (int t = wave; t < a1.tiles_y * a1.tiles_x; t += nwaves) {
@@ -1003,7 +1096,7 @@ k_band64(ConvArgs a, Band64 b) {
 // frame idx[s], correctly rounded, and a zero channel 3.
 __device__ __forceinline__ uint2 first_input_bf16(const ConvArgs& a, int64_t s, int y, int x) {
   const int32_t* S = a.sums + (int64_t)a.idx[s] * a.sums_h * a.sums_w * 3;
-  int64_t acc[3] = {0, 0, 0};
+  int32_t acc[3] = {0, 0, 0};  // below 255 * den_c < 2^31 (checked on the host)
   for (int dy = 0; dy < a.fy; ++dy)
     for (int dx = 0; dx < a.fx; ++dx) {
       const int32_t* q = S + ((int64_t)(y * a.fy + dy) * a.sums_w + (x * a.fx + dx)) * 3;
@@ -1013,10 +1106,11 @@ __device__ __forceinline__ uint2 first_input_bf16(const ConvArgs& a, int64_t s, 
     }
   uint16_t v[3];
   const bool f32div = a.den255 < (1 << 24);
+  const float inv = 1.0f / (float)a.den255;
 #pragma unroll
   for (int c = 0; c < 3; ++c) {
-    const int64_t num = 2 * acc[c] - a.den255;
-    v[c] = f32div ? div_to_bf16_bits((int32_t)num, (int32_t)a.den255)
+    const int64_t num = 2 * (int64_t)acc[c] - a.den255;
+    v[c] = f32div ? div_to_bf16_bits_fast((int32_t)num, (int32_t)a.den255, inv)
                   : f64_to_bf16_bits((double)num / (double)a.den255);
   }
   return make_uint2((uint32_t)v[0] | ((uint32_t)v[1] << 16), (uint32_t)v[2]);
@@ -1197,36 +1291,40 @@ struct DenseArgs {
   int64_t per_cam;
 };
 
-// Waves of a dense workgroup: they split K, so that a group of 16 survivors
-// is a short dependence chain per wave even when there are few groups.
+// Dense workgroups: kDenseWaves waves split K (so that a group is a short
+// dependence chain per wave even when there are few groups), and each wave
+// keeps MT tiles of 16 survivors, so that every weight fragment it loads
+// serves MT x 16 survivors.  The partial sums meet in LDS (MT x NT x 4 KB per
+// wave, at most 64 KB).
+constexpr int kDenseWaves = 4;
 template <int NT>
-constexpr int dense_waves() {
-  return NT >= 16 ? 4 : 8;
+constexpr int dense_mt() {
+  return NT >= 16 ? 1 : (NT >= 8 ? 2 : 4);
 }
 
 template <typename T, int NT, bool G>
-__global__ void __launch_bounds__(512) k_dense(DenseArgs a) {
+__global__ void __launch_bounds__(64 * kDenseWaves) k_dense(DenseArgs a) {
   using X = Elt<T>;
   constexpr int E = X::E, KS = X::KS;
   constexpr bool SPLIT = X::SPLIT;
-  constexpr int NW = dense_waves<NT>();
-  // per wave and output tile, each lane's 4 partial sums
-  __shared__ f32x4 part[NW][NT][64];
+  constexpr int NW = kDenseWaves, MT = dense_mt<NT>(), R = 16 * MT;  // rows of a group
+  // per wave, row tile and output tile, each lane's 4 partial sums
+  __shared__ f32x4 part[NW][MT][NT][64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int m = lane & 15, g = lane >> 4;
   int64_t cnt = *a.count;
   if (cnt > a.max_count) cnt = a.max_count;
-  const int64_t groups = (cnt + 15) / 16;
+  const int64_t groups = (cnt + R - 1) / R;
   const int nks = (a.flat + KS - 1) / KS;  // K steps
   const int ks0 = wave * nks / NW, ks1 = (wave + 1) * nks / NW;
   // camera of survivor slot u of a camera group (slots are in frame order, so
   // a group's cameras are non-decreasing)
   auto cam_of = [&](int64_t u) -> int64_t { return a.idx[u] / a.per_cam; };
   for (int64_t grp = blockIdx.x; grp < groups; grp += gridDim.x) {
-    // A group of 16 slots runs once per camera among its rows (once without a
-    // camera group), each pass with that camera's weights over its own rows.
-    int64_t cam = G ? cam_of(grp * 16) : 0;
+    // A group runs once per camera among its rows (once without a camera
+    // group), each pass with that camera's weights over its own rows.
+    int64_t cam = G ? cam_of(grp * R) : 0;
     for (;;) {
       int64_t off = 0;
       float b2 = a.b2;
@@ -1241,56 +1339,68 @@ __global__ void __launch_bounds__(512) k_dense(DenseArgs a) {
       const T* w1 = at_off(reinterpret_cast<const T*>(a.w1), off);
       const float* b1 = at_off(a.b1, off);
       const float* w2 = at_off(a.w2, off);
-      const int64_t s = grp * 16 + m;
-      const bool valid = s < cnt && (!G || cam_of(s) == cam);
-      const float* arow = a.feat + (valid ? s : 0) * (int64_t)a.flat + g * E;
-      f32x4 acc[NT], acc_lo[NT];
+      bool valid[MT];
+      const float* arow[MT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        acc_lo[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int mt = 0; mt < MT; ++mt) {
+        const int64_t s = grp * R + mt * 16 + m;
+        valid[mt] = s < cnt && (!G || cam_of(s) == cam);
+        arow[mt] = a.feat + (valid[mt] ? s : 0) * (int64_t)a.flat + g * E;
       }
+      f32x4 acc[MT][NT];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
       // flat is a multiple of 16 (and of E): a lane group's E values of the last,
-      // partial K step are either all inside or all past the end (zero)
+      // partial K step are either all inside or all past the end (zero); the
+      // hi and lo products of a bf16 network share the accumulators
       for (int ks = ks0; ks < ks1; ++ks) {
         const int k0 = ks * KS;
         const bool kin = k0 + g * E < a.flat;
-        typename X::frag av = X::zero(), av_lo = X::zero();
-        if constexpr (SPLIT) {
-          if (valid && kin) X::split8(arow + k0, av, av_lo);
-        } else {
-          if (valid && kin) av = arow[k0];
-        }
+        typename X::frag bv[NT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-          typename X::frag bv = X::zero();
-          if (kin) bv = X::load(w1 + (int64_t)(nt * 16 + m) * a.flat + k0 + g * E);
-          acc[nt] = X::mma(av, bv, acc[nt]);
-          if constexpr (SPLIT) acc_lo[nt] = X::mma(av_lo, bv, acc_lo[nt]);
+          bv[nt] = X::zero();
+          if (kin) bv[nt] = X::load(w1 + (int64_t)(nt * 16 + m) * a.flat + k0 + g * E);
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          typename X::frag av = X::zero(), av_lo = X::zero();
+          if constexpr (SPLIT) {
+            if (valid[mt] && kin) X::split8(arow[mt] + k0, av, av_lo);
+          } else {
+            if (valid[mt] && kin) av = arow[mt][k0];
+          }
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            acc[mt][nt] = X::mma(av, bv[nt], acc[mt][nt]);
+            if constexpr (SPLIT) acc[mt][nt] = X::mma(av_lo, bv[nt], acc[mt][nt]);
+          }
         }
       }
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        if constexpr (SPLIT) acc[nt] += acc_lo[nt];
-        part[wave][nt][lane] = acc[nt];
-      }
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) part[wave][mt][nt][lane] = acc[mt][nt];
       __syncthreads();
-      if (wave == 0) {
+      // wave w finishes row tiles w, w + NW, ...
+      for (int mt = wave; mt < MT; mt += NW) {
+        f32x4 t[NT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-          f32x4 t = part[0][nt][lane];
+          t[nt] = part[0][mt][nt][lane];
 #pragma unroll
-          for (int w = 1; w < NW; ++w) t += part[w][nt][lane];
-          acc[nt] = t;
+          for (int w = 1; w < NW; ++w) t[nt] += part[w][mt][nt][lane];
         }
-        // hidden = ReLU(acc + b1); z = b2 + sum_n w2[n] * hidden[n]
+        // hidden = ReLU(t + b1); z = b2 + sum_n w2[n] * hidden[n]
         float sum[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
           const int n = nt * 16 + m;
           const float b = b1[n], w = w2[n];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) sum[r] += w * fmaxf(acc[nt][r] + b, 0.0f);
+          for (int r = 0; r < 4; ++r) sum[r] += w * fmaxf(t[nt][r] + b, 0.0f);
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -1300,7 +1410,7 @@ __global__ void __launch_bounds__(512) k_dense(DenseArgs a) {
         if (m == 0) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const int64_t slot = grp * 16 + 4 * g + r;
+            const int64_t slot = grp * R + mt * 16 + 4 * g + r;
             if (slot < cnt && (!G || cam_of(slot) == cam)) {
               const float z = sum[r] + b2;
               const double p = 1.0 / (1.0 + exp(-(double)z));
@@ -1319,8 +1429,8 @@ __global__ void __launch_bounds__(512) k_dense(DenseArgs a) {
       if constexpr (!G) break;
       // the next camera among the group's rows (uniform)
       int64_t next = -1;
-      for (int r = 0; r < 16 && next < 0; ++r) {
-        const int64_t u = grp * 16 + r;
+      for (int r = 0; r < R && next < 0; ++r) {
+        const int64_t u = grp * R + r;
         if (u < cnt && cam_of(u) > cam) next = cam_of(u);
       }
       if (next < 0) break;
@@ -1363,11 +1473,9 @@ int launch_dense_nt(int nt, const DenseArgs& a, unsigned grid, hipStream_t st) {
 #define NSC_DENSE_CASE(N)                                                                      \
   case N:                                                                                      \
     if (a.nets)                                                                                \
-      hipLaunchKernelGGL((k_dense<T, N, true>), dim3(grid), dim3(64 * dense_waves<N>()), 0, st, \
-                         a);                                                                   \
+      hipLaunchKernelGGL((k_dense<T, N, true>), dim3(grid), dim3(64 * kDenseWaves), 0, st, a);   \
     else                                                                                       \
-      hipLaunchKernelGGL((k_dense<T, N, false>), dim3(grid), dim3(64 * dense_waves<N>()), 0,   \
-                         st, a);                                                               \
+      hipLaunchKernelGGL((k_dense<T, N, false>), dim3(grid), dim3(64 * kDenseWaves), 0, st, a);  \
     break;
   switch (nt) {
     NSC_DENSE_CASE(1)
@@ -1749,11 +1857,12 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
   d.c_high = r.c_high;
   d.nets = r.nets;
   d.per_cam = r.per_cam;
-  int64_t groups = (r.max_count + 15) / 16;  // one workgroup per 16-survivor group
+  const int nt = cnn.dense / 16;
+  const int64_t rows = nt >= 16 ? 16 : (nt >= 8 ? 32 : 64);  // 16 x dense_mt<NT>()
+  int64_t groups = (r.max_count + rows - 1) / rows;  // one workgroup per group of rows
   int64_t grid = groups;
   if (grid > kNumCU * 2) grid = kNumCU * 2;
   if (grid < 1) grid = 1;
-  const int nt = cnn.dense / 16;
   return cnn.bf16 ? launch_dense_nt<uint16_t>(nt, d, (unsigned)grid, stream)
                   : launch_dense_nt<float>(nt, d, (unsigned)grid, stream);
 }
