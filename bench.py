@@ -121,6 +121,28 @@ def measured_traffic(workload: str):
     return float(t["traffic_bytes"]), os.path.relpath(path, ROOT)
 
 
+CNN_SOURCES = ("paper_1703_02529_amd/csrc/cnn.hip", "paper_1703_02529_amd/csrc/nsc_internal.h")
+CNN_KERNELS = "k_conv,k_prep_input,k_pair64,k_band64,k_dense"
+
+
+def measured_mfma_busy(workload: str):
+    """Matrix-core busy fraction of the CNN stage (rocprofv3 counters: issued
+    MFMA cycles over the stage's SIMD-cycles, hi / lo passes and K padding
+    included) from the committed counter summary, or None when there is none
+    or the kernels' sources changed since."""
+    from paper_1703_02529_amd.profsum import sources_hash
+
+    path = os.path.join(ROOT, "profiles", f"mfma_{workload}.json")
+    if not os.path.exists(path):
+        return None, "no counter summary"
+    with open(path) as fh:
+        t = json.load(fh)
+    now = sources_hash([os.path.join(ROOT, p) for p in CNN_SOURCES])
+    if t.get("sources_sha256_16") != now:
+        return None, "kernel sources changed since the counters were taken"
+    return float(t["stage_mfma_busy"]), os.path.relpath(path, ROOT)
+
+
 def copy_calibration(torch, dev):
     """A plain copy (negation) of COPY_BYTES bytes: the reference point that
     scales the FETCH_SIZE / WRITE_SIZE counters of a profiled run."""
@@ -576,6 +598,7 @@ def bench_chunked(args):
     area_ms, cnn_ms = float(stage[0]), float(stage[3])
     achieved = n * fb / (area_ms * 1e-3) / 1e9
     cnn_tflops = fired * cnn_flops(wl.cnn) / (cnn_ms * 1e-3) / 1e12 if cnn_ms > 0 else 0.0
+    busy, busy_src = measured_mfma_busy(wl.name)
     layers = ", ".join(f"{c}{'+pool' if p else ''}" for c, p in zip(wl.cnn.conv, wl.cnn.pool))
     result = {
         "metric": "cascade frames/sec on 1 MI355X + % HBM roofline (diff) / % MFMA peak (CNN)",
@@ -619,7 +642,8 @@ def bench_chunked(args):
                      "frac": cnn_tflops / BF16_PEAK_TFLOPS,
                      "measured_peak_tflops": peaks["mfma_bf16_tflops"],
                      "frac_of_measured": cnn_tflops / peaks["mfma_bf16_tflops"],
-                     "flop_per_survivor": cnn_flops(wl.cnn), "survivors": fired},
+                     "flop_per_survivor": cnn_flops(wl.cnn), "survivors": fired,
+                     "busy_counter": busy, "busy_source": busy_src},
         "cascade_only_ms": casc_ms,
         "overlapped_wall_ms": wall_ms,
         "overlapped_wall_fps": n / (wall_ms * 1e-3),
@@ -739,6 +763,7 @@ def main():
     cnn_ms = float(stage[:, 3].mean())
     fired = int(stats["fired"])
     cnn_tflops = fired * cnn_flops(wl.cnn) / (cnn_ms * 1e-3) / 1e12 if cnn_ms > 0 else 0.0
+    busy, busy_src = measured_mfma_busy(W.VGA.name)  # the network does not depend on the metric
 
     result = {
         "metric": "cascade frames/sec on 1 MI355X + % HBM roofline (diff) / % MFMA peak (CNN)",
@@ -798,6 +823,8 @@ def main():
             "frac_of_measured": cnn_tflops / peaks["mfma_bf16_tflops"],
             "flop_per_survivor": cnn_flops(wl.cnn),
             "survivors": fired,
+            "busy_counter": busy,
+            "busy_source": busy_src,
         },
     }
     del frames

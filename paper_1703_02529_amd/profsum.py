@@ -1,6 +1,6 @@
 """Summaries of rocprofv3 CSV output for the committed profile notes.
 
-Two sub-commands, both reading the CSV files rocprofv3 writes with
+Three sub-commands, each reading the CSV files rocprofv3 writes with
 ``--output-format csv`` under a run's output directory:
 
 ``stats DIR --title T --command C``
@@ -16,6 +16,14 @@ Two sub-commands, both reading the CSV files rocprofv3 writes with
     copy's own accounting.  The summary records a hash of the sources listed
     with ``--source`` so that a reader can tell when the kernel has changed
     since the counters were taken.
+
+``mfma DIR --kernels K1,K2,... --workload W``
+    JSON summary of the matrix-core utilisation of the kernels whose names
+    contain one of K1, K2, ... (the CNN stage), from a ``--pmc
+    SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_MFMA SQ_INSTS_VALU GRBM_GUI_ACTIVE`` run:
+    per kernel the busy fraction SQ_VALU_MFMA_BUSY_CYCLES / (cycles x SIMDs),
+    cycles being GRBM_GUI_ACTIVE / XCDs, and over the stage the same with
+    busy and cycles summed over its dispatches.
 """
 from __future__ import annotations
 
@@ -143,6 +151,50 @@ def cmd_traffic(a) -> None:
     sys.stdout.write(text)
 
 
+SIMDS = 1024  # MI355X: 256 compute units x 4 SIMDs
+XCDS = 8      # GRBM_GUI_ACTIVE counts once per XCD
+CLOCK_HZ = 2.4e9
+
+
+def cmd_mfma(a) -> None:
+    busy = _per_dispatch(a.dir, "SQ_VALU_MFMA_BUSY_CYCLES")
+    gui = _per_dispatch(a.dir, "GRBM_GUI_ACTIVE")
+    mfma = _per_dispatch(a.dir, "SQ_INSTS_MFMA")
+    valu = _per_dispatch(a.dir, "SQ_INSTS_VALU")
+    pats = [k for k in a.kernels.split(",") if k]
+    kernels, tot_busy, tot_cyc = {}, 0.0, 0.0
+    for name in sorted(busy):
+        if not any(p in name for p in pats):
+            continue
+        cyc = [g / XCDS for g in gui[name]]
+        b, c = sum(busy[name]), sum(cyc)
+        n_m, n_v = sum(mfma.get(name, [0.0])), sum(valu.get(name, [0.0]))
+        kernels[short_name(name)] = {
+            "dispatches": len(cyc),
+            "avg_ms": c / len(cyc) / CLOCK_HZ * 1e3,
+            "mfma_busy": b / (c * SIMDS) if c else None,
+            "mfma_insts_per_dispatch": n_m / len(cyc),
+            "valu_insts_per_mfma": n_v / n_m if n_m else None,
+        }
+        tot_busy += b
+        tot_cyc += c
+    res = {
+        "workload": a.workload,
+        "kernels": kernels,
+        "stage_mfma_busy": tot_busy / (tot_cyc * SIMDS) if tot_cyc else None,
+        "note": "busy = SQ_VALU_MFMA_BUSY_CYCLES / ((GRBM_GUI_ACTIVE / 8) x 1024 SIMDs): the "
+                "issued matrix-core work, hi / lo passes and K padding included",
+        "sources": sorted(os.path.relpath(p) for p in a.source),
+        "sources_sha256_16": sources_hash(a.source) if a.source else None,
+        "commands": a.command,
+    }
+    text = json.dumps(res, indent=1) + "\n"
+    if a.out:
+        with open(a.out, "w") as fh:
+            fh.write(text)
+    sys.stdout.write(text)
+
+
 def main(argv=None) -> None:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -162,8 +214,15 @@ def main(argv=None) -> None:
     t.add_argument("--source", action="append", default=[])
     t.add_argument("--command", action="append", default=[])
     t.add_argument("--out")
+    m = sub.add_parser("mfma")
+    m.add_argument("dir")
+    m.add_argument("--kernels", required=True)
+    m.add_argument("--workload", default="")
+    m.add_argument("--source", action="append", default=[])
+    m.add_argument("--command", action="append", default=[])
+    m.add_argument("--out")
     a = ap.parse_args(argv)
-    cmd_stats(a) if a.cmd == "stats" else cmd_traffic(a)
+    {"stats": cmd_stats, "traffic": cmd_traffic, "mfma": cmd_mfma}[a.cmd](a)
 
 
 if __name__ == "__main__":
