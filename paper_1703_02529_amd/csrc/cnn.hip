@@ -118,15 +118,18 @@ template <> struct Elt<uint16_t> {  // bf16 stored as raw bits
   // conversions are the hardware's packed round-to-nearest-even.
   static constexpr bool SPLIT = true;
   // two fp32 values -> (hi0, hi1) and (lo0, lo1), packed as bf16 pairs
-  static __device__ __forceinline__ void split2(float v0, float v1, bf16x2& hi, bf16x2& lo) {
-    hi = bf16x2{(__bf16)v0, (__bf16)v1};
-    lo = bf16x2{(__bf16)(v0 - (float)hi[0]), (__bf16)(v1 - (float)hi[1])};
-  }
+  // (one packed conversion for the hi pair; its fp32 values are the pair's
+  // bits moved into the upper halves)
   static __device__ __forceinline__ void split2(float v0, float v1, uint32_t& hi, uint32_t& lo) {
-    bf16x2 h, l;
+    hi = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)v0, (__bf16)v1});
+    const float h0 = __uint_as_float(hi << 16), h1 = __uint_as_float(hi & 0xFFFF0000u);
+    lo = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)(v0 - h0), (__bf16)(v1 - h1)});
+  }
+  static __device__ __forceinline__ void split2(float v0, float v1, bf16x2& hi, bf16x2& lo) {
+    uint32_t h, l;
     split2(v0, v1, h, l);
-    hi = __builtin_bit_cast(uint32_t, h);
-    lo = __builtin_bit_cast(uint32_t, l);
+    hi = __builtin_bit_cast(bf16x2, h);
+    lo = __builtin_bit_cast(bf16x2, l);
   }
   // 4 fp32 values -> 4 hi and 4 lo bf16 values, packed pairwise in uint2
   static __device__ __forceinline__ void split4(const float4& v, uint2& hi, uint2& lo) {
