@@ -987,11 +987,16 @@ __device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const fl
     float v[4] = {fmaxf(acc[nt][0] + bb.x, 0.f), fmaxf(acc[nt][1] + bb.y, 0.f),
                   fmaxf(acc[nt][2] + bb.z, 0.f), fmaxf(acc[nt][3] + bb.w, 0.f)};
     if (pool) {
-      // the four pixels of a pooling window are the four lanes of a quad
+      // the four pixels of a pooling window are the four lanes of a quad; the
+      // values are >= 0 (or -0) after the ReLU, so their maximum is the
+      // signed-integer maximum of their bits (which needs no NaN quieting of
+      // the permuted operands, and takes the permutation as a DPP operand)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        v[r] = fmaxf(v[r], quad_perm<kQuadXor1>(v[r]));
-        v[r] = fmaxf(v[r], quad_perm<kQuadXor2>(v[r]));
+        int iv = __float_as_int(v[r]);
+        iv = max(iv, __builtin_amdgcn_update_dpp(0, iv, kQuadXor1, 0xF, 0xF, false));
+        iv = max(iv, __builtin_amdgcn_update_dpp(0, iv, kQuadXor2, 0xF, 0xF, false));
+        v[r] = __int_as_float(iv);
       }
       const int qy = oy >> 1, qx = ox >> 1;
       if ((m & 3) == 0 && qy < h / 2 && qx < w / 2)
