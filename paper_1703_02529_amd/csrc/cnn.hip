@@ -1168,7 +1168,6 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
   int64_t cnt = *a0.count;
   if (cnt > a0.max_count) cnt = a0.max_count;
   const int bands = (a1.tiles_y + a1.band_tiles - 1) / a1.band_tiles;
-  const int64_t items = (cnt + 7) / 8 * 8 * bands;
   const int ho = a1.pool ? a1.h / 2 : a1.h, wo = a1.pool ? a1.w / 2 : a1.w;
   const int tx0 = (b.w + 7) / 8;      // first-layer tile columns
   const int qy = m >> 3, qx = m & 7;  // first-layer lane pixel in a 2 x 8 tile
@@ -1179,19 +1178,6 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
   const int off1 = (k1 >> 4) * xw + ((k1 >> 2) & 3);
   const bool use1 = k1 < 48;
 
-  // this workgroup's items from `it` on, skipping padding images (uniform)
-  auto next_item = [&](int64_t it, int64_t* s, int* ty0, int* nty) {
-    for (; it < items; it += gridDim.x) {
-      int bi;
-      band_item(it, bands, s, &bi);
-      if (*s < cnt) {
-        *ty0 = bi * a1.band_tiles;
-        *nty = min(a1.band_tiles, a1.tiles_y - *ty0);
-        break;
-      }
-    }
-    return it;
-  };
   // the two K chunks of first-layer tile t of a band (band row 0 = image row y0)
   auto l1_load = [&](const uint2* xs, int y0, int t, uint4 (&x)[2]) {
     const int ti = t / tx0, tj = t - ti * tx0;
@@ -1241,40 +1227,59 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     }
   };
 
-  int64_t s = 0;
-  int ty0 = 0, nty = 0;
-  int64_t item = next_item(blockIdx.x, &s, &ty0, &nty);
-  while (item < items) {
-    const int y0 = 4 * ty0 - 1;
-    const int t0n = (2 * nty + 1) * tx0;  // first-layer tiles: rows 4 nty + 2
+  // A workgroup runs the bands of an image in order (workgroup i and so one
+  // XCD takes images i, i + grid, ...): the two halo rows a band shares with
+  // the previous one (its rows 0-1, the previous band's last two) are copied
+  // inside the planes instead of being computed again.
+  const int bt = a1.band_tiles;
+  for (int64_t s = blockIdx.x; s < cnt; s += gridDim.x) {
     const uint2* xs = xin + s * (int64_t)xr * xw;
     const int64_t off = G ? slot_woff(a0.nets, a0.per_cam, a0.idx, s) : 0;  // camera group
     bias0 = at_off(a0.bias, off);
-    uint4 xc[2], xn[2];
-    if (wave < t0n) l1_load(xs, y0, wave, xc);
-    // first-layer weights for this band's first-layer phase only: an opaque
-    // zero keeps the compiler from hoisting them out of the band loop (which
-    // would hold 32 registers through the second layer)
-    int opaque = 0;
-    asm volatile("" : "+s"(opaque));
-    const bf16x8* w0p = at_off(wf0, off) + opaque + lane;
-    bf16x8 w0[2][4];
+    int prev_rows = 0;  // planes rows of the previous band (0: none)
+    for (int bi = 0; bi < bands; ++bi) {
+      const int ty0 = bi * bt;
+      const int nty = min(bt, a1.tiles_y - ty0);
+      const int y0 = 4 * ty0 - 1;
+      const int t0n = (2 * nty + 1) * tx0;   // first-layer tiles: rows 4 nty + 2
+      const int tfirst = prev_rows ? tx0 : 0;  // rows 0-1 copied after the first band
+      uint4 xc[2], xn[2];
+      if (tfirst + wave < t0n) l1_load(xs, y0, tfirst + wave, xc);
+      // first-layer weights for this band's first-layer phase only: an opaque
+      // zero keeps the compiler from hoisting them out of the band loop (which
+      // would hold 32 registers through the second layer)
+      int opaque = 0;
+      asm volatile("" : "+s"(opaque));
+      const bf16x8* w0p = at_off(wf0, off) + opaque + lane;
+      bf16x8 w0[2][4];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+      for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) w0[ks][nt] = w0p[(ks * 4 + nt) * 64];
-    __syncthreads();  // the previous band's second layer is done with the planes
-    for (int t = wave; t < t0n; t += kBandWaves) {
-      if (t + kBandWaves < t0n) l1_load(xs, y0, t + kBandWaves, xn);
-      l1_tile(w0, y0, t, xc);
-      xc[0] = xn[0];
-      xc[1] = xn[1];
+        for (int nt = 0; nt < 4; ++nt) w0[ks][nt] = w0p[(ks * 4 + nt) * 64];
+      __syncthreads();  // the previous band's second layer is done with the planes
+      if (prev_rows) {
+        // rows prev_rows - 2, prev_rows - 1 -> rows 0, 1 of every chunk plane
+        const int per = 2 * b.wb;
+        for (int u = threadIdx.x; u < 16 * per; u += blockDim.x) {
+          const int pc = u / per, e = u - pc * per;  // plane x chunk, unit in the two rows
+          const int base = ((pc >> 3) * 8 * b.cp + (pc & 7) * b.cp) * 16;
+          const uint4 v = *reinterpret_cast<const uint4*>(lds + base + ((prev_rows - 2) * b.wb + e) * 16);
+          *reinterpret_cast<uint4*>(lds + base + e * 16) = v;
+        }
+        __syncthreads();  // copied before the first layer overwrites the source rows
+      }
+      for (int t = tfirst + wave; t < t0n; t += kBandWaves) {
+        if (t + kBandWaves < t0n) l1_load(xs, y0, t + kBandWaves, xn);
+        l1_tile(w0, y0, t, xc);
+        xc[0] = xn[0];
+        xc[1] = xn[1];
+      }
+      __syncthreads();  // planes complete
+      band64_layer<NT>(lds, b, ty0, nty * a1.tiles_x, at_off(wf1, off), at_off(a1.bias, off),
+                       a1.act_out + s * (int64_t)ho * wo * a1.cout, a1.cout, a1.pool, a1.tiles_x,
+                       wave, py, px, m, g, lane);
+      prev_rows = 4 * nty + 2;
     }
-    __syncthreads();  // planes complete
-    band64_layer<NT>(lds, b, ty0, nty * a1.tiles_x, at_off(wf1, off), at_off(a1.bias, off),
-                     a1.act_out + s * (int64_t)ho * wo * a1.cout, a1.cout, a1.pool, a1.tiles_x,
-                     wave, py, px, m, g, lane);
-    item = next_item(item + gridDim.x, &s, &ty0, &nty);
   }
 }
 
