@@ -1227,58 +1227,81 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     }
   };
 
-  // A workgroup runs the bands of an image in order (workgroup i and so one
-  // XCD takes images i, i + grid, ...): the two halo rows a band shares with
-  // the previous one (its rows 0-1, the previous band's last two) are copied
-  // inside the planes instead of being computed again.
+  // The first layer of band (ty0, nty) of image s into the planes, rows
+  // 2 tfirst_row .. 4 nty + 1 (rows 0-1 taken from the previous band when
+  // tfirst_row is 1), then the second layer from them.
   const int bt = a1.band_tiles;
-  for (int64_t s = blockIdx.x; s < cnt; s += gridDim.x) {
+  auto band = [&](int64_t s, int ty0, int nty, int prev_rows) {
     const uint2* xs = xin + s * (int64_t)xr * xw;
     const int64_t off = G ? slot_woff(a0.nets, a0.per_cam, a0.idx, s) : 0;  // camera group
     bias0 = at_off(a0.bias, off);
-    int prev_rows = 0;  // planes rows of the previous band (0: none)
-    for (int bi = 0; bi < bands; ++bi) {
+    const int y0 = 4 * ty0 - 1;
+    const int t0n = (2 * nty + 1) * tx0;     // first-layer tiles: rows 4 nty + 2
+    const int tfirst = prev_rows ? tx0 : 0;  // rows 0-1 copied after an image's first band
+    uint4 xc[2], xn[2];
+    if (tfirst + wave < t0n) l1_load(xs, y0, tfirst + wave, xc);
+    // first-layer weights for this band's first-layer phase only: an opaque
+    // zero keeps the compiler from hoisting them out of the band loop (which
+    // would hold 32 registers through the second layer)
+    int opaque = 0;
+    asm volatile("" : "+s"(opaque));
+    const bf16x8* w0p = at_off(wf0, off) + opaque + lane;
+    bf16x8 w0[2][4];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) w0[ks][nt] = w0p[(ks * 4 + nt) * 64];
+    __syncthreads();  // the previous band's second layer is done with the planes
+    if (prev_rows) {
+      // rows prev_rows - 2, prev_rows - 1 -> rows 0, 1 of every chunk plane
+      const int per = 2 * b.wb;
+      for (int u = threadIdx.x; u < 16 * per; u += blockDim.x) {
+        const int pc = u / per, e = u - pc * per;  // plane x chunk, unit in the two rows
+        const int base = ((pc >> 3) * 8 * b.cp + (pc & 7) * b.cp) * 16;
+        const uint4 v = *reinterpret_cast<const uint4*>(lds + base + ((prev_rows - 2) * b.wb + e) * 16);
+        *reinterpret_cast<uint4*>(lds + base + e * 16) = v;
+      }
+      __syncthreads();  // copied before the first layer overwrites the source rows
+    }
+    for (int t = tfirst + wave; t < t0n; t += kBandWaves) {
+      if (t + kBandWaves < t0n) l1_load(xs, y0, t + kBandWaves, xn);
+      l1_tile(w0, y0, t, xc);
+      xc[0] = xn[0];
+      xc[1] = xn[1];
+    }
+    __syncthreads();  // planes complete
+    band64_layer<NT>(lds, b, ty0, nty * a1.tiles_x, at_off(wf1, off), at_off(a1.bias, off),
+                     a1.act_out + s * (int64_t)ho * wo * a1.cout, a1.cout, a1.pool, a1.tiles_x,
+                     wave, py, px, m, g, lane);
+  };
+  // Rounds of work either way: image-major (a band there skips recomputing
+  // two of its first-layer rows, counted as a tenth of its cost) or one band
+  // per item.
+  const int64_t items = (cnt + 7) / 8 * 8 * bands;
+  const int64_t im_rounds = (cnt + gridDim.x - 1) / gridDim.x * bands;
+  const int64_t bp_rounds = (items + gridDim.x - 1) / gridDim.x;
+  if (10 * im_rounds <= 11 * bp_rounds) {
+    // a workgroup runs the bands of an image in order (workgroup i, and so
+    // one XCD, takes images i, i + grid, ...), copying the two halo rows a
+    // band shares with the previous one
+    for (int64_t s = blockIdx.x; s < cnt; s += gridDim.x) {
+      int prev_rows = 0;
+      for (int bi = 0; bi < bands; ++bi) {
+        const int ty0 = bi * bt, nty = min(bt, a1.tiles_y - ty0);
+        band(s, ty0, nty, prev_rows);
+        prev_rows = 4 * nty + 2;
+      }
+    }
+  } else {
+    // few images: every (image, band) is a work item of its own (all bands of
+    // an image on one XCD, see band_item), each band computing its halo rows
+    for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
+      int64_t s;
+      int bi;
+      band_item(it, bands, &s, &bi);
+      if (s >= cnt) continue;  // workgroup-uniform
       const int ty0 = bi * bt;
-      const int nty = min(bt, a1.tiles_y - ty0);
-      const int y0 = 4 * ty0 - 1;
-      const int t0n = (2 * nty + 1) * tx0;   // first-layer tiles: rows 4 nty + 2
-      const int tfirst = prev_rows ? tx0 : 0;  // rows 0-1 copied after the first band
-      uint4 xc[2], xn[2];
-      if (tfirst + wave < t0n) l1_load(xs, y0, tfirst + wave, xc);
-      // first-layer weights for this band's first-layer phase only: an opaque
-      // zero keeps the compiler from hoisting them out of the band loop (which
-      // would hold 32 registers through the second layer)
-      int opaque = 0;
-      asm volatile("" : "+s"(opaque));
-      const bf16x8* w0p = at_off(wf0, off) + opaque + lane;
-      bf16x8 w0[2][4];
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) w0[ks][nt] = w0p[(ks * 4 + nt) * 64];
-      __syncthreads();  // the previous band's second layer is done with the planes
-      if (prev_rows) {
-        // rows prev_rows - 2, prev_rows - 1 -> rows 0, 1 of every chunk plane
-        const int per = 2 * b.wb;
-        for (int u = threadIdx.x; u < 16 * per; u += blockDim.x) {
-          const int pc = u / per, e = u - pc * per;  // plane x chunk, unit in the two rows
-          const int base = ((pc >> 3) * 8 * b.cp + (pc & 7) * b.cp) * 16;
-          const uint4 v = *reinterpret_cast<const uint4*>(lds + base + ((prev_rows - 2) * b.wb + e) * 16);
-          *reinterpret_cast<uint4*>(lds + base + e * 16) = v;
-        }
-        __syncthreads();  // copied before the first layer overwrites the source rows
-      }
-      for (int t = tfirst + wave; t < t0n; t += kBandWaves) {
-        if (t + kBandWaves < t0n) l1_load(xs, y0, t + kBandWaves, xn);
-        l1_tile(w0, y0, t, xc);
-        xc[0] = xn[0];
-        xc[1] = xn[1];
-      }
-      __syncthreads();  // planes complete
-      band64_layer<NT>(lds, b, ty0, nty * a1.tiles_x, at_off(wf1, off), at_off(a1.bias, off),
-                       a1.act_out + s * (int64_t)ho * wo * a1.cout, a1.cout, a1.pool, a1.tiles_x,
-                       wave, py, px, m, g, lane);
-      prev_rows = 4 * nty + 2;
+      band(s, ty0, min(bt, a1.tiles_y - ty0), 0);
     }
   }
 }
@@ -1304,23 +1327,28 @@ struct DenseArgs {
   int64_t per_cam;
 };
 
-// Dense workgroups: kDenseWaves waves split K (so that a group is a short
-// dependence chain per wave even when there are few groups), and each wave
-// keeps MT tiles of 16 survivors, so that every weight fragment it loads
-// serves MT x 16 survivors.  The partial sums meet in LDS (MT x NT x 4 KB per
-// wave, at most 64 KB).
-constexpr int kDenseWaves = 4;
-template <int NT>
+// Dense workgroups: NW waves split K (so that a group is a short dependence
+// chain per wave even when there are few groups), and each wave keeps MT
+// tiles of 16 survivors, so that every weight fragment it loads serves
+// MT x 16 survivors.  The partial sums meet in LDS (NW x MT x NT x 1 KB, at
+// most 64 KB).  Large batches take the blocked shape; small ones (a stream's
+// chunk with few survivors) one tile per group over more waves.
+template <int NT, bool BIG>
 constexpr int dense_mt() {
-  return NT >= 16 ? 1 : (NT >= 8 ? 2 : 4);
+  return !BIG ? 1 : (NT >= 16 ? 1 : (NT >= 8 ? 2 : 4));
 }
+template <int NT, bool BIG>
+constexpr int dense_nw() {
+  return BIG || NT >= 16 ? 4 : 8;
+}
+constexpr int64_t kDenseBig = 16384;  // max_count from which the blocked shape is used
 
-template <typename T, int NT, bool G>
-__global__ void __launch_bounds__(64 * kDenseWaves) k_dense(DenseArgs a) {
+template <typename T, int NT, bool G, bool BIG>
+__global__ void __launch_bounds__((64 * dense_nw<NT, BIG>())) k_dense(DenseArgs a) {
   using X = Elt<T>;
   constexpr int E = X::E, KS = X::KS;
   constexpr bool SPLIT = X::SPLIT;
-  constexpr int NW = kDenseWaves, MT = dense_mt<NT>(), R = 16 * MT;  // rows of a group
+  constexpr int NW = dense_nw<NT, BIG>(), MT = dense_mt<NT, BIG>(), R = 16 * MT;  // rows of a group
   // per wave, row tile and output tile, each lane's 4 partial sums
   __shared__ f32x4 part[NW][MT][NT][64];
   const int lane = threadIdx.x & 63;
@@ -1482,13 +1510,16 @@ int launch_conv_nt(int nt, const ConvArgs& a, unsigned grid, size_t lds, hipStre
 }
 
 template <typename T>
-int launch_dense_nt(int nt, const DenseArgs& a, unsigned grid, hipStream_t st) {
+int launch_dense_nt(int nt, const DenseArgs& a, bool big, unsigned grid, hipStream_t st) {
+#define NSC_DENSE_LAUNCH(N, G, B)                                                              \
+  hipLaunchKernelGGL((k_dense<T, N, G, B>), dim3(grid), dim3(64 * dense_nw<N, B>()), 0, st, a)
 #define NSC_DENSE_CASE(N)                                                                      \
   case N:                                                                                      \
-    if (a.nets)                                                                                \
-      hipLaunchKernelGGL((k_dense<T, N, true>), dim3(grid), dim3(64 * kDenseWaves), 0, st, a);   \
-    else                                                                                       \
-      hipLaunchKernelGGL((k_dense<T, N, false>), dim3(grid), dim3(64 * kDenseWaves), 0, st, a);  \
+    if (big) {                                                                                 \
+      if (a.nets) NSC_DENSE_LAUNCH(N, true, true); else NSC_DENSE_LAUNCH(N, false, true);      \
+    } else {                                                                                   \
+      if (a.nets) NSC_DENSE_LAUNCH(N, true, false); else NSC_DENSE_LAUNCH(N, false, false);    \
+    }                                                                                          \
     break;
   switch (nt) {
     NSC_DENSE_CASE(1)
@@ -1500,6 +1531,7 @@ int launch_dense_nt(int nt, const DenseArgs& a, unsigned grid, hipStream_t st) {
       return fail(NSC_E_SHAPE, "dense layer of %d units is not supported", nt * 16);
   }
 #undef NSC_DENSE_CASE
+#undef NSC_DENSE_LAUNCH
   NSC_CHECK_LAUNCH("k_dense");
   return NSC_OK;
 }
@@ -1871,13 +1903,14 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
   d.nets = r.nets;
   d.per_cam = r.per_cam;
   const int nt = cnn.dense / 16;
-  const int64_t rows = nt >= 16 ? 16 : (nt >= 8 ? 32 : 64);  // 16 x dense_mt<NT>()
+  const bool big = r.max_count >= kDenseBig;
+  const int64_t rows = !big || nt >= 16 ? 16 : (nt >= 8 ? 32 : 64);  // 16 x dense_mt
   int64_t groups = (r.max_count + rows - 1) / rows;  // one workgroup per group of rows
   int64_t grid = groups;
   if (grid > kNumCU * 2) grid = kNumCU * 2;
   if (grid < 1) grid = 1;
-  return cnn.bf16 ? launch_dense_nt<uint16_t>(nt, d, (unsigned)grid, stream)
-                  : launch_dense_nt<float>(nt, d, (unsigned)grid, stream);
+  return cnn.bf16 ? launch_dense_nt<uint16_t>(nt, d, big, (unsigned)grid, stream)
+                  : launch_dense_nt<float>(nt, d, big, (unsigned)grid, stream);
 }
 
 }  // namespace nsc
