@@ -42,6 +42,12 @@ class Workload:
     def replace(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
 
+    def with_occupancy(self, occ: float) -> "Workload":
+        """The same workload with another fraction of frames inside an object
+        episode, named with a suffix such as "-occ50" (percent)."""
+        return dataclasses.replace(self, name=f"{self.name}-occ{occ * 100:g}",
+                                   video=dataclasses.replace(self.video, occupancy=occ))
+
 
 def _cnn(conv, pool, dense, bf16, hw=50):
     return CNNSpec(in_h=hw, in_w=hw, conv=tuple(conv), pool=tuple(pool), dense=dense, bf16=bf16)
@@ -86,6 +92,9 @@ FHD_STREAM = Workload(
     dd_h=100, dd_w=100,
     cnn=_cnn((64, 64, 64, 64), (False, True, False, True), 128, bf16=True),
     ref_mode=PREV, delta=30, grid=(10, 10), delta_diff=0.0, weight_seed=1005, chunk=4096)
+
+# the streamed workload's occupancy sweep: 1 %, 10 % (FHD_STREAM itself) and 50 %
+FHD_OCCUPANCIES = (0.01, 0.1, 0.5)
 
 ALL = [TINY, VGA, HD_REF, HD_BLOCKED, FHD_STREAM]
 BY_NAME = {w.name: w for w in ALL}

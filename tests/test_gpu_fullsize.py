@@ -131,10 +131,12 @@ def test_hd_full_length_in_chunks(wl, chunk):
     torch.cuda.empty_cache()
 
 
-def test_fhd_1m_streamed():
+@pytest.mark.parametrize("occ", W.FHD_OCCUPANCIES, ids=lambda o: f"occ{o * 100:g}")
+def test_fhd_1m_streamed(occ):
     """The million-frame 1080p video in chunks of 4096 through two frame buffers
-    on two streams (the generator fills one while the cascade reads the other)."""
-    wl = W.FHD_STREAM
+    on two streams (the generator fills one while the cascade reads the other),
+    at each occupancy of the sweep."""
+    wl = W.FHD_STREAM if occ == W.FHD_STREAM.video.occupancy else W.FHD_STREAM.with_occupancy(occ)
     n = wl.video.n
     v = synth.Video(wl.video)
     blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))

@@ -359,8 +359,11 @@ def _run_and_compare_from_zero_window(wl, t0, n):
 
 
 @pytest.mark.parametrize("wl,lead,n", [(W.HD_REF, 4, 14), (W.HD_BLOCKED, 4, 16),
-                                       (W.FHD_STREAM, 2, 40)],
-                         ids=["hd-ref", "hd-blocked", "fhd-blocked"])
+                                       (W.FHD_STREAM, 2, 40),
+                                       (W.FHD_STREAM.with_occupancy(0.01), 2, 40),
+                                       (W.FHD_STREAM.with_occupancy(0.5), 2, 40)],
+                         ids=["hd-ref", "hd-blocked", "fhd-blocked", "fhd-blocked-occ1",
+                              "fhd-blocked-occ50"])
 def test_cascade_large_windows(wl, lead, n):
     t0 = _first_occupied(wl, lead)
     rep = _run_and_compare_from_zero_window(wl, t0, n)
