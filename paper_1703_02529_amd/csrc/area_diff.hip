@@ -340,18 +340,99 @@ struct DiffSums {
   }
 };
 
+// Blocked score by rows: a wave streams the frame row by row, lane l taking
+// values l + 64 j of each row (coalesced), whose block column is fixed; the
+// lane keeps one partial sum per slot j over a block row's rows, and at the
+// end of the block row the slots are added into per-block LDS sums (64-bit
+// LDS atomics, exact), from which lane bx computes block bx's metric.  Rows
+// of up to 64 x kDiffSlots values and up to 64 block columns.
+constexpr int kDiffSlots = 6;
+
+struct BlockRowSums {  // one wave's sums of the block row in progress
+  unsigned long long e[64], s[64], r[64];
+};
+
+template <int M, int J>  // J = slots per lane: rows of 64 (J - 1) + 1 .. 64 J values
+__device__ __forceinline__ double blocked_score_rows(const int32_t* __restrict__ cur,
+                                                     const int32_t* __restrict__ ref,
+                                                     const DiffArgs& a, int32_t grid_h,
+                                                     int32_t grid_w, const float* lr_w,
+                                                     double lr_b, int lane, BlockRowSums* bs) {
+#pragma clang fp contract(off)
+  const int rl = a.dd_w * 3;  // values per row
+  // every lane loads all J slots (from value 0 where a slot is past the row,
+  // counted as no difference) so that the loads of a row issue together
+  int bxs[J], off[J];         // block column (-1: none) and offset of each slot's value
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int c = lane + 64 * j;
+    bxs[j] = c < rl ? ((c / 3 + 1) * grid_w - 1) / a.dd_w : -1;
+    off[j] = c < rl ? c : 0;
+  }
+  double z = lr_b;
+  for (int by = 0; by < grid_h; ++by) {
+    const int y0 = (int)((int64_t)by * a.dd_h / grid_h);
+    const int y1 = (int)((int64_t)(by + 1) * a.dd_h / grid_h);
+    DiffSums<M> acc[J];
+#pragma unroll 2
+    for (int y = y0; y < y1; ++y) {
+      const int32_t* cr = cur + (int64_t)y * rl;
+      const int32_t* rr = ref + (int64_t)y * rl;
+      int32_t xv[J], yv[J];
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        xv[j] = cr[off[j]];
+        yv[j] = rr[off[j]];
+      }
+#pragma unroll
+      for (int j = 0; j < J; ++j) acc[j].add(bxs[j] >= 0 ? xv[j] : 0, bxs[j] >= 0 ? yv[j] : 0);
+    }
+    if (lane < grid_w) {
+      bs->e[lane] = 0;
+      bs->s[lane] = 0;
+      bs->r[lane] = 0;
+    }
+    __syncwarp();  // cleared before the adds
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      if (bxs[j] < 0) continue;
+      if constexpr (M != NSC_METRIC_SAD) atomicAdd(&bs->e[bxs[j]], (unsigned long long)acc[j].e);
+      if constexpr (M == NSC_METRIC_SAD) atomicAdd(&bs->s[bxs[j]], (unsigned long long)acc[j].s);
+      if constexpr (M == NSC_METRIC_NRMSE)
+        atomicAdd(&bs->r[bxs[j]], (unsigned long long)acc[j].r);
+    }
+    __syncwarp();  // block sums complete
+    double m = 0.0;
+    if (lane < grid_w) {
+      DiffSums<M> b;
+      b.e = (int64_t)bs->e[lane];
+      b.s = (int64_t)bs->s[lane];
+      b.r = (int64_t)bs->r[lane];
+      const int x0 = (int)((int64_t)lane * a.dd_w / grid_w);
+      const int x1 = (int)((int64_t)(lane + 1) * a.dd_w / grid_w);
+      const double ncell = ((double)(y1 - y0) * (double)(x1 - x0)) * 3.0;
+      m = b.value(a, ncell);
+    }
+    __syncwarp();  // sums read before the next block row clears them
+    // in block order, as separate multiplies and adds
+    for (int bx = 0; bx < grid_w; ++bx) z = z + (double)lr_w[by * grid_w + bx] * __shfl(m, bx, 64);
+  }
+  return z;
+}
+
 // The detector score of one frame (area sums `cur`) against its reference
 // `ref`, by one wave: the metric over the whole grid, or the logistic score of
 // the per-block metrics (blocks in row-major order, weights lr_w).
-template <int M>
+template <int M, bool BLK>  // BLK: blocked grids possible (else grid_h = grid_w = 1)
 __device__ __forceinline__ double frame_score(const int32_t* cur, const int32_t* ref,
                                               const DiffArgs& a, int32_t grid_h, int32_t grid_w,
-                                              const float* lr_w, double lr_b, int lane) {
+                                              const float* lr_w, double lr_b, int lane,
+                                              BlockRowSums* bs) {
   // the blocked score is summed with separate multiplies and adds, in block
   // order, so it is reproducible bit for bit
 #pragma clang fp contract(off)
   const int64_t cells = (int64_t)a.dd_h * a.dd_w * 3;
-  if (grid_h * grid_w == 1) {
+  if (!BLK || grid_h * grid_w == 1) {
     DiffSums<M> acc;
     if ((cells & 3) == 0 && (((uintptr_t)cur | (uintptr_t)ref) & 15) == 0) {
       const int4* c4 = reinterpret_cast<const int4*>(cur);
@@ -368,6 +449,23 @@ __device__ __forceinline__ double frame_score(const int32_t* cur, const int32_t*
     }
     acc.reduce();
     return acc.value(a, (double)cells);
+  }
+  if constexpr (!BLK) return 0.0;
+  if (grid_w <= 64 && a.dd_w * 3 <= 64 * kDiffSlots) {
+    switch ((a.dd_w * 3 + 63) / 64) {
+#define NSC_ROWS_CASE(J) \
+  case J:                \
+    return blocked_score_rows<M, J>(cur, ref, a, grid_h, grid_w, lr_w, lr_b, lane, bs);
+      NSC_ROWS_CASE(1)
+      NSC_ROWS_CASE(2)
+      NSC_ROWS_CASE(3)
+      NSC_ROWS_CASE(4)
+      NSC_ROWS_CASE(5)
+      NSC_ROWS_CASE(6)
+#undef NSC_ROWS_CASE
+      default:
+        break;
+    }
   }
   double z = lr_b;
   for (int by = 0; by < grid_h; ++by) {
@@ -393,8 +491,9 @@ __device__ __forceinline__ double frame_score(const int32_t* cur, const int32_t*
   return z;
 }
 
-template <int M>
+template <int M, bool BLK>
 __global__ void __launch_bounds__(256) k_diff(DiffArgs a) {
+  __shared__ BlockRowSums bsums[4];
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (i >= a.n) return;
@@ -411,7 +510,8 @@ __global__ void __launch_bounds__(256) k_diff(DiffArgs a) {
       ref = a.sums + (i - a.delta) * cells;
     else
       ref = a.prev_sums + i * cells;  // frame t - delta = t0 - delta + i
-    score = frame_score<M>(cur, ref, a, a.grid_h, a.grid_w, a.lr_w, a.lr_b, lane);
+    score = frame_score<M, BLK>(cur, ref, a, a.grid_h, a.grid_w, a.lr_w, a.lr_b, lane,
+                          &bsums[threadIdx.x >> 6]);
   }
   if (lane == 0) {
     a.fire[i] = (forced || score > a.delta_diff) ? 1 : 0;
@@ -425,6 +525,7 @@ __global__ void __launch_bounds__(256) k_diff(DiffArgs a) {
 // the camera's state slot.
 template <int M>
 __global__ void __launch_bounds__(256) k_diff_group(DiffArgs a) {
+  __shared__ BlockRowSums bsums[4];
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (i >= a.n) return;
@@ -444,7 +545,8 @@ __global__ void __launch_bounds__(256) k_diff_group(DiffArgs a) {
       ref = a.sums + (i - cd.delta) * cells;
     else  // frame t0 - delta + j, kept in the camera's state
       ref = reinterpret_cast<const int32_t*>(a.state + cam * a.state_stride) + j * cells;
-    score = frame_score<M>(cur, ref, a, cd.grid_h, cd.grid_w, cd.lr_w, cd.lr_b, lane);
+    score = frame_score<M, true>(cur, ref, a, cd.grid_h, cd.grid_w, cd.lr_w, cd.lr_b, lane,
+                          &bsums[threadIdx.x >> 6]);
   }
   if (lane == 0) {
     a.fire[i] = (forced || score > cd.delta_diff) ? 1 : 0;
@@ -561,8 +663,10 @@ int launch_diff(const DiffArgs& a, hipStream_t stream) {
 #define NSC_DIFF_LAUNCH(M)                                                                    \
   if (a.cams)                                                                                 \
     hipLaunchKernelGGL(k_diff_group<M>, dim3((unsigned)blocks), dim3(256), 0, stream, a);     \
+  else if (a.grid_h * a.grid_w > 1)                                                           \
+    hipLaunchKernelGGL((k_diff<M, true>), dim3((unsigned)blocks), dim3(256), 0, stream, a);   \
   else                                                                                        \
-    hipLaunchKernelGGL(k_diff<M>, dim3((unsigned)blocks), dim3(256), 0, stream, a)
+    hipLaunchKernelGGL((k_diff<M, false>), dim3((unsigned)blocks), dim3(256), 0, stream, a)
   switch (a.metric) {
     case NSC_METRIC_MSE:
       NSC_DIFF_LAUNCH(NSC_METRIC_MSE);
