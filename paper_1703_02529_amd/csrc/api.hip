@@ -764,6 +764,7 @@ struct nsc_group {
   nsc_cascade_cfg geo;   // camera 0's cfg: the shared geometry and metric
   const nsc_cnn* base;   // camera 0's network: kernel plans and base weights
   int32_t max_delta;     // largest delta of an earlier-frame camera (0: none)
+  int32_t blocked;       // some camera scores a blocked grid
   int64_t slot;          // state bytes per camera
   void* dev;             // CamDiff[n_cams], then CamNet[n_cams]
   CamDiff* cams;
@@ -902,6 +903,9 @@ int nsc_group_create(const nsc_cascade_cfg* cfgs, const nsc_cnn* const* cnns, in
   g->geo = g0;
   g->base = cnns[0];
   g->max_delta = max_delta;
+  g->blocked = 0;
+  for (int32_t c = 0; c < n_cams; ++c)
+    if (cfgs[c].grid_h * cfgs[c].grid_w > 1) g->blocked = 1;
   g->slot = (int64_t)slot;
   g->dev = dev;
   g->cams = reinterpret_cast<CamDiff*>(b);
@@ -998,6 +1002,7 @@ int nsc_group_run(const nsc_group* g, const uint8_t* frames, int64_t n, int64_t 
     a.score = outs ? outs->score : nullptr;
     a.fire = fire;
     a.cams = g->cams;
+    a.cams_blocked = g->blocked;
     a.per_cam = n;
     a.state = st_bytes;
     a.state_stride = g->slot;

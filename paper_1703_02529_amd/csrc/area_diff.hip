@@ -523,7 +523,7 @@ __global__ void __launch_bounds__(256) k_diff(DiffArgs a) {
 // frames c * n .. c * n + n - 1 of the batch, each scored with its camera's
 // reference, blocks, weights and threshold; the frames before t0 come from
 // the camera's state slot.
-template <int M>
+template <int M, bool BLK>
 __global__ void __launch_bounds__(256) k_diff_group(DiffArgs a) {
   __shared__ BlockRowSums bsums[4];
   const int lane = threadIdx.x & 63;
@@ -545,7 +545,7 @@ __global__ void __launch_bounds__(256) k_diff_group(DiffArgs a) {
       ref = a.sums + (i - cd.delta) * cells;
     else  // frame t0 - delta + j, kept in the camera's state
       ref = reinterpret_cast<const int32_t*>(a.state + cam * a.state_stride) + j * cells;
-    score = frame_score<M, true>(cur, ref, a, cd.grid_h, cd.grid_w, cd.lr_w, cd.lr_b, lane,
+    score = frame_score<M, BLK>(cur, ref, a, cd.grid_h, cd.grid_w, cd.lr_w, cd.lr_b, lane,
                           &bsums[threadIdx.x >> 6]);
   }
   if (lane == 0) {
@@ -661,8 +661,10 @@ int launch_diff(const DiffArgs& a, hipStream_t stream) {
   const int64_t blocks = (a.n + 3) / 4;
   if (blocks > 0x7FFFFFFF) return fail(NSC_E_SHAPE, "too many frames in one call");
 #define NSC_DIFF_LAUNCH(M)                                                                    \
-  if (a.cams)                                                                                 \
-    hipLaunchKernelGGL(k_diff_group<M>, dim3((unsigned)blocks), dim3(256), 0, stream, a);     \
+  if (a.cams && a.cams_blocked)                                                               \
+    hipLaunchKernelGGL((k_diff_group<M, true>), dim3((unsigned)blocks), dim3(256), 0, stream, a); \
+  else if (a.cams)                                                                            \
+    hipLaunchKernelGGL((k_diff_group<M, false>), dim3((unsigned)blocks), dim3(256), 0, stream, a); \
   else if (a.grid_h * a.grid_w > 1)                                                           \
     hipLaunchKernelGGL((k_diff<M, true>), dim3((unsigned)blocks), dim3(256), 0, stream, a);   \
   else                                                                                        \

@@ -102,6 +102,7 @@ struct DiffArgs {
   double* score;             // nullable
   uint8_t* fire;
   const CamDiff* cams;       // camera group (else null)
+  int32_t cams_blocked;      // camera group: some camera scores a blocked grid
   int64_t per_cam;
   const unsigned char* state;
   int64_t state_stride;
