@@ -1327,28 +1327,67 @@ struct DenseArgs {
   int64_t per_cam;
 };
 
-// Dense workgroups: NW waves split K (so that a group is a short dependence
-// chain per wave even when there are few groups), and each wave keeps MT
-// tiles of 16 survivors, so that every weight fragment it loads serves
-// MT x 16 survivors.  The partial sums meet in LDS (NW x MT x NT x 1 KB, at
-// most 64 KB).  Large batches take the blocked shape; small ones (a stream's
-// chunk with few survivors) one tile per group over more waves.
-template <int NT, bool BIG>
-constexpr int dense_mt() {
-  return !BIG ? 1 : (NT >= 16 ? 1 : (NT >= 8 ? 2 : 4));
+// The output of one 16-survivor tile from its hidden pre-activations t (lane
+// (m, g): rows row0 + 4 g + r, units 16 nt + m): hidden = ReLU(t + b1),
+// z = b2 + sum_n w2[n] hidden[n] (a 16-lane shuffle reduction), then the
+// logit, the sigmoid and the decision at the frame's position, for the rows
+// of camera cam (every row without a camera group).
+template <int NT, bool G>
+__device__ __forceinline__ void dense_out(const DenseArgs& a, const f32x4 (&t)[NT],
+                                          const float* b1, const float* w2, float b2,
+                                          double c_low, double c_high, int64_t row0,
+                                          int64_t cnt, int64_t cam, int m, int g) {
+  float sum[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int n = nt * 16 + m;
+    const float b = b1[n], w = w2[n];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sum[r] += w * fmaxf(t[nt][r] + b, 0.0f);
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) sum[r] += __shfl_xor(sum[r], o, 64);
+  }
+  if (m == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t slot = row0 + 4 * g + r;
+      if (slot < cnt && (!G || a.idx[slot] / a.per_cam == cam)) {
+        const float z = sum[r] + b2;
+        const double p = 1.0 / (1.0 + exp(-(double)z));
+        a.logit[slot] = z;
+        if (a.prob) a.prob[slot] = (float)p;
+        if (a.dec || a.frame_logit) {
+          const int32_t f = a.idx[slot];
+          if (a.dec) a.dec[f] = p < c_low ? 0 : (p > c_high ? 1 : 2);
+          if (a.frame_logit) a.frame_logit[f] = z;
+        }
+      }
+    }
+  }
 }
-template <int NT, bool BIG>
-constexpr int dense_nw() {
-  return BIG || NT >= 16 ? 4 : 8;
-}
-constexpr int64_t kDenseBig = 16384;  // max_count from which the blocked shape is used
 
-template <typename T, int NT, bool G, bool BIG>
-__global__ void __launch_bounds__((64 * dense_nw<NT, BIG>())) k_dense(DenseArgs a) {
+// Dense workgroups for large batches (kDenseBig survivors and more): NW
+// waves split K (so that a group is a short dependence chain per wave), and
+// each wave keeps MT tiles of 16 survivors, so that every weight fragment it
+// loads serves MT x 16 survivors.  The partial sums meet in LDS
+// (NW x MT x NT x 1 KB, at most 64 KB).  Smaller batches take
+// k_dense_part / k_dense_finish below.
+template <int NT>
+constexpr int dense_mt() {
+  return NT >= 16 ? 1 : (NT >= 8 ? 2 : 4);
+}
+constexpr int kDenseWaves = 4;
+constexpr int64_t kDenseBig = 16384;  // max_count from which k_dense is used
+
+template <typename T, int NT, bool G>
+__global__ void __launch_bounds__(64 * kDenseWaves) k_dense(DenseArgs a) {
   using X = Elt<T>;
   constexpr int E = X::E, KS = X::KS;
   constexpr bool SPLIT = X::SPLIT;
-  constexpr int NW = dense_nw<NT, BIG>(), MT = dense_mt<NT, BIG>(), R = 16 * MT;  // rows of a group
+  constexpr int NW = kDenseWaves, MT = dense_mt<NT>(), R = 16 * MT;  // rows of a group
   // per wave, row tile and output tile, each lane's 4 partial sums
   __shared__ f32x4 part[NW][MT][NT][64];
   const int lane = threadIdx.x & 63;
@@ -1434,37 +1473,7 @@ __global__ void __launch_bounds__((64 * dense_nw<NT, BIG>())) k_dense(DenseArgs 
 #pragma unroll
           for (int w = 1; w < NW; ++w) t[nt] += part[w][mt][nt][lane];
         }
-        // hidden = ReLU(t + b1); z = b2 + sum_n w2[n] * hidden[n]
-        float sum[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int n = nt * 16 + m;
-          const float b = b1[n], w = w2[n];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) sum[r] += w * fmaxf(t[nt][r] + b, 0.0f);
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-#pragma unroll
-          for (int o = 1; o < 16; o <<= 1) sum[r] += __shfl_xor(sum[r], o, 64);
-        }
-        if (m == 0) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int64_t slot = grp * R + mt * 16 + 4 * g + r;
-            if (slot < cnt && (!G || cam_of(slot) == cam)) {
-              const float z = sum[r] + b2;
-              const double p = 1.0 / (1.0 + exp(-(double)z));
-              a.logit[slot] = z;
-              if (a.prob) a.prob[slot] = (float)p;
-              if (a.dec || a.frame_logit) {
-                const int32_t f = a.idx[slot];
-                if (a.dec) a.dec[f] = p < c_low ? 0 : (p > c_high ? 1 : 2);
-                if (a.frame_logit) a.frame_logit[f] = z;
-              }
-            }
-          }
-        }
+        dense_out<NT, G>(a, t, b1, w2, b2, c_low, c_high, grp * R + mt * 16, cnt, cam, m, g);
       }
       __syncthreads();  // the partial sums are read before the next pass writes them
       if constexpr (!G) break;
@@ -1473,6 +1482,151 @@ __global__ void __launch_bounds__((64 * dense_nw<NT, BIG>())) k_dense(DenseArgs 
       for (int r = 0; r < R && next < 0; ++r) {
         const int64_t u = grp * R + r;
         if (u < cnt && cam_of(u) > cam) next = cam_of(u);
+      }
+      if (next < 0) break;
+      cam = next;
+    }
+  }
+}
+
+// Small batches (a stream's chunk with a few hundred survivors): the K
+// range is split over workgroups as well, so that the few 16-survivor tiles
+// still spread over the chip and every wave's dependence chain is short.
+// k_dense_part: a (tile, K part) item per workgroup, whose 8 waves split the
+// part and add their sums through LDS into the item's partial block
+// (NT x 1 KB, lane layout of the accumulators); in a camera group each
+// camera among the tile's rows is a pass with its own weights over its own
+// rows, all passes into the same accumulators.  k_dense_finish: a wave per
+// tile adds its parts in order and applies dense_out.  Deterministic.
+constexpr int kDenseSplitItems = 1024;  // most (tile, K part) items, so the partial blocks' bound
+constexpr int kDenseSplitWaves = 8;
+
+// K parts per tile: enough items to fill the chip, at least one K step per wave.
+__device__ __forceinline__ int dense_kparts(int64_t tiles, int nks) {
+  int64_t k = kDenseSplitItems / (tiles > 0 ? tiles : 1);
+  const int64_t kmax = nks / kDenseSplitWaves > 0 ? nks / kDenseSplitWaves : 1;
+  if (k > kmax) k = kmax;
+  return k < 1 ? 1 : (int)k;
+}
+
+template <typename T, int NT, bool G>
+__global__ void __launch_bounds__(64 * kDenseSplitWaves) k_dense_part(DenseArgs a,
+                                                                      f32x4* __restrict__ part) {
+  using X = Elt<T>;
+  constexpr int E = X::E, KS = X::KS;
+  constexpr bool SPLIT = X::SPLIT;
+  constexpr int NW = kDenseSplitWaves;
+  __shared__ f32x4 red[NW][NT][64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int m = lane & 15, g = lane >> 4;
+  int64_t cnt = *a.count;
+  if (cnt > a.max_count) cnt = a.max_count;
+  const int64_t tiles = (cnt + 15) / 16;
+  const int nks = (a.flat + KS - 1) / KS;
+  const int kparts = dense_kparts(tiles, nks);
+  const int64_t items = tiles * kparts;
+  auto cam_of = [&](int64_t u) -> int64_t { return a.idx[u] / a.per_cam; };
+  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+    const int64_t tile = item / kparts;
+    const int kp = (int)(item - tile * kparts);
+    const int kb = (int)((int64_t)kp * nks / kparts), ke = (int)((int64_t)(kp + 1) * nks / kparts);
+    const int ks0 = kb + wave * (ke - kb) / NW, ks1 = kb + (wave + 1) * (ke - kb) / NW;
+    const int64_t s = tile * 16 + m;  // this lane's row (survivor slot)
+    f32x4 acc[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    int64_t cam = G ? cam_of(tile * 16) : 0;
+    for (;;) {
+      const int64_t off = G ? (int64_t)a.nets[cam].woff : 0;
+      const T* w1 = at_off(reinterpret_cast<const T*>(a.w1), off);
+      const bool valid = s < cnt && (!G || cam_of(s) == cam);
+      const float* arow = a.feat + (valid ? s : 0) * (int64_t)a.flat + g * E;
+      // as in k_dense: a lane group's E values of the last K step are all
+      // inside or all past the end; hi and lo products share the accumulators
+      for (int ks = ks0; ks < ks1; ++ks) {
+        const int k0 = ks * KS;
+        const bool kin = k0 + g * E < a.flat;
+        typename X::frag bv[NT];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          bv[nt] = X::zero();
+          if (kin) bv[nt] = X::load(w1 + (int64_t)(nt * 16 + m) * a.flat + k0 + g * E);
+        }
+        typename X::frag av = X::zero(), av_lo = X::zero();
+        if constexpr (SPLIT) {
+          if (valid && kin) X::split8(arow + k0, av, av_lo);
+        } else {
+          if (valid && kin) av = arow[k0];
+        }
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          acc[nt] = X::mma(av, bv[nt], acc[nt]);
+          if constexpr (SPLIT) acc[nt] = X::mma(av_lo, bv[nt], acc[nt]);
+        }
+      }
+      if constexpr (!G) break;
+      // the next camera among the tile's rows (uniform)
+      int64_t next = -1;
+      for (int r = 0; r < 16 && next < 0; ++r) {
+        const int64_t u = tile * 16 + r;
+        if (u < cnt && cam_of(u) > cam) next = cam_of(u);
+      }
+      if (next < 0) break;
+      cam = next;
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) red[wave][nt][lane] = acc[nt];
+    __syncthreads();
+    for (int nt = wave; nt < NT; nt += NW) {
+      f32x4 t = red[0][nt][lane];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) t += red[w][nt][lane];
+      part[(item * NT + nt) * 64 + lane] = t;
+    }
+    __syncthreads();  // red is read before the next item writes it
+  }
+}
+
+template <typename T, int NT, bool G>
+__global__ void __launch_bounds__(256) k_dense_finish(DenseArgs a, const f32x4* __restrict__ part) {
+  constexpr int KS = Elt<T>::KS;
+  const int lane = threadIdx.x & 63;
+  const int m = lane & 15, g = lane >> 4;
+  int64_t cnt = *a.count;
+  if (cnt > a.max_count) cnt = a.max_count;
+  const int64_t tiles = (cnt + 15) / 16;
+  const int kparts = dense_kparts(tiles, (a.flat + KS - 1) / KS);
+  const int64_t nw = (int64_t)gridDim.x * (blockDim.x >> 6);
+  for (int64_t tile = (int64_t)blockIdx.x * (blockDim.x >> 6) +
+                      __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+       tile < tiles; tile += nw) {
+    f32x4 t[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) t[nt] = part[((tile * kparts) * NT + nt) * 64 + lane];
+    for (int kp = 1; kp < kparts; ++kp) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) t[nt] += part[((tile * kparts + kp) * NT + nt) * 64 + lane];
+    }
+    int64_t cam = G ? a.idx[tile * 16] / a.per_cam : 0;
+    for (;;) {
+      int64_t off = 0;
+      float b2 = a.b2;
+      double c_low = a.c_low, c_high = a.c_high;
+      if constexpr (G) {
+        const CamNet& cn = a.nets[cam];
+        off = cn.woff;
+        b2 = cn.b2;
+        c_low = cn.c_low;
+        c_high = cn.c_high;
+      }
+      dense_out<NT, G>(a, t, at_off(a.b1, off), at_off(a.w2, off), b2, c_low, c_high, tile * 16,
+                       cnt, cam, m, g);
+      if constexpr (!G) break;
+      int64_t next = -1;
+      for (int r = 0; r < 16 && next < 0; ++r) {
+        const int64_t u = tile * 16 + r;
+        if (u < cnt && a.idx[u] / a.per_cam > cam) next = a.idx[u] / a.per_cam;
       }
       if (next < 0) break;
       cam = next;
@@ -1510,16 +1664,43 @@ int launch_conv_nt(int nt, const ConvArgs& a, unsigned grid, size_t lds, hipStre
 }
 
 template <typename T>
-int launch_dense_nt(int nt, const DenseArgs& a, bool big, unsigned grid, hipStream_t st) {
-#define NSC_DENSE_LAUNCH(N, G, B)                                                              \
-  hipLaunchKernelGGL((k_dense<T, N, G, B>), dim3(grid), dim3(64 * dense_nw<N, B>()), 0, st, a)
+int launch_dense_split_nt(int nt, const DenseArgs& a, f32x4* part, unsigned grid_part,
+                          unsigned grid_fin, hipStream_t st) {
+#define NSC_SPLIT_LAUNCH(N, G)                                                                  \
+  hipLaunchKernelGGL((k_dense_part<T, N, G>), dim3(grid_part), dim3(64 * kDenseSplitWaves), 0, \
+                     st, a, part);                                                              \
+  hipLaunchKernelGGL((k_dense_finish<T, N, G>), dim3(grid_fin), dim3(256), 0, st, a,           \
+                     (const f32x4*)part)
+#define NSC_SPLIT_CASE(N)                                                                       \
+  case N:                                                                                       \
+    if (a.nets) {                                                                               \
+      NSC_SPLIT_LAUNCH(N, true);                                                                \
+    } else {                                                                                    \
+      NSC_SPLIT_LAUNCH(N, false);                                                               \
+    }                                                                                           \
+    break;
+  switch (nt) {
+    NSC_SPLIT_CASE(1)
+    NSC_SPLIT_CASE(2)
+    NSC_SPLIT_CASE(4)
+    NSC_SPLIT_CASE(8)
+    NSC_SPLIT_CASE(16)
+    default:
+      return fail(NSC_E_SHAPE, "dense layer of %d units is not supported", nt * 16);
+  }
+#undef NSC_SPLIT_CASE
+#undef NSC_SPLIT_LAUNCH
+  NSC_CHECK_LAUNCH("k_dense_part / k_dense_finish");
+  return NSC_OK;
+}
+
+template <typename T>
+int launch_dense_nt(int nt, const DenseArgs& a, unsigned grid, hipStream_t st) {
+#define NSC_DENSE_LAUNCH(N, G)                                                                 \
+  hipLaunchKernelGGL((k_dense<T, N, G>), dim3(grid), dim3(64 * kDenseWaves), 0, st, a)
 #define NSC_DENSE_CASE(N)                                                                      \
   case N:                                                                                      \
-    if (big) {                                                                                 \
-      if (a.nets) NSC_DENSE_LAUNCH(N, true, true); else NSC_DENSE_LAUNCH(N, false, true);      \
-    } else {                                                                                   \
-      if (a.nets) NSC_DENSE_LAUNCH(N, true, false); else NSC_DENSE_LAUNCH(N, false, false);    \
-    }                                                                                          \
+    if (a.nets) NSC_DENSE_LAUNCH(N, true); else NSC_DENSE_LAUNCH(N, false);                    \
     break;
   switch (nt) {
     NSC_DENSE_CASE(1)
@@ -1763,9 +1944,17 @@ size_t cnn_xin_bytes(const Cnn& cnn, int64_t max_count) {
   return align_up((size_t)xr * xw * 8 * (size_t)(max_count > 0 ? max_count : 0), 256);
 }
 
+// The dense layer's partial blocks when it splits K over workgroups (fewer
+// than kDenseBig survivors): one NT x 1 KB block per (tile, K part) item.
+size_t cnn_dense_part_bytes(const Cnn& cnn, int64_t max_count) {
+  if (max_count <= 0 || max_count >= kDenseBig) return 0;
+  return (size_t)kDenseSplitItems * (size_t)(cnn.dense / 16) * 64 * sizeof(f32x4);
+}
+
 size_t cnn_workspace_bytes(const Cnn& cnn, int64_t max_count) {
   const size_t per = align_up(cnn.act_elems * sizeof(float), 256);
-  return 2 * per * (size_t)(max_count > 0 ? max_count : 0) + 256 + cnn_xin_bytes(cnn, max_count);
+  return 2 * per * (size_t)(max_count > 0 ? max_count : 0) + 256 + cnn_xin_bytes(cnn, max_count) +
+         cnn_dense_part_bytes(cnn, max_count);
 }
 
 int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipStream_t stream) {
@@ -1903,14 +2092,29 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
   d.nets = r.nets;
   d.per_cam = r.per_cam;
   const int nt = cnn.dense / 16;
-  const bool big = r.max_count >= kDenseBig;
-  const int64_t rows = !big || nt >= 16 ? 16 : (nt >= 8 ? 32 : 64);  // 16 x dense_mt
+  if (r.max_count < kDenseBig) {
+    f32x4* part = reinterpret_cast<f32x4*>(static_cast<unsigned char*>(ws) +
+                                           2 * per * (size_t)r.max_count + 256 +
+                                           cnn_xin_bytes(cnn, r.max_count));
+    // items: up to kDenseSplitItems; finishing: a wave per 16-survivor tile
+    const int64_t tiles = (r.max_count + 15) / 16;
+    int64_t grid_part = kDenseSplitItems;
+    if (grid_part > kNumCU * 4) grid_part = kNumCU * 4;
+    int64_t grid_fin = (tiles + 3) / 4;
+    if (grid_fin > kNumCU * 4) grid_fin = kNumCU * 4;
+    if (grid_fin < 1) grid_fin = 1;
+    return cnn.bf16 ? launch_dense_split_nt<uint16_t>(nt, d, part, (unsigned)grid_part,
+                                                      (unsigned)grid_fin, stream)
+                    : launch_dense_split_nt<float>(nt, d, part, (unsigned)grid_part,
+                                                   (unsigned)grid_fin, stream);
+  }
+  const int64_t rows = nt >= 16 ? 16 : (nt >= 8 ? 32 : 64);  // 16 x dense_mt
   int64_t groups = (r.max_count + rows - 1) / rows;  // one workgroup per group of rows
   int64_t grid = groups;
   if (grid > kNumCU * 2) grid = kNumCU * 2;
   if (grid < 1) grid = 1;
-  return cnn.bf16 ? launch_dense_nt<uint16_t>(nt, d, big, (unsigned)grid, stream)
-                  : launch_dense_nt<float>(nt, d, big, (unsigned)grid, stream);
+  return cnn.bf16 ? launch_dense_nt<uint16_t>(nt, d, (unsigned)grid, stream)
+                  : launch_dense_nt<float>(nt, d, (unsigned)grid, stream);
 }
 
 }  // namespace nsc

@@ -104,6 +104,14 @@ CASES = {
                           n=12, t0=9),
     "blocked-uneven": dict(H=90, W_=120, Ho=50, Wo=50, ref_mode=0, delta=2, grid=(3, 4), n=12,
                            t0=0),
+    # rows of exactly 6 x 64 values (the row-streaming path's widest), then
+    # rows too wide for it and more than 64 block columns (the per-block path)
+    "blocked-rows384": dict(H=128, W_=256, Ho=64, Wo=128, ref_mode=0, delta=1, grid=(4, 16), n=6,
+                            t0=3),
+    "blocked-rows480": dict(H=80, W_=320, Ho=40, Wo=160, ref_mode=1, delta=1, grid=(5, 8), n=6,
+                            t0=0),
+    "blocked-80-columns": dict(H=100, W_=200, Ho=50, Wo=100, ref_mode=0, delta=1, grid=(2, 80), n=6,
+                               t0=1),
 }
 
 

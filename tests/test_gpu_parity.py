@@ -165,7 +165,7 @@ def test_compact_parity(n, density):
 
 # -------------------------------------------------------------------- CNN
 
-def _cnn_case(spec, n_frames, n_img, fy=1, seed=5):
+def _cnn_case(spec, n_frames, n_img, fy=1, seed=5, max_count=None):
     hs, ws_ = spec.in_h * fy, spec.in_w * fy
     den = 9
     S = rng.integers(0, 255 * den + 1, size=(n_frames, hs, ws_, 3)).astype(np.int32)
@@ -174,7 +174,7 @@ def _cnn_case(spec, n_frames, n_img, fy=1, seed=5):
     blob = synth.weight_blob(spec, wts)
     desc = nsc.make_desc(spec.conv, spec.pool, spec.dense, spec.in_h, spec.in_w, spec.bf16)
     cnn = nsc.Cnn(desc, blob)
-    max_count = n_img + 5
+    max_count = n_img + 5 if max_count is None else max_count
     ws = torch.empty(nsc.nsc_cnn_workspace_bytes(cnn, max_count), dtype=torch.uint8, device=DEV)
     logit = torch.full((max_count,), math.nan, dtype=torch.float32, device=DEV)
     prob = torch.full((max_count,), math.nan, dtype=torch.float32, device=DEV)
@@ -256,6 +256,20 @@ def test_cnn_banded_shapes(conv, pool, hw, fy):
     # bf16 layers with 64 input channels run banded, weights streamed in fragment order
     spec = synth.CNNSpec(in_h=hw[0], in_w=hw[1], conv=conv, pool=pool, dense=32, bf16=True)
     _cnn_case(spec, n_frames=16, n_img=9, fy=fy)
+
+
+@pytest.mark.parametrize("dense", [16, 32, 64, 128, 256])
+@pytest.mark.parametrize("bf16", [True, False], ids=["bf16", "fp32"])
+def test_cnn_dense_paths(dense, bf16):
+    """The dense layer below 16,384 survivors' capacity (K split over
+    workgroups, then a finishing pass) and from it on (row-blocked
+    workgroups), at every dense width: a count of 1, 3 or 133 survivors in
+    both."""
+    spec = synth.CNNSpec(in_h=10, in_w=12, conv=(32, 32), pool=(True, False), dense=dense,
+                         bf16=bf16)
+    for n_img in (1, 3, 133):
+        _cnn_case(spec, n_frames=140, n_img=n_img)
+        _cnn_case(spec, n_frames=140, n_img=n_img, max_count=16400)
 
 
 def test_cnn_zero_count():
