@@ -251,6 +251,10 @@ def test_cnn_fused_pair_shapes(conv, pool, hw, fy):
     ((32, 64, 64), (True, False, True), (30, 61), 1),      # banded layer after a layered one
     ((64, 64), (False, False), (6, 80), 1),                # pair band over 80 KB: 1 group per CU
     ((32, 64, 64), (True, False, False), (11, 200), 1),    # banded layer 100 wide (160 KB plan)
+    ((64, 64), (True, True), (13, 9), 1),                  # pooled 64-channel first layer fused
+    ((64, 32, 64), (True, False, True), (23, 31), 1),      # ... into 32 channels, odd map
+    ((64, 64, 64), (True, True, True), (50, 50), 2),       # the 3-layer net, nested cells
+    ((64, 64), (True, False), (10, 96), 1),                # ... 48-wide second layer
 ])
 def test_cnn_banded_shapes(conv, pool, hw, fy):
     # bf16 layers with 64 input channels run banded, weights streamed in fragment order
