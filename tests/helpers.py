@@ -1,7 +1,9 @@
 """Shared helpers of the GPU parity tests: inputs, oracle runs and comparisons."""
 from __future__ import annotations
 
+import concurrent.futures
 import math
+import os
 
 import numpy as np
 
@@ -107,6 +109,9 @@ def compare_cascade(wl, gpu: dict, ref: dict, t0: int = 0, state_excluded=None):
 
 # ------------------------------------------- sampled frames of long runs
 
+SAMPLE_THREADS = min(16, os.cpu_count() or 1)
+
+
 def oracle_frame(wl, v, blob, lr, ref_sums_o, t):
     """Oracle score of frame t and, when it fires, its logit, scale and decision
     (a frame between checks has score NaN and does not fire)."""
@@ -162,10 +167,16 @@ def check_properties(wl, g, t0=0):
 
 
 def check_samples(wl, v, blob, lr, ref_o, g, ts, t0=0):
+    """Frames ts of a run over [t0, ...) against the oracle, one by one.  The
+    oracle frames are computed on a thread pool: the oracle library's calls
+    release the GIL, and so does most of the numpy frame rendering (no
+    process is forked from one that has initialised the GPU)."""
     tol = LOGIT_TOL[wl.cnn.bf16]
     worst = 0.0
-    for t in ts:
-        o = oracle_frame(wl, v, blob, lr, ref_o, int(t))
+    oracle.lib()  # loaded once, before the threads use it
+    with concurrent.futures.ThreadPoolExecutor(max_workers=SAMPLE_THREADS) as ex:
+        outs = list(ex.map(lambda t: oracle_frame(wl, v, blob, lr, ref_o, int(t)), ts))
+    for t, o in zip(ts, outs):
         u = int(t) - t0
         assert g["score"][u] == o["score"] or (math.isnan(g["score"][u]) and math.isnan(o["score"])), \
             (t, g["score"][u], o["score"])

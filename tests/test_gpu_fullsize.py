@@ -6,9 +6,11 @@ The 100,000-frame 640x480 run uses the launch configuration bench.py times
 chunks through the carried state.  For sampled frames the oracle recomputes,
 from host-rendered frames t and t - delta, the detector score (bit-exact), the
 fire flag, and for fired frames the logit (relative to its scale) and the
-decision.  For every frame: frames t < delta fire; a frame that does not fire
-repeats the output of frame t - delta (or is "no object" with a fixed
-reference); logits exist exactly for fired frames; runs are deterministic.
+decision; about 1,000 frames per video (random and occupied ones, chunk
+boundaries), checked on a thread pool.  For every frame: frames t < delta
+fire; a frame that does not fire repeats the output of frame t - delta (or is
+"no object" with a fixed reference); logits exist exactly for fired frames;
+runs are deterministic.
 """
 import numpy as np
 import pytest
@@ -36,6 +38,11 @@ def _thresholds_from_oracle(wl, v, blob, ts):
         ps.append(oracle.sigmoid(oracle.cnn_logit(wl.cnn, blob, Sc, den_c)))
     lo, hi = np.quantile(ps, [0.3, 0.7])
     return float(lo), float(hi)
+
+
+# random and occupied frames checked per sampled chunk of the chunked runs:
+# about 1,000 frames per video in all
+SAMPLES_PER_CHUNK = {W.HD_REF.name: 170, W.HD_BLOCKED.name: 100}
 
 
 def _sample_times(v, t0, n, rng, k=12):
@@ -71,7 +78,7 @@ def test_vga_100k_as_benchmarked():
         g = outs[0]
         assert st["fired"] == int(g["fire"].sum())
         check_properties(w, g)
-        ts = _sample_times(v, 0, n, rng)
+        ts = _sample_times(v, 0, n, rng, k=500)
         worst = check_samples(w, v, blob, None, None, g, ts)
         results[name] = dict(fired=int(g["fire"].sum()), positive=int(st["positive"]),
                              deferred=int(st["deferred"]), samples=len(ts), worst_logit=worst)
@@ -122,7 +129,7 @@ def test_hd_full_length_in_chunks(wl, chunk):
             prev_tail = (g["label"][-wl.delta:].copy(), g["defer"][-wl.delta:].copy())
         fired += int(g["fire"].sum())
         if t0 % (3 * chunk) == 0 or t0 + m == n:
-            ts = _sample_times(v, t0, m, rng, k=3)
+            ts = _sample_times(v, t0, m, rng, k=SAMPLES_PER_CHUNK[wl.name])
             worst = max(worst, check_samples(wl, v, blob, lr, ref_o, g, ts, t0))
             checked += len(ts)
     run.close()
@@ -159,7 +166,7 @@ def test_fhd_1m_streamed(occ):
     rng = np.random.default_rng(5)
     # frames at chunk boundaries (their reference frame t - 30 lies in the previous chunk)
     # and random / occupied ones
-    ts = sorted(set(_sample_times(v, 0, n, rng, k=5)) |
+    ts = sorted(set(_sample_times(v, 0, n, rng, k=200)) |
                 {wl.chunk, wl.chunk + wl.delta - 1, 100 * wl.chunk + 7, n - 1})
     worst = check_samples(wl, v, blob, lr, None, g, ts)
     print(dict(frames=n, chunks=st["chunks"], fired=int(g["fire"].sum()),
