@@ -354,6 +354,20 @@ def test_cascade_vga_window():
     print(rep)
 
 
+@pytest.mark.parametrize("frac", [0.0, 0.25, 0.5, 0.9], ids=["start", "q1", "mid", "end"])
+def test_cascade_vga_512_windows(frac):
+    """Whole windows of 512 consecutive 640x480 frames at four offsets of the
+    100k-frame video, every frame compared (the t - 15 label chains included)."""
+    wl = W.VGA
+    v = synth.Video(wl.video)
+    occ = np.flatnonzero(v.occupied)
+    t0 = int(occ[np.searchsorted(occ, int(frac * wl.video.n))]) if frac > 0 else 0
+    t0 = max(0, min(t0 - 40, wl.video.n - 512))
+    rep = _run_and_compare_from_zero_window(wl, t0, 512)
+    print(t0, rep)
+    assert rep["fired"] > 0
+
+
 def _run_and_compare_from_zero_window(wl, t0, n):
     """Window [t0, t0+n) of a video whose frames before t0 are dropped: the
     window is treated as its own video (frame indices restart at 0)."""
