@@ -19,7 +19,7 @@ import synth
 from paper_1703_02529_amd.runner import CascadeRunner, GroupRunner
 from synth import workloads as W
 
-from helpers import compare_cascade, lr_weights_for
+from helpers import check_samples, compare_cascade, lr_weights_for
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -173,6 +173,40 @@ def test_group_hd_blocked_cameras():
     reps = _check_group(cams, max(0, int(occ[0]) - 2), [4, 2])
     print(reps)
     assert sum(r["fired"] for r in reps) > 0
+
+
+def test_group_large_batch():
+    """Two 100x100 cameras x 8,192 frames in one call: 16,384 frames, so the
+    dense layer takes its large-batch kernel with per-camera weights.  Every
+    camera's sampled frames against the oracle (score and fire flag exact,
+    logit within the fp32 tolerance, decision of fired frames)."""
+    b = W.TINY
+    n = 8192
+    cams = [_camera(b, 51, weight_seed=6001, delta=2, delta_diff=10.0),
+            _camera(b, 52, weight_seed=6002, delta=5, delta_diff=20.0, c_low=0.3, c_high=0.6)]
+    cams = [w.with_frames(n) for w in cams]
+    videos = [synth.Video(w.video) for w in cams]
+    fb = b.video.frame_bytes
+    frames = torch.empty(len(cams) * n * fb, dtype=torch.uint8, device=DEV)
+    for c, v in enumerate(videos):
+        v.render_device(frames[c * n * fb:(c + 1) * n * fb], 0, n)
+    blobs = [_blob(w) for w in cams]
+    run = GroupRunner(cams, blobs, frames_per_cam=n)
+    run.run(frames, n, t0=0)
+    keys = ("score", "fire", "logit", "label", "defer")
+    outs = {k: getattr(run, k)[:len(cams) * n].cpu().numpy().reshape(len(cams), n) for k in keys}
+    run.close()
+    rng = np.random.default_rng(9)
+    fired = 0
+    for c, (w, v) in enumerate(zip(cams, videos)):
+        g = {k: outs[k][c] for k in keys}
+        fired += int(g["fire"].sum())
+        occ = np.flatnonzero(v.occupied)
+        ts = sorted(set(rng.integers(0, n, 40).tolist()) |
+                    set(rng.choice(occ, min(40, occ.size), replace=False).tolist()) | {0, n - 1})
+        worst = check_samples(w, v, blobs[c], None, None, g, ts)
+        print(w.name, dict(fired=int(g["fire"].sum()), sampled=len(ts), worst_logit=worst))
+    assert fired > 1000
 
 
 def test_group_rejects_mixed_geometry_and_skipping():
