@@ -1,0 +1,37 @@
+"""Host-side checks of bench.py: the one-GPU contract and the algorithmic
+FLOP count per survivor that the CNN's MFMA fraction is quoted on."""
+import os
+import subprocess
+import sys
+
+import bench
+from synth import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_bench_refuses_more_than_one_gpu():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def _conv(cin, cout, h, w):
+    return 2 * h * w * cin * cout * 9
+
+
+def test_cnn_flops_per_survivor():
+    # conv layers at their input resolution (pooling halves it for the next),
+    # then dense (flat -> D) and the output unit (D -> 1)
+    tiny = _conv(3, 32, 50, 50) + _conv(32, 32, 25, 25) + 2 * (12 * 12 * 32) * 32 + 2 * 32
+    vga = _conv(3, 32, 50, 50) + _conv(32, 32, 25, 25) + 2 * (12 * 12 * 32) * 128 + 2 * 128
+    hd4 = (_conv(3, 64, 50, 50) + _conv(64, 64, 50, 50) + _conv(64, 64, 25, 25) +
+           _conv(64, 64, 25, 25) + 2 * (12 * 12 * 64) * 128 + 2 * 128)
+    hd3 = (_conv(3, 64, 50, 50) + _conv(64, 64, 25, 25) + _conv(64, 64, 12, 12) +
+           2 * (6 * 6 * 64) * 64 + 2 * 64)
+    assert bench.cnn_flops(W.TINY.cnn) == tiny == 16_134_976
+    assert bench.cnn_flops(W.VGA.cnn) == vga == 17_019_904
+    assert bench.cnn_flops(W.HD_REF.cnn) == hd4 == 287_479_552
+    assert bench.cnn_flops(W.HD_BLOCKED.cnn) == hd3 == 65_631_872
+    assert bench.cnn_flops(W.FHD_STREAM.cnn) == hd4
