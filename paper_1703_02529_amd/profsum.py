@@ -98,24 +98,26 @@ def _per_dispatch(directory: str, counter: str):
         key = (r["Kernel_Name"], r.get("Dispatch_Id") or r.get("Correlation_Id"))
         acc[key] = acc.get(key, 0.0) + float(r["Counter_Value"])
     out = {}
-    for (name, _), v in acc.items():
+    for (name, _), v in sorted(acc.items(), key=lambda kv: int(kv[0][1] or 0)):
         out.setdefault(name, []).append(v)
     return out
 
 
-def _pick(table, pattern: str, what: str):
+def _pick(table, pattern: str, what: str, skip: int = 0):
+    """The one kernel matching pattern: its mean per dispatch, in dispatch
+    order after the first `skip` dispatches."""
     names = [n for n in table if pattern in n]
     if len(names) != 1:
         raise SystemExit(f"{what}: {len(names)} kernels match {pattern!r}: {names[:5]}")
-    vals = table[names[0]]
+    vals = table[names[0]][skip:]
     return names[0], sum(vals) / len(vals), len(vals)
 
 
 def cmd_traffic(a) -> None:
     fetch = _per_dispatch(a.fetch, "FETCH_SIZE")
     write = _per_dispatch(a.write, "WRITE_SIZE")
-    kname, f_kib, nf = _pick(fetch, a.kernel, "FETCH_SIZE kernel")
-    _, w_kib, nw = _pick(write, a.kernel, "WRITE_SIZE kernel")
+    kname, f_kib, nf = _pick(fetch, a.kernel, "FETCH_SIZE kernel", a.skip_first)
+    _, w_kib, nw = _pick(write, a.kernel, "WRITE_SIZE kernel", a.skip_first)
     cname, cf_kib, _ = _pick(fetch, a.copy_kernel, "FETCH_SIZE copy")
     _, cw_kib, _ = _pick(write, a.copy_kernel, "WRITE_SIZE copy")
     sf = a.copy_bytes / (cf_kib * 1024.0)
@@ -210,6 +212,8 @@ def main(argv=None) -> None:
     t.add_argument("--copy-kernel", required=True)
     t.add_argument("--copy-bytes", type=float, required=True)
     t.add_argument("--algorithmic-bytes", type=float, default=0.0)
+    t.add_argument("--skip-first", type=int, default=0,
+                   help="leave out the kernel's first dispatches (set-up work of the run)")
     t.add_argument("--workload", default="")
     t.add_argument("--source", action="append", default=[])
     t.add_argument("--command", action="append", default=[])
