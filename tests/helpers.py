@@ -40,7 +40,8 @@ def compare_scores(wl, g: np.ndarray, o: np.ndarray):
 def logit_rel_err(g: np.ndarray, o: np.ndarray, scale: np.ndarray) -> np.ndarray:
     """|g - o| / scale, scale = |b2| + sum_j |w2_j h_j| from the oracle: the error
     relative to the magnitude of the terms the output layer sums (equal to the
-    plain relative error when they do not cancel)."""
+    plain relative error when they do not cancel).  This is the measure the
+    tolerance is asserted on."""
     g = np.asarray(g, np.float64)
     o = np.asarray(o, np.float64)
     if o.size == 0:
@@ -48,14 +49,80 @@ def logit_rel_err(g: np.ndarray, o: np.ndarray, scale: np.ndarray) -> np.ndarray
     return np.abs(g - o) / np.maximum(np.asarray(scale, np.float64), 1e-300)
 
 
-def decision_excluded(z_oracle: float, c_low: float, c_high: float, tol: float, scale: float) -> bool:
-    """A fired frame's decision is only pinned when its logit is farther from the
-    logit of a threshold than the logit tolerance allows the GPU value to move."""
-    band = 2.0 * tol * scale
-    for c in (c_low, c_high):
-        if 0.0 < c < 1.0 and abs(z_oracle - math.log(c / (1.0 - c))) <= band:
-            return True
-    return False
+FLOOR_FRAC = 2.0 ** -10   # floored relative error: |g - o| / max(|o|, 2^-10 max_batch |o|)
+
+
+class LogitErrors:
+    """Worst logit errors of a test in three measures, side by side:
+    - scale: |g - o| / (|b2| + sum_j |w2_j h_j|) (asserted against the tolerance);
+    - plain: |g - o| / |o|;
+    - floored: |g - o| / max(|o|, 2^-10 max |o| over the batch), with the
+      number of logits whose denominator is the floor;
+    plus the decision counts: `excluded` frames (an oracle confidence within
+    1e-5 relative of c_low or c_high, and frames reusing their output) and
+    `straddled` frames (outside that band, but the GPU and oracle logits lie on
+    opposite sides of a threshold, so their decisions differ by the logit error
+    alone; also excluded with the frames reusing their output)."""
+
+    def __init__(self):
+        self.n = 0
+        self.scale = self.plain = self.floored = 0.0
+        self.floor_hits = self.excluded = self.straddled = 0
+
+    def add(self, g, o, scale):
+        g = np.asarray(g, np.float64).reshape(-1)
+        o = np.asarray(o, np.float64).reshape(-1)
+        if o.size == 0:
+            return self
+        d = np.abs(g - o)
+        self.n += int(o.size)
+        self.scale = max(self.scale, float(logit_rel_err(g, o, scale).max()))
+        ao = np.abs(o)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            plain = np.where(ao > 0, d / np.where(ao > 0, ao, 1.0), np.where(d > 0, np.inf, 0.0))
+        self.plain = max(self.plain, float(plain.max()))
+        floor = FLOOR_FRAC * float(ao.max())
+        den = np.maximum(ao, floor)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            fl = np.where(den > 0, d / np.where(den > 0, den, 1.0), np.where(d > 0, np.inf, 0.0))
+        self.floored = max(self.floored, float(fl.max()))
+        self.floor_hits += int(np.sum(ao < floor))
+        return self
+
+    def merge(self, other: "LogitErrors"):
+        self.n += other.n
+        self.scale = max(self.scale, other.scale)
+        self.plain = max(self.plain, other.plain)
+        self.floored = max(self.floored, other.floored)
+        self.floor_hits += other.floor_hits
+        self.excluded += other.excluded
+        self.straddled += other.straddled
+        return self
+
+    def as_dict(self):
+        return dict(logits=self.n, max_logit_rel_scale=self.scale, max_logit_rel_plain=self.plain,
+                    max_logit_rel_floored=self.floored, floor_hits=self.floor_hits,
+                    excluded=self.excluded, straddled=self.straddled)
+
+    def __repr__(self):
+        return (f"logit errors over {self.n}: scale-relative {self.scale:.3g}, plain relative "
+                f"{self.plain:.3g}, floored {self.floored:.3g} ({self.floor_hits} at the floor); "
+                f"decisions excluded {self.excluded}, straddled {self.straddled}")
+
+
+DECISION_BAND = 1e-5   # a confidence within 1e-5 relative of a threshold is not compared
+
+
+def decision_excluded(p_oracle: float, c_low: float, c_high: float) -> bool:
+    """A fired frame's decision is not pinned when the oracle's confidence lies
+    within 1e-5 relative of c_low or c_high."""
+    return any(abs(p_oracle - c) <= DECISION_BAND * c for c in (c_low, c_high))
+
+
+def decision_of_logit(z: float, c_low: float, c_high: float) -> int:
+    """label | defer << 1 that the decision rule gives a logit (the oracle's
+    sigmoid and rule, in fp64)."""
+    return oracle.decide(oracle.sigmoid(float(z)), c_low, c_high)
 
 
 def oracle_decision(z: float, c_low: float, c_high: float) -> int:
@@ -70,19 +137,23 @@ def compare_cascade(wl, gpu: dict, ref: dict, t0: int = 0, state_excluded=None):
     """Element-by-element comparison of a GPU cascade run with the oracle's.
 
     gpu / ref: dicts of numpy arrays score, fire, logit, label, defer over the
-    same frames.  Returns (report dict).  Scores (see compare_scores) and fire
-    flags must be bit-identical; logits within the network's tolerance; labels and defer
-    flags identical outside the excluded frames (fired frames whose logit lies
-    within the tolerance band of a threshold, and frames inheriting from them)."""
+    same frames (ref also prob and lscale).  Scores (see compare_scores) and
+    fire flags must be bit-identical; logits within the network's tolerance
+    (scale-relative; the plain and floored relative errors are reported beside
+    it); labels and defer flags identical outside the excluded frames: fired
+    frames whose oracle confidence lies within 1e-5 relative of c_low or
+    c_high, fired frames whose GPU and oracle logits straddle a threshold (the
+    GPU's decision must then be the rule's decision on its own logit), and
+    frames reusing their output.  Returns the report dict."""
     n = len(ref["fire"])
     s = max(getattr(wl, "check_stride", 1), 1)
     compare_scores(wl, gpu["score"], ref["score"])
     assert np.array_equal(gpu["fire"], ref["fire"]), "fire flags differ"
     fired = np.flatnonzero(ref["fire"])
     tol = LOGIT_TOL[wl.cnn.bf16]
-    rel = logit_rel_err(gpu["logit"][fired], ref["logit"][fired], ref["lscale"][fired])
+    errs = LogitErrors().add(gpu["logit"][fired], ref["logit"][fired], ref["lscale"][fired])
     assert np.isnan(gpu["logit"][ref["fire"] == 0]).all()
-    assert rel.size == 0 or rel.max() <= tol, f"max logit rel err {rel.max():.3g} > {tol}"
+    assert errs.scale <= tol, f"max logit rel err {errs.scale:.3g} > {tol} ({errs})"
     excluded = np.zeros(n, bool)
     for u in range(n):
         if (t0 + u) % s:  # not checked: inherits from its checked frame
@@ -91,20 +162,29 @@ def compare_cascade(wl, gpu: dict, ref: dict, t0: int = 0, state_excluded=None):
             elif state_excluded is not None:
                 excluded[u] = state_excluded[u]
         elif ref["fire"][u]:
-            excluded[u] = decision_excluded(ref["logit"][u], wl.c_low, wl.c_high, tol,
-                                            ref["lscale"][u])
+            if decision_excluded(ref["prob"][u], wl.c_low, wl.c_high):
+                excluded[u] = True
+            else:
+                dg = decision_of_logit(gpu["logit"][u], wl.c_low, wl.c_high)
+                if dg != decision_of_logit(ref["logit"][u], wl.c_low, wl.c_high):
+                    excluded[u] = True
+                    errs.straddled += 1
+                    got = int(gpu["label"][u]) | (int(gpu["defer"][u]) << 1)
+                    assert got == dg, f"frame {t0 + u}: decision {got}, its logit gives {dg}"
         elif wl.ref_mode == 0:
             if u >= wl.delta:
                 excluded[u] = excluded[u - wl.delta]
             elif state_excluded is not None:
                 excluded[u] = state_excluded[u]
+    errs.excluded = int(excluded.sum())
     keep = ~excluded
     bad = np.flatnonzero(keep & ((gpu["label"] != ref["label"]) | (gpu["defer"] != ref["defer"])))
     assert bad.size == 0, f"labels differ at frames {bad[:10] + t0}"
-    return dict(frames=n, fired=int(fired.size), excluded=int(excluded.sum()),
-                max_logit_rel=float(rel.max()) if rel.size else 0.0,
-                near_delta=int(np.sum(np.abs(ref["score"] - wl.delta_diff) <=
-                                      1e-5 * max(abs(wl.delta_diff), 1.0))))
+    rep = dict(frames=n, fired=int(fired.size), max_logit_rel=errs.scale,
+               near_delta=int(np.sum(np.abs(ref["score"] - wl.delta_diff) <=
+                                     1e-5 * max(abs(wl.delta_diff), 1.0))))
+    rep.update(errs.as_dict())
+    return rep
 
 
 # ------------------------------------------- sampled frames of long runs
@@ -166,16 +246,19 @@ def check_properties(wl, g, t0=0):
     assert not (g["label"].astype(bool) & g["defer"].astype(bool)).any()
 
 
-def check_samples(wl, v, blob, lr, ref_o, g, ts, t0=0):
-    """Frames ts of a run over [t0, ...) against the oracle, one by one.  The
-    oracle frames are computed on a thread pool: the oracle library's calls
-    release the GIL, and so does most of the numpy frame rendering (no
-    process is forked from one that has initialised the GPU)."""
+def check_samples(wl, v, blob, lr, ref_o, g, ts, t0=0) -> LogitErrors:
+    """Frames ts of a run over [t0, ...) against the oracle, one by one: scores
+    and fire flags exactly, logits within the tolerance (the three error
+    measures are returned), decisions as in compare_cascade (a sampled frame's
+    decision is compared where it fired).  The oracle frames are computed on a
+    thread pool: the oracle library's calls release the GIL, and so does most
+    of the numpy frame rendering (no process is forked from one that has
+    initialised the GPU)."""
     tol = LOGIT_TOL[wl.cnn.bf16]
-    worst = 0.0
     oracle.lib()  # loaded once, before the threads use it
     with concurrent.futures.ThreadPoolExecutor(max_workers=SAMPLE_THREADS) as ex:
         outs = list(ex.map(lambda t: oracle_frame(wl, v, blob, lr, ref_o, int(t)), ts))
+    gz, oz, sc = [], [], []
     for t, o in zip(ts, outs):
         u = int(t) - t0
         assert g["score"][u] == o["score"] or (math.isnan(g["score"][u]) and math.isnan(o["score"])), \
@@ -184,9 +267,23 @@ def check_samples(wl, v, blob, lr, ref_o, g, ts, t0=0):
         if o["fire"]:
             err = float(logit_rel_err(np.array([g["logit"][u]]), np.array([o["logit"]]),
                                       np.array([o["scale"]]))[0])
-            worst = max(worst, err)
             assert err <= tol, (t, g["logit"][u], o["logit"], err)
-            if not decision_excluded(o["logit"], wl.c_low, wl.c_high, tol, o["scale"]):
-                dec = int(g["label"][u]) | (int(g["defer"][u]) << 1)
-                assert dec == o["dec"], (t, dec, o["dec"])
-    return worst
+            gz.append(g["logit"][u])
+            oz.append(o["logit"])
+            sc.append(o["scale"])
+    errs = LogitErrors().add(np.array(gz), np.array(oz), np.array(sc))
+    for t, o in zip(ts, outs):
+        u = int(t) - t0
+        if not o["fire"]:
+            continue
+        dec = int(g["label"][u]) | (int(g["defer"][u]) << 1)
+        if decision_excluded(oracle.sigmoid(o["logit"]), wl.c_low, wl.c_high):
+            errs.excluded += 1
+            continue
+        dg = decision_of_logit(g["logit"][u], wl.c_low, wl.c_high)
+        if dg != o["dec"]:
+            errs.straddled += 1
+            assert dec == dg, (t, dec, dg)
+        else:
+            assert dec == o["dec"], (t, dec, o["dec"])
+    return errs

@@ -22,7 +22,7 @@ from paper_1703_02529_amd.runner import CascadeRunner
 from paper_1703_02529_amd.streaming import StreamingCascade
 from synth import workloads as W
 
-from helpers import check_properties, check_samples, lr_weights_for
+from helpers import LogitErrors, check_properties, check_samples, lr_weights_for
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -79,9 +79,9 @@ def test_vga_100k_as_benchmarked():
         assert st["fired"] == int(g["fire"].sum())
         check_properties(w, g)
         ts = _sample_times(v, 0, n, rng, k=500)
-        worst = check_samples(w, v, blob, None, None, g, ts)
+        errs = check_samples(w, v, blob, None, None, g, ts)
         results[name] = dict(fired=int(g["fire"].sum()), positive=int(st["positive"]),
-                             deferred=int(st["deferred"]), samples=len(ts), worst_logit=worst)
+                             deferred=int(st["deferred"]), samples=len(ts), **errs.as_dict())
     print(results)
     q = results["quantile thresholds"]
     assert q["positive"] > 0 and q["deferred"] > 0 and q["positive"] + q["deferred"] < n
@@ -112,7 +112,7 @@ def test_hd_full_length_in_chunks(wl, chunk):
     rng = np.random.default_rng(11)
     keys = ("score", "fire", "logit", "label", "defer")
     prev_tail = None   # label/defer of the last delta frames of the previous chunk
-    worst, fired, checked = 0.0, 0, 0
+    errs, fired, checked = LogitErrors(), 0, 0
     for t0 in range(0, n, chunk):
         m = min(chunk, n - t0)
         v.render_device(buf, t0, m, tables)
@@ -130,10 +130,10 @@ def test_hd_full_length_in_chunks(wl, chunk):
         fired += int(g["fire"].sum())
         if t0 % (3 * chunk) == 0 or t0 + m == n:
             ts = _sample_times(v, t0, m, rng, k=SAMPLES_PER_CHUNK[wl.name])
-            worst = max(worst, check_samples(wl, v, blob, lr, ref_o, g, ts, t0))
+            errs.merge(check_samples(wl, v, blob, lr, ref_o, g, ts, t0))
             checked += len(ts)
     run.close()
-    print(dict(frames=n, fired=fired, sampled=checked, worst_logit=worst))
+    print(dict(frames=n, fired=fired, sampled=checked, **errs.as_dict()))
     del buf
     torch.cuda.empty_cache()
 
@@ -168,9 +168,9 @@ def test_fhd_1m_streamed(occ):
     # and random / occupied ones
     ts = sorted(set(_sample_times(v, 0, n, rng, k=200)) |
                 {wl.chunk, wl.chunk + wl.delta - 1, 100 * wl.chunk + 7, n - 1})
-    worst = check_samples(wl, v, blob, lr, None, g, ts)
+    errs = check_samples(wl, v, blob, lr, None, g, ts)
     print(dict(frames=n, chunks=st["chunks"], fired=int(g["fire"].sum()),
                cascade_ms=round(st["cascade_ms"], 1), wall_ms=round(st["wall_ms"], 1),
-               sampled=len(ts), worst_logit=worst))
+               sampled=len(ts), **errs.as_dict()))
     del out
     torch.cuda.empty_cache()

@@ -204,8 +204,8 @@ def test_group_large_batch():
         occ = np.flatnonzero(v.occupied)
         ts = sorted(set(rng.integers(0, n, 40).tolist()) |
                     set(rng.choice(occ, min(40, occ.size), replace=False).tolist()) | {0, n - 1})
-        worst = check_samples(w, v, blobs[c], None, None, g, ts)
-        print(w.name, dict(fired=int(g["fire"].sum()), sampled=len(ts), worst_logit=worst))
+        errs = check_samples(w, v, blobs[c], None, None, g, ts)
+        print(w.name, dict(fired=int(g["fire"].sum()), sampled=len(ts), **errs.as_dict()))
     assert fired > 1000
 
 

@@ -447,6 +447,53 @@ def test_decision_rule_ties_defer():
     assert oracle.decide(0.5, 0.2, 0.8) == 2
 
 
+def _ulp(x: float) -> float:
+    return abs(np.nextafter(x, math.inf) - x)
+
+
+def test_sigmoid_exact_rationals():
+    """sigma(ln k) = k / (1 + k): the confidence at a logit whose odds are a
+    rational number.  At ln 4 and -ln 4 these are exactly the workloads'
+    c_high = 0.8 and c_low = 0.2; a sign error (1 / (1 + e^z)) swaps them."""
+    assert abs(oracle.sigmoid(math.log(4.0)) - 0.8) <= _ulp(0.8)
+    assert abs(oracle.sigmoid(-math.log(4.0)) - 0.2) <= _ulp(0.2)
+    for k in (1.0, 2.0, 3.0, 9.0, 0.5, 0.1, 1000.0):
+        want = k / (1.0 + k)
+        assert abs(oracle.sigmoid(math.log(k)) - want) <= 2 * _ulp(want), k
+
+
+def test_sigmoid_shape():
+    """Symmetry sigma(z) + sigma(-z) = 1, strict increase, slope 1/4 at 0 and
+    the limits 0 and 1: a dropped minus sign, a wrong offset or a missing
+    reciprocal each break one of them."""
+    zs = rng.normal(0.0, 4.0, 200)
+    for z in zs:
+        assert oracle.sigmoid(z) + oracle.sigmoid(-z) == pytest.approx(1.0, abs=5e-16)
+    srt = np.unique(np.clip(zs, -30.0, 30.0))
+    vals = [oracle.sigmoid(z) for z in srt]
+    assert all(a < b for a, b in zip(vals, vals[1:]))
+    h = 1e-5
+    assert (oracle.sigmoid(h) - oracle.sigmoid(-h)) / (2 * h) == pytest.approx(0.25, rel=1e-9)
+    assert oracle.sigmoid(-40.0) == pytest.approx(math.exp(-40.0), rel=1e-15)
+    assert oracle.sigmoid(-800.0) == 0.0 and oracle.sigmoid(40.0) == 1.0
+    assert 0.0 < oracle.sigmoid(-700.0) < 1e-300
+
+
+def test_decision_at_threshold_logits():
+    """decide(sigmoid(z)) on both sides of logit(c_low) = -ln 4 and
+    logit(c_high) = ln 4: below c_low no object, between the two defer, above
+    c_high object (ties defer, as the paper's open intervals leave them)."""
+    lo, hi = -math.log(4.0), math.log(4.0)
+    eps = 1e-9  # moves the confidence by about 1.6e-10, far beyond rounding
+    assert oracle.decide(oracle.sigmoid(lo - eps), 0.2, 0.8) == 0
+    assert oracle.decide(oracle.sigmoid(lo + eps), 0.2, 0.8) == 2
+    assert oracle.decide(oracle.sigmoid(hi - eps), 0.2, 0.8) == 2
+    assert oracle.decide(oracle.sigmoid(hi + eps), 0.2, 0.8) == 1
+    assert oracle.decide(oracle.sigmoid(0.0), 0.2, 0.8) == 2
+    assert oracle.decide(oracle.sigmoid(-5.0), 0.2, 0.8) == 0
+    assert oracle.decide(oracle.sigmoid(5.0), 0.2, 0.8) == 1
+
+
 # ------------------------------------------------------------------ cascade
 
 def _small(wl, n):
