@@ -24,6 +24,10 @@ _i32, _i64, _u32, _dbl = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes
 _vp, _sz = ctypes.c_void_p, ctypes.c_size_t
 
 
+NSC_OK, NSC_E_INVAL, NSC_E_SHAPE, NSC_E_DTYPE, NSC_E_WORKSPACE, NSC_E_HIP, NSC_E_NOMEM, \
+    NSC_E_STATE = 0, -1, -2, -3, -4, -5, -6, -7
+
+
 class NscError(RuntimeError):
     def __init__(self, status: int, what: str, detail: str):
         super().__init__(f"{what}: {status_string(status)} ({status}): {detail}")

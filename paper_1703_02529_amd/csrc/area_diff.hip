@@ -223,7 +223,9 @@ __global__ void __launch_bounds__(256) k_area_sums_wave(const uint8_t* __restric
     xtab[x] = make_int4(i0, il - i0, il == i0 ? px : (i0 + 1) * qx - b0, b1 - il * qx);
   }
   __syncthreads();  // the only workgroup barrier
-  const size_t per_wave = (size_t)64 * CB * sizeof(cell_t) + (size_t)g.band_rows * scols * 3 * 4;
+  // each wave's region starts 16-byte aligned (the column sums are stored as uint4)
+  const size_t per_wave =
+      ((size_t)64 * CB * sizeof(cell_t) + (size_t)g.band_rows * scols * 3 * 4 + 15) & ~(size_t)15;
   unsigned char* wbase = smem + (size_t)scols * 16 + (size_t)wv * per_wave;
   cell_t* buf = reinterpret_cast<cell_t*>(wbase);                              // column sums
   int32_t* sbuf = reinterpret_cast<int32_t*>(wbase + (size_t)64 * CB * sizeof(cell_t));  // band sums
@@ -600,7 +602,8 @@ int make_area_plan(int32_t in_h, int32_t in_w, int64_t stride, const void* frame
       g.band_rows = (int32_t)((out_h + wb - 1) / wb);
       const int64_t scols = (int64_t)g.groups_per_wave * g.group_cols;
       const int64_t cellb = p.packed ? 2 : 4;
-      g.lds_bytes = (size_t)(scols * 16 + 4 * (64 * p.chunk_bytes * cellb + (int64_t)g.band_rows * scols * 3 * 4));
+      const int64_t per_wave = (64 * p.chunk_bytes * cellb + (int64_t)g.band_rows * scols * 3 * 4 + 15) & ~(int64_t)15;
+      g.lds_bytes = (size_t)(scols * 16 + 4 * per_wave);
       p.wave = g.lds_bytes <= 64 * 1024;
     }
   }

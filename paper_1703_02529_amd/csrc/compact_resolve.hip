@@ -1,10 +1,11 @@
 // Stream compaction of fired frames and label resolution (gfx950).
 //
 // Compaction (frames batched for the GPU model, Sec. 7): tiles of 4096 flags.
-// A first kernel counts each tile with wave ballots; a second one gives every
-// tile its offset (sum of the earlier tiles' counts), scans its four waves'
-// counts in LDS and writes the ascending indices with ballot + lane-mask
-// popcounts, so the output order is the frame order.
+// A first kernel counts each tile with wave ballots; one workgroup turns the
+// counts into exclusive tile offsets (a single scan, linear in the number of
+// tiles) and writes the total; a third kernel scans each tile's four waves'
+// counts in LDS and writes the ascending indices at the tile's offset with
+// ballot + lane-mask popcounts, so the output order is the frame order.
 //
 // Resolution (Sec. 5: a frame on which the earlier-frame detector does not
 // fire reuses the compared frame's output): frame u copies frame u - delta,
@@ -46,24 +47,45 @@ __global__ void __launch_bounds__(kTileThreads) k_tile_count(const uint8_t* __re
   }
 }
 
+// Exclusive scan of the tile counts in place (tile offsets) and the total
+// into *count; one workgroup walks the tiles 1024 at a time.
+constexpr int kScanThreads = 1024;
+
+__global__ void __launch_bounds__(kScanThreads) k_tile_scan(int32_t* __restrict__ tile_counts,
+                                                            int64_t tiles,
+                                                            int32_t* __restrict__ count) {
+  __shared__ int32_t wsum[kScanThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int32_t carry = 0;  // the same in every thread
+  for (int64_t b0 = 0; b0 < tiles; b0 += kScanThreads) {
+    const int64_t b = b0 + tid;
+    const int32_t v = b < tiles ? tile_counts[b] : 0;
+    int32_t x = v;  // inclusive scan within the wave
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int32_t y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) wsum[wave] = x;
+    __syncthreads();
+    int32_t before = 0, total = 0;
+    for (int w = 0; w < kScanThreads / 64; ++w) {
+      before += w < wave ? wsum[w] : 0;
+      total += wsum[w];
+    }
+    if (b < tiles) tile_counts[b] = carry + before + x - v;
+    carry += total;
+    __syncthreads();  // wsum is rewritten by the next round
+  }
+  if (tid == 0) *count = carry;
+}
+
 __global__ void __launch_bounds__(kTileThreads) k_tile_scatter(const uint8_t* __restrict__ fire,
                                                                int64_t n,
-                                                               const int32_t* __restrict__ tile_counts,
-                                                               int32_t* __restrict__ idx,
-                                                               int32_t* __restrict__ count) {
-  __shared__ int64_t red[kTileThreads];
+                                                               const int32_t* __restrict__ tile_off,
+                                                               int32_t* __restrict__ idx) {
   __shared__ int32_t wcount[kTileThreads / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // offset of this tile = sum of the counts of all earlier tiles
-  int64_t s = 0;
-  for (int b = tid; b < (int)blockIdx.x; b += kTileThreads) s += tile_counts[b];
-  red[tid] = s;
-  __syncthreads();
-  for (int o = kTileThreads / 2; o > 0; o >>= 1) {
-    if (tid < o) red[tid] += red[tid + o];
-    __syncthreads();
-  }
-  const int64_t tile_off = red[0];
   const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)wave * (kTile / 4);
   // pass 1: this wave's count
   int32_t c = 0;
@@ -73,7 +95,7 @@ __global__ void __launch_bounds__(kTileThreads) k_tile_scatter(const uint8_t* __
   }
   if (lane == 0) wcount[wave] = c;
   __syncthreads();
-  int64_t off = tile_off;
+  int64_t off = tile_off[blockIdx.x];
   for (int w = 0; w < wave; ++w) off += wcount[w];
   // pass 2: write ascending indices
   for (int st = 0; st < kTile / 4 / 64; ++st) {
@@ -82,11 +104,6 @@ __global__ void __launch_bounds__(kTileThreads) k_tile_scatter(const uint8_t* __
     const uint64_t m = __ballot(f);
     if (f) idx[off + __popcll(m & lanemask_lt(lane))] = (int32_t)u;
     off += __popcll(m);
-  }
-  if (blockIdx.x == gridDim.x - 1 && tid == 0) {
-    int64_t total = tile_off;
-    for (int w = 0; w < kTileThreads / 64; ++w) total += wcount[w];
-    *count = (int32_t)total;
   }
 }
 
@@ -317,8 +334,11 @@ int launch_compact(const uint8_t* fire, int64_t n, int32_t* idx, int32_t* count,
   hipLaunchKernelGGL(k_tile_count, dim3((unsigned)tiles), dim3(kTileThreads), 0, stream, fire, n,
                      tile_counts);
   NSC_CHECK_LAUNCH("k_tile_count");
+  hipLaunchKernelGGL(k_tile_scan, dim3(1), dim3(kScanThreads), 0, stream, tile_counts, tiles,
+                     count);
+  NSC_CHECK_LAUNCH("k_tile_scan");
   hipLaunchKernelGGL(k_tile_scatter, dim3((unsigned)tiles), dim3(kTileThreads), 0, stream, fire, n,
-                     tile_counts, idx, count);
+                     tile_counts, idx);
   NSC_CHECK_LAUNCH("k_tile_scatter");
   return NSC_OK;
 }
