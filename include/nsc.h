@@ -33,8 +33,9 @@
  *    returns a thread-local description.  Outputs are unspecified after an
  *    error.  Faults of already-enqueued work surface on a later HIP call.
  *  - The library owns only what its own *_create calls allocate (packed CNN
- *    weights); it allocates nothing else.  Scratch space is the caller's
- *    workspace, whose size the *_workspace_bytes calls report.
+ *    weights) and one static 64 KB device array per GPU (the scratch of
+ *    nsc_compact_noalloc); it allocates nothing else.  Scratch space is the
+ *    caller's workspace, whose size the *_workspace_bytes calls report.
  *  - Calls that share a workspace or state buffer must be ordered on one
  *    stream by the caller.
  */
@@ -76,6 +77,8 @@ enum { NSC_METRIC_MSE = 0, NSC_METRIC_SAD = 1, NSC_METRIC_NRMSE = 2, NSC_METRIC_
 enum { NSC_F32 = 0, NSC_BF16 = 1 };
 enum { NSC_MAX_CONV = 8, NSC_MAX_DELTA = 256, NSC_MAX_BLOCKS = 1024, NSC_MAX_STRIDE = 4096,
        NSC_MAX_SWEEP = 65535 };
+/* Largest n of nsc_compact_noalloc (16,384 tiles of 4,096 flags). */
+#define NSC_NOALLOC_MAX_FLAGS 67108864LL
 
 /* Stage boundaries at which nsc_cascade_run records optional events:
  * [0] start, [1] after the area sums, [2] after the detector, [3] after the
@@ -225,6 +228,21 @@ int nsc_diff_detect(const nsc_cascade_cfg* cfg, const uint8_t* frames, int64_t n
  * NSC_E_WORKSPACE, NSC_E_HIP. */
 int nsc_compact(const uint8_t* fire, int64_t n, int32_t* idx_out, int32_t* count_out, void* ws,
                 size_t ws_bytes, void* stream);
+
+/* Step 3 without a workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation).  Same outputs as nsc_compact: idx_out (device, n int32) gets
+ * the ascending indices i with fire[i] != 0 and count_out (device, one int32)
+ * their number.  The tile offsets live in a static device array inside the
+ * library (64 KB, held by every GPU the library runs on until the process
+ * ends), which limits n to NSC_NOALLOC_MAX_FLAGS; a larger n is rejected with
+ * NSC_E_WORKSPACE before any GPU work.  The call allocates nothing.  Every
+ * call on one GPU shares that array: calls that overlap on the same GPU (on
+ * different streams or host threads) race and must be ordered by the caller.
+ * The stream must belong to the current device.  Errors: NSC_E_INVAL,
+ * NSC_E_WORKSPACE, NSC_E_HIP. */
+int nsc_compact_noalloc(const uint8_t* fire, int64_t n, int32_t* idx_out, int32_t* count_out,
+                        void* stream);
 
 /* Step 4 (Sec. 4 model, Sec. 7 pre-processing).  For i < *count (device),
  * evaluates the network on frame idx[i]'s area sums: sums (device,

@@ -91,6 +91,7 @@ def lib() -> ctypes.CDLL:
             "nsc_downsample": (ctypes.c_int, [_vp, _i64, _i32, _i32, _i64, _i32, _i32, _vp, _vp]),
             "nsc_diff_detect": (ctypes.c_int, [_vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp]),
             "nsc_compact": (ctypes.c_int, [_vp, _i64, _vp, _vp, _vp, _sz, _vp]),
+            "nsc_compact_noalloc": (ctypes.c_int, [_vp, _i64, _vp, _vp, _vp]),
             "nsc_threshold_sweep": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _i32, _vp, _vp,
                                                    _vp]),
             "nsc_specialized_cnn": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i64, _vp, _vp, _i64,
@@ -262,6 +263,14 @@ def nsc_compact(fire, n, idx_out, count_out, ws, stream=None):
     _check(lib().nsc_compact(_ptr(fire), n, _ptr(idx_out), _ptr(count_out), _ptr(ws),
                              ws.numel() * ws.element_size() if ws is not None else 0,
                              _stream(stream)), "nsc_compact")
+
+
+NSC_NOALLOC_MAX_FLAGS = 67108864
+
+
+def nsc_compact_noalloc(fire, n, idx_out, count_out, stream=None):
+    _check(lib().nsc_compact_noalloc(_ptr(fire), n, _ptr(idx_out), _ptr(count_out),
+                                     _stream(stream)), "nsc_compact_noalloc")
 
 
 def nsc_specialized_cnn(cnn: Cnn, sums, sums_h, sums_w, den, idx, count, max_count, logit_out,

@@ -520,6 +520,18 @@ int nsc_compact(const uint8_t* fire, int64_t n, int32_t* idx_out, int32_t* count
   return launch_compact(fire, n, idx_out, count_out, static_cast<int32_t*>(ws), (hipStream_t)stream);
 }
 
+int nsc_compact_noalloc(const uint8_t* fire, int64_t n, int32_t* idx_out, int32_t* count_out,
+                        void* stream) {
+  g_err[0] = 0;
+  NSC_REQUIRE(n >= 0 && n <= kMaxFrames, NSC_E_INVAL, "n = %lld out of range", (long long)n);
+  NSC_REQUIRE(n <= NSC_NOALLOC_MAX_FLAGS, NSC_E_WORKSPACE,
+              "n = %lld exceeds the %lld flags the static scratch holds", (long long)n,
+              (long long)NSC_NOALLOC_MAX_FLAGS);
+  NSC_REQUIRE(count_out != nullptr, NSC_E_INVAL, "count_out is NULL");
+  if (n > 0) NSC_REQUIRE(fire && idx_out, NSC_E_INVAL, "fire or idx_out is NULL");
+  return launch_compact_noalloc(fire, n, idx_out, count_out, (hipStream_t)stream);
+}
+
 int nsc_specialized_cnn(const nsc_cnn* cnn, const int32_t* sums, int32_t sums_h, int32_t sums_w,
                         int64_t den, const int32_t* idx, const int32_t* count, int64_t max_count,
                         float* logit_out, float* prob_out, void* ws, size_t ws_bytes,

@@ -16,6 +16,8 @@
 // across tiles per column, and a per-tile sequential walk down each column.
 #include "nsc_internal.h"
 
+#include <mutex>
+
 namespace nsc {
 namespace {
 
@@ -341,6 +343,53 @@ int launch_compact(const uint8_t* fire, int64_t n, int32_t* idx, int32_t* count,
                      tile_counts, idx);
   NSC_CHECK_LAUNCH("k_tile_scatter");
   return NSC_OK;
+}
+
+// Compaction without a caller workspace, for callers that cannot allocate:
+// the tile offsets live in this file-scope device array (every GPU holds its
+// own copy until the process ends), so at most NSC_NOALLOC_MAX_FLAGS flags
+// (kNoAllocTiles tiles) per call.  Every call on one GPU shares the array:
+// calls that overlap on a GPU race.  Nothing in it has to start at zero
+// (each call writes every tile count it reads).
+constexpr int64_t kNoAllocTiles = NSC_NOALLOC_MAX_FLAGS / kTile;
+static_assert(NSC_NOALLOC_MAX_FLAGS % kTile == 0, "the flag limit is whole tiles");
+static __device__ __align__(256) int32_t scratch[kNoAllocTiles];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+int32_t* g_scratch[kMaxDevices] = {};
+}  // namespace
+
+// Device address of the current device's copy of `scratch`, looked up once per
+// device (the array's name in host code is not a device address).
+int noalloc_scratch(int32_t** out) {
+  int dev = -1;
+  NSC_TRY_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(NSC_E_HIP, "device %d beyond the %d devices the static scratch tracks", dev,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(NSC_E_HIP, "hipGetSymbolAddress of the compaction scratch failed on device %d: %s",
+                  dev, hipGetErrorString(e));
+    g_scratch[dev] = static_cast<int32_t*>(p);
+  }
+  *out = g_scratch[dev];
+  return NSC_OK;
+}
+
+int launch_compact_noalloc(const uint8_t* fire, int64_t n, int32_t* idx, int32_t* count,
+                           hipStream_t stream) {
+  if (compact_tiles(n) > kNoAllocTiles)
+    return fail(NSC_E_WORKSPACE, "%lld flags exceed the static scratch's %lld", (long long)n,
+                (long long)NSC_NOALLOC_MAX_FLAGS);
+  int32_t* tiles = nullptr;
+  if (int rc = noalloc_scratch(&tiles)) return rc;
+  return launch_compact(fire, n, idx, count, tiles, stream);
 }
 
 ResolvePlan make_resolve_plan(int64_t n, int64_t t0, int32_t delta) {

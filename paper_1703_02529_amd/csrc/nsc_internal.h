@@ -113,6 +113,9 @@ int launch_diff(const DiffArgs& a, hipStream_t stream);
 int64_t compact_tiles(int64_t n);
 int launch_compact(const uint8_t* fire, int64_t n, int32_t* idx, int32_t* count, int32_t* tile_counts,
                    hipStream_t stream);
+// The same with the tile offsets in a static device array (no workspace).
+int launch_compact_noalloc(const uint8_t* fire, int64_t n, int32_t* idx, int32_t* count,
+                           hipStream_t stream);
 
 // Label resolution (PREV: reuse the decision of frame t-delta; FIXED: 0).
 struct ResolvePlan {

@@ -156,6 +156,17 @@ def test_status_strings():
     assert nsc.status_string(-99) == "NSC_E_UNKNOWN"
 
 
+def test_compact_noalloc_validation():
+    """nsc_compact_noalloc refuses bad arguments on the host, before any HIP call."""
+    L = nsc.lib()
+    big = nsc.NSC_NOALLOC_MAX_FLAGS + 1
+    assert L.nsc_compact_noalloc(16, big, 16, 16, None) == nsc.NSC_E_WORKSPACE
+    assert "exceeds" in nsc.last_error()
+    assert L.nsc_compact_noalloc(16, -1, 16, 16, None) == nsc.NSC_E_INVAL
+    assert L.nsc_compact_noalloc(16, 10, 16, None, None) == nsc.NSC_E_INVAL
+    assert L.nsc_compact_noalloc(None, 10, 16, 16, None) == nsc.NSC_E_INVAL
+
+
 def test_compact_workspace_size():
     assert nsc.nsc_compact_workspace_bytes(0) >= 4
     assert nsc.nsc_compact_workspace_bytes(4097) >= 2 * 4
