@@ -1,28 +1,34 @@
 #!/usr/bin/env python3
 """Cascade frames/s on one MI355X, with roofline fractions and the oracle's CPU rate.
 
-Workload (default): 100,000 synthetic fixed-camera frames of 640x480 RGB
-uint8, already resident in HBM; area downsample to 50x50, global MSE against
-frame t-15, delta_diff = 15; specialized CNN (2 x conv3x3 32 + ReLU +
-max-pool, dense 128, bf16) on the frames that fire; c_low = 0.2, c_high =
-0.8.  One step is one nsc_cascade_run over all frames (downsample, detector,
-compaction, CNN, decisions and label resolution).
+Workload (default, the largest): 1,000,000 synthetic fixed-camera frames of
+1920x1080 RGB uint8 in chunks of 4,096 through two frame buffers on two HIP
+streams; area downsample to 100x100, 10x10 blocked logistic score against
+frame t-30, delta_diff = 0; specialized CNN (4 x conv3x3 64, max-pool after
+the second and fourth, dense 128, bf16) on the frames that fire; c_low = 0.2,
+c_high = 0.8; 10 % of frames hold objects (--occupancy 0.01 / 0.5 give the
+other two points of its occupancy sweep).  One step is one pass over the
+whole video: each chunk is rendered on the device into a frame buffer, then
+its nsc_cascade_run (downsample, detector, compaction, CNN, decisions and
+label resolution) runs alone on the GPU and is timed with HIP events on the
+cascade stream.  `value` is the cascade-only rate (generator time excluded,
+as the paper excludes decoding); after the timed steps one more pass with the
+generator filling the other buffer concurrently gives the overlapped
+wall-clock rate, reported beside it.  The stage split comes from events at
+the stage boundaries of every chunk.
 
---workload hd-ref / hd-blocked / fhd-stream run the larger videos in chunks
-through two frame buffers on two streams, the synthetic generator filling one
-buffer while the cascade reads the other:
+--workload hd-ref / hd-blocked run the other chunked videos the same way:
   hd-ref      100,000 frames of 1280x720, MSE against a fixed median-background
               image, 4-layer 64-channel CNN (the CNN-heavy regime), chunks of 16,384;
   hd-blocked  200,000 frames of 1280x720, 10x10 blocked logistic score against
-              frame t-1, 3-layer 64-channel CNN, chunks of 16,384;
-  fhd-stream  1,000,000 frames of 1920x1080, blocked score against frame t-30,
-              4-layer 64-channel CNN, chunks of 4,096; 10 % of frames hold
-              objects, --occupancy 0.01 / 0.5 give the other two points of
-              its occupancy sweep.
-Their `value` is the cascade-only rate (each chunk's cascade timed alone with
-HIP events, generator time excluded, as the paper excludes decoding); the
-overlapped wall-clock rate, bound by the generator, is reported beside it, and
-the stage split comes from events at the stage boundaries of every chunk.
+              frame t-1, 3-layer 64-channel CNN, chunks of 16,384.
+--workload vga and tiny keep a whole video resident in HBM and time one
+nsc_cascade_run over all its frames per step:
+  vga         100,000 frames of 640x480, global MSE against frame t-15,
+              delta_diff 15, 2 x conv3x3 32 + max-pool, dense 128, bf16;
+  tiny        1,000 frames of 100x100 (30 MB, cache-resident and
+              latency-bound), global MSE against frame t-1, delta_diff 20,
+              fp32 CNN 2 x conv3x3 32, dense 32.
 
 --workload vga-sweep measures the threshold search of the cost-based optimizer
 (Sec. 6.3) on the 640x480 video: one cascade run with delta_diff = -inf logs
@@ -40,8 +46,8 @@ call through nsc_group_run; the same frames through one nsc_cascade_run per
 camera are timed beside it (`per_camera_calls`), with their outputs checked
 to be identical.
 
---metric sad / nrmse / psnr runs the 640x480 workload with one of the
-alternative detector metrics (Sec. 5), at a threshold matching MSE 15.
+--metric sad / nrmse / psnr runs the 640x480 workload (--workload vga) with one
+of the alternative detector metrics (Sec. 5), at a threshold matching MSE 15.
 
 Every run also measures the peaks the roofline fractions are quoted against:
 a streaming read of the resident frame buffer (HBM) and a loop of independent
@@ -67,6 +73,9 @@ AREA_KERNEL = "k_area_sums_wave"
 AREA_SOURCES = ("paper_1703_02529_amd/csrc/area_diff.hip", "paper_1703_02529_amd/csrc/nsc_internal.h")
 COPY_BYTES = 1 << 31           # plain copy of known size for counter calibration
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+DTYPE_BF16 = ("u8 frames, i32/i64 detector; CNN: bf16 weights, bf16 input, later activations "
+              "as bf16 hi/lo pairs (two MFMAs per product), fp32 accumulate")
+DTYPE_FP32 = "u8 frames, i32/i64 detector; CNN: fp32 weights and activations, fp32 MFMA"
 FP32_PEAK_TFLOPS = 157.3
 
 
@@ -207,37 +216,112 @@ def measured_peaks(torch, buf, nbytes: int) -> dict:
     return res
 
 
-def cpu_baseline(wl, budget_s: float, lr_w=None, ref_img=None) -> dict:
-    """The oracle, single-threaded, on a contiguous window of the same video."""
+def cpu_model() -> str:
+    """The host CPU's model name (first /proc/cpuinfo entry)."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(wl, budget_s: float, fire_frac: float, lr_w=None, ref_img=None,
+                 n_video=None) -> dict:
+    """The oracle, single-threaded, on a window of the same video whose share
+    of frames with objects matches the video's, so that its detector fires on
+    about as many frames as the GPU run's (fire_frac, used only to size the
+    window: a fired frame costs the oracle the CNN as well).  The window is
+    continued from the area sums of the frames before it (computed untimed;
+    their decisions are taken as 0, which only labels inherited in the
+    window's first frames), so no frame is forced to fire."""
     import numpy as np
 
     import oracle
     import synth
 
     v = synth.Video(wl.video)
+    n_video = n_video or wl.video.n
     blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
     ref_sums = oracle.area_sums(ref_img, wl.dd_h, wl.dd_w) if ref_img is not None else None
     cfg, keep = oracle.make_cfg(wl, lr_w=lr_w, ref_sums=ref_sums)
-    occ = v.occupied
-    start = int(np.flatnonzero(occ)[0]) if occ.any() else 0
-    start = max(0, start - 200)
-    # probe a few frames to size the sample to the budget
-    n_probe = 40 if wl.video.w <= 640 else 8
-    probe = v.frames(start, start + n_probe)
+    D = oracle.history(cfg)
+
+    def state_before(t0):
+        if D == 0 or t0 == 0:
+            return None
+        S = np.stack([oracle.area_sums(v.frame(t), wl.dd_h, wl.dd_w).reshape(-1)
+                      for t in range(t0 - D, t0)]).astype(np.int64)
+        return S, np.zeros(D, np.uint8)
+
+    def run(t0, m):
+        st = state_before(t0)
+        frames = v.frames(t0, t0 + m)
+        t = time.perf_counter()
+        out, _ = oracle.cascade(cfg, wl.cnn, blob, frames, t0=t0, state=st)
+        return out, time.perf_counter() - t
+
+    # cost of a frame that does not fire (area sums and score) and of one that
+    # does (plus the CNN): frames [D, D + k) of an unoccupied stretch, then the
+    # same with every frame firing (delta_diff = -inf)
+    quiet = np.flatnonzero(~v.occupied[:n_video])
+    t_q = int(quiet[quiet >= D][0]) if (quiet >= D).any() else D
+    k = 4 if wl.video.w > 640 else 16
+    o1, dt1 = run(t_q, k)
+    cfg_all, keep2 = oracle.make_cfg(wl, lr_w=lr_w, ref_sums=ref_sums, delta_diff=-math.inf)
+    st = state_before(t_q)
     t = time.perf_counter()
-    oracle.cascade(cfg, wl.cnn, blob, probe, t0=0)
-    per = (time.perf_counter() - t) / n_probe
-    n = int(max(16, min(4000, budget_s / max(per, 1e-6))))
-    log(f"cpu baseline: oracle ~{per * 1e3:.1f} ms/frame, sampling {n} frames from {start}")
-    frames = v.frames(start, start + n)
-    t = time.perf_counter()
-    out, _ = oracle.cascade(cfg, wl.cnn, blob, frames, t0=0)
-    dt = time.perf_counter() - t
-    forced = f"first {wl.delta} forced to fire; " if wl.ref_mode == 0 else ""
-    return {"value": n / dt, "unit": "frames/s", "cores": 1, "kind": "oracle",
-            "sample": f"frames [{start}, {start + n}) of the same video run as their own video "
-                      f"({forced}{out['fired']} fired, {out['fired'] / n:.1%}); {dt:.1f} s "
-                      f"single-threaded fp64; host has {os.cpu_count()} logical CPUs"}
+    oracle.cascade(cfg_all, wl.cnn, blob, v.frames(t_q, t_q + k), t0=t_q, state=st)
+    dt_all = time.perf_counter() - t
+    t_f = dt_all / k
+    f1 = o1["fired"]
+    t_nf = (dt1 - f1 * t_f) / (k - f1) if f1 < k else t_f
+    t_nf = min(max(t_nf, 1e-6), t_f)
+    per = (1 - fire_frac) * t_nf + fire_frac * t_f
+    n = int(max(64, min(20000, budget_s / max(per, 1e-6))))
+    n = min(n, n_video - D)
+    # 8 windows of m frames, evenly spaced over the video, at the phase whose
+    # share of frames with objects is closest to the video's
+    n_win = 8
+    m = max(8, n // n_win)
+    occ = v.occupied[:n_video].astype(np.int64)
+    target = occ.mean()
+    csum = np.concatenate([[0], np.cumsum(occ)])
+    spacing = (n_video - D - m) // n_win
+    best = None
+    for o in range(0, max(1, spacing), max(1, m // 4)):
+        starts = D + o + spacing * np.arange(n_win)
+        share = float((csum[starts + m] - csum[starts]).sum()) / (n_win * m)
+        if best is None or abs(share - target) < abs(best[1] - target):
+            best = (starts, share)
+    starts, share = best
+    log(f"cpu baseline: oracle {t_nf * 1e3:.1f} ms per quiet frame, {t_f * 1e3:.1f} ms per fired "
+        f"frame; {n_win} windows of {m} frames (share with objects {share:.3f}, video "
+        f"{target:.3f})")
+    dt = 0.0
+    fired = 0
+    for s0 in starts:
+        out, d = run(int(s0), m)
+        dt += d
+        fired += out["fired"]
+    tot = n_win * m
+    # the sample's time per frame, moved to the GPU run's fire fraction by the
+    # oracle's own cost of a fired frame over a quiet one (probed above)
+    per_frame = dt / tot + (fire_frac - fired / tot) * (t_f - t_nf)
+    return {"value": 1.0 / per_frame, "unit": "frames/s", "cores": 1, "kind": "oracle",
+            "sample_rate": tot / dt,
+            "sample": f"{n_win} windows of {m} frames of the same video, {spacing} frames apart "
+                      f"from frame {int(starts[0])}, each continued from the area sums of the {D} "
+                      f"frames before it: {dt:.1f} s single-threaded fp64, {tot / dt:.1f} "
+                      f"frames/s with {fired} fired ({fired / tot:.1%}; {share:.1%} of frames "
+                      f"with objects, video {target:.1%}); value = 1 / (sample time per frame + "
+                      f"(fire fraction of the GPU run {fire_frac:.2%} - the sample's) x (oracle "
+                      f"time of a fired frame {t_f * 1e3:.1f} ms - of a quiet one "
+                      f"{t_nf * 1e3:.1f} ms))",
+            "cpu_model": cpu_model(), "host_logical_cpus": os.cpu_count()}
 
 
 CHUNKED = ("hd-ref", "hd-blocked", "fhd-stream")
@@ -353,7 +437,7 @@ def bench_cameras(args):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "u8 frames, i32/i64 detector, bf16 CNN (fp32 accumulate)",
+        "dtype": DTYPE_BF16,
         "data": "synthetic",
         "config": {
             "workload": f"cameras-{CAMERAS}x{CAM_BATCH}-640x480-prev15-bf16",
@@ -399,7 +483,7 @@ def bench_cameras(args):
     if args.cpu_seconds > 0:
         # camera 0's video, long enough for the sample
         w0 = wls[0].replace(video=dataclasses.replace(wls[0].video, n=base.video.n))
-        result["cpu_baseline"] = cpu_baseline(w0, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(w0, args.cpu_seconds, fired / m)
     print(json.dumps(result), flush=True)
 
 
@@ -546,6 +630,10 @@ def bench_chunked(args):
         wl = wl.with_occupancy(args.occupancy)
     chunk = wl.chunk or 16384
     n, fb = wl.video.n, wl.video.frame_bytes
+    if args.frames is not None:
+        if not 0 < args.frames <= n:
+            raise SystemExit(f"--frames must lie in 1..{n}")
+        n = args.frames
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     v = synth.Video(wl.video)
@@ -580,35 +668,46 @@ def bench_chunked(args):
     if args.calibrate_copy:
         copy_calibration(torch, dev)
     peaks = measured_peaks(torch, sc.bufs[0], chunk * fb)
+    # a step: frames [0, n) in chunks, each chunk's cascade alone on the GPU
+    # (its fill waits for the previous cascade), timed with events per chunk
     for _ in range(args.warmup):
-        sc.run(min(n, 2 * chunk), produce, label, defer, fire=fire)
+        sc.run(n, produce, label, defer, fire=fire, overlap=False)
     torch.cuda.synchronize()
     hip = HipEvents()
     n_chunks = -(-n // chunk)
     evs = [hip.create(6) for _ in range(n_chunks)]
-    alone, over, stage_tot = [], [], np.zeros(5)
+    alone, stage_tot = [], np.zeros(5)
+    torch.cuda.synchronize()
+    t_steps = time.perf_counter()
     for k in range(args.steps):
         alone.append(sc.run(n, produce, label, defer, fire=fire, timing=True, overlap=False,
                             stage_events=lambda j: evs[j]))
         stage_tot += np.array([[hip.ms(e[i], e[i + 1]) for i in range(5)] for e in evs]).sum(0)
-        log(f"pass {k}: chunks run alone: {alone[-1]}")
-        over.append(sc.run(n, produce, label, defer, fire=fire, timing=True, overlap=True))
-        log(f"pass {k}: overlapped: {over[-1]}")
+        log(f"step {k}: {alone[-1]}")
+    torch.cuda.synchronize()
+    steps_wall = time.perf_counter() - t_steps
+    # the generator filling the other buffer while the cascade runs: wall clock of one pass
+    over = sc.run(n, produce, label, defer, fire=fire, timing=True, overlap=True)
+    log(f"overlapped pass: {over}")
     for e in evs:
         hip.destroy(e)
-    fired = int(fire.sum().item())
+    fired = int(fire[:n].sum().item())
     sc.close()
     stage = stage_tot / args.steps
     casc_ms = sum(a["cascade_ms"] for a in alone) / len(alone)
-    wall_ms = sum(o["wall_ms"] for o in over) / len(over)
+    wall_ms = over["wall_ms"]
     area_ms, cnn_ms = float(stage[0]), float(stage[3])
     achieved = n * fb / (area_ms * 1e-3) / 1e9
+    diff_ms = float(stage[0] + stage[1] + stage[2])
+    diff_gbs = (n * fb + n) / (diff_ms * 1e-3) / 1e9
     cnn_tflops = fired * cnn_flops(wl.cnn) / (cnn_ms * 1e-3) / 1e12 if cnn_ms > 0 else 0.0
     busy, busy_src = measured_mfma_busy(wl.name)
     # HBM bytes per area launch (the mean over the chunks, as avg_launch_ms);
     # the area kernel does not depend on the occupancy
     base = {"hd-ref": W.HD_REF, "hd-blocked": W.HD_BLOCKED, "fhd-stream": W.FHD_STREAM}[args.workload]
     traffic, traffic_src = measured_traffic(base.name)
+    if args.frames is not None and traffic is not None:
+        traffic_src += " (counters of the whole video)"
     layers = ", ".join(f"{c}{'+pool' if p else ''}" for c, p in zip(wl.cnn.conv, wl.cnn.pool))
     result = {
         "metric": "cascade frames/sec on 1 MI355X + % HBM roofline (diff) / % MFMA peak (CNN)",
@@ -621,17 +720,21 @@ def bench_chunked(args):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "u8 frames, i32/i64 detector, bf16 CNN (fp32 accumulate)",
+        "dtype": DTYPE_BF16,
         "data": "synthetic",
-        "config": {"workload": wl.name, "frames": n, "frame": f"{wl.video.w}x{wl.video.h} RGB u8",
-                   "chunk": chunk,
+        "config": {"workload": wl.name + ("" if n == wl.video.n else f"-first{n}"),
+                   "frames": n, "frame": f"{wl.video.w}x{wl.video.h} RGB u8",
+                   "chunk": chunk, "chunks": n_chunks, "occupancy": wl.video.occupancy,
                    "detector": f"{wl.dd_w}x{wl.dd_h}, " + (
                        "fixed median-background reference" if wl.ref_mode == W.FIXED else
                        f"frame t-{wl.delta}") + (
                        f", {wl.grid[0]}x{wl.grid[1]} blocked logistic score" if wl.grid != (1, 1)
                        else ", global MSE") + f", delta_diff {wl.delta_diff}",
                    "cnn": f"conv3x3 [{layers}], dense {wl.cnn.dense}, sigmoid; bf16",
-                   "c_low": wl.c_low, "c_high": wl.c_high, "fired": fired},
+                   "c_low": wl.c_low, "c_high": wl.c_high, "fired": fired,
+                   "step": "one pass over all frames; each chunk rendered into one of two "
+                           "frame buffers, then its cascade timed alone (HIP events on the "
+                           "cascade stream); ms_per_step is the cascade time of a pass"},
         "roofline": {
             "bound": "hbm",
             "kernel": AREA_KERNEL,
@@ -641,11 +744,16 @@ def bench_chunked(args):
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": traffic,
             "traffic_source": traffic_src,
-            "bytes_per_launch": chunk * fb,
+            "bytes_per_launch": n * fb / n_chunks,
             "avg_launch_ms": area_ms / n_chunks,
             "measured_peak": peaks["hbm_read_gbs"],
             "frac_of_measured": achieved / peaks["hbm_read_gbs"],
         },
+        "diff_compaction_stage": {
+            "what": "area sums + detector + compaction (stages 1-3): raw frame bytes and fire "
+                    "flags over the stages' summed time",
+            "achieved": diff_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": diff_gbs / HBM_PEAK_GBS, "ms_per_step": diff_ms},
         "stages_ms": {"area_sums": area_ms, "detector": float(stage[1]),
                       "compaction": float(stage[2]), "cnn": cnn_ms, "resolve": float(stage[4])},
         "cnn_mfma": {"achieved_tflops": cnn_tflops, "peak_tflops": BF16_PEAK_TFLOPS,
@@ -657,65 +765,21 @@ def bench_chunked(args):
         "cascade_only_ms": casc_ms,
         "overlapped_wall_ms": wall_ms,
         "overlapped_wall_fps": n / (wall_ms * 1e-3),
-        "note": "value: each chunk's cascade timed alone with HIP events (generator excluded); "
-                "overlapped: generator filling the other buffer concurrently, wall clock",
+        "steps_wall_s": steps_wall,
+        "note": "value: each chunk's cascade timed alone with HIP events (generator excluded, as "
+                "the paper excludes decoding); overlapped: one more pass with the generator "
+                "filling the other buffer concurrently, wall clock",
     }
     torch.cuda.empty_cache()
-    result["cpu_baseline"] = (cpu_baseline(wl, args.cpu_seconds, lr_w=lr, ref_img=ref_img)
+    result["cpu_baseline"] = (cpu_baseline(wl, args.cpu_seconds, fired / n, lr_w=lr,
+                                           ref_img=ref_img, n_video=n)
                               if args.cpu_seconds > 0 else None)
     print(json.dumps(result), flush=True)
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=None, help="timed steps (20; chunked: 1)")
-    ap.add_argument("--warmup", type=int, default=None, help="warm-up steps (3; chunked: 1)")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0,
-                    help="oracle time budget for the CPU baseline (0 disables it)")
-    ap.add_argument("--calibrate-copy", action="store_true",
-                    help="also run a plain copy of known size (for counter calibration)")
-    ap.add_argument("--workload", choices=("vga", "vga-sweep", "cameras") + CHUNKED,
-                    default="vga")
-    ap.add_argument("--metric", choices=tuple(METRIC_DD), default="mse",
-                    help="detector metric on the 640x480 workload (Sec. 5 and the alternatives "
-                         "it names), at the threshold matching MSE 15 (see METRIC_DD)")
-    ap.add_argument("--occupancy", type=float, default=None,
-                    help="fraction of frames with objects for the chunked workloads (the "
-                         "1920x1080 stream is measured at 0.01, 0.1 and 0.5; default: the "
-                         "workload's own)")
-    ap.add_argument("--check-stride", type=int, default=1,
-                    help="frame skipping on the 640x480 workload: check every s-th frame "
-                         "(s must divide 15); 1 is the headline configuration")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (the cascade's frames are independent across "
-              f"streams; see the design notes for how it would shard): got --gpus {args.gpus}",
-              file=sys.stderr)
-        sys.exit(2)
-    if args.workload == "cameras":
-        if args.steps is None:
-            args.steps = 20
-        if args.warmup is None:
-            args.warmup = 2
-        bench_cameras(args)
-        return
-    if args.workload == "vga-sweep":
-        if args.steps is None:
-            args.steps = 20
-        if args.warmup is None:
-            args.warmup = 2
-        bench_sweep(args)
-        return
-    chunked = args.workload in CHUNKED
-    if args.steps is None:
-        args.steps = 1 if chunked else 20
-    if args.warmup is None:
-        args.warmup = 1 if chunked else 3
-    if chunked:
-        bench_chunked(args)
-        return
-
+def bench_resident(args):
+    """A video resident in HBM, one nsc_cascade_run over all its frames per
+    step: the 640x480 workload (vga) or the 1,000-frame 100x100 one (tiny)."""
     import numpy as np
     import torch
 
@@ -723,7 +787,9 @@ def main():
     from paper_1703_02529_amd.runner import CascadeRunner
     from synth import workloads as W
 
-    wl = W.VGA.replace(check_stride=args.check_stride)
+    tiny = args.workload == "tiny"
+    base = W.TINY if tiny else W.VGA
+    wl = base.replace(check_stride=args.check_stride)
     if args.metric != "mse":
         code, dd = METRIC_DD[args.metric]
         wl = wl.replace(metric=code, delta_diff=dd, name=f"{wl.name}-{args.metric}")
@@ -731,7 +797,7 @@ def main():
     fb = wl.video.frame_bytes
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    log(f"workload {wl.name}: {n} frames x {fb} bytes = {n * fb / 1e9:.1f} GB")
+    log(f"workload {wl.name}: {n} frames x {fb} bytes = {n * fb / 1e9:.2f} GB")
 
     v = synth.Video(wl.video)
     frames = torch.empty(n * fb, dtype=torch.uint8, device=dev)
@@ -771,13 +837,18 @@ def main():
     checked = -(-n // wl.check_stride)        # frames the detector reads
     area_bytes = checked * fb                 # algorithmic: every checked frame's bytes once
     achieved = area_bytes / (area_ms * 1e-3) / 1e9
-    traffic, traffic_src = measured_traffic(W.VGA.name)  # the area kernel ignores the metric
+    diff_ms = float(stage[:, 0:3].sum(1).mean())
+    diff_gbs = (area_bytes + checked) / (diff_ms * 1e-3) / 1e9
+    traffic, traffic_src = measured_traffic(base.name)  # the area kernel ignores the metric
     if wl.check_stride != 1:
         traffic, traffic_src = None, "counters were taken without frame skipping"
     cnn_ms = float(stage[:, 3].mean())
     fired = int(stats["fired"])
-    cnn_tflops = fired * cnn_flops(wl.cnn) / (cnn_ms * 1e-3) / 1e12 if cnn_ms > 0 else 0.0
-    busy, busy_src = measured_mfma_busy(W.VGA.name)  # the network does not depend on the metric
+    flop = cnn_flops(wl.cnn)
+    cnn_tflops = fired * flop / (cnn_ms * 1e-3) / 1e12 if cnn_ms > 0 else 0.0
+    busy, busy_src = measured_mfma_busy(base.name)  # the network does not depend on the metric
+    peak_tf = BF16_PEAK_TFLOPS if wl.cnn.bf16 else FP32_PEAK_TFLOPS
+    layers = ", ".join(f"{c}{'+pool' if p else ''}" for c, p in zip(wl.cnn.conv, wl.cnn.pool))
 
     result = {
         "metric": "cascade frames/sec on 1 MI355X + % HBM roofline (diff) / % MFMA peak (CNN)",
@@ -790,7 +861,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "u8 frames, i32/i64 detector, bf16 CNN (fp32 accumulate)",
+        "dtype": DTYPE_BF16 if wl.cnn.bf16 else DTYPE_FP32,
         "data": "synthetic",
         "config": {
             "workload": wl.name,
@@ -800,12 +871,14 @@ def main():
                         f"{'-PSNR' if args.metric == 'psnr' else args.metric.upper()} vs frame "
                         f"t-{wl.delta}, delta_diff {wl.delta_diff:.6g}",
             "check_stride": wl.check_stride,
-            "cnn": "2 x (conv3x3 32 + ReLU + maxpool2), dense 128, sigmoid; bf16",
+            "cnn": f"conv3x3 [{layers}], dense {wl.cnn.dense}, sigmoid; "
+                   f"{'bf16' if wl.cnn.bf16 else 'fp32'}",
             "c_low": wl.c_low,
             "c_high": wl.c_high,
             "fired": fired,
             "deferred": int(stats["deferred"]),
             "positive": int(stats["positive"]),
+            "step": "one nsc_cascade_run over all frames, resident in HBM",
         },
         "roofline": {
             "bound": "hbm",
@@ -821,6 +894,11 @@ def main():
             "measured_peak": peaks["hbm_read_gbs"],
             "frac_of_measured": achieved / peaks["hbm_read_gbs"],
         },
+        "diff_compaction_stage": {
+            "what": "area sums + detector + compaction (stages 1-3): raw frame bytes and fire "
+                    "flags over the stages' summed time",
+            "achieved": diff_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": diff_gbs / HBM_PEAK_GBS, "ms_per_step": diff_ms},
         "stages_ms": {
             "area_sums": area_ms,
             "detector": float(stage[:, 1].mean()),
@@ -831,24 +909,87 @@ def main():
         },
         "cnn_mfma": {
             "achieved_tflops": cnn_tflops,
-            "peak_tflops": BF16_PEAK_TFLOPS,
-            "frac": cnn_tflops / BF16_PEAK_TFLOPS,
-            "measured_peak_tflops": peaks["mfma_bf16_tflops"],
-            "frac_of_measured": cnn_tflops / peaks["mfma_bf16_tflops"],
-            "flop_per_survivor": cnn_flops(wl.cnn),
+            "peak_tflops": peak_tf,
+            "frac": cnn_tflops / peak_tf,
+            "measured_peak_tflops": peaks["mfma_bf16_tflops"] if wl.cnn.bf16 else None,
+            "frac_of_measured": cnn_tflops / peaks["mfma_bf16_tflops"] if wl.cnn.bf16 else None,
+            "flop_per_survivor": flop,
             "survivors": fired,
             "busy_counter": busy,
             "busy_source": busy_src,
         },
     }
+    if tiny:
+        result["roofline"]["note"] = (
+            f"{n * fb / 1e6:.0f} MB of frames fit in the 256 MB MALL: the step is latency-bound "
+            "(a few microseconds per launch), so its HBM fraction is not a meaningful roofline")
     del frames
     run.close()
     torch.cuda.empty_cache()
     if args.cpu_seconds > 0:
-        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, fired / n)
     else:
         result["cpu_baseline"] = None
     print(json.dumps(result), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (resident workloads 20; chunked 10)")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="warm-up steps (resident 3; chunked 2)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="oracle time budget for the CPU baseline (0 disables it)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain copy of known size (for counter calibration)")
+    ap.add_argument("--workload", choices=("tiny", "vga", "vga-sweep", "cameras") + CHUNKED,
+                    default="fhd-stream")
+    ap.add_argument("--frames", type=int, default=None,
+                    help="chunked workloads: run only the first N frames of the video (for "
+                         "profiling runs; the benchmark line runs all of them)")
+    ap.add_argument("--metric", choices=tuple(METRIC_DD), default="mse",
+                    help="detector metric on the 640x480 workload (Sec. 5 and the alternatives "
+                         "it names), at the threshold matching MSE 15 (see METRIC_DD)")
+    ap.add_argument("--occupancy", type=float, default=None,
+                    help="fraction of frames with objects for the chunked workloads (the "
+                         "1920x1080 stream is measured at 0.01, 0.1 and 0.5; default: the "
+                         "workload's own)")
+    ap.add_argument("--check-stride", type=int, default=1,
+                    help="frame skipping on the 640x480 workload: check every s-th frame "
+                         "(s must divide 15); 1 is the headline configuration")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (the cascade's frames are independent across "
+              f"streams; see the design notes for how it would shard): got --gpus {args.gpus}",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.workload == "cameras":
+        if args.steps is None:
+            args.steps = 20
+        if args.warmup is None:
+            args.warmup = 2
+        bench_cameras(args)
+        return
+    if args.workload == "vga-sweep":
+        if args.steps is None:
+            args.steps = 20
+        if args.warmup is None:
+            args.warmup = 2
+        bench_sweep(args)
+        return
+    chunked = args.workload in CHUNKED
+    if args.metric != "mse" and args.workload not in ("vga", "tiny"):
+        raise SystemExit("--metric applies to the resident workloads (--workload vga or tiny)")
+    if args.steps is None:
+        args.steps = 10 if chunked else 20
+    if args.warmup is None:
+        args.warmup = 2 if chunked else 3
+    if chunked:
+        bench_chunked(args)
+    else:
+        bench_resident(args)
 
 
 if __name__ == "__main__":

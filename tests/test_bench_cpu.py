@@ -35,3 +35,13 @@ def test_cnn_flops_per_survivor():
     assert bench.cnn_flops(W.HD_REF.cnn) == hd4 == 287_479_552
     assert bench.cnn_flops(W.HD_BLOCKED.cnn) == hd3 == 65_631_872
     assert bench.cnn_flops(W.FHD_STREAM.cnn) == hd4
+
+
+def test_cpu_baseline_window_and_fields():
+    """The CPU baseline leg runs the oracle on a window continued from the
+    frames before it (no forced firing) and names the host CPU."""
+    r = bench.cpu_baseline(W.VGA, 1.0, 0.226)
+    assert r["value"] > 0 and r["cores"] == 1 and r["kind"] == "oracle"
+    assert r["cpu_model"] and "continued from the area sums of the 15 frames" in r["sample"]
+    r = bench.cpu_baseline(W.TINY, 0.3, 0.3)
+    assert r["value"] > 0
