@@ -628,7 +628,7 @@ def bench_chunked(args):
     wl = {"hd-ref": W.HD_REF, "hd-blocked": W.HD_BLOCKED, "fhd-stream": W.FHD_STREAM}[args.workload]
     if args.occupancy is not None and args.occupancy != wl.video.occupancy:
         wl = wl.with_occupancy(args.occupancy)
-    chunk = wl.chunk or 16384
+    chunk = args.chunk or wl.chunk or 16384
     n, fb = wl.video.n, wl.video.frame_bytes
     if args.frames is not None:
         if not 0 < args.frames <= n:
@@ -722,7 +722,8 @@ def bench_chunked(args):
         "vs_baseline": None,
         "dtype": DTYPE_BF16,
         "data": "synthetic",
-        "config": {"workload": wl.name + ("" if n == wl.video.n else f"-first{n}"),
+        "config": {"workload": wl.name + ("" if n == wl.video.n else f"-first{n}") +
+                               ("" if chunk == (wl.chunk or 16384) else f"-chunk{chunk}"),
                    "frames": n, "frame": f"{wl.video.w}x{wl.video.h} RGB u8",
                    "chunk": chunk, "chunks": n_chunks, "occupancy": wl.video.occupancy,
                    "detector": f"{wl.dd_w}x{wl.dd_h}, " + (
@@ -949,6 +950,9 @@ def main():
     ap.add_argument("--frames", type=int, default=None,
                     help="chunked workloads: run only the first N frames of the video (for "
                          "profiling runs; the benchmark line runs all of them)")
+    ap.add_argument("--chunk", type=int, default=None,
+                    help="chunked workloads: frames per chunk (default: the workload's own, "
+                         "4,096 for the 1080p stream and 16,384 for the 720p videos)")
     ap.add_argument("--metric", choices=tuple(METRIC_DD), default="mse",
                     help="detector metric on the 640x480 workload (Sec. 5 and the alternatives "
                          "it names), at the threshold matching MSE 15 (see METRIC_DD)")

@@ -37,7 +37,18 @@ __device__ __forceinline__ uint32_t bytes13(uint32_t x) {
 
 template <int CB>
 __device__ __forceinline__ void load_chunk(const uint8_t* p, uint32_t (&v)[CB >= 4 ? CB / 4 : 1]) {
-  if constexpr (CB == 16) {
+  if constexpr (CB == 32) {
+    const u32x4 x = *reinterpret_cast<const u32x4*>(p);
+    const u32x4 y = *reinterpret_cast<const u32x4*>(p + 16);
+    v[0] = x[0];
+    v[1] = x[1];
+    v[2] = x[2];
+    v[3] = x[3];
+    v[4] = y[0];
+    v[5] = y[1];
+    v[6] = y[2];
+    v[7] = y[3];
+  } else if constexpr (CB == 16) {
     const u32x4 x = *reinterpret_cast<const u32x4*>(p);
     v[0] = x[0];
     v[1] = x[1];
@@ -254,12 +265,12 @@ __global__ void __launch_bounds__(256) k_area_sums_wave(const uint8_t* __restric
     int32_t v[CB];
     vertical_sums<CB, PACKED, RB>(col, row_bytes, a0, a1, ay.q, j0, j1, v);
     if (active) {
-      if constexpr (PACKED && CB == 16) {  // 32 bytes per lane as two 16-byte stores
+      if constexpr (PACKED && CB % 8 == 0) {  // 2 CB bytes per lane as 16-byte stores
         uint4* d = reinterpret_cast<uint4*>(buf + lane * CB);
-        d[0] = make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16),
-                          v[6] | (v[7] << 16));
-        d[1] = make_uint4(v[8] | (v[9] << 16), v[10] | (v[11] << 16), v[12] | (v[13] << 16),
-                          v[14] | (v[15] << 16));
+#pragma unroll
+        for (int q = 0; q < CB / 8; ++q)
+          d[q] = make_uint4(v[8 * q] | (v[8 * q + 1] << 16), v[8 * q + 2] | (v[8 * q + 3] << 16),
+                            v[8 * q + 4] | (v[8 * q + 5] << 16), v[8 * q + 6] | (v[8 * q + 7] << 16));
       } else {
 #pragma unroll
         for (int b = 0; b < CB; ++b) buf[lane * CB + b] = (cell_t)v[b];
@@ -579,20 +590,40 @@ int make_area_plan(int32_t in_h, int32_t in_w, int64_t stride, const void* frame
   if (p.threads < 64) p.threads = 64;
   // vertical column sums reach 255 * p_y; 16-bit packing is exact below 65536
   p.packed = 255LL * p.ay.p < 65536;
-  // wave strips: whole periods of the horizontal pattern in 16/4-byte chunks
+  // wave strips: whole periods of the horizontal pattern in 32/16/4-byte
+  // chunks; 32-byte chunks (two 16-byte loads per lane) where they leave
+  // fewer lanes of a wave idle
   p.wave = false;
   if (p.chunk_bytes != 1) {
-    int k = 1;
-    while ((3 * (int64_t)p.ax.p * k) % p.chunk_bytes != 0) k *= 2;
-    const int64_t glanes = 3 * (int64_t)p.ax.p * k / p.chunk_bytes;
-    const int64_t gpix = (int64_t)p.ax.p * k;
-    if (glanes <= 64 && in_w % gpix == 0) {
+    int best_cb = 0, best_used = 0;
+    int64_t best_glanes = 0, best_gpix = 0;
+    const int cands[2] = {p.chunk_bytes, p.chunk_bytes == 16 ? 32 : 0};
+    for (int cb : cands) {
+      if (cb == 0) continue;
+      int k = 1;
+      while ((3 * (int64_t)p.ax.p * k) % cb != 0) k *= 2;
+      const int64_t glanes = 3 * (int64_t)p.ax.p * k / cb;
+      const int64_t gpix = (int64_t)p.ax.p * k;
+      if (glanes > 64 || in_w % gpix != 0) continue;
+      const int used = (int)(64 / glanes * glanes);
+      if (used > best_used + 2) {  // 32-byte chunks only for a clear gain
+        best_used = used;
+        best_cb = cb;
+        best_glanes = glanes;
+        best_gpix = gpix;
+      }
+    }
+    if (best_cb != 0) {
       WaveGeom& g = p.wg;
-      g.group_lanes = (int32_t)glanes;
-      g.group_cols = p.ax.q * k;
-      g.groups_per_wave = (int32_t)(64 / glanes);
-      g.groups_per_row = (int32_t)(in_w / gpix);
+      g.chunk_bytes = best_cb;
+      g.group_lanes = (int32_t)best_glanes;
+      g.group_cols = (int32_t)(p.ax.q * (best_gpix / p.ax.p));
+      g.groups_per_wave = (int32_t)(64 / best_glanes);
+      g.groups_per_row = (int32_t)(in_w / best_gpix);
       g.waves_per_frame = (g.groups_per_row + g.groups_per_wave - 1) / g.groups_per_wave;
+      // a workgroup reads whole source rows (all strips of its bands) at once, so that
+      // the cache lines two strips share are fetched once, by one CU
+      g.waves_per_block = g.waves_per_frame <= 4 ? g.waves_per_frame * (4 / g.waves_per_frame) : 4;
       // bands of about 10 output rows; more when there are too few frames to fill the chip
       int64_t wb = (out_h + 9) / 10;
       const int64_t fill = (16384 + n * g.waves_per_frame - 1) / (n * g.waves_per_frame > 0 ? n * g.waves_per_frame : 1);
@@ -602,8 +633,8 @@ int make_area_plan(int32_t in_h, int32_t in_w, int64_t stride, const void* frame
       g.band_rows = (int32_t)((out_h + wb - 1) / wb);
       const int64_t scols = (int64_t)g.groups_per_wave * g.group_cols;
       const int64_t cellb = p.packed ? 2 : 4;
-      const int64_t per_wave = (64 * p.chunk_bytes * cellb + (int64_t)g.band_rows * scols * 3 * 4 + 15) & ~(int64_t)15;
-      g.lds_bytes = (size_t)(scols * 16 + 4 * per_wave);
+      const int64_t per_wave = (64 * best_cb * cellb + (int64_t)g.band_rows * scols * 3 * 4 + 15) & ~(int64_t)15;
+      g.lds_bytes = (size_t)(scols * 16 + g.waves_per_block * per_wave);
       p.wave = g.lds_bytes <= 64 * 1024;
     }
   }
@@ -626,12 +657,15 @@ int launch_area_sums(const AreaPlan& p, const uint8_t* frames, int64_t stride, i
   if (p.wave) {
     const WaveGeom& g = p.wg;
     const int64_t units = n * g.bands * g.waves_per_frame;
-    const int64_t wblocks = (units + 3) / 4;
+    const int64_t wblocks = (units + g.waves_per_block - 1) / g.waves_per_block;
     if (wblocks > 0x7FFFFFFF) return fail(NSC_E_SHAPE, "too many frames in one call");
 #define NSC_WAVE_LAUNCH(CB, PK)                                                          \
-  hipLaunchKernelGGL((k_area_sums_wave<CB, PK>), dim3((unsigned)wblocks), dim3(256),      \
+  hipLaunchKernelGGL((k_area_sums_wave<CB, PK, CB == 32 ? NSC_ROWS_BATCH / 2 : NSC_ROWS_BATCH>), \
+                     dim3((unsigned)wblocks), dim3(64 * g.waves_per_block),               \
                      g.lds_bytes, stream, frames, stride, p.ay, p.ax, g, g.bands, n, sums)
-    if (p.chunk_bytes == 16) {
+    if (g.chunk_bytes == 32) {
+      if (p.packed) NSC_WAVE_LAUNCH(32, true); else NSC_WAVE_LAUNCH(32, false);
+    } else if (g.chunk_bytes == 16) {
       if (p.packed) NSC_WAVE_LAUNCH(16, true); else NSC_WAVE_LAUNCH(16, false);
     } else {
       if (p.packed) NSC_WAVE_LAUNCH(4, true); else NSC_WAVE_LAUNCH(4, false);

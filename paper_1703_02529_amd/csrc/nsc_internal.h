@@ -50,14 +50,16 @@ struct Axis {
 
 // Column strips of the wave-autonomous area kernel.
 struct WaveGeom {
+  int32_t chunk_bytes;      // bytes one lane reads per source row: 32 (two 16-byte loads), 16 or 4
   int32_t group_lanes;      // lanes of one group (whole periods of the column pattern)
   int32_t group_cols;       // output columns of one group
   int32_t groups_per_wave;  // groups in one wave's strip
   int32_t groups_per_row;   // groups across the frame
   int32_t waves_per_frame;  // strips across the frame
+  int32_t waves_per_block;  // waves of a workgroup: whole rows of strips where they fit in 4
   int32_t bands;            // bands of output rows per frame (one wave each per strip)
   int32_t band_rows;        // at most this many output rows per band
-  size_t lds_bytes;         // dynamic LDS of a 4-wave workgroup
+  size_t lds_bytes;         // dynamic LDS of a workgroup
 };
 
 // Area-sum launch plan for one frame geometry.
