@@ -73,8 +73,9 @@ AREA_KERNEL = "k_area_sums_wave"
 AREA_SOURCES = ("paper_1703_02529_amd/csrc/area_diff.hip", "paper_1703_02529_amd/csrc/nsc_internal.h")
 COPY_BYTES = 1 << 31           # plain copy of known size for counter calibration
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
-DTYPE_BF16 = ("u8 frames, i32/i64 detector; CNN: bf16 weights, bf16 input, later activations "
-              "as bf16 hi/lo pairs (two MFMAs per product), fp32 accumulate")
+DTYPE_BF16 = ("u8 frames, i32/i64 detector; CNN: bf16 weights and input; fp16 activations on "
+              "the fp16 matrix cores in the 64-channel and dense layers, bf16 hi/lo activation "
+              "pairs in the others; fp32 accumulate")
 DTYPE_FP32 = "u8 frames, i32/i64 detector; CNN: fp32 weights and activations, fp32 MFMA"
 FP32_PEAK_TFLOPS = 157.3
 

@@ -74,7 +74,20 @@ enum { NSC_REF_PREV = 0, NSC_REF_FIXED = 1 };
  * MSE, SAD and NRMSE are correctly rounded fp64 functions of exact integer
  * sums; PSNR goes through the device log10 (within a few ulp). */
 enum { NSC_METRIC_MSE = 0, NSC_METRIC_SAD = 1, NSC_METRIC_NRMSE = 2, NSC_METRIC_PSNR = 3 };
-enum { NSC_F32 = 0, NSC_BF16 = 1 };
+/* Element types of a specialized CNN (its weights and activations):
+ *   NSC_F32        fp32 weights and activations, fp32 matrix cores;
+ *   NSC_BF16       bf16 weights; the pre-processed input rounded to bf16; the
+ *                  64-input-channel layers and the dense layer run on the fp16
+ *                  matrix cores with their activations rounded to fp16 (the
+ *                  bf16 weights are scaled by powers of two, exactly, and the
+ *                  activations by powers of two chosen from a worst-case bound
+ *                  so that no fp16 value overflows), other layers as with
+ *                  NSC_BF16_PAIRS; fp32 accumulation;
+ *   NSC_BF16_PAIRS bf16 weights and input; every later activation enters the
+ *                  bf16 matrix cores as a pair hi = bf16(a), lo = bf16(a - hi)
+ *                  (two products per weight, about 2^-17 relative); fp32
+ *                  accumulation. */
+enum { NSC_F32 = 0, NSC_BF16 = 1, NSC_BF16_PAIRS = 2 };
 enum { NSC_MAX_CONV = 8, NSC_MAX_DELTA = 256, NSC_MAX_BLOCKS = 1024, NSC_MAX_STRIDE = 4096,
        NSC_MAX_SWEEP = 65535 };
 /* Largest n of nsc_compact_noalloc (16,384 tiles of 4,096 flags). */
@@ -123,7 +136,7 @@ typedef struct nsc_cnn_desc {
   uint32_t pool_after_mask;       /* bit l: max-pool after conv layer l        */
   int32_t dense;                  /* hidden units, multiple of 16             */
   int32_t in_h, in_w;             /* input grid (equal to cfg cnn_h, cnn_w)    */
-  int32_t dtype;                  /* NSC_F32 or NSC_BF16 weights/activations   */
+  int32_t dtype;                  /* NSC_F32, NSC_BF16 or NSC_BF16_PAIRS       */
 } nsc_cnn_desc;
 
 typedef struct nsc_cnn nsc_cnn; /* opaque: packed device weights */
@@ -169,7 +182,7 @@ int nsc_cnn_check(const nsc_cnn_desc* desc);
  * Returns a negative nsc_status on an invalid description. */
 int64_t nsc_cnn_blob_floats(const nsc_cnn_desc* desc);
 
-/* Packs a host fp32 weight blob (NSC_BF16 nets round each value to the
+/* Packs a host fp32 weight blob (bf16 nets round each value to the
  * nearest bf16) into device memory owned by the returned handle.  Synchronous;
  * uses the current HIP device.  Errors: NSC_E_INVAL, NSC_E_SHAPE,
  * NSC_E_DTYPE, NSC_E_NOMEM, NSC_E_HIP. */

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libnsc.so")
 
 NSC_REF_PREV, NSC_REF_FIXED = 0, 1
 NSC_METRIC_MSE, NSC_METRIC_SAD, NSC_METRIC_NRMSE, NSC_METRIC_PSNR = 0, 1, 2, 3
-NSC_F32, NSC_BF16 = 0, 1
+NSC_F32, NSC_BF16, NSC_BF16_PAIRS = 0, 1, 2
 NSC_MAX_CONV = 8
 
 _i32, _i64, _u32, _dbl = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_double
@@ -163,7 +163,9 @@ def make_cfg(*, in_h, in_w, dd_h, dd_w, cnn_h, cnn_w, ref_mode=NSC_REF_PREV, del
     return c
 
 
-def make_desc(conv, pool, dense, in_h, in_w, bf16) -> CnnDesc:
+def make_desc(conv, pool, dense, in_h, in_w, bf16, pairs=False) -> CnnDesc:
+    """pairs: a bf16 network whose later activations enter the matrix cores as
+    bf16 hi / lo pairs (NSC_BF16_PAIRS) instead of fp16 (NSC_BF16)."""
     d = CnnDesc()
     d.n_conv = len(conv)
     mask = 0
@@ -172,7 +174,7 @@ def make_desc(conv, pool, dense, in_h, in_w, bf16) -> CnnDesc:
         mask |= (1 << i) if p else 0
     d.pool_after_mask = mask
     d.dense, d.in_h, d.in_w = dense, in_h, in_w
-    d.dtype = NSC_BF16 if bf16 else NSC_F32
+    d.dtype = (NSC_BF16_PAIRS if pairs else NSC_BF16) if bf16 else NSC_F32
     return d
 
 

@@ -103,7 +103,8 @@ int check_cfg(const nsc_cascade_cfg* c) {
 // Layer shapes of a CNN description; fills `cnn` (no device memory).
 int plan_cnn(const nsc_cnn_desc* d, Cnn* cnn) {
   NSC_REQUIRE(d != nullptr, NSC_E_INVAL, "CNN description is NULL");
-  NSC_REQUIRE(d->dtype == NSC_F32 || d->dtype == NSC_BF16, NSC_E_DTYPE, "dtype %d is unknown",
+  NSC_REQUIRE(d->dtype == NSC_F32 || d->dtype == NSC_BF16 || d->dtype == NSC_BF16_PAIRS,
+              NSC_E_DTYPE, "dtype %d is unknown",
               d->dtype);
   NSC_REQUIRE(d->n_conv >= 1 && d->n_conv <= NSC_MAX_CONV, NSC_E_SHAPE,
               "n_conv %d outside 1..%d", d->n_conv, NSC_MAX_CONV);
@@ -112,10 +113,11 @@ int plan_cnn(const nsc_cnn_desc* d, Cnn* cnn) {
   NSC_REQUIRE(d->dense >= 16 && d->dense <= 256 && d->dense % 16 == 0 && (d->dense / 16) != 3 &&
                   ((d->dense / 16) & (d->dense / 16 - 1)) == 0,
               NSC_E_SHAPE, "dense width %d must be 16, 32, 64, 128 or 256", d->dense);
-  const bool bf16 = d->dtype == NSC_BF16;
+  const bool bf16 = d->dtype == NSC_BF16 || d->dtype == NSC_BF16_PAIRS;
   Cnn c{};
   c.desc = *d;
   c.bf16 = bf16;
+  c.h16 = d->dtype == NSC_BF16;
   c.n_layers = d->n_conv;
   int cin = 3, h = d->in_h, w = d->in_w;
   size_t woff = 0, boff = 0, act = 0;
@@ -169,6 +171,45 @@ uint16_t host_bf16(float f) {
   if ((u & 0x7F800000u) == 0x7F800000u) return (uint16_t)(u >> 16);  // inf / nan
   u += 0x7FFFu + ((u >> 16) & 1u);
   return (uint16_t)(u >> 16);
+}
+
+float host_bf16_value(float f) {
+  const uint32_t u = (uint32_t)host_bf16(f) << 16;
+  float v;
+  memcpy(&v, &u, 4);
+  return v;
+}
+
+// fp16 bits of v * 2^e, rounded to nearest even.
+uint16_t host_f16_scaled(float v, int e) {
+  const _Float16 h = (_Float16)ldexpf(v, e);
+  uint16_t b;
+  memcpy(&b, &h, 2);
+  return b;
+}
+
+// Scale exponent of a weight array for the fp16 matrix cores: the largest
+// magnitude times 2^e lies in [2^14, 2^15), so every bf16 value within 2^31
+// of it (8 significant bits) is an fp16 value after scaling.  0 for all-zero
+// weights.
+int fp16_weight_exp(const float* w, size_t n) {
+  float mx = 0.0f;
+  for (size_t i = 0; i < n; ++i) {
+    const float a = fabsf(host_bf16_value(w[i]));
+    mx = a > mx ? a : mx;
+  }
+  if (mx == 0.0f) return 0;
+  int e = 0;
+  frexpf(mx, &e);  // mx = f 2^e, f in [0.5, 1): floor(log2 mx) = e - 1
+  return 14 - (e - 1);
+}
+
+// Down-scale exponent (>= 0) of activations bounded by `bound` so that they
+// stay below 2^15 in fp16 (whose largest finite value is 65504).
+int fp16_act_exp(double bound) {
+  int e = 0;
+  while (bound * ldexp(1.0, -e) > 32768.0) ++e;
+  return e;
 }
 
 // Frame skipping: the checked frames of a stream form a video of their own
@@ -363,14 +404,58 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
             }
     }
   }
-  // device image: [conv_w][conv_wf][conv_b][w1][b1][w2]
+  // bf16: fp16 copies for the layers whose activations run through the fp16
+  // matrix cores (see CnnLayer::wexp / aexp): fragment order like conv_wf,
+  // each layer scaled by 2^wexp, and the dense weights likewise
+  std::vector<uint16_t> convwh, w1h;
+  if (c.bf16) {
+    convwh.resize(conv_elems);
+    w1h.resize(w1.size());
+    double bound = 1.0;  // |input| <= 1 after pre-processing
+    for (int l = 0; l < c.n_layers; ++l) {
+      CnnLayer& L = c.layers[l];
+      const size_t n = (size_t)L.cout * L.kpad;
+      L.wexp = fp16_weight_exp(&convwf[L.w_off], n);
+      L.aexp = fp16_act_exp(bound);
+      for (size_t i = 0; i < n; ++i)
+        convwh[L.w_off + i] = host_f16_scaled(host_bf16_value(convwf[L.w_off + i]), L.wexp);
+      // the layer's output bound: max over channels of sum |w| x bound + |b|
+      double nb = 0.0;
+      for (int o = 0; o < L.cout; ++o) {
+        double sw = 0.0;
+        for (int k = 0; k < L.kpad; ++k)
+          sw += fabs((double)host_bf16_value(convw[L.w_off + (size_t)o * L.kpad + k]));
+        const double v = sw * bound + fabs((double)convb[L.b_off + o]);
+        nb = v > nb ? v : nb;
+      }
+      bound = nb;
+    }
+    c.dense_wexp = fp16_weight_exp(w1.data(), w1.size());
+    c.dense_aexp = fp16_act_exp(bound);
+    for (size_t i = 0; i < w1.size(); ++i)
+      w1h[i] = host_f16_scaled(host_bf16_value(w1[i]), c.dense_wexp);
+  }
+  // per layer (then the dense layer) the fp16 path's input and output scales
+  std::vector<float> scales(2 * (size_t)(c.n_layers + 1), 1.0f);
+  if (c.bf16) {
+    for (int l = 0; l < c.n_layers; ++l) {
+      scales[2 * l] = ldexpf(1.0f, -c.layers[l].aexp);
+      scales[2 * l + 1] = ldexpf(1.0f, c.layers[l].aexp - c.layers[l].wexp);
+    }
+    scales[2 * c.n_layers] = ldexpf(1.0f, -c.dense_aexp);
+    scales[2 * c.n_layers + 1] = ldexpf(1.0f, c.dense_aexp - c.dense_wexp);
+  }
+  // device image: [conv_w][conv_wf][conv_wh][conv_b][w1][w1h][b1][w2][scales]
   const size_t o_cw = 0;
   const size_t o_cwf = align_up(o_cw + conv_elems * es, kAlign);
-  const size_t o_cb = align_up(o_cwf + convwf.size() * es, kAlign);
+  const size_t o_cwh = align_up(o_cwf + convwf.size() * es, kAlign);
+  const size_t o_cb = align_up(o_cwh + convwh.size() * 2, kAlign);
   const size_t o_w1 = align_up(o_cb + bias_elems * 4, kAlign);
-  const size_t o_b1 = align_up(o_w1 + w1.size() * es, kAlign);
+  const size_t o_w1h = align_up(o_w1 + w1.size() * es, kAlign);
+  const size_t o_b1 = align_up(o_w1h + w1h.size() * 2, kAlign);
   const size_t o_w2 = align_up(o_b1 + (size_t)c.dense * 4, kAlign);
-  const size_t total = align_up(o_w2 + (size_t)c.dense * 4, kAlign);
+  const size_t o_sc = align_up(o_w2 + (size_t)c.dense * 4, kAlign);
+  const size_t total = align_up(o_sc + scales.size() * 4, kAlign);
   std::vector<unsigned char> img(total, 0);
   auto put = [&](size_t off, const std::vector<float>& v, bool as_bf16) {
     if (as_bf16) {
@@ -384,8 +469,13 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
   if (c.bf16) put(o_cwf, convwf, true);
   put(o_cb, convb, false);
   put(o_w1, w1, c.bf16);
+  if (c.bf16) {
+    memcpy(img.data() + o_cwh, convwh.data(), convwh.size() * 2);
+    memcpy(img.data() + o_w1h, w1h.data(), w1h.size() * 2);
+  }
   put(o_b1, b1, false);
   put(o_w2, w2, false);
+  put(o_sc, scales, false);
   void* dev = nullptr;
   if (hipMalloc(&dev, total) != hipSuccess)
     return fail(NSC_E_NOMEM, "hipMalloc of %zu bytes for CNN weights failed", total);
@@ -397,10 +487,13 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
   c.dev = dev;
   c.conv_w = b + o_cw;
   c.conv_wf = c.bf16 ? b + o_cwf : nullptr;
+  c.conv_wh = c.bf16 ? b + o_cwh : nullptr;
+  c.w1h = c.bf16 ? b + o_w1h : nullptr;
   c.conv_b = reinterpret_cast<float*>(b + o_cb);
   c.w1 = b + o_w1;
   c.b1 = reinterpret_cast<float*>(b + o_b1);
   c.w2 = reinterpret_cast<float*>(b + o_w2);
+  c.scales = reinterpret_cast<float*>(b + o_sc);
   nsc_cnn* h = new (std::nothrow) nsc_cnn;
   if (!h) {
     (void)hipFree(dev);

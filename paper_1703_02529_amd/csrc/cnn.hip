@@ -12,13 +12,23 @@
 // v_mfma_f32_16x16x32_bf16, fp32 layers v_mfma_f32_16x16x4_f32; both
 // accumulate in fp32.
 //
-// Activations between layers are fp32 in the workspace.  A bf16 network has
-// bf16 weights and a bf16-rounded input; each later activation a enters the
-// bf16 matrix cores as the pair hi = bf16(a), lo = bf16(a - hi) (the
-// difference is exact in fp32), multiplied by the same weights into a second
-// accumulator.  a is then carried to about 2^-17 of itself, so the result is a
-// continuous function of the fp32 accumulation error instead of flipping
-// bf16 roundings of intermediate values.
+// A bf16 network has bf16 weights and a bf16-rounded input.  Its later
+// activations enter the matrix cores in one of two ways:
+//  - NSC_BF16: the 64-input-channel (banded) layers and the dense layer run on
+//    the fp16 matrix cores, activations rounded to fp16 once (2^-12 of
+//    themselves), one product per weight.  The bf16 weights are scaled by 2^wexp
+//    per layer so that each is an fp16 value, the activations by 2^-aexp (from
+//    a worst-case bound of the layer's input, so that none overflows), and the
+//    accumulators are multiplied back in the epilogue; activations passed
+//    between two such layers (or into the dense layer) are stored as fp16,
+//    already scaled for the next layer.  The other layers use the pairs below.
+//  - NSC_BF16_PAIRS: each later activation a enters the bf16 matrix cores as
+//    the pair hi = bf16(a), lo = bf16(a - hi) (the difference is exact in
+//    fp32), multiplied by the same weights into the same accumulator: a is
+//    carried to about 2^-17 of itself, at two products per weight.
+// Either way the result is a continuous function of the activations' rounding
+// and of the fp32 accumulation error; activations are fp32 in the workspace
+// otherwise.
 //
 // The dense layer is a GEMM over 16-survivor tiles (M) x hidden units (N) x
 // features (K) on the same MFMA shapes, one workgroup per tile whose waves
@@ -36,6 +46,25 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+// fp16 matrix cores (the fp16 path of a bf16 network's later layers).
+__device__ __forceinline__ f32x4 mma_f16(const f16x8& a, const f16x8& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+// Two fp32 values times sc (a power of two) rounded to fp16 (nearest even),
+// packed.
+__device__ __forceinline__ uint32_t f16x2_bits(float a, float b, float sc) {
+  return __builtin_bit_cast(uint32_t, f16x2{(_Float16)(a * sc), (_Float16)(b * sc)});
+}
+__device__ __forceinline__ uint2 f16x4_bits(float a, float b, float c, float d, float sc) {
+  return make_uint2(f16x2_bits(a, b, sc), f16x2_bits(c, d, sc));
+}
+__device__ __forceinline__ uint4 f16x8_bits(const float4& a, const float4& b, float sc) {
+  return make_uint4(f16x2_bits(a.x, a.y, sc), f16x2_bits(a.z, a.w, sc), f16x2_bits(b.x, b.y, sc),
+                    f16x2_bits(b.z, b.w, sc));
+}
 
 // ---------------------------------------------------------------- numerics
 
@@ -117,6 +146,7 @@ template <> struct Elt<uint16_t> {  // bf16 stored as raw bits
   // Activations enter as hi + lo pairs (see the top of this file); the
   // conversions are the hardware's packed round-to-nearest-even.
   static constexpr bool SPLIT = true;
+  static constexpr bool CVT = false;
   // two fp32 values -> (hi0, hi1) and (lo0, lo1), packed as bf16 pairs
   // (one packed conversion for the hi pair; its fp32 values are the pair's
   // bits moved into the upper halves)
@@ -166,6 +196,34 @@ template <> struct Elt<float> {
   static __device__ __forceinline__ float zero() { return 0.0f; }
   static __device__ __forceinline__ void set(float& f, int, float v) { f = v; }
   static constexpr bool SPLIT = false;
+  static constexpr bool CVT = false;
+};
+// fp16 path of a bf16 network's dense layer: scaled fp16 weights, fp32
+// activations converted to fp16 (times a power-of-two input scale) as they are
+// loaded, one MFMA per product.
+template <> struct Elt<_Float16> {
+  static constexpr int E = 8, KS = 32;
+  typedef f16x8 frag;
+  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b, f32x4 c) {
+    return mma_f16(a, b, c);
+  }
+  static __device__ __forceinline__ frag load(const _Float16* p) {  // 16-byte aligned
+    return *reinterpret_cast<const frag*>(p);
+  }
+  static __device__ __forceinline__ frag zero() {
+    frag z;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) z[e] = (_Float16)0.0f;
+    return z;
+  }
+  // 8 consecutive fp32 values (16-byte aligned) times sc
+  static __device__ __forceinline__ frag cvt8(const float* p, float sc) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    return __builtin_bit_cast(frag, f16x8_bits(a, b, sc));
+  }
+  static constexpr bool SPLIT = false;
+  static constexpr bool CVT = true;
 };
 
 // ------------------------------------------------------------------- conv
@@ -191,6 +249,11 @@ struct ConvArgs {
   int32_t w_lds;            // row stride of staged weights (elements)
   int32_t band_w;           // staged columns of a segment (halo and tail zero-filled)
   int32_t lo_plane;         // elements from a staged hi value to its lo value (split layers)
+  const float* scl;         // fp16 path: the layer's (input scale 2^-aexp, output scale
+                            // 2^(aexp - wexp)) in the network's weight image, followed by
+                            // the next layer's (or the dense layer's) pair
+  int32_t in_f16;           // act_in holds fp16 values already times the input scale
+  int32_t out_f16;          // act_out gets fp16 values times the next layer's input scale
   const CamNet* nets;       // camera group: per-camera weight offsets (else null)
   int64_t per_cam;          // frames per camera of a group
 };
@@ -835,12 +898,13 @@ struct Band64 {
   int32_t rows;      // staged rows of a band: 4 * band_tiles + 2
   int32_t wb;        // pixels per band row
   int32_t cp;        // pixels per chunk plane: rows * wb + 1
-  int32_t lo_bytes;  // bytes from the hi plane to the lo plane: 8 * cp * 16
+  int32_t lo_bytes;  // bytes of one plane (from the hi plane to the lo plane): 8 * cp * 16
+  int32_t planes;    // 2: bf16 hi and lo planes; 1: one fp16 plane
 };
 
-// Bytes of the two planes plus 32 bytes for the overhanging reads.
+// Bytes of the planes plus 32 bytes for the overhanging reads.
 __host__ __device__ inline size_t band64_bytes(const Band64& b) {
-  return (size_t)2 * b.lo_bytes + 32;
+  return (size_t)b.planes * b.lo_bytes + 32;
 }
 
 // Work item -> (image, band).  Workgroup i of a grid that is a multiple of 8
@@ -861,11 +925,13 @@ __device__ __forceinline__ void band64_clear(unsigned char* lds, const Band64& b
 }
 
 // Stages band rows [0, rows_used), columns 1..w: image rows y0 + r inside the
-// image from one image's fp32 NHWC 64-channel activations split into hi / lo
-// bf16, zeros for rows outside.  Eight consecutive threads read one pixel's
-// 256 bytes.
+// image from one image's fp32 NHWC 64-channel activations, split into hi / lo
+// bf16 (H = false) or as fp16 times in_scale (H), zeros for rows outside.
+// Eight consecutive threads read one pixel's 256 bytes.
+template <bool H>
 __device__ __forceinline__ void stage_band64(const float* __restrict__ src, const Band64& b,
-                                             unsigned char* lds, int y0, int rows_used) {
+                                             unsigned char* lds, int y0, int rows_used,
+                                             float in_scale) {
   const int units = rows_used * b.w * 8;
   for (int u = threadIdx.x; u < units; u += blockDim.x) {
     const int pix = u >> 3, c = u & 7;
@@ -876,15 +942,35 @@ __device__ __forceinline__ void stage_band64(const float* __restrict__ src, cons
       const float* p = src + ((int64_t)y * b.w + x) * 64 + c * 8;
       const float4 v0 = *reinterpret_cast<const float4*>(p);
       const float4 v1 = *reinterpret_cast<const float4*>(p + 4);
-      uint2 h0, l0, h1, l1;
-      Elt<uint16_t>::split4(v0, h0, l0);
-      Elt<uint16_t>::split4(v1, h1, l1);
-      hi = make_uint4(h0.x, h0.y, h1.x, h1.y);
-      lo = make_uint4(l0.x, l0.y, l1.x, l1.y);
+      if constexpr (H) {
+        hi = f16x8_bits(v0, v1, in_scale);
+      } else {
+        uint2 h0, l0, h1, l1;
+        Elt<uint16_t>::split4(v0, h0, l0);
+        Elt<uint16_t>::split4(v1, h1, l1);
+        hi = make_uint4(h0.x, h0.y, h1.x, h1.y);
+        lo = make_uint4(l0.x, l0.y, l1.x, l1.y);
+      }
     }
     const int addr = (c * b.cp + r * b.wb + x + 1) * 16;
     *reinterpret_cast<uint4*>(lds + addr) = hi;
-    *reinterpret_cast<uint4*>(lds + b.lo_bytes + addr) = lo;
+    if constexpr (!H) *reinterpret_cast<uint4*>(lds + b.lo_bytes + addr) = lo;
+  }
+}
+
+// The same from fp16 activations already scaled by the producing layer: a
+// 16-byte copy per chunk.
+__device__ __forceinline__ void stage_band64_f16(const _Float16* __restrict__ src, const Band64& b,
+                                                 unsigned char* lds, int y0, int rows_used) {
+  const int units = rows_used * b.w * 8;
+  for (int u = threadIdx.x; u < units; u += blockDim.x) {
+    const int pix = u >> 3, c = u & 7;
+    const int r = pix / b.w, x = pix - r * b.w;
+    const int y = y0 + r;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if ((unsigned)y < (unsigned)b.h)
+      v = *reinterpret_cast<const uint4*>(src + ((int64_t)y * b.w + x) * 64 + c * 8);
+    *reinterpret_cast<uint4*>(lds + (c * b.cp + r * b.wb + x + 1) * 16) = v;
   }
 }
 
@@ -895,45 +981,58 @@ __device__ __forceinline__ void stage_band64(const float* __restrict__ src, cons
 // current one, in two register sets (steps A and B of a tap), and scheduling
 // fences keep the compiler from sinking those loads to their first use.  The
 // hi products of all tiles are issued before the lo products.
-template <int MT, int NT>
+// H: fp16 fragments (one plane, fp16 weights), else bf16 hi / lo pairs.
+template <bool H> struct Band64Frag { typedef bf16x8 type; };
+template <> struct Band64Frag<true> { typedef f16x8 type; };
+
+template <int MT, int NT, bool H>
 struct Band64Step {
-  bf16x8 w[NT];
-  bf16x8 xh[MT], xl[MT];
+  typedef typename Band64Frag<H>::type frag;
+  frag w[NT];
+  frag xh[MT], xl[H ? 1 : MT];
 };
 
-template <int MT, int NT>
-__device__ __forceinline__ void band64_load(const unsigned char* lds, const bf16x8* __restrict__ wp,
+template <int MT, int NT, bool H>
+__device__ __forceinline__ void band64_load(const unsigned char* lds,
+                                            const typename Band64Frag<H>::type* __restrict__ wp,
                                             int ks, const uint32_t (&base)[MT],
                                             const uint32_t (&base_lo)[MT], uint32_t off,
-                                            Band64Step<MT, NT>& st) {
-  using X = Elt<uint16_t>;
+                                            Band64Step<MT, NT, H>& st) {
+  typedef typename Band64Frag<H>::type frag;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) st.w[nt] = wp[(ks * NT + nt) * 64];
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
-    st.xh[i] = X::load(reinterpret_cast<const uint16_t*>(lds + base[i] + off));
-    st.xl[i] = X::load(reinterpret_cast<const uint16_t*>(lds + base_lo[i] + off));
+    st.xh[i] = *reinterpret_cast<const frag*>(lds + base[i] + off);
+    if constexpr (!H) st.xl[i] = *reinterpret_cast<const frag*>(lds + base_lo[i] + off);
   }
 }
 
-template <int MT, int NT>
-__device__ __forceinline__ void band64_mma(const Band64Step<MT, NT>& st, f32x4 (&acc)[MT][NT]) {
-  using X = Elt<uint16_t>;
+template <int MT, int NT, bool H>
+__device__ __forceinline__ void band64_mma(const Band64Step<MT, NT, H>& st, f32x4 (&acc)[MT][NT]) {
+  if constexpr (H) {
 #pragma unroll
-  for (int i = 0; i < MT; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(st.w[nt], st.xh[i], acc[i][nt]);
+      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = mma_f16(st.w[nt], st.xh[i], acc[i][nt]);
+  } else {
+    using X = Elt<uint16_t>;
 #pragma unroll
-  for (int i = 0; i < MT; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(st.w[nt], st.xl[i], acc[i][nt]);
+      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(st.w[nt], st.xh[i], acc[i][nt]);
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = X::mma(st.w[nt], st.xl[i], acc[i][nt]);
+  }
 }
 
-template <int MT, int NT>
+template <int MT, int NT, bool H>
 __device__ __forceinline__ void band64_tiles(const unsigned char* lds, const Band64& b,
-                                             const bf16x8* __restrict__ wf, const int (&tr)[MT],
-                                             const int (&tc)[MT], int py, int px, int g, int lane,
-                                             f32x4 (&acc)[MT][NT]) {
+                                             const typename Band64Frag<H>::type* __restrict__ wf,
+                                             const int (&tr)[MT], const int (&tc)[MT], int py,
+                                             int px, int g, int lane, f32x4 (&acc)[MT][NT]) {
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -945,24 +1044,68 @@ __device__ __forceinline__ void band64_tiles(const unsigned char* lds, const Ban
     base_lo[i] = base[i] + (uint32_t)b.lo_bytes;
   }
   const uint32_t step2 = (uint32_t)b.cp * 64u;  // chunks 4..7: 4 chunk planes on
-  const bf16x8* wp = wf + lane;
-  Band64Step<MT, NT> sa, sb;
-  band64_load<MT, NT>(lds, wp, 0, base, base_lo, 0u, sa);
+  const typename Band64Frag<H>::type* wp = wf + lane;
+  if constexpr (H) {
+    // fp16: the weight fragments (from L2) of the next tap are loaded while
+    // the current tap computes; the activations (LDS) one step ahead
+    f16x8 w0[NT], w1[NT], v0[NT], v1[NT], x0[MT], x1[MT];
+    auto ldw = [&](int j, f16x8 (&d)[NT]) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) d[nt] = wp[(j * NT + nt) * 64];
+    };
+    auto ldx = [&](int j, f16x8 (&d)[MT]) {
+      const int tap = j >> 1, dy = tap / 3, dx = tap - 3 * dy;
+      const uint32_t off = (uint32_t)(dy * b.wb + dx) * 16u + ((j & 1) ? step2 : 0u);
+#pragma unroll
+      for (int i = 0; i < MT; ++i) d[i] = *reinterpret_cast<const f16x8*>(lds + base[i] + off);
+    };
+    auto mma = [&](const f16x8 (&wv)[NT], const f16x8 (&xv)[MT]) {
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[i][nt] = mma_f16(wv[nt], xv[i], acc[i][nt]);
+    };
+    ldw(0, w0);
+    ldw(1, w1);
+    ldx(0, x0);
+#pragma unroll 1
+    for (int tap = 0; tap < 9; ++tap) {
+      const int tn = tap < 8 ? tap + 1 : tap;  // the last tap reloads its own, unused
+      ldw(2 * tn, v0);
+      ldw(2 * tn + 1, v1);
+      ldx(2 * tap + 1, x1);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(w0, x0);
+      __builtin_amdgcn_sched_barrier(0);
+      ldx(2 * tn, x0);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(w1, x1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        w0[nt] = v0[nt];
+        w1[nt] = v1[nt];
+      }
+    }
+    return;
+  }
+  Band64Step<MT, NT, H> sa, sb;
+  band64_load<MT, NT, H>(lds, wp, 0, base, base_lo, 0u, sa);
 #pragma unroll 1
   for (int tap = 0; tap < 9; ++tap) {
     const int dy = tap / 3, dx = tap - 3 * dy;
     const uint32_t toff = (uint32_t)(dy * b.wb + dx) * 16u;
     // step B of this tap in flight while step A computes
-    band64_load<MT, NT>(lds, wp, 2 * tap + 1, base, base_lo, toff + step2, sb);
+    band64_load<MT, NT, H>(lds, wp, 2 * tap + 1, base, base_lo, toff + step2, sb);
     __builtin_amdgcn_sched_barrier(0);
-    band64_mma<MT, NT>(sa, acc);
+    band64_mma<MT, NT, H>(sa, acc);
     __builtin_amdgcn_sched_barrier(0);
     // step A of the next tap (the last tap reloads its own, unused)
     const int tn = tap < 8 ? tap + 1 : tap;
     const int dyn = tn / 3, dxn = tn - 3 * dyn;
-    band64_load<MT, NT>(lds, wp, 2 * tn, base, base_lo, (uint32_t)(dyn * b.wb + dxn) * 16u, sa);
+    band64_load<MT, NT, H>(lds, wp, 2 * tn, base, base_lo, (uint32_t)(dyn * b.wb + dxn) * 16u, sa);
     __builtin_amdgcn_sched_barrier(0);
-    band64_mma<MT, NT>(sb, acc);
+    band64_mma<MT, NT, H>(sb, acc);
     __builtin_amdgcn_sched_barrier(0);
   }
 }
@@ -975,17 +1118,29 @@ __device__ __forceinline__ float quad_perm(float v) {
 constexpr int kQuadXor1 = 0xB1;  // [1, 0, 3, 2]
 constexpr int kQuadXor2 = 0x4E;  // [2, 3, 0, 1]
 
-// Bias, ReLU, optional 2x2 max-pool and 16-byte fp32 NHWC stores of one
-// transposed tile; (oy, ox) is this lane's pixel in the layer's input grid.
-template <int NT>
+// Bias, ReLU, optional 2x2 max-pool and NHWC stores of one transposed tile;
+// (oy, ox) is this lane's pixel in the layer's input grid.  The fp16 path
+// first multiplies the accumulators by sc (a power of two).  The output is
+// fp32 (16-byte stores), or with st16 != 0 fp16 values times st16 (the next
+// layer's input scale; 8-byte stores).
+template <int NT, bool H>
 __device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const float* __restrict__ bp,
-                                                float* out, int cout, int oy, int ox, int h, int w,
-                                                int pool, int m, int g) {
+                                                void* out, int cout, int oy, int ox, int h, int w,
+                                                int pool, int m, int g, float sc, float st16) {
+  auto store = [&](int64_t e, const float (&v)[4]) {  // element offset e, 4 channels
+    if (st16 != 0.0f)
+      *reinterpret_cast<uint2*>(static_cast<_Float16*>(out) + e) =
+          f16x4_bits(v[0], v[1], v[2], v[3], st16);
+    else
+      *reinterpret_cast<float4*>(static_cast<float*>(out) + e) = make_float4(v[0], v[1], v[2], v[3]);
+  };
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const float4 bb = *reinterpret_cast<const float4*>(bp + nt * 16 + 4 * g);
-    float v[4] = {fmaxf(acc[nt][0] + bb.x, 0.f), fmaxf(acc[nt][1] + bb.y, 0.f),
-                  fmaxf(acc[nt][2] + bb.z, 0.f), fmaxf(acc[nt][3] + bb.w, 0.f)};
+    f32x4 t = acc[nt];
+    if constexpr (H) t *= sc;
+    float v[4] = {fmaxf(t[0] + bb.x, 0.f), fmaxf(t[1] + bb.y, 0.f), fmaxf(t[2] + bb.z, 0.f),
+                  fmaxf(t[3] + bb.w, 0.f)};
     if (pool) {
       // the four pixels of a pooling window are the four lanes of a quad; the
       // values are >= 0 (or -0) after the ReLU, so their maximum is the
@@ -1000,22 +1155,21 @@ __device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const fl
       }
       const int qy = oy >> 1, qx = ox >> 1;
       if ((m & 3) == 0 && qy < h / 2 && qx < w / 2)
-        *reinterpret_cast<float4*>(out + ((int64_t)qy * (w / 2) + qx) * cout + nt * 16 + 4 * g) =
-            make_float4(v[0], v[1], v[2], v[3]);
+        store(((int64_t)qy * (w / 2) + qx) * cout + nt * 16 + 4 * g, v);
     } else if (oy < h && ox < w) {
-      *reinterpret_cast<float4*>(out + ((int64_t)oy * w + ox) * cout + nt * 16 + 4 * g) =
-          make_float4(v[0], v[1], v[2], v[3]);
+      store(((int64_t)oy * w + ox) * cout + nt * 16 + 4 * g, v);
     }
   }
 }
 
 // MT tiles of a band: tiles first, first + 4, ... (band-local tile index,
 // tiles_x per tile row), through the epilogue.
-template <int MT, int NT>
+template <int MT, int NT, bool H>
 __device__ __forceinline__ void band64_run(const unsigned char* lds, const Band64& b, int ty0,
-                                           const bf16x8* __restrict__ wf, const float* __restrict__ bias,
-                                           float* out, int cout, int pool, int tiles_x, int first,
-                                           int py, int px, int m, int g, int lane) {
+                                           const typename Band64Frag<H>::type* __restrict__ wf,
+                                           const float* __restrict__ bias, void* out, int cout,
+                                           int pool, int tiles_x, int first, int py, int px, int m,
+                                           int g, int lane, float out_scale, float st16) {
   int tr[MT], tc[MT];
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
@@ -1024,40 +1178,41 @@ __device__ __forceinline__ void band64_run(const unsigned char* lds, const Band6
     tc[i] = t - tr[i] * tiles_x;
   }
   f32x4 acc[MT][NT];
-  band64_tiles<MT, NT>(lds, b, wf, tr, tc, py, px, g, lane, acc);
+  band64_tiles<MT, NT, H>(lds, b, wf, tr, tc, py, px, g, lane, acc);
 #pragma unroll
   for (int i = 0; i < MT; ++i)
-    band64_epilogue<NT>(acc[i], bias, out, cout, 4 * (ty0 + tr[i]) + py, 4 * tc[i] + px, b.h, b.w,
-                        pool, m, g);
+    band64_epilogue<NT, H>(acc[i], bias, out, cout, 4 * (ty0 + tr[i]) + py, 4 * tc[i] + px, b.h,
+                           b.w, pool, m, g, out_scale, st16);
 }
 
 // One band's work of a 64-input-channel layer: ntile tiles over the 4 waves,
 // at most 4 per wave per round.
-template <int NT>
+template <int NT, bool H>
 __device__ __forceinline__ void band64_layer(const unsigned char* lds, const Band64& b, int ty0,
-                                             int ntile, const bf16x8* __restrict__ wf,
-                                             const float* __restrict__ bias, float* out, int cout,
+                                             int ntile,
+                                             const typename Band64Frag<H>::type* __restrict__ wf,
+                                             const float* __restrict__ bias, void* out, int cout,
                                              int pool, int tiles_x, int wave, int py, int px, int m,
-                                             int g, int lane) {
+                                             int g, int lane, float out_scale, float st16) {
   for (int base = 0; base < ntile; base += 4 * kBandWaves) {
     const int first = base + wave;
     const int mt = first >= ntile ? 0 : min(4, (ntile - first + kBandWaves - 1) / kBandWaves);
     switch (mt) {
       case 4:
-        band64_run<4, NT>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
-                          lane);
+        band64_run<4, NT, H>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m,
+                             g, lane, out_scale, st16);
         break;
       case 3:
-        band64_run<3, NT>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
-                          lane);
+        band64_run<3, NT, H>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m,
+                             g, lane, out_scale, st16);
         break;
       case 2:
-        band64_run<2, NT>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
-                          lane);
+        band64_run<2, NT, H>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m,
+                             g, lane, out_scale, st16);
         break;
       case 1:
-        band64_run<1, NT>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m, g,
-                          lane);
+        band64_run<1, NT, H>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m,
+                             g, lane, out_scale, st16);
         break;
       default:
         break;
@@ -1065,17 +1220,19 @@ __device__ __forceinline__ void band64_layer(const unsigned char* lds, const Ban
   }
 }
 
-// One 64-input-channel layer over bands of fp32 activations.
-template <int NT, bool G>
+// One 64-input-channel layer over bands of fp32 activations (H: through the
+// fp16 matrix cores, weights a.wts in scaled fp16 fragments).
+template <int NT, bool G, bool H>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_band64(ConvArgs a, Band64 b) {
+  typedef typename Band64Frag<H>::type frag;
   extern __shared__ __align__(16) unsigned char lds[];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int m = lane & 15, g = lane >> 4;
   int py, px;
   tile_pixel(m, py, px);
-  const bf16x8* wf = reinterpret_cast<const bf16x8*>(a.wts);
+  const frag* wf = reinterpret_cast<const frag*>(a.wts);
   band64_clear(lds, b);
   int64_t cnt = *a.count;
   if (cnt > a.max_count) cnt = a.max_count;
@@ -1090,12 +1247,25 @@ k_band64(ConvArgs a, Band64 b) {
     const int ty0 = bi * a.band_tiles;
     const int nty = min(a.band_tiles, a.tiles_y - ty0);
     const int64_t off = G ? slot_woff(a.nets, a.per_cam, a.idx, s) : 0;  // camera group
+    float in_scale = 1.0f, out_scale = 1.0f, st16 = 0.0f;
+    if constexpr (H) {
+      const float* sc = at_off(a.scl, off);
+      in_scale = sc[0];
+      out_scale = sc[1];
+      if (a.out_f16) st16 = sc[2];
+    }
+    const int64_t in_e = s * (int64_t)a.h * a.w * 64, out_e = s * (int64_t)ho * wo * a.cout;
     __syncthreads();  // the previous band's readers are done (and the clear)
-    stage_band64(a.act_in + s * (int64_t)a.h * a.w * 64, b, lds, 4 * ty0 - 1, 4 * nty + 2);
+    if (H && a.in_f16)
+      stage_band64_f16(reinterpret_cast<const _Float16*>(a.act_in) + in_e, b, lds, 4 * ty0 - 1,
+                       4 * nty + 2);
+    else
+      stage_band64<H>(a.act_in + in_e, b, lds, 4 * ty0 - 1, 4 * nty + 2, in_scale);
     __syncthreads();
-    band64_layer<NT>(lds, b, ty0, nty * a.tiles_x, at_off(wf, off), at_off(a.bias, off),
-                     a.act_out + s * (int64_t)ho * wo * a.cout, a.cout, a.pool, a.tiles_x, wave,
-                     py, px, m, g, lane);
+    void* out = st16 != 0.0f ? static_cast<void*>(reinterpret_cast<_Float16*>(a.act_out) + out_e)
+                             : static_cast<void*>(a.act_out + out_e);
+    band64_layer<NT, H>(lds, b, ty0, nty * a.tiles_x, at_off(wf, off), at_off(a.bias, off), out,
+                        a.cout, a.pool, a.tiles_x, wave, py, px, m, g, lane, out_scale, st16);
   }
 }
 
@@ -1151,11 +1321,12 @@ __global__ void __launch_bounds__(256) k_prep_input(ConvArgs a, uint2* xin, int3
 // A wave loads the input of its next first-layer tile while computing the
 // current one.
 
-template <int NT, bool G>
+template <int NT, bool G, bool H>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int32_t xr,
          int32_t xw) {
   using X = Elt<uint16_t>;
+  typedef typename Band64Frag<H>::type frag1;
   extern __shared__ __align__(16) unsigned char lds[];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1163,7 +1334,7 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
   int py, px;
   tile_pixel(m, py, px);
   const bf16x8* wf0 = reinterpret_cast<const bf16x8*>(a0.wts);
-  const bf16x8* wf1 = reinterpret_cast<const bf16x8*>(a1.wts);
+  const frag1* wf1 = reinterpret_cast<const frag1*>(a1.wts);
   band64_clear(lds, b);
   int64_t cnt = *a0.count;
   if (cnt > a0.max_count) cnt = a0.max_count;
@@ -1195,6 +1366,7 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
   };
   // first-layer tile t: 8 MFMAs, bias, ReLU, hi / lo split into the planes
   const float* bias0 = a0.bias;  // the item's network (camera group)
+  float in_scale1 = 1.0f, out_scale1 = 1.0f, st16 = 0.0f;  // fp16 path: the second layer's scales
   auto l1_tile = [&](const bf16x8 (&w0)[2][4], int y0, int t, const uint4 (&x)[2]) {
     const int ti = t / tx0, tj = t - ti * tx0;
     const int r = 2 * ti + qy, col = 8 * tj + qx;
@@ -1217,12 +1389,16 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
         const float v1 = inside ? fmaxf(acc[nt][1] + bb.y, 0.f) : 0.f;
         const float v2 = inside ? fmaxf(acc[nt][2] + bb.z, 0.f) : 0.f;
         const float v3 = inside ? fmaxf(acc[nt][3] + bb.w, 0.f) : 0.f;
-        uint32_t h01, l01, h23, l23;
-        X::split2(v0, v1, h01, l01);
-        X::split2(v2, v3, h23, l23);
         const int ad = addr + 2 * nt * b.cp * 16;  // chunk 2 nt + g / 2
-        *reinterpret_cast<uint2*>(lds + ad) = make_uint2(h01, h23);
-        *reinterpret_cast<uint2*>(lds + b.lo_bytes + ad) = make_uint2(l01, l23);
+        if constexpr (H) {
+          *reinterpret_cast<uint2*>(lds + ad) = f16x4_bits(v0, v1, v2, v3, in_scale1);
+        } else {
+          uint32_t h01, l01, h23, l23;
+          X::split2(v0, v1, h01, l01);
+          X::split2(v2, v3, h23, l23);
+          *reinterpret_cast<uint2*>(lds + ad) = make_uint2(h01, h23);
+          *reinterpret_cast<uint2*>(lds + b.lo_bytes + ad) = make_uint2(l01, l23);
+        }
       }
     }
   };
@@ -1235,6 +1411,12 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     const uint2* xs = xin + s * (int64_t)xr * xw;
     const int64_t off = G ? slot_woff(a0.nets, a0.per_cam, a0.idx, s) : 0;  // camera group
     bias0 = at_off(a0.bias, off);
+    if constexpr (H) {
+      const float* sc = at_off(a1.scl, off);
+      in_scale1 = sc[0];
+      out_scale1 = sc[1];
+      if (a1.out_f16) st16 = sc[2];
+    }
     const int y0 = 4 * ty0 - 1;
     const int t0n = (2 * nty + 1) * tx0;     // first-layer tiles: rows 4 nty + 2
     const int tfirst = prev_rows ? tx0 : 0;  // rows 0-1 copied after an image's first band
@@ -1255,7 +1437,7 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     if (prev_rows) {
       // rows prev_rows - 2, prev_rows - 1 -> rows 0, 1 of every chunk plane
       const int per = 2 * b.wb;
-      for (int u = threadIdx.x; u < 16 * per; u += blockDim.x) {
+      for (int u = threadIdx.x; u < 8 * b.planes * per; u += blockDim.x) {
         const int pc = u / per, e = u - pc * per;  // plane x chunk, unit in the two rows
         const int base = ((pc >> 3) * 8 * b.cp + (pc & 7) * b.cp) * 16;
         const uint4 v = *reinterpret_cast<const uint4*>(lds + base + ((prev_rows - 2) * b.wb + e) * 16);
@@ -1270,9 +1452,11 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
       xc[1] = xn[1];
     }
     __syncthreads();  // planes complete
-    band64_layer<NT>(lds, b, ty0, nty * a1.tiles_x, at_off(wf1, off), at_off(a1.bias, off),
-                     a1.act_out + s * (int64_t)ho * wo * a1.cout, a1.cout, a1.pool, a1.tiles_x,
-                     wave, py, px, m, g, lane);
+    const int64_t out_e = s * (int64_t)ho * wo * a1.cout;
+    void* out = st16 != 0.0f ? static_cast<void*>(reinterpret_cast<_Float16*>(a1.act_out) + out_e)
+                             : static_cast<void*>(a1.act_out + out_e);
+    band64_layer<NT, H>(lds, b, ty0, nty * a1.tiles_x, at_off(wf1, off), at_off(a1.bias, off), out,
+                        a1.cout, a1.pool, a1.tiles_x, wave, py, px, m, g, lane, out_scale1, st16);
   };
   // Rounds of work either way: image-major (a band there skips recomputing
   // two of its first-layer rows, counted as a tenth of its cost) or one band
@@ -1323,6 +1507,8 @@ struct DenseArgs {
   uint8_t* dec;
   float* frame_logit;
   double c_low, c_high;
+  const float* scl;         // fp16 path: (input scale, output scale) in the weight image
+  int32_t feat_f16;         // fp16 path: feat holds fp16 values already times the input scale
   const CamNet* nets;       // camera group (else null)
   int64_t per_cam;
 };
@@ -1419,6 +1605,12 @@ __global__ void __launch_bounds__(64 * kDenseWaves) k_dense(DenseArgs a) {
       const T* w1 = at_off(reinterpret_cast<const T*>(a.w1), off);
       const float* b1 = at_off(a.b1, off);
       const float* w2 = at_off(a.w2, off);
+      float in_scale = 1.0f, out_scale = 1.0f;
+      if constexpr (X::CVT) {
+        const float* sc = at_off(a.scl, off);
+        in_scale = sc[0];
+        out_scale = sc[1];
+      }
       bool valid[MT];
       const float* arow[MT];
 #pragma unroll
@@ -1449,6 +1641,10 @@ __global__ void __launch_bounds__(64 * kDenseWaves) k_dense(DenseArgs a) {
           typename X::frag av = X::zero(), av_lo = X::zero();
           if constexpr (SPLIT) {
             if (valid[mt] && kin) X::split8(arow[mt] + k0, av, av_lo);
+          } else if constexpr (X::CVT) {
+            if (valid[mt] && kin)
+              av = a.feat_f16 ? X::load(reinterpret_cast<const _Float16*>(a.feat) + (arow[mt] - a.feat) + k0)
+                              : X::cvt8(arow[mt] + k0, in_scale);
           } else {
             if (valid[mt] && kin) av = arow[mt][k0];
           }
@@ -1472,6 +1668,7 @@ __global__ void __launch_bounds__(64 * kDenseWaves) k_dense(DenseArgs a) {
           t[nt] = part[0][mt][nt][lane];
 #pragma unroll
           for (int w = 1; w < NW; ++w) t[nt] += part[w][mt][nt][lane];
+          if constexpr (X::CVT) t[nt] *= out_scale;
         }
         dense_out<NT, G>(a, t, b1, w2, b2, c_low, c_high, grp * R + mt * 16, cnt, cam, m, g);
       }
@@ -1540,6 +1737,7 @@ __global__ void __launch_bounds__(64 * kDenseSplitWaves) k_dense_part(DenseArgs 
     for (;;) {
       const int64_t off = G ? (int64_t)a.nets[cam].woff : 0;
       const T* w1 = at_off(reinterpret_cast<const T*>(a.w1), off);
+      const float in_scale = X::CVT ? at_off(a.scl, off)[0] : 1.0f;
       const bool valid = s < cnt && (!G || cam_of(s) == cam);
       const float* arow = a.feat + (valid ? s : 0) * (int64_t)a.flat + g * E;
       // as in k_dense: a lane group's E values of the last K step are all
@@ -1556,6 +1754,10 @@ __global__ void __launch_bounds__(64 * kDenseSplitWaves) k_dense_part(DenseArgs 
         typename X::frag av = X::zero(), av_lo = X::zero();
         if constexpr (SPLIT) {
           if (valid && kin) X::split8(arow + k0, av, av_lo);
+        } else if constexpr (X::CVT) {
+          if (valid && kin)
+            av = a.feat_f16 ? X::load(reinterpret_cast<const _Float16*>(a.feat) + (arow - a.feat) + k0)
+                            : X::cvt8(arow + k0, in_scale);
         } else {
           if (valid && kin) av = arow[k0];
         }
@@ -1620,8 +1822,19 @@ __global__ void __launch_bounds__(256) k_dense_finish(DenseArgs a, const f32x4* 
         c_low = cn.c_low;
         c_high = cn.c_high;
       }
-      dense_out<NT, G>(a, t, at_off(a.b1, off), at_off(a.w2, off), b2, c_low, c_high, tile * 16,
-                       cnt, cam, m, g);
+      if constexpr (Elt<T>::CVT) {
+        // the camera's output scale (a row's partial sums hold only its own
+        // camera's products, and this pass writes only that camera's rows)
+        f32x4 u[NT];
+        const float sc = at_off(a.scl, off)[1];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) u[nt] = t[nt] * sc;
+        dense_out<NT, G>(a, u, at_off(a.b1, off), at_off(a.w2, off), b2, c_low, c_high,
+                         tile * 16, cnt, cam, m, g);
+      } else {
+        dense_out<NT, G>(a, t, at_off(a.b1, off), at_off(a.w2, off), b2, c_low, c_high,
+                         tile * 16, cnt, cam, m, g);
+      }
       if constexpr (!G) break;
       int64_t next = -1;
       for (int r = 0; r < 16 && next < 0; ++r) {
@@ -1852,10 +2065,11 @@ int launch_pair(int nt0, int nt1, const ConvArgs& a0, const ConvArgs& a1, const 
 }  // namespace
 
 // Band plan of a 64-input-channel bf16 layer (k_band64 / k_pair64): the
-// tallest band of at most 16 tiles (4 per wave) whose planes fit 80 KB, so
-// that two workgroups share a CU, else one band row in up to 160 KB.  False
-// when the layer does not qualify or no band fits.
-bool band64_plan(const CnnLayer& L, Band64* b, int32_t* band_tiles, size_t* lds) {
+// tallest band of at most 16 tiles (4 per wave) whose planes (one fp16 plane
+// with h16, else the bf16 hi and lo planes) fit 80 KB, so that two workgroups
+// share a CU, else one band row in up to 160 KB.  The fp16 scales are those
+// of the layer.  False when the layer does not qualify or no band fits.
+bool band64_plan(const CnnLayer& L, bool h16, Band64* b, int32_t* band_tiles, size_t* lds) {
   if (L.cin != 64 || (L.cout != 64 && L.cout != 32)) return false;
   int32_t ty, tx;
   conv_tiles(L, &ty, &tx);
@@ -1869,6 +2083,7 @@ bool band64_plan(const CnnLayer& L, Band64* b, int32_t* band_tiles, size_t* lds)
     p.wb = wb;
     p.cp = p.rows * wb + 1;
     p.lo_bytes = 8 * p.cp * 16;
+    p.planes = h16 ? 1 : 2;
     return p;
   };
   int32_t bt = 16 / tx;
@@ -1888,7 +2103,7 @@ bool band64_plan(const CnnLayer& L, Band64* b, int32_t* band_tiles, size_t* lds)
 bool pair64_plan(const Cnn& cnn, Band64* b, int32_t* band_tiles, size_t* lds, int32_t* xr,
                  int32_t* xw) {
   if (!cnn.bf16 || cnn.n_layers < 2 || cnn.layers[0].cout != 64 || cnn.layers[0].pool) return false;
-  if (!band64_plan(cnn.layers[1], b, band_tiles, lds)) return false;
+  if (!band64_plan(cnn.layers[1], cnn.h16, b, band_tiles, lds)) return false;
   int32_t ty, tx;
   conv_tiles(cnn.layers[1], &ty, &tx);
   *xr = 4 * ty + 4;
@@ -1906,13 +2121,19 @@ int launch_band64(bool pair, int nt, const ConvArgs& a0, const ConvArgs& a1, con
   int64_t grid = kNumCU * per_cu;  // a multiple of 8 (see band_item)
   if (grid > items) grid = items;
   if (grid < 1) grid = 1;
-#define NSC_BAND_LAUNCH(N, G)                                                                   \
+#define NSC_BAND_LAUNCH2(N, G, H)                                                               \
   if (pair)                                                                                     \
-    hipLaunchKernelGGL((k_pair64<N, G>), dim3((unsigned)grid), dim3(64 * kBandWaves), lds, st,  \
-                       a0, a1, b, xin, xr, xw);                                                 \
+    hipLaunchKernelGGL((k_pair64<N, G, H>), dim3((unsigned)grid), dim3(64 * kBandWaves), lds,   \
+                       st, a0, a1, b, xin, xr, xw);                                             \
   else                                                                                          \
-    hipLaunchKernelGGL((k_band64<N, G>), dim3((unsigned)grid), dim3(64 * kBandWaves), lds, st,  \
-                       a1, b)
+    hipLaunchKernelGGL((k_band64<N, G, H>), dim3((unsigned)grid), dim3(64 * kBandWaves), lds,   \
+                       st, a1, b)
+#define NSC_BAND_LAUNCH(N, G)                                                                   \
+  if (b.planes == 1) {                                                                          \
+    NSC_BAND_LAUNCH2(N, G, true);                                                               \
+  } else {                                                                                      \
+    NSC_BAND_LAUNCH2(N, G, false);                                                              \
+  }
 #define NSC_BAND_CASE(N)                                                                        \
   case N:                                                                                       \
     if (a1.nets) {                                                                              \
@@ -1929,6 +2150,7 @@ int launch_band64(bool pair, int nt, const ConvArgs& a0, const ConvArgs& a1, con
   }
 #undef NSC_BAND_CASE
 #undef NSC_BAND_LAUNCH
+#undef NSC_BAND_LAUNCH2
   NSC_CHECK_LAUNCH(pair ? "k_pair64" : "k_band64");
   return NSC_OK;
 }
@@ -1989,14 +2211,50 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
     a.kpad = L.kpad;
     a.pool = L.pool ? 1 : 0;
     conv_tiles(L, &a.tiles_y, &a.tiles_x);
+    a.scl = cnn.scales + 2 * l;
     a.nets = r.nets;
     a.per_cam = r.per_cam;
     return a;
   };
-  // weights in fragment order for the banded kernels
-  auto frag_weights = [&](int l) {
-    return static_cast<const void*>(static_cast<const unsigned char*>(cnn.conv_wf) +
+  // weights in fragment order for the banded kernels (bf16; scaled fp16 for
+  // the layers on the fp16 path)
+  auto frag_weights = [&](int l, bool h16) {
+    return static_cast<const void*>(static_cast<const unsigned char*>(h16 ? cnn.conv_wh : cnn.conv_wf) +
                                     cnn.layers[l].w_off * 2);
+  };
+  // Which layers run on the fp16 band path (k_pair64's second layer,
+  // k_band64), and where activations between two such layers (or into the
+  // fp16 dense layer) are stored as fp16: the producer writes them scaled for
+  // the consumer, which stages them as they are.
+  bool band[NSC_MAX_CONV] = {};
+  bool out16[NSC_MAX_CONV] = {};
+  {
+    Band64 pb{};
+    int32_t pbt = 0, pxr = 0, pxw = 0;
+    size_t plds = 0;
+    const bool p64 = pair64_plan(cnn, &pb, &pbt, &plds, &pxr, &pxw);
+    bool pair = false;
+    if (!p64 && cnn.n_layers >= 2) {
+      ConvArgs t0 = layer_args(0), t1 = layer_args(1);
+      PairArgs tp{};
+      size_t tl = 0;
+      pair = pair_plan(cnn, &t0, &t1, &tp, &tl);
+    }
+    for (int l = 1; l < cnn.n_layers; ++l) {
+      Band64 b{};
+      int32_t bt = 0;
+      size_t lds = 0;
+      if (l == 1 && (p64 || pair))
+        band[l] = p64 && cnn.h16;
+      else
+        band[l] = cnn.h16 && band64_plan(cnn.layers[l], true, &b, &bt, &lds);
+    }
+    for (int l = 0; l < cnn.n_layers; ++l)
+      out16[l] = band[l] && (l + 1 < cnn.n_layers ? band[l + 1] : cnn.h16);
+  }
+  auto set_formats = [&](ConvArgs& a, int l) {
+    a.in_f16 = l > 0 && out16[l - 1];
+    a.out_f16 = out16[l];
   };
   int first_layered = 0;
   {
@@ -2005,8 +2263,9 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
     size_t lds = 0;
     if (pair64_plan(cnn, &b, &bt, &lds, &xr, &xw)) {
       ConvArgs a0 = layer_args(0), a1 = layer_args(1);
-      a0.wts = frag_weights(0);
-      a1.wts = frag_weights(1);
+      set_formats(a1, 1);
+      a0.wts = frag_weights(0, false);
+      a1.wts = frag_weights(1, cnn.h16);
       a1.band_tiles = bt;
       uint2* xin = reinterpret_cast<uint2*>(static_cast<unsigned char*>(ws) +
                                             2 * per * (size_t)r.max_count + 256);
@@ -2039,12 +2298,13 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
   for (int l = first_layered; l < cnn.n_layers; ++l) {
     const CnnLayer& L = cnn.layers[l];
     ConvArgs a = layer_args(l);
+    set_formats(a, l);
     if (cnn.bf16 && l > 0) {
       Band64 b{};
       int32_t bt = 0;
       size_t lds = 0;
-      if (band64_plan(L, &b, &bt, &lds)) {
-        a.wts = frag_weights(l);
+      if (band64_plan(L, cnn.h16, &b, &bt, &lds)) {
+        a.wts = frag_weights(l, cnn.h16);
         a.band_tiles = bt;
         const int rc =
             launch_band64(false, L.cout / 16, a, a, b, nullptr, 0, 0, lds, r.max_count, stream);
@@ -2075,7 +2335,9 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
   }
   DenseArgs d{};
   d.feat = buf[(cnn.n_layers - 1) & 1];
-  d.w1 = cnn.w1;
+  d.w1 = cnn.h16 ? cnn.w1h : cnn.w1;
+  d.scl = cnn.scales + 2 * cnn.n_layers;
+  d.feat_f16 = out16[cnn.n_layers - 1];
   d.b1 = cnn.b1;
   d.w2 = cnn.w2;
   d.b2 = cnn.b2;
@@ -2103,6 +2365,9 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
     int64_t grid_fin = (tiles + 3) / 4;
     if (grid_fin > kNumCU * 4) grid_fin = kNumCU * 4;
     if (grid_fin < 1) grid_fin = 1;
+    if (cnn.h16)
+      return launch_dense_split_nt<_Float16>(nt, d, part, (unsigned)grid_part, (unsigned)grid_fin,
+                                             stream);
     return cnn.bf16 ? launch_dense_split_nt<uint16_t>(nt, d, part, (unsigned)grid_part,
                                                       (unsigned)grid_fin, stream)
                     : launch_dense_split_nt<float>(nt, d, part, (unsigned)grid_part,
@@ -2113,6 +2378,7 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
   int64_t grid = groups;
   if (grid > kNumCU * 2) grid = kNumCU * 2;
   if (grid < 1) grid = 1;
+  if (cnn.h16) return launch_dense_nt<_Float16>(nt, d, (unsigned)grid, stream);
   return cnn.bf16 ? launch_dense_nt<uint16_t>(nt, d, (unsigned)grid, stream)
                   : launch_dense_nt<float>(nt, d, (unsigned)grid, stream);
 }

@@ -175,13 +175,21 @@ struct CnnLayer {
   bool pool;
   int32_t kpad;             // padded reduction length of the packed weights
   size_t w_off, b_off;      // offsets (elements) into the packed weight/bias arrays
+  // bf16 networks, fp16 path (layers after the first): the layer's weights
+  // enter the fp16 matrix cores multiplied by 2^wexp (exact: every bf16
+  // weight within 2^31 of the largest is an fp16 value after the scaling) and
+  // its input activations multiplied by 2^-aexp (aexp >= 0, from the
+  // worst-case bound of the input for inputs in [-1, 1], so that no fp16
+  // value overflows); the accumulators are multiplied back by 2^(aexp - wexp)
+  int32_t wexp, aexp;
 };
 // bf16 networks also hold every layer's weights in MFMA fragment order
 // (conv_wf, same offsets w_off): for K step ks (32 values of the layer's K
 // order) and output-channel block nt, lane l = 16 g + m holds the 8 values
 // W[16 nt + m][32 ks + 8 g .. 32 ks + 8 g + 7], 16 bytes at element
 // ((ks * (cout / 16) + nt) * 64 + l) * 8, so one wave's fragment is 1 KB of
-// consecutive memory.
+// consecutive memory; conv_wh holds the same fragments as scaled fp16 values
+// for the layers whose activations run through the fp16 matrix cores.
 struct Cnn {
   nsc_cnn_desc desc;
   int32_t n_layers;
@@ -191,10 +199,17 @@ struct Cnn {
   void* dev;                // one allocation holding everything below
   void* conv_w;             // packed conv weights, bf16 or fp32
   void* conv_wf;            // bf16 networks: the same in fragment order (else null)
+  void* conv_wh;            // bf16 networks: the same as fp16, each layer times 2^wexp
+  void* w1h;                // bf16 networks: dense weights as fp16 times 2^dense_wexp
+  int32_t dense_wexp, dense_aexp;  // as CnnLayer::wexp / aexp, for the dense layer
+  bool h16;                 // bf16 network whose banded layers and dense layer take the
+                            // fp16 path (activations as fp16, one MFMA per product)
   float* conv_b;            // fp32 biases
   void* w1;                 // dense weights [D][flat] in (y, x, c) order
   float* b1;
   float* w2;                // output layer weights [D] (fp32)
+  float* scales;            // [2 (n_layers + 1)]: per layer, then the dense layer, the fp16
+                            // path's input scale 2^-aexp and output scale 2^(aexp - wexp)
   float b2;
   size_t act_elems;         // largest per-image activation (elements)
 };

@@ -148,6 +148,12 @@ def test_cnn_desc_checks_and_blob_size():
     d = nsc.make_desc((32,), (True,), 32, 50, 50, True)
     d.dtype = 7
     assert nsc.nsc_cnn_check(d) == -3
+    d.dtype = 3
+    assert nsc.nsc_cnn_check(d) == -3
+    for pairs in (False, True):
+        d = nsc.make_desc((64, 64), (False, True), 32, 50, 50, True, pairs)
+        assert d.dtype == (nsc.NSC_BF16_PAIRS if pairs else nsc.NSC_BF16)
+        assert nsc.nsc_cnn_check(d) == 0
 
 
 def test_status_strings():

@@ -167,14 +167,14 @@ def test_compact_parity(n, density):
 
 # -------------------------------------------------------------------- CNN
 
-def _cnn_case(spec, n_frames, n_img, fy=1, seed=5, max_count=None):
+def _cnn_case(spec, n_frames, n_img, fy=1, seed=5, max_count=None, pairs=False):
     hs, ws_ = spec.in_h * fy, spec.in_w * fy
     den = 9
     S = rng.integers(0, 255 * den + 1, size=(n_frames, hs, ws_, 3)).astype(np.int32)
     idx = np.sort(rng.choice(n_frames, size=n_img, replace=False)).astype(np.int32)
     wts = synth.cnn_weights(spec, seed)
     blob = synth.weight_blob(spec, wts)
-    desc = nsc.make_desc(spec.conv, spec.pool, spec.dense, spec.in_h, spec.in_w, spec.bf16)
+    desc = nsc.make_desc(spec.conv, spec.pool, spec.dense, spec.in_h, spec.in_w, spec.bf16, pairs)
     cnn = nsc.Cnn(desc, blob)
     max_count = n_img + 5 if max_count is None else max_count
     ws = torch.empty(nsc.nsc_cnn_workspace_bytes(cnn, max_count), dtype=torch.uint8, device=DEV)
@@ -259,10 +259,13 @@ def test_cnn_fused_pair_shapes(conv, pool, hw, fy):
     ((64, 64, 64), (True, True, True), (50, 50), 2),       # the 3-layer net, nested cells
     ((64, 64), (True, False), (10, 96), 1),                # ... 48-wide second layer
 ])
-def test_cnn_banded_shapes(conv, pool, hw, fy):
-    # bf16 layers with 64 input channels run banded, weights streamed in fragment order
+@pytest.mark.parametrize("pairs", [False, True], ids=["fp16-acts", "bf16-pairs"])
+def test_cnn_banded_shapes(conv, pool, hw, fy, pairs):
+    # bf16 layers with 64 input channels run banded, weights streamed in fragment
+    # order: on the fp16 matrix cores (fp16 activations between banded layers),
+    # or with hi / lo bf16 activation pairs
     spec = synth.CNNSpec(in_h=hw[0], in_w=hw[1], conv=conv, pool=pool, dense=32, bf16=True)
-    _cnn_case(spec, n_frames=16, n_img=9, fy=fy)
+    _cnn_case(spec, n_frames=16, n_img=9, fy=fy, pairs=pairs)
 
 
 @pytest.mark.parametrize("dense", [16, 32, 64, 128, 256])
