@@ -235,8 +235,9 @@ void checked_range(int64_t t0, int64_t n, int32_t s, int64_t* k0, int64_t* nc) {
 // Workspace layout of nsc_cascade_run (of the checked-frame cascade, plus the
 // checked frames' outputs before they are spread over their skip blocks).
 struct RunLayout {
-  size_t sums, fire, dec, idx, count, tiles, tile_last, carry, logit, scratch, cnn;
+  size_t sums, fire, dec, idx, count, tiles, tile_last, carry, logit, scratch, cnn, part;
   size_t sk_label, sk_defer, sk_fire, sk_score, sk_logit;
+  int64_t part_units;  // units the partial-sum section holds
   size_t total;
 };
 
@@ -273,6 +274,17 @@ RunLayout run_layout(const nsc_cascade_cfg* c0, const Cnn& cnn, int64_t n_frames
     L.sk_logit = take((size_t)n * 4);
   }
   L.cnn = take(cnn_workspace_bytes(cnn, n));
+  // fixed-reference detector fused into the area kernel: per-unit partial
+  // sums, bounded by the plan's units at one output row per band
+  if (c->ref_mode == NSC_REF_FIXED && c->grid_h * c->grid_w == 1) {
+    AreaPlan ap;
+    if (make_area_plan(c->in_h, c->in_w, c->frame_stride, reinterpret_cast<const void*>(kAlign),
+                       c->dd_h, c->dd_w, n > 0 ? n : 1, &ap) == NSC_OK &&
+        ap.wave) {
+      L.part_units = (int64_t)n * c->dd_h * ap.wg.waves_per_frame;
+      L.part = take((size_t)L.part_units * 3 * sizeof(int64_t));
+    }
+  }
   L.total = o;
   return L;
 }
@@ -689,9 +701,8 @@ int run_checked(const nsc_cascade_cfg* cfg, const Cnn& c, const uint8_t* frames,
   if (int rc = make_area_plan(cfg->in_h, cfg->in_w, cfg->frame_stride, frames, cfg->dd_h,
                               cfg->dd_w, n, &ap))
     return rc;
-  if (int rc = launch_area_sums(ap, frames, cfg->frame_stride, n, sums, st)) return rc;
-  if (int rc = mark(1)) return rc;
-  // 2: detector
+  // 2: detector (against a fixed reference image fused into step 1, its
+  // partial sums added up by a finishing kernel, when the plan allows)
   {
     const double den = (double)nsc_area_den(cfg->in_h, cfg->in_w, cfg->dd_h, cfg->dd_w);
     DiffArgs a{};
@@ -714,7 +725,18 @@ int run_checked(const nsc_cascade_cfg* cfg, const Cnn& c, const uint8_t* frames,
     a.delta = prev ? cfg->delta : 0;
     a.score = score_out;
     a.fire = fire;
-    if (int rc = launch_diff(a, st)) return rc;
+    int64_t* part = reinterpret_cast<int64_t*>(w + L.part);
+    const bool fused = area_detect_fused(ap, a) && L.part_units > 0 &&
+                       area_detect_part_count(ap, n) <= L.part_units;
+    if (fused) {
+      if (int rc = launch_area_detect_fixed(ap, frames, cfg->frame_stride, n, sums, a, part, st))
+        return rc;
+      if (int rc = mark(1)) return rc;
+    } else {
+      if (int rc = launch_area_sums(ap, frames, cfg->frame_stride, n, sums, st)) return rc;
+      if (int rc = mark(1)) return rc;
+      if (int rc = launch_diff(a, st)) return rc;
+    }
   }
   if (int rc = mark(2)) return rc;
   // 3: compaction

@@ -61,6 +61,45 @@ __device__ __forceinline__ void load_chunk(const uint8_t* p, uint32_t (&v)[CB >=
   }
 }
 
+__device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// The sums one metric needs over a set of values: squared differences e,
+// absolute differences s, squared reference values r.  All exact in int64.
+template <int M>
+struct DiffSums {
+  int64_t e = 0, s = 0, r = 0;
+  __device__ __forceinline__ void add(int32_t x, int32_t y) {
+    const int64_t d = (int64_t)x - y;
+    if constexpr (M != NSC_METRIC_SAD) e += d * d;
+    if constexpr (M == NSC_METRIC_SAD) s += d < 0 ? -d : d;
+    if constexpr (M == NSC_METRIC_NRMSE) r += (int64_t)y * y;
+  }
+  __device__ __forceinline__ void reduce() {
+    if constexpr (M != NSC_METRIC_SAD) e = wave_sum_i64(e);
+    if constexpr (M == NSC_METRIC_SAD) s = wave_sum_i64(s);
+    if constexpr (M == NSC_METRIC_NRMSE) r = wave_sum_i64(r);
+  }
+  // The metric over `count` values (Sec. 5 and the alternatives it names):
+  // each is one fp64 expression of the exact sums, in a fixed operation order.
+  __device__ __forceinline__ double value(const DiffArgs& a, double count) const {
+    if constexpr (M == NSC_METRIC_MSE) {
+      return (double)e / (a.den2 * count);
+    } else if constexpr (M == NSC_METRIC_SAD) {
+      return (double)s / a.den;
+    } else if constexpr (M == NSC_METRIC_NRMSE) {
+      if (r == 0) return e == 0 ? 0.0 : INFINITY;
+      return sqrt((double)e / (double)r);
+    } else {  // the negated PSNR, -10 log10(255^2 / MSE); -inf for identical images
+      const double mse = (double)e / (a.den2 * count);
+      return -(10.0 * log10(65025.0 / mse));
+    }
+  }
+};
+
 // Vertical pass of one output row for one lane's chunk of CB bytes: the
 // output row covers source rows j0..j1-1; the first and last may be partial
 // (weights wf, wl), every row in between has the full weight q.  Each row is
@@ -211,11 +250,21 @@ __global__ void __launch_bounds__(1024) k_area_sums_rows(const uint8_t* __restri
 // once, after the last source row: on this architecture a store makes the
 // wave wait for it before it may consume later loads, so stores interleaved
 // with the row stream would stall it.
-template <int CB, bool PACKED, int RB = NSC_ROWS_BATCH>
+//
+// FM >= 0 fuses the difference detector against a fixed reference image
+// (global metric FM): as the wave stores its band's sums it also adds up the
+// metric's exact integer sums of its cells against the reference sums (read
+// once per wave from L2, where the small reference image stays resident) and
+// writes them as the unit's partial sums, part[unit][3] = (sum of squared
+// differences, of absolute differences, of squared reference values);
+// k_diff_fixed_finish adds a frame's partials and applies the metric.
+template <int CB, bool PACKED, int RB = NSC_ROWS_BATCH, int FM = -1>
 __global__ void __launch_bounds__(256) k_area_sums_wave(const uint8_t* __restrict__ frames,
                                                         int64_t stride, Axis ay, Axis ax,
                                                         WaveGeom g, int32_t bands, int64_t n,
-                                                        int32_t* __restrict__ sums) {
+                                                        int32_t* __restrict__ sums,
+                                                        const int32_t* __restrict__ ref,
+                                                        int64_t* __restrict__ part) {
   using cell_t = typename std::conditional<PACKED, uint16_t, int32_t>::type;
   extern __shared__ __align__(16) unsigned char smem[];
   // the wave index is uniform across the wave; say so, so that everything
@@ -305,53 +354,28 @@ __global__ void __launch_bounds__(256) k_area_sums_wave(const uint8_t* __restric
   }
   // the band's sums, one output row segment after another
   int32_t* out = sums + (f * (int64_t)Ho * Wo + X0) * 3;
+  DiffSums<FM < 0 ? NSC_METRIC_MSE : FM> acc;
   for (int Y = Y0; Y < Y1; ++Y) {
     const int32_t* srow = sbuf + (Y - Y0) * ncells;
     int32_t* orow = out + (int64_t)Y * Wo * 3;
-    for (int t = lane; t < ncells; t += 64) orow[t] = srow[t];
+    for (int t = lane; t < ncells; t += 64) {
+      const int32_t v = srow[t];
+      orow[t] = v;
+      if constexpr (FM >= 0) acc.add(v, ref[((int64_t)Y * Wo + X0) * 3 + t]);
+    }
+  }
+  if constexpr (FM >= 0) {
+    acc.reduce();
+    if (lane == 0) {
+      int64_t* pp = part + (f * per_frame + rem) * 3;
+      pp[0] = acc.e;
+      pp[1] = acc.s;
+      pp[2] = acc.r;
+    }
   }
 }
 
 // ------------------------------------------------------------- detector
-
-__device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
-// The sums one metric needs over a set of values: squared differences e,
-// absolute differences s, squared reference values r.  All exact in int64.
-template <int M>
-struct DiffSums {
-  int64_t e = 0, s = 0, r = 0;
-  __device__ __forceinline__ void add(int32_t x, int32_t y) {
-    const int64_t d = (int64_t)x - y;
-    if constexpr (M != NSC_METRIC_SAD) e += d * d;
-    if constexpr (M == NSC_METRIC_SAD) s += d < 0 ? -d : d;
-    if constexpr (M == NSC_METRIC_NRMSE) r += (int64_t)y * y;
-  }
-  __device__ __forceinline__ void reduce() {
-    if constexpr (M != NSC_METRIC_SAD) e = wave_sum_i64(e);
-    if constexpr (M == NSC_METRIC_SAD) s = wave_sum_i64(s);
-    if constexpr (M == NSC_METRIC_NRMSE) r = wave_sum_i64(r);
-  }
-  // The metric over `count` values (Sec. 5 and the alternatives it names):
-  // each is one fp64 expression of the exact sums, in a fixed operation order.
-  __device__ __forceinline__ double value(const DiffArgs& a, double count) const {
-    if constexpr (M == NSC_METRIC_MSE) {
-      return (double)e / (a.den2 * count);
-    } else if constexpr (M == NSC_METRIC_SAD) {
-      return (double)s / a.den;
-    } else if constexpr (M == NSC_METRIC_NRMSE) {
-      if (r == 0) return e == 0 ? 0.0 : INFINITY;
-      return sqrt((double)e / (double)r);
-    } else {  // the negated PSNR, -10 log10(255^2 / MSE); -inf for identical images
-      const double mse = (double)e / (a.den2 * count);
-      return -(10.0 * log10(65025.0 / mse));
-    }
-  }
-};
 
 // Blocked score by rows: a wave streams the frame row by row, lane l taking
 // values l + 64 j of each row (coalesced), whose block column is fixed; the
@@ -502,6 +526,27 @@ __device__ __forceinline__ double frame_score(const int32_t* cur, const int32_t*
     }
   }
   return z;
+}
+
+// The fixed-reference detector fused into the area kernel: a thread per
+// frame adds the frame's per-unit partial sums (exact integers, so their order
+// does not matter) and applies the metric as k_diff does.
+template <int M>
+__global__ void __launch_bounds__(256) k_diff_fixed_finish(DiffArgs a, const int64_t* __restrict__ part,
+                                                           int32_t units) {
+#pragma clang fp contract(off)
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.n) return;
+  DiffSums<M> acc;
+  const int64_t* p = part + i * units * 3;
+  for (int u = 0; u < units; ++u) {
+    acc.e += p[3 * u];
+    acc.s += p[3 * u + 1];
+    acc.r += p[3 * u + 2];
+  }
+  const double score = acc.value(a, (double)((int64_t)a.dd_h * a.dd_w * 3));
+  a.fire[i] = score > a.delta_diff ? 1 : 0;
+  if (a.score) a.score[i] = score;
 }
 
 template <int M, bool BLK>
@@ -662,7 +707,8 @@ int launch_area_sums(const AreaPlan& p, const uint8_t* frames, int64_t stride, i
 #define NSC_WAVE_LAUNCH(CB, PK)                                                          \
   hipLaunchKernelGGL((k_area_sums_wave<CB, PK, CB == 32 ? NSC_ROWS_BATCH / 2 : NSC_ROWS_BATCH>), \
                      dim3((unsigned)wblocks), dim3(64 * g.waves_per_block),               \
-                     g.lds_bytes, stream, frames, stride, p.ay, p.ax, g, g.bands, n, sums)
+                     g.lds_bytes, stream, frames, stride, p.ay, p.ax, g, g.bands, n, sums,   \
+                     nullptr, nullptr)
     if (g.chunk_bytes == 32) {
       if (p.packed) NSC_WAVE_LAUNCH(32, true); else NSC_WAVE_LAUNCH(32, false);
     } else if (g.chunk_bytes == 16) {
@@ -724,6 +770,58 @@ int launch_diff(const DiffArgs& a, hipStream_t stream) {
   }
 #undef NSC_DIFF_LAUNCH
   NSC_CHECK_LAUNCH("k_diff");
+  return NSC_OK;
+}
+
+bool area_detect_fused(const AreaPlan& p, const DiffArgs& a) {
+  return p.wave && a.ref_mode == NSC_REF_FIXED && a.grid_h * a.grid_w == 1 && a.cams == nullptr &&
+         a.metric >= NSC_METRIC_MSE && a.metric <= NSC_METRIC_PSNR;
+}
+
+int64_t area_detect_part_count(const AreaPlan& p, int64_t n) {
+  return p.wave ? n * p.wg.bands * p.wg.waves_per_frame : 0;
+}
+
+int launch_area_detect_fixed(const AreaPlan& p, const uint8_t* frames, int64_t stride, int64_t n,
+                             int32_t* sums, const DiffArgs& a, int64_t* part, hipStream_t stream) {
+  if (n <= 0) return NSC_OK;
+  if (!area_detect_fused(p, a)) return fail(NSC_E_SHAPE, "the fused fixed-reference detector does not apply");
+  const WaveGeom& g = p.wg;
+  const int64_t units = n * g.bands * g.waves_per_frame;
+  const int64_t wblocks = (units + g.waves_per_block - 1) / g.waves_per_block;
+  if (wblocks > 0x7FFFFFFF) return fail(NSC_E_SHAPE, "too many frames in one call");
+#define NSC_FUSED_LAUNCH(CB, PK, M)                                                              \
+  hipLaunchKernelGGL((k_area_sums_wave<CB, PK, CB == 32 ? NSC_ROWS_BATCH / 2 : NSC_ROWS_BATCH, M>), \
+                     dim3((unsigned)wblocks), dim3(64 * g.waves_per_block), g.lds_bytes, stream,  \
+                     frames, stride, p.ay, p.ax, g, g.bands, n, sums, a.ref_sums, part)
+#define NSC_FUSED_CB(M)                                                                          \
+  if (g.chunk_bytes == 32) {                                                                     \
+    if (p.packed) NSC_FUSED_LAUNCH(32, true, M); else NSC_FUSED_LAUNCH(32, false, M);            \
+  } else if (g.chunk_bytes == 16) {                                                              \
+    if (p.packed) NSC_FUSED_LAUNCH(16, true, M); else NSC_FUSED_LAUNCH(16, false, M);            \
+  } else {                                                                                       \
+    if (p.packed) NSC_FUSED_LAUNCH(4, true, M); else NSC_FUSED_LAUNCH(4, false, M);              \
+  }                                                                                              \
+  NSC_CHECK_LAUNCH("k_area_sums_wave (fused detector)");                                         \
+  hipLaunchKernelGGL((k_diff_fixed_finish<M>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0,  \
+                     stream, a, (const int64_t*)part, (int32_t)(g.bands * g.waves_per_frame));   \
+  NSC_CHECK_LAUNCH("k_diff_fixed_finish")
+  switch (a.metric) {
+    case NSC_METRIC_MSE:
+      NSC_FUSED_CB(NSC_METRIC_MSE);
+      break;
+    case NSC_METRIC_SAD:
+      NSC_FUSED_CB(NSC_METRIC_SAD);
+      break;
+    case NSC_METRIC_NRMSE:
+      NSC_FUSED_CB(NSC_METRIC_NRMSE);
+      break;
+    default:
+      NSC_FUSED_CB(NSC_METRIC_PSNR);
+      break;
+  }
+#undef NSC_FUSED_CB
+#undef NSC_FUSED_LAUNCH
   return NSC_OK;
 }
 

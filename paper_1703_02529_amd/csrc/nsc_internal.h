@@ -110,6 +110,13 @@ struct DiffArgs {
   int64_t state_stride;
 };
 int launch_diff(const DiffArgs& a, hipStream_t stream);
+// Area sums with the fixed-reference global detector fused in (when
+// area_detect_fused): per-unit partial sums in `part` (area_detect_part_count
+// units x 3 int64), then the scores and fire flags of `a`.
+bool area_detect_fused(const AreaPlan& p, const DiffArgs& a);
+int64_t area_detect_part_count(const AreaPlan& p, int64_t n);
+int launch_area_detect_fixed(const AreaPlan& p, const uint8_t* frames, int64_t stride, int64_t n,
+                             int32_t* sums, const DiffArgs& a, int64_t* part, hipStream_t stream);
 
 // Compaction of fire flags into ascending indices.
 int64_t compact_tiles(int64_t n);
