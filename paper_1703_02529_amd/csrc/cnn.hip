@@ -924,6 +924,14 @@ __device__ __forceinline__ void band64_clear(unsigned char* lds, const Band64& b
     *reinterpret_cast<uint4*>(lds + (size_t)i * 16) = make_uint4(0u, 0u, 0u, 0u);
 }
 
+// floor(pix / w) for a band pixel index, without an integer division.  A
+// band's pixels fit the LDS (pix < rows * wb <= 1280), so the exact quotient
+// (pix + 1/2) / w lies at least 1 / (2 w) >= 3.9e-4 from an integer, while the
+// two fp32 roundings move it by at most 2^-23 of itself (< 1.6e-4).
+__device__ __forceinline__ int band_row(int pix, float inv_w) {
+  return (int)(((float)pix + 0.5f) * inv_w);
+}
+
 // Stages band rows [0, rows_used), columns 1..w: image rows y0 + r inside the
 // image from one image's fp32 NHWC 64-channel activations, split into hi / lo
 // bf16 (H = false) or as fp16 times in_scale (H), zeros for rows outside.
@@ -933,9 +941,10 @@ __device__ __forceinline__ void stage_band64(const float* __restrict__ src, cons
                                              unsigned char* lds, int y0, int rows_used,
                                              float in_scale) {
   const int units = rows_used * b.w * 8;
+  const float inv_w = 1.0f / (float)b.w;
   for (int u = threadIdx.x; u < units; u += blockDim.x) {
     const int pix = u >> 3, c = u & 7;
-    const int r = pix / b.w, x = pix - r * b.w;
+    const int r = band_row(pix, inv_w), x = pix - r * b.w;
     const int y = y0 + r;
     uint4 hi = make_uint4(0u, 0u, 0u, 0u), lo = hi;
     if ((unsigned)y < (unsigned)b.h) {
@@ -963,9 +972,10 @@ __device__ __forceinline__ void stage_band64(const float* __restrict__ src, cons
 __device__ __forceinline__ void stage_band64_f16(const _Float16* __restrict__ src, const Band64& b,
                                                  unsigned char* lds, int y0, int rows_used) {
   const int units = rows_used * b.w * 8;
+  const float inv_w = 1.0f / (float)b.w;
   for (int u = threadIdx.x; u < units; u += blockDim.x) {
     const int pix = u >> 3, c = u & 7;
-    const int r = pix / b.w, x = pix - r * b.w;
+    const int r = band_row(pix, inv_w), x = pix - r * b.w;
     const int y = y0 + r;
     uint4 v = make_uint4(0u, 0u, 0u, 0u);
     if ((unsigned)y < (unsigned)b.h)
