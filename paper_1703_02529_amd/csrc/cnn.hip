@@ -1800,60 +1800,77 @@ __global__ void __launch_bounds__(64 * kDenseSplitWaves) k_dense_part(DenseArgs 
   }
 }
 
+// k_dense_finish: a workgroup per 16-survivor tile; its kDenseFinWaves waves
+// add interleaved subsets of the tile's K parts (wave w: parts w, w + 4, ...),
+// wave 0 adds the waves' sums in wave order and applies dense_out.
+constexpr int kDenseFinWaves = 4;
+
 template <typename T, int NT, bool G>
-__global__ void __launch_bounds__(256) k_dense_finish(DenseArgs a, const f32x4* __restrict__ part) {
+__global__ void __launch_bounds__(64 * kDenseFinWaves) k_dense_finish(DenseArgs a,
+                                                                     const f32x4* __restrict__ part) {
   constexpr int KS = Elt<T>::KS;
+  __shared__ f32x4 red[kDenseFinWaves][NT][64];
   const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int m = lane & 15, g = lane >> 4;
   int64_t cnt = *a.count;
   if (cnt > a.max_count) cnt = a.max_count;
   const int64_t tiles = (cnt + 15) / 16;
   const int kparts = dense_kparts(tiles, (a.flat + KS - 1) / KS);
-  const int64_t nw = (int64_t)gridDim.x * (blockDim.x >> 6);
-  for (int64_t tile = (int64_t)blockIdx.x * (blockDim.x >> 6) +
-                      __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-       tile < tiles; tile += nw) {
+  for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
     f32x4 t[NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) t[nt] = part[((tile * kparts) * NT + nt) * 64 + lane];
-    for (int kp = 1; kp < kparts; ++kp) {
+    for (int nt = 0; nt < NT; ++nt) t[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kp = wave; kp < kparts; kp += kDenseFinWaves) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) t[nt] += part[((tile * kparts + kp) * NT + nt) * 64 + lane];
     }
-    int64_t cam = G ? a.idx[tile * 16] / a.per_cam : 0;
-    for (;;) {
-      int64_t off = 0;
-      float b2 = a.b2;
-      double c_low = a.c_low, c_high = a.c_high;
-      if constexpr (G) {
-        const CamNet& cn = a.nets[cam];
-        off = cn.woff;
-        b2 = cn.b2;
-        c_low = cn.c_low;
-        c_high = cn.c_high;
-      }
-      if constexpr (Elt<T>::CVT) {
-        // the camera's output scale (a row's partial sums hold only its own
-        // camera's products, and this pass writes only that camera's rows)
-        f32x4 u[NT];
-        const float sc = at_off(a.scl, off)[1];
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) u[nt] = t[nt] * sc;
-        dense_out<NT, G>(a, u, at_off(a.b1, off), at_off(a.w2, off), b2, c_low, c_high,
-                         tile * 16, cnt, cam, m, g);
-      } else {
-        dense_out<NT, G>(a, t, at_off(a.b1, off), at_off(a.w2, off), b2, c_low, c_high,
-                         tile * 16, cnt, cam, m, g);
+    for (int nt = 0; nt < NT; ++nt) red[wave][nt][lane] = t[nt];
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        t[nt] = red[0][nt][lane];
+#pragma unroll
+        for (int w = 1; w < kDenseFinWaves; ++w) t[nt] += red[w][nt][lane];
       }
-      if constexpr (!G) break;
-      int64_t next = -1;
-      for (int r = 0; r < 16 && next < 0; ++r) {
-        const int64_t u = tile * 16 + r;
-        if (u < cnt && a.idx[u] / a.per_cam > cam) next = a.idx[u] / a.per_cam;
+      int64_t cam = G ? a.idx[tile * 16] / a.per_cam : 0;
+      for (;;) {
+        int64_t off = 0;
+        float b2 = a.b2;
+        double c_low = a.c_low, c_high = a.c_high;
+        if constexpr (G) {
+          const CamNet& cn = a.nets[cam];
+          off = cn.woff;
+          b2 = cn.b2;
+          c_low = cn.c_low;
+          c_high = cn.c_high;
+        }
+        if constexpr (Elt<T>::CVT) {
+          // the camera's output scale (a row's partial sums hold only its own
+          // camera's products, and this pass writes only that camera's rows)
+          f32x4 u[NT];
+          const float sc = at_off(a.scl, off)[1];
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) u[nt] = t[nt] * sc;
+          dense_out<NT, G>(a, u, at_off(a.b1, off), at_off(a.w2, off), b2, c_low, c_high,
+                           tile * 16, cnt, cam, m, g);
+        } else {
+          dense_out<NT, G>(a, t, at_off(a.b1, off), at_off(a.w2, off), b2, c_low, c_high,
+                           tile * 16, cnt, cam, m, g);
+        }
+        if constexpr (!G) break;
+        int64_t next = -1;
+        for (int r = 0; r < 16 && next < 0; ++r) {
+          const int64_t u = tile * 16 + r;
+          if (u < cnt && a.idx[u] / a.per_cam > cam) next = a.idx[u] / a.per_cam;
+        }
+        if (next < 0) break;
+        cam = next;
       }
-      if (next < 0) break;
-      cam = next;
-    }
+    }  // wave 0
+    __syncthreads();  // red is read before the next tile writes it
   }
 }
 
@@ -1892,8 +1909,8 @@ int launch_dense_split_nt(int nt, const DenseArgs& a, f32x4* part, unsigned grid
 #define NSC_SPLIT_LAUNCH(N, G)                                                                  \
   hipLaunchKernelGGL((k_dense_part<T, N, G>), dim3(grid_part), dim3(64 * kDenseSplitWaves), 0, \
                      st, a, part);                                                              \
-  hipLaunchKernelGGL((k_dense_finish<T, N, G>), dim3(grid_fin), dim3(256), 0, st, a,           \
-                     (const f32x4*)part)
+  hipLaunchKernelGGL((k_dense_finish<T, N, G>), dim3(grid_fin), dim3(64 * kDenseFinWaves), 0,  \
+                     st, a, (const f32x4*)part)
 #define NSC_SPLIT_CASE(N)                                                                       \
   case N:                                                                                       \
     if (a.nets) {                                                                               \
@@ -2372,7 +2389,7 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
     const int64_t tiles = (r.max_count + 15) / 16;
     int64_t grid_part = kDenseSplitItems;
     if (grid_part > kNumCU * 4) grid_part = kNumCU * 4;
-    int64_t grid_fin = (tiles + 3) / 4;
+    int64_t grid_fin = tiles;  // a workgroup per tile
     if (grid_fin > kNumCU * 4) grid_fin = kNumCU * 4;
     if (grid_fin < 1) grid_fin = 1;
     if (cnn.h16)
