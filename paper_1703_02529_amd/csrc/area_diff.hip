@@ -290,7 +290,9 @@ __global__ void __launch_bounds__(256) k_area_sums_wave(const uint8_t* __restric
   cell_t* buf = reinterpret_cast<cell_t*>(wbase);                              // column sums
   int32_t* sbuf = reinterpret_cast<int32_t*>(wbase + (size_t)64 * CB * sizeof(cell_t));  // band sums
 
-  const int64_t unit = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
+  // each XCD walks a contiguous range of frames, so the source rows that two
+  // bands of a frame share are fetched into one L2
+  const int64_t unit = xcd_block(blockIdx.x, gridDim.x) * (blockDim.x >> 6) + wv;
   const int64_t per_frame = (int64_t)bands * g.waves_per_frame;
   if (unit >= n * per_frame) return;
   const int64_t f = unit / per_frame;

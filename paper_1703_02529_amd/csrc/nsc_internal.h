@@ -26,6 +26,17 @@ int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
   } while (0)
 
 constexpr int kNumCU = 256;  // MI355X compute units (8 XCDs x 32)
+constexpr int kNumXCD = 8;
+
+// Logical index of workgroup b of a grid of nb: the hardware hands workgroup b
+// to XCD b mod 8, so numbering each XCD's workgroups consecutively gives each
+// XCD one contiguous range of the logical work (in its dispatch order), whose
+// neighbouring items share that XCD's L2.  A bijection of [0, nb).
+__device__ __forceinline__ int64_t xcd_block(int64_t b, int64_t nb) {
+  const int64_t x = b % kNumXCD, slot = b / kNumXCD;
+  const int64_t q = nb / kNumXCD, r = nb % kNumXCD;
+  return x * q + (x < r ? x : r) + slot;
+}
 
 inline int64_t gcd64(int64_t a, int64_t b) {
   while (b) {
