@@ -457,7 +457,33 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
     scales[2 * c.n_layers] = ldexpf(1.0f, -c.dense_aexp);
     scales[2 * c.n_layers + 1] = ldexpf(1.0f, c.dense_aexp - c.dense_wexp);
   }
-  // device image: [conv_w][conv_wf][conv_wh][conv_b][w1][w1h][b1][w2][scales]
+  // fp16 path with a 3-channel first layer (fused with the second by
+  // k_pair64): the first layer's bf16 fragments multiplied by the second
+  // layer's input scale 2^-aexp (exact), with the bias as two bf16 values
+  // (hi, and the remainder lo) in the taps (0, 0) and (0, 1) of channel 3,
+  // whose input is the constant 1: the matrix cores then produce the biased,
+  // scaled pre-activation, and the epilogue only applies the ReLU
+  std::vector<float> w0h;
+  if (c.h16 && c.n_layers >= 2 && c.layers[0].cin == 3 && c.layers[0].kpad == 64) {
+    const CnnLayer& L = c.layers[0];
+    const float s1 = ldexpf(1.0f, -c.layers[1].aexp);
+    const int nts = L.cout / 16;
+    w0h.assign((size_t)L.cout * L.kpad, 0.0f);
+    for (int ks = 0; ks < 2; ++ks)
+      for (int nt = 0; nt < nts; ++nt)
+        for (int lane = 0; lane < 64; ++lane)
+          for (int e = 0; e < 8; ++e) {
+            const int o = nt * 16 + (lane & 15), k = ks * 32 + (lane >> 4) * 8 + e;
+            float v = host_bf16_value(convw[L.w_off + (size_t)o * L.kpad + k]) * s1;
+            if (k == 3 || k == 7) {  // (dy, dx, c) = (0, 0, 3), (0, 1, 3): the bias
+              const float b = convb[L.b_off + o] * s1;
+              const float hi = host_bf16_value(b);
+              v = k == 3 ? hi : host_bf16_value(b - hi);
+            }
+            w0h[(((size_t)ks * nts + nt) * 64 + lane) * 8 + e] = v;
+          }
+  }
+  // device image: [conv_w][conv_wf][conv_wh][conv_b][w1][w1h][b1][w2][scales][w0h]
   const size_t o_cw = 0;
   const size_t o_cwf = align_up(o_cw + conv_elems * es, kAlign);
   const size_t o_cwh = align_up(o_cwf + convwf.size() * es, kAlign);
@@ -467,7 +493,8 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
   const size_t o_b1 = align_up(o_w1h + w1h.size() * 2, kAlign);
   const size_t o_w2 = align_up(o_b1 + (size_t)c.dense * 4, kAlign);
   const size_t o_sc = align_up(o_w2 + (size_t)c.dense * 4, kAlign);
-  const size_t total = align_up(o_sc + scales.size() * 4, kAlign);
+  const size_t o_w0h = align_up(o_sc + scales.size() * 4, kAlign);
+  const size_t total = align_up(o_w0h + w0h.size() * 2, kAlign);
   std::vector<unsigned char> img(total, 0);
   auto put = [&](size_t off, const std::vector<float>& v, bool as_bf16) {
     if (as_bf16) {
@@ -488,6 +515,7 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
   put(o_b1, b1, false);
   put(o_w2, w2, false);
   put(o_sc, scales, false);
+  if (!w0h.empty()) put(o_w0h, w0h, true);
   void* dev = nullptr;
   if (hipMalloc(&dev, total) != hipSuccess)
     return fail(NSC_E_NOMEM, "hipMalloc of %zu bytes for CNN weights failed", total);
@@ -506,6 +534,7 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
   c.b1 = reinterpret_cast<float*>(b + o_b1);
   c.w2 = reinterpret_cast<float*>(b + o_w2);
   c.scales = reinterpret_cast<float*>(b + o_sc);
+  c.conv_w0h = w0h.empty() ? nullptr : b + o_w0h;
   nsc_cnn* h = new (std::nothrow) nsc_cnn;
   if (!h) {
     (void)hipFree(dev);

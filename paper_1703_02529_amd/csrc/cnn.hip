@@ -1129,28 +1129,33 @@ constexpr int kQuadXor1 = 0xB1;  // [1, 0, 3, 2]
 constexpr int kQuadXor2 = 0x4E;  // [2, 3, 0, 1]
 
 // Bias, ReLU, optional 2x2 max-pool and NHWC stores of one transposed tile;
-// (oy, ox) is this lane's pixel in the layer's input grid.  The fp16 path
-// first multiplies the accumulators by sc (a power of two).  The output is
-// fp32 (16-byte stores), or with st16 != 0 fp16 values times st16 (the next
-// layer's input scale; 8-byte stores).
-template <int NT, bool H>
-__device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const float* __restrict__ bp,
-                                                void* out, int cout, int oy, int ox, int h, int w,
-                                                int pool, int m, int g, float sc, float st16) {
+// (oy, ox) is this lane's pixel in the layer's input grid.  Each value is
+// max(acc * k + bb, 0) in one fused multiply-add: on the fp16 path k is the
+// accumulator scale times the output scale s and bb the bias times s (s the
+// next layer's input scale when the output is fp16, else 1; all scales are
+// powers of two, so this equals scaling after the bias and the ReLU, bit for
+// bit); otherwise k = 1 and bb is the bias.  The output is fp32 (16-byte
+// stores), or with f16out fp16 (8-byte stores).
+template <int NT>
+__device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const float4 (&bb)[NT],
+                                                float k, void* out, int cout, int oy, int ox, int h,
+                                                int w, int pool, int m, bool f16out) {
   auto store = [&](int64_t e, const float (&v)[4]) {  // element offset e, 4 channels
-    if (st16 != 0.0f)
+    if (f16out)
       *reinterpret_cast<uint2*>(static_cast<_Float16*>(out) + e) =
-          f16x4_bits(v[0], v[1], v[2], v[3], st16);
+          make_uint2(__builtin_bit_cast(uint32_t, f16x2{(_Float16)v[0], (_Float16)v[1]}),
+                     __builtin_bit_cast(uint32_t, f16x2{(_Float16)v[2], (_Float16)v[3]}));
     else
       *reinterpret_cast<float4*>(static_cast<float*>(out) + e) = make_float4(v[0], v[1], v[2], v[3]);
   };
+  const int qy = oy >> 1, qx = ox >> 1;
+  const bool st = pool ? ((m & 3) == 0 && qy < (h >> 1) && qx < (w >> 1)) : (oy < h && ox < w);
+  const int64_t e0 = pool ? ((int64_t)qy * (w >> 1) + qx) * cout : ((int64_t)oy * w + ox) * cout;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    const float4 bb = *reinterpret_cast<const float4*>(bp + nt * 16 + 4 * g);
-    f32x4 t = acc[nt];
-    if constexpr (H) t *= sc;
-    float v[4] = {fmaxf(t[0] + bb.x, 0.f), fmaxf(t[1] + bb.y, 0.f), fmaxf(t[2] + bb.z, 0.f),
-                  fmaxf(t[3] + bb.w, 0.f)};
+    const f32x4 t = acc[nt];
+    float v[4] = {fmaxf(fmaf(t[0], k, bb[nt].x), 0.f), fmaxf(fmaf(t[1], k, bb[nt].y), 0.f),
+                  fmaxf(fmaf(t[2], k, bb[nt].z), 0.f), fmaxf(fmaf(t[3], k, bb[nt].w), 0.f)};
     if (pool) {
       // the four pixels of a pooling window are the four lanes of a quad; the
       // values are >= 0 (or -0) after the ReLU, so their maximum is the
@@ -1163,23 +1168,20 @@ __device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const fl
         iv = max(iv, __builtin_amdgcn_update_dpp(0, iv, kQuadXor2, 0xF, 0xF, false));
         v[r] = __int_as_float(iv);
       }
-      const int qy = oy >> 1, qx = ox >> 1;
-      if ((m & 3) == 0 && qy < h / 2 && qx < w / 2)
-        store(((int64_t)qy * (w / 2) + qx) * cout + nt * 16 + 4 * g, v);
-    } else if (oy < h && ox < w) {
-      store(((int64_t)oy * w + ox) * cout + nt * 16 + 4 * g, v);
     }
+    if (st) store(e0 + nt * 16, v);
   }
 }
 
 // MT tiles of a band: tiles first, first + 4, ... (band-local tile index,
-// tiles_x per tile row), through the epilogue.
+// tiles_x per tile row), through the epilogue.  out already points at this
+// lane's channel group (4 g).
 template <int MT, int NT, bool H>
 __device__ __forceinline__ void band64_run(const unsigned char* lds, const Band64& b, int ty0,
                                            const typename Band64Frag<H>::type* __restrict__ wf,
-                                           const float* __restrict__ bias, void* out, int cout,
+                                           const float4 (&bb)[NT], float k, void* out, int cout,
                                            int pool, int tiles_x, int first, int py, int px, int m,
-                                           int g, int lane, float out_scale, float st16) {
+                                           int g, int lane, bool f16out) {
   int tr[MT], tc[MT];
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
@@ -1191,38 +1193,50 @@ __device__ __forceinline__ void band64_run(const unsigned char* lds, const Band6
   band64_tiles<MT, NT, H>(lds, b, wf, tr, tc, py, px, g, lane, acc);
 #pragma unroll
   for (int i = 0; i < MT; ++i)
-    band64_epilogue<NT, H>(acc[i], bias, out, cout, 4 * (ty0 + tr[i]) + py, 4 * tc[i] + px, b.h,
-                           b.w, pool, m, g, out_scale, st16);
+    band64_epilogue<NT>(acc[i], bb, k, out, cout, 4 * (ty0 + tr[i]) + py, 4 * tc[i] + px, b.h,
+                        b.w, pool, m, f16out);
 }
 
 // One band's work of a 64-input-channel layer: ntile tiles over the 4 waves,
-// at most 4 per wave per round.
+// at most 4 per wave per round.  sc is the accumulator scale (fp16 path, else
+// 1) and st16 the next layer's input scale when the output is fp16 (else 0).
 template <int NT, bool H>
 __device__ __forceinline__ void band64_layer(const unsigned char* lds, const Band64& b, int ty0,
                                              int ntile,
                                              const typename Band64Frag<H>::type* __restrict__ wf,
                                              const float* __restrict__ bias, void* out, int cout,
                                              int pool, int tiles_x, int wave, int py, int px, int m,
-                                             int g, int lane, float out_scale, float st16) {
+                                             int g, int lane, float sc, float st16) {
+  const bool f16out = st16 != 0.0f;
+  const float s = f16out ? st16 : 1.0f;
+  const float k = H ? sc * s : 1.0f;
+  float4 bb[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const float4 v = *reinterpret_cast<const float4*>(bias + nt * 16 + 4 * g);
+    bb[nt] = make_float4(v.x * s, v.y * s, v.z * s, v.w * s);
+  }
+  out = f16out ? static_cast<void*>(static_cast<_Float16*>(out) + 4 * g)
+               : static_cast<void*>(static_cast<float*>(out) + 4 * g);
   for (int base = 0; base < ntile; base += 4 * kBandWaves) {
     const int first = base + wave;
     const int mt = first >= ntile ? 0 : min(4, (ntile - first + kBandWaves - 1) / kBandWaves);
     switch (mt) {
       case 4:
-        band64_run<4, NT, H>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m,
-                             g, lane, out_scale, st16);
+        band64_run<4, NT, H>(lds, b, ty0, wf, bb, k, out, cout, pool, tiles_x, first, py, px, m,
+                             g, lane, f16out);
         break;
       case 3:
-        band64_run<3, NT, H>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m,
-                             g, lane, out_scale, st16);
+        band64_run<3, NT, H>(lds, b, ty0, wf, bb, k, out, cout, pool, tiles_x, first, py, px, m,
+                             g, lane, f16out);
         break;
       case 2:
-        band64_run<2, NT, H>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m,
-                             g, lane, out_scale, st16);
+        band64_run<2, NT, H>(lds, b, ty0, wf, bb, k, out, cout, pool, tiles_x, first, py, px, m,
+                             g, lane, f16out);
         break;
       case 1:
-        band64_run<1, NT, H>(lds, b, ty0, wf, bias, out, cout, pool, tiles_x, first, py, px, m,
-                             g, lane, out_scale, st16);
+        band64_run<1, NT, H>(lds, b, ty0, wf, bb, k, out, cout, pool, tiles_x, first, py, px, m,
+                             g, lane, f16out);
         break;
       default:
         break;
@@ -1279,9 +1293,15 @@ k_band64(ConvArgs a, Band64 b) {
   }
 }
 
+// Channel 3 of the pre-processed input is the constant 1 (bf16 bits 0x3F80 in
+// the upper half of the pixel's second word), also on the zero border: the
+// fp16 path's first-layer weights carry the bias there; elsewhere its
+// weights are 0.
+constexpr uint32_t kOneBf16Hi = 0x3F800000u;
+
 // The pre-processed bf16 input of one first-layer pixel: channels 0-2 of
 // (S / den) / 127.5 - 1 from the fy x fx cell sums of image pixel (y, x) of
-// frame idx[s], correctly rounded, and a zero channel 3.
+// frame idx[s], correctly rounded, and channel 3 = 1.
 __device__ __forceinline__ uint2 first_input_bf16(const ConvArgs& a, int64_t s, int y, int x) {
   const int32_t* S = a.sums + (int64_t)a.idx[s] * a.sums_h * a.sums_w * 3;
   int32_t acc[3] = {0, 0, 0};  // below 255 * den_c < 2^31 (checked on the host)
@@ -1301,11 +1321,12 @@ __device__ __forceinline__ uint2 first_input_bf16(const ConvArgs& a, int64_t s, 
     v[c] = f32div ? div_to_bf16_bits_fast((int32_t)num, (int32_t)a.den255, inv)
                   : f64_to_bf16_bits((double)num / (double)a.den255);
   }
-  return make_uint2((uint32_t)v[0] | ((uint32_t)v[1] << 16), (uint32_t)v[2]);
+  return make_uint2((uint32_t)v[0] | ((uint32_t)v[1] << 16), (uint32_t)v[2] | kOneBf16Hi);
 }
 
-// Pre-processed bf16 input of every survivor for k_pair64, zero-bordered:
-// xin[slot][xr][xw] pixels of 4 bf16, image pixel (y, x) at (y + 2, x + 1).
+// Pre-processed bf16 input of every survivor for k_pair64, zero-bordered
+// (channel 3 = 1 everywhere): xin[slot][xr][xw] pixels of 4 bf16, image pixel
+// (y, x) at (y + 2, x + 1).
 __global__ void __launch_bounds__(256) k_prep_input(ConvArgs a, uint2* xin, int32_t xr, int32_t xw) {
   int64_t cnt = *a.count;
   if (cnt > a.max_count) cnt = a.max_count;
@@ -1317,7 +1338,7 @@ __global__ void __launch_bounds__(256) k_prep_input(ConvArgs a, uint2* xin, int3
     const int q = (int)(i - s * per);
     const int row = q / xw, col = q - row * xw;
     const int y = row - 2, x = col - 1;
-    uint2 v = make_uint2(0u, 0u);
+    uint2 v = make_uint2(0u, kOneBf16Hi);
     if ((unsigned)y < (unsigned)a.h && (unsigned)x < (unsigned)a.w) v = first_input_bf16(a, s, y, x);
     xin[i] = v;
   }
@@ -1374,9 +1395,11 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     x[0] = make_uint4(p00.x, p00.y, p01.x, p01.y);
     x[1] = make_uint4(p10.x, p10.y, p11.x, p11.y);
   };
-  // first-layer tile t: 8 MFMAs, bias, ReLU, hi / lo split into the planes
+  // first-layer tile t: 8 MFMAs, then into the planes: on the fp16 path the
+  // ReLU of the (biased, scaled) result as fp16, else bias, ReLU and the hi /
+  // lo split
   const float* bias0 = a0.bias;  // the item's network (camera group)
-  float in_scale1 = 1.0f, out_scale1 = 1.0f, st16 = 0.0f;  // fp16 path: the second layer's scales
+  float out_scale1 = 1.0f, st16 = 0.0f;  // fp16 path: the second layer's scales
   auto l1_tile = [&](const bf16x8 (&w0)[2][4], int y0, int t, const uint4 (&x)[2]) {
     const int ti = t / tx0, tj = t - ti * tx0;
     const int r = 2 * ti + qy, col = 8 * tj + qx;
@@ -1392,6 +1415,22 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     if (col < b.w) {
       const bool inside = (unsigned)y < (unsigned)b.h;  // rows outside are zero
       const int addr = ((g >> 1) * b.cp + r * b.wb + col + 1) * 16 + (g & 1) * 8;
+      if constexpr (H) {
+        // the weights carry the bias and the second layer's input scale:
+        // fp16 of the ReLU (the conversion is monotonic and keeps 0)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+          const f16x2 z = {(_Float16)0.0f, (_Float16)0.0f};
+          const f16x2 p0 = __builtin_elementwise_max(
+              f16x2{(_Float16)acc[nt][0], (_Float16)acc[nt][1]}, z);
+          const f16x2 p1 = __builtin_elementwise_max(
+              f16x2{(_Float16)acc[nt][2], (_Float16)acc[nt][3]}, z);
+          *reinterpret_cast<uint2*>(lds + addr + 2 * nt * b.cp * 16) =
+              inside ? make_uint2(__builtin_bit_cast(uint32_t, p0), __builtin_bit_cast(uint32_t, p1))
+                     : make_uint2(0u, 0u);
+        }
+        return;
+      }
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) {
         const float4 bb = *reinterpret_cast<const float4*>(bias0 + nt * 16 + 4 * g);
@@ -1400,15 +1439,11 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
         const float v2 = inside ? fmaxf(acc[nt][2] + bb.z, 0.f) : 0.f;
         const float v3 = inside ? fmaxf(acc[nt][3] + bb.w, 0.f) : 0.f;
         const int ad = addr + 2 * nt * b.cp * 16;  // chunk 2 nt + g / 2
-        if constexpr (H) {
-          *reinterpret_cast<uint2*>(lds + ad) = f16x4_bits(v0, v1, v2, v3, in_scale1);
-        } else {
-          uint32_t h01, l01, h23, l23;
-          X::split2(v0, v1, h01, l01);
-          X::split2(v2, v3, h23, l23);
-          *reinterpret_cast<uint2*>(lds + ad) = make_uint2(h01, h23);
-          *reinterpret_cast<uint2*>(lds + b.lo_bytes + ad) = make_uint2(l01, l23);
-        }
+        uint32_t h01, l01, h23, l23;
+        X::split2(v0, v1, h01, l01);
+        X::split2(v2, v3, h23, l23);
+        *reinterpret_cast<uint2*>(lds + ad) = make_uint2(h01, h23);
+        *reinterpret_cast<uint2*>(lds + b.lo_bytes + ad) = make_uint2(l01, l23);
       }
     }
   };
@@ -1423,7 +1458,6 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     bias0 = at_off(a0.bias, off);
     if constexpr (H) {
       const float* sc = at_off(a1.scl, off);
-      in_scale1 = sc[0];
       out_scale1 = sc[1];
       if (a1.out_f16) st16 = sc[2];
     }
@@ -2291,7 +2325,7 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
     if (pair64_plan(cnn, &b, &bt, &lds, &xr, &xw)) {
       ConvArgs a0 = layer_args(0), a1 = layer_args(1);
       set_formats(a1, 1);
-      a0.wts = frag_weights(0, false);
+      a0.wts = cnn.h16 && cnn.conv_w0h ? cnn.conv_w0h : frag_weights(0, false);
       a1.wts = frag_weights(1, cnn.h16);
       a1.band_tiles = bt;
       uint2* xin = reinterpret_cast<uint2*>(static_cast<unsigned char*>(ws) +

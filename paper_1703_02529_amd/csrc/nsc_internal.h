@@ -219,6 +219,7 @@ struct Cnn {
   void* conv_wf;            // bf16 networks: the same in fragment order (else null)
   void* conv_wh;            // bf16 networks: the same as fp16, each layer times 2^wexp
   void* w1h;                // bf16 networks: dense weights as fp16 times 2^dense_wexp
+  void* conv_w0h;           // fp16 path: k_pair64's first layer, scaled, bias folded in (or null)
   int32_t dense_wexp, dense_aexp;  // as CnnLayer::wexp / aexp, for the dense layer
   bool h16;                 // bf16 network whose banded layers and dense layer take the
                             // fp16 path (activations as fp16, one MFMA per product)
