@@ -935,35 +935,47 @@ __device__ __forceinline__ int band_row(int pix, float inv_w) {
 // Stages band rows [0, rows_used), columns 1..w: image rows y0 + r inside the
 // image from one image's fp32 NHWC 64-channel activations, split into hi / lo
 // bf16 (H = false) or as fp16 times in_scale (H), zeros for rows outside.
-// Eight consecutive threads read one pixel's 256 bytes.
+// Eight consecutive threads read one pixel's 256 bytes.  Each thread issues
+// the loads of kStageBatch units before it stores any, so that their
+// latencies overlap.
+constexpr int kStageBatch = 8;
+
 template <bool H>
 __device__ __forceinline__ void stage_band64(const float* __restrict__ src, const Band64& b,
                                              unsigned char* lds, int y0, int rows_used,
                                              float in_scale) {
   const int units = rows_used * b.w * 8;
   const float inv_w = 1.0f / (float)b.w;
-  for (int u = threadIdx.x; u < units; u += blockDim.x) {
-    const int pix = u >> 3, c = u & 7;
-    const int r = band_row(pix, inv_w), x = pix - r * b.w;
-    const int y = y0 + r;
-    uint4 hi = make_uint4(0u, 0u, 0u, 0u), lo = hi;
-    if ((unsigned)y < (unsigned)b.h) {
-      const float* p = src + ((int64_t)y * b.w + x) * 64 + c * 8;
-      const float4 v0 = *reinterpret_cast<const float4*>(p);
-      const float4 v1 = *reinterpret_cast<const float4*>(p + 4);
-      if constexpr (H) {
-        hi = f16x8_bits(v0, v1, in_scale);
-      } else {
-        uint2 h0, l0, h1, l1;
-        Elt<uint16_t>::split4(v0, h0, l0);
-        Elt<uint16_t>::split4(v1, h1, l1);
-        hi = make_uint4(h0.x, h0.y, h1.x, h1.y);
-        lo = make_uint4(l0.x, l0.y, l1.x, l1.y);
+  for (int u0 = threadIdx.x; u0 < units; u0 += kStageBatch * blockDim.x) {
+    float4 v[kStageBatch][2];
+    int addr[kStageBatch];
+#pragma unroll
+    for (int j = 0; j < kStageBatch; ++j) {
+      const int u = u0 + j * blockDim.x;
+      const int pix = u >> 3, c = u & 7;
+      const int r = band_row(pix, inv_w), x = pix - r * b.w;
+      const int y = y0 + r;
+      addr[j] = u < units ? (c * b.cp + r * b.wb + x + 1) * 16 : -1;
+      v[j][0] = v[j][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (u < units && (unsigned)y < (unsigned)b.h) {
+        const float* p = src + ((int64_t)y * b.w + x) * 64 + c * 8;
+        v[j][0] = *reinterpret_cast<const float4*>(p);
+        v[j][1] = *reinterpret_cast<const float4*>(p + 4);
       }
     }
-    const int addr = (c * b.cp + r * b.wb + x + 1) * 16;
-    *reinterpret_cast<uint4*>(lds + addr) = hi;
-    if constexpr (!H) *reinterpret_cast<uint4*>(lds + b.lo_bytes + addr) = lo;
+#pragma unroll
+    for (int j = 0; j < kStageBatch; ++j) {
+      if (addr[j] < 0) continue;
+      if constexpr (H) {
+        *reinterpret_cast<uint4*>(lds + addr[j]) = f16x8_bits(v[j][0], v[j][1], in_scale);
+      } else {
+        uint2 h0, l0, h1, l1;
+        Elt<uint16_t>::split4(v[j][0], h0, l0);
+        Elt<uint16_t>::split4(v[j][1], h1, l1);
+        *reinterpret_cast<uint4*>(lds + addr[j]) = make_uint4(h0.x, h0.y, h1.x, h1.y);
+        *reinterpret_cast<uint4*>(lds + b.lo_bytes + addr[j]) = make_uint4(l0.x, l0.y, l1.x, l1.y);
+      }
+    }
   }
 }
 
@@ -973,14 +985,23 @@ __device__ __forceinline__ void stage_band64_f16(const _Float16* __restrict__ sr
                                                  unsigned char* lds, int y0, int rows_used) {
   const int units = rows_used * b.w * 8;
   const float inv_w = 1.0f / (float)b.w;
-  for (int u = threadIdx.x; u < units; u += blockDim.x) {
-    const int pix = u >> 3, c = u & 7;
-    const int r = band_row(pix, inv_w), x = pix - r * b.w;
-    const int y = y0 + r;
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if ((unsigned)y < (unsigned)b.h)
-      v = *reinterpret_cast<const uint4*>(src + ((int64_t)y * b.w + x) * 64 + c * 8);
-    *reinterpret_cast<uint4*>(lds + (c * b.cp + r * b.wb + x + 1) * 16) = v;
+  for (int u0 = threadIdx.x; u0 < units; u0 += kStageBatch * blockDim.x) {
+    uint4 v[kStageBatch];
+    int addr[kStageBatch];
+#pragma unroll
+    for (int j = 0; j < kStageBatch; ++j) {
+      const int u = u0 + j * blockDim.x;
+      const int pix = u >> 3, c = u & 7;
+      const int r = band_row(pix, inv_w), x = pix - r * b.w;
+      const int y = y0 + r;
+      addr[j] = u < units ? (c * b.cp + r * b.wb + x + 1) * 16 : -1;
+      v[j] = make_uint4(0u, 0u, 0u, 0u);
+      if (u < units && (unsigned)y < (unsigned)b.h)
+        v[j] = *reinterpret_cast<const uint4*>(src + ((int64_t)y * b.w + x) * 64 + c * 8);
+    }
+#pragma unroll
+    for (int j = 0; j < kStageBatch; ++j)
+      if (addr[j] >= 0) *reinterpret_cast<uint4*>(lds + addr[j]) = v[j];
   }
 }
 
