@@ -1370,8 +1370,10 @@ __global__ void __launch_bounds__(256) k_prep_input(ConvArgs a, uint2* xin, int3
 // (with the halo rows) from the pre-processed input (k_prep_input) straight
 // into the hi / lo planes, then the second layer runs from them.  First-layer
 // tiles are 2 rows x 8 columns; its K is (dy, dx of 4, c of 4) = 48 of 64.
-// A wave loads the input of its next first-layer tile while computing the
-// current one.
+// A wave issues the input loads of up to kPairL1Batch of its first-layer tiles
+// of a band before computing the first of them.
+
+constexpr int kPairL1Batch = 6;  // first-layer tiles per wave whose loads are issued together
 
 template <int NT, bool G, bool H>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -1485,8 +1487,15 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     const int y0 = 4 * ty0 - 1;
     const int t0n = (2 * nty + 1) * tx0;     // first-layer tiles: rows 4 nty + 2
     const int tfirst = prev_rows ? tx0 : 0;  // rows 0-1 copied after an image's first band
-    uint4 xc[2], xn[2];
-    if (tfirst + wave < t0n) l1_load(xs, y0, tfirst + wave, xc);
+    // this wave's first-layer tiles of the band (up to kPairL1Batch at once):
+    // all their input loads are issued before the first is used
+    uint4 xb[kPairL1Batch][2];
+    auto load_batch = [&](int tb) {
+#pragma unroll
+      for (int i = 0; i < kPairL1Batch; ++i)
+        if (tb + kBandWaves * i < t0n) l1_load(xs, y0, tb + kBandWaves * i, xb[i]);
+    };
+    load_batch(tfirst + wave);
     // first-layer weights for this band's first-layer phase only: an opaque
     // zero keeps the compiler from hoisting them out of the band loop (which
     // would hold 32 registers through the second layer)
@@ -1510,11 +1519,11 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
       }
       __syncthreads();  // copied before the first layer overwrites the source rows
     }
-    for (int t = tfirst + wave; t < t0n; t += kBandWaves) {
-      if (t + kBandWaves < t0n) l1_load(xs, y0, t + kBandWaves, xn);
-      l1_tile(w0, y0, t, xc);
-      xc[0] = xn[0];
-      xc[1] = xn[1];
+    for (int tb = tfirst + wave; tb < t0n; tb += kBandWaves * kPairL1Batch) {
+      if (tb != tfirst + wave) load_batch(tb);
+#pragma unroll
+      for (int i = 0; i < kPairL1Batch; ++i)
+        if (tb + kBandWaves * i < t0n) l1_tile(w0, y0, tb + kBandWaves * i, xb[i]);
     }
     __syncthreads();  // planes complete
     const int64_t out_e = s * (int64_t)ho * wo * a1.cout;
