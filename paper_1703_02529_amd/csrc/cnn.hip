@@ -1373,7 +1373,7 @@ __global__ void __launch_bounds__(256) k_prep_input(ConvArgs a, uint2* xin, int3
 // A wave issues the input loads of up to kPairL1Batch of its first-layer tiles
 // of a band before computing the first of them.
 
-constexpr int kPairL1Batch = 6;  // first-layer tiles per wave whose loads are issued together
+constexpr int kPairL1Batch = 7;  // first-layer tiles per wave whose loads are issued together
 
 template <int NT, bool G, bool H>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -2155,11 +2155,14 @@ int launch_pair(int nt0, int nt1, const ConvArgs& a0, const ConvArgs& a1, const 
 }
 }  // namespace
 
-// Band plan of a 64-input-channel bf16 layer (k_band64 / k_pair64): the
-// tallest band of at most 16 tiles (4 per wave) whose planes (one fp16 plane
-// with h16, else the bf16 hi and lo planes) fit 80 KB, so that two workgroups
-// share a CU, else one band row in up to 160 KB.  The fp16 scales are those
-// of the layer.  False when the layer does not qualify or no band fits.
+// Band plan of a 64-input-channel bf16 layer (k_band64 / k_pair64): among
+// the band heights of at most 16 tiles or two tile rows whose planes (one
+// fp16 plane with h16, else the bf16 hi and lo planes) fit 80 KB, so that two
+// workgroups share a CU, the one with
+// the least work per image for the busiest wave: per band the most tiles any
+// of the 4 waves computes, plus half a tile for the band's staging and
+// barriers; else one band row in up to 160 KB.  False when the layer does not
+// qualify or no band fits.
 bool band64_plan(const CnnLayer& L, bool h16, Band64* b, int32_t* band_tiles, size_t* lds) {
   if (L.cin != 64 || (L.cout != 64 && L.cout != 32)) return false;
   int32_t ty, tx;
@@ -2177,10 +2180,24 @@ bool band64_plan(const CnnLayer& L, bool h16, Band64* b, int32_t* band_tiles, si
     p.planes = h16 ? 1 : 2;
     return p;
   };
-  int32_t bt = 16 / tx;
-  if (bt > ty) bt = ty;
-  if (bt < 1) bt = 1;
-  while (bt > 1 && band64_bytes(plan(bt)) > 80 * 1024) --bt;
+  int32_t bt = 1;
+  double best = 1e30;
+  // at most 16 tiles (4 per wave) or two tile rows per band: taller bands
+  // measured slower (4 tile rows of a 25 x 25 map: 523 against 459 us per
+  // 8,192 images)
+  const int32_t cmax = 16 / tx > 2 ? 16 / tx : 2;
+  for (int32_t c = 1; c <= ty && c <= cmax; ++c) {
+    if (band64_bytes(plan(c)) > 80 * 1024) break;
+    double cost = 0.0;
+    for (int32_t y0 = 0; y0 < ty; y0 += c) {
+      const int32_t tiles = (y0 + c <= ty ? c : ty - y0) * tx;
+      cost += (tiles + kBandWaves - 1) / kBandWaves + 0.5;
+    }
+    if (cost < best) {
+      best = cost;
+      bt = c;
+    }
+  }
   if (band64_bytes(plan(bt)) > 160 * 1024) return false;
   *b = plan(bt);
   *band_tiles = bt;
