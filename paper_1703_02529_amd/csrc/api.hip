@@ -483,7 +483,27 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
             w0h[(((size_t)ks * nts + nt) * 64 + lane) * 8 + e] = v;
           }
   }
-  // device image: [conv_w][conv_wf][conv_wh][conv_b][w1][w1h][b1][w2][scales][w0h]
+  // fp16 path: the dense weights again in MFMA fragment order for
+  // k_dense_tiles, K steps of 32 padded with zeros to whole chunks of
+  // kDenseChunk steps: fragment (ks, nt), lane l = 16 g + m holds units
+  // 16 nt + m, features 32 ks + 8 g .. + 7, so that a chunk is one contiguous
+  // block of kDenseChunk x (D / 16) KB
+  std::vector<uint16_t> w1f;
+  if (c.bf16) {
+    const int nts = c.dense / 16;
+    const int nks = (c.flat + 31) / 32;
+    const int nkc = (nks + kDenseChunk - 1) / kDenseChunk * kDenseChunk;
+    w1f.assign((size_t)nkc * nts * 64 * 8, 0);
+    for (int ks = 0; ks < nks; ++ks)
+      for (int nt = 0; nt < nts; ++nt)
+        for (int lane = 0; lane < 64; ++lane)
+          for (int e = 0; e < 8; ++e) {
+            const int u = nt * 16 + (lane & 15), k = ks * 32 + (lane >> 4) * 8 + e;
+            if (k < c.flat)
+              w1f[(((size_t)ks * nts + nt) * 64 + lane) * 8 + e] = w1h[(size_t)u * c.flat + k];
+          }
+  }
+  // device image: [conv_w][conv_wf][conv_wh][conv_b][w1][w1h][b1][w2][scales][w0h][w1f]
   const size_t o_cw = 0;
   const size_t o_cwf = align_up(o_cw + conv_elems * es, kAlign);
   const size_t o_cwh = align_up(o_cwf + convwf.size() * es, kAlign);
@@ -494,7 +514,8 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
   const size_t o_w2 = align_up(o_b1 + (size_t)c.dense * 4, kAlign);
   const size_t o_sc = align_up(o_w2 + (size_t)c.dense * 4, kAlign);
   const size_t o_w0h = align_up(o_sc + scales.size() * 4, kAlign);
-  const size_t total = align_up(o_w0h + w0h.size() * 2, kAlign);
+  const size_t o_w1f = align_up(o_w0h + w0h.size() * 2, kAlign);
+  const size_t total = align_up(o_w1f + w1f.size() * 2, kAlign);
   std::vector<unsigned char> img(total, 0);
   auto put = [&](size_t off, const std::vector<float>& v, bool as_bf16) {
     if (as_bf16) {
@@ -516,6 +537,7 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
   put(o_w2, w2, false);
   put(o_sc, scales, false);
   if (!w0h.empty()) put(o_w0h, w0h, true);
+  if (!w1f.empty()) memcpy(img.data() + o_w1f, w1f.data(), w1f.size() * 2);
   void* dev = nullptr;
   if (hipMalloc(&dev, total) != hipSuccess)
     return fail(NSC_E_NOMEM, "hipMalloc of %zu bytes for CNN weights failed", total);
@@ -535,6 +557,7 @@ int nsc_cnn_create(const nsc_cnn_desc* desc, const float* hw, int64_t n_floats, 
   c.w2 = reinterpret_cast<float*>(b + o_w2);
   c.scales = reinterpret_cast<float*>(b + o_sc);
   c.conv_w0h = w0h.empty() ? nullptr : b + o_w0h;
+  c.w1f = w1f.empty() ? nullptr : b + o_w1f;
   nsc_cnn* h = new (std::nothrow) nsc_cnn;
   if (!h) {
     (void)hipFree(dev);

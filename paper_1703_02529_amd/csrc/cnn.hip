@@ -1583,6 +1583,7 @@ struct DenseArgs {
   double c_low, c_high;
   const float* scl;         // fp16 path: (input scale, output scale) in the weight image
   int32_t feat_f16;         // fp16 path: feat holds fp16 values already times the input scale
+  int32_t tiled;            // the partial blocks come from k_dense_tiles (its K parts)
   const CamNet* nets;       // camera group (else null)
   int64_t per_cam;
 };
@@ -1864,6 +1865,106 @@ __global__ void __launch_bounds__(64 * kDenseSplitWaves) k_dense_part(DenseArgs 
   }
 }
 
+// Tiled dense layer (fp16 path, single network): an item is a block of
+// kDenseTileRows survivors and a K part; its 4 waves take 32 survivors each
+// (two 16-row tiles) and walk the part's K range together in chunks of
+// kDenseChunk K steps, whose weight fragments the workgroup stages in LDS
+// (one contiguous block of the fragment-ordered copy), so that each weight is
+// read from memory once per 128 survivors.  The activation fragments of the
+// next K step are loaded while the current one computes.  Each item writes
+// one partial block per 16-row tile and NT; k_dense_finish adds the parts.
+constexpr int kDenseTileRows = 128;
+constexpr int kDenseTileItems = 512;  // K parts are chosen for about this many items
+
+__device__ __forceinline__ int dense_tile_kparts(int64_t cnt, int nks) {
+  const int64_t blocks = (cnt + kDenseTileRows - 1) / kDenseTileRows;
+  const int nch = (nks + kDenseChunk - 1) / kDenseChunk;
+  int64_t k = kDenseTileItems / (blocks > 0 ? blocks : 1);
+  if (k > nch) k = nch;
+  return k < 1 ? 1 : (int)k;
+}
+
+template <int NT>
+__global__ void __launch_bounds__(256) k_dense_tiles(DenseArgs a, f32x4* __restrict__ part) {
+  constexpr int MT = 2;
+  __shared__ __align__(16) f16x8 wl[kDenseChunk][NT][64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int m = lane & 15, g = lane >> 4;
+  int64_t cnt = *a.count;
+  if (cnt > a.max_count) cnt = a.max_count;
+  const int nks = (a.flat + 31) / 32;
+  const int nch = (nks + kDenseChunk - 1) / kDenseChunk;
+  const int kparts = dense_tile_kparts(cnt, nks);
+  const int64_t blocks = (cnt + kDenseTileRows - 1) / kDenseTileRows;
+  const int64_t items = blocks * kparts;
+  const float in_scale = a.scl[0];
+  const f16x8* wsrc = reinterpret_cast<const f16x8*>(a.w1);
+  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+    const int64_t blk = item / kparts;
+    const int kp = (int)(item - blk * kparts);
+    const int c0 = (int)((int64_t)kp * nch / kparts), c1 = (int)((int64_t)(kp + 1) * nch / kparts);
+    const int64_t tile0 = blk * (kDenseTileRows / 16) + wave * MT;  // this wave's 16-row tiles
+    bool valid[MT];
+    int64_t row[MT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const int64_t s = (tile0 + i) * 16 + m;
+      valid[i] = s < cnt;
+      row[i] = (valid[i] ? s : 0) * (int64_t)a.flat + g * 8;
+    }
+    // the activation fragment of K step ks for tile i (zero past the end)
+    auto ldx = [&](int ks, f16x8 (&x)[MT]) {
+      const int k0 = ks * 32;
+      const bool kin = k0 + g * 8 < a.flat;
+#pragma unroll
+      for (int i = 0; i < MT; ++i) {
+        x[i] = Elt<_Float16>::zero();
+        if (valid[i] && kin)
+          x[i] = a.feat_f16 ? *reinterpret_cast<const f16x8*>(
+                                  reinterpret_cast<const _Float16*>(a.feat) + row[i] + k0)
+                            : Elt<_Float16>::cvt8(a.feat + row[i] + k0, in_scale);
+      }
+    };
+    f32x4 acc[MT][NT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    f16x8 xc[MT], xn[MT];
+    ldx(c0 * kDenseChunk, xc);
+#pragma unroll
+    for (int i = 0; i < MT; ++i) xn[i] = xc[i];
+    for (int c = c0; c < c1; ++c) {
+      __syncthreads();  // the previous chunk's fragments are read
+      {
+        const f16x8* src = wsrc + (size_t)c * kDenseChunk * NT * 64;
+        f16x8* dst = &wl[0][0][0];
+        for (int i = threadIdx.x; i < kDenseChunk * NT * 64; i += 256) dst[i] = src[i];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < kDenseChunk; ++j) {
+        const int ks = c * kDenseChunk + j;
+        if (ks + 1 < c1 * kDenseChunk) ldx(ks + 1, xn);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const f16x8 w = wl[j][nt][lane];
+#pragma unroll
+          for (int i = 0; i < MT; ++i) acc[i][nt] = mma_f16(xc[i], w, acc[i][nt]);
+        }
+#pragma unroll
+        for (int i = 0; i < MT; ++i) xc[i] = xn[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        part[(((tile0 + i) * kparts + kp) * NT + nt) * 64 + lane] = acc[i][nt];
+  }
+}
+
 // k_dense_finish: a workgroup per 16-survivor tile; its kDenseFinWaves waves
 // add interleaved subsets of the tile's K parts (wave w: parts w, w + 4, ...),
 // wave 0 adds the waves' sums in wave order and applies dense_out.
@@ -1880,7 +1981,8 @@ __global__ void __launch_bounds__(64 * kDenseFinWaves) k_dense_finish(DenseArgs 
   int64_t cnt = *a.count;
   if (cnt > a.max_count) cnt = a.max_count;
   const int64_t tiles = (cnt + 15) / 16;
-  const int kparts = dense_kparts(tiles, (a.flat + KS - 1) / KS);
+  const int kparts = a.tiled ? dense_tile_kparts(cnt, (a.flat + 31) / 32)
+                             : dense_kparts(tiles, (a.flat + KS - 1) / KS);
   for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
     f32x4 t[NT];
 #pragma unroll
@@ -1995,6 +2097,28 @@ int launch_dense_split_nt(int nt, const DenseArgs& a, f32x4* part, unsigned grid
 #undef NSC_SPLIT_CASE
 #undef NSC_SPLIT_LAUNCH
   NSC_CHECK_LAUNCH("k_dense_part / k_dense_finish");
+  return NSC_OK;
+}
+
+int launch_dense_tiles_nt(int nt, const DenseArgs& a, f32x4* part, unsigned grid,
+                          unsigned grid_fin, hipStream_t st) {
+#define NSC_TILES_CASE(N)                                                                       \
+  case N:                                                                                       \
+    hipLaunchKernelGGL((k_dense_tiles<N>), dim3(grid), dim3(256), 0, st, a, part);             \
+    hipLaunchKernelGGL((k_dense_finish<_Float16, N, false>), dim3(grid_fin),                   \
+                       dim3(64 * kDenseFinWaves), 0, st, a, (const f32x4*)part);                \
+    break;
+  switch (nt) {
+    NSC_TILES_CASE(1)
+    NSC_TILES_CASE(2)
+    NSC_TILES_CASE(4)
+    NSC_TILES_CASE(8)
+    NSC_TILES_CASE(16)
+    default:
+      return fail(NSC_E_SHAPE, "dense layer of %d units is not supported", nt * 16);
+  }
+#undef NSC_TILES_CASE
+  NSC_CHECK_LAUNCH("k_dense_tiles / k_dense_finish");
   return NSC_OK;
 }
 
@@ -2274,11 +2398,21 @@ size_t cnn_xin_bytes(const Cnn& cnn, int64_t max_count) {
   return align_up((size_t)xr * xw * 8 * (size_t)(max_count > 0 ? max_count : 0), 256);
 }
 
-// The dense layer's partial blocks when it splits K over workgroups (fewer
-// than kDenseBig survivors): one NT x 1 KB block per (tile, K part) item.
+// The dense layer's partial blocks when it splits K over workgroups: one
+// NT x 1 KB block per (16-row tile, K part), for k_dense_tiles (fp16 path
+// without a camera group: its 128-row blocks times their K parts, at most the
+// larger of kDenseTileItems x 8 and the tiles of max_count) or k_dense_part
+// (fewer than kDenseBig survivors otherwise); room for both.
 size_t cnn_dense_part_bytes(const Cnn& cnn, int64_t max_count) {
-  if (max_count <= 0 || max_count >= kDenseBig) return 0;
-  return (size_t)kDenseSplitItems * (size_t)(cnn.dense / 16) * 64 * sizeof(f32x4);
+  if (max_count <= 0) return 0;
+  const size_t blk = (size_t)(cnn.dense / 16) * 64 * sizeof(f32x4);
+  size_t n = max_count < kDenseBig ? (size_t)kDenseSplitItems * blk : 0;
+  if (cnn.h16 && cnn.w1f) {
+    const int64_t t8 = (max_count + kDenseTileRows - 1) / kDenseTileRows * 8;
+    const int64_t blocks = t8 > (int64_t)kDenseTileItems * 8 ? t8 : (int64_t)kDenseTileItems * 8;
+    if ((size_t)blocks * blk > n) n = (size_t)blocks * blk;
+  }
+  return n;
 }
 
 size_t cnn_workspace_bytes(const Cnn& cnn, int64_t max_count) {
@@ -2462,10 +2596,19 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
   d.nets = r.nets;
   d.per_cam = r.per_cam;
   const int nt = cnn.dense / 16;
+  f32x4* part = reinterpret_cast<f32x4*>(static_cast<unsigned char*>(ws) +
+                                         2 * per * (size_t)r.max_count + 256 +
+                                         cnn_xin_bytes(cnn, r.max_count));
+  if (cnn.h16 && cnn.w1f && !r.nets) {
+    d.w1 = cnn.w1f;
+    d.tiled = 1;
+    const int64_t grid = kDenseTileItems;  // the kernel loops over its items
+    int64_t grid_fin = (r.max_count + 15) / 16;
+    if (grid_fin > kNumCU * 4) grid_fin = kNumCU * 4;
+    if (grid_fin < 1) grid_fin = 1;
+    return launch_dense_tiles_nt(nt, d, part, (unsigned)grid, (unsigned)grid_fin, stream);
+  }
   if (r.max_count < kDenseBig) {
-    f32x4* part = reinterpret_cast<f32x4*>(static_cast<unsigned char*>(ws) +
-                                           2 * per * (size_t)r.max_count + 256 +
-                                           cnn_xin_bytes(cnn, r.max_count));
     // items: up to kDenseSplitItems; finishing: a wave per 16-survivor tile
     const int64_t tiles = (r.max_count + 15) / 16;
     int64_t grid_part = kDenseSplitItems;

@@ -188,6 +188,9 @@ int launch_skip_expand(const SkipExpand& e, hipStream_t stream);
 int launch_copy_u8(const uint8_t* src, uint8_t* dst, int64_t n, hipStream_t stream);
 
 // Specialized CNN.
+// K steps (of 32 features) per weight chunk of the tiled dense kernel.
+constexpr int kDenseChunk = 4;
+
 struct CnnLayer {
   int32_t cin, cout, h, w;  // input channels, output channels, input grid
   bool pool;
@@ -220,6 +223,7 @@ struct Cnn {
   void* conv_wh;            // bf16 networks: the same as fp16, each layer times 2^wexp
   void* w1h;                // bf16 networks: dense weights as fp16 times 2^dense_wexp
   void* conv_w0h;           // fp16 path: k_pair64's first layer, scaled, bias folded in (or null)
+  void* w1f;                // fp16 path: w1h in fragment order, padded to whole chunks
   int32_t dense_wexp, dense_aexp;  // as CnnLayer::wexp / aexp, for the dense layer
   bool h16;                 // bf16 network whose banded layers and dense layer take the
                             // fp16 path (activations as fp16, one MFMA per product)
