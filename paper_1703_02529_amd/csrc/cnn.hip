@@ -297,12 +297,20 @@ __device__ __forceinline__ void load_bias(const float* bias, int m, float (&b)[N
   for (int nt = 0; nt < NT; ++nt) b[nt] = bias[nt * 16 + m];
 }
 
-// Bias, ReLU, optional 2x2 max-pool and fp32 NHWC store of one 4x4 tile.
-// Lane (m, g) holds rows 4g..4g+3 (one pooling window) of output channel m.
+// Bias, ReLU, optional 2x2 max-pool and NHWC store of one 4x4 tile: fp32,
+// or with st16 != 0 fp16 values times st16 (the next layer's input scale on
+// the fp16 path).  Lane (m, g) holds rows 4g..4g+3 (one pooling window) of
+// output channel m.
 template <int NT>
 __device__ __forceinline__ void conv_epilogue(const ConvArgs& a, const f32x4 (&acc)[NT],
-                                              const float (&bias)[NT], float* out, int ty, int tx,
-                                              int ho, int wo, int m, int g) {
+                                              const float (&bias)[NT], void* out, int ty, int tx,
+                                              int ho, int wo, int m, int g, float st16 = 0.0f) {
+  auto store = [&](int64_t e, float v) {
+    if (st16 != 0.0f)
+      static_cast<_Float16*>(out)[e] = (_Float16)(v * st16);
+    else
+      static_cast<float*>(out)[e] = v;
+  };
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const int n = nt * 16 + m;
@@ -313,13 +321,12 @@ __device__ __forceinline__ void conv_epilogue(const ConvArgs& a, const f32x4 (&a
 #pragma unroll
       for (int r = 0; r < 4; ++r) v = fmaxf(v, acc[nt][r] + b);
       const int oy = 2 * ty + wy, ox = 2 * tx + wx;
-      if (oy < ho && ox < wo) out[((int64_t)oy * wo + ox) * a.cout + n] = v;
+      if (oy < ho && ox < wo) store(((int64_t)oy * wo + ox) * a.cout + n, v);
     } else {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int oy = 4 * ty + 2 * wy + (r >> 1), ox = 4 * tx + 2 * wx + (r & 1);
-        if (oy < ho && ox < wo)
-          out[((int64_t)oy * wo + ox) * a.cout + n] = fmaxf(acc[nt][r] + b, 0.0f);
+        if (oy < ho && ox < wo) store(((int64_t)oy * wo + ox) * a.cout + n, fmaxf(acc[nt][r] + b, 0.0f));
       }
     }
   }
@@ -484,12 +491,17 @@ __global__ void __launch_bounds__(256) k_conv_first(ConvArgs a) {
     }
     stage_first(a, in, s, 4 * ty0 - 1, 4 * tx0 - 1, 4 * nty + 2, a.band_w, 0, (int)blockDim.x);
     __syncthreads();
-    float* out = a.act_out + s * (int64_t)ho * wo * a.cout;
+    // fp16 output (the next layer on the fp16 path): times its input scale
+    const float st16 = a.out_f16 ? at_off(a.scl, G ? slot_woff(a.nets, a.per_cam, a.idx, s) : 0)[2]
+                                 : 0.0f;
+    const int64_t out_e = s * (int64_t)ho * wo * a.cout;
+    void* out = a.out_f16 ? static_cast<void*>(reinterpret_cast<_Float16*>(a.act_out) + out_e)
+                          : static_cast<void*>(a.act_out + out_e);
     for (int t = wave; t < nty * ntx; t += nwaves) {
       const int tyl = t / ntx, txl = t - tyl * ntx;
       f32x4 acc[NT];
       first_tile<T, NT>(in, wl, a.w_lds, a.band_w, 4 * tyl + py, 4 * txl + px, m, g, acc);
-      conv_epilogue<NT>(a, acc, bias, out, ty0 + tyl, tx0 + txl, ho, wo, m, g);
+      conv_epilogue<NT>(a, acc, bias, out, ty0 + tyl, tx0 + txl, ho, wo, m, g, st16);
     }
   }
 }
@@ -2493,6 +2505,9 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
     }
     for (int l = 0; l < cnn.n_layers; ++l)
       out16[l] = band[l] && (l + 1 < cnn.n_layers ? band[l + 1] : cnn.h16);
+    // a first layer run alone (k_conv_first) writes fp16 for a banded fp16
+    // second layer
+    if (!p64 && !pair && cnn.n_layers > 1) out16[0] = band[1];
   }
   auto set_formats = [&](ConvArgs& a, int l) {
     a.in_f16 = l > 0 && out16[l - 1];
