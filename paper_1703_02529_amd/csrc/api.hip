@@ -274,8 +274,25 @@ RunLayout run_layout(const nsc_cascade_cfg* c0, const Cnn& cnn, int64_t n_frames
     L.sk_logit = take((size_t)n * 4);
   }
   L.cnn = take(cnn_workspace_bytes(cnn, n));
-  // fixed-reference detector fused into the area kernel: per-unit partial
-  // sums, bounded by the plan's units at one output row per band
+  // detector fused into the area kernel: per-unit partial sums, bounded by
+  // the plan's units at one output row per band (fixed reference), or by the
+  // fused earlier-frame plan's count
+  if (c->ref_mode == NSC_REF_PREV && c->metric == NSC_METRIC_MSE) {
+    AreaPlan ap;
+    DiffArgs a{};
+    a.ref_mode = c->ref_mode;
+    a.metric = c->metric;
+    a.delta = c->delta;
+    a.grid_h = c->grid_h;
+    a.grid_w = c->grid_w;
+    PrevFusePlan fp;
+    if (make_area_plan(c->in_h, c->in_w, c->frame_stride, reinterpret_cast<const void*>(kAlign),
+                       c->dd_h, c->dd_w, n > 0 ? n : 1, &ap) == NSC_OK &&
+        area_prev_plan(ap, a, n, &fp)) {
+      L.part_units = fp.part_elems;
+      L.part = take((size_t)L.part_units * sizeof(int64_t));
+    }
+  }
   if (c->ref_mode == NSC_REF_FIXED && c->grid_h * c->grid_w == 1) {
     AreaPlan ap;
     if (make_area_plan(c->in_h, c->in_w, c->frame_stride, reinterpret_cast<const void*>(kAlign),
@@ -780,7 +797,15 @@ int run_checked(const nsc_cascade_cfg* cfg, const Cnn& c, const uint8_t* frames,
     int64_t* part = reinterpret_cast<int64_t*>(w + L.part);
     const bool fused = area_detect_fused(ap, a) && L.part_units > 0 &&
                        area_detect_part_count(ap, n) <= L.part_units;
-    if (fused) {
+    PrevFusePlan fp;
+    const bool fused_prev = !fused && L.part_units > 0 && area_prev_plan(ap, a, n, &fp) &&
+                            fp.part_elems <= L.part_units;
+    if (fused_prev) {
+      if (int rc = launch_area_prev(fp, frames, cfg->frame_stride, n, sums, a, part, st)) return rc;
+      if (int rc = mark(1)) return rc;
+      area_prev_diff_args(fp, part, &a);
+      if (int rc = launch_diff(a, st)) return rc;
+    } else if (fused) {
       if (int rc = launch_area_detect_fixed(ap, frames, cfg->frame_stride, n, sums, a, part, st))
         return rc;
       if (int rc = mark(1)) return rc;

@@ -238,6 +238,75 @@ __global__ void __launch_bounds__(1024) k_area_sums_rows(const uint8_t* __restri
   }
 }
 
+// Area sums of one wave's strip (lanes' chunks of CB bytes starting at col)
+// for output rows Y0..Y1-1: per output row, the vertical pass into the wave's
+// LDS column sums buf, then the horizontal pass; value t of band row r
+// (cell (t / 3) of the strip, channel t mod 3) with sum s is handed to
+// cell(t, r, s).  Lane l handles the values t = l, l + 64, ... of every row.
+// With MAXS > 0 (at most 64 MAXS values per row) the loop over a lane's
+// values is unrolled and cell(k, t, r, s) also gets the slot k (t = l + 64 k).
+template <int CB, bool PACKED, int RB, int MAXS = 0, class Cell, class Buf>
+__device__ __forceinline__ void strip_band_sums(const uint8_t* __restrict__ col, int64_t row_bytes,
+                                                const Axis& ay, int qx, int Y0, int Y1, int lane,
+                                                bool active, Buf* buf, const int4* xtab,
+                                                int ncells, Cell&& cell) {
+  using cell_t = Buf;
+  for (int Y = Y0; Y < Y1; ++Y) {
+    // uniform row bounds (divisions run on the vector unit; move them to scalars)
+    const int a0 = Y * ay.p, a1 = a0 + ay.p;
+    const int j0 = __builtin_amdgcn_readfirstlane(a0 / ay.q);
+    const int j1 = __builtin_amdgcn_readfirstlane((a1 + ay.q - 1) / ay.q);
+    int32_t v[CB];
+    vertical_sums<CB, PACKED, RB>(col, row_bytes, a0, a1, ay.q, j0, j1, v);
+    if (active) {
+      if constexpr (PACKED && CB % 8 == 0) {  // 2 CB bytes per lane as 16-byte stores
+        uint4* d = reinterpret_cast<uint4*>(buf + lane * CB);
+#pragma unroll
+        for (int q = 0; q < CB / 8; ++q)
+          d[q] = make_uint4(v[8 * q] | (v[8 * q + 1] << 16), v[8 * q + 2] | (v[8 * q + 3] << 16),
+                            v[8 * q + 4] | (v[8 * q + 5] << 16), v[8 * q + 6] | (v[8 * q + 7] << 16));
+      } else {
+#pragma unroll
+        for (int b = 0; b < CB; ++b) buf[lane * CB + b] = (cell_t)v[b];
+      }
+    }
+    __syncwarp();
+    auto horizontal = [&](int t) -> int32_t {
+      const int x = t / 3, c = t - 3 * x;
+      const int4 e = xtab[x];
+      const cell_t* bp = buf + 3 * e.x + c;
+      int32_t mid = 0;
+      int i = 1;
+      for (; i + 8 <= e.y; i += 8) {
+        int32_t m8 = 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) m8 += (int32_t)bp[3 * (i + u)];
+        mid += m8;
+      }
+      for (; i < e.y; ++i) mid += (int32_t)bp[3 * i];
+      int32_t s;
+      if constexpr (PACKED) {  // all factors below 2^24
+        s = (int32_t)(__umul24((uint32_t)e.z, bp[0]) + __umul24((uint32_t)qx, (uint32_t)mid));
+        if (e.y > 0) s += (int32_t)__umul24((uint32_t)e.w, bp[3 * e.y]);
+      } else {
+        s = e.z * (int32_t)bp[0] + qx * mid;
+        if (e.y > 0) s += e.w * (int32_t)bp[3 * e.y];
+      }
+      return s;
+    };
+    if constexpr (MAXS > 0) {
+#pragma unroll
+      for (int k = 0; k < MAXS; ++k) {
+        const int t = lane + 64 * k;
+        if (t < ncells) cell(k, t, Y - Y0, horizontal(t));
+      }
+    } else {
+      for (int t = lane; t < ncells; t += 64) cell(t, Y - Y0, horizontal(t));
+    }
+    __syncwarp();  // reads of this row's strip precede the next row's writes
+  }
+}
+
 // Wave-autonomous kernel: no workgroup barriers, and no global stores until
 // the end of a wave's work.  The horizontal resampling pattern repeats every
 // p_x source pixels (q_x output columns); a "group" is the smallest whole
@@ -308,52 +377,8 @@ __global__ void __launch_bounds__(256) k_area_sums_wave(const uint8_t* __restric
   const int64_t row_bytes = (int64_t)ax.n_in * 3;
   const uint8_t* col =
       frames + f * stride + ((int64_t)group0 * g.group_lanes + (active ? lane : 0)) * CB;
-  for (int Y = Y0; Y < Y1; ++Y) {
-    // uniform row bounds (divisions run on the vector unit; move them to scalars)
-    const int a0 = Y * ay.p, a1 = a0 + ay.p;
-    const int j0 = __builtin_amdgcn_readfirstlane(a0 / ay.q);
-    const int j1 = __builtin_amdgcn_readfirstlane((a1 + ay.q - 1) / ay.q);
-    int32_t v[CB];
-    vertical_sums<CB, PACKED, RB>(col, row_bytes, a0, a1, ay.q, j0, j1, v);
-    if (active) {
-      if constexpr (PACKED && CB % 8 == 0) {  // 2 CB bytes per lane as 16-byte stores
-        uint4* d = reinterpret_cast<uint4*>(buf + lane * CB);
-#pragma unroll
-        for (int q = 0; q < CB / 8; ++q)
-          d[q] = make_uint4(v[8 * q] | (v[8 * q + 1] << 16), v[8 * q + 2] | (v[8 * q + 3] << 16),
-                            v[8 * q + 4] | (v[8 * q + 5] << 16), v[8 * q + 6] | (v[8 * q + 7] << 16));
-      } else {
-#pragma unroll
-        for (int b = 0; b < CB; ++b) buf[lane * CB + b] = (cell_t)v[b];
-      }
-    }
-    __syncwarp();
-    int32_t* srow = sbuf + (Y - Y0) * ncells;
-    for (int t = lane; t < ncells; t += 64) {
-      const int x = t / 3, c = t - 3 * x;
-      const int4 e = xtab[x];
-      const cell_t* bp = buf + 3 * e.x + c;
-      int32_t mid = 0;
-      int i = 1;
-      for (; i + 8 <= e.y; i += 8) {
-        int32_t m8 = 0;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) m8 += (int32_t)bp[3 * (i + u)];
-        mid += m8;
-      }
-      for (; i < e.y; ++i) mid += (int32_t)bp[3 * i];
-      int32_t s;
-      if constexpr (PACKED) {  // all factors below 2^24
-        s = (int32_t)(__umul24((uint32_t)e.z, bp[0]) + __umul24((uint32_t)qx, (uint32_t)mid));
-        if (e.y > 0) s += (int32_t)__umul24((uint32_t)e.w, bp[3 * e.y]);
-      } else {
-        s = e.z * (int32_t)bp[0] + qx * mid;
-        if (e.y > 0) s += e.w * (int32_t)bp[3 * e.y];
-      }
-      srow[t] = s;
-    }
-    __syncwarp();  // reads of this row's strip precede the next row's writes
-  }
+  strip_band_sums<CB, PACKED, RB>(col, row_bytes, ay, qx, Y0, Y1, lane, active, buf, xtab, ncells,
+                                  [&](int t, int r, int32_t s) { sbuf[r * ncells + t] = s; });
   // the band's sums, one output row segment after another
   int32_t* out = sums + (f * (int64_t)Ho * Wo + X0) * 3;
   DiffSums<FM < 0 ? NSC_METRIC_MSE : FM> acc;
@@ -373,6 +398,118 @@ __global__ void __launch_bounds__(256) k_area_sums_wave(const uint8_t* __restric
       pp[0] = acc.e;
       pp[1] = acc.s;
       pp[2] = acc.r;
+    }
+  }
+}
+
+// The earlier-frame MSE detector fused into the area kernel by temporal
+// tiling along the reuse distance delta: a wave owns one (band, strip) of the
+// R frames f_i = r + delta (sg R + i), i = 0 .. R-1, of chain (sg, r), so
+// that while it forms the sums of f_i its LDS block still holds those of
+// f_(i-1) = f_i - delta, and each value's squared difference is added as the
+// new value replaces the old one.  For every chain frame after the first the
+// wave writes its partial sums of squared differences (exact int64): one
+// (global score) or one per block column its strip touches (BLK: bands are
+// the block rows), at part[(f * bands + band) * strips + strip] or
+// part[((f * bands + band) * grid_w + bx) * strips + strip].  The first frame
+// of a chain, whose frame f - delta is another wave's (or in the state), is
+// scored from the sums by k_diff afterwards, which also adds up the partials
+// of the other frames.  Sums stores and the LDS layout are those of
+// k_area_sums_wave.
+constexpr int kPrevSlots = 4;  // values per lane and row (at most 256 per strip row)
+
+template <int CB, bool PACKED, int RB, bool BLK>
+__global__ void __launch_bounds__(256) k_area_prev_wave(const uint8_t* __restrict__ frames,
+                                                        int64_t stride, Axis ay, Axis ax,
+                                                        WaveGeom g, int64_t n, int32_t delta,
+                                                        int32_t R, int32_t grid_w,
+                                                        int32_t* __restrict__ sums,
+                                                        int64_t* __restrict__ part) {
+  using cell_t = typename std::conditional<PACKED, uint16_t, int32_t>::type;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int Ho = ay.n_out, Wo = ax.n_out;
+  const int qx = ax.q;
+  const int scols = g.groups_per_wave * g.group_cols;
+  int4* xtab = reinterpret_cast<int4*>(smem);
+  for (int x = threadIdx.x; x < scols; x += blockDim.x) {
+    const int b0 = x * ax.p, b1 = b0 + ax.p;
+    const int i0 = b0 / qx, il = (b1 - 1) / qx;
+    xtab[x] = make_int4(i0, il - i0, il == i0 ? ax.p : (i0 + 1) * qx - b0, b1 - il * qx);
+  }
+  __syncthreads();  // the only workgroup barrier
+  const size_t per_wave =
+      ((size_t)64 * CB * sizeof(cell_t) + (size_t)g.band_rows * scols * 3 * 4 + 15) & ~(size_t)15;
+  unsigned char* wbase = smem + (size_t)scols * 16 + (size_t)wv * per_wave;
+  cell_t* buf = reinterpret_cast<cell_t*>(wbase);
+  int32_t* sbuf = reinterpret_cast<int32_t*>(wbase + (size_t)64 * CB * sizeof(cell_t));
+
+  const int bands = g.bands, strips = g.waves_per_frame;
+  const int64_t unit = xcd_block(blockIdx.x, gridDim.x) * (blockDim.x >> 6) + wv;
+  const int64_t per_chain = (int64_t)bands * strips;
+  const int64_t chain = unit / per_chain;
+  const int rem = (int)(unit - chain * per_chain);
+  const int band = rem / strips, strip = rem - band * strips;
+  const int64_t sg = chain / delta;
+  const int r = (int)(chain - sg * delta);
+  if (sg * R * delta + r >= n) return;  // no frames (uniform)
+  const int group0 = strip * g.groups_per_wave;
+  const int ngroups = min(g.groups_per_wave, g.groups_per_row - group0);
+  const bool active = lane < ngroups * g.group_lanes;
+  const int ncols = ngroups * g.group_cols;
+  const int ncells = ncols * 3;
+  const int X0 = group0 * g.group_cols;
+  const int Y0 = (int)((int64_t)band * Ho / bands);
+  const int Y1 = (int)((int64_t)(band + 1) * Ho / bands);
+  const int64_t row_bytes = (int64_t)ax.n_in * 3;
+  // block column of each of this lane's value slots, and the strip's range
+  int bxs[kPrevSlots];
+#pragma unroll
+  for (int k = 0; k < kPrevSlots; ++k)
+    bxs[k] = BLK ? ((X0 + (lane + 64 * k) / 3 + 1) * grid_w - 1) / Wo : 0;
+  const int bx_lo = BLK ? ((X0 + 1) * grid_w - 1) / Wo : 0;
+  const int bx_hi = BLK ? ((X0 + ncols) * grid_w - 1) / Wo : 0;
+  for (int i = 0; i < R; ++i) {
+    const int64_t f = (sg * R + i) * delta + r;
+    if (f >= n) break;
+    const uint8_t* col =
+        frames + f * stride + ((int64_t)group0 * g.group_lanes + (active ? lane : 0)) * CB;
+    int64_t e[kPrevSlots];
+#pragma unroll
+    for (int k = 0; k < kPrevSlots; ++k) e[k] = 0;
+    const bool diff = i > 0;
+    strip_band_sums<CB, PACKED, RB, kPrevSlots>(
+        col, row_bytes, ay, qx, Y0, Y1, lane, active, buf, xtab, ncells,
+        [&](int k, int t, int rr, int32_t s) {
+          int32_t* q = sbuf + rr * ncells + t;
+          if (diff) {
+            const int64_t d = (int64_t)s - *q;
+            e[k] += d * d;
+          }
+          *q = s;
+        });
+    int32_t* out = sums + (f * (int64_t)Ho * Wo + X0) * 3;
+    for (int Y = Y0; Y < Y1; ++Y) {
+      const int32_t* srow = sbuf + (Y - Y0) * ncells;
+      int32_t* orow = out + (int64_t)Y * Wo * 3;
+      for (int t = lane; t < ncells; t += 64) orow[t] = srow[t];
+    }
+    if (!diff) continue;
+    if constexpr (!BLK) {
+      int64_t v = 0;
+#pragma unroll
+      for (int k = 0; k < kPrevSlots; ++k) v += e[k];
+      v = wave_sum_i64(v);
+      if (lane == 0) part[(f * bands + band) * strips + strip] = v;
+    } else {
+      for (int bc = bx_lo; bc <= bx_hi; ++bc) {
+        int64_t v = 0;
+#pragma unroll
+        for (int k = 0; k < kPrevSlots; ++k) v += bxs[k] == bc ? e[k] : 0;
+        v = wave_sum_i64(v);
+        if (lane == 0) part[((f * bands + band) * grid_w + bc) * strips + strip] = v;
+      }
     }
   }
 }
@@ -530,6 +667,47 @@ __device__ __forceinline__ double frame_score(const int32_t* cur, const int32_t*
   return z;
 }
 
+// The MSE score of frame i from the fused kernel's partial sums (exact
+// integers, so their grouping does not matter): the global score, or the
+// logistic score of the per-block MSEs in block order, each as frame_score
+// computes it from the sums.
+template <bool BLK>
+__device__ __forceinline__ double part_score(const DiffArgs& a, int64_t i, int lane) {
+#pragma clang fp contract(off)
+  const int bands = a.part_bands, strips = a.part_strips;
+  if (!BLK || a.grid_h * a.grid_w == 1) {
+    const int64_t* p = a.part + i * bands * strips;
+    int64_t e = 0;
+    for (int u = lane; u < bands * strips; u += 64) e += p[u];
+    DiffSums<NSC_METRIC_MSE> acc;
+    acc.e = wave_sum_i64(e);
+    return acc.value(a, (double)((int64_t)a.dd_h * a.dd_w * 3));
+  }
+  if constexpr (!BLK) return 0.0;
+  const int gw = a.grid_w;
+  double z = a.lr_b;
+  for (int by = 0; by < a.grid_h; ++by) {
+    double m = 0.0;
+    if (lane < gw) {
+      const int x0 = (int)((int64_t)lane * a.dd_w / gw);
+      const int x1 = (int)((int64_t)(lane + 1) * a.dd_w / gw);
+      const int64_t* p = a.part + ((i * bands + by) * gw + lane) * strips;
+      int64_t e = 0;
+      for (int s = 0; s < strips; ++s) {
+        const int X0 = s * a.strip_cols, X1 = min(X0 + a.strip_cols, a.dd_w);
+        if (X0 < x1 && x0 < X1) e += p[s];
+      }
+      const int y0 = (int)((int64_t)by * a.dd_h / a.grid_h);
+      const int y1 = (int)((int64_t)(by + 1) * a.dd_h / a.grid_h);
+      DiffSums<NSC_METRIC_MSE> b;
+      b.e = e;
+      m = b.value(a, ((double)(y1 - y0) * (double)(x1 - x0)) * 3.0);
+    }
+    for (int bx = 0; bx < gw; ++bx) z = z + (double)a.lr_w[by * gw + bx] * __shfl(m, bx, 64);
+  }
+  return z;
+}
+
 // The fixed-reference detector fused into the area kernel: a thread per
 // frame adds the frame's per-unit partial sums (exact integers, so their order
 // does not matter) and applies the metric as k_diff does.
@@ -561,7 +739,11 @@ __global__ void __launch_bounds__(256) k_diff(DiffArgs a) {
   const int64_t cells = (int64_t)a.dd_h * a.dd_w * 3;
   const bool forced = a.ref_mode == NSC_REF_PREV && t < a.delta;
   double score = INFINITY;
-  if (!forced) {
+  const bool from_part =
+      M == NSC_METRIC_MSE && a.part != nullptr && !forced && (i / a.delta) % a.chain_r != 0;
+  if (from_part) {
+    score = part_score<BLK>(a, i, lane);
+  } else if (!forced) {
     const int32_t* cur = a.sums + i * cells;
     const int32_t* ref;
     if (a.ref_mode == NSC_REF_FIXED)
@@ -773,6 +955,81 @@ int launch_diff(const DiffArgs& a, hipStream_t stream) {
 #undef NSC_DIFF_LAUNCH
   NSC_CHECK_LAUNCH("k_diff");
   return NSC_OK;
+}
+
+bool area_prev_plan(const AreaPlan& p, const DiffArgs& a, int64_t n, PrevFusePlan* out) {
+  if (!p.wave || a.ref_mode != NSC_REF_PREV || a.metric != NSC_METRIC_MSE || a.cams != nullptr ||
+      a.delta < 1 || n < 2 * (int64_t)a.delta)
+    return false;
+  const bool blk = a.grid_h * a.grid_w > 1;
+  if (blk && (a.grid_w > 64 || a.grid_h > p.ay.n_out)) return false;
+  AreaPlan q = p;
+  WaveGeom& g = q.wg;
+  const int64_t scols = (int64_t)g.groups_per_wave * g.group_cols;
+  if (scols * 3 > 64 * kPrevSlots) return false;
+  if (blk) {  // one band per block row
+    g.bands = a.grid_h;
+    g.band_rows = (p.ay.n_out + a.grid_h - 1) / a.grid_h;
+    const int64_t cellb = q.packed ? 2 : 4;
+    const int64_t per_wave =
+        (64 * g.chunk_bytes * cellb + (int64_t)g.band_rows * scols * 3 * 4 + 15) & ~(int64_t)15;
+    g.lds_bytes = (size_t)(scols * 16 + g.waves_per_block * per_wave);
+    if (g.lds_bytes > 64 * 1024) return false;
+  }
+  // chains of R frames, as long as the launch keeps about 8 rounds of the
+  // chip's resident waves (18 per CU) busy, between 2 and 16 frames
+  const int64_t units = n * g.bands * g.waves_per_frame;
+  int64_t R = units / (8LL * kNumCU * 18);
+  const int64_t q_max = (n + a.delta - 1) / a.delta;
+  if (R > 16) R = 16;
+  if (R > q_max) R = q_max;
+  if (R < 2) R = 2;
+  out->ap = q;
+  out->chain_r = (int32_t)R;
+  out->part_elems = n * g.bands * g.waves_per_frame * (blk ? a.grid_w : 1);
+  return true;
+}
+
+int launch_area_prev(const PrevFusePlan& fp, const uint8_t* frames, int64_t stride, int64_t n,
+                     int32_t* sums, const DiffArgs& a, int64_t* part, hipStream_t stream) {
+  if (n <= 0) return NSC_OK;
+  const WaveGeom& g = fp.ap.wg;
+  const int64_t q = (n + a.delta - 1) / a.delta;        // frames per residue (at most)
+  const int64_t chains = (q + fp.chain_r - 1) / fp.chain_r * a.delta;
+  const int64_t units = chains * g.bands * g.waves_per_frame;
+  const int64_t wblocks = (units + g.waves_per_block - 1) / g.waves_per_block;
+  if (wblocks > 0x7FFFFFFF) return fail(NSC_E_SHAPE, "too many frames in one call");
+  const bool blk = a.grid_h * a.grid_w > 1;
+#define NSC_PREV_LAUNCH(CB, PK, B)                                                               \
+  hipLaunchKernelGGL((k_area_prev_wave<CB, PK, CB == 32 ? NSC_ROWS_BATCH / 2 : NSC_ROWS_BATCH, B>), \
+                     dim3((unsigned)wblocks), dim3(64 * g.waves_per_block), g.lds_bytes, stream,  \
+                     frames, stride, fp.ap.ay, fp.ap.ax, g, n, a.delta, fp.chain_r, a.grid_w, sums, \
+                     part)
+#define NSC_PREV_CB(B)                                                                           \
+  if (g.chunk_bytes == 32) {                                                                     \
+    if (fp.ap.packed) NSC_PREV_LAUNCH(32, true, B); else NSC_PREV_LAUNCH(32, false, B);          \
+  } else if (g.chunk_bytes == 16) {                                                              \
+    if (fp.ap.packed) NSC_PREV_LAUNCH(16, true, B); else NSC_PREV_LAUNCH(16, false, B);          \
+  } else {                                                                                       \
+    if (fp.ap.packed) NSC_PREV_LAUNCH(4, true, B); else NSC_PREV_LAUNCH(4, false, B);            \
+  }
+  if (blk) {
+    NSC_PREV_CB(true)
+  } else {
+    NSC_PREV_CB(false)
+  }
+#undef NSC_PREV_CB
+#undef NSC_PREV_LAUNCH
+  NSC_CHECK_LAUNCH("k_area_prev_wave");
+  return NSC_OK;
+}
+
+void area_prev_diff_args(const PrevFusePlan& fp, const int64_t* part, DiffArgs* a) {
+  a->part = part;
+  a->chain_r = fp.chain_r;
+  a->part_bands = fp.ap.wg.bands;
+  a->part_strips = fp.ap.wg.waves_per_frame;
+  a->strip_cols = fp.ap.wg.groups_per_wave * fp.ap.wg.group_cols;
 }
 
 bool area_detect_fused(const AreaPlan& p, const DiffArgs& a) {

@@ -1877,7 +1877,7 @@ __global__ void __launch_bounds__(64 * kDenseSplitWaves) k_dense_part(DenseArgs 
   }
 }
 
-// Tiled dense layer (fp16 path, single network): an item is a block of
+// Tiled dense layer (fp16 path): an item is a block of
 // kDenseTileRows survivors and a K part; its 4 waves take 32 survivors each
 // (two 16-row tiles) and walk the part's K range together in chunks of
 // kDenseChunk K steps, whose weight fragments the workgroup stages in LDS
@@ -1896,7 +1896,7 @@ __device__ __forceinline__ int dense_tile_kparts(int64_t cnt, int nks) {
   return k < 1 ? 1 : (int)k;
 }
 
-template <int NT>
+template <int NT, bool G>
 __global__ void __launch_bounds__(256) k_dense_tiles(DenseArgs a, f32x4* __restrict__ part) {
   constexpr int MT = 2;
   __shared__ __align__(16) f16x8 wl[kDenseChunk][NT][64];
@@ -1910,64 +1910,81 @@ __global__ void __launch_bounds__(256) k_dense_tiles(DenseArgs a, f32x4* __restr
   const int kparts = dense_tile_kparts(cnt, nks);
   const int64_t blocks = (cnt + kDenseTileRows - 1) / kDenseTileRows;
   const int64_t items = blocks * kparts;
-  const float in_scale = a.scl[0];
-  const f16x8* wsrc = reinterpret_cast<const f16x8*>(a.w1);
+  auto cam_of = [&](int64_t u) -> int64_t { return a.idx[u] / a.per_cam; };
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
     const int64_t blk = item / kparts;
     const int kp = (int)(item - blk * kparts);
     const int c0 = (int)((int64_t)kp * nch / kparts), c1 = (int)((int64_t)(kp + 1) * nch / kparts);
     const int64_t tile0 = blk * (kDenseTileRows / 16) + wave * MT;  // this wave's 16-row tiles
-    bool valid[MT];
-    int64_t row[MT];
-#pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      const int64_t s = (tile0 + i) * 16 + m;
-      valid[i] = s < cnt;
-      row[i] = (valid[i] ? s : 0) * (int64_t)a.flat + g * 8;
-    }
-    // the activation fragment of K step ks for tile i (zero past the end)
-    auto ldx = [&](int ks, f16x8 (&x)[MT]) {
-      const int k0 = ks * 32;
-      const bool kin = k0 + g * 8 < a.flat;
-#pragma unroll
-      for (int i = 0; i < MT; ++i) {
-        x[i] = Elt<_Float16>::zero();
-        if (valid[i] && kin)
-          x[i] = a.feat_f16 ? *reinterpret_cast<const f16x8*>(
-                                  reinterpret_cast<const _Float16*>(a.feat) + row[i] + k0)
-                            : Elt<_Float16>::cvt8(a.feat + row[i] + k0, in_scale);
-      }
-    };
     f32x4 acc[MT][NT];
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    f16x8 xc[MT], xn[MT];
-    ldx(c0 * kDenseChunk, xc);
+    // In a camera group the block runs once per camera among its rows, each
+    // pass with that camera's weights over its own rows (the other rows add
+    // zero products, which leave their sums unchanged).
+    int64_t cam = G ? cam_of(blk * kDenseTileRows) : 0;
+    for (;;) {
+      const int64_t off = G ? (int64_t)a.nets[cam].woff : 0;
+      const float in_scale = at_off(a.scl, off)[0];
+      const f16x8* wsrc = at_off(reinterpret_cast<const f16x8*>(a.w1), off);
+      bool valid[MT];
+      int64_t row[MT];
 #pragma unroll
-    for (int i = 0; i < MT; ++i) xn[i] = xc[i];
-    for (int c = c0; c < c1; ++c) {
-      __syncthreads();  // the previous chunk's fragments are read
-      {
-        const f16x8* src = wsrc + (size_t)c * kDenseChunk * NT * 64;
-        f16x8* dst = &wl[0][0][0];
-        for (int i = threadIdx.x; i < kDenseChunk * NT * 64; i += 256) dst[i] = src[i];
+      for (int i = 0; i < MT; ++i) {
+        const int64_t s = (tile0 + i) * 16 + m;
+        valid[i] = s < cnt && (!G || cam_of(s) == cam);
+        row[i] = (valid[i] ? s : 0) * (int64_t)a.flat + g * 8;
       }
-      __syncthreads();
+      // the activation fragment of K step ks for tile i (zero past the end)
+      auto ldx = [&](int ks, f16x8 (&x)[MT]) {
+        const int k0 = ks * 32;
+        const bool kin = k0 + g * 8 < a.flat;
 #pragma unroll
-      for (int j = 0; j < kDenseChunk; ++j) {
-        const int ks = c * kDenseChunk + j;
-        if (ks + 1 < c1 * kDenseChunk) ldx(ks + 1, xn);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const f16x8 w = wl[j][nt][lane];
-#pragma unroll
-          for (int i = 0; i < MT; ++i) acc[i][nt] = mma_f16(xc[i], w, acc[i][nt]);
+        for (int i = 0; i < MT; ++i) {
+          x[i] = Elt<_Float16>::zero();
+          if (valid[i] && kin)
+            x[i] = a.feat_f16 ? *reinterpret_cast<const f16x8*>(
+                                    reinterpret_cast<const _Float16*>(a.feat) + row[i] + k0)
+                              : Elt<_Float16>::cvt8(a.feat + row[i] + k0, in_scale);
         }
+      };
+      f16x8 xc[MT], xn[MT];
+      ldx(c0 * kDenseChunk, xc);
 #pragma unroll
-        for (int i = 0; i < MT; ++i) xc[i] = xn[i];
+      for (int i = 0; i < MT; ++i) xn[i] = xc[i];
+      for (int c = c0; c < c1; ++c) {
+        __syncthreads();  // the previous chunk's fragments are read
+        {
+          const f16x8* src = wsrc + (size_t)c * kDenseChunk * NT * 64;
+          f16x8* dst = &wl[0][0][0];
+          for (int i = threadIdx.x; i < kDenseChunk * NT * 64; i += 256) dst[i] = src[i];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kDenseChunk; ++j) {
+          const int ks = c * kDenseChunk + j;
+          if (ks + 1 < c1 * kDenseChunk) ldx(ks + 1, xn);
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            const f16x8 w = wl[j][nt][lane];
+#pragma unroll
+            for (int i = 0; i < MT; ++i) acc[i][nt] = mma_f16(xc[i], w, acc[i][nt]);
+          }
+#pragma unroll
+          for (int i = 0; i < MT; ++i) xc[i] = xn[i];
+        }
       }
+      if constexpr (!G) break;
+      // the next camera among the block's rows (uniform)
+      int64_t next = -1;
+      for (int r = 0; r < kDenseTileRows && next < 0; ++r) {
+        const int64_t u = blk * kDenseTileRows + r;
+        if (u < cnt && cam_of(u) > cam) next = cam_of(u);
+      }
+      if (next < 0) break;
+      cam = next;
     }
 #pragma unroll
     for (int i = 0; i < MT; ++i)
@@ -2114,11 +2131,17 @@ int launch_dense_split_nt(int nt, const DenseArgs& a, f32x4* part, unsigned grid
 
 int launch_dense_tiles_nt(int nt, const DenseArgs& a, f32x4* part, unsigned grid,
                           unsigned grid_fin, hipStream_t st) {
+#define NSC_TILES_LAUNCH(N, G)                                                                  \
+  hipLaunchKernelGGL((k_dense_tiles<N, G>), dim3(grid), dim3(256), 0, st, a, part);            \
+  hipLaunchKernelGGL((k_dense_finish<_Float16, N, G>), dim3(grid_fin),                         \
+                     dim3(64 * kDenseFinWaves), 0, st, a, (const f32x4*)part)
 #define NSC_TILES_CASE(N)                                                                       \
   case N:                                                                                       \
-    hipLaunchKernelGGL((k_dense_tiles<N>), dim3(grid), dim3(256), 0, st, a, part);             \
-    hipLaunchKernelGGL((k_dense_finish<_Float16, N, false>), dim3(grid_fin),                   \
-                       dim3(64 * kDenseFinWaves), 0, st, a, (const f32x4*)part);                \
+    if (a.nets) {                                                                               \
+      NSC_TILES_LAUNCH(N, true);                                                                \
+    } else {                                                                                    \
+      NSC_TILES_LAUNCH(N, false);                                                               \
+    }                                                                                           \
     break;
   switch (nt) {
     NSC_TILES_CASE(1)
@@ -2130,6 +2153,7 @@ int launch_dense_tiles_nt(int nt, const DenseArgs& a, f32x4* part, unsigned grid
       return fail(NSC_E_SHAPE, "dense layer of %d units is not supported", nt * 16);
   }
 #undef NSC_TILES_CASE
+#undef NSC_TILES_LAUNCH
   NSC_CHECK_LAUNCH("k_dense_tiles / k_dense_finish");
   return NSC_OK;
 }
@@ -2411,8 +2435,8 @@ size_t cnn_xin_bytes(const Cnn& cnn, int64_t max_count) {
 }
 
 // The dense layer's partial blocks when it splits K over workgroups: one
-// NT x 1 KB block per (16-row tile, K part), for k_dense_tiles (fp16 path
-// without a camera group: its 128-row blocks times their K parts, at most the
+// NT x 1 KB block per (16-row tile, K part), for k_dense_tiles (fp16 path:
+// its 128-row blocks times their K parts, at most the
 // larger of kDenseTileItems x 8 and the tiles of max_count) or k_dense_part
 // (fewer than kDenseBig survivors otherwise); room for both.
 size_t cnn_dense_part_bytes(const Cnn& cnn, int64_t max_count) {
@@ -2614,7 +2638,7 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
   f32x4* part = reinterpret_cast<f32x4*>(static_cast<unsigned char*>(ws) +
                                          2 * per * (size_t)r.max_count + 256 +
                                          cnn_xin_bytes(cnn, r.max_count));
-  if (cnn.h16 && cnn.w1f && !r.nets) {
+  if (cnn.h16 && cnn.w1f) {
     d.w1 = cnn.w1f;
     d.tiled = 1;
     const int64_t grid = kDenseTileItems;  // the kernel loops over its items

@@ -119,8 +119,29 @@ struct DiffArgs {
   int64_t per_cam;
   const unsigned char* state;
   int64_t state_stride;
+  // earlier-frame MSE detector fused into the area kernel (k_area_prev_wave):
+  // frames whose index i has (i / delta) mod chain_r != 0 take their score
+  // from the partial sums (part_bands bands x part_strips strips of
+  // strip_cols output columns, per block column when blocked); the others
+  // from the sums.  part == null: every frame from the sums.
+  const int64_t* part;
+  int32_t chain_r, part_bands, part_strips, strip_cols;
 };
 int launch_diff(const DiffArgs& a, hipStream_t stream);
+// The earlier-frame MSE detector fused into the area kernel: whether it
+// applies to a call of n frames, and then its plan (bands = block rows when
+// blocked), chain length and partial-sum count.
+struct PrevFusePlan {
+  AreaPlan ap;
+  int32_t chain_r;
+  int64_t part_elems;
+};
+bool area_prev_plan(const AreaPlan& p, const DiffArgs& a, int64_t n, PrevFusePlan* out);
+// Launches the fused area kernel (sums and partial sums), then k_diff is
+// launched with the fields area_prev_diff_args sets.
+int launch_area_prev(const PrevFusePlan& fp, const uint8_t* frames, int64_t stride, int64_t n,
+                     int32_t* sums, const DiffArgs& a, int64_t* part, hipStream_t stream);
+void area_prev_diff_args(const PrevFusePlan& fp, const int64_t* part, DiffArgs* a);
 // Area sums with the fixed-reference global detector fused in (when
 // area_detect_fused): per-unit partial sums in `part` (area_detect_part_count
 // units x 3 int64), then the scores and fire flags of `a`.
