@@ -70,6 +70,17 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 AREA_KERNEL = "k_area_sums_wave"
+
+
+def area_kernel(wl) -> str:
+    """The area kernel a workload's cascade runs: against an earlier frame at
+    least two frames back with the MSE metric, the one with the detector fused
+    in (k_area_prev_wave); otherwise k_area_sums_wave (which fuses the global
+    detector against a fixed reference image)."""
+    delta = wl.delta // max(1, getattr(wl, "check_stride", 1))  # in checked frames
+    if wl.ref_mode == 0 and delta >= 2 and getattr(wl, "metric", 0) == 0:
+        return "k_area_prev_wave"
+    return AREA_KERNEL
 AREA_SOURCES = ("paper_1703_02529_amd/csrc/area_diff.hip", "paper_1703_02529_amd/csrc/nsc_internal.h")
 COPY_BYTES = 1 << 31           # plain copy of known size for counter calibration
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
@@ -117,12 +128,12 @@ class HipEvents:
             self.hip.hipEventDestroy(ctypes.c_void_p(e))
 
 
-def measured_traffic(workload: str):
+def measured_traffic(workload: str, kernel: str = AREA_KERNEL):
     """HBM bytes per launch of the area kernel from the committed counter
     summary, or None when there is none or the kernel's sources changed since."""
     from paper_1703_02529_amd.profsum import sources_hash
 
-    path = os.path.join(ROOT, "profiles", f"traffic_{AREA_KERNEL}_{workload}.json")
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
     if not os.path.exists(path):
         return None, "no counter summary"
     with open(path) as fh:
@@ -708,7 +719,8 @@ def bench_chunked(args):
     # HBM bytes per area launch (the mean over the chunks, as avg_launch_ms);
     # the area kernel does not depend on the occupancy
     base = {"hd-ref": W.HD_REF, "hd-blocked": W.HD_BLOCKED, "fhd-stream": W.FHD_STREAM}[args.workload]
-    traffic, traffic_src = measured_traffic(base.name)
+    kern = area_kernel(wl)
+    traffic, traffic_src = measured_traffic(base.name, kern)
     if args.frames is not None and traffic is not None:
         traffic_src += " (counters of the whole video)"
     layers = ", ".join(f"{c}{'+pool' if p else ''}" for c, p in zip(wl.cnn.conv, wl.cnn.pool))
@@ -741,7 +753,7 @@ def bench_chunked(args):
                            "cascade stream); ms_per_step is the cascade time of a pass"},
         "roofline": {
             "bound": "hbm",
-            "kernel": AREA_KERNEL,
+            "kernel": kern,
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
@@ -843,7 +855,10 @@ def bench_resident(args):
     achieved = area_bytes / (area_ms * 1e-3) / 1e9
     diff_ms = float(stage[:, 0:3].sum(1).mean())
     diff_gbs = (area_bytes + checked) / (diff_ms * 1e-3) / 1e9
-    traffic, traffic_src = measured_traffic(base.name)  # the area kernel ignores the metric
+    kern = area_kernel(wl)
+    traffic, traffic_src = measured_traffic(base.name, kern)  # counters of the MSE run
+    if kern != area_kernel(base):
+        traffic, traffic_src = None, f"counters were taken of {area_kernel(base)}"
     if wl.check_stride != 1:
         traffic, traffic_src = None, "counters were taken without frame skipping"
     cnn_ms = float(stage[:, 3].mean())
@@ -886,7 +901,7 @@ def bench_resident(args):
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": AREA_KERNEL,
+            "kernel": kern,
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
