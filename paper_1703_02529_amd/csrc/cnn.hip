@@ -904,6 +904,7 @@ __global__ void __launch_bounds__(1024) k_conv_pair(ConvArgs a0, ConvArgs a1, Pa
 // the four lanes of one quad (DPP) and every store is 16 bytes.
 
 constexpr int kBandWaves = 4;  // waves per workgroup of the banded kernels
+constexpr int kBandMaxTilesH = 7;  // tiles per wave and round on the fp16 path (4 with hi / lo)
 
 struct Band64 {
   int32_t w, h;      // layer input grid
@@ -1089,9 +1090,11 @@ __device__ __forceinline__ void band64_tiles(const unsigned char* lds, const Ban
   const uint32_t step2 = (uint32_t)b.cp * 64u;  // chunks 4..7: 4 chunk planes on
   const typename Band64Frag<H>::type* wp = wf + lane;
   if constexpr (H) {
-    // fp16: the weight fragments (from L2) of the next tap are loaded while
-    // the current tap computes; the activations (LDS) one step ahead
-    f16x8 w0[NT], w1[NT], v0[NT], v1[NT], x0[MT], x1[MT];
+    // fp16: the weight fragments (from L2) and the activation fragments (LDS)
+    // of the next K step are loaded while the current one computes, in two
+    // register sets (steps 2 j and 2 j + 1), so that up to 7 tiles fit
+    constexpr int KSTEPS = 18;  // 9 taps x 2 steps of 32 channels
+    f16x8 wa[NT], wb[NT], xa[MT], xb[MT];
     auto ldw = [&](int j, f16x8 (&d)[NT]) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) d[nt] = wp[(j * NT + nt) * 64];
@@ -1108,27 +1111,21 @@ __device__ __forceinline__ void band64_tiles(const unsigned char* lds, const Ban
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) acc[i][nt] = mma_f16(wv[nt], xv[i], acc[i][nt]);
     };
-    ldw(0, w0);
-    ldw(1, w1);
-    ldx(0, x0);
+    ldw(0, wa);
+    ldx(0, xa);
 #pragma unroll 1
-    for (int tap = 0; tap < 9; ++tap) {
-      const int tn = tap < 8 ? tap + 1 : tap;  // the last tap reloads its own, unused
-      ldw(2 * tn, v0);
-      ldw(2 * tn + 1, v1);
-      ldx(2 * tap + 1, x1);
+    for (int j = 0; j < KSTEPS; j += 2) {
+      ldw(j + 1, wb);
+      ldx(j + 1, xb);
       __builtin_amdgcn_sched_barrier(0);
-      mma(w0, x0);
+      mma(wa, xa);
       __builtin_amdgcn_sched_barrier(0);
-      ldx(2 * tn, x0);
+      const int jn = j + 2 < KSTEPS ? j + 2 : j + 1;  // the last step reloads its own, unused
+      ldw(jn, wa);
+      ldx(jn, xa);
       __builtin_amdgcn_sched_barrier(0);
-      mma(w1, x1);
+      mma(wb, xb);
       __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        w0[nt] = v0[nt];
-        w1[nt] = v1[nt];
-      }
     }
     return;
   }
@@ -1170,9 +1167,9 @@ constexpr int kQuadXor2 = 0x4E;  // [2, 3, 0, 1]
 // bit); otherwise k = 1 and bb is the bias.  The output is fp32 (16-byte
 // stores), or with f16out fp16 (8-byte stores).
 template <int NT>
-__device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const float4 (&bb)[NT],
-                                                float k, void* out, int cout, int oy, int ox, int h,
-                                                int w, int pool, int m, bool f16out) {
+__device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const float* __restrict__ bp,
+                                                float s, float k, void* out, int cout, int oy,
+                                                int ox, int h, int w, int pool, int m, bool f16out) {
   auto store = [&](int64_t e, const float (&v)[4]) {  // element offset e, 4 channels
     if (f16out)
       *reinterpret_cast<uint2*>(static_cast<_Float16*>(out) + e) =
@@ -1187,8 +1184,9 @@ __device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const fl
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const f32x4 t = acc[nt];
-    float v[4] = {fmaxf(fmaf(t[0], k, bb[nt].x), 0.f), fmaxf(fmaf(t[1], k, bb[nt].y), 0.f),
-                  fmaxf(fmaf(t[2], k, bb[nt].z), 0.f), fmaxf(fmaf(t[3], k, bb[nt].w), 0.f)};
+    const float4 bb = *reinterpret_cast<const float4*>(bp + nt * 16);
+    float v[4] = {fmaxf(fmaf(t[0], k, bb.x * s), 0.f), fmaxf(fmaf(t[1], k, bb.y * s), 0.f),
+                  fmaxf(fmaf(t[2], k, bb.z * s), 0.f), fmaxf(fmaf(t[3], k, bb.w * s), 0.f)};
     if (pool) {
       // the four pixels of a pooling window are the four lanes of a quad; the
       // values are >= 0 (or -0) after the ReLU, so their maximum is the
@@ -1212,9 +1210,9 @@ __device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const fl
 template <int MT, int NT, bool H>
 __device__ __forceinline__ void band64_run(const unsigned char* lds, const Band64& b, int ty0,
                                            const typename Band64Frag<H>::type* __restrict__ wf,
-                                           const float4 (&bb)[NT], float k, void* out, int cout,
-                                           int pool, int tiles_x, int first, int py, int px, int m,
-                                           int g, int lane, bool f16out) {
+                                           const float* __restrict__ bp, float s, float k,
+                                           void* out, int cout, int pool, int tiles_x, int first,
+                                           int py, int px, int m, int g, int lane, bool f16out) {
   int tr[MT], tc[MT];
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
@@ -1226,8 +1224,8 @@ __device__ __forceinline__ void band64_run(const unsigned char* lds, const Band6
   band64_tiles<MT, NT, H>(lds, b, wf, tr, tc, py, px, g, lane, acc);
 #pragma unroll
   for (int i = 0; i < MT; ++i)
-    band64_epilogue<NT>(acc[i], bb, k, out, cout, 4 * (ty0 + tr[i]) + py, 4 * tc[i] + px, b.h,
-                        b.w, pool, m, f16out);
+    band64_epilogue<NT>(acc[i], bp, s, k, out, cout, 4 * (ty0 + tr[i]) + py, 4 * tc[i] + px,
+                        b.h, b.w, pool, m, f16out);
 }
 
 // One band's work of a 64-input-channel layer: ntile tiles over the 4 waves,
@@ -1243,32 +1241,46 @@ __device__ __forceinline__ void band64_layer(const unsigned char* lds, const Ban
   const bool f16out = st16 != 0.0f;
   const float s = f16out ? st16 : 1.0f;
   const float k = H ? sc * s : 1.0f;
-  float4 bb[NT];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const float4 v = *reinterpret_cast<const float4*>(bias + nt * 16 + 4 * g);
-    bb[nt] = make_float4(v.x * s, v.y * s, v.z * s, v.w * s);
-  }
+  const float* bp = bias + 4 * g;  // this lane's channel group
   out = f16out ? static_cast<void*>(static_cast<_Float16*>(out) + 4 * g)
                : static_cast<void*>(static_cast<float*>(out) + 4 * g);
-  for (int base = 0; base < ntile; base += 4 * kBandWaves) {
+  constexpr int MTMAX = H ? kBandMaxTilesH : 4;
+  for (int base = 0; base < ntile; base += MTMAX * kBandWaves) {
     const int first = base + wave;
-    const int mt = first >= ntile ? 0 : min(4, (ntile - first + kBandWaves - 1) / kBandWaves);
+    const int mt = first >= ntile ? 0 : min(MTMAX, (ntile - first + kBandWaves - 1) / kBandWaves);
+    if constexpr (H) {
+      switch (mt) {
+        case 7:
+          band64_run<7, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
+                               g, lane, f16out);
+          continue;
+        case 6:
+          band64_run<6, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
+                               g, lane, f16out);
+          continue;
+        case 5:
+          band64_run<5, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
+                               g, lane, f16out);
+          continue;
+        default:
+          break;
+      }
+    }
     switch (mt) {
       case 4:
-        band64_run<4, NT, H>(lds, b, ty0, wf, bb, k, out, cout, pool, tiles_x, first, py, px, m,
+        band64_run<4, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
                              g, lane, f16out);
         break;
       case 3:
-        band64_run<3, NT, H>(lds, b, ty0, wf, bb, k, out, cout, pool, tiles_x, first, py, px, m,
+        band64_run<3, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
                              g, lane, f16out);
         break;
       case 2:
-        band64_run<2, NT, H>(lds, b, ty0, wf, bb, k, out, cout, pool, tiles_x, first, py, px, m,
+        band64_run<2, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
                              g, lane, f16out);
         break;
       case 1:
-        band64_run<1, NT, H>(lds, b, ty0, wf, bb, k, out, cout, pool, tiles_x, first, py, px, m,
+        band64_run<1, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
                              g, lane, f16out);
         break;
       default:
@@ -2342,10 +2354,12 @@ bool band64_plan(const CnnLayer& L, bool h16, Band64* b, int32_t* band_tiles, si
   };
   int32_t bt = 1;
   double best = 1e30;
-  // at most 16 tiles (4 per wave) or two tile rows per band: taller bands
-  // measured slower (4 tile rows of a 25 x 25 map: 523 against 459 us per
-  // 8,192 images)
-  const int32_t cmax = 16 / tx > 2 ? 16 / tx : 2;
+  // at most one round of tiles (4 per wave with hi / lo planes, 8 on the
+  // fp16 path) or two tile rows per band: taller bands with two rounds
+  // measured slower (4 tile rows of a 25 x 25 map with 4 tiles per wave and
+  // round: 523 against 459 us per 8,192 images)
+  const int32_t per_round = (h16 ? kBandMaxTilesH : 4) * kBandWaves;
+  const int32_t cmax = per_round / tx > 2 ? per_round / tx : 2;
   for (int32_t c = 1; c <= ty && c <= cmax; ++c) {
     if (band64_bytes(plan(c)) > 80 * 1024) break;
     double cost = 0.0;
