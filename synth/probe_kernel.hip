@@ -6,19 +6,33 @@
 
 namespace {
 
-// Every thread reads 16-byte vectors a grid stride apart, four in flight; the
-// folded value is stored only under a condition that the data never meets, so
-// the loads stay live without any writes.
+// Each workgroup reads contiguous blocks of kProbeBlock16 16-byte vectors
+// (blocks gridDim.x apart), every thread sixteen vectors in flight, then the
+// tail of the buffer a grid stride apart; the folded value is stored only
+// under a condition that the data never meets, so the loads stay live
+// without any writes.  (Of the patterns tried on one MI355X, 256 KB blocks
+// with 16 loads in flight read fastest: 6.36 TB/s, against 6.19 for a grid
+// stride with 8 or 16 in flight and 6.09 with 4.)
+constexpr int64_t kProbeBlock16 = (256 << 10) / 16;
+constexpr int kProbeInFlight = 16;
+
 __global__ void __launch_bounds__(256) probe_read(const uint4* __restrict__ p, int64_t n16,
                                                   uint32_t* out) {
   uint32_t acc = 0;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  for (; i + 3 * stride < n16; i += 4 * stride) {
-    const uint4 a = p[i], b = p[i + stride], c = p[i + 2 * stride], d = p[i + 3 * stride];
-    acc ^= a.x ^ b.y ^ c.z ^ d.w ^ a.w ^ b.x ^ c.y ^ d.z;
+  const int64_t nblk = n16 / kProbeBlock16;
+  for (int64_t b = blockIdx.x; b < nblk; b += gridDim.x) {
+    const uint4* q = p + b * kProbeBlock16;
+    for (int64_t i = threadIdx.x; i < kProbeBlock16; i += kProbeInFlight * 256) {
+      uint4 v[kProbeInFlight];
+#pragma unroll
+      for (int u = 0; u < kProbeInFlight; ++u) v[u] = q[i + u * 256];
+#pragma unroll
+      for (int u = 0; u < kProbeInFlight; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+    }
   }
-  for (; i < n16; i += stride) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = nblk * kProbeBlock16 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16;
+       i += stride) {
     const uint4 v = p[i];
     acc ^= v.x ^ v.w;
   }
