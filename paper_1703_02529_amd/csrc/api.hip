@@ -1236,6 +1236,7 @@ int nsc_group_run(const nsc_group* g, const uint8_t* frames, int64_t n, int64_t 
   r.frame_logit = outs ? outs->logit : nullptr;
   r.nets = g->nets;
   r.per_cam = n;
+  r.n_nets = g->n_cams;
   if (int rc = run_cnn(c, r, w + L.cnn, L.total - L.cnn, st)) return rc;
   if (int rc = mark(4)) return rc;
   // 5: decisions of the frames that did not fire, then the cameras' state

@@ -2652,7 +2652,11 @@ int run_cnn(const Cnn& cnn, const CnnRunArgs& r, void* ws, size_t ws_bytes, hipS
   f32x4* part = reinterpret_cast<f32x4*>(static_cast<unsigned char*>(ws) +
                                          2 * per * (size_t)r.max_count + 256 +
                                          cnn_xin_bytes(cnn, r.max_count));
-  if (cnn.h16 && cnn.w1f) {
+  // the tiled kernel for one network (also a one-camera group, which then
+  // gives nsc_cascade_run's results bit for bit); a group of several cameras
+  // runs a block's 128 rows once per camera among them, slower than the
+  // 16-row tiles below (0.19 against 0.09 ms for 100 cameras' 500 survivors)
+  if (cnn.h16 && cnn.w1f && (!r.nets || r.n_nets == 1)) {
     d.w1 = cnn.w1f;
     d.tiled = 1;
     const int64_t grid = kDenseTileItems;  // the kernel loops over its items

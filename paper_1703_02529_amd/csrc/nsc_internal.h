@@ -285,6 +285,7 @@ struct CnnRunArgs {
   // runs that camera's network, bias b2 and thresholds from nets[]
   const CamNet* nets;
   int64_t per_cam;
+  int32_t n_nets;           // cameras of the group (0 without a group)
 };
 size_t cnn_workspace_bytes(const Cnn& cnn, int64_t max_count);
 int run_cnn(const Cnn& cnn, const CnnRunArgs& a, void* ws, size_t ws_bytes, hipStream_t stream);
