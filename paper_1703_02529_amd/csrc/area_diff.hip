@@ -35,11 +35,15 @@ __device__ __forceinline__ uint32_t bytes13(uint32_t x) {
   return __builtin_amdgcn_perm(0u, x, 0x0C030C01u);  // (x.b1, 0, x.b3, 0)
 }
 
+// A lane's CB bytes of one row; a 32-byte chunk is two 16-byte halves `split`
+// bytes apart (the halves of all lanes of a strip are two contiguous runs, so
+// that each load instruction of the wave reads consecutive bytes).
 template <int CB>
-__device__ __forceinline__ void load_chunk(const uint8_t* p, uint32_t (&v)[CB >= 4 ? CB / 4 : 1]) {
+__device__ __forceinline__ void load_chunk(const uint8_t* p, uint32_t (&v)[CB >= 4 ? CB / 4 : 1],
+                                           int split = 16) {
   if constexpr (CB == 32) {
     const u32x4 x = *reinterpret_cast<const u32x4*>(p);
-    const u32x4 y = *reinterpret_cast<const u32x4*>(p + 16);
+    const u32x4 y = *reinterpret_cast<const u32x4*>(p + split);
     v[0] = x[0];
     v[1] = x[1];
     v[2] = x[2];
@@ -112,7 +116,7 @@ struct DiffSums {
 template <int CB, bool PACKED, int RB = NSC_ROWS_BATCH>
 __device__ __forceinline__ void vertical_sums(const uint8_t* __restrict__ col, int64_t row_bytes,
                                               int a0, int a1, int q, int j0, int j1,
-                                              int32_t out[CB]) {
+                                              int32_t out[CB], int split = 16) {
   constexpr int ND = CB >= 4 ? CB / 4 : 1;
   constexpr int NA = CB == 1 ? 1 : (PACKED ? 2 * ND : CB);
   const int nrows = j1 - j0;
@@ -127,7 +131,7 @@ __device__ __forceinline__ void vertical_sums(const uint8_t* __restrict__ col, i
     uint32_t v[RB][ND];
 #pragma unroll
     for (int k = 0; k < RB; ++k)
-      if (k < cnt) load_chunk<CB>(p + k * row_bytes, v[k]);
+      if (k < cnt) load_chunk<CB>(p + k * row_bytes, v[k], split);
 #pragma unroll
     for (int k = 0; k < RB; ++k) {
       if (k < cnt) {
@@ -238,36 +242,43 @@ __global__ void __launch_bounds__(1024) k_area_sums_rows(const uint8_t* __restri
   }
 }
 
-// Area sums of one wave's strip (lanes' chunks of CB bytes starting at col)
-// for output rows Y0..Y1-1: per output row, the vertical pass into the wave's
-// LDS column sums buf, then the horizontal pass; value t of band row r
-// (cell (t / 3) of the strip, channel t mod 3) with sum s is handed to
-// cell(t, r, s).  Lane l handles the values t = l, l + 64, ... of every row.
+// Area sums of one wave's strip for output rows Y0..Y1-1: per output row, the
+// vertical pass into the wave's LDS column sums buf, then the horizontal
+// pass; value t of band row r (cell (t / 3) of the strip, channel t mod 3)
+// with sum s is handed to cell(t, r, s).  Lane l handles the values t = l,
+// l + 64, ... of every row.  The nl active lanes read the strip's CB x nl
+// bytes: 16 or 4 bytes at col = strip + CB l, or with CB = 32 the 16-byte
+// pieces l and nl + l (col = strip + 16 l).
 // With MAXS > 0 (at most 64 MAXS values per row) the loop over a lane's
 // values is unrolled and cell(k, t, r, s) also gets the slot k (t = l + 64 k).
 template <int CB, bool PACKED, int RB, int MAXS = 0, class Cell, class Buf>
 __device__ __forceinline__ void strip_band_sums(const uint8_t* __restrict__ col, int64_t row_bytes,
                                                 const Axis& ay, int qx, int Y0, int Y1, int lane,
-                                                bool active, Buf* buf, const int4* xtab,
-                                                int ncells, Cell&& cell) {
+                                                int nl, Buf* buf, const int4* xtab, int ncells,
+                                                Cell&& cell) {
   using cell_t = Buf;
+  const bool active = lane < nl;
+  const int split = 16 * nl;  // CB = 32: bytes from a lane's first piece to its second
+  // LDS position (cells) of the lane's c-th 16-byte piece (c = 0, 1 for CB = 32)
+  auto piece = [&](int c) { return CB == 32 ? (c * nl + lane) * 16 : lane * CB; };
   for (int Y = Y0; Y < Y1; ++Y) {
     // uniform row bounds (divisions run on the vector unit; move them to scalars)
     const int a0 = Y * ay.p, a1 = a0 + ay.p;
     const int j0 = __builtin_amdgcn_readfirstlane(a0 / ay.q);
     const int j1 = __builtin_amdgcn_readfirstlane((a1 + ay.q - 1) / ay.q);
     int32_t v[CB];
-    vertical_sums<CB, PACKED, RB>(col, row_bytes, a0, a1, ay.q, j0, j1, v);
+    vertical_sums<CB, PACKED, RB>(col, row_bytes, a0, a1, ay.q, j0, j1, v, split);
     if (active) {
       if constexpr (PACKED && CB % 8 == 0) {  // 2 CB bytes per lane as 16-byte stores
-        uint4* d = reinterpret_cast<uint4*>(buf + lane * CB);
 #pragma unroll
-        for (int q = 0; q < CB / 8; ++q)
-          d[q] = make_uint4(v[8 * q] | (v[8 * q + 1] << 16), v[8 * q + 2] | (v[8 * q + 3] << 16),
-                            v[8 * q + 4] | (v[8 * q + 5] << 16), v[8 * q + 6] | (v[8 * q + 7] << 16));
+        for (int q = 0; q < CB / 8; ++q) {
+          uint4* d = reinterpret_cast<uint4*>(buf + piece(q / 2)) + (q & 1);
+          *d = make_uint4(v[8 * q] | (v[8 * q + 1] << 16), v[8 * q + 2] | (v[8 * q + 3] << 16),
+                          v[8 * q + 4] | (v[8 * q + 5] << 16), v[8 * q + 6] | (v[8 * q + 7] << 16));
+        }
       } else {
 #pragma unroll
-        for (int b = 0; b < CB; ++b) buf[lane * CB + b] = (cell_t)v[b];
+        for (int b = 0; b < CB; ++b) buf[piece(b / 16) + (b & 15)] = (cell_t)v[b];
       }
     }
     __syncwarp();
@@ -369,15 +380,15 @@ __global__ void __launch_bounds__(256) k_area_sums_wave(const uint8_t* __restric
   const int band = rem / g.waves_per_frame, strip = rem - band * g.waves_per_frame;
   const int group0 = strip * g.groups_per_wave;
   const int ngroups = min(g.groups_per_wave, g.groups_per_row - group0);
-  const bool active = lane < ngroups * g.group_lanes;
+  const int nl = ngroups * g.group_lanes;  // active lanes
   const int ncells = ngroups * g.group_cols * 3;
   const int X0 = group0 * g.group_cols;
   const int Y0 = (int)((int64_t)band * Ho / bands);
   const int Y1 = (int)((int64_t)(band + 1) * Ho / bands);
   const int64_t row_bytes = (int64_t)ax.n_in * 3;
-  const uint8_t* col =
-      frames + f * stride + ((int64_t)group0 * g.group_lanes + (active ? lane : 0)) * CB;
-  strip_band_sums<CB, PACKED, RB>(col, row_bytes, ay, qx, Y0, Y1, lane, active, buf, xtab, ncells,
+  const uint8_t* col = frames + f * stride + (int64_t)group0 * g.group_lanes * CB +
+                       (int64_t)(lane < nl ? lane : 0) * (CB == 32 ? 16 : CB);
+  strip_band_sums<CB, PACKED, RB>(col, row_bytes, ay, qx, Y0, Y1, lane, nl, buf, xtab, ncells,
                                   [&](int t, int r, int32_t s) { sbuf[r * ncells + t] = s; });
   // the band's sums, one output row segment after another
   int32_t* out = sums + (f * (int64_t)Ho * Wo + X0) * 3;
@@ -456,7 +467,7 @@ __global__ void __launch_bounds__(256) k_area_prev_wave(const uint8_t* __restric
   if (sg * R * delta + r >= n) return;  // no frames (uniform)
   const int group0 = strip * g.groups_per_wave;
   const int ngroups = min(g.groups_per_wave, g.groups_per_row - group0);
-  const bool active = lane < ngroups * g.group_lanes;
+  const int nl = ngroups * g.group_lanes;  // active lanes
   const int ncols = ngroups * g.group_cols;
   const int ncells = ncols * 3;
   const int X0 = group0 * g.group_cols;
@@ -473,14 +484,14 @@ __global__ void __launch_bounds__(256) k_area_prev_wave(const uint8_t* __restric
   for (int i = 0; i < R; ++i) {
     const int64_t f = (sg * R + i) * delta + r;
     if (f >= n) break;
-    const uint8_t* col =
-        frames + f * stride + ((int64_t)group0 * g.group_lanes + (active ? lane : 0)) * CB;
+    const uint8_t* col = frames + f * stride + (int64_t)group0 * g.group_lanes * CB +
+                         (int64_t)(lane < nl ? lane : 0) * (CB == 32 ? 16 : CB);
     int64_t e[kPrevSlots];
 #pragma unroll
     for (int k = 0; k < kPrevSlots; ++k) e[k] = 0;
     const bool diff = i > 0;
     strip_band_sums<CB, PACKED, RB, kPrevSlots>(
-        col, row_bytes, ay, qx, Y0, Y1, lane, active, buf, xtab, ncells,
+        col, row_bytes, ay, qx, Y0, Y1, lane, nl, buf, xtab, ncells,
         [&](int k, int t, int rr, int32_t s) {
           int32_t* q = sbuf + rr * ncells + t;
           if (diff) {
