@@ -969,12 +969,16 @@ int launch_diff(const DiffArgs& a, hipStream_t stream) {
 }
 
 bool area_prev_plan(const AreaPlan& p, const DiffArgs& a, int64_t n, PrevFusePlan* out) {
-  // against the frame just before (delta = 1) the chains are runs of
-  // consecutive frames, and the fused kernel measured 2.4 % slower than the
-  // two passes on 16,384 frames of 720p (blocked); from delta = 2 on it is not
-  // slower (640x480, delta 15: +0.2 %; 1920x1080, delta 30: -0.4 %)
-  if (!p.wave || a.ref_mode != NSC_REF_PREV || a.metric != NSC_METRIC_MSE || a.cams != nullptr ||
-      a.delta < 2 || n < 2 * (int64_t)a.delta)
+  // Measured against the two passes (whole cascade per call, alternating
+  // order in one process): with 16-byte lane chunks the fused kernel keeps
+  // the two-pass kernel's four waves per SIMD and is as fast (640x480, delta
+  // 15: within 0.1 %); with 32-byte chunks it needs 126 registers against
+  // 102 (four waves per SIMD instead of five) and is 3 % slower (1920x1080,
+  // delta 30, blocked; 2.4 % with chains of two frames); against the frame
+  // just before (delta = 1, chains of consecutive frames) 3.5 % slower on
+  // 720p blocked.  So it is taken with 16-byte chunks from delta = 2 on.
+  if (!p.wave || p.wg.chunk_bytes == 32 || a.ref_mode != NSC_REF_PREV ||
+      a.metric != NSC_METRIC_MSE || a.cams != nullptr || a.delta < 2 || n < 2 * (int64_t)a.delta)
     return false;
   const bool blk = a.grid_h * a.grid_w > 1;
   if (blk && (a.grid_w > 64 || a.grid_h > p.ay.n_out)) return false;
