@@ -292,6 +292,52 @@ int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_
                     nsc_run_stats* stats, void* const* stage_events, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Staged batches (Sec. 8: batching trades latency for throughput; Sec. 7:
+ * frames are batched for the GPU).  Frames that arrive in chunks (a decoder's
+ * or a generator's buffers) can be batched for steps 2-5 without keeping the
+ * raw frames: nsc_cascade_stage runs step 1 of one chunk into the batch's
+ * workspace, after which the chunk's frame buffer may be reused, and
+ * nsc_cascade_finish runs steps 2-5 once over everything staged, so the CNN
+ * sees the survivors of all the batch's chunks together.  Labels of a
+ * staged chunk exist only once its batch is finished: the latency grows with
+ * batch_frames.  The outputs equal those of nsc_cascade_run on the batch's
+ * frames in one call, logits up to the rounding order of the dense layer's
+ * sums (which depends on how many survivors share a pass).  The detector
+ * runs as a pass of its own over the staged sums.  Frame skipping is not
+ * available (check_stride 0 or 1).
+ *
+ * batch_frames (> 0) is the batch's capacity in frames; cnn_pass (>= 0)
+ * bounds the survivors of one CNN pass (0: min(16384, batch_frames)): the
+ * CNN runs ceil(batch_frames / pass) passes over the compacted list, each
+ * sized on the device (empty passes cost their launches only), and the
+ * workspace holds the CNN's buffers for one pass.  All three calls of one
+ * batch take the same cfg, cnn, batch_frames and cnn_pass.  Errors of all
+ * three: NSC_E_INVAL (a bad cfg or argument, frame skipping), NSC_E_SHAPE. */
+/* Workspace of a staged batch: the area sums of batch_frames frames, the
+ * detector, compaction and resolve buffers, and one CNN pass. */
+int nsc_batch_workspace_bytes(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, int64_t batch_frames,
+                              int64_t cnn_pass, size_t* bytes);
+/* Step 1 of n frames (device, frame i at frames + i * frame_stride) into
+ * batch slots [at, at + n) (at + n <= batch_frames) of ws
+ * (nsc_batch_workspace_bytes, 256-byte aligned).  Enqueued on `stream`; the
+ * frames are not read after this call's work has run.  Errors also
+ * NSC_E_WORKSPACE, NSC_E_HIP. */
+int nsc_cascade_stage(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, int64_t batch_frames,
+                      int64_t cnn_pass, const uint8_t* frames, int64_t n, int64_t at, void* ws,
+                      size_t ws_bytes, void* stream);
+/* Steps 2-5 on the frames staged in slots [0, n) (n <= batch_frames), which
+ * are frames [t0, t0 + n) of the stream: label_out, defer_out, outs, stats,
+ * state and stage_events as for nsc_cascade_run (stage events 0 and 1 are
+ * recorded together at the start: step 1 ran in the stage calls).  The
+ * state continues across batches and plain nsc_cascade_run calls of the same
+ * cfg.  Errors also NSC_E_WORKSPACE, NSC_E_STATE, NSC_E_HIP. */
+int nsc_cascade_finish(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, int64_t batch_frames,
+                       int64_t cnn_pass, int64_t n, int64_t t0, void* state, void* ws,
+                       size_t ws_bytes, uint8_t* label_out, uint8_t* defer_out,
+                       const nsc_frame_outputs* outs, nsc_run_stats* stats,
+                       void* const* stage_events, void* stream);
+
+/* ------------------------------------------------------------------------
  * Camera groups (Sec. 8: a system that watches many streams can batch frames
  * of different streams together, each stream with its own model).  A group of
  * n_cams fixed cameras shares the frame geometry (in_h, in_w, frame_stride,

@@ -98,6 +98,11 @@ def lib() -> ctypes.CDLL:
                                                    _vp, _vp, _vp, _sz, _vp]),
             "nsc_cascade_run": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i64, _vp, _vp, _sz, _vp, _vp,
                                                _vp, _vp, _vp, _vp]),
+            "nsc_batch_workspace_bytes": (ctypes.c_int, [_vp, _vp, _i64, _i64, _vp]),
+            "nsc_cascade_stage": (ctypes.c_int, [_vp, _vp, _i64, _i64, _vp, _i64, _i64, _vp, _sz,
+                                                 _vp]),
+            "nsc_cascade_finish": (ctypes.c_int, [_vp, _vp, _i64, _i64, _i64, _i64, _vp, _vp, _sz,
+                                                  _vp, _vp, _vp, _vp, _vp, _vp]),
             "nsc_group_create": (ctypes.c_int, [_vp, _vp, _i32, _vp]),
             "nsc_group_destroy": (ctypes.c_int, [_vp]),
             "nsc_group_state_bytes": (ctypes.c_int, [_vp, _vp, _vp]),
@@ -303,6 +308,43 @@ def nsc_cascade_run(cfg, cnn: Cnn, frames, n, t0, state, ws, label_out, defer_ou
                                  _ptr(defer_out), ctypes.byref(outs) if outs else None,
                                  ctypes.byref(st) if st else None, ev, _stream(stream)),
            "nsc_cascade_run")
+    if st is not None:
+        return dict(frames=st.frames, fired=st.fired, positive=st.positive, deferred=st.deferred)
+    return None
+
+
+def nsc_batch_workspace_bytes(cfg, cnn: Cnn, batch_frames: int, cnn_pass: int = 0) -> int:
+    b = _sz()
+    _check(lib().nsc_batch_workspace_bytes(ctypes.byref(cfg), cnn.handle, batch_frames, cnn_pass,
+                                           ctypes.byref(b)), "nsc_batch_workspace_bytes")
+    return b.value
+
+
+def nsc_cascade_stage(cfg, cnn: Cnn, batch_frames, cnn_pass, frames, n, at, ws, stream=None):
+    _check(lib().nsc_cascade_stage(ctypes.byref(cfg), cnn.handle, batch_frames, cnn_pass,
+                                   _ptr(frames), n, at, _ptr(ws), ws.numel() * ws.element_size(),
+                                   _stream(stream)), "nsc_cascade_stage")
+
+
+def nsc_cascade_finish(cfg, cnn: Cnn, batch_frames, cnn_pass, n, t0, state, ws, label_out,
+                       defer_out, score=None, fire=None, logit=None, want_stats=False,
+                       stage_events=None, stream=None):
+    """Arguments after cnn_pass as for nsc_cascade_run, without frames."""
+    outs = None
+    if score is not None or fire is not None or logit is not None:
+        outs = FrameOutputs(_ptr(score), _ptr(fire), _ptr(logit))
+    st = RunStats() if want_stats else None
+    ev = None
+    if stage_events is not None:
+        if len(stage_events) != NSC_STAGE_EVENTS:
+            raise ValueError(f"stage_events needs {NSC_STAGE_EVENTS} entries")
+        ev = (_vp * NSC_STAGE_EVENTS)(*[e if e else None for e in stage_events])
+    _check(lib().nsc_cascade_finish(ctypes.byref(cfg), cnn.handle, batch_frames, cnn_pass, n, t0,
+                                    _ptr(state), _ptr(ws), ws.numel() * ws.element_size(),
+                                    _ptr(label_out), _ptr(defer_out),
+                                    ctypes.byref(outs) if outs else None,
+                                    ctypes.byref(st) if st else None, ev, _stream(stream)),
+           "nsc_cascade_finish")
     if st is not None:
         return dict(frames=st.frames, fired=st.fired, positive=st.positive, deferred=st.deferred)
     return None

@@ -241,7 +241,11 @@ struct RunLayout {
   size_t total;
 };
 
-RunLayout run_layout(const nsc_cascade_cfg* c0, const Cnn& cnn, int64_t n_frames) {
+// cnn_pass > 0 sizes the CNN's share for passes of at most that many
+// survivors; a staged run (area sums written by earlier calls, detector in
+// its own pass) reserves no partial sums.
+RunLayout run_layout(const nsc_cascade_cfg* c0, const Cnn& cnn, int64_t n_frames,
+                     int64_t cnn_pass = 0, bool staged = false) {
   RunLayout L{};
   const nsc_cascade_cfg kc = checked_cfg(c0);
   const nsc_cascade_cfg* c = &kc;
@@ -273,11 +277,11 @@ RunLayout run_layout(const nsc_cascade_cfg* c0, const Cnn& cnn, int64_t n_frames
     L.sk_score = take((size_t)n * 8);
     L.sk_logit = take((size_t)n * 4);
   }
-  L.cnn = take(cnn_workspace_bytes(cnn, n));
+  L.cnn = take(cnn_workspace_bytes(cnn, cnn_pass > 0 && cnn_pass < n ? cnn_pass : n));
   // detector fused into the area kernel: per-unit partial sums, bounded by
   // the plan's units at one output row per band (fixed reference), or by the
   // fused earlier-frame plan's count
-  if (c->ref_mode == NSC_REF_PREV && c->metric == NSC_METRIC_MSE) {
+  if (!staged && c->ref_mode == NSC_REF_PREV && c->metric == NSC_METRIC_MSE) {
     AreaPlan ap;
     DiffArgs a{};
     a.ref_mode = c->ref_mode;
@@ -293,7 +297,7 @@ RunLayout run_layout(const nsc_cascade_cfg* c0, const Cnn& cnn, int64_t n_frames
       L.part = take((size_t)L.part_units * sizeof(int64_t));
     }
   }
-  if (c->ref_mode == NSC_REF_FIXED && c->grid_h * c->grid_w == 1) {
+  if (!staged && c->ref_mode == NSC_REF_FIXED && c->grid_h * c->grid_w == 1) {
     AreaPlan ap;
     if (make_area_plan(c->in_h, c->in_w, c->frame_stride, reinterpret_cast<const void*>(kAlign),
                        c->dd_h, c->dd_w, n > 0 ? n : 1, &ap) == NSC_OK &&
@@ -745,13 +749,34 @@ int nsc_specialized_cnn(const nsc_cnn* cnn, const int32_t* sums, int32_t sums_h,
 namespace nsc {
 namespace {
 
+// Counts of a finished run, read back to the host (synchronizes the stream).
+int run_stats(const uint8_t* label, const uint8_t* defer, const int32_t* count, int64_t n,
+              hipStream_t st, nsc_run_stats* stats) {
+  std::vector<uint8_t> hl(n), hd(n);
+  int32_t hc = 0;
+  NSC_TRY_HIP(hipMemcpyAsync(hl.data(), label, n, hipMemcpyDeviceToHost, st));
+  NSC_TRY_HIP(hipMemcpyAsync(hd.data(), defer, n, hipMemcpyDeviceToHost, st));
+  NSC_TRY_HIP(hipMemcpyAsync(&hc, count, 4, hipMemcpyDeviceToHost, st));
+  NSC_TRY_HIP(hipStreamSynchronize(st));
+  nsc_run_stats r{n, hc, 0, 0};
+  for (int64_t i = 0; i < n; ++i) {
+    r.positive += hl[i] && !hd[i];
+    r.deferred += hd[i];
+  }
+  *stats = r;
+  return NSC_OK;
+}
+
 // Steps 1-5 on frames [t0, t0 + n) of a configuration without frame skipping
-// (the checked frames); records stage events 0..4 through `mark`.
+// (the checked frames); records stage events 0..4 through `mark`.  With
+// frames == nullptr step 1 is skipped: the area sums of the n frames are
+// already in the workspace (staged by earlier calls).  cnn_pass > 0 runs the
+// CNN in passes over at most that many compacted slots each.
 template <class Mark>
 int run_checked(const nsc_cascade_cfg* cfg, const Cnn& c, const uint8_t* frames, int64_t n,
                 int64_t t0, void* state, unsigned char* w, const RunLayout& L, uint8_t* label_out,
                 uint8_t* defer_out, double* score_out, uint8_t* fire_out, float* logit_out,
-                hipStream_t st, Mark&& mark) {
+                int64_t cnn_pass, hipStream_t st, Mark&& mark) {
   const bool prev = cfg->ref_mode == NSC_REF_PREV;
   int32_t* sums = reinterpret_cast<int32_t*>(w + L.sums);
   uint8_t* fire = fire_out ? fire_out : w + L.fire;
@@ -766,10 +791,11 @@ int run_checked(const nsc_cascade_cfg* cfg, const Cnn& c, const uint8_t* frames,
 
   // 1: area sums
   if (int rc = mark(0)) return rc;
-  AreaPlan ap;
-  if (int rc = make_area_plan(cfg->in_h, cfg->in_w, cfg->frame_stride, frames, cfg->dd_h,
-                              cfg->dd_w, n, &ap))
-    return rc;
+  AreaPlan ap{};
+  if (frames)
+    if (int rc = make_area_plan(cfg->in_h, cfg->in_w, cfg->frame_stride, frames, cfg->dd_h,
+                                cfg->dd_w, n, &ap))
+      return rc;
   // 2: detector (against a fixed reference image fused into step 1, its
   // partial sums added up by a finishing kernel, when the plan allows)
   {
@@ -795,12 +821,15 @@ int run_checked(const nsc_cascade_cfg* cfg, const Cnn& c, const uint8_t* frames,
     a.score = score_out;
     a.fire = fire;
     int64_t* part = reinterpret_cast<int64_t*>(w + L.part);
-    const bool fused = area_detect_fused(ap, a) && L.part_units > 0 &&
+    const bool fused = frames && area_detect_fused(ap, a) && L.part_units > 0 &&
                        area_detect_part_count(ap, n) <= L.part_units;
     PrevFusePlan fp;
-    const bool fused_prev = !fused && L.part_units > 0 && area_prev_plan(ap, a, n, &fp) &&
-                            fp.part_elems <= L.part_units;
-    if (fused_prev) {
+    const bool fused_prev = frames && !fused && L.part_units > 0 &&
+                            area_prev_plan(ap, a, n, &fp) && fp.part_elems <= L.part_units;
+    if (!frames) {
+      if (int rc = mark(1)) return rc;
+      if (int rc = launch_diff(a, st)) return rc;
+    } else if (fused_prev) {
       if (int rc = launch_area_prev(fp, frames, cfg->frame_stride, n, sums, a, part, st)) return rc;
       if (int rc = mark(1)) return rc;
       area_prev_diff_args(fp, part, &a);
@@ -839,7 +868,19 @@ int run_checked(const nsc_cascade_cfg* cfg, const Cnn& c, const uint8_t* frames,
   r.c_low = cfg->c_low;
   r.c_high = cfg->c_high;
   r.frame_logit = logit_out;
-  if (int rc = run_cnn(c, r, w + L.cnn, L.total - L.cnn, st)) return rc;
+  const int64_t pass = cnn_pass > 0 && cnn_pass < n ? cnn_pass : n;
+  for (int64_t p0 = 0; p0 < n; p0 += pass) {
+    if (pass < n) {
+      // slots [p0, p0 + m) of the compacted list; the pass's count in count[1]
+      const int64_t m = n - p0 < pass ? n - p0 : pass;
+      if (int rc = launch_pass_count(count, p0, m, count + 1, st)) return rc;
+      r.idx = idx + p0;
+      r.count = count + 1;
+      r.max_count = m;
+      r.logit = reinterpret_cast<float*>(w + L.logit) + p0;
+    }
+    if (int rc = run_cnn(c, r, w + L.cnn, L.total - L.cnn, st)) return rc;
+  }
   if (int rc = mark(4)) return rc;
   // 5: decisions of frames that did not fire
   const ResolvePlan rp = make_resolve_plan(n, t0, prev ? cfg->delta : 1);
@@ -898,7 +939,7 @@ int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_
   if (s == 1) {
     if (int rc = run_checked(cfg, c, frames, n, t0, state, w, L, label_out, defer_out,
                              outs ? outs->score : nullptr, outs ? outs->fire : nullptr,
-                             outs ? outs->logit : nullptr, st, mark))
+                             outs ? outs->logit : nullptr, 0, st, mark))
       return rc;
   } else {
     // the checked frames [k0, k0 + nc) as a video of their own, then every frame
@@ -914,7 +955,7 @@ int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_
     if (nc > 0) {
       const uint8_t* kf = frames + (k0 * s - t0) * cfg->frame_stride;
       if (int rc = run_checked(&kc, c, kf, nc, k0, state, w, L, k_label, k_defer, k_score, k_fire,
-                               k_logit, st, mark))
+                               k_logit, 0, st, mark))
         return rc;
     } else {
       for (int k = 0; k < 5; ++k)
@@ -942,20 +983,113 @@ int nsc_cascade_run(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, const uint8_
     if (int rc = launch_skip_expand(e, st)) return rc;
   }
   if (int rc = mark(5)) return rc;
-  if (stats) {
-    std::vector<uint8_t> hl(n), hd(n);
-    int32_t hc = 0;
-    NSC_TRY_HIP(hipMemcpyAsync(hl.data(), label_out, n, hipMemcpyDeviceToHost, st));
-    NSC_TRY_HIP(hipMemcpyAsync(hd.data(), defer_out, n, hipMemcpyDeviceToHost, st));
-    NSC_TRY_HIP(hipMemcpyAsync(&hc, count, 4, hipMemcpyDeviceToHost, st));
-    NSC_TRY_HIP(hipStreamSynchronize(st));
-    nsc_run_stats r{n, hc, 0, 0};
-    for (int64_t i = 0; i < n; ++i) {
-      r.positive += hl[i] && !hd[i];
-      r.deferred += hd[i];
-    }
-    *stats = r;
+  if (stats) return run_stats(label_out, defer_out, count, n, st, stats);
+  return NSC_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------- batches of staged chunks
+
+namespace nsc {
+namespace {
+
+// Default bound on the survivors of one CNN pass in a staged batch.
+constexpr int64_t kBatchCnnPass = 16384;
+
+int64_t batch_cnn_pass(int64_t batch_frames, int64_t cnn_pass) {
+  const int64_t p = cnn_pass > 0 ? cnn_pass : kBatchCnnPass;
+  return p < batch_frames ? p : batch_frames;
+}
+
+int check_batch(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, int64_t batch_frames,
+                int64_t cnn_pass) {
+  if (int rc = check_cfg(cfg)) return rc;
+  NSC_REQUIRE(cnn != nullptr, NSC_E_INVAL, "cnn is NULL");
+  NSC_REQUIRE(cnn->c.desc.in_h == cfg->cnn_h && cnn->c.desc.in_w == cfg->cnn_w, NSC_E_SHAPE,
+              "CNN input %dx%d differs from the configured %dx%d", cnn->c.desc.in_h,
+              cnn->c.desc.in_w, cfg->cnn_h, cfg->cnn_w);
+  NSC_REQUIRE(stride_of(cfg) == 1, NSC_E_INVAL, "a staged batch needs check_stride 1, got %d",
+              cfg->check_stride);
+  NSC_REQUIRE(batch_frames > 0 && batch_frames <= kMaxFrames && cnn_pass >= 0, NSC_E_INVAL,
+              "batch_frames %lld or cnn_pass %lld out of range", (long long)batch_frames,
+              (long long)cnn_pass);
+  return NSC_OK;
+}
+
+}  // namespace
+}  // namespace nsc
+
+extern "C" {
+
+int nsc_batch_workspace_bytes(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, int64_t batch_frames,
+                              int64_t cnn_pass, size_t* bytes) {
+  g_err[0] = 0;
+  if (int rc = check_batch(cfg, cnn, batch_frames, cnn_pass)) return rc;
+  NSC_REQUIRE(bytes != nullptr, NSC_E_INVAL, "bytes is NULL");
+  *bytes = run_layout(cfg, cnn->c, batch_frames, batch_cnn_pass(batch_frames, cnn_pass), true).total;
+  return NSC_OK;
+}
+
+int nsc_cascade_stage(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, int64_t batch_frames,
+                      int64_t cnn_pass, const uint8_t* frames, int64_t n, int64_t at, void* ws,
+                      size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  if (int rc = check_batch(cfg, cnn, batch_frames, cnn_pass)) return rc;
+  NSC_REQUIRE(n >= 0 && at >= 0 && at + n <= batch_frames, NSC_E_INVAL,
+              "slots [%lld, %lld) outside the batch of %lld", (long long)at,
+              (long long)(at + n), (long long)batch_frames);
+  if (n == 0) return NSC_OK;
+  NSC_REQUIRE(frames != nullptr, NSC_E_INVAL, "frames is NULL");
+  const RunLayout L =
+      run_layout(cfg, cnn->c, batch_frames, batch_cnn_pass(batch_frames, cnn_pass), true);
+  NSC_REQUIRE(ws != nullptr && ((uintptr_t)ws % kAlign) == 0 && ws_bytes >= L.total,
+              NSC_E_WORKSPACE, "workspace needs %zu bytes (256-byte aligned), got %zu", L.total,
+              ws_bytes);
+  AreaPlan ap;
+  if (int rc = make_area_plan(cfg->in_h, cfg->in_w, cfg->frame_stride, frames, cfg->dd_h,
+                              cfg->dd_w, n, &ap))
+    return rc;
+  const int64_t cells = (int64_t)cfg->dd_h * cfg->dd_w * 3;
+  int32_t* sums = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(ws) + L.sums) + at * cells;
+  return launch_area_sums(ap, frames, cfg->frame_stride, n, sums, (hipStream_t)stream);
+}
+
+int nsc_cascade_finish(const nsc_cascade_cfg* cfg, const nsc_cnn* cnn, int64_t batch_frames,
+                       int64_t cnn_pass, int64_t n, int64_t t0, void* state, void* ws,
+                       size_t ws_bytes, uint8_t* label_out, uint8_t* defer_out,
+                       const nsc_frame_outputs* outs, nsc_run_stats* stats,
+                       void* const* stage_events, void* stream) {
+  g_err[0] = 0;
+  if (int rc = check_batch(cfg, cnn, batch_frames, cnn_pass)) return rc;
+  NSC_REQUIRE(n >= 0 && n <= batch_frames && t0 >= 0, NSC_E_INVAL,
+              "n %lld (batch of %lld) or t0 out of range", (long long)n, (long long)batch_frames);
+  auto mark = [&](int k) -> int {
+    if (stage_events && stage_events[k])
+      NSC_TRY_HIP(hipEventRecord((hipEvent_t)stage_events[k], (hipStream_t)stream));
+    return NSC_OK;
+  };
+  if (n == 0) {
+    if (stats) *stats = nsc_run_stats{0, 0, 0, 0};
+    return NSC_OK;
   }
+  NSC_REQUIRE(label_out && defer_out, NSC_E_INVAL, "label_out or defer_out is NULL");
+  NSC_REQUIRE(!(cfg->ref_mode == NSC_REF_PREV && state == nullptr), NSC_E_STATE,
+              "earlier-frame mode needs a state buffer");
+  const int64_t pass = batch_cnn_pass(batch_frames, cnn_pass);
+  const RunLayout L = run_layout(cfg, cnn->c, batch_frames, pass, true);
+  NSC_REQUIRE(ws != nullptr && ((uintptr_t)ws % kAlign) == 0 && ws_bytes >= L.total,
+              NSC_E_WORKSPACE, "workspace needs %zu bytes (256-byte aligned), got %zu", L.total,
+              ws_bytes);
+  const hipStream_t st = (hipStream_t)stream;
+  unsigned char* w = static_cast<unsigned char*>(ws);
+  if (int rc = run_checked(cfg, cnn->c, nullptr, n, t0, state, w, L, label_out, defer_out,
+                           outs ? outs->score : nullptr, outs ? outs->fire : nullptr,
+                           outs ? outs->logit : nullptr, pass, st, mark))
+    return rc;
+  if (int rc = mark(5)) return rc;
+  if (stats)
+    return run_stats(label_out, defer_out, reinterpret_cast<int32_t*>(w + L.count), n, st, stats);
   return NSC_OK;
 }
 

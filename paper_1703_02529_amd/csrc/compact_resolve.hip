@@ -111,6 +111,14 @@ __global__ void __launch_bounds__(kTileThreads) k_tile_scatter(const uint8_t* __
 
 __global__ void k_set_i32(int32_t* p, int32_t v) { *p = v; }
 
+// Survivors of one CNN pass: the slots [off, off + m) of the compacted list
+// that exist, i.e. clamp(*count - off, 0, m).
+__global__ void k_pass_count(const int32_t* __restrict__ count, int64_t off, int64_t m,
+                             int32_t* __restrict__ out) {
+  const int64_t left = (int64_t)*count - off;
+  *out = (int32_t)(left < 0 ? 0 : left < m ? left : m);
+}
+
 // Per-tile last fired local index per residue column (or -1).
 __global__ void __launch_bounds__(256) k_resolve_tile_last(const uint8_t* __restrict__ fire,
                                                            int64_t n, int32_t delta,
@@ -484,6 +492,13 @@ int launch_group_state(const CamDiff* cams, int32_t n_cams, int32_t max_delta,
   hipLaunchKernelGGL(k_group_state, dim3(gx, (unsigned)n_cams), dim3(256), 0, stream, cams, sums,
                      label, defer, n, cells, old, state, state_stride);
   NSC_CHECK_LAUNCH("k_group_state");
+  return NSC_OK;
+}
+
+int launch_pass_count(const int32_t* count, int64_t off, int64_t m, int32_t* out,
+                      hipStream_t stream) {
+  hipLaunchKernelGGL(k_pass_count, dim3(1), dim3(1), 0, stream, count, off, m, out);
+  NSC_CHECK_LAUNCH("k_pass_count");
   return NSC_OK;
 }
 

@@ -183,6 +183,10 @@ int launch_group_state(const CamDiff* cams, int32_t n_cams, int32_t max_delta,
                        int64_t cells, unsigned char* state, int64_t state_stride, void* scratch,
                        hipStream_t stream);
 int launch_set_i32(int32_t* p, int32_t v, hipStream_t stream);
+// *out = clamp(*count - off, 0, m): the survivors of the CNN pass over the
+// compacted slots [off, off + m).
+int launch_pass_count(const int32_t* count, int64_t off, int64_t m, int32_t* out,
+                      hipStream_t stream);
 
 // Frame skipping: frames [t0, t0+n) take the outputs of their checked frame
 // floor(t / s) * s.  Checked frames [k0, k0+nc) (absolute checked indices)

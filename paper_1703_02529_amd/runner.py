@@ -13,7 +13,8 @@ from typing import Optional
 import torch
 
 from . import (NSC_METRIC_MSE, NSC_REF_FIXED, NSC_REF_PREV, Cnn, Group, make_cfg, make_desc,
-               nsc_cascade_run, nsc_cascade_workspace_bytes, nsc_group_run,
+               nsc_batch_workspace_bytes, nsc_cascade_finish, nsc_cascade_run,
+               nsc_cascade_stage, nsc_cascade_workspace_bytes, nsc_group_run,
                nsc_group_state_bytes, nsc_group_workspace_bytes, nsc_state_bytes)
 
 
@@ -27,8 +28,13 @@ def _cfg_of(wl, lr_w=None, ref_sums=None, frame_stride=None):
 
 
 class CascadeRunner:
+    """batch=True sizes the workspace for staged batches of up to max_frames
+    frames (stage() per chunk, then finish()); cnn_pass bounds the survivors
+    of one CNN pass in a batch (0: the library's default)."""
+
     def __init__(self, wl, blob, max_frames: int, lr_w: Optional[torch.Tensor] = None,
-                 ref_sums: Optional[torch.Tensor] = None, device="cuda", frame_stride=None):
+                 ref_sums: Optional[torch.Tensor] = None, device="cuda", frame_stride=None,
+                 batch: bool = False, cnn_pass: int = 0):
         self.wl = wl
         self.device = torch.device(device)
         self.lr_w = lr_w
@@ -38,7 +44,12 @@ class CascadeRunner:
                               wl.cnn.bf16)
         self.cnn = Cnn(self.desc, blob)
         self.max_frames = max_frames
-        ws = nsc_cascade_workspace_bytes(self.cfg, self.cnn, max_frames)
+        self.batch = batch
+        self.cnn_pass = cnn_pass
+        if batch:
+            ws = nsc_batch_workspace_bytes(self.cfg, self.cnn, max_frames, cnn_pass)
+        else:
+            ws = nsc_cascade_workspace_bytes(self.cfg, self.cnn, max_frames)
         self.ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=self.device)
         self.state = torch.zeros(max(nsc_state_bytes(self.cfg), 256), dtype=torch.uint8,
                                  device=self.device)
@@ -59,6 +70,31 @@ class CascadeRunner:
         st = nsc_cascade_run(self.cfg, self.cnn, frames, n, t0, self.state, self.ws,
                              self.label[:n], self.defer[:n], want_stats=want_stats,
                              stage_events=stage_events, stream=stream, **kw)
+        self.next_t = t0 + n
+        return st
+
+    def stage(self, frames: torch.Tensor, n: int, at: int, stream=None):
+        """Area sums of n frames into batch slots [at, at + n)."""
+        if not self.batch:
+            raise ValueError("stage() needs a runner made with batch=True")
+        nsc_cascade_stage(self.cfg, self.cnn, self.max_frames, self.cnn_pass, frames, n, at,
+                          self.ws, stream=stream)
+
+    def finish(self, n: int, t0: Optional[int] = None, label=None, defer=None, score=None,
+               fire=None, logit=None, want_stats: bool = False, stage_events=None, stream=None):
+        """Steps 2-5 on the n staged frames, frames [t0, t0 + n) (default:
+        continue where the last call ended).  Per-frame outputs go to the
+        given device tensors, else to the runner's own buffers."""
+        if not self.batch:
+            raise ValueError("finish() needs a runner made with batch=True")
+        t0 = self.next_t if t0 is None else t0
+        if label is None:
+            label, defer = self.label[:n], self.defer[:n]
+            score, fire, logit = self.score[:n], self.fire[:n], self.logit[:n]
+        st = nsc_cascade_finish(self.cfg, self.cnn, self.max_frames, self.cnn_pass, n, t0,
+                                self.state, self.ws, label, defer, score=score, fire=fire,
+                                logit=logit, want_stats=want_stats, stage_events=stage_events,
+                                stream=stream)
         self.next_t = t0 + n
         return st
 

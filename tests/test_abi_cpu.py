@@ -198,3 +198,18 @@ def test_threshold_sweep_rejects_bad_arguments_on_the_host():
                 nsc.SweepCfg(0, 1, 0.01, 0.01, 0, math.inf, 0)):
         assert L.nsc_threshold_sweep(*args(bad)) == E_INVAL
         assert nsc.last_error()
+
+
+def test_staged_batch_calls_check_on_the_host():
+    """nsc_batch_workspace_bytes, nsc_cascade_stage and nsc_cascade_finish
+    refuse a bad cfg or a NULL network before any device call."""
+    L = nsc.lib()
+    b = ctypes.c_size_t()
+    good, bad = _cfg(), _cfg(delta=0)
+    assert L.nsc_batch_workspace_bytes(ctypes.byref(good), None, 64, 0, ctypes.byref(b)) == -1
+    assert "cnn" in nsc.last_error()
+    assert L.nsc_batch_workspace_bytes(ctypes.byref(bad), None, 64, 0, ctypes.byref(b)) == -1
+    p = ctypes.c_void_p(256)
+    assert L.nsc_cascade_stage(ctypes.byref(good), None, 64, 0, p, 8, 0, p, 1 << 20, None) == -1
+    assert L.nsc_cascade_finish(ctypes.byref(bad), None, 64, 0, 8, 0, p, p, 1 << 20, p, p, None,
+                                None, None, None) == -1
