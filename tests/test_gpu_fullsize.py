@@ -138,18 +138,22 @@ def test_hd_full_length_in_chunks(wl, chunk):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("occ", W.FHD_OCCUPANCIES, ids=lambda o: f"occ{o * 100:g}")
-def test_fhd_1m_streamed(occ):
+@pytest.mark.parametrize("occ,batch", [(o, 1) for o in W.FHD_OCCUPANCIES] +
+                         [(0.01, 8), (0.1, 8)],
+                         ids=lambda v: f"occ{v * 100:g}" if isinstance(v, float) else f"b{v}")
+def test_fhd_1m_streamed(occ, batch):
     """The million-frame 1080p video in chunks of 4096 through two frame buffers
     on two streams (the generator fills one while the cascade reads the other),
-    at each occupancy of the sweep."""
+    at each occupancy of the sweep; with batch 8, each chunk's area sums are
+    staged and the rest of the cascade runs once per 8 chunks (as the
+    benchmark runs it)."""
     wl = W.FHD_STREAM if occ == W.FHD_STREAM.video.occupancy else W.FHD_STREAM.with_occupancy(occ)
     n = wl.video.n
     v = synth.Video(wl.video)
     blob = synth.weight_blob(wl.cnn, synth.cnn_weights(wl.cnn, wl.weight_seed))
     lr = lr_weights_for(wl)
     tables = v.device_tables(DEV)
-    sc = StreamingCascade(wl, blob, wl.chunk, lr_w=torch.from_numpy(lr).to(DEV))
+    sc = StreamingCascade(wl, blob, wl.chunk, lr_w=torch.from_numpy(lr).to(DEV), batch_chunks=batch)
     out = dict(label=torch.empty(n, dtype=torch.uint8, device=DEV),
                defer=torch.empty(n, dtype=torch.uint8, device=DEV),
                score=torch.empty(n, dtype=torch.float64, device=DEV),
@@ -169,7 +173,7 @@ def test_fhd_1m_streamed(occ):
     ts = sorted(set(_sample_times(v, 0, n, rng, k=200)) |
                 {wl.chunk, wl.chunk + wl.delta - 1, 100 * wl.chunk + 7, n - 1})
     errs = check_samples(wl, v, blob, lr, None, g, ts)
-    print(dict(frames=n, chunks=st["chunks"], fired=int(g["fire"].sum()),
+    print(dict(frames=n, chunks=st["chunks"], batches=st.get("batches"), fired=int(g["fire"].sum()),
                cascade_ms=round(st["cascade_ms"], 1), wall_ms=round(st["wall_ms"], 1),
                sampled=len(ts), **errs.as_dict()))
     del out
