@@ -74,21 +74,22 @@ AREA_KERNEL = "k_area_sums_wave"
 
 def area_kernel(wl) -> str:
     """The area kernel a workload's cascade runs: against an earlier frame at
-    least two frames back with the MSE metric and 16-byte lane chunks, the one
-    with the detector fused in (k_area_prev_wave); otherwise k_area_sums_wave
-    (which fuses the global detector against a fixed reference image)."""
+    least two frames back with the global MSE metric and 16-byte lane chunks,
+    the one with the detector fused in (k_area_prev_wave); otherwise
+    k_area_sums_wave (which fuses the global detector against a fixed
+    reference image)."""
     delta = wl.delta // max(1, getattr(wl, "check_stride", 1))  # in checked frames
     if wl.ref_mode == 0 and delta >= 2 and getattr(wl, "metric", 0) == 0 and \
-            lane_chunk_bytes(wl.video.w, wl.dd_w) == 16:
+            tuple(wl.grid) == (1, 1) and lane_chunk_bytes(wl.video.w, wl.dd_w) == 16:
         return "k_area_prev_wave"
     return AREA_KERNEL
 
 
 def lane_chunk_bytes(w: int, wo: int) -> int:
     """Bytes one lane of the area kernel reads per source row for rows of w
-    pixels (16-byte aligned) resampled to wo columns: 32 where whole periods
-    of the column pattern in 32-byte chunks leave more than two more lanes of
-    a wave busy than in 16-byte chunks, else 16 (the library's plan)."""
+    pixels (16-byte aligned) resampled to wo columns: 16, or 32 where whole
+    periods of the column pattern in 16-byte chunks leave more than a fifth
+    of a wave's lanes idle and 32-byte chunks fewer (the library's plan)."""
     import math
     px = w // math.gcd(w, wo)
     best_cb, best_used = 0, 0
@@ -100,7 +101,7 @@ def lane_chunk_bytes(w: int, wo: int) -> int:
         if glanes > 64 or w % (px * k):
             continue
         used = 64 // glanes * glanes
-        if used > best_used + 2:
+        if best_cb == 0 or (5 * best_used < 4 * 64 and used > best_used):
             best_cb, best_used = cb, used
     return best_cb
 AREA_SOURCES = ("paper_1703_02529_amd/csrc/area_diff.hip", "paper_1703_02529_amd/csrc/nsc_internal.h")

@@ -413,28 +413,25 @@ __global__ void __launch_bounds__(256) k_area_sums_wave(const uint8_t* __restric
   }
 }
 
-// The earlier-frame MSE detector fused into the area kernel by temporal
-// tiling along the reuse distance delta: a wave owns one (band, strip) of the
-// R frames f_i = r + delta (sg R + i), i = 0 .. R-1, of chain (sg, r), so
-// that while it forms the sums of f_i its LDS block still holds those of
-// f_(i-1) = f_i - delta, and each value's squared difference is added as the
-// new value replaces the old one.  For every chain frame after the first the
-// wave writes its partial sums of squared differences (exact int64): one
-// (global score) or one per block column its strip touches (BLK: bands are
-// the block rows), at part[(f * bands + band) * strips + strip] or
-// part[((f * bands + band) * grid_w + bx) * strips + strip].  The first frame
-// of a chain, whose frame f - delta is another wave's (or in the state), is
-// scored from the sums by k_diff afterwards, which also adds up the partials
-// of the other frames.  Sums stores and the LDS layout are those of
+// The earlier-frame global MSE detector fused into the area kernel by
+// temporal tiling along the reuse distance delta: a wave owns one (band,
+// strip) of the R frames f_i = r + delta (sg R + i), i = 0 .. R-1, of chain
+// (sg, r), so that while it forms the sums of f_i its LDS block still holds
+// those of f_(i-1) = f_i - delta, and each value's squared difference is
+// added as the new value replaces the old one.  For every chain frame after
+// the first the wave writes its partial sum of squared differences (exact
+// int64) at part[(f * bands + band) * strips + strip].  The first frame of a
+// chain, whose frame f - delta is another wave's (or in the state), is scored
+// from the sums by k_diff afterwards, which also adds up the partials of the
+// other frames.  Sums stores and the LDS layout are those of
 // k_area_sums_wave.
 constexpr int kPrevSlots = 4;  // values per lane and row (at most 256 per strip row)
 
-template <int CB, bool PACKED, int RB, bool BLK>
+template <int CB, bool PACKED, int RB>
 __global__ void __launch_bounds__(256) k_area_prev_wave(const uint8_t* __restrict__ frames,
                                                         int64_t stride, Axis ay, Axis ax,
                                                         WaveGeom g, int64_t n, int32_t delta,
-                                                        int32_t R, int32_t grid_w,
-                                                        int32_t* __restrict__ sums,
+                                                        int32_t R, int32_t* __restrict__ sums,
                                                         int64_t* __restrict__ part) {
   using cell_t = typename std::conditional<PACKED, uint16_t, int32_t>::type;
   extern __shared__ __align__(16) unsigned char smem[];
@@ -468,19 +465,11 @@ __global__ void __launch_bounds__(256) k_area_prev_wave(const uint8_t* __restric
   const int group0 = strip * g.groups_per_wave;
   const int ngroups = min(g.groups_per_wave, g.groups_per_row - group0);
   const int nl = ngroups * g.group_lanes;  // active lanes
-  const int ncols = ngroups * g.group_cols;
-  const int ncells = ncols * 3;
+  const int ncells = ngroups * g.group_cols * 3;
   const int X0 = group0 * g.group_cols;
   const int Y0 = (int)((int64_t)band * Ho / bands);
   const int Y1 = (int)((int64_t)(band + 1) * Ho / bands);
   const int64_t row_bytes = (int64_t)ax.n_in * 3;
-  // block column of each of this lane's value slots, and the strip's range
-  int bxs[kPrevSlots];
-#pragma unroll
-  for (int k = 0; k < kPrevSlots; ++k)
-    bxs[k] = BLK ? ((X0 + (lane + 64 * k) / 3 + 1) * grid_w - 1) / Wo : 0;
-  const int bx_lo = BLK ? ((X0 + 1) * grid_w - 1) / Wo : 0;
-  const int bx_hi = BLK ? ((X0 + ncols) * grid_w - 1) / Wo : 0;
   for (int i = 0; i < R; ++i) {
     const int64_t f = (sg * R + i) * delta + r;
     if (f >= n) break;
@@ -507,21 +496,11 @@ __global__ void __launch_bounds__(256) k_area_prev_wave(const uint8_t* __restric
       for (int t = lane; t < ncells; t += 64) orow[t] = srow[t];
     }
     if (!diff) continue;
-    if constexpr (!BLK) {
-      int64_t v = 0;
+    int64_t v = 0;
 #pragma unroll
-      for (int k = 0; k < kPrevSlots; ++k) v += e[k];
-      v = wave_sum_i64(v);
-      if (lane == 0) part[(f * bands + band) * strips + strip] = v;
-    } else {
-      for (int bc = bx_lo; bc <= bx_hi; ++bc) {
-        int64_t v = 0;
-#pragma unroll
-        for (int k = 0; k < kPrevSlots; ++k) v += bxs[k] == bc ? e[k] : 0;
-        v = wave_sum_i64(v);
-        if (lane == 0) part[((f * bands + band) * grid_w + bc) * strips + strip] = v;
-      }
-    }
+    for (int k = 0; k < kPrevSlots; ++k) v += e[k];
+    v = wave_sum_i64(v);
+    if (lane == 0) part[(f * bands + band) * strips + strip] = v;
   }
 }
 
@@ -678,45 +657,18 @@ __device__ __forceinline__ double frame_score(const int32_t* cur, const int32_t*
   return z;
 }
 
-// The MSE score of frame i from the fused kernel's partial sums (exact
-// integers, so their grouping does not matter): the global score, or the
-// logistic score of the per-block MSEs in block order, each as frame_score
+// The global MSE score of frame i from the fused kernel's partial sums
+// (exact integers, so their grouping does not matter), as frame_score
 // computes it from the sums.
-template <bool BLK>
 __device__ __forceinline__ double part_score(const DiffArgs& a, int64_t i, int lane) {
 #pragma clang fp contract(off)
-  const int bands = a.part_bands, strips = a.part_strips;
-  if (!BLK || a.grid_h * a.grid_w == 1) {
-    const int64_t* p = a.part + i * bands * strips;
-    int64_t e = 0;
-    for (int u = lane; u < bands * strips; u += 64) e += p[u];
-    DiffSums<NSC_METRIC_MSE> acc;
-    acc.e = wave_sum_i64(e);
-    return acc.value(a, (double)((int64_t)a.dd_h * a.dd_w * 3));
-  }
-  if constexpr (!BLK) return 0.0;
-  const int gw = a.grid_w;
-  double z = a.lr_b;
-  for (int by = 0; by < a.grid_h; ++by) {
-    double m = 0.0;
-    if (lane < gw) {
-      const int x0 = (int)((int64_t)lane * a.dd_w / gw);
-      const int x1 = (int)((int64_t)(lane + 1) * a.dd_w / gw);
-      const int64_t* p = a.part + ((i * bands + by) * gw + lane) * strips;
-      int64_t e = 0;
-      for (int s = 0; s < strips; ++s) {
-        const int X0 = s * a.strip_cols, X1 = min(X0 + a.strip_cols, a.dd_w);
-        if (X0 < x1 && x0 < X1) e += p[s];
-      }
-      const int y0 = (int)((int64_t)by * a.dd_h / a.grid_h);
-      const int y1 = (int)((int64_t)(by + 1) * a.dd_h / a.grid_h);
-      DiffSums<NSC_METRIC_MSE> b;
-      b.e = e;
-      m = b.value(a, ((double)(y1 - y0) * (double)(x1 - x0)) * 3.0);
-    }
-    for (int bx = 0; bx < gw; ++bx) z = z + (double)a.lr_w[by * gw + bx] * __shfl(m, bx, 64);
-  }
-  return z;
+  const int units = a.part_bands * a.part_strips;
+  const int64_t* p = a.part + i * units;
+  int64_t e = 0;
+  for (int u = lane; u < units; u += 64) e += p[u];
+  DiffSums<NSC_METRIC_MSE> acc;
+  acc.e = wave_sum_i64(e);
+  return acc.value(a, (double)((int64_t)a.dd_h * a.dd_w * 3));
 }
 
 // The fixed-reference detector fused into the area kernel: a thread per
@@ -750,10 +702,10 @@ __global__ void __launch_bounds__(256) k_diff(DiffArgs a) {
   const int64_t cells = (int64_t)a.dd_h * a.dd_w * 3;
   const bool forced = a.ref_mode == NSC_REF_PREV && t < a.delta;
   double score = INFINITY;
-  const bool from_part =
-      M == NSC_METRIC_MSE && a.part != nullptr && !forced && (i / a.delta) % a.chain_r != 0;
+  const bool from_part = M == NSC_METRIC_MSE && !BLK && a.part != nullptr && !forced &&
+                         (i / a.delta) % a.chain_r != 0;
   if (from_part) {
-    score = part_score<BLK>(a, i, lane);
+    score = part_score(a, i, lane);
   } else if (!forced) {
     const int32_t* cur = a.sums + i * cells;
     const int32_t* ref;
@@ -830,9 +782,13 @@ int make_area_plan(int32_t in_h, int32_t in_w, int64_t stride, const void* frame
   if (p.threads < 64) p.threads = 64;
   // vertical column sums reach 255 * p_y; 16-bit packing is exact below 65536
   p.packed = 255LL * p.ay.p < 65536;
-  // wave strips: whole periods of the horizontal pattern in 32/16/4-byte
-  // chunks; 32-byte chunks (two 16-byte loads per lane) where they leave
-  // fewer lanes of a wave idle
+  // wave strips: whole periods of the horizontal pattern in 16/4-byte
+  // chunks; 32-byte chunks (two 16-byte loads per lane) only where 16-byte
+  // ones leave more than a fifth of a wave's lanes idle.  (1920x1080 ->
+  // 100x100, 54 of 64 lanes busy in 16-byte chunks against 63 in 32-byte
+  // ones: 16-byte chunks 3.3 % faster; 1280x720 -> 50x50, 48 against 60:
+  // 32-byte chunks 3 % faster; area kernels alone, alternating in one
+  // process.)
   p.wave = false;
   if (p.chunk_bytes != 1) {
     int best_cb = 0, best_used = 0;
@@ -846,7 +802,7 @@ int make_area_plan(int32_t in_h, int32_t in_w, int64_t stride, const void* frame
       const int64_t gpix = (int64_t)p.ax.p * k;
       if (glanes > 64 || in_w % gpix != 0) continue;
       const int used = (int)(64 / glanes * glanes);
-      if (used > best_used + 2) {  // 32-byte chunks only for a clear gain
+      if (best_cb == 0 || (5 * best_used < 4 * 64 && used > best_used)) {
         best_used = used;
         best_cb = cb;
         best_glanes = glanes;
@@ -977,31 +933,23 @@ int launch_diff(const DiffArgs& a, hipStream_t stream) {
 
 bool area_prev_plan(const AreaPlan& p, const DiffArgs& a, int64_t n, PrevFusePlan* out) {
   // Measured against the two passes (whole cascade per call, alternating
-  // order in one process): with 16-byte lane chunks the fused kernel keeps
-  // the two-pass kernel's four waves per SIMD and is as fast (640x480, delta
-  // 15: within 0.1 %); with 32-byte chunks it needs 126 registers against
-  // 102 (four waves per SIMD instead of five) and is 3 % slower (1920x1080,
-  // delta 30, blocked; 2.4 % with chains of two frames); against the frame
-  // just before (delta = 1, chains of consecutive frames) 3.5 % slower on
-  // 720p blocked.  So it is taken with 16-byte chunks from delta = 2 on.
+  // order in one process): with 16-byte lane chunks and a global score the
+  // fused kernel is as fast (640x480, delta 15: within 0.3 %); with 32-byte
+  // chunks it needs 126 registers against 102 (four waves per SIMD instead
+  // of five) and was 3 % slower (1920x1080, delta 30, blocked); against the
+  // frame just before (delta = 1) 3.5 % slower on 720p blocked; and a
+  // blocked score, which needs a band per block row, 9.7 % slower at
+  // 1920x1080, delta 30 (bands of 10 rows instead of 2, frames of a chain
+  // far apart).  So it is taken for a global score with 16-byte or smaller
+  // chunks from delta = 2 on.
   if (!p.wave || p.wg.chunk_bytes == 32 || a.ref_mode != NSC_REF_PREV ||
-      a.metric != NSC_METRIC_MSE || a.cams != nullptr || a.delta < 2 || n < 2 * (int64_t)a.delta)
+      a.metric != NSC_METRIC_MSE || a.cams != nullptr || a.delta < 2 ||
+      n < 2 * (int64_t)a.delta || a.grid_h * a.grid_w != 1)
     return false;
-  const bool blk = a.grid_h * a.grid_w > 1;
-  if (blk && (a.grid_w > 64 || a.grid_h > p.ay.n_out)) return false;
-  AreaPlan q = p;
-  WaveGeom& g = q.wg;
+  const AreaPlan& q = p;
+  const WaveGeom& g = q.wg;
   const int64_t scols = (int64_t)g.groups_per_wave * g.group_cols;
   if (scols * 3 > 64 * kPrevSlots) return false;
-  if (blk) {  // one band per block row
-    g.bands = a.grid_h;
-    g.band_rows = (p.ay.n_out + a.grid_h - 1) / a.grid_h;
-    const int64_t cellb = q.packed ? 2 : 4;
-    const int64_t per_wave =
-        (64 * g.chunk_bytes * cellb + (int64_t)g.band_rows * scols * 3 * 4 + 15) & ~(int64_t)15;
-    g.lds_bytes = (size_t)(scols * 16 + g.waves_per_block * per_wave);
-    if (g.lds_bytes > 64 * 1024) return false;
-  }
   // chains of R frames, as long as the launch keeps about 8 rounds of the
   // chip's resident waves (18 per CU) busy, between 2 and 16 frames
   const int64_t units = n * g.bands * g.waves_per_frame;
@@ -1012,7 +960,7 @@ bool area_prev_plan(const AreaPlan& p, const DiffArgs& a, int64_t n, PrevFusePla
   if (R < 2) R = 2;
   out->ap = q;
   out->chain_r = (int32_t)R;
-  out->part_elems = n * g.bands * g.waves_per_frame * (blk ? a.grid_w : 1);
+  out->part_elems = n * g.bands * g.waves_per_frame;
   return true;
 }
 
@@ -1025,26 +973,17 @@ int launch_area_prev(const PrevFusePlan& fp, const uint8_t* frames, int64_t stri
   const int64_t units = chains * g.bands * g.waves_per_frame;
   const int64_t wblocks = (units + g.waves_per_block - 1) / g.waves_per_block;
   if (wblocks > 0x7FFFFFFF) return fail(NSC_E_SHAPE, "too many frames in one call");
-  const bool blk = a.grid_h * a.grid_w > 1;
-#define NSC_PREV_LAUNCH(CB, PK, B)                                                               \
-  hipLaunchKernelGGL((k_area_prev_wave<CB, PK, CB == 32 ? NSC_ROWS_BATCH / 2 : NSC_ROWS_BATCH, B>), \
-                     dim3((unsigned)wblocks), dim3(64 * g.waves_per_block), g.lds_bytes, stream,  \
-                     frames, stride, fp.ap.ay, fp.ap.ax, g, n, a.delta, fp.chain_r, a.grid_w, sums, \
-                     part)
-#define NSC_PREV_CB(B)                                                                           \
-  if (g.chunk_bytes == 32) {                                                                     \
-    if (fp.ap.packed) NSC_PREV_LAUNCH(32, true, B); else NSC_PREV_LAUNCH(32, false, B);          \
-  } else if (g.chunk_bytes == 16) {                                                              \
-    if (fp.ap.packed) NSC_PREV_LAUNCH(16, true, B); else NSC_PREV_LAUNCH(16, false, B);          \
-  } else {                                                                                       \
-    if (fp.ap.packed) NSC_PREV_LAUNCH(4, true, B); else NSC_PREV_LAUNCH(4, false, B);            \
-  }
-  if (blk) {
-    NSC_PREV_CB(true)
+  if (g.chunk_bytes != 16 && g.chunk_bytes != 4)
+    return fail(NSC_E_SHAPE, "the fused earlier-frame detector takes 16- or 4-byte lane chunks");
+#define NSC_PREV_LAUNCH(CB, PK)                                                                  \
+  hipLaunchKernelGGL((k_area_prev_wave<CB, PK, NSC_ROWS_BATCH>), dim3((unsigned)wblocks),        \
+                     dim3(64 * g.waves_per_block), g.lds_bytes, stream, frames, stride, fp.ap.ay,   \
+                     fp.ap.ax, g, n, a.delta, fp.chain_r, sums, part)
+  if (g.chunk_bytes == 16) {
+    if (fp.ap.packed) NSC_PREV_LAUNCH(16, true); else NSC_PREV_LAUNCH(16, false);
   } else {
-    NSC_PREV_CB(false)
+    if (fp.ap.packed) NSC_PREV_LAUNCH(4, true); else NSC_PREV_LAUNCH(4, false);
   }
-#undef NSC_PREV_CB
 #undef NSC_PREV_LAUNCH
   NSC_CHECK_LAUNCH("k_area_prev_wave");
   return NSC_OK;
@@ -1055,7 +994,6 @@ void area_prev_diff_args(const PrevFusePlan& fp, const int64_t* part, DiffArgs* 
   a->chain_r = fp.chain_r;
   a->part_bands = fp.ap.wg.bands;
   a->part_strips = fp.ap.wg.waves_per_frame;
-  a->strip_cols = fp.ap.wg.groups_per_wave * fp.ap.wg.group_cols;
 }
 
 bool area_detect_fused(const AreaPlan& p, const DiffArgs& a) {

@@ -119,18 +119,18 @@ struct DiffArgs {
   int64_t per_cam;
   const unsigned char* state;
   int64_t state_stride;
-  // earlier-frame MSE detector fused into the area kernel (k_area_prev_wave):
-  // frames whose index i has (i / delta) mod chain_r != 0 take their score
-  // from the partial sums (part_bands bands x part_strips strips of
-  // strip_cols output columns, per block column when blocked); the others
-  // from the sums.  part == null: every frame from the sums.
+  // earlier-frame global MSE detector fused into the area kernel
+  // (k_area_prev_wave): frames whose index i has (i / delta) mod chain_r != 0
+  // take their score from the partial sums (part_bands bands x part_strips
+  // strips per frame); the others from the sums.  part == null: every frame
+  // from the sums.
   const int64_t* part;
-  int32_t chain_r, part_bands, part_strips, strip_cols;
+  int32_t chain_r, part_bands, part_strips;
 };
 int launch_diff(const DiffArgs& a, hipStream_t stream);
-// The earlier-frame MSE detector fused into the area kernel: whether it
-// applies to a call of n frames, and then its plan (bands = block rows when
-// blocked), chain length and partial-sum count.
+// The earlier-frame global MSE detector fused into the area kernel: whether
+// it applies to a call of n frames, and then its plan, chain length and
+// partial-sum count.
 struct PrevFusePlan {
   AreaPlan ap;
   int32_t chain_r;

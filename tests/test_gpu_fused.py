@@ -89,16 +89,19 @@ def test_fused_fixed_detector(H, W, Ho, Wo, metric):
 # ------------------------------------------------------------ earlier frame
 
 @pytest.mark.parametrize("H,W,Ho,Wo,grid,delta,chunks", [
-    (480, 640, 50, 50, (1, 1), 2, [37, 9, 30]),         # 16-byte lane chunks, global
-    (480, 640, 50, 50, (5, 5), 3, [50, 26]),            # 16-byte lane chunks, blocked
-    (1080, 1920, 100, 100, (10, 10), 7, [36, 22]),      # 32-byte lane chunks, blocked
-    (720, 1280, 100, 100, (3, 7), 4, [40]),             # uneven block grid
-    (100, 100, 50, 50, (1, 1), 5, [64, 11, 25]),        # 4-byte lane chunks, global
+    (480, 640, 50, 50, (1, 1), 2, [37, 9, 30]),         # 16-byte lane chunks, global: fused
+    (1080, 1920, 100, 100, (1, 1), 7, [36, 22]),        # 16-byte lane chunks, global: fused
+    (100, 100, 50, 50, (1, 1), 5, [64, 11, 25]),        # 4-byte lane chunks, global: fused
+    (720, 1280, 50, 50, (1, 1), 3, [30, 20]),           # 32-byte lane chunks: two passes
+    (480, 640, 50, 50, (5, 5), 3, [50, 26]),            # blocked: two passes
+    (1080, 1920, 100, 100, (10, 10), 7, [36, 22]),      # blocked: two passes
+    (720, 1280, 100, 100, (3, 7), 4, [40]),             # uneven block grid: two passes
 ])
 def test_fused_prev_detector(H, W, Ho, Wo, grid, delta, chunks):
-    """The MSE detector against frame t - delta fused into the area kernel
-    (chains of frames delta apart, partial sums; each chain's first frame from
-    the sums), as nsc_cascade_run runs it over consecutive calls, against
+    """The MSE detector against frame t - delta as nsc_cascade_run runs it
+    over consecutive calls: for a global score with 16- or 4-byte lane chunks
+    fused into the area kernel (chains of frames delta apart, partial sums;
+    each chain's first frame from the sums), otherwise in two passes; against
     the two-pass scores of one nsc_diff_detect call over all frames and the
     oracle: bit-identical scores, identical fire flags."""
     n = sum(chunks)

@@ -65,7 +65,7 @@ def test_device_renderer_odd_frame_size():
     (480, 640, 50, 50, 48),     # padded frame stride
     (720, 1280, 100, 100, 0),
     (720, 1280, 50, 50, 0),     # 32-byte lane chunks (two 16-byte loads per lane)
-    (1080, 1920, 100, 100, 0),  # 32-byte lane chunks
+    (1080, 1920, 100, 100, 0),  # 16-byte lane chunks, 54 of 64 lanes
     (1080, 1920, 50, 50, 32),   # padded stride, 16-byte chunks
     (33, 17, 5, 4, 0),          # 1-byte chunks, ragged
     (600, 64, 2, 16, 0),        # 300 source rows per output row: unpacked sums
