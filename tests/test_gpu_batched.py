@@ -20,7 +20,7 @@ from paper_1703_02529_amd.runner import CascadeRunner
 from paper_1703_02529_amd.streaming import StreamingCascade
 from synth import workloads as W
 
-from helpers import check_properties, compare_cascade, lr_weights_for
+from helpers import check_properties, check_samples, compare_cascade, lr_weights_for
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -172,6 +172,43 @@ def test_batched_cnn_passes_against_oracle():
     rep = compare_cascade(wl, g, ref, t0=0)
     assert rep["fired"] > 64
     print(rep)
+
+
+def test_batched_million_frames():
+    """1,048,583 frames of the 100x100 video staged in 17 chunks of up to
+    65,536 and finished in one call: compaction over a million fire flags, the
+    CNN in 65 passes of up to 16,384 survivors (most of them empty), label
+    chains of the whole video.  Sampled frames against the oracle, properties
+    over every frame."""
+    chunk = 65536
+    wl = W.TINY.with_frames(16 * chunk + 7)
+    n, fb = wl.video.n, wl.video.frame_bytes
+    v, blob = synth.Video(wl.video), _blob(wl)
+    tables = v.device_tables(DEV)
+    run = CascadeRunner(wl, blob, max_frames=n, batch=True)
+    buf = torch.empty(chunk * fb, dtype=torch.uint8, device=DEV)
+    for at in range(0, n, chunk):
+        m = min(chunk, n - at)
+        v.render_device(buf, at, m, tables)
+        run.stage(buf, m, at)
+    st = run.finish(n, t0=0, want_stats=True)
+    g = {k: getattr(run, k)[:n].cpu().numpy() for k in KEYS}
+    run.close()
+    del buf
+    fired = int(g["fire"].sum())
+    assert st["fired"] == fired > 2 * 16384
+    check_properties(wl, g)
+    rng = np.random.default_rng(11)
+    occ = np.flatnonzero(v.occupied)
+    fired_at = np.flatnonzero(g["fire"])
+    # random frames, occupied ones, the ends, and the fired frames that open
+    # and close each CNN pass
+    ts = set(rng.integers(0, n, 120).tolist()) | set(rng.choice(occ, 120, replace=False).tolist())
+    ts |= {0, n - 1} | {int(fired_at[k]) for k in range(0, fired, 16384)}
+    ts |= {int(fired_at[min(k + 16383, fired - 1)]) for k in range(0, fired, 16384)}
+    errs = check_samples(wl, v, blob, None, None, g, sorted(ts))
+    print(dict(frames=n, fired=fired, sampled=len(ts), **errs.as_dict()))
+    torch.cuda.empty_cache()
 
 
 def test_stage_and_finish_check_their_arguments():

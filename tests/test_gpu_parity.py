@@ -152,7 +152,7 @@ def test_diff_detect_parity(case):
 
 # ------------------------------------------------------------- compaction
 
-@pytest.mark.parametrize("n", [0, 1, 63, 64, 65, 4095, 4096, 4097, 12345, 100_000])
+@pytest.mark.parametrize("n", [0, 1, 63, 64, 65, 4095, 4096, 4097, 12345, 100_000, 4_194_305])
 @pytest.mark.parametrize("density", [0.0, 0.013, 0.5, 1.0])
 def test_compact_parity(n, density):
     fire = (rng.random(n) < density).astype(np.uint8)
