@@ -73,14 +73,15 @@ AREA_KERNEL = "k_area_sums_wave"
 
 
 def area_kernel(wl) -> str:
-    """The area kernel a workload's cascade runs: against an earlier frame at
-    least two frames back with the global MSE metric and 16-byte lane chunks,
-    the one with the detector fused in (k_area_prev_wave); otherwise
-    k_area_sums_wave (which fuses the global detector against a fixed
-    reference image)."""
+    """The area kernel a workload's cascade runs: with fuse_prev set, against
+    an earlier frame at least two frames back with the global MSE metric and
+    16-byte lane chunks, the one with the detector fused in
+    (k_area_prev_wave); otherwise k_area_sums_wave (which fuses the global
+    detector against a fixed reference image)."""
     delta = wl.delta // max(1, getattr(wl, "check_stride", 1))  # in checked frames
-    if wl.ref_mode == 0 and delta >= 2 and getattr(wl, "metric", 0) == 0 and \
-            tuple(wl.grid) == (1, 1) and lane_chunk_bytes(wl.video.w, wl.dd_w) == 16:
+    if getattr(wl, "fuse_prev", 0) and wl.ref_mode == 0 and delta >= 2 and \
+            getattr(wl, "metric", 0) == 0 and tuple(wl.grid) == (1, 1) and \
+            lane_chunk_bytes(wl.video.w, wl.dd_w) == 16:
         return "k_area_prev_wave"
     return AREA_KERNEL
 

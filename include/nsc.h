@@ -124,6 +124,15 @@ typedef struct nsc_cascade_cfg {
                                 checked one)                                   */
   int32_t metric;            /* NSC_METRIC_* (0 = MSE); the blocked detector
                                 takes MSE, SAD or NRMSE per block              */
+  int32_t fuse_prev;         /* 0 or 1.  1: PREV with the global MSE metric and
+                                delta >= 2 runs the detector inside the area
+                                kernel by temporal tiling (chains of frames
+                                delta apart, partial sums) where the frame
+                                geometry allows (16- or 4-byte lane chunks);
+                                0: area sums, then the detector as its own
+                                pass.  Same scores bit for bit; 0 measured
+                                6-7 % faster on 640x480 frames.  Ignored by
+                                camera groups and staged batches.              */
 } nsc_cascade_cfg;
 
 /* Shape of a specialized CNN (Sec. 4): n_conv x [conv3x3 'same' + bias + ReLU

@@ -39,7 +39,7 @@ class CascadeCfg(ctypes.Structure):
                 ("dd_w", _i32), ("cnn_h", _i32), ("cnn_w", _i32), ("ref_mode", _i32),
                 ("delta", _i32), ("grid_h", _i32), ("grid_w", _i32), ("lr_w", _vp),
                 ("lr_b", _dbl), ("ref_sums", _vp), ("delta_diff", _dbl), ("c_low", _dbl),
-                ("c_high", _dbl), ("check_stride", _i32), ("metric", _i32)]
+                ("c_high", _dbl), ("check_stride", _i32), ("metric", _i32), ("fuse_prev", _i32)]
 
 
 class CnnDesc(ctypes.Structure):
@@ -151,7 +151,7 @@ def _stream(stream) -> Optional[int]:
 
 def make_cfg(*, in_h, in_w, dd_h, dd_w, cnn_h, cnn_w, ref_mode=NSC_REF_PREV, delta=1,
              grid=(1, 1), lr_w=None, lr_b=0.0, ref_sums=None, delta_diff=0.0, c_low=0.2,
-             c_high=0.8, frame_stride=None, check_stride=1, metric=0) -> CascadeCfg:
+             c_high=0.8, frame_stride=None, check_stride=1, metric=0, fuse_prev=0) -> CascadeCfg:
     """Builds a CascadeCfg; lr_w and ref_sums are device tensors (kept alive by the caller)."""
     c = CascadeCfg()
     c.in_h, c.in_w = in_h, in_w
@@ -165,6 +165,7 @@ def make_cfg(*, in_h, in_w, dd_h, dd_w, cnn_h, cnn_w, ref_mode=NSC_REF_PREV, del
     c.delta_diff, c.c_low, c.c_high = delta_diff, c_low, c_high
     c.check_stride = check_stride
     c.metric = metric
+    c.fuse_prev = fuse_prev
     return c
 
 

@@ -94,6 +94,8 @@ int check_cfg(const nsc_cascade_cfg* c) {
   NSC_REQUIRE(!(c->metric == NSC_METRIC_PSNR && c->grid_h * c->grid_w > 1), NSC_E_INVAL,
               "the blocked detector takes MSE, SAD or NRMSE (an unchanged block's -PSNR is "
               "-inf)");
+  NSC_REQUIRE(c->fuse_prev == 0 || c->fuse_prev == 1, NSC_E_INVAL, "fuse_prev %d is not 0 or 1",
+              c->fuse_prev);
   // exact int64 squared-difference sums (and sums of squared reference values)
   const double emax = (255.0 * (double)den) * (255.0 * (double)den) * (double)c->dd_h * c->dd_w * 3;
   NSC_REQUIRE(emax < 9.0e18, NSC_E_SHAPE, "squared-difference sums may overflow 64 bits");
@@ -281,7 +283,7 @@ RunLayout run_layout(const nsc_cascade_cfg* c0, const Cnn& cnn, int64_t n_frames
   // detector fused into the area kernel: per-unit partial sums, bounded by
   // the plan's units at one output row per band (fixed reference), or by the
   // fused earlier-frame plan's count
-  if (!staged && c->ref_mode == NSC_REF_PREV && c->metric == NSC_METRIC_MSE) {
+  if (!staged && c->fuse_prev && c->ref_mode == NSC_REF_PREV && c->metric == NSC_METRIC_MSE) {
     AreaPlan ap;
     DiffArgs a{};
     a.ref_mode = c->ref_mode;
@@ -824,7 +826,7 @@ int run_checked(const nsc_cascade_cfg* cfg, const Cnn& c, const uint8_t* frames,
     const bool fused = frames && area_detect_fused(ap, a) && L.part_units > 0 &&
                        area_detect_part_count(ap, n) <= L.part_units;
     PrevFusePlan fp;
-    const bool fused_prev = frames && !fused && L.part_units > 0 &&
+    const bool fused_prev = frames && cfg->fuse_prev && !fused && L.part_units > 0 &&
                             area_prev_plan(ap, a, n, &fp) && fp.part_elems <= L.part_units;
     if (!frames) {
       if (int rc = mark(1)) return rc;

@@ -932,16 +932,17 @@ int launch_diff(const DiffArgs& a, hipStream_t stream) {
 }
 
 bool area_prev_plan(const AreaPlan& p, const DiffArgs& a, int64_t n, PrevFusePlan* out) {
-  // Measured against the two passes (whole cascade per call, alternating
-  // order in one process): with 16-byte lane chunks and a global score the
-  // fused kernel is as fast (640x480, delta 15: within 0.3 %); with 32-byte
-  // chunks it needs 126 registers against 102 (four waves per SIMD instead
-  // of five) and was 3 % slower (1920x1080, delta 30, blocked); against the
-  // frame just before (delta = 1) 3.5 % slower on 720p blocked; and a
-  // blocked score, which needs a band per block row, 9.7 % slower at
-  // 1920x1080, delta 30 (bands of 10 rows instead of 2, frames of a chain
-  // far apart).  So it is taken for a global score with 16-byte or smaller
-  // chunks from delta = 2 on.
+  // Where it applies: a global MSE score with 16- or 4-byte lane chunks from
+  // delta = 2 on.  Measured against the two passes (whole cascade per call,
+  // alternating builds in one process): with 32-byte chunks it needs 126
+  // registers against 102 (four waves per SIMD instead of five) and was 3 %
+  // slower (1920x1080, delta 30, blocked); against the frame just before
+  // (delta = 1) 3.5 % slower on 720p blocked; a blocked score, which needs a
+  // band per block row, 9.7 % slower at 1920x1080, delta 30; and since the
+  // area kernel's bands are two rows high, 6-7 % slower than the two passes
+  // on 640x480 too (a chain spreads the frames the resident waves read over
+  // R times as many frames).  The caller takes it only when the
+  // configuration asks for it.
   if (!p.wave || p.wg.chunk_bytes == 32 || a.ref_mode != NSC_REF_PREV ||
       a.metric != NSC_METRIC_MSE || a.cams != nullptr || a.delta < 2 ||
       n < 2 * (int64_t)a.delta || a.grid_h * a.grid_w != 1)

@@ -3,8 +3,8 @@
 Allocates (through torch) the workspace, the carried state and the per-frame
 output buffers, creates the CNN handle, and calls nsc_cascade_run.  It reads a
 workload description by attribute (video.h, video.w, dd_h, dd_w, cnn, ref_mode,
-delta, grid, delta_diff, c_low, c_high, lr_bias; check_stride and metric if
-present) and imports nothing else.
+delta, grid, delta_diff, c_low, c_high, lr_bias; check_stride, metric and
+fuse_prev if present) and imports nothing else.
 """
 from __future__ import annotations
 
@@ -24,7 +24,8 @@ def _cfg_of(wl, lr_w=None, ref_sums=None, frame_stride=None):
                     grid=tuple(wl.grid), lr_w=lr_w, lr_b=wl.lr_bias, ref_sums=ref_sums,
                     delta_diff=wl.delta_diff, c_low=wl.c_low, c_high=wl.c_high,
                     frame_stride=frame_stride, check_stride=getattr(wl, "check_stride", 1),
-                    metric=getattr(wl, "metric", NSC_METRIC_MSE))
+                    metric=getattr(wl, "metric", NSC_METRIC_MSE),
+                    fuse_prev=getattr(wl, "fuse_prev", 0))
 
 
 class CascadeRunner:

@@ -67,6 +67,8 @@ def test_valid_configs_pass():
     (dict(check_stride=4), -1),           # delta 15 is not a multiple of the stride
     (dict(metric=-1), -1),
     (dict(metric=4), -1),
+    (dict(fuse_prev=2), -1),
+    (dict(fuse_prev=-1), -1),
 ])
 def test_invalid_configs(kw, code):
     assert nsc.nsc_cfg_check(_cfg(**kw)) == code

@@ -99,11 +99,11 @@ def test_fused_fixed_detector(H, W, Ho, Wo, metric):
 ])
 def test_fused_prev_detector(H, W, Ho, Wo, grid, delta, chunks):
     """The MSE detector against frame t - delta as nsc_cascade_run runs it
-    over consecutive calls: for a global score with 16- or 4-byte lane chunks
-    fused into the area kernel (chains of frames delta apart, partial sums;
-    each chain's first frame from the sums), otherwise in two passes; against
-    the two-pass scores of one nsc_diff_detect call over all frames and the
-    oracle: bit-identical scores, identical fire flags."""
+    over consecutive calls with fuse_prev set: for a global score with 16- or
+    4-byte lane chunks fused into the area kernel (chains of frames delta
+    apart, partial sums; each chain's first frame from the sums), otherwise in
+    two passes; against the two-pass scores of one nsc_diff_detect call over
+    all frames and the oracle: bit-identical scores, identical fire flags."""
     n = sum(chunks)
     vid = _frames(n, H, W)
     dframes = torch.from_numpy(vid.reshape(-1)).to(DEV)
@@ -120,7 +120,7 @@ def test_fused_prev_detector(H, W, Ho, Wo, grid, delta, chunks):
     two = s2.cpu().numpy()
     fin = two[np.isfinite(two)]
     thr = float(np.median(fin))
-    cfg = nsc.make_cfg(delta_diff=thr, **kw)
+    cfg = nsc.make_cfg(delta_diff=thr, fuse_prev=1, **kw)
     spec = synth.CNNSpec(in_h=Ho, in_w=Wo, conv=(16,), pool=(True,), dense=16, bf16=False)
     blob = synth.weight_blob(spec, synth.cnn_weights(spec, 3))
     cnn = nsc.Cnn(nsc.make_desc(spec.conv, spec.pool, spec.dense, Ho, Wo, False), blob)
