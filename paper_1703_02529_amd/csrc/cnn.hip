@@ -1026,6 +1026,38 @@ __device__ __forceinline__ void stage_band64_f16(const _Float16* __restrict__ sr
 // fences keep the compiler from sinking those loads to their first use.  The
 // hi products of all tiles are issued before the lo products.
 // H: fp16 fragments (one plane, fp16 weights), else bf16 hi / lo pairs.
+// Tiles of a band of a banded layer: 16 output pixels of the band in raster
+// order, or on a pooling layer 4 of its 2x2 windows in raster order (the four
+// pixels of a window in a quad of lanes, for the pooling in the epilogue), so
+// that no tile overhangs the map (a 25 x 25 map in 4 x 4 tiles computes 784
+// pixels for 625).  rows (even when pooling) and wn (the computed columns:
+// the width, even when pooling) bound the band.
+__host__ __device__ inline int band64_ntile(bool pool, int rows, int wn) {
+  return pool ? ((rows >> 1) * (wn >> 1) + 3) >> 2 : (rows * wn + 15) >> 4;
+}
+
+// Band-local output pixel (r, x) of lane m in tile t; false (and (0, 0))
+// past the band's last pixel or window.
+__device__ __forceinline__ bool band_pixel(int t, int m, int pool, int rows, int wn, int& r,
+                                           int& x) {
+  r = 0;
+  x = 0;
+  if (pool) {
+    const int wc = wn >> 1;  // windows per row
+    const int wi = 4 * t + (m >> 2), j = m & 3;
+    if (wi >= (rows >> 1) * wc) return false;
+    const int wr = wi / wc;
+    r = 2 * wr + (j >> 1);
+    x = 2 * (wi - wr * wc) + (j & 1);
+    return true;
+  }
+  const int q = 16 * t + m;
+  if (q >= rows * wn) return false;
+  r = q / wn;
+  x = q - r * wn;
+  return true;
+}
+
 template <bool H> struct Band64Frag { typedef bf16x8 type; };
 template <> struct Band64Frag<true> { typedef f16x8 type; };
 
@@ -1075,8 +1107,8 @@ __device__ __forceinline__ void band64_mma(const Band64Step<MT, NT, H>& st, f32x
 template <int MT, int NT, bool H>
 __device__ __forceinline__ void band64_tiles(const unsigned char* lds, const Band64& b,
                                              const typename Band64Frag<H>::type* __restrict__ wf,
-                                             const int (&tr)[MT], const int (&tc)[MT], int py,
-                                             int px, int g, int lane, f32x4 (&acc)[MT][NT]) {
+                                             const int (&pix)[MT], int g, int lane,
+                                             f32x4 (&acc)[MT][NT]) {
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -1084,7 +1116,7 @@ __device__ __forceinline__ void band64_tiles(const unsigned char* lds, const Ban
   uint32_t base[MT], base_lo[MT];
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
-    base[i] = (uint32_t)(g * b.cp + (4 * tr[i] + py) * b.wb + 4 * tc[i] + px) * 16u;
+    base[i] = (uint32_t)(g * b.cp + pix[i]) * 16u;
     base_lo[i] = base[i] + (uint32_t)b.lo_bytes;
   }
   const uint32_t step2 = (uint32_t)b.cp * 64u;  // chunks 4..7: 4 chunk planes on
@@ -1204,40 +1236,52 @@ __device__ __forceinline__ void band64_epilogue(const f32x4 (&acc)[NT], const fl
   }
 }
 
-// MT tiles of a band: tiles first, first + 4, ... (band-local tile index,
-// tiles_x per tile row), through the epilogue.  out already points at this
-// lane's channel group (4 g).
+// MT tiles of a band: tiles first, first + 4, ... (band-local tile index, see
+// band_pixel), through the epilogue.  out already points at this lane's
+// channel group (4 g).
 template <int MT, int NT, bool H>
 __device__ __forceinline__ void band64_run(const unsigned char* lds, const Band64& b, int ty0,
                                            const typename Band64Frag<H>::type* __restrict__ wf,
                                            const float* __restrict__ bp, float s, float k,
-                                           void* out, int cout, int pool, int tiles_x, int first,
-                                           int py, int px, int m, int g, int lane, bool f16out) {
-  int tr[MT], tc[MT];
+                                           void* out, int cout, int pool, int rows, int wn,
+                                           int first, int m, int g, int lane, bool f16out) {
+  int pix[MT];
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
-    const int t = first + kBandWaves * i;
-    tr[i] = t / tiles_x;
-    tc[i] = t - tr[i] * tiles_x;
+    int r, x;
+    band_pixel(first + kBandWaves * i, m, pool, rows, wn, r, x);
+    pix[i] = r * b.wb + x;  // (0, 0) past the band's last pixel: in bounds
   }
   f32x4 acc[MT][NT];
-  band64_tiles<MT, NT, H>(lds, b, wf, tr, tc, py, px, g, lane, acc);
+  band64_tiles<MT, NT, H>(lds, b, wf, pix, g, lane, acc);
+  // the pixels again, computed only now (an opaque copy of `first` after the
+  // tiles' loads) so that they take no registers through the tiles
+  int first2 = first;
+  asm volatile("" : "+s"(first2) : : "memory");
 #pragma unroll
-  for (int i = 0; i < MT; ++i)
-    band64_epilogue<NT>(acc[i], bp, s, k, out, cout, 4 * (ty0 + tr[i]) + py, 4 * tc[i] + px,
-                        b.h, b.w, pool, m, f16out);
+  for (int i = 0; i < MT; ++i) {
+    int r, x;
+    const bool in = band_pixel(first2 + kBandWaves * i, m, pool, rows, wn, r, x);
+    band64_epilogue<NT>(acc[i], bp, s, k, out, cout, in ? 4 * ty0 + r : b.h, x, b.h, b.w, pool, m,
+                        f16out);  // no store past the band's last pixel
+  }
 }
 
-// One band's work of a 64-input-channel layer: ntile tiles over the 4 waves,
-// at most 4 per wave per round.  sc is the accumulator scale (fp16 path, else
-// 1) and st16 the next layer's input scale when the output is fp16 (else 0).
+// One band's work of a 64-input-channel layer: the band's output rows 4 ty0
+// .. 4 (ty0 + nty) - 1 (those the layer computes) as band64_ntile tiles over
+// the 4 waves, at most MTMAX per wave per round.  sc is the accumulator scale
+// (fp16 path, else 1) and st16 the next layer's input scale when the output
+// is fp16 (else 0).
 template <int NT, bool H>
 __device__ __forceinline__ void band64_layer(const unsigned char* lds, const Band64& b, int ty0,
-                                             int ntile,
+                                             int nty,
                                              const typename Band64Frag<H>::type* __restrict__ wf,
                                              const float* __restrict__ bias, void* out, int cout,
-                                             int pool, int tiles_x, int wave, int py, int px, int m,
-                                             int g, int lane, float sc, float st16) {
+                                             int pool, int wave, int m, int g, int lane, float sc,
+                                             float st16) {
+  const int hn = pool ? (b.h / 2) * 2 : b.h, wn = pool ? (b.w / 2) * 2 : b.w;
+  const int rows = min(4 * nty, hn - 4 * ty0);
+  const int ntile = band64_ntile(pool != 0, rows, wn);
   const bool f16out = st16 != 0.0f;
   const float s = f16out ? st16 : 1.0f;
   const float k = H ? sc * s : 1.0f;
@@ -1251,16 +1295,16 @@ __device__ __forceinline__ void band64_layer(const unsigned char* lds, const Ban
     if constexpr (H) {
       switch (mt) {
         case 7:
-          band64_run<7, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
-                               g, lane, f16out);
+          band64_run<7, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, rows, wn, first, m, g,
+                               lane, f16out);
           continue;
         case 6:
-          band64_run<6, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
-                               g, lane, f16out);
+          band64_run<6, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, rows, wn, first, m, g,
+                               lane, f16out);
           continue;
         case 5:
-          band64_run<5, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
-                               g, lane, f16out);
+          band64_run<5, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, rows, wn, first, m, g,
+                               lane, f16out);
           continue;
         default:
           break;
@@ -1268,20 +1312,20 @@ __device__ __forceinline__ void band64_layer(const unsigned char* lds, const Ban
     }
     switch (mt) {
       case 4:
-        band64_run<4, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
-                             g, lane, f16out);
+        band64_run<4, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, rows, wn, first, m, g,
+                             lane, f16out);
         break;
       case 3:
-        band64_run<3, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
-                             g, lane, f16out);
+        band64_run<3, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, rows, wn, first, m, g,
+                             lane, f16out);
         break;
       case 2:
-        band64_run<2, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
-                             g, lane, f16out);
+        band64_run<2, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, rows, wn, first, m, g,
+                             lane, f16out);
         break;
       case 1:
-        band64_run<1, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, tiles_x, first, py, px, m,
-                             g, lane, f16out);
+        band64_run<1, NT, H>(lds, b, ty0, wf, bp, s, k, out, cout, pool, rows, wn, first, m, g,
+                             lane, f16out);
         break;
       default:
         break;
@@ -1299,8 +1343,6 @@ k_band64(ConvArgs a, Band64 b) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int m = lane & 15, g = lane >> 4;
-  int py, px;
-  tile_pixel(m, py, px);
   const frag* wf = reinterpret_cast<const frag*>(a.wts);
   band64_clear(lds, b);
   int64_t cnt = *a.count;
@@ -1333,8 +1375,8 @@ k_band64(ConvArgs a, Band64 b) {
     __syncthreads();
     void* out = st16 != 0.0f ? static_cast<void*>(reinterpret_cast<_Float16*>(a.act_out) + out_e)
                              : static_cast<void*>(a.act_out + out_e);
-    band64_layer<NT, H>(lds, b, ty0, nty * a.tiles_x, at_off(wf, off), at_off(a.bias, off), out,
-                        a.cout, a.pool, a.tiles_x, wave, py, px, m, g, lane, out_scale, st16);
+    band64_layer<NT, H>(lds, b, ty0, nty, at_off(wf, off), at_off(a.bias, off), out, a.cout,
+                        a.pool, wave, m, g, lane, out_scale, st16);
   }
 }
 
@@ -1409,8 +1451,6 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int m = lane & 15, g = lane >> 4;
-  int py, px;
-  tile_pixel(m, py, px);
   const bf16x8* wf0 = reinterpret_cast<const bf16x8*>(a0.wts);
   const frag1* wf1 = reinterpret_cast<const frag1*>(a1.wts);
   band64_clear(lds, b);
@@ -1553,8 +1593,8 @@ k_pair64(ConvArgs a0, ConvArgs a1, Band64 b, const uint2* __restrict__ xin, int3
     const int64_t out_e = s * (int64_t)ho * wo * a1.cout;
     void* out = st16 != 0.0f ? static_cast<void*>(reinterpret_cast<_Float16*>(a1.act_out) + out_e)
                              : static_cast<void*>(a1.act_out + out_e);
-    band64_layer<NT, H>(lds, b, ty0, nty * a1.tiles_x, at_off(wf1, off), at_off(a1.bias, off), out,
-                        a1.cout, a1.pool, a1.tiles_x, wave, py, px, m, g, lane, out_scale1, st16);
+    band64_layer<NT, H>(lds, b, ty0, nty, at_off(wf1, off), at_off(a1.bias, off), out, a1.cout,
+                        a1.pool, wave, m, g, lane, out_scale1, st16);
   };
   // Rounds of work either way: image-major (a band there skips recomputing
   // two of its first-layer rows, counted as a tenth of its cost) or one band
@@ -2366,11 +2406,16 @@ bool band64_plan(const CnnLayer& L, bool h16, Band64* b, int32_t* band_tiles, si
   // 25 x 25 map, 6 x 6 tiles: 4 rows (6 and 3 tiles per wave) 447 us, 3 rows
   // 407, 2 rows 403.
   const int32_t per_round = (h16 ? kBandMaxTilesH : 4) * kBandWaves;
-  const int32_t cmax = per_round / tx > 2 ? per_round / tx : 2;
-  for (int32_t c = 1; c <= ty && c <= cmax; ++c) {
+  const int32_t hn = L.pool ? (L.h / 2) * 2 : L.h, wn = L.pool ? (L.w / 2) * 2 : L.w;
+  for (int32_t c = 1; c <= ty; ++c) {
+    if (c > 2 && band64_ntile(L.pool, std::min(4 * c, hn), wn) > per_round) break;
     if (band64_bytes(plan(c)) > 80 * 1024) break;
     const int64_t bands = (ty + c - 1) / c;
-    const int64_t per_wave = ((int64_t)c * tx + kBandWaves - 1) / kBandWaves;
+    int64_t per_wave = 0;  // the fullest band's tiles per wave
+    for (int32_t y0 = 0; y0 < ty; y0 += c) {
+      const int64_t t = band64_ntile(L.pool, std::min(4 * c, hn - 4 * y0), wn);
+      per_wave = std::max(per_wave, (t + kBandWaves - 1) / kBandWaves);
+    }
     if (bands * per_wave <= best) {
       best = bands * per_wave;
       bt = c;
