@@ -353,6 +353,41 @@ __device__ __forceinline__ void pool_epilogue_at(const f32x4 (&acc)[NT], const f
 // are the 4 channels of two horizontally adjacent pixels: one 16-byte LDS read
 // per MFMA for bf16.  K = 48, run as 2 steps of 32 (bf16) or 12 of 4 (fp32).
 
+// Sums over the fy x fx cells of input pixel (y, x) of one frame's area sums
+// S (3 channels per cell); below 255 * den_c < 2^31 (checked on the host).
+// With two cells per row (fx = 2), an even row length and an 8-byte-aligned
+// frame, the two cells of a row are 24 consecutive 8-byte-aligned bytes:
+// three 8-byte loads instead of six 4-byte ones.
+__device__ __forceinline__ void cell_sums(const ConvArgs& a, const int32_t* __restrict__ S, int y,
+                                          int x, int32_t (&acc)[3]) {
+  if (a.fy == 1 && a.fx == 1) {  // the area sums are at the CNN's grid
+    const int32_t* q = S + ((int64_t)y * a.sums_w + x) * 3;
+    acc[0] = q[0];
+    acc[1] = q[1];
+    acc[2] = q[2];
+    return;
+  }
+  acc[0] = acc[1] = acc[2] = 0;
+  if (a.fx == 2 && (a.sums_w & 1) == 0 && ((uintptr_t)S & 7) == 0) {
+    for (int dy = 0; dy < a.fy; ++dy) {
+      const int2* q =
+          reinterpret_cast<const int2*>(S + ((int64_t)(y * a.fy + dy) * a.sums_w + 2 * x) * 3);
+      const int2 u = q[0], v = q[1], w = q[2];  // cell 2x: u.x u.y v.x, cell 2x + 1: v.y w.x w.y
+      acc[0] += u.x + v.y;
+      acc[1] += u.y + w.x;
+      acc[2] += v.x + w.y;
+    }
+    return;
+  }
+  for (int dy = 0; dy < a.fy; ++dy)
+    for (int dx = 0; dx < a.fx; ++dx) {
+      const int32_t* q = S + ((int64_t)(y * a.fy + dy) * a.sums_w + (x * a.fx + dx)) * 3;
+      acc[0] += q[0];
+      acc[1] += q[1];
+      acc[2] += q[2];
+    }
+}
+
 // Stages rows x band_w pixels starting at input (y_top, x_left) of frame
 // idx[s], one pixel (3 channels + a zero, one 8- or 16-byte LDS store) per
 // thread and step, by the nthreads threads from thread tid0 on.
@@ -372,14 +407,8 @@ __device__ __forceinline__ void stage_first(const ConvArgs& a, T* in, int64_t s,
     const int y = y_top + br, x = x_left + bc;
     T v[4] = {X::from_f32(0.0f), X::from_f32(0.0f), X::from_f32(0.0f), X::from_f32(0.0f)};
     if (y >= 0 && y < a.h && x >= 0 && x < a.w) {
-      int32_t acc[3] = {0, 0, 0};  // below 255 * den_c < 2^31 (checked on the host)
-      for (int dy = 0; dy < a.fy; ++dy)
-        for (int dx = 0; dx < a.fx; ++dx) {
-          const int32_t* q = S + ((int64_t)(y * a.fy + dy) * a.sums_w + (x * a.fx + dx)) * 3;
-          acc[0] += q[0];
-          acc[1] += q[1];
-          acc[2] += q[2];
-        }
+      int32_t acc[3];
+      cell_sums(a, S, y, x, acc);
 #pragma unroll
       for (int c = 0; c < 3; ++c) {
         // (S / den) / 127.5 - 1 = (2 S - den255) / den255, rounded once (exact ties included)
@@ -1391,14 +1420,8 @@ constexpr uint32_t kOneBf16Hi = 0x3F800000u;
 // frame idx[s], correctly rounded, and channel 3 = 1.
 __device__ __forceinline__ uint2 first_input_bf16(const ConvArgs& a, int64_t s, int y, int x) {
   const int32_t* S = a.sums + (int64_t)a.idx[s] * a.sums_h * a.sums_w * 3;
-  int32_t acc[3] = {0, 0, 0};  // below 255 * den_c < 2^31 (checked on the host)
-  for (int dy = 0; dy < a.fy; ++dy)
-    for (int dx = 0; dx < a.fx; ++dx) {
-      const int32_t* q = S + ((int64_t)(y * a.fy + dy) * a.sums_w + (x * a.fx + dx)) * 3;
-      acc[0] += q[0];
-      acc[1] += q[1];
-      acc[2] += q[2];
-    }
+  int32_t acc[3];
+  cell_sums(a, S, y, x, acc);
   uint16_t v[3];
   const bool f32div = a.den255 < (1 << 24);
   const float inv = 1.0f / (float)a.den255;
