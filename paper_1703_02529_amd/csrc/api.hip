@@ -24,7 +24,8 @@ int fail(int code, const char* fmt, ...) {
 }
 
 size_t conv_lds_bytes(const CnnLayer& L, bool bf16, int32_t* cin_lds, int32_t* w_lds,
-                      int32_t* band_w, int32_t* band_tiles, int32_t* seg_tiles);
+                      int32_t* band_w, int32_t* band_tiles, int32_t* seg_tiles,
+                      int32_t max_bt = 0);
 
 namespace {
 
