@@ -820,15 +820,17 @@ int make_area_plan(int32_t in_h, int32_t in_w, int64_t stride, const void* frame
       // a workgroup reads whole source rows (all strips of its bands) at once, so that
       // the cache lines two strips share are fetched once, by one CU
       g.waves_per_block = g.waves_per_frame <= 4 ? g.waves_per_frame * (4 / g.waves_per_frame) : 4;
-      // bands of two output rows (more when there are too few frames to fill
-      // the chip): with units this short, the waves resident on an XCD at a
-      // time read fewer frames.  Measured against bands of 10 rows (area
-      // sums alone, all heights timed in turn in one process, on two
-      // machines): 640x480 -> 50x50 4.6 and 7.6 % faster, 1280x720 -> 100x100
-      // 0 and 6 %, 1920x1080 -> 100x100 1.2 and 1 %, 1280x720 -> 50x50 within
-      // 0.5 %; a single row was faster still at 640x480 but 5 % slower at
-      // 1280x720 -> 100x100.
-      int64_t wb = (out_h + 1) / 2;
+      // bands of two output rows with 16- or 32-byte lane chunks (more when
+      // there are too few frames to fill the chip): with units this short,
+      // the waves resident on an XCD at a time read fewer frames.  Measured
+      // against bands of 10 rows (area sums alone, all heights timed in turn
+      // in one process, on two machines): 640x480 -> 50x50 4.6 and 7.6 %
+      // faster, 1280x720 -> 100x100 0 and 6 %, 1920x1080 -> 100x100 1.2 and
+      // 1 %, 1280x720 -> 50x50 within 0.5 %; a single row was faster still at
+      // 640x480 but 5 % slower at 1280x720 -> 100x100.  Rows of a few hundred
+      // bytes (4-byte chunks) keep bands of about 10 rows: 100x100 -> 50x50,
+      // 20,000 frames, 663 us against 847 with two rows.
+      int64_t wb = best_cb >= 16 ? (out_h + 1) / 2 : (out_h + 9) / 10;
       const int64_t fill = (16384 + n * g.waves_per_frame - 1) / (n * g.waves_per_frame > 0 ? n * g.waves_per_frame : 1);
       if (fill > wb) wb = fill;
       if (wb > out_h) wb = out_h;
