@@ -3,6 +3,7 @@ FLOP count per survivor that the CNN's MFMA fraction is quoted on."""
 import os
 import subprocess
 import sys
+import types
 
 import bench
 from synth import workloads as W
@@ -45,3 +46,17 @@ def test_cpu_baseline_window_and_fields():
     assert r["cpu_model"] and "continued from the area sums of the 15 frames" in r["sample"]
     r = bench.cpu_baseline(W.TINY, 0.3, 0.3)
     assert r["value"] > 0
+
+
+def test_area_kernel_names_match_the_library_plan():
+    """The kernel whose launches the roofline figure times: 16-byte lane
+    chunks unless they leave more than a fifth of a wave idle (then 32), and
+    the fused earlier-frame kernel only when the workload asks for it."""
+    assert bench.lane_chunk_bytes(640, 50) == 16     # 60 of 64 lanes busy
+    assert bench.lane_chunk_bytes(1280, 100) == 16   # 48 of 64
+    assert bench.lane_chunk_bytes(1920, 100) == 16   # 54 of 64
+    assert bench.lane_chunk_bytes(1280, 50) == 32    # 48 of 64 at 16 bytes, 60 at 32
+    for wl in W.ALL:
+        assert bench.area_kernel(wl) == "k_area_sums_wave", wl.name
+    fused = types.SimpleNamespace(**vars(W.VGA), fuse_prev=1)  # a description asking for it
+    assert bench.area_kernel(fused) == "k_area_prev_wave"
